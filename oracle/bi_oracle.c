@@ -1,0 +1,275 @@
+/*
+ * Reference ("oracle") implementation of the discrete HMM/POMDP belief updates
+ * of "A Hardware-oriented Approach for Efficient Bayesian Inference
+ * Computation and Deployment": variational filtering (FPI), variational
+ * message passing (VMP) and marginal message passing (MMP).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+ * CPU definition that the GPU library is checked against.  It is compiled by
+ * the build step, called only from the tests, the smoke check and the CPU
+ * baseline leg of the benchmark, and it shares no code, header or table with
+ * the GPU library (neither includes nor links the other).
+ *
+ * Everything is computed in double precision, in the looped per-modality
+ * form (Sec. III-C, the "original" loop of contractions that the merged
+ * layouts reproduce), one agent at a time (OpenMP over agents only).
+ *
+ * Model (Sec. III-B, the factorised joint over o_{1:T}, s_{1:T} given u):
+ *   A[m] : [mb][K_m][n_{d1}]..[n_{dk}]   P(o^m | s^{d1..dk}), dep list ascending
+ *   B[f] : [mb][n_f][n_f][U_f]           B[i][j][u] = P(s_{t+1}=i | s_t=j, u)
+ *   D[f] : [mb][n_f]                     p(s_1)
+ *   mb = 1 (shared by all agents) or the number of agents.
+ *   obs  : [b][T][M] int,  act : [b][T-1][F] int,  q : [b][T][sum n_f].
+ *
+ * Readings of points the paper leaves open (the paper gives only the generic
+ * coordinate update of Sec. III-A and the joint of Sec. III-B):
+ *   LN(x) = log(max(x, 1e-16))  (log of zero is clamped, never -inf)
+ *   q initialised uniform; fixed iteration count; Jacobi schedule (every
+ *   marginal of iteration k is computed from the marginals of iteration k-1);
+ *   no damping.
+ *   Likelihood message (Sec. IV: marginalisation of the log-likelihood under
+ *   the other factors' marginals, summed over the Markov blanket):
+ *     lam_{t,f}(s) = sum_{m: f in dep(m)} sum_{s_dep: s_f = s}
+ *                    LN(A_m[o_{t,m}, s_dep]) * prod_{g in dep(m), g != f} q_{t,g}(s_g)
+ *   FPI: for t = 0..T-1 in order, prior p_{t,f} = D_f (t = 0) or
+ *        B_f[:,:,u_{t-1,f}] q_{t-1,f} (final marginal of step t-1);
+ *        q_t <- uniform, then iters times q_{t,f} = softmax(lam_{t,f} + LN(p_{t,f})).
+ *   VMP: the generic update of Sec. III-A applied to the joint of Sec. III-B
+ *        under q = prod_{t,f} q_{t,f}:
+ *        q_{t,f} = softmax(lam + fwd + bwd),
+ *        fwd = LN(D_f) (t = 0) else sum_{s'} LN(B_f[s, s', u_{t-1}]) q_{t-1,f}(s'),
+ *        bwd = 0 (t = T-1) else sum_{s''} q_{t+1,f}(s'') LN(B_f[s'', s, u_t]).
+ *   MMP: fwd = LN(D_f) (t = 0) else LN(B_f[:,:,u_{t-1}] q_{t-1,f}),
+ *        bwd = LN(B_f[:,:,u_t]^T q_{t+1,f}) (t < T-1),
+ *        q_{t,f} = softmax(lam + mean of the temporal messages present at t):
+ *        (fwd + bwd)/2 for t < T-1, fwd alone at t = T-1.
+ */
+#include <math.h>
+#include <omp.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_EPS 1e-16
+#define ORC_MAX_RANK 32
+
+enum { ORC_FPI = 0, ORC_VMP = 1, ORC_MMP = 2 };
+
+typedef struct {
+    int F, M, mb;
+    const int *n, *U, *K, *dep_off, *dep;
+    const double *const *A;
+    const double *const *B;
+    const double *const *D;
+} orc_model;
+
+static double LN(double x) { return log(x > ORC_EPS ? x : ORC_EPS); }
+
+/* In-place softmax over v[0..n-1]. */
+static void softmax(double *v, int n)
+{
+    double mx = v[0];
+    for (int i = 1; i < n; ++i)
+        if (v[i] > mx) mx = v[i];
+    double s = 0.0;
+    for (int i = 0; i < n; ++i) {
+        v[i] = exp(v[i] - mx);
+        s += v[i];
+    }
+    for (int i = 0; i < n; ++i) v[i] /= s;
+}
+
+static size_t slice_size(const orc_model *md, int m)
+{
+    size_t p = 1;
+    for (int i = md->dep_off[m]; i < md->dep_off[m + 1]; ++i) p *= (size_t)md->n[md->dep[i]];
+    return p;
+}
+
+/* Likelihood messages of one context (agent a, one time step).
+ * o: [M] observed outcomes; q: [sum n] marginals of the context;
+ * lam: [sum n] output.  qoff[f] is the offset of factor f in q / lam. */
+static void likelihood_messages(const orc_model *md, int a, const int *o, const double *q, const int *qoff,
+                                int ntot, double *lam)
+{
+    int am = md->mb == 1 ? 0 : a;
+    for (int i = 0; i < ntot; ++i) lam[i] = 0.0;
+    for (int m = 0; m < md->M; ++m) {
+        const int k = md->dep_off[m + 1] - md->dep_off[m];
+        const int *d = md->dep + md->dep_off[m];
+        const size_t P = slice_size(md, m);
+        const double *slice = md->A[m] + ((size_t)am * md->K[m] + (size_t)o[m]) * P;
+        int idx[ORC_MAX_RANK];
+        for (int i = 0; i < k; ++i) idx[i] = 0;
+        for (size_t e = 0; e < P; ++e) {
+            const double ll = LN(slice[e]);
+            for (int i = 0; i < k; ++i) {
+                double w = 1.0;
+                for (int j = 0; j < k; ++j)
+                    if (j != i) w *= q[qoff[d[j]] + idx[j]];
+                lam[qoff[d[i]] + idx[i]] += ll * w;
+            }
+            /* odometer over s_dep, last axis fastest (row-major A) */
+            for (int i = k - 1; i >= 0; --i) {
+                if (++idx[i] < md->n[d[i]]) break;
+                idx[i] = 0;
+            }
+        }
+    }
+}
+
+static const double *B_at(const orc_model *md, int f, int a)
+{
+    int am = md->mb == 1 ? 0 : a;
+    size_t nf = (size_t)md->n[f];
+    return md->B[f] + (size_t)am * nf * nf * (size_t)md->U[f];
+}
+
+/* B_f[i][j][u] */
+static double Bv(const orc_model *md, const double *Bf, int f, int i, int j, int u)
+{
+    return Bf[((size_t)i * md->n[f] + j) * md->U[f] + u];
+}
+
+static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int *act, int iters, double *q,
+                    const int *qoff, int ntot, double *work)
+{
+    double *cur = work, *lam = work + ntot, *logp = work + 2 * ntot;
+    for (int t = 0; t < T; ++t) {
+        for (int f = 0; f < md->F; ++f) {
+            const int nf = md->n[f];
+            if (t == 0) {
+                const double *Df = md->D[f] + (size_t)(md->mb == 1 ? 0 : a) * nf;
+                for (int s = 0; s < nf; ++s) logp[qoff[f] + s] = LN(Df[s]);
+            } else {
+                const double *Bf = B_at(md, f, a);
+                const int u = act[(size_t)(t - 1) * md->F + f];
+                const double *qp = q + (size_t)(t - 1) * ntot + qoff[f];
+                for (int i = 0; i < nf; ++i) {
+                    double p = 0.0;
+                    for (int j = 0; j < nf; ++j) p += Bv(md, Bf, f, i, j, u) * qp[j];
+                    logp[qoff[f] + i] = LN(p);
+                }
+            }
+            for (int s = 0; s < nf; ++s) cur[qoff[f] + s] = 1.0 / nf;
+        }
+        for (int k = 0; k < iters; ++k) {
+            likelihood_messages(md, a, obs + (size_t)t * md->M, cur, qoff, ntot, lam);
+            for (int f = 0; f < md->F; ++f) {
+                double *v = cur + qoff[f];
+                for (int s = 0; s < md->n[f]; ++s) v[s] = lam[qoff[f] + s] + logp[qoff[f] + s];
+                softmax(v, md->n[f]);
+            }
+        }
+        memcpy(q + (size_t)t * ntot, cur, sizeof(double) * (size_t)ntot);
+    }
+}
+
+static void run_window(const orc_model *md, int algo, int a, int T, const int *obs, const int *act, int iters,
+                       double *q, const int *qoff, int ntot, double *work)
+{
+    double *qn = work;                               /* [T][ntot] next iterate */
+    double *lam = work + (size_t)T * ntot;            /* [T][ntot] */
+    for (int t = 0; t < T; ++t)
+        for (int f = 0; f < md->F; ++f)
+            for (int s = 0; s < md->n[f]; ++s) q[(size_t)t * ntot + qoff[f] + s] = 1.0 / md->n[f];
+    for (int k = 0; k < iters; ++k) {
+        for (int t = 0; t < T; ++t)
+            likelihood_messages(md, a, obs + (size_t)t * md->M, q + (size_t)t * ntot, qoff, ntot,
+                                lam + (size_t)t * ntot);
+        for (int t = 0; t < T; ++t) {
+            for (int f = 0; f < md->F; ++f) {
+                const int nf = md->n[f];
+                const double *Bf = B_at(md, f, a);
+                const double *Df = md->D[f] + (size_t)(md->mb == 1 ? 0 : a) * nf;
+                const double *qprev = t > 0 ? q + (size_t)(t - 1) * ntot + qoff[f] : NULL;
+                const double *qnext = t + 1 < T ? q + (size_t)(t + 1) * ntot + qoff[f] : NULL;
+                const int uprev = t > 0 ? act[(size_t)(t - 1) * md->F + f] : 0;
+                const int unext = t + 1 < T ? act[(size_t)t * md->F + f] : 0;
+                double *v = qn + (size_t)t * ntot + qoff[f];
+                for (int s = 0; s < nf; ++s) {
+                    double fwd, bwd = 0.0;
+                    if (algo == ORC_VMP) {
+                        if (t == 0) {
+                            fwd = LN(Df[s]);
+                        } else {
+                            fwd = 0.0;
+                            for (int sp = 0; sp < nf; ++sp) fwd += LN(Bv(md, Bf, f, s, sp, uprev)) * qprev[sp];
+                        }
+                        if (qnext)
+                            for (int sn = 0; sn < nf; ++sn) bwd += qnext[sn] * LN(Bv(md, Bf, f, sn, s, unext));
+                        v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd + bwd;
+                    } else { /* MMP */
+                        if (t == 0) {
+                            fwd = LN(Df[s]);
+                        } else {
+                            double p = 0.0;
+                            for (int sp = 0; sp < nf; ++sp) p += Bv(md, Bf, f, s, sp, uprev) * qprev[sp];
+                            fwd = LN(p);
+                        }
+                        if (qnext) {
+                            double p = 0.0;
+                            for (int sn = 0; sn < nf; ++sn) p += Bv(md, Bf, f, sn, s, unext) * qnext[sn];
+                            bwd = LN(p);
+                            v[s] = lam[(size_t)t * ntot + qoff[f] + s] + 0.5 * (fwd + bwd);
+                        } else {
+                            v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd;
+                        }
+                    }
+                }
+                softmax(v, nf);
+            }
+        }
+        memcpy(q, qn, sizeof(double) * (size_t)T * ntot);
+    }
+}
+
+/*
+ * Run `algo` (0 FPI, 1 VMP, 2 MMP) for b agents.  Returns 0, or -1 on an
+ * invalid argument.  nthreads <= 0 uses the OpenMP default.
+ */
+int orc_infer(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
+              const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
+              int b, int T, const int *obs, const int *act, int iters, double *q, int nthreads)
+{
+    if (algo < 0 || algo > 2 || F < 1 || M < 1 || b < 1 || T < 1 || iters < 1) return -1;
+    if (mb != 1 && mb != b) return -1;
+    if (!n || !U || !K || !dep_off || !dep || !A || !B || !D || !obs || !q) return -1;
+    if (T > 1 && !act) return -1;
+    int ntot = 0;
+    int *qoff = (int *)malloc(sizeof(int) * (size_t)F);
+    if (!qoff) return -1;
+    for (int f = 0; f < F; ++f) {
+        if (n[f] < 1 || U[f] < 1) { free(qoff); return -1; }
+        qoff[f] = ntot;
+        ntot += n[f];
+    }
+    for (int m = 0; m < M; ++m) {
+        int k = dep_off[m + 1] - dep_off[m];
+        if (k < 1 || k > ORC_MAX_RANK || K[m] < 1) { free(qoff); return -1; }
+        for (int i = dep_off[m]; i < dep_off[m + 1]; ++i)
+            if (dep[i] < 0 || dep[i] >= F) { free(qoff); return -1; }
+    }
+    orc_model md = {F, M, mb, n, U, K, dep_off, dep, A, B, D};
+    const size_t work_per = (size_t)(3 + 2 * T) * (size_t)ntot;
+    int bad = 0;
+    const int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nt) reduction(| : bad)
+    for (int a = 0; a < b; ++a) {
+        double *work = (double *)malloc(sizeof(double) * work_per);
+        if (!work) { bad = 1; continue; }
+        const int *oa = obs + (size_t)a * T * M;
+        const int *ua = T > 1 ? act + (size_t)a * (T - 1) * F : NULL;
+        double *qa = q + (size_t)a * T * ntot;
+        if (algo == ORC_FPI)
+            run_fpi(&md, a, T, oa, ua, iters, qa, qoff, ntot, work);
+        else
+            run_window(&md, algo, a, T, oa, ua, iters, qa, qoff, ntot, work);
+        free(work);
+    }
+    free(qoff);
+    return bad ? -1 : 0;
+}
+
+/* Number of OpenMP threads orc_infer uses when nthreads <= 0. */
+int orc_default_threads(void) { return omp_get_max_threads(); }

@@ -1,0 +1,95 @@
+"""ctypes front end of ``bi_oracle.c`` (test infrastructure only).
+
+``infer(algo, model, obs, act, iters)`` converts the float32 model arrays of a
+:class:`paper_2607_17855_amd.synth.Model` to float64 and runs the C oracle.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "bi_oracle.c")
+_LIB = os.path.join(_HERE, "libbi_oracle.so")
+ALGOS = {"fpi": 0, "vmp": 1, "mmp": 2}
+_lib = None
+
+
+def lib_path() -> str:
+    return _LIB
+
+
+def build() -> str:
+    """Compile the oracle with gcc (plain C11 + OpenMP, no fast-math)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fopenmp", "-fPIC", "-shared", "-o", _LIB + ".tmp",
+           _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+def load_library(path: str):
+    """Open an oracle shared library (the built one, or a test's mutant copy)."""
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    lib.orc_infer.restype = ctypes.c_int
+    lib.orc_infer.argtypes = [ctypes.c_int, ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                              P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                              P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p), ctypes.c_int,
+                              ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                              P(ctypes.c_double), ctypes.c_int]
+    lib.orc_default_threads.restype = ctypes.c_int
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        _lib = load_library(_LIB)
+    return _lib
+
+
+def default_threads() -> int:
+    return int(_load().orc_default_threads())
+
+
+def _i32(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+
+def infer(algo: str, model, obs: np.ndarray, act: np.ndarray, iters: int,
+          agents: Optional[Sequence[int]] = None, threads: int = 0, lib=None) -> np.ndarray:
+    """Posterior marginals q [b][T][sum n] (float64) of ``algo`` for every agent,
+    or for the listed ``agents`` only (agents are independent)."""
+    if lib is None:
+        lib = _load()
+    if agents is not None:
+        agents = list(agents)
+        model = model.agent_slice(agents)
+        obs = obs[agents]
+        act = act[agents]
+    b, T, M = obs.shape
+    F = len(model.n)
+    n, U, K = _i32(model.n), _i32(model.U), _i32(model.K)
+    dep_off = _i32(np.cumsum([0] + [len(d) for d in model.deps]))
+    dep = _i32([f for d in model.deps for f in d])
+    A = [np.ascontiguousarray(a, dtype=np.float64) for a in model.A]
+    B = [np.ascontiguousarray(x, dtype=np.float64) for x in model.B]
+    D = [np.ascontiguousarray(x, dtype=np.float64) for x in model.D]
+    ptrs = lambda arrs: (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])  # noqa: E731
+    obs_c = _i32(obs)
+    act_c = _i32(act) if T > 1 else _i32(np.zeros((b, 1, F)))
+    q = np.zeros((b, T, int(sum(model.n))), dtype=np.float64)
+    ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))  # noqa: E731
+    rc = lib.orc_infer(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
+                       ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c), int(iters),
+                       q.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(threads))
+    if rc != 0:
+        raise ValueError(f"oracle rejected the arguments (rc={rc})")
+    return q

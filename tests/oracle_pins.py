@@ -1,0 +1,279 @@
+"""Pins of the oracle against results fixed by the paper and by mathematics.
+
+Each ``pin_*`` takes an ``infer(algo, model, obs, act, iters)`` callable (the
+oracle, or a deliberately broken copy of it in the mutation tests) and returns
+the largest absolute deviation from the independently computed expectation.
+"""
+from __future__ import annotations
+
+import os
+from fractions import Fraction
+
+import numpy as np
+
+from paper_2607_17855_amd import synth
+import bruteforce as bf
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _hmm(seed, n=4, K=(3,), U=2, T=6, b=2, alpha=1.0, mb=None, uniform_D=False):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    model = synth.make_model(rng, [n], [U], list(K), [[0]] * len(K), b if mb is None else mb, alpha, alpha,
+                             uniform_D=uniform_D)
+    obs, act = synth.sample_sequences(rng, model, b, T)
+    return model, obs, act
+
+
+def pin_bayes_filter(infer):
+    """F = 1: variational filtering is exact filtering (Sec. III-A update with a
+    single factor has no mean-field approximation), so FPI must equal the
+    textbook forward algorithm, for any iteration count."""
+    err = 0.0
+    for seed, K, iters in [(1, (3,), 1), (2, (5, 2), 3), (3, (2, 2, 4), 16)]:
+        model, obs, act = _hmm(seed, n=5, K=K, T=7, b=3)
+        q = infer("fpi", model, obs, act, iters)
+        for a in range(obs.shape[0]):
+            alpha = bf.forward_filter([np.float64(A[a]) for A in model.A], np.float64(model.B[0][a]),
+                                      np.float64(model.D[0][a]), obs[a], act[a, :, 0])
+            err = max(err, float(np.abs(q[a] - alpha).max()))
+    return err
+
+
+def pin_golden_hmm2(infer):
+    """Hand-derived two-state filter (tests/golden/hmm2_filter.txt)."""
+    vals = {}
+    with open(os.path.join(GOLDEN, "hmm2_filter.txt")) as fh:
+        for line in fh:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            key, rhs = line.split("=", 1)
+            vals[key.strip()] = [float(Fraction(x)) for x in rhs.split()]
+    A = np.array([vals["A0"], vals["A1"]], dtype=np.float32)          # A[o][s]
+    B = np.array(vals["B"], dtype=np.float32).reshape(2, 2, 1)         # B[i][j][u]
+    D = np.array(vals["D"], dtype=np.float32)
+    model = synth.Model([2], [1], [2], [[0]], 1, [A[None]], [B[None]], [D[None]])
+    obs = np.array(vals["obs"], dtype=np.int32).reshape(1, -1, 1)
+    act = np.zeros((1, obs.shape[1] - 1, 1), dtype=np.int32)
+    q = infer("fpi", model, obs, act, 4)
+    want = np.array([vals["q0"], vals["q1"]])
+    # inputs were rounded to float32, so compare at float32 input precision
+    return float(np.abs(q[0] - want).max())
+
+
+def pin_vmp_bruteforce(infer, seeds=range(12)):
+    """VMP = the coordinate update of Sec. III-A on the window joint of Sec.
+    III-B under a fully factorised q, evaluated by enumerating the joint."""
+    err = 0.0
+    for seed in seeds:
+        # odd seeds carry exact zeros in A and B (the clamped-log reading)
+        w = synth.random_small(seed, F_max=3, n_max=3, M_max=3, K_max=3, T_max=3, b=2,
+                               sparsity=0.4 if seed % 2 else 0.0)
+        ref = bf.vmp_bruteforce(w.model, w.obs, w.act, w.iters)
+        q = infer("vmp", w.model, w.obs, w.act, w.iters)
+        err = max(err, float(np.abs(q - ref).max()))
+    return err
+
+
+def pin_fpi_bruteforce(infer, seeds=range(12)):
+    """FPI = per-step coordinate updates over the enumerated single-step joint."""
+    err = 0.0
+    for seed in seeds:
+        w = synth.random_small(100 + seed, F_max=3, n_max=4, M_max=3, K_max=3, T_max=4, b=2,
+                               sparsity=0.4 if seed % 2 else 0.0)
+        ref = bf.fpi_bruteforce(w.model, w.obs, w.act, w.iters)
+        q = infer("fpi", w.model, w.obs, w.act, w.iters)
+        err = max(err, float(np.abs(q - ref).max()))
+    return err
+
+
+def pin_factorised_exact(infer):
+    """Every dependency list a singleton: the joint factorises over factors, so
+    filtering is exact per factor and FPI equals a forward filter per factor."""
+    rng = np.random.Generator(np.random.PCG64(7))
+    n, U, K = [3, 4, 2], [2, 1, 3], [3, 2, 4, 3]
+    deps = [[0], [1], [2], [0]]
+    b, T = 2, 5
+    model = synth.make_model(rng, n, U, K, deps, b, 1.0, 1.0, uniform_D=False)
+    obs, act = synth.sample_sequences(rng, model, b, T)
+    q = infer("fpi", model, obs, act, 2)
+    offs = np.cumsum([0] + n)
+    err = 0.0
+    for a in range(b):
+        for f in range(len(n)):
+            ms = [m for m, d in enumerate(deps) if d == [f]]
+            alpha = bf.forward_filter([np.float64(model.A[m][a]) for m in ms], np.float64(model.B[f][a]),
+                                      np.float64(model.D[f][a]), obs[a][:, ms], act[a, :, f])
+            err = max(err, float(np.abs(q[a, :, offs[f]:offs[f + 1]] - alpha).max()))
+    return err
+
+
+def pin_t1_identity(infer):
+    """T = 1: no temporal messages, the three schemes coincide and equal the
+    single-step mean-field fixed-point iteration (checked by enumeration)."""
+    err = 0.0
+    for seed in range(6):
+        w = synth.random_small(200 + seed, F_max=3, n_max=4, T_max=1, b=2)
+        ref = bf.vmp_bruteforce(w.model, w.obs, w.act, w.iters)
+        for algo in ("fpi", "vmp", "mmp"):
+            err = max(err, float(np.abs(infer(algo, w.model, w.obs, w.act, w.iters) - ref).max()))
+    return err
+
+
+def _iid_model(seed, n=4, U=3, K=(3, 2), T=5, b=2):
+    """Single factor whose transition ignores the previous state:
+    B[:, j, u] = p_u for every j."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    model = synth.make_model(rng, [n], [U], list(K), [[0]] * len(K), b, 1.0, 1.0, uniform_D=False)
+    p = rng.dirichlet(np.ones(n), size=(b, U))                   # [b][U][n]
+    B = np.repeat(np.transpose(p, (0, 2, 1))[:, :, None, :], n, axis=2)   # [b][i][j][u] = p_u(i)
+    model.B[0] = np.ascontiguousarray(B, dtype=np.float32)
+    obs, act = synth.sample_sequences(rng, model, b, T)
+    return model, obs, act
+
+
+def pin_iid_closed_forms(infer):
+    """Transitions that ignore the previous state: the backward message is
+    constant in s and cancels, the forward message is log p_u; hence the closed
+    forms  VMP: q_0 ~ L_0 D, q_t ~ L_t p;  MMP: q_0 ~ L_0 D^(1/2), q_t ~ L_t p^(1/2)
+    inside the window and L_{T-1} p at its end (L_t = prod_m A_m[o_t])."""
+    err = 0.0
+    for seed, T in [(11, 5), (12, 2), (13, 6)]:
+        model, obs, act = _iid_model(seed, T=T)
+        b = obs.shape[0]
+        qv = infer("vmp", model, obs, act, 3)
+        qm = infer("mmp", model, obs, act, 3)
+        for a in range(b):
+            B = np.float64(model.B[0][a])
+            D = np.float64(model.D[0][a])
+            for t in range(T):
+                L = np.ones(model.n[0])
+                for m in range(model.M):
+                    L = L * np.float64(model.A[m][a][obs[a, t, m]])
+                prior = D if t == 0 else B[:, 0, act[a, t - 1, 0]]
+                v = L * prior
+                err = max(err, float(np.abs(qv[a, t] - v / v.sum()).max()))
+                w = L * (prior if t == T - 1 else np.sqrt(prior))
+                err = max(err, float(np.abs(qm[a, t] - w / w.sum()).max()))
+    return err
+
+
+def pin_mmp_permutation_smoothing(infer):
+    """Deterministic cyclic transition s' = pi(s), uniform D, an uninformative
+    first outcome and an informative second one (T = 2).  The backward message
+    of MMP is the likelihood of the future marginal under the transition, so at
+    the fixed point q_0(s) equals the exact smoothing posterior
+    p(s_0 = s | o_0, o_1) ~ A[o_1][pi(s)]."""
+    n = 3
+    pi = np.array([1, 2, 0])                       # a 3-cycle: pi != pi^-1
+    B = np.zeros((1, n, n, 1), dtype=np.float32)
+    for j in range(n):
+        B[0, pi[j], j, 0] = 1.0
+    A = np.array([[0.2, 0.2, 0.2],                 # outcome 0: uninformative
+                  [0.7, 0.1, 0.3],
+                  [0.1, 0.7, 0.5]], dtype=np.float32)
+    A /= A.sum(axis=0, keepdims=True)
+    D = np.full((1, n), 1.0 / n, dtype=np.float32)
+    model = synth.Model([n], [1], [3], [[0]], 1, [A[None]], [B], [D])
+    err = 0.0
+    for o1 in (1, 2):
+        obs = np.array([[[0], [o1]]], dtype=np.int32)
+        act = np.zeros((1, 1, 1), dtype=np.int32)
+        q = infer("mmp", model, obs, act, 200)
+        exact = bf.exact_window_marginals(model, obs[0], act[0], 0)[0]
+        want = np.float64(A[o1][pi])
+        want /= want.sum()
+        err = max(err, float(np.abs(exact - want).max()), float(np.abs(q[0, 0] - want).max()))
+    return err
+
+
+def _relabel_states(model, f, perm):
+    """New label i' of factor f's state perm[i'] (state perm[i'] is renamed i')."""
+    A = []
+    for m, d in enumerate(model.deps):
+        a = model.A[m]
+        if f in d:
+            a = np.take(a, perm, axis=2 + d.index(f))
+        A.append(np.ascontiguousarray(a))
+    B = list(model.B)
+    B[f] = np.ascontiguousarray(np.take(np.take(model.B[f], perm, axis=1), perm, axis=2))
+    D = list(model.D)
+    D[f] = np.ascontiguousarray(np.take(model.D[f], perm, axis=1))
+    return synth.Model(list(model.n), list(model.U), list(model.K), [list(d) for d in model.deps], model.mb, A, B, D)
+
+
+def _reorder_factors(model, order, act):
+    """Factor g of the new model is factor order[g] of the old one."""
+    inv = np.argsort(order)
+    deps, A = [], []
+    for m, d in enumerate(model.deps):
+        nd = sorted(int(inv[f]) for f in d)
+        # axis of new factor g comes from old factor order[g]
+        src = [d.index(int(order[g])) for g in nd]
+        A.append(np.ascontiguousarray(np.transpose(model.A[m], [0, 1] + [2 + s for s in src])))
+        deps.append(nd)
+    nm = synth.Model([model.n[o] for o in order], [model.U[o] for o in order], list(model.K), deps, model.mb, A,
+                     [model.B[o] for o in order], [model.D[o] for o in order])
+    return nm, np.ascontiguousarray(act[:, :, order])
+
+
+def pin_invariants(infer):
+    """Normalisation, non-negativity, agent-permutation, state-relabelling,
+    factor- and modality-reorder equivariance, shared == replicated model, and
+    finiteness with exact zeros in A and B."""
+    worst = 0.0
+    for seed in range(4):
+        w = synth.random_small(300 + seed, F_max=3, n_max=5, M_max=3, K_max=4, T_max=5, b=4, per_agent=True,
+                               sparsity=0.3 if seed % 2 else 0.0)
+        mdl, obs, act = w.model, w.obs, w.act
+        offs = np.cumsum([0] + mdl.n)
+        for algo in ("fpi", "vmp", "mmp"):
+            q = infer(algo, mdl, obs, act, w.iters)
+            if not np.all(np.isfinite(q)) or q.min() < 0:
+                return np.inf
+            for f in range(mdl.F):
+                worst = max(worst, float(np.abs(q[..., offs[f]:offs[f + 1]].sum(-1) - 1).max()))
+            perm = np.array([3, 1, 0, 2])
+            qp = infer(algo, mdl.agent_slice(perm), obs[perm], act[perm], w.iters)
+            worst = max(worst, float(np.abs(qp - q[perm]).max()))
+            f = int(np.argmax(mdl.n))
+            sp = np.random.Generator(np.random.PCG64(seed)).permutation(mdl.n[f])
+            qr = infer(algo, _relabel_states(mdl, f, sp), obs, act, w.iters)
+            worst = max(worst, float(np.abs(qr[..., offs[f] + np.arange(mdl.n[f])] - q[..., offs[f] + sp]).max()))
+            if mdl.F > 1:
+                order = np.arange(mdl.F)[::-1].copy()
+                m2, act2 = _reorder_factors(mdl, order, act)
+                q2 = infer(algo, m2, obs, act2, w.iters)
+                offs2 = np.cumsum([0] + m2.n)
+                for g, o in enumerate(order):
+                    worst = max(worst, float(np.abs(q2[..., offs2[g]:offs2[g + 1]] -
+                                                    q[..., offs[o]:offs[o + 1]]).max()))
+            if mdl.M > 1:
+                mo = np.arange(mdl.M)[::-1].copy()
+                m3 = synth.Model(mdl.n, mdl.U, [mdl.K[i] for i in mo], [mdl.deps[i] for i in mo], mdl.mb,
+                                 [mdl.A[i] for i in mo], mdl.B, mdl.D)
+                q3 = infer(algo, m3, np.ascontiguousarray(obs[:, :, mo]), act, w.iters)
+                worst = max(worst, float(np.abs(q3 - q).max()))
+    # shared == replicated
+    w = synth.random_small(400, F_max=3, n_max=4, b=3, per_agent=False)
+    rep = synth.Model(w.model.n, w.model.U, w.model.K, w.model.deps, w.b,
+                      [np.repeat(a, w.b, axis=0) for a in w.model.A], [np.repeat(a, w.b, axis=0) for a in w.model.B],
+                      [np.repeat(a, w.b, axis=0) for a in w.model.D])
+    for algo in ("fpi", "vmp", "mmp"):
+        worst = max(worst, float(np.abs(infer(algo, w.model, w.obs, w.act, w.iters) -
+                                        infer(algo, rep, w.obs, w.act, w.iters)).max()))
+    return worst
+
+
+ALL_PINS = {
+    "bayes_filter": (pin_bayes_filter, 1e-12),
+    "golden_hmm2": (pin_golden_hmm2, 1e-7),
+    "vmp_bruteforce": (pin_vmp_bruteforce, 1e-12),
+    "fpi_bruteforce": (pin_fpi_bruteforce, 1e-12),
+    "factorised_exact": (pin_factorised_exact, 1e-12),
+    "t1_identity": (pin_t1_identity, 1e-12),
+    "iid_closed_forms": (pin_iid_closed_forms, 1e-12),
+    "mmp_permutation_smoothing": (pin_mmp_permutation_smoothing, 1e-10),
+    "invariants": (pin_invariants, 1e-12),
+}

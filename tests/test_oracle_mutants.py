@@ -1,0 +1,65 @@
+"""Plant plausible mistakes into a copy of the oracle (CPU only) and check that
+at least one pin catches each of them."""
+import functools
+import os
+import subprocess
+
+import pytest
+
+import oracle
+from oracle import oracle as orc_mod
+from oracle_pins import ALL_PINS
+
+SRC = os.path.join(os.path.dirname(orc_mod.__file__), "bi_oracle.c")
+
+# (name, text in bi_oracle.c, replacement, count)
+MUTANTS = [
+    ("vmp_fwd_transposed", "fwd += LN(Bv(md, Bf, f, s, sp, uprev)) * qprev[sp];",
+     "fwd += LN(Bv(md, Bf, f, sp, s, uprev)) * qprev[sp];", 1),
+    ("vmp_bwd_transposed", "bwd += qnext[sn] * LN(Bv(md, Bf, f, sn, s, unext));",
+     "bwd += qnext[sn] * LN(Bv(md, Bf, f, s, sn, unext));", 1),
+    ("mmp_fwd_transposed", "p += Bv(md, Bf, f, s, sp, uprev) * qprev[sp];",
+     "p += Bv(md, Bf, f, sp, s, uprev) * qprev[sp];", 1),
+    ("mmp_bwd_transposed", "p += Bv(md, Bf, f, sn, s, unext) * qnext[sn];",
+     "p += Bv(md, Bf, f, s, sn, unext) * qnext[sn];", 1),
+    ("mmp_no_half", "0.5 * (fwd + bwd)", "(fwd + bwd)", 1),
+    ("mmp_last_half", "v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd;",
+     "v[s] = lam[(size_t)t * ntot + qoff[f] + s] + 0.5 * fwd;", 1),
+    ("fpi_prior_transposed", "p += Bv(md, Bf, f, i, j, u) * qp[j];", "p += Bv(md, Bf, f, j, i, u) * qp[j];", 1),
+    ("lik_keeps_own_factor", "if (j != i) w *= q[qoff[d[j]] + idx[j]];", "w *= q[qoff[d[j]] + idx[j]];", 1),
+    ("lik_axis_order", "for (int i = k - 1; i >= 0; --i) {\n                if (++idx[i]",
+     "for (int i = 0; i < k; ++i) {\n                if (++idx[i]", 1),
+    ("vmp_drops_prior", "fwd = LN(Df[s]);", "fwd = 0.0;", 1),
+    ("softmax_sign", "v[i] = exp(v[i] - mx);", "v[i] = exp(mx - v[i]);", 1),
+    ("no_log_clamp", "return log(x > ORC_EPS ? x : ORC_EPS);", "return log(x > 0 ? x : 1e-300);", 1),
+]
+
+
+@functools.lru_cache(maxsize=None)
+def _mutant_lib(tmpdir, name):
+    src = open(SRC).read()
+    for mname, old, new, count in MUTANTS:
+        if mname == name:
+            assert old in src, f"mutation anchor of {name} not found"
+            src = src.replace(old, new, count)
+    path = os.path.join(tmpdir, f"mut_{name}.c")
+    with open(path, "w") as fh:
+        fh.write(src)
+    so = path[:-2] + ".so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-o", so, path, "-lm"], check=True)
+    return orc_mod.load_library(so)
+
+
+@pytest.mark.parametrize("name", [m[0] for m in MUTANTS if m[3] > 0])
+def test_mutant_is_caught(name, tmp_path_factory):
+    lib = _mutant_lib(str(tmp_path_factory.getbasetemp()), name)
+    infer = functools.partial(oracle.infer, lib=lib)
+    failed = []
+    for pin, (fn, tol) in ALL_PINS.items():
+        try:
+            err = fn(infer)
+        except (ValueError, FloatingPointError):
+            err = float("inf")
+        if not err <= tol:
+            failed.append(pin)
+    assert failed, f"planted mistake {name} passed every pin"

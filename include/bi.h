@@ -1,0 +1,194 @@
+/*
+ * bi.h — C-ABI of libbi, MI355X (gfx950) belief updates for discrete
+ * HMM / POMDP generative models: variational filtering (FPI), variational
+ * message passing (VMP) and marginal message passing (MMP).
+ *
+ * The generative model is the factorised POMDP of Sec. III-B of "A
+ * Hardware-oriented Approach for Efficient Bayesian Inference Computation and
+ * Deployment" (joint over o_{1:T}, s_{1:T} given u_{1:T-1}; emission tensors
+ * A_m with arbitrary A-dependency lists, transition tensors B_f with trivial
+ * B-dependencies, prior D).  The three updates are built from the likelihood
+ * and transition messages of Sec. IV, each an instance of the coordinate
+ * update of Sec. III-A; the exact readings are stated per entry point.
+ *
+ * Conventions shared by every entry point:
+ *  - Every function returns 0 (BI_OK) or a negative BI_ERR_* code and never
+ *    throws; bi_last_error() then describes the failure (thread-local).
+ *  - "host" pointers are ordinary CPU memory; "device" pointers are HIP device
+ *    memory of the current device (e.g. torch tensors).  The caller owns all
+ *    memory; the library borrows device pointers until the work it enqueued
+ *    on the given stream has completed.
+ *  - hip_stream is a hipStream_t passed as void* (NULL = the null stream).
+ *    Inference calls only enqueue kernels on it: no host synchronisation, no
+ *    device allocation, no host<->device copies.  Arguments are validated on
+ *    the host before anything is enqueued.
+ *  - Layouts are C row-major.  sum_n = n_0 + ... + n_{F-1}.
+ */
+#ifndef BI_H
+#define BI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define BI_OK 0
+#define BI_ERR_INVALID_ARG (-1)      /* null pointer, non-positive size, bad enum, ... */
+#define BI_ERR_SHAPE (-2)            /* inconsistent shapes or dependency lists       */
+#define BI_ERR_BUFFER_TOO_SMALL (-3) /* dev_bytes / ws_bytes below what is required   */
+#define BI_ERR_UNSUPPORTED (-4)      /* valid, but beyond what this build handles     */
+#define BI_ERR_DEVICE (-5)           /* a HIP runtime call failed                     */
+
+/* bi_model_desc.flags: layout of the emission tensors on the device. */
+#define BI_DENSE_A 1u  /* dense log-domain slices (default)                         */
+#define BI_SPARSE_A 2u /* sparse slices: only nonzero A entries are stored           */
+
+/* Algorithm ids (bi_workspace_size). */
+#define BI_ALGO_FPI 0
+#define BI_ALGO_VMP 1
+#define BI_ALGO_MMP 2
+
+/*
+ * Shape of a generative model (Sec. III-B).
+ *   F factors with n[f] states and U[f] actions each; M modalities with K[m]
+ *   outcomes each; modality m depends on the factors
+ *   dep[dep_off[m] .. dep_off[m+1]-1], a non-empty, strictly ascending list
+ *   (the A-dependency list).  model_batch is 1 when every agent shares the
+ *   model, otherwise the number of agents, each with its own parameters (the
+ *   batch axis b of Sec. III-B).  flags: BI_DENSE_A or BI_SPARSE_A (0 = dense).
+ */
+typedef struct bi_model_desc {
+    int32_t F;
+    const int32_t *n;       /* [F] host */
+    const int32_t *U;       /* [F] host */
+    int32_t M;
+    const int32_t *K;       /* [M] host */
+    const int32_t *dep_off; /* [M+1] host, dep_off[0] = 0 */
+    const int32_t *dep;     /* [dep_off[M]] host */
+    int32_t model_batch;
+    uint32_t flags;
+} bi_model_desc;
+
+/* Opaque handle: host-side metadata of a packed model (the packed tensors
+ * live in the caller's device buffer). */
+typedef struct bi_model bi_model;
+
+/* Parameter counts of a packed model (the paper's memory proxy, Sec. V). */
+typedef struct bi_model_stats {
+    int64_t a_raw;        /* entries of the A tensors as given                 */
+    int64_t a_stored;     /* A entries stored on the device (dense incl. pad)  */
+    int64_t a_nnz;        /* nonzero A entries                                 */
+    int64_t device_bytes; /* bytes of the packed device buffer in use          */
+} bi_model_stats;
+
+/* Thread-local description of the last error (never NULL). */
+const char *bi_last_error(void);
+
+/*
+ * Size of the device buffer that bi_pack_model needs for this model shape.
+ * Host only.  For BI_SPARSE_A the size depends on the values of A, so this
+ * returns an upper bound (the dense size plus index storage); bi_pack_model
+ * reports the exact use in bi_model_stats.device_bytes.
+ */
+int bi_plan_model(const bi_model_desc *desc, size_t *device_bytes);
+
+/*
+ * Pack a model into the caller's device buffer (the one-time layout step of
+ * Sec. III-C: "performed only once during initialization").
+ *   A[m]: host float [model_batch][K_m][n_{d1}]..[n_{dk}], P(o^m | s^{dep(m)})
+ *   B[f]: host float [model_batch][n_f][n_f][U_f], B[i][j][u] = P(s'=i | s=j, u)
+ *   D[f]: host float [model_batch][n_f], p(s_1^f)
+ *   dev_buf: device memory of at least bi_plan_model bytes, 256-byte aligned.
+ * The host arrays are read before the call returns (they may be freed
+ * afterwards).  The call copies to the device on hip_stream and synchronises
+ * that stream before returning.  *out receives a handle to free with
+ * bi_free_model; the caller keeps dev_buf alive while the handle is used.
+ * Probabilities are not required to be normalised; zeros are allowed (their
+ * logarithm is clamped to log(1e-16)).
+ */
+int bi_pack_model(const bi_model_desc *desc, const float *const *A, const float *const *B,
+                  const float *const *D, void *dev_buf, size_t dev_bytes, void *hip_stream, bi_model **out);
+
+/*
+ * Host-only variant of bi_pack_model: writes the same packed image into host
+ * memory (host_buf, at least bi_plan_model bytes, 256-byte aligned) and
+ * returns a handle that has no device buffer yet.  Copy the image to a device
+ * buffer yourself (or save it and reload it later) and declare it with
+ * bi_attach_device_buffer before inference.  Needs no GPU.
+ */
+int bi_pack_model_host(const bi_model_desc *desc, const float *const *A, const float *const *B,
+                       const float *const *D, void *host_buf, size_t host_bytes, bi_model **out);
+
+/*
+ * Declare that dev_buf (device memory, 256-byte aligned, dev_bytes >= the
+ * packed size) holds a byte-identical copy of the image that
+ * bi_pack_model_host wrote for this handle.  The library does not check the
+ * contents.  Replaces any buffer attached before.
+ */
+int bi_attach_device_buffer(bi_model *model, void *dev_buf, size_t dev_bytes);
+
+/* Parameter counts of a packed model. */
+int bi_get_model_stats(const bi_model *model, bi_model_stats *out);
+
+/*
+ * Device workspace (bytes, 256-byte aligned start required) that an inference
+ * call with b agents, window T and algorithm algo needs; may be 0, in which
+ * case ws_dev may be NULL.
+ */
+int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo, size_t *bytes);
+
+/*
+ * Variational filtering ("FPI", Sec. I and IV): for t = 0..T-1 in order, the
+ * prior of step t is D (t = 0) or B_f[:,:,u_{t-1,f}] q_{t-1,f} (the final
+ * marginal of the previous step); q_t starts uniform and takes `iters`
+ * Jacobi sweeps of q_{t,f} = softmax(lam_{t,f} + log prior_{t,f}), where the
+ * likelihood message is
+ *   lam_{t,f}(s) = sum_{m: f in dep(m)} sum_{s_dep: s_f = s}
+ *                  log A_m[o_{t,m}, s_dep] prod_{g in dep(m), g != f} q_{t,g}(s_g)
+ * (the marginalisation step of Sec. IV).
+ *   obs_dev: device int32 [b][T][M], 0 <= obs < K_m
+ *   act_dev: device int32 [b][T-1][F], 0 <= act < U_f (may be NULL if T == 1)
+ *   q_dev:   device float [b][T][sum_n], output posterior marginals
+ *   ws_dev:  device workspace of ws_bytes >= bi_workspace_size(..., BI_ALGO_FPI)
+ * b must equal model_batch unless model_batch == 1.  Out-of-range obs/act
+ * values are undefined behaviour.
+ */
+int bi_vfilter(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+               int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream);
+
+/*
+ * Variational message passing over the window (Sec. III-A update applied to
+ * the joint of Sec. III-B with q = prod_{t,f} q_{t,f}): q starts uniform and
+ * takes `iters` Jacobi sweeps over every (t, f) of
+ *   q_{t,f} = softmax(lam_{t,f} + fwd_{t,f} + bwd_{t,f}),
+ *   fwd = log D_f (t = 0), else sum_{s'} log B_f[s, s', u_{t-1}] q_{t-1,f}(s'),
+ *   bwd = 0 (t = T-1),    else sum_{s''} q_{t+1,f}(s'') log B_f[s'', s, u_t].
+ * Arguments as bi_vfilter.
+ */
+int bi_vmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+           int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream);
+
+/*
+ * Marginal message passing over the window (Sec. I and IV): as bi_vmp but with
+ * the marginal (log-of-expectation) transition messages
+ *   fwd = log D_f (t = 0), else log(B_f[:,:,u_{t-1}] q_{t-1,f}),
+ *   bwd = log(B_f[:,:,u_t]^T q_{t+1,f}) (t < T-1),
+ * averaged over the messages present:
+ *   q_{t,f} = softmax(lam + (fwd + bwd) / 2) for t < T-1, softmax(lam + fwd) at t = T-1.
+ * Arguments as bi_vfilter.
+ */
+int bi_mmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+           int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream);
+
+/* Free the host metadata of a packed model (not the caller's device buffer).
+ * NULL is ignored. */
+void bi_free_model(bi_model *model);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BI_H */

@@ -1,0 +1,239 @@
+"""Thin ctypes binding of libbi's C-ABI (include/bi.h).
+
+Functions keep the C names.  Device buffers are torch tensors on the current
+HIP device; streams are torch streams.  This module only marshals arguments:
+every step of the belief updates runs in the HIP kernels of libbi.so, and the
+module raises if the library is missing or cannot be loaded.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libbi.so")
+
+BI_OK = 0
+BI_ERR_INVALID_ARG = -1
+BI_ERR_SHAPE = -2
+BI_ERR_BUFFER_TOO_SMALL = -3
+BI_ERR_UNSUPPORTED = -4
+BI_ERR_DEVICE = -5
+BI_DENSE_A = 1
+BI_SPARSE_A = 2
+BI_ALGO_FPI, BI_ALGO_VMP, BI_ALGO_MMP = 0, 1, 2
+ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
+
+EXPORTS = ("bi_last_error", "bi_plan_model", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
+           "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_free_model")
+
+
+class BiError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{msg} (code {code})")
+        self.code = code
+
+
+class bi_model_desc(ctypes.Structure):
+    _fields_ = [("F", ctypes.c_int32), ("n", ctypes.POINTER(ctypes.c_int32)), ("U", ctypes.POINTER(ctypes.c_int32)),
+                ("M", ctypes.c_int32), ("K", ctypes.POINTER(ctypes.c_int32)),
+                ("dep_off", ctypes.POINTER(ctypes.c_int32)), ("dep", ctypes.POINTER(ctypes.c_int32)),
+                ("model_batch", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+class bi_model_stats(ctypes.Structure):
+    _fields_ = [("a_raw", ctypes.c_int64), ("a_stored", ctypes.c_int64), ("a_nnz", ctypes.c_int64),
+                ("device_bytes", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libbi.so (built in-tree by paper_2607_17855_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"libbi.so not found at {path}: build it with `python -m paper_2607_17855_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    P = ctypes.POINTER
+    lib.bi_last_error.restype = ctypes.c_char_p
+    lib.bi_last_error.argtypes = []
+    lib.bi_plan_model.argtypes = [P(bi_model_desc), P(sz)]
+    lib.bi_pack_model.argtypes = [P(bi_model_desc), P(vp), P(vp), P(vp), vp, sz, vp, P(vp)]
+    lib.bi_pack_model_host.argtypes = [P(bi_model_desc), P(vp), P(vp), P(vp), vp, sz, P(vp)]
+    lib.bi_attach_device_buffer.argtypes = [vp, vp, sz]
+    lib.bi_get_model_stats.argtypes = [vp, P(bi_model_stats)]
+    lib.bi_workspace_size.argtypes = [vp, i32, i32, i32, P(sz)]
+    for name in ("bi_vfilter", "bi_vmp", "bi_mmp"):
+        getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, sz, vp]
+    lib.bi_free_model.argtypes = [vp]
+    lib.bi_free_model.restype = None
+    for name in EXPORTS[1:-1]:
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def bi_last_error() -> str:
+    return load().bi_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != BI_OK:
+        raise BiError(rc, bi_last_error())
+
+
+class _Desc:
+    """Keeps the int32 arrays of a bi_model_desc alive."""
+
+    def __init__(self, n, U, K, deps, model_batch: int, flags: int):
+        self.n = np.ascontiguousarray(n, dtype=np.int32)
+        self.U = np.ascontiguousarray(U, dtype=np.int32)
+        self.K = np.ascontiguousarray(K, dtype=np.int32)
+        self.dep_off = np.ascontiguousarray(np.cumsum([0] + [len(d) for d in deps]), dtype=np.int32)
+        self.dep = np.ascontiguousarray([f for d in deps for f in d], dtype=np.int32)
+        if self.dep.size == 0:
+            self.dep = np.zeros(1, dtype=np.int32)
+        ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))  # noqa: E731
+        self.c = bi_model_desc(len(self.n), ip(self.n), ip(self.U), len(self.K), ip(self.K), ip(self.dep_off),
+                               ip(self.dep), int(model_batch), int(flags))
+
+
+def bi_plan_model(n, U, K, deps, model_batch: int, flags: int = BI_DENSE_A) -> int:
+    d = _Desc(n, U, K, deps, model_batch, flags)
+    out = ctypes.c_size_t(0)
+    _check(load().bi_plan_model(ctypes.byref(d.c), ctypes.byref(out)))
+    return int(out.value)
+
+
+def _stream_ptr(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def bi_pack_model(n, U, K, deps, model_batch: int, A: Sequence[np.ndarray], B: Sequence[np.ndarray],
+                  D: Sequence[np.ndarray], dev_buf, flags: int = BI_DENSE_A, stream=None) -> int:
+    """Pack host float32 A/B/D into the device tensor ``dev_buf``; returns the handle."""
+    d = _Desc(n, U, K, deps, model_batch, flags)
+    A = [np.ascontiguousarray(a, dtype=np.float32) for a in A]
+    B = [np.ascontiguousarray(b, dtype=np.float32) for b in B]
+    D = [np.ascontiguousarray(x, dtype=np.float32) for x in D]
+    ptrs = lambda arrs: (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])  # noqa: E731
+    out = ctypes.c_void_p(0)
+    nbytes = dev_buf.numel() * dev_buf.element_size()
+    _check(load().bi_pack_model(ctypes.byref(d.c), ptrs(A), ptrs(B), ptrs(D), ctypes.c_void_p(dev_buf.data_ptr()),
+                                nbytes, ctypes.c_void_p(_stream_ptr(stream)), ctypes.byref(out)))
+    return int(out.value)
+
+
+def bi_pack_model_host(n, U, K, deps, model_batch: int, A, B, D, flags: int = BI_DENSE_A):
+    """Pack into host memory; returns (handle, uint8 numpy image)."""
+    d = _Desc(n, U, K, deps, model_batch, flags)
+    nbytes = bi_plan_model(n, U, K, deps, model_batch, flags)
+    raw = np.zeros(nbytes + 512, dtype=np.uint8)
+    start = (-raw.ctypes.data) % 256
+    img = raw[start:start + nbytes]
+    A = [np.ascontiguousarray(a, dtype=np.float32) for a in A]
+    B = [np.ascontiguousarray(b, dtype=np.float32) for b in B]
+    D = [np.ascontiguousarray(x, dtype=np.float32) for x in D]
+    ptrs = lambda arrs: (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])  # noqa: E731
+    out = ctypes.c_void_p(0)
+    _check(load().bi_pack_model_host(ctypes.byref(d.c), ptrs(A), ptrs(B), ptrs(D), ctypes.c_void_p(img.ctypes.data),
+                                     nbytes, ctypes.byref(out)))
+    return int(out.value), img
+
+
+def bi_attach_device_buffer(handle: int, dev_buf):
+    nbytes = dev_buf.numel() * dev_buf.element_size()
+    _check(load().bi_attach_device_buffer(ctypes.c_void_p(handle), ctypes.c_void_p(dev_buf.data_ptr()), nbytes))
+
+
+def bi_get_model_stats(handle: int) -> dict:
+    st = bi_model_stats()
+    _check(load().bi_get_model_stats(ctypes.c_void_p(handle), ctypes.byref(st)))
+    return {k: int(getattr(st, k)) for k, _ in bi_model_stats._fields_}
+
+
+def bi_workspace_size(handle: int, b: int, T: int, algo: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().bi_workspace_size(ctypes.c_void_p(handle), int(b), int(T), int(algo), ctypes.byref(out)))
+    return int(out.value)
+
+
+def _infer(fn_name, handle, b, T, obs, act, iters, q, ws, stream):
+    ws_ptr = ws.data_ptr() if ws is not None else 0
+    ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    act_ptr = act.data_ptr() if act is not None and act.numel() > 0 else 0
+    _check(getattr(load(), fn_name)(ctypes.c_void_p(handle), int(b), int(T), ctypes.c_void_p(obs.data_ptr()),
+                                    ctypes.c_void_p(act_ptr), int(iters), ctypes.c_void_p(q.data_ptr()),
+                                    ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(_stream_ptr(stream))))
+
+
+def bi_vfilter(handle, b, T, obs, act, iters, q, ws=None, stream=None):
+    _infer("bi_vfilter", handle, b, T, obs, act, iters, q, ws, stream)
+
+
+def bi_vmp(handle, b, T, obs, act, iters, q, ws=None, stream=None):
+    _infer("bi_vmp", handle, b, T, obs, act, iters, q, ws, stream)
+
+
+def bi_mmp(handle, b, T, obs, act, iters, q, ws=None, stream=None):
+    _infer("bi_mmp", handle, b, T, obs, act, iters, q, ws, stream)
+
+
+def bi_free_model(handle: int):
+    load().bi_free_model(ctypes.c_void_p(handle))
+
+
+_ENTRY = {"fpi": bi_vfilter, "vmp": bi_vmp, "mmp": bi_mmp}
+
+
+class PackedModel:
+    """A model packed into a torch device buffer, with its C handle."""
+
+    def __init__(self, model, flags: int = BI_DENSE_A, device=None, stream=None):
+        import torch
+        self.model = model
+        nbytes = bi_plan_model(model.n, model.U, model.K, model.deps, model.mb, flags)
+        self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device or "cuda")
+        self.handle = bi_pack_model(model.n, model.U, model.K, model.deps, model.mb, model.A, model.B, model.D,
+                                    self.buf, flags, stream)
+        self.flags = flags
+
+    def stats(self) -> dict:
+        return bi_get_model_stats(self.handle)
+
+    def workspace(self, b: int, T: int, algo: str):
+        import torch
+        nb = bi_workspace_size(self.handle, b, T, ALGO_IDS[algo])
+        return torch.empty(nb, dtype=torch.uint8, device=self.buf.device) if nb else None
+
+    def infer(self, algo: str, obs, act, iters: int, q=None, ws=None, stream=None):
+        """obs [b][T][M] / act [b][T-1][F] int32 device tensors -> q [b][T][sum n] float32."""
+        import torch
+        b, T = int(obs.shape[0]), int(obs.shape[1])
+        if q is None:
+            q = torch.empty((b, T, sum(self.model.n)), dtype=torch.float32, device=self.buf.device)
+        if ws is None:
+            ws = self.workspace(b, T, algo)
+        _ENTRY[algo](self.handle, b, T, obs, act, iters, q, ws, stream)
+        return q
+
+    def close(self):
+        if getattr(self, "handle", 0):
+            bi_free_model(self.handle)
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,207 @@
+// extern "C" entry points of libbi (declared in include/bi.h).
+#include <cstring>
+#include <new>
+
+#include "internal.h"
+
+namespace bi {
+const char *last_error();
+int fill(const bi_model *m, const float *const *A, const float *const *B, const float *const *D, char *host,
+         int64_t *nnz_out);
+}  // namespace bi
+
+using bi::fail;
+
+extern "C" {
+
+const char *bi_last_error(void) { return bi::last_error(); }
+
+int bi_plan_model(const bi_model_desc *desc, size_t *device_bytes)
+{
+    try {
+        if (!device_bytes) return fail(BI_ERR_INVALID_ARG, "device_bytes is NULL");
+        bi_model m;
+        const int rc = bi::plan(desc, &m);
+        if (rc != BI_OK) return rc;
+        *device_bytes = (size_t)m.bytes;
+        return BI_OK;
+    } catch (const std::bad_alloc &) {
+        return fail(BI_ERR_INVALID_ARG, "host allocation failed");
+    } catch (...) {
+        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
+    }
+}
+
+// Plan + fill into host memory; on success *out owns the metadata.
+static int pack_host(const bi_model_desc *desc, const float *const *A, const float *const *B, const float *const *D,
+                     char *host, size_t host_bytes, bi_model **out)
+{
+    *out = nullptr;
+    if (!A || !B || !D) return fail(BI_ERR_INVALID_ARG, "A, B and D must be non-NULL");
+    bi_model *m = new bi_model;
+    int rc = bi::plan(desc, m);
+    if (rc != BI_OK) {
+        delete m;
+        return rc;
+    }
+    for (int i = 0; i < m->M; ++i)
+        if (!A[i]) {
+            delete m;
+            return fail(BI_ERR_INVALID_ARG, "A[%d] is NULL", i);
+        }
+    for (int i = 0; i < m->F; ++i)
+        if (!B[i] || !D[i]) {
+            delete m;
+            return fail(BI_ERR_INVALID_ARG, "B[%d] or D[%d] is NULL", i, i);
+        }
+    if (host == nullptr) {  // caller only wanted the plan checked
+        *out = m;
+        return BI_OK;
+    }
+    if ((int64_t)host_bytes < m->bytes) {
+        const long long need = (long long)m->bytes;
+        delete m;
+        return fail(BI_ERR_BUFFER_TOO_SMALL, "buffer of %zu bytes < %lld required", host_bytes, need);
+    }
+    std::memset(host, 0, (size_t)m->bytes);
+    int64_t nnz = 0;
+    bi::fill(m, A, B, D, host, &nnz);
+    m->stats.a_nnz = nnz;
+    *out = m;
+    return BI_OK;
+}
+
+int bi_pack_model_host(const bi_model_desc *desc, const float *const *A, const float *const *B,
+                       const float *const *D, void *host_buf, size_t host_bytes, bi_model **out)
+{
+    try {
+        if (!out) return fail(BI_ERR_INVALID_ARG, "out is NULL");
+        *out = nullptr;
+        if (!host_buf) return fail(BI_ERR_INVALID_ARG, "host_buf is NULL");
+        if (reinterpret_cast<uintptr_t>(host_buf) % bi::kAlign)
+            return fail(BI_ERR_INVALID_ARG, "host_buf must be %d-byte aligned", bi::kAlign);
+        return pack_host(desc, A, B, D, reinterpret_cast<char *>(host_buf), host_bytes, out);
+    } catch (const std::bad_alloc &) {
+        return fail(BI_ERR_INVALID_ARG, "host allocation failed");
+    } catch (...) {
+        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
+    }
+}
+
+int bi_attach_device_buffer(bi_model *model, void *dev_buf, size_t dev_bytes)
+{
+    if (!model || !dev_buf) return fail(BI_ERR_INVALID_ARG, "model and dev_buf must be non-NULL");
+    if (reinterpret_cast<uintptr_t>(dev_buf) % bi::kAlign)
+        return fail(BI_ERR_INVALID_ARG, "dev_buf must be %d-byte aligned", bi::kAlign);
+    if ((int64_t)dev_bytes < model->bytes)
+        return fail(BI_ERR_BUFFER_TOO_SMALL, "dev_bytes %zu < %lld required", dev_bytes, (long long)model->bytes);
+    model->dev = reinterpret_cast<char *>(dev_buf);
+    if (hipGetDevice(&model->device) != hipSuccess) model->device = 0;
+    return BI_OK;
+}
+
+int bi_pack_model(const bi_model_desc *desc, const float *const *A, const float *const *B, const float *const *D,
+                  void *dev_buf, size_t dev_bytes, void *hip_stream, bi_model **out)
+{
+    try {
+        if (!out) return fail(BI_ERR_INVALID_ARG, "out is NULL");
+        *out = nullptr;
+        if (!dev_buf) return fail(BI_ERR_INVALID_ARG, "dev_buf is NULL");
+        if (reinterpret_cast<uintptr_t>(dev_buf) % bi::kAlign)
+            return fail(BI_ERR_INVALID_ARG, "dev_buf must be %d-byte aligned", bi::kAlign);
+        bi_model *m = nullptr;
+        int rc = pack_host(desc, A, B, D, nullptr, 0, &m);  // validate before allocating
+        if (rc != BI_OK) return rc;
+        if ((int64_t)dev_bytes < m->bytes) {
+            const long long need = (long long)m->bytes;
+            delete m;
+            return fail(BI_ERR_BUFFER_TOO_SMALL, "dev_bytes %zu < %lld required", dev_bytes, need);
+        }
+        const size_t bytes = (size_t)m->bytes;
+        delete m;
+        char *host = nullptr;
+        if (hipHostMalloc((void **)&host, bytes, hipHostMallocDefault) != hipSuccess)
+            return fail(BI_ERR_DEVICE, "hipHostMalloc of %zu bytes failed", bytes);
+        rc = pack_host(desc, A, B, D, host, bytes, &m);
+        if (rc != BI_OK) {
+            hipHostFree(host);
+            return rc;
+        }
+        hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+        hipError_t e = hipMemcpyAsync(dev_buf, host, bytes, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        hipHostFree(host);
+        if (e != hipSuccess) {
+            delete m;
+            return fail(BI_ERR_DEVICE, "copy to device failed: %s", hipGetErrorString(e));
+        }
+        m->dev = reinterpret_cast<char *>(dev_buf);
+        if (hipGetDevice(&m->device) != hipSuccess) m->device = 0;
+        *out = m;
+        return BI_OK;
+    } catch (const std::bad_alloc &) {
+        return fail(BI_ERR_INVALID_ARG, "host allocation failed");
+    } catch (...) {
+        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
+    }
+}
+
+int bi_get_model_stats(const bi_model *model, bi_model_stats *out)
+{
+    if (!model || !out) return fail(BI_ERR_INVALID_ARG, "model and out must be non-NULL");
+    *out = model->stats;
+    return BI_OK;
+}
+
+int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo, size_t *bytes)
+{
+    if (!model || !bytes) return fail(BI_ERR_INVALID_ARG, "model and bytes must be non-NULL");
+    if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
+    if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
+    *bytes = 0;
+    return BI_OK;
+}
+
+static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const int32_t *obs, const int32_t *act,
+                 int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream)
+{
+    try {
+        if (!model) return fail(BI_ERR_INVALID_ARG, "model is NULL");
+        if (!model->dev) return fail(BI_ERR_INVALID_ARG, "model has no device buffer (bi_attach_device_buffer)");
+        if (b < 1 || T < 1 || iters < 1) return fail(BI_ERR_INVALID_ARG, "b, T and iters must be >= 1");
+        if (model->mb != 1 && model->mb != b)
+            return fail(BI_ERR_SHAPE, "b=%d but the model holds %d agents", b, model->mb);
+        if (!obs || !q) return fail(BI_ERR_INVALID_ARG, "obs and q must be non-NULL");
+        if (T > 1 && !act) return fail(BI_ERR_INVALID_ARG, "act must be non-NULL when T > 1");
+        size_t need = 0;
+        int rc = bi_workspace_size(model, b, T, algo, &need);
+        if (rc != BI_OK) return rc;
+        if (ws_bytes < need) return fail(BI_ERR_BUFFER_TOO_SMALL, "ws_bytes %zu < %zu required", ws_bytes, need);
+        if (need > 0 && !ws) return fail(BI_ERR_INVALID_ARG, "ws is NULL");
+        return bi::launch_agent(model, algo, b, T, obs, act, iters, q, reinterpret_cast<hipStream_t>(stream));
+    } catch (...) {
+        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
+    }
+}
+
+int bi_vfilter(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+               int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
+{
+    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_vmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+           int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
+{
+    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_mmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+           int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
+{
+    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+void bi_free_model(bi_model *model) { delete model; }
+
+}  // extern "C"

@@ -1,0 +1,42 @@
+// Host-side state of libbi (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/bi.h"
+#include "layout.h"
+
+struct bi_model {
+    int32_t F = 0, M = 0, mb = 1;
+    uint32_t flags = BI_DENSE_A;
+    std::vector<int32_t> n, U, K, dep_off, dep;
+    std::vector<bi::ModDesc> mods;
+    std::vector<bi::FacDesc> facs;
+    int32_t ntot = 0;      // sum of n
+    int32_t zvpc = 0;      // floats of Z/V scratch per context: sum_m (R_m + C_m)
+    int32_t max_rank = 0;
+    int64_t bytes = 0;     // bytes of the packed device buffer in use
+    char *dev = nullptr;   // caller's device buffer
+    int device = 0;        // HIP device the buffer lives on
+    bi_model_stats stats{};
+};
+
+namespace bi {
+
+// Record a failure for bi_last_error() and return `code`.
+int fail(int code, const char *fmt, ...);
+
+// Layout planning shared by bi_plan_model and bi_pack_model; fills the
+// descriptors and offsets of `m` (no data).  Returns BI_OK or an error code.
+int plan(const bi_model_desc *desc, bi_model *m);
+
+// Agent-resident launches (one workgroup per agent, every iteration in-kernel).
+// Returns BI_OK or an error code.
+int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
+                 float *q, hipStream_t stream);
+
+}  // namespace bi

@@ -1,0 +1,73 @@
+// Device layout of a packed model (internal to libbi; not part of the ABI).
+//
+// The packed buffer starts with the descriptor tables, followed by the
+// parameter arrays, each 256-byte aligned (all offsets below are in bytes):
+//
+//   ModDesc[M] | FacDesc[F] | LA (dense, fp64) | sparse A | B (fp32) | LB (fp64) | LD (fp64)
+//
+// Precision.  The mean-field fixed-point iterations are ill-conditioned for
+// some models: a relative perturbation of 1e-7 in A (fp32 rounding) moves
+// some marginals by more than 1e-4 after 16 Jacobi sweeps.  Everything in the
+// log domain is therefore stored and combined in double precision; B keeps
+// the caller's fp32 values exactly.
+//
+// Emission slices ("two-sided" view).  For modality m with A-dependency list
+// (d_1 < ... < d_k) the slice LA_m[o] of every outcome o is stored as a
+// matrix X[r][c] with the first p dependency axes flattened into rows and the
+// remaining k-p into columns (row-major, last axis fastest, exactly the order
+// of the user's A).  Columns are padded with zeros to a multiple of 4 so that
+// every row starts 32-byte aligned.  The stored value is the shifted log
+//   X = log(max(A, 1e-16)) - c_{m,o}
+// where c_{m,o} is the median of the slice (dense) or log(1e-16) (sparse).
+// The shift is exact in the updates: it adds c * prod_{g != f} sum_s q_g(s) to
+// every entry of lam_f, a constant over the states of f that the softmax
+// removes.
+//
+// With this view the likelihood messages of one context need two passes over
+// the slice, Z = X t and V = s X, where t is the outer product of the column
+// factors' marginals and s that of the row factors'; every lam_f of the
+// modality is then a small contraction of Z (row factors) or V (column
+// factors).
+#pragma once
+
+#include <stdint.h>
+
+namespace bi {
+
+constexpr double kEps = 1e-16;
+constexpr int kMaxSide = 2;   // factors per side of the two-sided view (rank <= 4)
+constexpr int kAlign = 256;   // byte alignment of every array in the packed buffer
+
+struct ModDesc {
+    int64_t la_off;    // byte offset of the dense fp64 slices [agent][K][R][Cp]
+    int64_t la_agent;  // elements per agent (0 when the model is shared)
+    int32_t K;         // outcomes
+    int32_t slice;     // elements per outcome slice = R * Cp
+    int32_t rank;      // |dep(m)|
+    int32_t R, C, Cp;  // rows, columns, padded columns
+    int32_t nrow;      // factors on the row side (0..2)
+    int32_t ncol;      // factors on the column side (1..2)
+    int32_t rf[kMaxSide], rn[kMaxSide];  // row factors, ascending, and their sizes
+    int32_t cf[kMaxSide], cn[kMaxSide];  // column factors, ascending, and sizes
+    int32_t zv_off;    // offset of this modality's Z (R values) then V (C values) in a context's block
+    int32_t pad0;
+    // sparse layout (BI_SPARSE_A): per (agent, outcome) slice, the nonzero
+    // entries in row-major order as (row, col) index pairs and shifted values
+    int64_t sp_ptr_off;  // byte offset of int64 [agent][K+1] entry pointers, or -1
+    int64_t sp_idx_off;  // byte offset of packed (row << 16 | col) uint32 indices
+    int64_t sp_val_off;  // byte offset of values
+};
+
+struct FacDesc {
+    int64_t b_off;    // byte offset of fp32 B as [agent][u][i][j] = P(s'=i | s=j, u)
+    int64_t lb_off;   // byte offset of fp64 log B, same layout
+    int64_t ld_off;   // byte offset of fp64 log D as [agent][n]
+    int64_t b_agent;  // elements per agent of B / LB (0 when shared)
+    int32_t ld_agent; // elements per agent of LD (0 when shared)
+    int32_t n, U;
+    int32_t q_off;    // offset of this factor in a context's marginal vector
+};
+
+inline int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace bi

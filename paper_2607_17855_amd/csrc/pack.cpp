@@ -1,0 +1,240 @@
+// Host packer: validates a model description, plans the device layout of
+// layout.h and converts the user's A / B / D tensors into it.  This is the
+// one-time padding/merging step of Sec. III-C (done once at initialisation,
+// no cost at inference time); the layout itself is the two-sided slice view
+// described in layout.h rather than the paper's axis-aligned or
+// block-diagonal merge.
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <thread>
+
+#include "internal.h"
+
+namespace bi {
+
+static thread_local std::string g_err = "no error";
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+const char *last_error() { return g_err.c_str(); }
+
+static int64_t prod(const int32_t *n, const int32_t *f, int k)
+{
+    int64_t p = 1;
+    for (int i = 0; i < k; ++i) p *= n[f[i]];
+    return p;
+}
+
+int plan(const bi_model_desc *d, bi_model *m)
+{
+    if (!d) return fail(BI_ERR_INVALID_ARG, "desc is NULL");
+    if (d->F < 1 || d->M < 1) return fail(BI_ERR_INVALID_ARG, "F and M must be >= 1 (F=%d, M=%d)", d->F, d->M);
+    if (!d->n || !d->U || !d->K || !d->dep_off || !d->dep)
+        return fail(BI_ERR_INVALID_ARG, "desc has a NULL array");
+    if (d->model_batch < 1) return fail(BI_ERR_INVALID_ARG, "model_batch must be >= 1");
+    const uint32_t flags = d->flags ? d->flags : BI_DENSE_A;
+    if (flags != BI_DENSE_A && flags != BI_SPARSE_A)
+        return fail(BI_ERR_INVALID_ARG, "flags must be BI_DENSE_A or BI_SPARSE_A");
+    if (flags == BI_SPARSE_A) return fail(BI_ERR_UNSUPPORTED, "sparse A layout not available in this build");
+    m->F = d->F;
+    m->M = d->M;
+    m->mb = d->model_batch;
+    m->flags = flags;
+    m->n.assign(d->n, d->n + d->F);
+    m->U.assign(d->U, d->U + d->F);
+    m->K.assign(d->K, d->K + d->M);
+    m->dep_off.assign(d->dep_off, d->dep_off + d->M + 1);
+    for (int f = 0; f < d->F; ++f) {
+        if (d->n[f] < 1 || d->U[f] < 1) return fail(BI_ERR_SHAPE, "factor %d: n and U must be >= 1", f);
+        if (d->n[f] > 65535) return fail(BI_ERR_UNSUPPORTED, "factor %d: more than 65535 states", f);
+    }
+    if (d->dep_off[0] != 0) return fail(BI_ERR_SHAPE, "dep_off[0] must be 0");
+    for (int mm = 0; mm < d->M; ++mm) {
+        const int k = d->dep_off[mm + 1] - d->dep_off[mm];
+        if (k < 1) return fail(BI_ERR_SHAPE, "modality %d: empty dependency list", mm);
+        if (d->K[mm] < 1) return fail(BI_ERR_SHAPE, "modality %d: K must be >= 1", mm);
+        for (int i = d->dep_off[mm]; i < d->dep_off[mm + 1]; ++i) {
+            if (d->dep[i] < 0 || d->dep[i] >= d->F)
+                return fail(BI_ERR_SHAPE, "modality %d: dependency %d out of range", mm, d->dep[i]);
+            if (i > d->dep_off[mm] && d->dep[i] <= d->dep[i - 1])
+                return fail(BI_ERR_SHAPE, "modality %d: dependency list not strictly ascending", mm);
+        }
+        if (k > 2 * kMaxSide)
+            return fail(BI_ERR_UNSUPPORTED, "modality %d depends on %d factors; this build handles up to %d", mm, k,
+                        2 * kMaxSide);
+    }
+    m->dep.assign(d->dep, d->dep + d->dep_off[d->M]);
+
+    // descriptor tables first
+    int64_t off = 0;
+    off += (int64_t)sizeof(ModDesc) * m->M;
+    off = align_up(off, kAlign);
+    off += (int64_t)sizeof(FacDesc) * m->F;
+    off = align_up(off, kAlign);
+
+    m->mods.assign(m->M, ModDesc{});
+    m->facs.assign(m->F, FacDesc{});
+    int32_t qoff = 0;
+    for (int f = 0; f < m->F; ++f) {
+        m->facs[f].n = m->n[f];
+        m->facs[f].U = m->U[f];
+        m->facs[f].q_off = qoff;
+        qoff += m->n[f];
+    }
+    m->ntot = qoff;
+
+    int64_t a_raw = 0, a_stored = 0;
+    int32_t zv = 0;
+    m->max_rank = 0;
+    for (int mm = 0; mm < m->M; ++mm) {
+        ModDesc &md = m->mods[mm];
+        const int32_t *dl = m->dep.data() + m->dep_off[mm];
+        const int k = m->dep_off[mm + 1] - m->dep_off[mm];
+        m->max_rank = std::max(m->max_rank, k);
+        // rows = first p factors, columns = the rest; 0 <= p <= 2, 1 <= k-p <= 2,
+        // chosen to balance the two sides
+        int best_p = -1;
+        int64_t best = INT64_MAX;
+        for (int p = std::max(0, k - kMaxSide); p <= std::min(kMaxSide, k - 1); ++p) {
+            const int64_t R = prod(m->n.data(), dl, p), C = prod(m->n.data(), dl + p, k - p);
+            const int64_t cost = R > C ? R - C : C - R;
+            if (cost < best) {
+                best = cost;
+                best_p = p;
+            }
+        }
+        const int p = best_p;
+        const int64_t R = prod(m->n.data(), dl, p), C = prod(m->n.data(), dl + p, k - p);
+        const int64_t Cp = align_up(C, 4);
+        if (R * Cp > INT32_MAX / 2) return fail(BI_ERR_UNSUPPORTED, "modality %d: slice too large", mm);
+        md.K = m->K[mm];
+        md.rank = k;
+        md.R = (int32_t)R;
+        md.C = (int32_t)C;
+        md.Cp = (int32_t)Cp;
+        md.slice = (int32_t)(R * Cp);
+        md.nrow = p;
+        md.ncol = k - p;
+        for (int i = 0; i < kMaxSide; ++i) {
+            md.rf[i] = i < p ? dl[i] : -1;
+            md.rn[i] = i < p ? m->n[dl[i]] : 1;
+            md.cf[i] = i < k - p ? dl[p + i] : -1;
+            md.cn[i] = i < k - p ? m->n[dl[p + i]] : 1;
+        }
+        md.zv_off = zv;
+        zv += (int32_t)(R + C);
+        md.la_off = off;
+        md.la_agent = m->mb == 1 ? 0 : (int64_t)md.K * md.slice;
+        md.sp_ptr_off = md.sp_idx_off = md.sp_val_off = -1;
+        off = align_up(off + 8 * (int64_t)m->mb * md.K * md.slice, kAlign);
+        a_raw += (int64_t)m->mb * md.K * R * C;
+        a_stored += (int64_t)m->mb * md.K * md.slice;
+    }
+    m->zvpc = zv;
+    for (int f = 0; f < m->F; ++f) {
+        FacDesc &fd = m->facs[f];
+        const int64_t per = (int64_t)fd.U * fd.n * fd.n;
+        fd.b_agent = m->mb == 1 ? 0 : per;
+        fd.b_off = off;
+        off = align_up(off + 4 * per * m->mb, kAlign);
+        fd.lb_off = off;
+        off = align_up(off + 8 * per * m->mb, kAlign);
+        fd.ld_agent = m->mb == 1 ? 0 : fd.n;
+        fd.ld_off = off;
+        off = align_up(off + 8 * (int64_t)fd.n * m->mb, kAlign);
+    }
+    m->bytes = off;
+    m->stats.a_raw = a_raw;
+    m->stats.a_stored = a_stored;
+    m->stats.a_nnz = 0;
+    m->stats.device_bytes = off;
+    return BI_OK;
+}
+
+// Run fn(i) for i in [0, count) on up to 16 host threads.
+template <class Fn>
+static void parallel_for(int64_t count, Fn fn)
+{
+    const int64_t nt = std::max<int64_t>(1, std::min<int64_t>({16, (int64_t)std::thread::hardware_concurrency(), count}));
+    if (nt <= 1) {
+        for (int64_t i = 0; i < count; ++i) fn(i);
+        return;
+    }
+    std::atomic<int64_t> next{0};
+    std::vector<std::thread> th;
+    for (int64_t t = 0; t < nt; ++t)
+        th.emplace_back([&] {
+            for (int64_t i; (i = next.fetch_add(1)) < count;) fn(i);
+        });
+    for (auto &x : th) x.join();
+}
+
+static inline double ln_clamped(double x) { return std::log(x > kEps ? x : kEps); }
+
+int fill(const bi_model *m, const float *const *A, const float *const *B, const float *const *D, char *host,
+         int64_t *nnz_out)
+{
+    std::memcpy(host, m->mods.data(), sizeof(ModDesc) * m->M);
+    std::memcpy(host + align_up((int64_t)sizeof(ModDesc) * m->M, kAlign), m->facs.data(), sizeof(FacDesc) * m->F);
+    std::atomic<int64_t> nnz{0};
+    for (int mm = 0; mm < m->M; ++mm) {
+        const ModDesc &md = m->mods[mm];
+        const int64_t RC = (int64_t)md.R * md.C;
+        const float *src = A[mm];
+        parallel_for((int64_t)m->mb * md.K, [&](int64_t s) {
+            const float *a = src + s * RC;
+            double *dst = reinterpret_cast<double *>(host + md.la_off) + s * md.slice;
+            std::vector<double> lv(RC);
+            int64_t cnt = 0;
+            for (int64_t e = 0; e < RC; ++e) {
+                lv[e] = ln_clamped((double)a[e]);
+                cnt += a[e] != 0.0f;
+            }
+            // shift: the slice median (exact in the updates, see layout.h)
+            std::vector<double> tmp(lv);
+            std::nth_element(tmp.begin(), tmp.begin() + RC / 2, tmp.end());
+            const double c = tmp[RC / 2];
+            for (int64_t r = 0; r < md.R; ++r) {
+                for (int64_t col = 0; col < md.C; ++col) dst[r * md.Cp + col] = lv[r * md.C + col] - c;
+                for (int64_t col = md.C; col < md.Cp; ++col) dst[r * md.Cp + col] = 0.0;
+            }
+            nnz += cnt;
+        });
+    }
+    for (int f = 0; f < m->F; ++f) {
+        const FacDesc &fd = m->facs[f];
+        const int n = fd.n, U = fd.U;
+        for (int a = 0; a < m->mb; ++a) {
+            const float *src = B[f] + (int64_t)a * n * n * U;          // [i][j][u]
+            float *b = reinterpret_cast<float *>(host + fd.b_off) + (int64_t)a * U * n * n;   // [u][i][j]
+            double *lb = reinterpret_cast<double *>(host + fd.lb_off) + (int64_t)a * U * n * n;
+            for (int u = 0; u < U; ++u)
+                for (int i = 0; i < n; ++i)
+                    for (int j = 0; j < n; ++j) {
+                        const float v = src[((int64_t)i * n + j) * U + u];
+                        b[((int64_t)u * n + i) * n + j] = v;
+                        lb[((int64_t)u * n + i) * n + j] = ln_clamped((double)v);
+                    }
+            const float *dsrc = D[f] + (int64_t)a * n;
+            double *ld = reinterpret_cast<double *>(host + fd.ld_off) + (int64_t)a * n;
+            for (int s = 0; s < n; ++s) ld[s] = ln_clamped((double)dsrc[s]);
+        }
+    }
+    *nnz_out = nnz.load();
+    return BI_OK;
+}
+
+}  // namespace bi

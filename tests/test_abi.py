@@ -1,0 +1,167 @@
+"""C-ABI checks that need no GPU: exports, argument validation, host packing."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_17855_amd import bi, synth
+import bruteforce as bfm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = set()
+    inc = os.path.join(ROOT, "include")
+    for fn in os.listdir(inc):
+        if fn.endswith(".h"):
+            txt = open(os.path.join(inc, fn)).read()
+            txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+            names |= set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(bi_\w+)\s*\(", txt, flags=re.M))
+    return names
+
+
+def test_library_exports_every_declared_function():
+    lib = bi.load()
+    declared = _declared_functions()
+    assert {"bi_pack_model", "bi_vfilter", "bi_vmp", "bi_mmp"} <= declared
+    for name in declared:
+        assert hasattr(lib, name), f"{name} declared in include/ but not exported"
+    assert set(bi.EXPORTS) == declared
+
+
+class ModDesc(ctypes.Structure):
+    _fields_ = [("la_off", ctypes.c_int64), ("la_agent", ctypes.c_int64), ("K", ctypes.c_int32),
+                ("slice", ctypes.c_int32), ("rank", ctypes.c_int32), ("R", ctypes.c_int32), ("C", ctypes.c_int32),
+                ("Cp", ctypes.c_int32), ("nrow", ctypes.c_int32), ("ncol", ctypes.c_int32),
+                ("rf", ctypes.c_int32 * 2), ("rn", ctypes.c_int32 * 2), ("cf", ctypes.c_int32 * 2),
+                ("cn", ctypes.c_int32 * 2), ("zv_off", ctypes.c_int32), ("pad0", ctypes.c_int32),
+                ("sp_ptr_off", ctypes.c_int64), ("sp_idx_off", ctypes.c_int64), ("sp_val_off", ctypes.c_int64)]
+
+
+class FacDesc(ctypes.Structure):
+    _fields_ = [("b_off", ctypes.c_int64), ("lb_off", ctypes.c_int64), ("ld_off", ctypes.c_int64),
+                ("b_agent", ctypes.c_int64), ("ld_agent", ctypes.c_int32), ("n", ctypes.c_int32),
+                ("U", ctypes.c_int32), ("q_off", ctypes.c_int32)]
+
+
+def _descs(img, M, F):
+    mods = (ModDesc * M).from_buffer_copy(img[:ctypes.sizeof(ModDesc) * M].tobytes())
+    foff = -(-ctypes.sizeof(ModDesc) * M // 256) * 256
+    facs = (FacDesc * F).from_buffer_copy(img[foff:foff + ctypes.sizeof(FacDesc) * F].tobytes())
+    return mods, facs
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_host_pack_round_trip(seed):
+    w = synth.random_small(500 + seed, F_max=4, n_max=6, M_max=4, K_max=5, T_max=2, b=3, sparsity=0.3 * (seed % 2))
+    m = w.model
+    h, img = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, m.mb, m.A, m.B, m.D)
+    try:
+        st = bi.bi_get_model_stats(h)
+        assert st["device_bytes"] == img.size == bi.bi_plan_model(m.n, m.U, m.K, m.deps, m.mb)
+        mods, facs = _descs(img, m.M, m.F)
+
+        def f64(off, count):
+            return img[off:off + 8 * count].view(np.float64)
+
+        def f32(off, count):
+            return img[off:off + 4 * count].view(np.float32)
+        raw = 0
+        for mi in range(m.M):
+            md = mods[mi]
+            d = m.deps[mi]
+            assert md.rank == len(d) and md.nrow + md.ncol == len(d)
+            assert [md.rf[i] for i in range(md.nrow)] + [md.cf[i] for i in range(md.ncol)] == d
+            assert md.R == int(np.prod([m.n[f] for f in d[:md.nrow]]))
+            assert md.C == int(np.prod([m.n[f] for f in d[md.nrow:]])) and md.Cp % 4 == 0
+            for a in range(m.mb):
+                for o in range(m.K[mi]):
+                    X = f64(md.la_off + 8 * (a * md.la_agent + o * md.slice), md.slice).reshape(md.R, md.Cp)
+                    assert np.all(X[:, md.C:] == 0)
+                    ln = bfm.LN(m.A[mi][a, o]).reshape(md.R, md.C)
+                    shift = ln - X[:, :md.C]
+                    # one constant per slice: the median of the slice's logs
+                    assert np.ptp(shift) < 1e-12
+                    assert abs(shift.flat[0] - np.sort(ln.ravel())[ln.size // 2]) < 1e-12
+            raw += m.mb * m.K[mi] * md.R * md.C
+        assert st["a_raw"] == raw
+        assert st["a_nnz"] == sum(int((a != 0).sum()) for a in m.A)
+        qoff = 0
+        for f in range(m.F):
+            fd = facs[f]
+            n, U = m.n[f], m.U[f]
+            assert (fd.n, fd.U, fd.q_off) == (n, U, qoff)
+            qoff += n
+            for a in range(m.mb):
+                Bp = f32(fd.b_off + 4 * a * fd.b_agent, U * n * n).reshape(U, n, n)
+                LB = f64(fd.lb_off + 8 * a * fd.b_agent, U * n * n).reshape(U, n, n)
+                np.testing.assert_array_equal(Bp, np.transpose(m.B[f][a], (2, 0, 1)))
+                np.testing.assert_allclose(LB, bfm.LN(np.transpose(m.B[f][a], (2, 0, 1))), rtol=0, atol=1e-14)
+                LD = f64(fd.ld_off + 8 * a * fd.ld_agent, n)
+                np.testing.assert_allclose(LD, bfm.LN(m.D[f][a]), rtol=0, atol=1e-14)
+    finally:
+        bi.bi_free_model(h)
+
+
+def _desc_err(n, U, K, deps, mb=1, flags=bi.BI_DENSE_A):
+    with pytest.raises(bi.BiError) as ei:
+        bi.bi_plan_model(n, U, K, deps, mb, flags)
+    return ei.value.code
+
+
+def test_plan_rejects_bad_descriptors():
+    assert _desc_err([3], [1], [2], [[1]]) == bi.BI_ERR_SHAPE               # dependency out of range
+    assert _desc_err([3, 2], [1, 1], [2], [[1, 0]]) == bi.BI_ERR_SHAPE      # not ascending
+    assert _desc_err([3, 2], [1, 1], [2], [[0, 0]]) == bi.BI_ERR_SHAPE      # repeated factor
+    assert _desc_err([3], [1], [2], [[]]) == bi.BI_ERR_SHAPE                # empty list
+    assert _desc_err([0], [1], [2], [[0]]) == bi.BI_ERR_SHAPE               # no states
+    assert _desc_err([3], [0], [2], [[0]]) == bi.BI_ERR_SHAPE               # no actions
+    assert _desc_err([3], [1], [0], [[0]]) == bi.BI_ERR_SHAPE               # no outcomes
+    assert _desc_err([2] * 5, [1] * 5, [2], [[0, 1, 2, 3, 4]]) == bi.BI_ERR_UNSUPPORTED
+    assert _desc_err([3], [1], [2], [[0]], mb=0) == bi.BI_ERR_INVALID_ARG
+    assert _desc_err([3], [1], [2], [[0]], flags=7) == bi.BI_ERR_INVALID_ARG
+    lib = bi.load()
+    out = ctypes.c_size_t(0)
+    assert lib.bi_plan_model(None, ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG
+    assert "NULL" in bi.bi_last_error()
+
+
+def test_plan_sizes_cover_every_array():
+    w = synth.config2(b=4)
+    m = w.model
+    nbytes = bi.bi_plan_model(m.n, m.U, m.K, m.deps, m.mb)
+    need = sum(8 * a.size for a in m.A) + sum(12 * b.size + 8 * d.size for b, d in zip(m.B, m.D))
+    assert need <= nbytes <= need + 256 * (2 + 2 * m.M + 3 * m.F) + 8 * 4 * 64 * m.M
+
+
+def test_inference_validates_on_host_before_launch():
+    w = synth.random_small(3, b=2, per_agent=True)
+    m = w.model
+    h, img = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, m.mb, m.A, m.B, m.D)
+    lib = bi.load()
+    fake = ctypes.c_void_p(1 << 20)   # never dereferenced: every call below fails validation first
+    try:
+        for fn in (lib.bi_vfilter, lib.bi_vmp, lib.bi_mmp):
+            # no device buffer attached yet
+            assert fn(ctypes.c_void_p(h), 2, 2, fake, fake, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+        assert lib.bi_attach_device_buffer(ctypes.c_void_p(h), ctypes.c_void_p(1 << 20), 16) == \
+            bi.BI_ERR_BUFFER_TOO_SMALL
+        assert lib.bi_attach_device_buffer(ctypes.c_void_p(h), ctypes.c_void_p((1 << 20) + 4), img.size) == \
+            bi.BI_ERR_INVALID_ARG
+        assert lib.bi_attach_device_buffer(ctypes.c_void_p(h), fake, img.size) == bi.BI_OK
+        for fn in (lib.bi_vfilter, lib.bi_vmp, lib.bi_mmp):
+            assert fn(None, 2, 2, fake, fake, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+            assert fn(ctypes.c_void_p(h), 3, 2, fake, fake, 3, fake, None, 0, None) == bi.BI_ERR_SHAPE   # b != mb
+            assert fn(ctypes.c_void_p(h), 2, 2, fake, fake, 0, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+            assert fn(ctypes.c_void_p(h), 2, 0, fake, fake, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+            assert fn(ctypes.c_void_p(h), 2, 2, fake, None, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+            assert fn(ctypes.c_void_p(h), 2, 2, None, fake, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+            assert fn(ctypes.c_void_p(h), 2, 2, fake, fake, 3, None, None, 0, None) == bi.BI_ERR_INVALID_ARG
+        sz = ctypes.c_size_t(0)
+        assert lib.bi_workspace_size(ctypes.c_void_p(h), 2, 2, 9, ctypes.byref(sz)) == bi.BI_ERR_INVALID_ARG
+    finally:
+        bi.bi_free_model(h)
+    bi.bi_free_model(0)   # NULL is ignored

@@ -42,9 +42,19 @@ extern "C" {
 #define BI_ERR_UNSUPPORTED (-4)      /* valid, but beyond what this build handles     */
 #define BI_ERR_DEVICE (-5)           /* a HIP runtime call failed                     */
 
-/* bi_model_desc.flags: layout of the emission tensors on the device. */
+/* bi_model_desc.flags: layout of the emission tensors on the device, ORed
+ * with an optional precision policy. */
 #define BI_DENSE_A 1u  /* dense log-domain slices (default)                         */
 #define BI_SPARSE_A 2u /* sparse slices: only nonzero A entries are stored           */
+/* Precision policy.  Without it every update is computed in fp64, which
+ * reproduces the fp64 definition to output rounding even where the Jacobi
+ * iterations amplify rounding errors by 10^3-10^4 (near-bifurcation models).
+ * With BI_FAST_F32 a model shared by all agents (model_batch == 1) runs VMP and
+ * MMP through the streaming kernels, whose slice contractions use fp32 matrix
+ * cores (messages and updates stay fp64).  Use it for models whose
+ * marginals are insensitive to fp32 rounding of the log-likelihoods; it
+ * stores an extra fp32 copy of the slices. */
+#define BI_FAST_F32 4u
 
 /* Algorithm ids (bi_workspace_size). */
 #define BI_ALGO_FPI 0
@@ -58,7 +68,8 @@ extern "C" {
  *   dep[dep_off[m] .. dep_off[m+1]-1], a non-empty, strictly ascending list
  *   (the A-dependency list).  model_batch is 1 when every agent shares the
  *   model, otherwise the number of agents, each with its own parameters (the
- *   batch axis b of Sec. III-B).  flags: BI_DENSE_A or BI_SPARSE_A (0 = dense).
+ *   batch axis b of Sec. III-B).  flags: BI_DENSE_A or BI_SPARSE_A (0 = dense),
+ *   optionally ORed with BI_FAST_F32.
  */
 typedef struct bi_model_desc {
     int32_t F;
@@ -186,6 +197,25 @@ int bi_mmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, 
 /* Free the host metadata of a packed model (not the caller's device buffer).
  * NULL is ignored. */
 void bi_free_model(bi_model *model);
+
+/*
+ * Kernel timing (profiling aid).  Between bi_profile_begin and bi_profile_end
+ * every kernel the library enqueues is bracketed by a pair of HIP events on
+ * the call's stream (the recording adds two small packets per launch).
+ * bi_profile_end waits for those events and reports, per kernel class
+ * ("lik", "update", "bucket", "init", "agent_window", "agent_filter"), the
+ * number of launches and their summed duration in milliseconds, in at most
+ * `cap` entries of `out`; *n_out receives the number of classes seen.
+ * Process-wide; not for concurrent use from several threads.
+ */
+typedef struct bi_profile_entry {
+    char name[32];
+    int64_t launches;
+    double total_ms;
+} bi_profile_entry;
+
+int bi_profile_begin(void);
+int bi_profile_end(bi_profile_entry *out, int32_t cap, int32_t *n_out);
 
 #ifdef __cplusplus
 }

@@ -24,11 +24,13 @@ BI_ERR_UNSUPPORTED = -4
 BI_ERR_DEVICE = -5
 BI_DENSE_A = 1
 BI_SPARSE_A = 2
+BI_FAST_F32 = 4
 BI_ALGO_FPI, BI_ALGO_VMP, BI_ALGO_MMP = 0, 1, 2
 ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
 
 EXPORTS = ("bi_last_error", "bi_plan_model", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
-           "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_free_model")
+           "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_free_model",
+           "bi_profile_begin", "bi_profile_end")
 
 
 class BiError(RuntimeError):
@@ -42,6 +44,10 @@ class bi_model_desc(ctypes.Structure):
                 ("M", ctypes.c_int32), ("K", ctypes.POINTER(ctypes.c_int32)),
                 ("dep_off", ctypes.POINTER(ctypes.c_int32)), ("dep", ctypes.POINTER(ctypes.c_int32)),
                 ("model_batch", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+class bi_profile_entry(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
 
 
 class bi_model_stats(ctypes.Structure):
@@ -74,8 +80,11 @@ def load(path: str = LIB_PATH):
         getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, sz, vp]
     lib.bi_free_model.argtypes = [vp]
     lib.bi_free_model.restype = None
-    for name in EXPORTS[1:-1]:
-        getattr(lib, name).restype = ctypes.c_int
+    lib.bi_profile_begin.argtypes = []
+    lib.bi_profile_end.argtypes = [P(bi_profile_entry), i32, P(i32)]
+    for name in EXPORTS[1:]:
+        if name != "bi_free_model":
+            getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -191,6 +200,19 @@ def bi_mmp(handle, b, T, obs, act, iters, q, ws=None, stream=None):
 
 def bi_free_model(handle: int):
     load().bi_free_model(ctypes.c_void_p(handle))
+
+
+def bi_profile_begin():
+    _check(load().bi_profile_begin())
+
+
+def bi_profile_end() -> dict:
+    """{kernel class: (launches, total_ms)} of the launches since bi_profile_begin."""
+    cap = 32
+    arr = (bi_profile_entry * cap)()
+    n = ctypes.c_int32(0)
+    _check(load().bi_profile_end(arr, cap, ctypes.byref(n)))
+    return {arr[i].name.decode(): (int(arr[i].launches), float(arr[i].total_ms)) for i in range(min(n.value, cap))}
 
 
 _ENTRY = {"fpi": bi_vfilter, "vmp": bi_vmp, "mmp": bi_mmp}

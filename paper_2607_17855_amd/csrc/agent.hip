@@ -22,6 +22,7 @@
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
+#include "profile.h"
 
 namespace bi {
 namespace {
@@ -388,6 +389,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
         e = hipFuncSetAttribute((const void *)agent_filter_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)kLdsMax);
         if (e == hipSuccess) {
+            ProfScope p("agent_filter", stream);
             hipLaunchKernelGGL(agent_filter_kernel, dim3(b), dim3(kThreads), lds, stream, a);
             e = hipGetLastError();
         }
@@ -395,6 +397,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
         e = hipFuncSetAttribute((const void *)agent_window_kernel<BI_ALGO_VMP>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
         if (e == hipSuccess) {
+            ProfScope p("agent_window", stream);
             hipLaunchKernelGGL(agent_window_kernel<BI_ALGO_VMP>, dim3(b), dim3(kThreads), lds, stream, a);
             e = hipGetLastError();
         }
@@ -402,6 +405,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
         e = hipFuncSetAttribute((const void *)agent_window_kernel<BI_ALGO_MMP>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
         if (e == hipSuccess) {
+            ProfScope p("agent_window", stream);
             hipLaunchKernelGGL(agent_window_kernel<BI_ALGO_MMP>, dim3(b), dim3(kThreads), lds, stream, a);
             e = hipGetLastError();
         }

@@ -1,8 +1,11 @@
 // extern "C" entry points of libbi (declared in include/bi.h).
+#include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 
 #include "internal.h"
+#include "stream.h"
 
 namespace bi {
 const char *last_error();
@@ -11,6 +14,27 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
 }  // namespace bi
 
 using bi::fail;
+
+namespace {
+
+enum class Path { Agent, Stream };
+
+// Dispatch: the streaming kernels serve large models shared by every agent
+// when the caller opted into fp32 contractions; everything else runs the
+// agent-resident fp64 kernels.  BI_FORCE_PATH=agent|stream overrides the size
+// rule (tests), never the eligibility.
+Path choose_path(const bi_model *m, int algo)
+{
+    if (!bi::stream_eligible(m, algo)) return Path::Agent;
+    const char *env = std::getenv("BI_FORCE_PATH");
+    if (env && std::strcmp(env, "agent") == 0) return Path::Agent;
+    if (env && std::strcmp(env, "stream") == 0) return Path::Stream;
+    int64_t biggest = 0;
+    for (const bi::ModDesc &md : m->mods) biggest = std::max<int64_t>(biggest, (int64_t)md.R * md.C);
+    return biggest >= 16384 ? Path::Stream : Path::Agent;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -158,7 +182,7 @@ int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo,
     if (!model || !bytes) return fail(BI_ERR_INVALID_ARG, "model and bytes must be non-NULL");
     if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
     if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
-    *bytes = 0;
+    *bytes = choose_path(model, algo) == Path::Stream ? bi::stream_workspace(model, b, T) : 0;
     return BI_OK;
 }
 
@@ -178,7 +202,12 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
         if (rc != BI_OK) return rc;
         if (ws_bytes < need) return fail(BI_ERR_BUFFER_TOO_SMALL, "ws_bytes %zu < %zu required", ws_bytes, need);
         if (need > 0 && !ws) return fail(BI_ERR_INVALID_ARG, "ws is NULL");
-        return bi::launch_agent(model, algo, b, T, obs, act, iters, q, reinterpret_cast<hipStream_t>(stream));
+        if (need > 0 && reinterpret_cast<uintptr_t>(ws) % bi::kAlign)
+            return fail(BI_ERR_INVALID_ARG, "ws must be %d-byte aligned", bi::kAlign);
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        if (choose_path(model, algo) == Path::Stream)
+            return bi::launch_stream(model, algo, b, T, obs, act, iters, q, ws, s);
+        return bi::launch_agent(model, algo, b, T, obs, act, iters, q, s);
     } catch (...) {
         return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
     }

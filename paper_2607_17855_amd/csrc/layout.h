@@ -3,7 +3,8 @@
 // The packed buffer starts with the descriptor tables, followed by the
 // parameter arrays, each 256-byte aligned (all offsets below are in bytes):
 //
-//   ModDesc[M] | FacDesc[F] | LA (dense, fp64) | sparse A | B (fp32) | LB (fp64) | LD (fp64)
+//   ModDesc[M] | FacDesc[F] | LA (dense, fp64) | LA32 (fp32, BI_FAST_F32 only) | sparse A |
+//   B (fp32) | LB (fp64) | LD (fp64)
 //
 // Precision.  The mean-field fixed-point iterations are ill-conditioned for
 // some models: a relative perturbation of 1e-7 in A (fp32 rounding) moves
@@ -50,7 +51,8 @@ struct ModDesc {
     int32_t rf[kMaxSide], rn[kMaxSide];  // row factors, ascending, and their sizes
     int32_t cf[kMaxSide], cn[kMaxSide];  // column factors, ascending, and sizes
     int32_t zv_off;    // offset of this modality's Z (R values) then V (C values) in a context's block
-    int32_t pad0;
+    int32_t dsum;      // sum of n over dep(m): length of one partial message vector
+    int64_t la32_off;  // byte offset of the fp32 copy of the slices (same shape), or -1
     // sparse layout (BI_SPARSE_A): per (agent, outcome) slice, the nonzero
     // entries in row-major order as (row, col) index pairs and shifted values
     int64_t sp_ptr_off;  // byte offset of int64 [agent][K+1] entry pointers, or -1

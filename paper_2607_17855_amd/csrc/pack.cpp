@@ -45,10 +45,13 @@ int plan(const bi_model_desc *d, bi_model *m)
     if (!d->n || !d->U || !d->K || !d->dep_off || !d->dep)
         return fail(BI_ERR_INVALID_ARG, "desc has a NULL array");
     if (d->model_batch < 1) return fail(BI_ERR_INVALID_ARG, "model_batch must be >= 1");
-    const uint32_t flags = d->flags ? d->flags : BI_DENSE_A;
-    if (flags != BI_DENSE_A && flags != BI_SPARSE_A)
-        return fail(BI_ERR_INVALID_ARG, "flags must be BI_DENSE_A or BI_SPARSE_A");
-    if (flags == BI_SPARSE_A) return fail(BI_ERR_UNSUPPORTED, "sparse A layout not available in this build");
+    uint32_t flags = d->flags ? d->flags : BI_DENSE_A;
+    if ((flags & ~(BI_DENSE_A | BI_SPARSE_A | BI_FAST_F32)) != 0)
+        return fail(BI_ERR_INVALID_ARG, "unknown bits in flags");
+    if ((flags & (BI_DENSE_A | BI_SPARSE_A)) == 0) flags |= BI_DENSE_A;
+    if ((flags & BI_DENSE_A) && (flags & BI_SPARSE_A))
+        return fail(BI_ERR_INVALID_ARG, "flags must hold one of BI_DENSE_A and BI_SPARSE_A");
+    if (flags & BI_SPARSE_A) return fail(BI_ERR_UNSUPPORTED, "sparse A layout not available in this build");
     m->F = d->F;
     m->M = d->M;
     m->mb = d->model_batch;
@@ -136,10 +139,17 @@ int plan(const bi_model_desc *d, bi_model *m)
         }
         md.zv_off = zv;
         zv += (int32_t)(R + C);
+        md.dsum = 0;
+        for (int i = 0; i < k; ++i) md.dsum += m->n[dl[i]];
         md.la_off = off;
         md.la_agent = m->mb == 1 ? 0 : (int64_t)md.K * md.slice;
         md.sp_ptr_off = md.sp_idx_off = md.sp_val_off = -1;
         off = align_up(off + 8 * (int64_t)m->mb * md.K * md.slice, kAlign);
+        md.la32_off = -1;
+        if (flags & BI_FAST_F32) {
+            md.la32_off = off;
+            off = align_up(off + 4 * (int64_t)m->mb * md.K * md.slice, kAlign);
+        }
         a_raw += (int64_t)m->mb * md.K * R * C;
         a_stored += (int64_t)m->mb * md.K * md.slice;
     }
@@ -210,6 +220,10 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
             for (int64_t r = 0; r < md.R; ++r) {
                 for (int64_t col = 0; col < md.C; ++col) dst[r * md.Cp + col] = lv[r * md.C + col] - c;
                 for (int64_t col = md.C; col < md.Cp; ++col) dst[r * md.Cp + col] = 0.0;
+            }
+            if (md.la32_off >= 0) {
+                float *d32 = reinterpret_cast<float *>(host + md.la32_off) + s * md.slice;
+                for (int64_t e = 0; e < md.slice; ++e) d32[e] = (float)dst[e];
             }
             nnz += cnt;
         });

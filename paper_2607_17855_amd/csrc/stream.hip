@@ -1,0 +1,636 @@
+// Streaming kernels for a model shared by every agent (BI_FAST_F32): VMP and
+// MMP over b*T contexts, one iteration = one likelihood launch + one update
+// launch, marginals double-buffered in the workspace.
+//
+// Likelihood messages (Sec. IV marginalisation, two-sided slice view of
+// layout.h).  Contexts are first bucketed by their observed outcome, per
+// modality; every slice X = LA_m[o] is then read from HBM once per iteration
+// and applied to all J contexts that observed o, which makes the work two
+// dense contractions with the slice as the shared operand:
+//   Z[c][r] = sum_col X[r][col] t_c[col]      (rows x contexts, K = columns)
+//   V[c][col] = sum_r s_c[r] X[r][col]        (contexts x columns, K = rows)
+// both on fp32 matrix cores (v_mfma_f32_16x16x4f32).  A workgroup (8 waves,
+// one per CU) owns 256 slice rows of one (m, o) bucket and streams the row
+// tile through LDS in 32-column blocks (register prefetch two blocks ahead):
+// Z accumulates in registers across the blocks (each wave owns 32 rows), V of
+// each block is computed as four row-quarter partials (each wave one column
+// group and one quarter), summed and folded at once into the column factors'
+// messages.  The tile height sets the ratio of matrix-core work to the
+// per-block folding and operand building.  Each workgroup writes one partial
+// message vector per context and tile; the update kernel sums the partials in
+// fp64 (fixed order, no atomics, bitwise reproducible), adds the transition
+// messages and applies the softmax.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "internal.h"
+#include "profile.h"
+#include "stream.h"
+
+namespace bi {
+namespace {
+
+constexpr int kRT = 256;       // slice rows per workgroup tile
+constexpr int kCB = 32;        // columns per staged block
+constexpr int kNKB = 3;        // 16-wide MFMA context blocks per pass
+constexpr int kJG = 16 * kNKB; // contexts per pass over the tile
+constexpr int kThreads = 512;  // 8 waves, one workgroup per CU
+constexpr int kQuarters = 4;   // row quarters of the V contraction
+constexpr int kXS = kCB + 4;   // padded LDS row strides (floats)
+constexpr int kSS = kRT + 4;
+constexpr int kTS = kCB + 4;
+constexpr int kVS = kCB + 4;   // 4 rows apart land 16 banks apart
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ inline double ln_clamped(double x) { return log(fmax(x, kEps)); }
+
+__device__ inline double wave_max(double v)
+{
+    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+__device__ inline double wave_sum(double v)
+{
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// ---------------------------------------------------------------------------
+// bucketing: contexts sorted by observed outcome, one workgroup per modality.
+// Slot order inside a bucket is not fixed (atomics) but results do not depend
+// on it: every context's outputs come from its own MFMA column.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void bucket_kernel(StreamArgs a)
+{
+    extern __shared__ int cnt[];   // [K + 1] counts, then starts; [K] fill counters
+    const int m = blockIdx.x;
+    const StreamMod &sm = a.sm[m];
+    int *fil = cnt + sm.K + 1;
+    int32_t *list = a.bctx + (int64_t)m * a.nctx;
+    for (int o = threadIdx.x; o < 2 * sm.K + 1; o += blockDim.x) cnt[o] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < a.nctx; i += blockDim.x) atomicAdd(&cnt[a.obs[(int64_t)i * a.M + m]], 1);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int o = 0; o < sm.K; ++o) {
+            const int c = cnt[o];
+            cnt[o] = run;
+            run += c;
+        }
+        cnt[sm.K] = run;
+    }
+    __syncthreads();
+    int32_t *start = a.bstart + sm.bofs;
+    for (int o = threadIdx.x; o <= sm.K; o += blockDim.x) start[o] = cnt[o];
+    for (int i = threadIdx.x; i < a.nctx; i += blockDim.x) {
+        const int o = a.obs[(int64_t)i * a.M + m];
+        list[cnt[o] + atomicAdd(&fil[o], 1)] = i;
+    }
+}
+
+__global__ void init_q_kernel(StreamArgs a, float *q)
+{
+    const int64_t total = (int64_t)a.nctx * a.ntot;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int j = (int)(i % a.ntot);
+        int f = 0;
+        while (f + 1 < a.F && a.facs[f + 1].q_off <= j) ++f;
+        q[i] = 1.0f / a.facs[f].n;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// likelihood partials
+// ---------------------------------------------------------------------------
+struct LikShared {
+    float xs[kRT][kXS];            // staged slice block; row-factor marginals at the end
+    float ss[kJG][kSS];            // s_c[r] for the tile's rows; Z at the end
+    float ts[kJG][kTS];            // t_c[col] for the current block
+    float vs[kQuarters][kJG][kVS]; // V row-quarter partials of the current block; partial vectors at the end
+};
+
+__device__ inline const float *qrow(const StreamArgs &a, const float *q, int ctx, int f)
+{
+    return q + (int64_t)ctx * a.ntot + a.facs[f].q_off;
+}
+
+// Fold a block of one side's values W[c][k] (k = index lo..hi-1 along that
+// side, stored at W[c][k - base]) into the messages of the side's factors:
+//   two == 0:  out[c][k] += W[c][k]
+//   two == 1:  k = (i0, i1) with i1 fastest (n1 states),
+//              out[c][n0 + i1] += sum_{i0} W[c][k] * q[c][i0]
+//              out[c][i0]      += sum_{i1} W[c][k] * q[c][n0 + i1]
+// q: [ctx][qs] marginals of the side's factors (first factor, then second).
+// Every output entry is owned by one thread or one 4-lane group (fixed
+// summation order, no atomics); loops carry no integer division.
+template <int NP>  // number of partial planes of W summed on the fly
+__device__ inline float wv(const float *Wf, int pstride, int idx)
+{
+    float v = Wf[idx];
+#pragma unroll
+    for (int p = 1; p < NP; ++p) v += Wf[p * pstride + idx];
+    return v;
+}
+
+template <int NP>
+__device__ inline void fold_block(const float *Wf, int pstride, int ws, int lo, int hi, int jl, int two, int n0,
+                                  int n1, const float *q, int qs, int base, float *out, int os)
+{
+    if (lo >= hi) return;
+    const int tid = threadIdx.x;
+    const int width = hi - lo;
+    if (!two) {
+        // items (c, k): tid -> k = lo + t % width ...  (width <= kCB or kRT)
+        for (int i = tid; i < jl * width; i += kThreads) {
+            const int c = i / width, k = i - c * width;
+            out[c * os + lo + k] += wv<NP>(Wf, pstride, c * ws + lo + k - base);
+        }
+        return;
+    }
+    const int i0lo = lo / n1, i0hi = (hi - 1) / n1;
+    const int ni0 = i0hi - i0lo + 1;
+    // second factor: items (c, i1), summed over the i0 of the block
+    {
+        int c = tid / n1, i1 = tid - c * n1;
+        const int dc = kThreads / n1, di = kThreads - dc * n1;
+        for (; c < jl;) {
+            float acc = 0.0f;
+            const int wo = c * ws - base;
+            const float *qc = q + c * qs;
+            int k = i0lo * n1 + i1;
+            for (int i0 = i0lo; i0 <= i0hi; ++i0, k += n1)
+                if (k >= lo && k < hi) acc = fmaf(wv<NP>(Wf, pstride, wo + k), qc[i0], acc);
+            out[c * os + n0 + i1] += acc;
+            c += dc;
+            i1 += di;
+            if (i1 >= n1) {
+                i1 -= n1;
+                ++c;
+            }
+        }
+    }
+    // first factor: items (c, i0) split over 4 lanes (i1 quarters) + shuffles
+    {
+        const int part = tid & 3;
+        const int ngroups = jl * ni0;
+        for (int g0 = 0; g0 < ngroups; g0 += kThreads / 4) {
+            const int g = g0 + (tid >> 2);
+            float acc = 0.0f;
+            int c = 0, i0 = 0;
+            if (g < ngroups) {
+                c = g / ni0;
+                i0 = i0lo + (g - c * ni0);
+                const int wo = c * ws - base;
+                const float *qc = q + c * qs + n0;
+                // lane `part` takes every fourth state (interleaved: neighbouring
+                // lanes hit neighbouring banks)
+                const int a0 = max(lo, i0 * n1), a1 = min(hi, (i0 + 1) * n1);
+                for (int k = a0 + part; k < a1; k += 4) acc = fmaf(wv<NP>(Wf, pstride, wo + k), qc[k - i0 * n1], acc);
+            }
+            acc += __shfl_xor(acc, 1, 64);
+            acc += __shfl_xor(acc, 2, 64);
+            if (g < ngroups && part == 0) out[c * os + i0] += acc;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kThreads, 1) void lik_kernel(StreamArgs a, const float *q, float *part)
+{
+    extern __shared__ float dyn[];
+    LikShared &sh = *reinterpret_cast<LikShared *>(dyn);
+    __shared__ int ctxs[kJG];
+
+    // decode (modality, outcome, row tile)
+    const int wg = blockIdx.x;
+    int m = 0;
+    while (m + 1 < a.M && a.sm[m + 1].wg0 <= wg) ++m;
+    const StreamMod &sm = a.sm[m];
+    const int local = wg - sm.wg0;
+    const int o = local / sm.ntiles, tile = local - o * sm.ntiles;
+    const int32_t *start = a.bstart + sm.bofs;
+    const int b0 = start[o], J = start[o + 1] - b0;
+    if (J == 0) return;
+    const ModDesc &md = a.mods[m];
+    const int R = md.R, C = md.C, Cp = md.Cp;
+    const int r0 = tile * kRT;
+    const int rows = min(kRT, R - r0);
+    const int two = md.ncol == 2;
+    const int n0 = md.cn[0], n1 = two ? md.cn[1] : 1;
+    const int ncs = two ? n0 + n1 : n0;
+    const int qcs = ncs | 1;                                  // odd row stride: contexts spread over banks
+    float *lamc = dyn + sizeof(LikShared) / sizeof(float);   // [kJG][qcs] column-factor messages
+    float *qc = lamc + kJG * qcs;                             // [kJG][qcs] column-factor marginals
+    const float *X = reinterpret_cast<const float *>(a.base + md.la32_off) + (int64_t)o * md.slice +
+                     (int64_t)r0 * Cp;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, lk = lane >> 4;
+    const int nblocks = (Cp + kCB - 1) / kCB;
+
+    // a thread's fixed column inside every block (for t_c), and its split
+    const int my_cc = tid & (kCB - 1);
+
+    constexpr int kSlots = kRT * kCB / 4 / kThreads;   // float4 slots of a block per thread
+    auto load_block = [&](int cb, f4 (&reg)[kSlots]) {
+#pragma unroll
+        for (int u = 0; u < kSlots; ++u) {
+            const int slot = tid + u * kThreads;
+            const int rr = slot / (kCB / 4), c4 = slot - rr * (kCB / 4);
+            const int col = cb * kCB + c4 * 4;
+            f4 v = {0.f, 0.f, 0.f, 0.f};
+            if (rr < rows && col < Cp) v = *reinterpret_cast<const f4 *>(X + (int64_t)rr * Cp + col);
+            reg[u] = v;
+        }
+    };
+    auto store_block = [&](const f4 (&reg)[kSlots]) {
+#pragma unroll
+        for (int u = 0; u < kSlots; ++u) {
+            const int slot = tid + u * kThreads;
+            const int rr = slot / (kCB / 4), c4 = slot - rr * (kCB / 4);
+            *reinterpret_cast<f4 *>(&sh.xs[rr][c4 * 4]) = reg[u];
+        }
+    };
+    auto build_t = [&](int cb) {
+        const int col = cb * kCB + my_cc;
+        const bool ok = col < C;
+        const int c0 = two ? col / n1 : col, c1 = two ? col - c0 * n1 : 0;
+        for (int c = tid / kCB; c < kJG; c += kThreads / kCB) {
+            float v = 0.0f;
+            if (ok) v = two ? qc[c * qcs + c0] * qc[c * qcs + n0 + c1] : qc[c * qcs + c0];
+            sh.ts[c][my_cc] = v;
+        }
+    };
+
+    for (int g0 = 0; g0 < J; g0 += kJG) {
+        const int jg = min(kJG, J - g0);
+        const int nkb = (jg + 15) >> 4;
+        if (tid < kJG) ctxs[tid] = tid < jg ? a.bctx[(int64_t)m * a.nctx + b0 + g0 + tid] : -1;
+        __syncthreads();
+        for (int i = tid; i < kJG * ncs; i += kThreads) {
+            const int c = i / ncs, e = i - c * ncs;
+            const int ctx = ctxs[c];
+            float v = 0.0f;
+            if (ctx >= 0) v = e < n0 ? qrow(a, q, ctx, md.cf[0])[e] : qrow(a, q, ctx, md.cf[1])[e - n0];
+            qc[c * qcs + e] = v;
+            lamc[c * qcs + e] = 0.0f;
+        }
+        for (int i = tid; i < kJG * kRT; i += kThreads) {
+            const int c = i / kRT, rr = i - c * kRT;
+            float v = 0.0f;
+            const int ctx = ctxs[c];
+            if (ctx >= 0 && rr < rows) {
+                const int r = r0 + rr;
+                if (md.nrow == 0) {
+                    v = 1.0f;
+                } else if (md.nrow == 1) {
+                    v = qrow(a, q, ctx, md.rf[0])[r];
+                } else {
+                    const int rn1 = md.rn[1];
+                    v = qrow(a, q, ctx, md.rf[0])[r / rn1] * qrow(a, q, ctx, md.rf[1])[r % rn1];
+                }
+            }
+            sh.ss[c][rr] = v;
+        }
+        f4 zacc[2][kNKB];
+#pragma unroll
+        for (int zb = 0; zb < 2; ++zb)
+#pragma unroll
+            for (int kb = 0; kb < kNKB; ++kb) zacc[zb][kb] = f4{0.f, 0.f, 0.f, 0.f};
+
+        f4 preA[kSlots], preB[kSlots];
+        load_block(0, preB);
+        store_block(preB);
+        if (nblocks > 1) load_block(1, preA);
+        __syncthreads();   // qc, ss, block 0 visible
+        build_t(0);
+        // the V operand s_c[r] of this wave's row quarter is the same for every
+        // column block: keep it in registers for the whole tile
+        const int vg = wave & 1, vh = wave >> 1;
+        f4 sreg[kRT / kQuarters / 16][kNKB];
+#pragma unroll
+        for (int k4 = 0; k4 < kRT / kQuarters / 16; ++k4)
+#pragma unroll
+            for (int kb = 0; kb < kNKB; ++kb)
+                sreg[k4][kb] = *reinterpret_cast<const f4 *>(
+                    &sh.ss[16 * kb + li][(kRT / kQuarters) * vh + 16 * k4 + 4 * lk]);
+        __syncthreads();
+
+        // one column block: MFMAs on block cb (in LDS), block cb+1 in `have`,
+        // block cb+2 fetched into `fetch`
+        auto body = [&](int cb, f4 (&have)[kSlots], f4 (&fetch)[kSlots]) {
+            if (cb + 2 < nblocks) load_block(cb + 2, fetch);
+            // Z: tile rows 32*wave.. (two 16-row blocks), K = block columns
+#pragma unroll
+            for (int k4 = 0; k4 < kCB / 16; ++k4) {
+                f4 xa[2], tb[kNKB];
+#pragma unroll
+                for (int zb = 0; zb < 2; ++zb)
+                    xa[zb] = *reinterpret_cast<const f4 *>(&sh.xs[32 * wave + 16 * zb + li][16 * k4 + 4 * lk]);
+#pragma unroll
+                for (int kb = 0; kb < kNKB; ++kb)
+                    if (kb < nkb) tb[kb] = *reinterpret_cast<const f4 *>(&sh.ts[16 * kb + li][16 * k4 + 4 * lk]);
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                    for (int zb = 0; zb < 2; ++zb)
+#pragma unroll
+                        for (int kb = 0; kb < kNKB; ++kb)
+                            if (kb < nkb)
+                                zacc[zb][kb] =
+                                    __builtin_amdgcn_mfma_f32_16x16x4f32(xa[zb][jj], tb[kb][jj], zacc[zb][kb], 0, 0, 0);
+            }
+            // V: column group (wave & 1) of the block, row quarter (wave >> 1)
+            f4 vacc[kNKB];
+#pragma unroll
+            for (int kb = 0; kb < kNKB; ++kb) vacc[kb] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k4 = 0; k4 < kRT / kQuarters / 16; ++k4) {
+                const int rb = (kRT / kQuarters) * vh + 16 * k4 + 4 * lk;
+                float xb[4];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) xb[jj] = sh.xs[rb + jj][16 * vg + li];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                    for (int kb = 0; kb < kNKB; ++kb)
+                        if (kb < nkb)
+                            vacc[kb] =
+                                __builtin_amdgcn_mfma_f32_16x16x4f32(sreg[k4][kb][jj], xb[jj], vacc[kb], 0, 0, 0);
+            }
+#pragma unroll
+            for (int kb = 0; kb < kNKB; ++kb)
+                if (kb < nkb)
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr) sh.vs[vh][16 * kb + 4 * lk + rr][16 * vg + li] = vacc[kb][rr];
+            __syncthreads();
+            if (cb + 1 < nblocks) store_block(have);
+            // fold V of this block into the column factors' messages
+            fold_block<kQuarters>(&sh.vs[0][0][0], kJG * kVS, kVS, cb * kCB, min(cb * kCB + kCB, C), nkb * 16, two,
+                                  n0, n1, qc, qcs, cb * kCB, lamc, qcs);
+            if (cb + 1 < nblocks) build_t(cb + 1);
+            __syncthreads();
+        };
+        for (int cb = 0; cb < nblocks; cb += 2) {
+            body(cb, preA, preB);
+            if (cb + 1 < nblocks) body(cb + 1, preB, preA);
+        }
+
+        // Z of the tile rows -> row factors' messages, staged with the column
+        // factors' messages into one partial vector per context
+        float(*zs)[kSS] = sh.ss;            // [kJG][kRT]
+        float *qr = &sh.xs[0][0];           // [kJG][nrs] row-factor marginals
+        float *pv = &sh.vs[0][0][0];        // [kJG][dsum] partial vectors
+        const int dsum = md.dsum;
+        const int nr0 = md.nrow >= 1 ? md.rn[0] : 0;
+        const int nr1 = md.nrow == 2 ? md.rn[1] : 1;
+        const int nrs = md.nrow == 2 ? nr0 + nr1 : nr0;
+        const int qrs = nrs | 1, pvs = dsum | 1;   // odd strides
+#pragma unroll
+        for (int zb = 0; zb < 2; ++zb)
+#pragma unroll
+            for (int kb = 0; kb < kNKB; ++kb)
+                if (kb < nkb)
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr) zs[16 * kb + li][32 * wave + 16 * zb + 4 * lk + rr] = zacc[zb][kb][rr];
+        for (int i = tid; i < kJG * nrs; i += kThreads) {
+            const int c = i / nrs, e = i - c * nrs;
+            const int ctx = ctxs[c];
+            float v = 0.0f;
+            if (ctx >= 0) v = e < nr0 ? qrow(a, q, ctx, md.rf[0])[e] : qrow(a, q, ctx, md.rf[1])[e - nr0];
+            qr[c * qrs + e] = v;
+        }
+        for (int i = tid; i < kJG * dsum; i += kThreads) {
+            const int c = i / dsum, e = i - c * dsum;
+            pv[c * pvs + e] = e >= nrs ? lamc[c * qcs + (e - nrs)] : 0.0f;
+        }
+        __syncthreads();
+        if (md.nrow >= 1)
+            fold_block<1>(&zs[0][0], 0, kSS, r0, r0 + rows, nkb * 16, md.nrow == 2, nr0, nr1, qr, qrs, r0, pv, pvs);
+        __syncthreads();
+        for (int i = tid; i < jg * dsum; i += kThreads) {
+            const int c = i / dsum, e = i - c * dsum;
+            part[(int64_t)ctxs[c] * a.pstride + sm.poff + (int64_t)tile * dsum + e] = pv[c * pvs + e];
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// update: messages summed over modalities and tiles (fp64), transition
+// messages, masked softmax; one workgroup per context, one wave per factor.
+// ---------------------------------------------------------------------------
+template <int ALGO>
+__global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const float *part, const float *qin, float *qout)
+{
+    extern __shared__ double vals[];   // [ntot]
+    const int ctx = blockIdx.x;
+    const int agent = ctx / a.T, t = ctx - agent * a.T;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const float *pc = part + (int64_t)ctx * a.pstride;
+    for (int f = wave; f < a.F; f += 4) {
+        const FacDesc &fd = a.facs[f];
+        const int n = fd.n;
+        const float *qprev = t > 0 ? qin + (int64_t)(ctx - 1) * a.ntot + fd.q_off : nullptr;
+        const float *qnext = t + 1 < a.T ? qin + (int64_t)(ctx + 1) * a.ntot + fd.q_off : nullptr;
+        const int up = t > 0 ? a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f] : 0;
+        const int un = t + 1 < a.T ? a.act[((int64_t)agent * (a.T - 1) + t) * a.F + f] : 0;
+        const double *LBp = reinterpret_cast<const double *>(a.base + fd.lb_off) + (int64_t)up * n * n;
+        const double *LBn = reinterpret_cast<const double *>(a.base + fd.lb_off) + (int64_t)un * n * n;
+        const float *Bp = reinterpret_cast<const float *>(a.base + fd.b_off) + (int64_t)up * n * n;
+        const float *Bn = reinterpret_cast<const float *>(a.base + fd.b_off) + (int64_t)un * n * n;
+        const double *ld = reinterpret_cast<const double *>(a.base + fd.ld_off);
+        double *v = vals + fd.q_off;
+        for (int s = lane; s < n; s += 64) {
+            double lam = 0.0;
+            for (int m = 0; m < a.M; ++m) {
+                const ModDesc &md = a.mods[m];
+                // offset of factor f inside the modality's partial vector
+                int e = -1, acc = 0;
+                for (int i = 0; i < md.nrow; ++i) {
+                    if (md.rf[i] == f) e = acc;
+                    acc += md.rn[i];
+                }
+                for (int i = 0; i < md.ncol; ++i) {
+                    if (md.cf[i] == f) e = acc;
+                    acc += md.cn[i];
+                }
+                if (e < 0) continue;
+                const StreamMod &sm = a.sm[m];
+                const float *pp = pc + sm.poff + e + s;
+                for (int tl = 0; tl < sm.ntiles; ++tl) lam += (double)pp[(int64_t)tl * md.dsum];
+            }
+            double fwd, bwd = 0.0;
+            if (t == 0) {
+                fwd = ld[s];
+            } else if (ALGO == BI_ALGO_VMP) {
+                double acc = 0.0;
+                for (int j = 0; j < n; ++j) acc = fma(LBp[s * n + j], (double)qprev[j], acc);
+                fwd = acc;
+            } else {
+                double acc = 0.0;
+                for (int j = 0; j < n; ++j) acc = fma((double)Bp[s * n + j], (double)qprev[j], acc);
+                fwd = ln_clamped(acc);
+            }
+            if (qnext) {
+                double acc = 0.0;
+                if (ALGO == BI_ALGO_VMP) {
+                    for (int i = 0; i < n; ++i) acc = fma((double)qnext[i], LBn[i * n + s], acc);
+                    bwd = acc;
+                } else {
+                    for (int i = 0; i < n; ++i) acc = fma((double)qnext[i], (double)Bn[i * n + s], acc);
+                    bwd = ln_clamped(acc);
+                }
+            }
+            if (ALGO == BI_ALGO_VMP)
+                v[s] = lam + fwd + bwd;
+            else
+                v[s] = qnext ? lam + 0.5 * (fwd + bwd) : lam + fwd;
+        }
+        double mx = -INFINITY;
+        for (int s = lane; s < n; s += 64) mx = fmax(mx, v[s]);
+        mx = wave_max(mx);
+        double sum = 0.0;
+        for (int s = lane; s < n; s += 64) {
+            const double ev = exp(v[s] - mx);
+            v[s] = ev;
+            sum += ev;
+        }
+        sum = wave_sum(sum);
+        float *out = qout + (int64_t)ctx * a.ntot + fd.q_off;
+        for (int s = lane; s < n; s += 64) out[s] = (float)(v[s] / sum);
+    }
+}
+
+}  // namespace
+
+bool stream_eligible(const bi_model *m, int algo)
+{
+    if (!(m->flags & BI_FAST_F32) || m->mb != 1 || algo == BI_ALGO_FPI) return false;
+    if (m->M > kStreamMaxM) return false;
+    for (const ModDesc &md : m->mods) {
+        if (md.la32_off < 0) return false;
+        const int ncs = md.ncol == 2 ? md.cn[0] + md.cn[1] : md.cn[0];
+        const int nrs = md.nrow == 2 ? md.rn[0] + md.rn[1] : (md.nrow == 1 ? md.rn[0] : 0);
+        // LDS staging limits of the likelihood kernel
+        if (sizeof(LikShared) + 2 * sizeof(float) * kJG * (ncs | 1) > 160 * 1024 || kJG * (nrs | 1) > kRT * kXS ||
+            kJG * (md.dsum | 1) > kQuarters * kJG * kVS)
+            return false;
+        if (md.K > kStreamMaxK) return false;
+    }
+    return true;
+}
+
+// Plan of the workspace: bucket starts / fill counters / sorted contexts /
+// partial messages / two fp32 marginal buffers.
+static void plan_ws(const bi_model *m, int b, int T, StreamArgs *a, int64_t *offs, int64_t *total)
+{
+    const int nctx = b * T;
+    int wg = 0, bofs = 0, fofs = 0;
+    int64_t poff = 0;
+    for (int i = 0; i < m->M; ++i) {
+        const ModDesc &md = m->mods[i];
+        StreamMod &sm = a->sm[i];
+        sm.K = md.K;
+        sm.ntiles = (md.R + kRT - 1) / kRT;
+        sm.wg0 = wg;
+        wg += md.K * sm.ntiles;
+        sm.bofs = bofs;
+        bofs += md.K + 1;
+        sm.fofs = fofs;
+        fofs += md.K;
+        sm.poff = poff;
+        poff += (int64_t)sm.ntiles * md.dsum;
+    }
+    a->nwg = wg;
+    a->pstride = poff;
+    int64_t off = 0;
+    offs[0] = off;  off = align_up(off + 4 * (int64_t)bofs, kAlign);
+    offs[1] = off;  off = align_up(off + 4 * (int64_t)fofs, kAlign);
+    offs[2] = off;  off = align_up(off + 4 * (int64_t)m->M * nctx, kAlign);
+    offs[3] = off;  off = align_up(off + 4 * (int64_t)nctx * poff, kAlign);
+    offs[4] = off;  off = align_up(off + 4 * (int64_t)nctx * m->ntot, kAlign);
+    offs[5] = off;  off = align_up(off + 4 * (int64_t)nctx * m->ntot, kAlign);
+    *total = off;
+}
+
+size_t stream_workspace(const bi_model *m, int b, int T)
+{
+    StreamArgs a{};
+    int64_t offs[6], total;
+    plan_ws(m, b, T, &a, offs, &total);
+    return (size_t)total;
+}
+
+int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
+                  float *q, void *ws, hipStream_t stream)
+{
+    StreamArgs a{};
+    int64_t offs[6], total;
+    plan_ws(m, b, T, &a, offs, &total);
+    char *w = reinterpret_cast<char *>(ws);
+    a.base = m->dev;
+    a.mods = reinterpret_cast<const ModDesc *>(m->dev);
+    a.facs = reinterpret_cast<const FacDesc *>(m->dev + align_up((int64_t)sizeof(ModDesc) * m->M, kAlign));
+    a.F = m->F;
+    a.M = m->M;
+    a.T = T;
+    a.nctx = b * T;
+    a.ntot = m->ntot;
+    a.obs = obs;
+    a.act = act;
+    a.bstart = reinterpret_cast<int32_t *>(w + offs[0]);
+    a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
+    float *part = reinterpret_cast<float *>(w + offs[3]);
+    float *qa = reinterpret_cast<float *>(w + offs[4]);
+    float *qb = reinterpret_cast<float *>(w + offs[5]);
+    int ncs_max = 1;
+    for (const ModDesc &md : m->mods) ncs_max = std::max(ncs_max, (md.ncol == 2 ? md.cn[0] + md.cn[1] : md.cn[0]) | 1);
+    const size_t lik_lds = sizeof(LikShared) + 2 * sizeof(float) * kJG * ncs_max;
+    const size_t upd_lds = sizeof(double) * m->ntot;
+    if (lik_lds > 160 * 1024 || upd_lds > 64 * 1024)
+        return fail(BI_ERR_UNSUPPORTED, "streaming working set exceeds LDS");
+
+    hipError_t e = hipFuncSetAttribute((const void *)lik_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)lik_lds);
+    if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    int kmax = 1;
+    for (const ModDesc &md : m->mods) kmax = std::max(kmax, md.K);
+    {
+        ProfScope p("bucket", stream);
+        hipLaunchKernelGGL(bucket_kernel, dim3(m->M), dim3(1024), sizeof(int) * (2 * kmax + 1), stream, a);
+    }
+    {
+        ProfScope p("init", stream);
+        hipLaunchKernelGGL(init_q_kernel, dim3(std::min<int64_t>(1024, ((int64_t)a.nctx * a.ntot + 255) / 256)),
+                           dim3(256), 0, stream, a, qa);
+    }
+    float *cur = qa, *nxt = qb;
+    for (int k = 0; k < iters; ++k) {
+        float *dst = k + 1 == iters ? q : nxt;
+        {
+            ProfScope p("lik", stream);
+            hipLaunchKernelGGL(lik_kernel, dim3(a.nwg), dim3(kThreads), lik_lds, stream, a, (const float *)cur,
+                               part);
+        }
+        {
+            ProfScope p("update", stream);
+            if (algo == BI_ALGO_VMP)
+                hipLaunchKernelGGL(update_kernel<BI_ALGO_VMP>, dim3(a.nctx), dim3(256), upd_lds, stream, a,
+                                   (const float *)part, (const float *)cur, dst);
+            else
+                hipLaunchKernelGGL(update_kernel<BI_ALGO_MMP>, dim3(a.nctx), dim3(256), upd_lds, stream, a,
+                                   (const float *)part, (const float *)cur, dst);
+        }
+        float *tmp = cur;
+        cur = nxt;
+        nxt = tmp;
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(BI_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
+    return BI_OK;
+}
+
+}  // namespace bi

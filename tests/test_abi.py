@@ -37,8 +37,8 @@ class ModDesc(ctypes.Structure):
                 ("slice", ctypes.c_int32), ("rank", ctypes.c_int32), ("R", ctypes.c_int32), ("C", ctypes.c_int32),
                 ("Cp", ctypes.c_int32), ("nrow", ctypes.c_int32), ("ncol", ctypes.c_int32),
                 ("rf", ctypes.c_int32 * 2), ("rn", ctypes.c_int32 * 2), ("cf", ctypes.c_int32 * 2),
-                ("cn", ctypes.c_int32 * 2), ("zv_off", ctypes.c_int32), ("pad0", ctypes.c_int32),
-                ("sp_ptr_off", ctypes.c_int64), ("sp_idx_off", ctypes.c_int64), ("sp_val_off", ctypes.c_int64)]
+                ("cn", ctypes.c_int32 * 2), ("zv_off", ctypes.c_int32), ("dsum", ctypes.c_int32),
+                ("la32_off", ctypes.c_int64), ("sp_ptr_off", ctypes.c_int64), ("sp_idx_off", ctypes.c_int64), ("sp_val_off", ctypes.c_int64)]
 
 
 class FacDesc(ctypes.Structure):
@@ -122,7 +122,8 @@ def test_plan_rejects_bad_descriptors():
     assert _desc_err([3], [1], [0], [[0]]) == bi.BI_ERR_SHAPE               # no outcomes
     assert _desc_err([2] * 5, [1] * 5, [2], [[0, 1, 2, 3, 4]]) == bi.BI_ERR_UNSUPPORTED
     assert _desc_err([3], [1], [2], [[0]], mb=0) == bi.BI_ERR_INVALID_ARG
-    assert _desc_err([3], [1], [2], [[0]], flags=7) == bi.BI_ERR_INVALID_ARG
+    assert _desc_err([3], [1], [2], [[0]], flags=3) == bi.BI_ERR_INVALID_ARG
+    assert _desc_err([3], [1], [2], [[0]], flags=64) == bi.BI_ERR_INVALID_ARG
     lib = bi.load()
     out = ctypes.c_size_t(0)
     assert lib.bi_plan_model(None, ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG

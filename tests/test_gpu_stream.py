@@ -1,0 +1,85 @@
+"""Streaming path (shared model, BI_FAST_F32: fp32 matrix-core contractions,
+fp64 updates) against the oracle and against the fp64 agent-resident path."""
+import functools
+import os
+
+import numpy as np
+import pytest
+
+from paper_2607_17855_amd import bi, synth
+import oracle
+from test_gpu_parity import check_invariants, run_gpu
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+
+
+@pytest.fixture
+def force_stream():
+    old = os.environ.get("BI_FORCE_PATH")
+    os.environ["BI_FORCE_PATH"] = "stream"
+    yield
+    if old is None:
+        os.environ.pop("BI_FORCE_PATH", None)
+    else:
+        os.environ["BI_FORCE_PATH"] = old
+
+
+def _shared_model(seed, n, U, K, deps, b, T, alpha=1.0, sparsity=0.0, iters=2):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    model = synth.make_model(rng, n, U, K, deps, 1, alpha, alpha, sparsity=sparsity, uniform_D=False)
+    obs, act = synth.sample_sequences(rng, model, b, T)
+    return synth.Workload(f"shared{seed}", ["vmp", "mmp"], model, obs, act, iters)
+
+
+CASES = [
+    # (n, U, K, deps, b, T): ragged row tiles (R % 64 != 0), ragged column blocks,
+    # every rank 1..4, buckets of more than 32 contexts (few outcomes)
+    ([9, 7, 5], [2, 1, 3], [3, 2, 4], [[0, 1, 2], [1], [0, 2]], 24, 5),
+    ([13, 11, 6, 3], [1, 2, 2, 1], [5, 3], [[0, 1, 2, 3], [1, 3]], 40, 4),
+    ([70], [2], [3], [[0]], 30, 3),
+    ([33, 5], [2, 2], [2, 2, 3], [[0, 1], [0], [1]], 64, 6),
+    ([4, 4, 4, 4], [1, 1, 1, 1], [2], [[0, 1, 2, 3]], 100, 2),
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+@pytest.mark.parametrize("iters", [1, 2])
+def test_stream_small_vs_oracle_and_agent(case, iters, force_stream):
+    n, U, K, deps, b, T = CASES[case]
+    w = _shared_model(50 + case, n, U, K, deps, b, T, iters=iters)
+    for algo in ("vmp", "mmp"):
+        q, pm = run_gpu(w, algo, flags=bi.BI_DENSE_A | bi.BI_FAST_F32)
+        check_invariants(w, q)
+        ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters)
+        err = float(np.abs(q - ref).max())
+        print(f"[gpu]   stream vs oracle {err:.3e}", flush=True)
+        assert err <= TOL
+        os.environ["BI_FORCE_PATH"] = "agent"
+        qa, _ = run_gpu(w, algo, pm=pm)
+        os.environ["BI_FORCE_PATH"] = "stream"
+        assert float(np.abs(q - qa).max()) <= TOL
+        pm.close()
+
+
+@functools.lru_cache(maxsize=None)
+def cfg5():
+    return synth.config5()
+
+
+CFG5_AGENTS = [0, 21, 42, 63]
+
+
+@pytest.mark.parametrize("algo", ["vmp", "mmp"])
+def test_config5_stream(algo):
+    w = cfg5()
+    q, pm = run_gpu(w, algo, flags=bi.BI_DENSE_A | bi.BI_FAST_F32)
+    assert pm.workspace(w.b, w.T, algo) is not None, "config 5 must take the streaming path"
+    check_invariants(w, q)
+    q2, _ = run_gpu(w, algo, pm=pm)
+    assert np.array_equal(q, q2), "streaming path is not reproducible"
+    ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=CFG5_AGENTS)
+    err = float(np.abs(q[CFG5_AGENTS] - ref).max())
+    print(f"[gpu]   config 5 {algo} stream vs oracle (agents {CFG5_AGENTS}): {err:.3e}", flush=True)
+    assert err <= TOL
+    pm.close()

@@ -45,7 +45,9 @@ extern "C" {
 /* bi_model_desc.flags: layout of the emission tensors on the device, ORed
  * with an optional precision policy. */
 #define BI_DENSE_A 1u  /* dense log-domain slices (default)                         */
-#define BI_SPARSE_A 2u /* sparse slices: only nonzero A entries are stored           */
+#define BI_SPARSE_A 2u /* also store the nonzero entries of every slice (by rows and by
+                          columns); models shared by every agent run VMP and MMP on
+                          sparse kernels (fp64 arithmetic).  FPI keeps the dense path. */
 /* Precision policy.  Without it every update is computed in fp64, which
  * reproduces the fp64 definition to output rounding even where the Jacobi
  * iterations amplify rounding errors by 10^3-10^4 (near-bifurcation models).
@@ -101,10 +103,14 @@ const char *bi_last_error(void);
 /*
  * Size of the device buffer that bi_pack_model needs for this model shape.
  * Host only.  For BI_SPARSE_A the size depends on the values of A, so this
- * returns an upper bound (the dense size plus index storage); bi_pack_model
- * reports the exact use in bi_model_stats.device_bytes.
+ * returns an upper bound (every entry nonzero); bi_plan_model_exact gives the
+ * exact size.
  */
 int bi_plan_model(const bi_model_desc *desc, size_t *device_bytes);
+
+/* Exact size of the packed buffer for these A tensors (layout as
+ * bi_pack_model).  Host only; A as in bi_pack_model. */
+int bi_plan_model_exact(const bi_model_desc *desc, const float *const *A, size_t *device_bytes);
 
 /*
  * Pack a model into the caller's device buffer (the one-time layout step of

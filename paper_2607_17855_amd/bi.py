@@ -28,7 +28,7 @@ BI_FAST_F32 = 4
 BI_ALGO_FPI, BI_ALGO_VMP, BI_ALGO_MMP = 0, 1, 2
 ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
 
-EXPORTS = ("bi_last_error", "bi_plan_model", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
+EXPORTS = ("bi_last_error", "bi_plan_model", "bi_plan_model_exact", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
            "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_free_model",
            "bi_profile_begin", "bi_profile_end")
 
@@ -71,6 +71,7 @@ def load(path: str = LIB_PATH):
     lib.bi_last_error.restype = ctypes.c_char_p
     lib.bi_last_error.argtypes = []
     lib.bi_plan_model.argtypes = [P(bi_model_desc), P(sz)]
+    lib.bi_plan_model_exact.argtypes = [P(bi_model_desc), P(vp), P(sz)]
     lib.bi_pack_model.argtypes = [P(bi_model_desc), P(vp), P(vp), P(vp), vp, sz, vp, P(vp)]
     lib.bi_pack_model_host.argtypes = [P(bi_model_desc), P(vp), P(vp), P(vp), vp, sz, P(vp)]
     lib.bi_attach_device_buffer.argtypes = [vp, vp, sz]
@@ -121,6 +122,23 @@ def bi_plan_model(n, U, K, deps, model_batch: int, flags: int = BI_DENSE_A) -> i
     return int(out.value)
 
 
+def _f32_list(arrs):
+    return [np.ascontiguousarray(a, dtype=np.float32) for a in arrs]
+
+
+def _ptrs(arrs):
+    return (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])
+
+
+def bi_plan_model_exact(n, U, K, deps, model_batch: int, A, flags: int = BI_DENSE_A) -> int:
+    """Exact packed size for these A tensors (differs from bi_plan_model for BI_SPARSE_A)."""
+    d = _Desc(n, U, K, deps, model_batch, flags)
+    A = _f32_list(A)
+    out = ctypes.c_size_t(0)
+    _check(load().bi_plan_model_exact(ctypes.byref(d.c), _ptrs(A), ctypes.byref(out)))
+    return int(out.value)
+
+
 def _stream_ptr(stream) -> Optional[int]:
     if stream is None:
         import torch
@@ -146,7 +164,7 @@ def bi_pack_model(n, U, K, deps, model_batch: int, A: Sequence[np.ndarray], B: S
 def bi_pack_model_host(n, U, K, deps, model_batch: int, A, B, D, flags: int = BI_DENSE_A):
     """Pack into host memory; returns (handle, uint8 numpy image)."""
     d = _Desc(n, U, K, deps, model_batch, flags)
-    nbytes = bi_plan_model(n, U, K, deps, model_batch, flags)
+    nbytes = bi_plan_model_exact(n, U, K, deps, model_batch, A, flags)
     raw = np.zeros(nbytes + 512, dtype=np.uint8)
     start = (-raw.ctypes.data) % 256
     img = raw[start:start + nbytes]
@@ -224,7 +242,7 @@ class PackedModel:
     def __init__(self, model, flags: int = BI_DENSE_A, device=None, stream=None):
         import torch
         self.model = model
-        nbytes = bi_plan_model(model.n, model.U, model.K, model.deps, model.mb, flags)
+        nbytes = bi_plan_model_exact(model.n, model.U, model.K, model.deps, model.mb, model.A, flags)
         self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device or "cuda")
         self.handle = bi_pack_model(model.n, model.U, model.K, model.deps, model.mb, model.A, model.B, model.D,
                                     self.buf, flags, stream)

@@ -17,17 +17,20 @@ using bi::fail;
 
 namespace {
 
-enum class Path { Agent, Stream };
+enum class Path { Agent, Stream, Sparse };
 
-// Dispatch: the streaming kernels serve large models shared by every agent
-// when the caller opted into fp32 contractions; everything else runs the
-// agent-resident fp64 kernels.  BI_FORCE_PATH=agent|stream overrides the size
-// rule (tests), never the eligibility.
+// Dispatch: a model packed with the sparse layout (shared by every agent)
+// runs VMP / MMP on the sparse streaming kernels; the dense streaming kernels
+// serve large shared models when the caller opted into fp32 contractions;
+// everything else runs the agent-resident fp64 kernels.
+// BI_FORCE_PATH=agent|stream overrides these rules (tests), never the
+// eligibility.
 Path choose_path(const bi_model *m, int algo)
 {
-    if (!bi::stream_eligible(m, algo)) return Path::Agent;
     const char *env = std::getenv("BI_FORCE_PATH");
-    if (env && std::strcmp(env, "agent") == 0) return Path::Agent;
+    const bool force_agent = env && std::strcmp(env, "agent") == 0;
+    if (bi::sparse_eligible(m, algo) && !force_agent) return Path::Sparse;
+    if (!bi::stream_eligible(m, algo) || force_agent) return Path::Agent;
     if (env && std::strcmp(env, "stream") == 0) return Path::Stream;
     int64_t biggest = 0;
     for (const bi::ModDesc &md : m->mods) biggest = std::max<int64_t>(biggest, (int64_t)md.R * md.C);
@@ -62,17 +65,15 @@ static int pack_host(const bi_model_desc *desc, const float *const *A, const flo
 {
     *out = nullptr;
     if (!A || !B || !D) return fail(BI_ERR_INVALID_ARG, "A, B and D must be non-NULL");
+    if (desc && desc->M > 0)
+        for (int i = 0; i < desc->M; ++i)
+            if (!A[i]) return fail(BI_ERR_INVALID_ARG, "A[%d] is NULL", i);
     bi_model *m = new bi_model;
-    int rc = bi::plan(desc, m);
+    int rc = bi::plan(desc, m, A);
     if (rc != BI_OK) {
         delete m;
         return rc;
     }
-    for (int i = 0; i < m->M; ++i)
-        if (!A[i]) {
-            delete m;
-            return fail(BI_ERR_INVALID_ARG, "A[%d] is NULL", i);
-        }
     for (int i = 0; i < m->F; ++i)
         if (!B[i] || !D[i]) {
             delete m;
@@ -93,6 +94,26 @@ static int pack_host(const bi_model_desc *desc, const float *const *A, const flo
     m->stats.a_nnz = nnz;
     *out = m;
     return BI_OK;
+}
+
+int bi_plan_model_exact(const bi_model_desc *desc, const float *const *A, size_t *device_bytes)
+{
+    try {
+        if (!device_bytes) return fail(BI_ERR_INVALID_ARG, "device_bytes is NULL");
+        if (!A) return fail(BI_ERR_INVALID_ARG, "A is NULL");
+        if (desc && desc->M > 0)
+            for (int i = 0; i < desc->M; ++i)
+                if (!A[i]) return fail(BI_ERR_INVALID_ARG, "A[%d] is NULL", i);
+        bi_model m;
+        const int rc = bi::plan(desc, &m, A);
+        if (rc != BI_OK) return rc;
+        *device_bytes = (size_t)m.bytes;
+        return BI_OK;
+    } catch (const std::bad_alloc &) {
+        return fail(BI_ERR_INVALID_ARG, "host allocation failed");
+    } catch (...) {
+        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
+    }
 }
 
 int bi_pack_model_host(const bi_model_desc *desc, const float *const *A, const float *const *B,
@@ -182,7 +203,8 @@ int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo,
     if (!model || !bytes) return fail(BI_ERR_INVALID_ARG, "model and bytes must be non-NULL");
     if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
     if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
-    *bytes = choose_path(model, algo) == Path::Stream ? bi::stream_workspace(model, b, T) : 0;
+    const Path p = choose_path(model, algo);
+    *bytes = p == Path::Agent ? 0 : bi::stream_workspace(model, b, T, p == Path::Sparse);
     return BI_OK;
 }
 
@@ -205,8 +227,8 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
         if (need > 0 && reinterpret_cast<uintptr_t>(ws) % bi::kAlign)
             return fail(BI_ERR_INVALID_ARG, "ws must be %d-byte aligned", bi::kAlign);
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        if (choose_path(model, algo) == Path::Stream)
-            return bi::launch_stream(model, algo, b, T, obs, act, iters, q, ws, s);
+        const Path p = choose_path(model, algo);
+        if (p != Path::Agent) return bi::launch_stream(model, algo, b, T, obs, act, iters, q, ws, s, p == Path::Sparse);
         return bi::launch_agent(model, algo, b, T, obs, act, iters, q, s);
     } catch (...) {
         return fail(BI_ERR_INVALID_ARG, "unexpected host exception");

@@ -32,7 +32,9 @@ int fail(int code, const char *fmt, ...);
 
 // Layout planning shared by bi_plan_model and bi_pack_model; fills the
 // descriptors and offsets of `m` (no data).  Returns BI_OK or an error code.
-int plan(const bi_model_desc *desc, bi_model *m);
+// A (host) is optional: with it the sparse layout is sized exactly, without
+// it for fully dense A (an upper bound).
+int plan(const bi_model_desc *desc, bi_model *m, const float *const *A = nullptr);
 
 // Agent-resident launches (one workgroup per agent, every iteration in-kernel).
 // Returns BI_OK or an error code.

@@ -3,8 +3,16 @@
 // The packed buffer starts with the descriptor tables, followed by the
 // parameter arrays, each 256-byte aligned (all offsets below are in bytes):
 //
-//   ModDesc[M] | FacDesc[F] | LA (dense, fp64) | LA32 (fp32, BI_FAST_F32 only) | sparse A |
-//   B (fp32) | LB (fp64) | LD (fp64)
+//   ModDesc[M] | FacDesc[F] | LA (dense, fp64) | LA32 (fp32, BI_FAST_F32 only) |
+//   sparse A (BI_SPARSE_A only) | B (fp32) | LB (fp64) | LD (fp64)
+//
+// Sparse A (models shared by every agent).  Every slice X of LA - shifted by
+// log(1e-16) instead of its median, so that the structural zeros of A are
+// exactly 0 and drop out - is stored twice, by rows (CSR) and by columns
+// (CSC).  An entry is {double value; uint32 (a << 16 | b)} where (a, b) is the
+// split of the other side's index over that side's one or two factors (row
+// entries carry the column's (c0, c1), column entries the row's (r0, r1)), so
+// the kernels never divide.
 //
 // Precision.  The mean-field fixed-point iterations are ill-conditioned for
 // some models: a relative perturbation of 1e-7 in A (fp32 rounding) moves
@@ -53,11 +61,11 @@ struct ModDesc {
     int32_t zv_off;    // offset of this modality's Z (R values) then V (C values) in a context's block
     int32_t dsum;      // sum of n over dep(m): length of one partial message vector
     int64_t la32_off;  // byte offset of the fp32 copy of the slices (same shape), or -1
-    // sparse layout (BI_SPARSE_A): per (agent, outcome) slice, the nonzero
-    // entries in row-major order as (row, col) index pairs and shifted values
-    int64_t sp_ptr_off;  // byte offset of int64 [agent][K+1] entry pointers, or -1
-    int64_t sp_idx_off;  // byte offset of packed (row << 16 | col) uint32 indices
-    int64_t sp_val_off;  // byte offset of values
+    // sparse layout (BI_SPARSE_A): line pointers int32 [K][R+1] / [K][C+1]
+    // (entry indices from the modality's first entry) and SpEntry arrays
+    int64_t csr_ptr_off, csr_ent_off;   // byte offsets, or -1
+    int64_t csc_ptr_off, csc_ent_off;
+    int64_t nnz;                        // entries of the modality (each stored twice)
 };
 
 struct FacDesc {
@@ -68,6 +76,12 @@ struct FacDesc {
     int32_t ld_agent; // elements per agent of LD (0 when shared)
     int32_t n, U;
     int32_t q_off;    // offset of this factor in a context's marginal vector
+};
+
+struct SpEntry {
+    double v;       // log(max(A, 1e-16)) - log(1e-16) > 0
+    uint32_t ab;    // (a << 16) | b: split of the other side's index
+    uint32_t pad;
 };
 
 inline int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }

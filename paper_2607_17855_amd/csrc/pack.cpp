@@ -38,7 +38,7 @@ static int64_t prod(const int32_t *n, const int32_t *f, int k)
     return p;
 }
 
-int plan(const bi_model_desc *d, bi_model *m)
+int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
 {
     if (!d) return fail(BI_ERR_INVALID_ARG, "desc is NULL");
     if (d->F < 1 || d->M < 1) return fail(BI_ERR_INVALID_ARG, "F and M must be >= 1 (F=%d, M=%d)", d->F, d->M);
@@ -51,7 +51,8 @@ int plan(const bi_model_desc *d, bi_model *m)
     if ((flags & (BI_DENSE_A | BI_SPARSE_A)) == 0) flags |= BI_DENSE_A;
     if ((flags & BI_DENSE_A) && (flags & BI_SPARSE_A))
         return fail(BI_ERR_INVALID_ARG, "flags must hold one of BI_DENSE_A and BI_SPARSE_A");
-    if (flags & BI_SPARSE_A) return fail(BI_ERR_UNSUPPORTED, "sparse A layout not available in this build");
+    if ((flags & BI_SPARSE_A) && d->model_batch != 1)
+        return fail(BI_ERR_UNSUPPORTED, "the sparse A layout is for models shared by every agent");
     m->F = d->F;
     m->M = d->M;
     m->mb = d->model_batch;
@@ -143,12 +144,35 @@ int plan(const bi_model_desc *d, bi_model *m)
         for (int i = 0; i < k; ++i) md.dsum += m->n[dl[i]];
         md.la_off = off;
         md.la_agent = m->mb == 1 ? 0 : (int64_t)md.K * md.slice;
-        md.sp_ptr_off = md.sp_idx_off = md.sp_val_off = -1;
         off = align_up(off + 8 * (int64_t)m->mb * md.K * md.slice, kAlign);
         md.la32_off = -1;
         if (flags & BI_FAST_F32) {
             md.la32_off = off;
             off = align_up(off + 4 * (int64_t)m->mb * md.K * md.slice, kAlign);
+        }
+        md.csr_ptr_off = md.csr_ent_off = md.csc_ptr_off = md.csc_ent_off = -1;
+        md.nnz = 0;
+        if (flags & BI_SPARSE_A) {
+            if (R > 65535 || C > 65535 || md.rn[0] > 65535 || md.cn[0] > 65535)
+                return fail(BI_ERR_UNSUPPORTED, "modality %d: sparse layout needs dimensions below 65536", mm);
+            // exact entry count when A is given, else an upper bound (dense)
+            int64_t nnz = (int64_t)md.K * R * C;
+            if (A) {
+                nnz = 0;
+                const float *a = A[mm];
+                const int64_t tot = (int64_t)md.K * R * C;
+                for (int64_t e = 0; e < tot; ++e) nnz += (double)a[e] > kEps;
+            }
+            if (nnz > INT32_MAX) return fail(BI_ERR_UNSUPPORTED, "modality %d: too many nonzero entries", mm);
+            md.nnz = nnz;
+            md.csr_ptr_off = off;
+            off = align_up(off + 4 * (int64_t)md.K * (R + 1), kAlign);
+            md.csr_ent_off = off;
+            off = align_up(off + (int64_t)sizeof(SpEntry) * nnz, kAlign);
+            md.csc_ptr_off = off;
+            off = align_up(off + 4 * (int64_t)md.K * (C + 1), kAlign);
+            md.csc_ent_off = off;
+            off = align_up(off + (int64_t)sizeof(SpEntry) * nnz, kAlign);
         }
         a_raw += (int64_t)m->mb * md.K * R * C;
         a_stored += (int64_t)m->mb * md.K * md.slice;
@@ -227,6 +251,46 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
             }
             nnz += cnt;
         });
+    }
+    for (int mm = 0; mm < m->M; ++mm) {
+        const ModDesc &md = m->mods[mm];
+        if (md.csr_ptr_off < 0) continue;
+        const int64_t R = md.R, C = md.C, RC = R * C;
+        const float *src = A[mm];
+        int32_t *rptr = reinterpret_cast<int32_t *>(host + md.csr_ptr_off);
+        int32_t *cptr = reinterpret_cast<int32_t *>(host + md.csc_ptr_off);
+        SpEntry *rent = reinterpret_cast<SpEntry *>(host + md.csr_ent_off);
+        SpEntry *cent = reinterpret_cast<SpEntry *>(host + md.csc_ent_off);
+        const double lne = std::log(kEps);
+        // split of a row / column index over its side's factors
+        const int rn1 = md.nrow == 2 ? md.rn[1] : 1;
+        const int cn1 = md.ncol == 2 ? md.cn[1] : 1;
+        auto rsplit = [&](int64_t r) { return (uint32_t)((r / rn1) << 16 | (r % rn1)); };
+        auto csplit = [&](int64_t c) { return (uint32_t)((c / cn1) << 16 | (c % cn1)); };
+        int64_t e = 0;
+        for (int o = 0; o < md.K; ++o) {
+            const float *a = src + (int64_t)o * RC;
+            for (int64_t r = 0; r < R; ++r) {
+                rptr[(int64_t)o * (R + 1) + r] = (int32_t)e;
+                for (int64_t c = 0; c < C; ++c) {
+                    const double x = a[r * C + c];
+                    if (x > kEps) rent[e++] = SpEntry{std::log(x) - lne, csplit(c), 0u};
+                }
+            }
+            rptr[(int64_t)o * (R + 1) + R] = (int32_t)e;
+        }
+        e = 0;
+        for (int o = 0; o < md.K; ++o) {
+            const float *a = src + (int64_t)o * RC;
+            for (int64_t c = 0; c < C; ++c) {
+                cptr[(int64_t)o * (C + 1) + c] = (int32_t)e;
+                for (int64_t r = 0; r < R; ++r) {
+                    const double x = a[r * C + c];
+                    if (x > kEps) cent[e++] = SpEntry{std::log(x) - lne, rsplit(r), 0u};
+                }
+            }
+            cptr[(int64_t)o * (C + 1) + C] = (int32_t)e;
+        }
     }
     for (int f = 0; f < m->F; ++f) {
         const FacDesc &fd = m->facs[f];

@@ -1,0 +1,299 @@
+// Sparse likelihood messages (BI_SPARSE_A, models shared by every agent):
+// fp64 gathers over the nonzero entries of the observed slices.
+//
+// With the slice X = LN(A_m[o]) - ln(eps) (layout.h) the structural zeros of
+// A are exact zeros of X and drop out of both contractions of the two-sided
+// view (Sec. IV marginalisation; the dropped constant ln(eps) times the
+// product of the other factors' marginals is the same for every state of the
+// receiving factor, so it cancels in the softmax):
+//   Z[c][r]   = sum_{(r,col) in X} X[r][col] q_c0[col_0] q_c1[col_1]   (CSR lines)
+//   V[c][col] = sum_{(r,col) in X} X[r][col] q_r0[r_0]   q_r1[r_1]     (CSC lines)
+// followed by the fold of the line values into the line factors' messages.
+// Both contractions are one "line" kernel: role 0 runs over the rows with the
+// column factors as the entry side, role 1 over the columns with the row
+// factors as the entry side.
+//
+// A workgroup (8 waves) owns one tile of lines of one (modality, role,
+// outcome).  Its lanes are the contexts that observed the outcome, 64 at a
+// time; every wave walks its lines' entries in order (the entry stream is
+// uniform across the wave, so entries come in through scalar loads) and each
+// lane gathers its own context's entry-side marginals from LDS tables
+// (laid out [state][lane], conflict-free).  Line values go to an LDS tile;
+// after a barrier the tile is folded into the line factors' messages in a
+// fixed order and written as partial messages: the first line factor's
+// messages of the tile's line groups directly (tiles own disjoint groups),
+// the second line factor's as one partial vector per tile (summed by the
+// update kernel).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "internal.h"
+#include "stream.h"
+
+namespace bi {
+namespace {
+
+constexpr int kSpThreads = 512;  // 8 waves
+constexpr int kSpWaves = kSpThreads / 64;
+constexpr int kSpLanes = 64;     // contexts per pass
+constexpr int kSpLines = 128;    // target lines per tile
+constexpr int kZS = kSpLanes + 1;  // padded line-tile stride (doubles)
+constexpr int kSpBatch = 8;      // entries per gather round
+
+// Geometry of one role of a modality.
+struct Side {
+    int lines, nline, ln0, ln1, lf0, lf1;   // line side
+    int nent, en0, en1, ef0, ef1;           // entry side
+    int64_t ptr_off, ent_off;
+};
+
+__host__ __device__ inline Side side_of(const ModDesc &md, int role)
+{
+    Side s;
+    const bool rows = role == 0;
+    s.nline = rows ? md.nrow : md.ncol;
+    s.lines = rows ? md.R : md.C;
+    s.lf0 = rows ? md.rf[0] : md.cf[0];
+    s.lf1 = rows ? md.rf[1] : md.cf[1];
+    s.ln0 = s.nline >= 1 ? (rows ? md.rn[0] : md.cn[0]) : 1;
+    s.ln1 = s.nline == 2 ? (rows ? md.rn[1] : md.cn[1]) : 1;
+    s.nent = rows ? md.ncol : md.nrow;
+    s.ef0 = rows ? md.cf[0] : md.rf[0];
+    s.ef1 = rows ? md.cf[1] : md.rf[1];
+    s.en0 = s.nent >= 1 ? (rows ? md.cn[0] : md.rn[0]) : 1;
+    s.en1 = s.nent == 2 ? (rows ? md.cn[1] : md.rn[1]) : 1;
+    s.ptr_off = rows ? md.csr_ptr_off : md.csc_ptr_off;
+    s.ent_off = rows ? md.csr_ent_off : md.csc_ent_off;
+    return s;
+}
+
+// line groups per tile: whole first-factor states, about kSpLines lines
+__host__ __device__ inline int groups_per_tile(const Side &s)
+{
+    return s.nline == 2 ? std::max(1, kSpLines / s.ln1) : kSpLines;
+}
+
+__global__ __launch_bounds__(kSpThreads, 1) void sparse_lik_kernel(StreamArgs a, const char *__restrict__ mbase,
+                                                                   const double *__restrict__ q,
+                                                                   double *__restrict__ part)
+{
+    extern __shared__ double sd[];
+    __shared__ int ctxs[kSpLanes];
+
+    const int wg = blockIdx.x;
+    int ti = 0;
+    while (ti + 1 < a.ntask && a.task[ti + 1].wg0 <= wg) ++ti;
+    const SpTask tk = a.task[ti];
+    const ModDesc &md = a.mods[tk.m];
+    const Side sd_ = side_of(md, tk.role);
+    const int local = wg - tk.wg0;
+    const int o = local / tk.tiles, tile = local - o * tk.tiles;
+    const int32_t *start = a.bstart + a.sm[tk.m].bofs;
+    const int b0 = start[o], J = start[o + 1] - b0;
+    if (J == 0) return;
+
+    // the tile's lines: groups [g0, g0 + ng) of the first line factor
+    const int G = tk.G;
+    const int g0 = tile * G;
+    const int ng = min(G, sd_.ln0 - g0);
+    const int lb = g0 * sd_.ln1, le = (g0 + ng) * sd_.ln1;
+    const int nl = le - lb;
+
+    const int ntab = sd_.en0 + sd_.en1;
+    double *tab = sd;                       // [en0 + en1][64]: entry-side marginals
+    double *zt = sd + ntab * kSpLanes;      // [lines of the tile][kZS]
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: entry stream via scalar loads
+
+    const int32_t *lptr = reinterpret_cast<const int32_t *>(mbase + sd_.ptr_off) + (int64_t)o * (sd_.lines + 1);
+    const SpEntry *ent = reinterpret_cast<const SpEntry *>(mbase + sd_.ent_off);
+    const int off_e0 = sd_.nent >= 1 ? a.facs[sd_.ef0].q_off : -1;
+    const int off_e1 = sd_.nent == 2 ? a.facs[sd_.ef1].q_off : -1;
+    const int off_l0 = a.facs[sd_.lf0].q_off;
+    const int off_l1 = sd_.nline == 2 ? a.facs[sd_.lf1].q_off : -1;
+    const int en0 = sd_.en0;
+
+    for (int c0 = 0; c0 < J; c0 += kSpLanes) {
+        const int jc = min(kSpLanes, J - c0);
+        if (tid < kSpLanes) ctxs[tid] = tid < jc ? a.bctx[(int64_t)tk.m * a.nctx + b0 + c0 + tid] : -1;
+        __syncthreads();
+        // entry-side marginal tables (1.0 for an absent factor)
+        for (int i = tid; i < ntab * kSpLanes; i += kSpThreads) {
+            const int c = i & (kSpLanes - 1), s = i >> 6;
+            const int ctx = ctxs[c];
+            double v = 0.0;
+            if (ctx >= 0) {
+                const double *qc = q + (int64_t)ctx * a.ntot;
+                if (s < en0)
+                    v = off_e0 >= 0 ? qc[off_e0 + s] : 1.0;
+                else
+                    v = off_e1 >= 0 ? qc[off_e1 + s - en0] : 1.0;
+            }
+            tab[i] = v;
+        }
+        __syncthreads();
+
+        // line values: wave w takes lines lb + w, lb + w + 8, ...
+        const double *t0 = tab + lane;
+        const double *t1 = tab + en0 * kSpLanes + lane;
+        for (int l = lb + wave; l < le; l += kSpWaves) {
+            const int e0 = lptr[l], e1 = lptr[l + 1];
+            double acc = 0.0;
+            int e = e0;
+            // batches of kSpBatch entries: one round of scalar loads, one of
+            // LDS gathers, then the FMAs (in entry order)
+            for (; e + kSpBatch <= e1; e += kSpBatch) {
+                double v[kSpBatch], p[kSpBatch];
+                uint32_t ab[kSpBatch];
+                const uint4 *eb = reinterpret_cast<const uint4 *>(ent + e);   // one base, constant offsets
+#pragma unroll
+                for (int k = 0; k < kSpBatch; ++k) {
+                    const uint4 x = eb[k];
+                    v[k] = __hiloint2double((int)x.y, (int)x.x);
+                    ab[k] = x.z;
+                }
+#pragma unroll
+                for (int k = 0; k < kSpBatch; ++k) p[k] = t0[(ab[k] >> 16) * kSpLanes] * t1[(ab[k] & 0xffffu) * kSpLanes];
+#pragma unroll
+                for (int k = 0; k < kSpBatch; ++k) acc = fma(v[k], p[k], acc);
+            }
+            for (; e < e1; ++e) {
+                const uint32_t ab = ent[e].ab;
+                acc = fma(ent[e].v, t0[(ab >> 16) * kSpLanes] * t1[(ab & 0xffffu) * kSpLanes], acc);
+            }
+            zt[(l - lb) * kZS + lane] = acc;
+        }
+        __syncthreads();
+
+        // fold and write
+        const int64_t ps = a.pstride;
+        if (sd_.nline == 1) {
+            // messages of the single line factor are the line values
+            for (int i = tid; i < jc * nl; i += kSpThreads) {
+                const int c = i / nl, k = i - c * nl;
+                part[(int64_t)ctxs[c] * ps + tk.so + lb + k] = zt[k * kZS + c];
+            }
+        } else {
+            const int ln1 = sd_.ln1;
+            // first line factor: one message per (context, group), summed over l1
+            for (int i = tid; i < jc * ng; i += kSpThreads) {
+                const int c = i / ng, g = i - c * ng;
+                const double *qc = q + (int64_t)ctxs[c] * a.ntot + off_l1;
+                const double *z = zt + g * ln1 * kZS + c;
+                double acc = 0.0;
+                for (int l1 = 0; l1 < ln1; ++l1) acc = fma(z[l1 * kZS], qc[l1], acc);
+                part[(int64_t)ctxs[c] * ps + tk.so + g0 + g] = acc;
+            }
+            // second line factor: the tile's partial, summed over its groups
+            for (int i = tid; i < jc * ln1; i += kSpThreads) {
+                const int c = i / ln1, l1 = i - c * ln1;
+                const double *qc = q + (int64_t)ctxs[c] * a.ntot + off_l0 + g0;
+                const double *z = zt + l1 * kZS + c;
+                double acc = 0.0;
+                for (int g = 0; g < ng; ++g) acc = fma(z[g * ln1 * kZS], qc[g], acc);
+                part[(int64_t)ctxs[c] * ps + tk.so + sd_.ln0 + (int64_t)tile * ln1 + l1] = acc;
+            }
+        }
+        __syncthreads();
+    }
+}
+
+inline size_t lds_for(const Side &s)
+{
+    const int G = groups_per_tile(s);
+    const int lines = std::min(G, s.ln0) * s.ln1;
+    return sizeof(double) * ((size_t)(s.en0 + s.en1) * kSpLanes + (size_t)lines * kZS);
+}
+
+}  // namespace
+
+bool sparse_eligible(const bi_model *m, int algo)
+{
+    if (!(m->flags & BI_SPARSE_A) || m->mb != 1 || algo == BI_ALGO_FPI) return false;
+    if (m->M > kStreamMaxM) return false;
+    int64_t pstride = 0;
+    for (const ModDesc &md : m->mods) {
+        if (md.csr_ptr_off < 0 || md.K > kStreamMaxK) return false;
+        for (int role = 0; role < 2; ++role) {
+            const Side s = side_of(md, role);
+            if (s.nline == 0) continue;
+            if (lds_for(s) > 160 * 1024) return false;
+            const int G = groups_per_tile(s);
+            const int64_t tiles = s.nline == 2 ? (s.ln0 + G - 1) / G : (s.lines + G - 1) / G;
+            pstride += s.nline == 2 ? s.ln0 + tiles * s.ln1 : s.lines;
+        }
+    }
+    return pstride < (int64_t)1 << 30;
+}
+
+size_t sparse_lds_bytes(const bi_model *m)
+{
+    size_t most = 0;
+    for (const ModDesc &md : m->mods)
+        for (int role = 0; role < 2; ++role) {
+            const Side s = side_of(md, role);
+            if (s.nline > 0) most = std::max(most, lds_for(s));
+        }
+    return most;
+}
+
+int64_t sparse_plan(const bi_model *m, StreamArgs *a)
+{
+    int wg = 0;
+    int64_t so = 0;
+    a->ntask = 0;
+    a->nmsg = 0;
+    for (int i = 0; i < m->M; ++i) {
+        const ModDesc &md = m->mods[i];
+        for (int role = 0; role < 2; ++role) {
+            const Side s = side_of(md, role);
+            if (s.nline == 0) continue;   // no row factors
+            SpTask &tk = a->task[a->ntask++];
+            tk.m = (int8_t)i;
+            tk.role = (int8_t)role;
+            const int G = groups_per_tile(s);
+            tk.G = (int16_t)G;
+            tk.tiles = s.nline == 2 ? (s.ln0 + G - 1) / G : (s.lines + G - 1) / G;
+            tk.wg0 = wg;
+            wg += md.K * tk.tiles;
+            tk.so = (int32_t)so;
+            MsgSrc &m0 = a->msg[a->nmsg++];
+            m0.f = s.lf0;
+            m0.copies = 1;
+            m0.stride = 0;
+            m0.off = (int32_t)so;
+            if (s.nline == 2) {
+                MsgSrc &m1 = a->msg[a->nmsg++];
+                m1.f = s.lf1;
+                m1.copies = tk.tiles;
+                m1.stride = s.ln1;
+                m1.off = (int32_t)(so + s.ln0);
+                so += s.ln0 + (int64_t)tk.tiles * s.ln1;
+            } else {
+                so += s.lines;
+            }
+        }
+    }
+    a->nwg = wg;
+    return so;
+}
+
+int sparse_prepare(const bi_model *m)
+{
+    const size_t lds = sparse_lds_bytes(m);
+    if (lds > 160 * 1024) return fail(BI_ERR_UNSUPPORTED, "sparse working set exceeds LDS");
+    const hipError_t e =
+        hipFuncSetAttribute((const void *)sparse_lik_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    return BI_OK;
+}
+
+void sparse_lik_launch(const bi_model *m, const StreamArgs &a, const double *q, double *part, hipStream_t stream)
+{
+    const size_t lds = sparse_lds_bytes(m);
+    hipLaunchKernelGGL(sparse_lik_kernel, dim3(a.nwg), dim3(kSpThreads), lds, stream, a, (const char *)m->dev, q,
+                       part);
+}
+
+}  // namespace bi

@@ -1,4 +1,15 @@
-// Streaming path (models shared by every agent, BI_FAST_F32): internal API.
+// Streaming paths (models shared by every agent): internal API.
+//
+// Both streaming paths run VMP / MMP over the b*T contexts of a call as one
+// likelihood launch + one update launch per iteration, with the marginals
+// double-buffered in the workspace:
+//   dense  (BI_FAST_F32): fp32 matrix-core contractions over the dense slices
+//          (stream.hip), fp32 marginals between iterations;
+//   sparse (BI_SPARSE_A): fp64 gathers over the nonzero entries of the slices
+//          (sparse.hip), fp64 marginals between iterations.
+// Contexts are bucketed by observed outcome per modality first; the
+// likelihood kernels write partial message vectors per context, which the
+// update kernel sums in a fixed order (no atomics: bitwise reproducible).
 #pragma once
 
 #include "internal.h"
@@ -6,16 +17,38 @@
 namespace bi {
 
 constexpr int kStreamMaxM = 16;
-constexpr int kStreamMaxK = 8000;   // outcomes per modality (bucket histogram in LDS)
+constexpr int kStreamMaxK = 8000;           // outcomes per modality (bucket histogram in LDS)
+constexpr int kStreamMaxMsg = 4 * kStreamMaxM;
+constexpr int kStreamMaxTask = 2 * kStreamMaxM;
 
 struct StreamMod {
     int K;        // outcomes
-    int ntiles;   // row tiles of a slice
-    int wg0;      // first workgroup of this modality in the likelihood grid
+    int ntiles;   // row tiles of a slice (dense path)
+    int wg0;      // first workgroup of this modality in the dense likelihood grid
     int bofs;     // offset of this modality's K+1 bucket starts
     int fofs;     // (reserved)
     int pad;
-    int64_t poff; // offset of its partial messages inside a context's partial block
+    int64_t poff; // offset of its partial messages inside a context's partial block (dense path)
+};
+
+// One source of likelihood messages for factor f: `copies` vectors of n_f
+// values at off + k*stride (k < copies) inside a context's partial block.
+struct MsgSrc {
+    int32_t f;
+    int32_t copies;
+    int32_t stride;
+    int32_t off;
+};
+
+// Sparse likelihood task: one side of one modality.  role 0 = row lines (the
+// row factors' messages, from the CSR entries), role 1 = column lines (the
+// column factors' messages, from the CSC entries).
+struct SpTask {
+    int8_t m, role;
+    int16_t G;      // line groups (first-factor states) per tile
+    int32_t wg0;    // first workgroup of the task
+    int32_t tiles;  // tiles per outcome
+    int32_t so;     // offset of the task's messages inside a context's partial block
 };
 
 struct StreamArgs {
@@ -23,19 +56,32 @@ struct StreamArgs {
     const ModDesc *mods;
     const FacDesc *facs;
     int F, M, T, nctx, ntot, nwg;
-    int64_t pstride;            // floats of partial messages per context
+    int64_t pstride;            // values of partial messages per context
     const int32_t *obs;
     const int32_t *act;
     int32_t *bstart, *bctx;
+    int nmsg, ntask;
     StreamMod sm[kStreamMaxM];
+    MsgSrc msg[kStreamMaxMsg];
+    SpTask task[kStreamMaxTask];
 };
 
-// Whether `m` can run `algo` on the streaming kernels.
+// Whether `m` can run `algo` on the dense streaming kernels.
 bool stream_eligible(const bi_model *m, int algo);
+// Whether `m` can run `algo` on the sparse streaming kernels.
+bool sparse_eligible(const bi_model *m, int algo);
 // Workspace bytes of a streaming call with b agents and window T.
-size_t stream_workspace(const bi_model *m, int b, int T);
-// Enqueue a streaming VMP / MMP call.
+size_t stream_workspace(const bi_model *m, int b, int T, bool sparse);
+// Enqueue a streaming VMP / MMP call (dense or sparse likelihood kernels).
 int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
-                  float *q, void *ws, hipStream_t stream);
+                  float *q, void *ws, hipStream_t stream, bool sparse);
+
+// Sparse likelihood kernel (sparse.hip): task planning and one launch.
+// sparse_plan fills a->task / a->ntask / a->nwg and the message sources,
+// and returns the values of partial messages per context.
+int64_t sparse_plan(const bi_model *m, StreamArgs *a);
+size_t sparse_lds_bytes(const bi_model *m);
+int sparse_prepare(const bi_model *m);   // once per call, before the launches
+void sparse_lik_launch(const bi_model *m, const StreamArgs &a, const double *q, double *part, hipStream_t stream);
 
 }  // namespace bi

@@ -92,14 +92,15 @@ __global__ __launch_bounds__(1024) void bucket_kernel(StreamArgs a)
     }
 }
 
-__global__ void init_q_kernel(StreamArgs a, float *q)
+template <typename QT>
+__global__ void init_q_kernel(StreamArgs a, QT *q)
 {
     const int64_t total = (int64_t)a.nctx * a.ntot;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
         const int j = (int)(i % a.ntot);
         int f = 0;
         while (f + 1 < a.F && a.facs[f + 1].q_off <= j) ++f;
-        q[i] = 1.0f / a.facs[f].n;
+        q[i] = QT(1) / QT(a.facs[f].n);
     }
 }
 
@@ -419,22 +420,24 @@ __global__ __launch_bounds__(kThreads, 1) void lik_kernel(StreamArgs a, const fl
 }
 
 // ---------------------------------------------------------------------------
-// update: messages summed over modalities and tiles (fp64), transition
-// messages, masked softmax; one workgroup per context, one wave per factor.
+// update: messages summed over their partial vectors (fp64, fixed order),
+// transition messages, masked softmax; one workgroup per context, one wave
+// per factor.  QT = marginals between iterations, PT = partial messages,
+// OT = this launch's output marginals.
 // ---------------------------------------------------------------------------
-template <int ALGO>
-__global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const float *part, const float *qin, float *qout)
+template <int ALGO, typename QT, typename PT, typename OT>
+__global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *part, const QT *qin, OT *qout)
 {
     extern __shared__ double vals[];   // [ntot]
     const int ctx = blockIdx.x;
     const int agent = ctx / a.T, t = ctx - agent * a.T;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const float *pc = part + (int64_t)ctx * a.pstride;
+    const PT *pc = part + (int64_t)ctx * a.pstride;
     for (int f = wave; f < a.F; f += 4) {
         const FacDesc &fd = a.facs[f];
         const int n = fd.n;
-        const float *qprev = t > 0 ? qin + (int64_t)(ctx - 1) * a.ntot + fd.q_off : nullptr;
-        const float *qnext = t + 1 < a.T ? qin + (int64_t)(ctx + 1) * a.ntot + fd.q_off : nullptr;
+        const QT *qprev = t > 0 ? qin + (int64_t)(ctx - 1) * a.ntot + fd.q_off : nullptr;
+        const QT *qnext = t + 1 < a.T ? qin + (int64_t)(ctx + 1) * a.ntot + fd.q_off : nullptr;
         const int up = t > 0 ? a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f] : 0;
         const int un = t + 1 < a.T ? a.act[((int64_t)agent * (a.T - 1) + t) * a.F + f] : 0;
         const double *LBp = reinterpret_cast<const double *>(a.base + fd.lb_off) + (int64_t)up * n * n;
@@ -445,22 +448,11 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const float *
         double *v = vals + fd.q_off;
         for (int s = lane; s < n; s += 64) {
             double lam = 0.0;
-            for (int m = 0; m < a.M; ++m) {
-                const ModDesc &md = a.mods[m];
-                // offset of factor f inside the modality's partial vector
-                int e = -1, acc = 0;
-                for (int i = 0; i < md.nrow; ++i) {
-                    if (md.rf[i] == f) e = acc;
-                    acc += md.rn[i];
-                }
-                for (int i = 0; i < md.ncol; ++i) {
-                    if (md.cf[i] == f) e = acc;
-                    acc += md.cn[i];
-                }
-                if (e < 0) continue;
-                const StreamMod &sm = a.sm[m];
-                const float *pp = pc + sm.poff + e + s;
-                for (int tl = 0; tl < sm.ntiles; ++tl) lam += (double)pp[(int64_t)tl * md.dsum];
+            for (int i = 0; i < a.nmsg; ++i) {
+                const MsgSrc src = a.msg[i];
+                if (src.f != f) continue;
+                const PT *pp = pc + src.off + s;
+                for (int k = 0; k < src.copies; ++k) lam += (double)pp[(int64_t)k * src.stride];
             }
             double fwd, bwd = 0.0;
             if (t == 0) {
@@ -499,9 +491,21 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const float *
             sum += ev;
         }
         sum = wave_sum(sum);
-        float *out = qout + (int64_t)ctx * a.ntot + fd.q_off;
-        for (int s = lane; s < n; s += 64) out[s] = (float)(v[s] / sum);
+        OT *out = qout + (int64_t)ctx * a.ntot + fd.q_off;
+        for (int s = lane; s < n; s += 64) out[s] = (OT)(v[s] / sum);
     }
+}
+
+template <typename QT, typename PT, typename OT>
+void launch_update(int algo, const StreamArgs &a, size_t lds, hipStream_t stream, const PT *part, const QT *qin,
+                   OT *qout)
+{
+    if (algo == BI_ALGO_VMP)
+        hipLaunchKernelGGL((update_kernel<BI_ALGO_VMP, QT, PT, OT>), dim3(a.nctx), dim3(256), lds, stream, a, part,
+                           qin, qout);
+    else
+        hipLaunchKernelGGL((update_kernel<BI_ALGO_MMP, QT, PT, OT>), dim3(a.nctx), dim3(256), lds, stream, a, part,
+                           qin, qout);
 }
 
 }  // namespace
@@ -523,53 +527,108 @@ bool stream_eligible(const bi_model *m, int algo)
     return true;
 }
 
-// Plan of the workspace: bucket starts / fill counters / sorted contexts /
-// partial messages / two fp32 marginal buffers.
-static void plan_ws(const bi_model *m, int b, int T, StreamArgs *a, int64_t *offs, int64_t *total)
+// Dense-path partial layout: per modality, one dsum vector per row tile
+// (row factors' messages, then column factors'), summed over the tiles.
+static int64_t dense_plan(const bi_model *m, StreamArgs *a)
 {
-    const int nctx = b * T;
-    int wg = 0, bofs = 0, fofs = 0;
+    int wg = 0;
     int64_t poff = 0;
+    a->nmsg = 0;
     for (int i = 0; i < m->M; ++i) {
         const ModDesc &md = m->mods[i];
         StreamMod &sm = a->sm[i];
-        sm.K = md.K;
         sm.ntiles = (md.R + kRT - 1) / kRT;
         sm.wg0 = wg;
         wg += md.K * sm.ntiles;
-        sm.bofs = bofs;
-        bofs += md.K + 1;
-        sm.fofs = fofs;
-        fofs += md.K;
         sm.poff = poff;
+        int e = 0;
+        for (int side = 0; side < 2; ++side) {
+            const int nf = side == 0 ? md.nrow : md.ncol;
+            for (int j = 0; j < nf; ++j) {
+                MsgSrc &src = a->msg[a->nmsg++];
+                src.f = side == 0 ? md.rf[j] : md.cf[j];
+                src.copies = sm.ntiles;
+                src.stride = md.dsum;
+                src.off = (int32_t)(poff + e);
+                e += side == 0 ? md.rn[j] : md.cn[j];
+            }
+        }
         poff += (int64_t)sm.ntiles * md.dsum;
     }
     a->nwg = wg;
-    a->pstride = poff;
+    return poff;
+}
+
+// Plan of the workspace: bucket starts / fill counters / sorted contexts /
+// partial messages / two marginal buffers (fp32 dense, fp64 sparse).
+static void plan_ws(const bi_model *m, int b, int T, bool sparse, StreamArgs *a, int64_t *offs, int64_t *total)
+{
+    const int nctx = b * T;
+    int bofs = 0, fofs = 0;
+    for (int i = 0; i < m->M; ++i) {
+        StreamMod &sm = a->sm[i];
+        sm.K = m->mods[i].K;
+        sm.bofs = bofs;
+        bofs += sm.K + 1;
+        sm.fofs = fofs;
+        fofs += sm.K;
+    }
+    a->pstride = sparse ? sparse_plan(m, a) : dense_plan(m, a);
+    const int64_t es = sparse ? 8 : 4;
     int64_t off = 0;
     offs[0] = off;  off = align_up(off + 4 * (int64_t)bofs, kAlign);
     offs[1] = off;  off = align_up(off + 4 * (int64_t)fofs, kAlign);
     offs[2] = off;  off = align_up(off + 4 * (int64_t)m->M * nctx, kAlign);
-    offs[3] = off;  off = align_up(off + 4 * (int64_t)nctx * poff, kAlign);
-    offs[4] = off;  off = align_up(off + 4 * (int64_t)nctx * m->ntot, kAlign);
-    offs[5] = off;  off = align_up(off + 4 * (int64_t)nctx * m->ntot, kAlign);
+    offs[3] = off;  off = align_up(off + es * (int64_t)nctx * a->pstride, kAlign);
+    offs[4] = off;  off = align_up(off + es * (int64_t)nctx * m->ntot, kAlign);
+    offs[5] = off;  off = align_up(off + es * (int64_t)nctx * m->ntot, kAlign);
     *total = off;
 }
 
-size_t stream_workspace(const bi_model *m, int b, int T)
+size_t stream_workspace(const bi_model *m, int b, int T, bool sparse)
 {
     StreamArgs a{};
     int64_t offs[6], total;
-    plan_ws(m, b, T, &a, offs, &total);
+    plan_ws(m, b, T, sparse, &a, offs, &total);
     return (size_t)total;
 }
 
+template <typename QT>
+static void run_iterations(const bi_model *m, int algo, int iters, const StreamArgs &a, char *part, QT *qa, QT *qb,
+                           float *q, size_t lik_lds, size_t upd_lds, hipStream_t stream, bool sparse)
+{
+    QT *cur = qa, *nxt = qb;
+    using PT = QT;
+    for (int k = 0; k < iters; ++k) {
+        {
+            ProfScope p(sparse ? "lik_sparse" : "lik", stream);
+            if (sparse)
+                sparse_lik_launch(m, a, reinterpret_cast<const double *>(cur), reinterpret_cast<double *>(part),
+                                  stream);
+            else
+                hipLaunchKernelGGL(lik_kernel, dim3(a.nwg), dim3(kThreads), lik_lds, stream, a,
+                                   reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part));
+        }
+        {
+            ProfScope p("update", stream);
+            const PT *pp = reinterpret_cast<const PT *>(part);
+            if (k + 1 == iters)
+                launch_update<QT, PT, float>(algo, a, upd_lds, stream, pp, cur, q);
+            else
+                launch_update<QT, PT, QT>(algo, a, upd_lds, stream, pp, cur, nxt);
+        }
+        QT *tmp = cur;
+        cur = nxt;
+        nxt = tmp;
+    }
+}
+
 int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
-                  float *q, void *ws, hipStream_t stream)
+                  float *q, void *ws, hipStream_t stream, bool sparse)
 {
     StreamArgs a{};
     int64_t offs[6], total;
-    plan_ws(m, b, T, &a, offs, &total);
+    plan_ws(m, b, T, sparse, &a, offs, &total);
     char *w = reinterpret_cast<char *>(ws);
     a.base = m->dev;
     a.mods = reinterpret_cast<const ModDesc *>(m->dev);
@@ -583,52 +642,52 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.act = act;
     a.bstart = reinterpret_cast<int32_t *>(w + offs[0]);
     a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
-    float *part = reinterpret_cast<float *>(w + offs[3]);
-    float *qa = reinterpret_cast<float *>(w + offs[4]);
-    float *qb = reinterpret_cast<float *>(w + offs[5]);
-    int ncs_max = 1;
-    for (const ModDesc &md : m->mods) ncs_max = std::max(ncs_max, (md.ncol == 2 ? md.cn[0] + md.cn[1] : md.cn[0]) | 1);
-    const size_t lik_lds = sizeof(LikShared) + 2 * sizeof(float) * kJG * ncs_max;
+    char *part = w + offs[3];
     const size_t upd_lds = sizeof(double) * m->ntot;
+    size_t lik_lds = 0;
+    if (sparse) {
+        lik_lds = sparse_lds_bytes(m);
+    } else {
+        int ncs_max = 1;
+        for (const ModDesc &md : m->mods)
+            ncs_max = std::max(ncs_max, (md.ncol == 2 ? md.cn[0] + md.cn[1] : md.cn[0]) | 1);
+        lik_lds = sizeof(LikShared) + 2 * sizeof(float) * kJG * ncs_max;
+    }
     if (lik_lds > 160 * 1024 || upd_lds > 64 * 1024)
         return fail(BI_ERR_UNSUPPORTED, "streaming working set exceeds LDS");
-
-    hipError_t e = hipFuncSetAttribute((const void *)lik_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)lik_lds);
-    if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    if (sparse) {
+        const int rc = sparse_prepare(m);
+        if (rc != BI_OK) return rc;
+    } else {
+        const hipError_t e = hipFuncSetAttribute((const void *)lik_kernel,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lik_lds);
+        if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    }
     int kmax = 1;
     for (const ModDesc &md : m->mods) kmax = std::max(kmax, md.K);
     {
         ProfScope p("bucket", stream);
         hipLaunchKernelGGL(bucket_kernel, dim3(m->M), dim3(1024), sizeof(int) * (2 * kmax + 1), stream, a);
     }
-    {
-        ProfScope p("init", stream);
-        hipLaunchKernelGGL(init_q_kernel, dim3(std::min<int64_t>(1024, ((int64_t)a.nctx * a.ntot + 255) / 256)),
-                           dim3(256), 0, stream, a, qa);
-    }
-    float *cur = qa, *nxt = qb;
-    for (int k = 0; k < iters; ++k) {
-        float *dst = k + 1 == iters ? q : nxt;
+    const int init_grid = (int)std::min<int64_t>(1024, ((int64_t)a.nctx * a.ntot + 255) / 256);
+    if (sparse) {
+        double *qa = reinterpret_cast<double *>(w + offs[4]);
+        double *qb = reinterpret_cast<double *>(w + offs[5]);
         {
-            ProfScope p("lik", stream);
-            hipLaunchKernelGGL(lik_kernel, dim3(a.nwg), dim3(kThreads), lik_lds, stream, a, (const float *)cur,
-                               part);
+            ProfScope p("init", stream);
+            hipLaunchKernelGGL(init_q_kernel<double>, dim3(init_grid), dim3(256), 0, stream, a, qa);
         }
+        run_iterations<double>(m, algo, iters, a, part, qa, qb, q, lik_lds, upd_lds, stream, true);
+    } else {
+        float *qa = reinterpret_cast<float *>(w + offs[4]);
+        float *qb = reinterpret_cast<float *>(w + offs[5]);
         {
-            ProfScope p("update", stream);
-            if (algo == BI_ALGO_VMP)
-                hipLaunchKernelGGL(update_kernel<BI_ALGO_VMP>, dim3(a.nctx), dim3(256), upd_lds, stream, a,
-                                   (const float *)part, (const float *)cur, dst);
-            else
-                hipLaunchKernelGGL(update_kernel<BI_ALGO_MMP>, dim3(a.nctx), dim3(256), upd_lds, stream, a,
-                                   (const float *)part, (const float *)cur, dst);
+            ProfScope p("init", stream);
+            hipLaunchKernelGGL(init_q_kernel<float>, dim3(init_grid), dim3(256), 0, stream, a, qa);
         }
-        float *tmp = cur;
-        cur = nxt;
-        nxt = tmp;
+        run_iterations<float>(m, algo, iters, a, part, qa, qb, q, lik_lds, upd_lds, stream, false);
     }
-    e = hipGetLastError();
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(BI_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
     return BI_OK;
 }

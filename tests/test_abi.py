@@ -38,7 +38,11 @@ class ModDesc(ctypes.Structure):
                 ("Cp", ctypes.c_int32), ("nrow", ctypes.c_int32), ("ncol", ctypes.c_int32),
                 ("rf", ctypes.c_int32 * 2), ("rn", ctypes.c_int32 * 2), ("cf", ctypes.c_int32 * 2),
                 ("cn", ctypes.c_int32 * 2), ("zv_off", ctypes.c_int32), ("dsum", ctypes.c_int32),
-                ("la32_off", ctypes.c_int64), ("sp_ptr_off", ctypes.c_int64), ("sp_idx_off", ctypes.c_int64), ("sp_val_off", ctypes.c_int64)]
+                ("la32_off", ctypes.c_int64), ("csr_ptr_off", ctypes.c_int64), ("csr_ent_off", ctypes.c_int64),
+                ("csc_ptr_off", ctypes.c_int64), ("csc_ent_off", ctypes.c_int64), ("nnz", ctypes.c_int64)]
+
+
+SpEntry = np.dtype([("v", np.float64), ("ab", np.uint32), ("pad", np.uint32)])
 
 
 class FacDesc(ctypes.Structure):
@@ -166,3 +170,69 @@ def test_inference_validates_on_host_before_launch():
     finally:
         bi.bi_free_model(h)
     bi.bi_free_model(0)   # NULL is ignored
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_host_pack_sparse_planes(seed):
+    """BI_SPARSE_A: the CSR and CSC planes hold exactly the entries LN(A) - ln(eps)
+    of A > eps, with the other side's index split over its factors."""
+    rng = np.random.Generator(np.random.PCG64(900 + seed))
+    F = int(rng.integers(1, 5))
+    n = [int(x) for x in rng.integers(1, 7, size=F)]
+    M = int(rng.integers(1, 4))
+    deps = []
+    for _ in range(M):
+        k = int(rng.integers(1, F + 1))
+        deps.append(sorted(int(x) for x in rng.choice(F, size=k, replace=False)))
+    K = [int(x) for x in rng.integers(1, 5, size=M)]
+    model = synth.make_model(rng, n, [2] * F, K, deps, 1, 1.0, 1.0, sparsity=0.5, uniform_D=False)
+    flags = bi.BI_SPARSE_A
+    upper = bi.bi_plan_model(model.n, model.U, model.K, model.deps, 1, flags)
+    exact = bi.bi_plan_model_exact(model.n, model.U, model.K, model.deps, 1, model.A, flags)
+    assert exact <= upper
+    h, img = bi.bi_pack_model_host(model.n, model.U, model.K, model.deps, 1, model.A, model.B, model.D, flags)
+    try:
+        assert img.size == exact == bi.bi_get_model_stats(h)["device_bytes"]
+        mods, _ = _descs(img, model.M, model.F)
+        lne = np.log(1e-16)
+        for mi in range(model.M):
+            md = mods[mi]
+            A = model.A[mi][0].astype(np.float64).reshape(md.K, md.R, md.C)
+            want = np.where(A > 1e-16, np.log(np.maximum(A, 1e-16)) - lne, 0.0)
+            assert md.nnz == int((A > 1e-16).sum())
+            rn1 = md.rn[1] if md.nrow == 2 else 1
+            cn1 = md.cn[1] if md.ncol == 2 else 1
+            for side in ("csr", "csc"):
+                lines = md.R if side == "csr" else md.C
+                ptr_off = getattr(md, side + "_ptr_off")
+                ent = img[getattr(md, side + "_ent_off"):].view(SpEntry)[:md.nnz]
+                ptr = img[ptr_off:ptr_off + 4 * md.K * (lines + 1)].view(np.int32).reshape(md.K, lines + 1)
+                assert ptr[0, 0] == 0 and ptr[-1, -1] == md.nnz
+                assert np.all(np.diff(ptr, axis=1) >= 0) and np.all(ptr[1:, 0] == ptr[:-1, -1])
+                got = np.zeros_like(want)
+                for o in range(md.K):
+                    for l in range(lines):
+                        for e in ent[ptr[o, l]:ptr[o, l + 1]]:
+                            a, b = int(e["ab"]) >> 16, int(e["ab"]) & 0xFFFF
+                            assert e["v"] > 0
+                            if side == "csr":
+                                c = a * cn1 + b
+                                assert b < cn1 and got[o, l, c] == 0
+                                got[o, l, c] = e["v"]
+                            else:
+                                r = a * rn1 + b
+                                assert b < rn1 and got[o, r, l] == 0
+                                got[o, r, l] = e["v"]
+                np.testing.assert_allclose(got, want, rtol=0, atol=1e-13)
+    finally:
+        bi.bi_free_model(h)
+
+
+def test_sparse_layout_needs_a_shared_model():
+    with pytest.raises(bi.BiError) as ei:
+        bi.bi_plan_model([3], [1], [2], [[0]], 2, bi.BI_SPARSE_A)
+    assert ei.value.code == bi.BI_ERR_UNSUPPORTED
+    lib = bi.load()
+    out = ctypes.c_size_t(0)
+    d = bi._Desc([3], [1], [2], [[0]], 1, bi.BI_SPARSE_A)
+    assert lib.bi_plan_model_exact(ctypes.byref(d.c), None, ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG

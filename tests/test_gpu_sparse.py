@@ -1,0 +1,99 @@
+"""Sparse path (BI_SPARSE_A, shared model: fp64 gathers over the nonzero
+entries) against the oracle, the agent-resident path and the dense layout."""
+import functools
+import os
+
+import numpy as np
+import pytest
+
+from paper_2607_17855_amd import bi, synth
+import oracle
+from test_gpu_parity import check_invariants, run_gpu
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+
+
+def _shared_model(seed, n, U, K, deps, b, T, sparsity, iters=2):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    model = synth.make_model(rng, n, U, K, deps, 1, 1.0, 1.0, sparsity=sparsity, uniform_D=False)
+    obs, act = synth.sample_sequences(rng, model, b, T)
+    return synth.Workload(f"sparse{seed}", ["vmp", "mmp"], model, obs, act, iters)
+
+
+CASES = [
+    # (n, U, K, deps, b, T, sparsity)
+    # rank 1 (no row factors: one side only), rank 2 / 3 / 4 with one or two
+    # factors per side, several tiles of two-factor lines (13 x 11 rows), a
+    # bucket of more than 64 contexts (200 contexts, 2 outcomes), single-state
+    # factors, dense A (sparsity 0) and very sparse A
+    ([9, 7, 5], [2, 1, 3], [3, 2, 4], [[0, 1, 2], [1], [0, 2]], 24, 5, 0.5),
+    ([13, 11, 6, 3], [1, 2, 2, 1], [5, 3], [[0, 1, 2, 3], [1, 3]], 40, 4, 0.7),
+    ([70], [2], [3], [[0]], 30, 3, 0.3),
+    ([33, 5], [2, 2], [2, 2, 3], [[0, 1], [0], [1]], 64, 6, 0.0),
+    ([4, 4, 4, 4], [1, 1, 1, 1], [2], [[0, 1, 2, 3]], 100, 2, 0.9),
+    ([1, 6, 1], [1, 2, 1], [3, 2], [[0, 1, 2], [1, 2]], 12, 3, 0.5),
+    ([40, 40], [3, 2], [4], [[0, 1]], 20, 4, 0.95),
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+@pytest.mark.parametrize("iters", [1, 3])
+def test_sparse_small_vs_oracle_and_agent(case, iters):
+    n, U, K, deps, b, T, sp = CASES[case]
+    w = _shared_model(70 + case, n, U, K, deps, b, T, sp, iters=iters)
+    for algo in ("vmp", "mmp"):
+        q, pm = run_gpu(w, algo, flags=bi.BI_SPARSE_A)
+        assert pm.workspace(w.b, w.T, algo) is not None, "sparse layout must take the sparse kernels"
+        check_invariants(w, q)
+        ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters)
+        err = float(np.abs(q - ref).max())
+        print(f"[gpu]   sparse vs oracle {err:.3e}", flush=True)
+        assert err <= TOL
+        old = os.environ.get("BI_FORCE_PATH")
+        os.environ["BI_FORCE_PATH"] = "agent"
+        try:
+            qa, _ = run_gpu(w, algo, pm=pm)
+        finally:
+            if old is None:
+                os.environ.pop("BI_FORCE_PATH", None)
+            else:
+                os.environ["BI_FORCE_PATH"] = old
+        assert float(np.abs(q - qa).max()) <= TOL
+        # FPI has no sparse kernel: the same packed model runs it agent-resident
+        if algo == "vmp":
+            assert pm.workspace(w.b, w.T, "fpi") is None
+        pm.close()
+
+
+def test_sparse_fpi_uses_dense_planes():
+    n, U, K, deps, b, T, sp = CASES[0]
+    w = _shared_model(90, n, U, K, deps, b, T, sp, iters=3)
+    q, pm = run_gpu(w, "fpi", flags=bi.BI_SPARSE_A)
+    ref = oracle.infer("fpi", w.model, w.obs, w.act, w.iters)
+    assert float(np.abs(q - ref).max()) <= TOL
+    pm.close()
+
+
+@functools.lru_cache(maxsize=None)
+def cfg5():
+    return synth.config5()
+
+
+CFG5_AGENTS = [0, 21, 42, 63]
+
+
+@pytest.mark.parametrize("algo", ["vmp", "mmp"])
+def test_config5_sparse(algo):
+    w = cfg5()
+    q, pm = run_gpu(w, algo, flags=bi.BI_SPARSE_A)
+    st = pm.stats()
+    print(f"[gpu]   config 5 sparse: nnz {st['a_nnz']} device bytes {st['device_bytes']}", flush=True)
+    check_invariants(w, q)
+    q2, _ = run_gpu(w, algo, pm=pm)
+    assert np.array_equal(q, q2), "sparse path is not reproducible"
+    ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=CFG5_AGENTS)
+    err = float(np.abs(q[CFG5_AGENTS] - ref).max())
+    print(f"[gpu]   config 5 {algo} sparse vs oracle (agents {CFG5_AGENTS}): {err:.3e}", flush=True)
+    assert err <= TOL
+    pm.close()

@@ -5,13 +5,16 @@ Workload: the large shared-model case -- F = 4 hidden factors of 32 states
 (4 actions each), M = 4 modalities of 32 outcomes that each depend on all four
 factors (32^5 entries per A_m, 90% random zeros, renormalised columns), one
 model shared by b = 64 agents, window T = 16, 16 iterations.  One step runs
-VMP and then MMP over the whole batch (dense A layout, fp32 matrix-core
-contractions with fp64 message sums and updates: BI_FAST_F32).  Inputs are
-resident in HBM before timing starts; the model is packed once outside the
-timed region (the one-time layout step).
+VMP and MMP over the whole batch on both A layouts:
+  dense  (BI_DENSE_A | BI_FAST_F32): fp32 matrix-core contractions over the
+         dense slices, fp64 message sums / transitions / softmax;
+  sparse (BI_SPARSE_A): fp64 gathers over the nonzero entries.
+Inputs are resident in HBM before timing starts; each model is packed once
+outside the timed region (the one-time layout step).
 
 Prints one JSON line.  value = belief updates per second over the whole job,
-one belief update being one (agent, time step, iteration) of one algorithm.
+one belief update being one (agent, time step, iteration) of one algorithm
+on one layout.
 """
 import argparse
 import hashlib
@@ -25,42 +28,59 @@ sys.path.insert(0, ROOT)
 
 METRIC = "belief updates/sec (agents×timesteps×iters) + achieved HBM GB/s, 1 MI355X"
 PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_FP64_VALU_TFLOPS = 78.6
 PEAK_HBM_GBPS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lik_cfg5_traffic.json")
-LIK_SOURCE = os.path.join(ROOT, "paper_2607_17855_amd", "csrc", "stream.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cfg5.json")
+CSRC = os.path.join(ROOT, "paper_2607_17855_amd", "csrc")
+# likelihood kernels: profile class -> (kernel symbol, source file)
+LIK = {"lik": ("lik_kernel", "stream.hip"), "lik_sparse": ("sparse_lik_kernel", "sparse.hip")}
+LAYOUTS = ("dense", "sparse")
+ALGOS = ("vmp", "mmp")
 
 
-def source_sha() -> str:
-    with open(LIK_SOURCE, "rb") as fh:
+def source_sha(fname: str) -> str:
+    with open(os.path.join(CSRC, fname), "rb") as fh:
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
-def lik_flops_per_launch(model, nctx: int) -> float:
-    """Algorithmic flops of one likelihood launch: per context and modality the
-    two passes Z = X t and V = s X over the R x C slice, one FMA (2 flops) per
-    slice entry each -- 16.8 MFLOP per belief update on this workload."""
-    per_ctx = 0.0
+def slice_sizes(model):
+    out = []
     for d in model.deps:
         P = 1
         for f in d:
             P *= model.n[f]
-        per_ctx += 2 * 2 * P
-    return per_ctx * nctx
+        out.append(P)
+    return out
 
 
-def lik_bytes_per_launch(model, obs) -> float:
-    """Algorithmic HBM bytes of one likelihood launch: every slice observed by at
-    least one context is read once (fp32), plus the fp32 marginals read and
-    the partial messages written (computed from the tile count)."""
+def dense_lik_work(model, obs):
+    """Algorithmic flops and HBM bytes of one dense likelihood launch: per
+    context and modality the two passes Z = X t and V = s X over the slice,
+    one FMA (2 flops) per slice entry each (16.8 MFLOP per belief update);
+    every slice observed by at least one context is read once in fp32."""
     import numpy as np
-    total = 0.0
-    for m, d in enumerate(model.deps):
-        P = 1
-        for f in d:
-            P *= model.n[f]
-        used = len(np.unique(obs[:, :, m]))
-        total += 4.0 * P * used
-    return total
+    nctx = obs.shape[0] * obs.shape[1]
+    flops = sum(2 * 2 * P for P in slice_sizes(model)) * nctx
+    used = [len(np.unique(obs[:, :, m])) for m in range(model.M)]
+    nbytes = sum(4.0 * P * u for P, u in zip(slice_sizes(model), used))
+    return float(flops), float(nbytes)
+
+
+def sparse_lik_work(model, obs):
+    """Algorithmic flops and HBM bytes of one sparse likelihood launch: for
+    every context, each nonzero of its observed slices is visited twice (row
+    lines and column lines), one multiply and one FMA (3 flops) each; every
+    observed slice's entries are read once per side (16 B per entry and side)."""
+    import numpy as np
+    flops = 0.0
+    nbytes = 0.0
+    for m in range(model.M):
+        A = model.A[m][0].reshape(model.K[m], -1)
+        nnz = (A.astype(np.float64) > 1e-16).sum(axis=1)
+        cnt = np.bincount(obs[:, :, m].ravel(), minlength=model.K[m])
+        flops += 2 * 3 * float((nnz * cnt).sum())
+        nbytes += 2 * 16.0 * float(nnz[cnt > 0].sum())
+    return flops, nbytes
 
 
 def cpu_baseline(w, algos, budget_s: float = 25.0):
@@ -82,15 +102,23 @@ def cpu_baseline(w, algos, budget_s: float = 25.0):
     return {"value": done_bu / dt, "unit": "belief_updates/s", "cores": min(threads, len(agents)),
             "kind": "oracle",
             "sample": f"{len(agents)} of {w.b} agents x T={w.T} x {w.iters} iters, "
-                      f"{'+'.join(algos[:calls])}, fp64 looped oracle, {dt:.1f} s wall"}
+                      f"{'+'.join(algos[:calls])}, fp64 looped oracle (layout-independent), {dt:.1f} s wall"}
+
+
+def load_traffic():
+    if not os.path.exists(TRAFFIC_FILE):
+        return {}
+    with open(TRAFFIC_FILE) as fh:
+        return json.load(fh)
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layouts", default=",".join(LAYOUTS), help="comma list of A layouts in a step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a device-to-device copy of MIB MiB (reference kernel for HBM byte counters)")
     args = ap.parse_args()
@@ -98,8 +126,9 @@ def main():
         print("bench.py: this library runs on one GPU; multi-GPU runs are not part of this build "
               "(agents shard across GPUs with no communication, see DESIGN.md)", file=sys.stderr)
         sys.exit(2)
+    layouts = [x for x in args.layouts.split(",") if x]
+    assert set(layouts) <= set(LAYOUTS) and layouts, f"layouts must be among {LAYOUTS}"
 
-    import numpy as np
     import torch
     from paper_2607_17855_amd import bi, synth
 
@@ -107,18 +136,21 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = synth.config5()
-    algos = ["vmp", "mmp"]
-    flags = bi.BI_DENSE_A | bi.BI_FAST_F32
-    pm = bi.PackedModel(w.model, flags=flags, device=dev)
+    flags = {"dense": bi.BI_DENSE_A | bi.BI_FAST_F32, "sparse": bi.BI_SPARSE_A}
+    pms = {lay: bi.PackedModel(w.model, flags=flags[lay], device=dev) for lay in layouts}
     obs = torch.from_numpy(w.obs).to(dev)
     act = torch.from_numpy(w.act).to(dev)
-    qs = {a: torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device=dev) for a in algos}
-    wss = {a: pm.workspace(w.b, w.T, a) for a in algos}
+    qs = {(lay, a): torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device=dev)
+          for lay in layouts for a in ALGOS}
+    wss = {(lay, a): pms[lay].workspace(w.b, w.T, a) for lay in layouts for a in ALGOS}
+    for key, ws in wss.items():
+        assert ws is not None, f"{key}: config 5 must run on the streaming kernels"
     stream = torch.cuda.current_stream()
 
     def step():
-        for a in algos:
-            pm.infer(a, obs, act, w.iters, q=qs[a], ws=wss[a], stream=stream)
+        for lay in layouts:
+            for a in ALGOS:
+                pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=stream)
 
     if args.copy_calibration > 0:
         n = args.copy_calibration * (1 << 20) // 4
@@ -145,24 +177,35 @@ def main():
     wall = time.perf_counter() - t0
     prof = bi.bi_profile_end()
     ms_step = ev0.elapsed_time(ev1) / args.steps
-    bu_per_step = len(algos) * w.b * w.T * w.iters
+    bu_per_step = len(layouts) * len(ALGOS) * w.b * w.T * w.iters
     value = bu_per_step / (ms_step / 1e3)
 
-    nctx = w.b * w.T
-    lik_name = "lik32" if "lik32" in prof else "lik"
-    lik_launches, lik_ms = prof.get(lik_name, (0, 0.0))
-    lik_avg_ms = lik_ms / max(lik_launches, 1)
-    flops = lik_flops_per_launch(w.model, nctx)
-    achieved = flops / (lik_avg_ms / 1e3) / 1e12
-    alg_bytes = lik_bytes_per_launch(w.model, w.obs)
-    traffic = None
-    hbm_gbps = None
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as fh:
-            tr = json.load(fh)
-        if tr.get("kernel_source_sha") == source_sha():
-            traffic = tr["hbm_bytes_per_launch"]
-            hbm_gbps = traffic / (lik_avg_ms / 1e3) / 1e9
+    traffic = load_traffic()
+    work = {"lik": dense_lik_work(w.model, w.obs), "lik_sparse": sparse_lik_work(w.model, w.obs)}
+    rooflines = {}
+    for cls, (kname, src) in LIK.items():
+        if cls not in prof:
+            continue
+        launches, total_ms = prof[cls]
+        avg_ms = total_ms / max(launches, 1)
+        flops, alg_bytes = work[cls]
+        tr = traffic.get(kname)
+        hbm = tr["hbm_bytes_per_launch"] if tr and tr.get("kernel_source_sha") == source_sha(src) else None
+        if cls == "lik":
+            bound, peak = "mfma", PEAK_FP32_MFMA_TFLOPS
+        else:
+            bound, peak = "alu", PEAK_FP64_VALU_TFLOPS
+        achieved = flops / (avg_ms / 1e3) / 1e12
+        rooflines[cls] = {
+            "bound": bound, "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+            "traffic": hbm, "kernel": kname, "avg_launch_ms": avg_ms, "launches": launches,
+            "total_ms": total_ms, "algorithmic_flops_per_launch": flops,
+            "algorithmic_bytes_per_launch": alg_bytes,
+            "algorithmic_GBps": alg_bytes / (avg_ms / 1e3) / 1e9,
+            "measured_hbm_GBps": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9,
+            "hbm_frac": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+        }
+    dominant = max(rooflines, key=lambda c: rooflines[c]["total_ms"])
     out = {
         "metric": METRIC,
         "value": value,
@@ -174,25 +217,21 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32+f64",
         "data": "synthetic",
         "config": {"workload": "shared model F=4x32 states (U=4), M=4x32 outcomes on all factors, 90% zeros, "
-                               "b=64, T=16, 16 iters; step = VMP + MMP, dense A, fp32 MFMA contractions",
-                   "b": w.b, "T": w.T, "iters": w.iters, "algos": algos, "layout": "dense",
-                   "flags": "BI_DENSE_A|BI_FAST_F32"},
-        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": traffic,
-                     "kernel": lik_name + "_kernel", "avg_launch_ms": lik_avg_ms, "launches": lik_launches,
-                     "algorithmic_flops_per_launch": flops, "algorithmic_bytes_per_launch": alg_bytes},
-        "hbm": {"algorithmic_GBps": alg_bytes / (lik_avg_ms / 1e3) / 1e9,
-                "measured_GBps": hbm_gbps, "peak_GBps": PEAK_HBM_GBPS},
+                               "b=64, T=16, 16 iters; step = VMP + MMP on the dense (fp32 MFMA) and sparse "
+                               "(fp64) A layouts",
+                   "b": w.b, "T": w.T, "iters": w.iters, "algos": list(ALGOS), "layouts": layouts},
+        "roofline": rooflines[dominant],
+        "roofline_all": rooflines,
         "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
         "wall_s_timed": wall,
-        "dtype_note": "fp32 matrix-core contractions (v_mfma_f32_16x16x4f32); fp64 message sums, transitions "
-                      "and softmax",
+        "dtype_note": "dense layout: fp32 matrix-core contractions (v_mfma_f32_16x16x4f32) with fp64 message sums, "
+                      "transitions and softmax; sparse layout: fp64 throughout",
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, algos)
+        out["cpu_baseline"] = cpu_baseline(w, list(ALGOS))
     print(json.dumps(out), flush=True)
 
 

@@ -12,7 +12,8 @@
 // (CSC).  An entry is {double value; uint32 (a << 16 | b)} where (a, b) is the
 // split of the other side's index over that side's one or two factors (row
 // entries carry the column's (c0, c1), column entries the row's (r0, r1)), so
-// the kernels never divide.
+// the kernels never divide.  Inside a line the entries are ordered by (a, b),
+// so entries with equal a form runs; the last entry of every run is flagged.
 //
 // Precision.  The mean-field fixed-point iterations are ill-conditioned for
 // some models: a relative perturbation of 1e-7 in A (fp32 rounding) moves
@@ -81,7 +82,7 @@ struct FacDesc {
 struct SpEntry {
     double v;       // log(max(A, 1e-16)) - log(1e-16) > 0
     uint32_t ab;    // (a << 16) | b: split of the other side's index
-    uint32_t pad;
+    uint32_t run;   // 1 if the next entry of the line has another a (or the line ends), else 0
 };
 
 inline int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }

@@ -216,6 +216,13 @@ static void parallel_for(int64_t count, Fn fn)
     for (auto &x : th) x.join();
 }
 
+// flag the last entry of every run of equal first-split index in a line
+static void mark_runs(SpEntry *line, int64_t count)
+{
+    for (int64_t i = 0; i < count; ++i)
+        line[i].run = (i + 1 == count || (line[i + 1].ab >> 16) != (line[i].ab >> 16)) ? 1u : 0u;
+}
+
 static inline double ln_clamped(double x) { return std::log(x > kEps ? x : kEps); }
 
 int fill(const bi_model *m, const float *const *A, const float *const *B, const float *const *D, char *host,
@@ -272,10 +279,12 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
             const float *a = src + (int64_t)o * RC;
             for (int64_t r = 0; r < R; ++r) {
                 rptr[(int64_t)o * (R + 1) + r] = (int32_t)e;
+                const int64_t first = e;
                 for (int64_t c = 0; c < C; ++c) {
                     const double x = a[r * C + c];
                     if (x > kEps) rent[e++] = SpEntry{std::log(x) - lne, csplit(c), 0u};
                 }
+                mark_runs(rent + first, e - first);
             }
             rptr[(int64_t)o * (R + 1) + R] = (int32_t)e;
         }
@@ -284,10 +293,12 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
             const float *a = src + (int64_t)o * RC;
             for (int64_t c = 0; c < C; ++c) {
                 cptr[(int64_t)o * (C + 1) + c] = (int32_t)e;
+                const int64_t first = e;
                 for (int64_t r = 0; r < R; ++r) {
                     const double x = a[r * C + c];
                     if (x > kEps) cent[e++] = SpEntry{std::log(x) - lne, rsplit(r), 0u};
                 }
+                mark_runs(cent + first, e - first);
             }
             cptr[(int64_t)o * (C + 1) + C] = (int32_t)e;
         }

@@ -13,7 +13,7 @@
 // column factors as the entry side, role 1 over the columns with the row
 // factors as the entry side.
 //
-// A workgroup (8 waves) owns one tile of lines of one (modality, role,
+// A workgroup (16 waves) owns one tile of lines of one (modality, role,
 // outcome).  Its lanes are the contexts that observed the outcome, 64 at a
 // time; every wave walks its lines' entries in order (the entry stream is
 // uniform across the wave, so entries come in through scalar loads) and each
@@ -34,12 +34,17 @@
 namespace bi {
 namespace {
 
-constexpr int kSpThreads = 512;  // 8 waves
+constexpr int kSpThreads = 1024; // 16 waves: the gathers are latency-bound, occupancy hides it
 constexpr int kSpWaves = kSpThreads / 64;
 constexpr int kSpLanes = 64;     // contexts per pass
 constexpr int kSpLines = 128;    // target lines per tile
 constexpr int kZS = kSpLanes + 1;  // padded line-tile stride (doubles)
-constexpr int kSpBatch = 8;      // entries per gather round
+constexpr int kSpBatch = 16;     // entries per gather round (4 x 64-byte scalar loads)
+
+// Entries and line pointers are read through the constant address space:
+// the addresses are wave-uniform, so every load is a wide scalar load.
+#define BI_CONST __attribute__((address_space(4)))
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 // Geometry of one role of a modality.
 struct Side {
@@ -106,8 +111,8 @@ __global__ __launch_bounds__(kSpThreads, 1) void sparse_lik_kernel(StreamArgs a,
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: entry stream via scalar loads
 
-    const int32_t *lptr = reinterpret_cast<const int32_t *>(mbase + sd_.ptr_off) + (int64_t)o * (sd_.lines + 1);
-    const SpEntry *ent = reinterpret_cast<const SpEntry *>(mbase + sd_.ent_off);
+    const BI_CONST int32_t *lptr = (const BI_CONST int32_t *)(mbase + sd_.ptr_off) + (int64_t)o * (sd_.lines + 1);
+    const BI_CONST u32x4 *ent = (const BI_CONST u32x4 *)(mbase + sd_.ent_off);   // SpEntry as 4 dwords
     const int off_e0 = sd_.nent >= 1 ? a.facs[sd_.ef0].q_off : -1;
     const int off_e1 = sd_.nent == 2 ? a.facs[sd_.ef1].q_off : -1;
     const int off_l0 = a.facs[sd_.lf0].q_off;
@@ -146,10 +151,10 @@ __global__ __launch_bounds__(kSpThreads, 1) void sparse_lik_kernel(StreamArgs a,
             for (; e + kSpBatch <= e1; e += kSpBatch) {
                 double v[kSpBatch], p[kSpBatch];
                 uint32_t ab[kSpBatch];
-                const uint4 *eb = reinterpret_cast<const uint4 *>(ent + e);   // one base, constant offsets
+                const BI_CONST u32x4 *eb = ent + e;   // one base, constant offsets
 #pragma unroll
                 for (int k = 0; k < kSpBatch; ++k) {
-                    const uint4 x = eb[k];
+                    const u32x4 x = eb[k];
                     v[k] = __hiloint2double((int)x.y, (int)x.x);
                     ab[k] = x.z;
                 }
@@ -159,8 +164,9 @@ __global__ __launch_bounds__(kSpThreads, 1) void sparse_lik_kernel(StreamArgs a,
                 for (int k = 0; k < kSpBatch; ++k) acc = fma(v[k], p[k], acc);
             }
             for (; e < e1; ++e) {
-                const uint32_t ab = ent[e].ab;
-                acc = fma(ent[e].v, t0[(ab >> 16) * kSpLanes] * t1[(ab & 0xffffu) * kSpLanes], acc);
+                const u32x4 x = ent[e];
+                acc = fma(__hiloint2double((int)x.y, (int)x.x), t0[(x.z >> 16) * kSpLanes] * t1[(x.z & 0xffffu) * kSpLanes],
+                          acc);
             }
             zt[(l - lb) * kZS + lane] = acc;
         }

@@ -9,11 +9,10 @@
 // Sparse A (models shared by every agent).  Every slice X of LA - shifted by
 // log(1e-16) instead of its median, so that the structural zeros of A are
 // exactly 0 and drop out - is stored twice, by rows (CSR) and by columns
-// (CSC).  An entry is {double value; uint32 (a << 16 | b)} where (a, b) is the
+// (CSC).  An entry is {double value; uint32 a; uint32 b} where (a, b) is the
 // split of the other side's index over that side's one or two factors (row
 // entries carry the column's (c0, c1), column entries the row's (r0, r1)), so
-// the kernels never divide.  Inside a line the entries are ordered by (a, b),
-// so entries with equal a form runs; the last entry of every run is flagged.
+// the kernels never divide.  Inside a line the entries are ordered by (a, b).
 //
 // Precision.  The mean-field fixed-point iterations are ill-conditioned for
 // some models: a relative perturbation of 1e-7 in A (fp32 rounding) moves
@@ -81,8 +80,7 @@ struct FacDesc {
 
 struct SpEntry {
     double v;       // log(max(A, 1e-16)) - log(1e-16) > 0
-    uint32_t ab;    // (a << 16) | b: split of the other side's index
-    uint32_t run;   // 1 if the next entry of the line has another a (or the line ends), else 0
+    uint32_t a, b;  // split of the other side's index over that side's factors
 };
 
 inline int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }

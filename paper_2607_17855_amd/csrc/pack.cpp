@@ -153,8 +153,6 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
         md.csr_ptr_off = md.csr_ent_off = md.csc_ptr_off = md.csc_ent_off = -1;
         md.nnz = 0;
         if (flags & BI_SPARSE_A) {
-            if (R > 65535 || C > 65535 || md.rn[0] > 65535 || md.cn[0] > 65535)
-                return fail(BI_ERR_UNSUPPORTED, "modality %d: sparse layout needs dimensions below 65536", mm);
             // exact entry count when A is given, else an upper bound (dense)
             int64_t nnz = (int64_t)md.K * R * C;
             if (A) {
@@ -216,13 +214,6 @@ static void parallel_for(int64_t count, Fn fn)
     for (auto &x : th) x.join();
 }
 
-// flag the last entry of every run of equal first-split index in a line
-static void mark_runs(SpEntry *line, int64_t count)
-{
-    for (int64_t i = 0; i < count; ++i)
-        line[i].run = (i + 1 == count || (line[i + 1].ab >> 16) != (line[i].ab >> 16)) ? 1u : 0u;
-}
-
 static inline double ln_clamped(double x) { return std::log(x > kEps ? x : kEps); }
 
 int fill(const bi_model *m, const float *const *A, const float *const *B, const float *const *D, char *host,
@@ -272,19 +263,17 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
         // split of a row / column index over its side's factors
         const int rn1 = md.nrow == 2 ? md.rn[1] : 1;
         const int cn1 = md.ncol == 2 ? md.cn[1] : 1;
-        auto rsplit = [&](int64_t r) { return (uint32_t)((r / rn1) << 16 | (r % rn1)); };
-        auto csplit = [&](int64_t c) { return (uint32_t)((c / cn1) << 16 | (c % cn1)); };
+        auto rentry = [&](double v, int64_t r) { return SpEntry{v, (uint32_t)(r / rn1), (uint32_t)(r % rn1)}; };
+        auto centry = [&](double v, int64_t c) { return SpEntry{v, (uint32_t)(c / cn1), (uint32_t)(c % cn1)}; };
         int64_t e = 0;
         for (int o = 0; o < md.K; ++o) {
             const float *a = src + (int64_t)o * RC;
             for (int64_t r = 0; r < R; ++r) {
                 rptr[(int64_t)o * (R + 1) + r] = (int32_t)e;
-                const int64_t first = e;
                 for (int64_t c = 0; c < C; ++c) {
                     const double x = a[r * C + c];
-                    if (x > kEps) rent[e++] = SpEntry{std::log(x) - lne, csplit(c), 0u};
+                    if (x > kEps) rent[e++] = centry(std::log(x) - lne, c);
                 }
-                mark_runs(rent + first, e - first);
             }
             rptr[(int64_t)o * (R + 1) + R] = (int32_t)e;
         }
@@ -293,12 +282,10 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
             const float *a = src + (int64_t)o * RC;
             for (int64_t c = 0; c < C; ++c) {
                 cptr[(int64_t)o * (C + 1) + c] = (int32_t)e;
-                const int64_t first = e;
                 for (int64_t r = 0; r < R; ++r) {
                     const double x = a[r * C + c];
-                    if (x > kEps) cent[e++] = SpEntry{std::log(x) - lne, rsplit(r), 0u};
+                    if (x > kEps) cent[e++] = rentry(std::log(x) - lne, r);
                 }
-                mark_runs(cent + first, e - first);
             }
             cptr[(int64_t)o * (C + 1) + C] = (int32_t)e;
         }

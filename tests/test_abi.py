@@ -42,7 +42,7 @@ class ModDesc(ctypes.Structure):
                 ("csc_ptr_off", ctypes.c_int64), ("csc_ent_off", ctypes.c_int64), ("nnz", ctypes.c_int64)]
 
 
-SpEntry = np.dtype([("v", np.float64), ("ab", np.uint32), ("run", np.uint32)])
+SpEntry = np.dtype([("v", np.float64), ("a", np.uint32), ("b", np.uint32)])
 
 
 class FacDesc(ctypes.Structure):
@@ -213,15 +213,12 @@ def test_host_pack_sparse_planes(seed):
                 for o in range(md.K):
                     for l in range(lines):
                         le = ent[ptr[o, l]:ptr[o, l + 1]]
-                        if le.size:
-                            # ordered by (a, b); the last entry of every run of equal a is flagged
-                            keys = le["ab"].astype(np.int64)
-                            assert np.all(np.diff(keys) > 0)
-                            a_idx = keys >> 16
-                            want_run = np.append(a_idx[1:] != a_idx[:-1], True)
-                            np.testing.assert_array_equal(le["run"], want_run.astype(np.uint32))
+                        on1 = cn1 if side == "csr" else rn1
+                        # ordered by the other side's index
+                        keys = le["a"].astype(np.int64) * on1 + le["b"]
+                        assert np.all(np.diff(keys) > 0)
                         for e in le:
-                            a, b = int(e["ab"]) >> 16, int(e["ab"]) & 0xFFFF
+                            a, b = int(e["a"]), int(e["b"])
                             assert e["v"] > 0
                             if side == "csr":
                                 c = a * cn1 + b

@@ -1,0 +1,330 @@
+// Dense likelihood messages on fp32 matrix cores, one contraction per
+// workgroup (BI_FAST_F32, models shared by every agent, every modality with
+// two factors on each side, the second factors of 16 or 32 states and the
+// first factors of an even number of states up to 32).
+//
+// The two leave-one-out contractions of a slice X (two-sided view of
+// layout.h, Sec. IV marginalisation) are done by separate workgroups, each
+// over "lines" of X and contracting the other side (the "entries"):
+//   role 0 (lines = rows):    Z[c][r]   = sum_{e0,e1} q_e0[c][e0] q_e1[c][e1] X[r][(e0,e1)]
+//   role 1 (lines = columns): V[c][col] = sum_{e0,e1} q_e0[c][e0] q_e1[c][e1] X[(e0,e1)][col]
+// For each state e0 of the entry side's first factor, the contraction over
+// e1 is a 16x16x4 fp32 MFMA chain whose A operand is q_e1 scaled by
+// q_e0[c][e0] (one multiply per operand element), so the outer product of the
+// marginals is never built and the result accumulates in registers over the
+// whole slice.  The B operand is streamed from HBM straight into registers
+// (one 16-byte load per lane feeds four MFMAs); a wave owns 64 lines, a
+// workgroup 4 waves.  At the end the line values go through LDS and are
+// folded into the line factors' messages (fixed order, no atomics): the
+// first line factor's messages of the tile's line groups directly, the
+// second line factor's as one partial vector per tile.  Both roles of a slice
+// are dispatched next to each other, so the second read of the slice mostly
+// hits the last-level cache.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "internal.h"
+#include "profile.h"
+#include "stream.h"
+
+namespace bi {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kWaveLines = 64;                 // lines per wave
+constexpr int kTileLines = kWaves * kWaveLines; // lines per workgroup (at most)
+constexpr int kMaxKb = 3;                      // 16-context MFMA blocks per pass
+constexpr int kCtx = 16 * kMaxKb;
+constexpr int kMaxT = 8;                       // k-steps per first-factor state (second factor <= 32)
+constexpr int kZS = kCtx + 1;                  // line-tile stride (floats)
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+struct Geo {
+    int lines, ln0, ln1, lf0, lf1;   // line side (two factors)
+    int en0, en1, ef0, ef1;          // entry side (two factors)
+};
+
+__host__ __device__ inline Geo geo_of(const ModDesc &md, int role)
+{
+    Geo g;
+    const bool rows = role == 0;
+    g.lines = rows ? md.R : md.C;
+    g.lf0 = rows ? md.rf[0] : md.cf[0];
+    g.lf1 = rows ? md.rf[1] : md.cf[1];
+    g.ln0 = rows ? md.rn[0] : md.cn[0];
+    g.ln1 = rows ? md.rn[1] : md.cn[1];
+    g.ef0 = rows ? md.cf[0] : md.rf[0];
+    g.ef1 = rows ? md.cf[1] : md.rf[1];
+    g.en0 = rows ? md.cn[0] : md.rn[0];
+    g.en1 = rows ? md.cn[1] : md.rn[1];
+    return g;
+}
+
+// line groups per tile: whole first-factor states, at most kTileLines lines
+__host__ __device__ inline int split_groups(const Geo &g) { return std::max(1, kTileLines / g.ln1); }
+
+template <int NKB, int ROLE, int NT>
+__device__ void split_tile(const StreamArgs &a, const Geo &g, const float *__restrict__ X, int64_t Cp, int lb,
+                           int le, const float *qe0, const float *qe1, float *zt)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wl0 = lb + kWaveLines * wave;
+    if (wl0 >= le) return;
+    const int li = lane & 15, lg = lane >> 4;
+    // NT = en1 / 4 k-steps per first-factor state.  A operand of k-step t,
+    // before the scaling by q_e0: q_e1[ctx][e1(t)]
+    float a1[NT][NKB];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int e1 = ROLE == 0 ? 16 * (t >> 2) + 4 * lg + (t & 3) : 4 * t + lg;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) a1[t][kb] = qe1[(16 * kb + li) * kMaxT * 4 + e1];
+    }
+    f4 acc[4][NKB];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) acc[j][kb] = f4{0.f, 0.f, 0.f, 0.f};
+
+    // B operand loads of one first-factor state, 16 bytes per lane each:
+    //   role 0: slot H j + h = line wl0 + 16 j + li, entries e0*en1 + 16 h + 4 lg .. +3 (H = NT / 4)
+    //   role 1: slot t = entry e0*en1 + 4 t + lg, lines wl0 + 4 li .. +3
+    // (lines past the tile are clamped to a valid one; their results are dropped)
+    // byte offsets inside the slice (a slice is below 2 GiB: 32-bit offsets
+    // from the wave-uniform slice base)
+    constexpr int H = NT / 4, NS = ROLE == 0 ? 4 * H : NT;
+    uint32_t bo[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (ROLE == 0) {
+            const int line = min(wl0 + 16 * (s / H) + li, le - 1);
+            bo[s] = 4u * (uint32_t)(line * (int)Cp + 16 * (s % H) + 4 * lg);
+        } else {
+            const int line = min(wl0 + 4 * li, le - 4);
+            bo[s] = 4u * (uint32_t)((4 * s + lg) * (int)Cp + line);
+        }
+    }
+    const uint32_t step = 4u * (ROLE == 0 ? 4 * NT : 4 * NT * (uint32_t)Cp);   // to the next first-factor state
+    const char *Xb = reinterpret_cast<const char *>(X);
+    auto load = [&](f4 (&b)[NS], int e0) {
+        const uint32_t eo = (uint32_t)e0 * step;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) b[s] = *reinterpret_cast<const f4 *>(Xb + (bo[s] + eo));
+    };
+    auto use = [&](const f4 (&b)[NS], int e0) {
+        float s0[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) s0[kb] = qe0[(16 * kb + li) * 32 + e0];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            float at[NKB];
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) at[kb] = a1[t][kb] * s0[kb];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float bv = ROLE == 0 ? b[H * j + (t >> 2)][t & 3] : b[t][j];
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb)
+                    acc[j][kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(at[kb], bv, acc[j][kb], 0, 0, 0);
+            }
+        }
+    };
+    // ping-pong: the loads of state e0 + 1 are in flight while state e0 is used
+    // (en0 is even; the last round re-reads the last state, unused)
+    f4 ba[NS], bb[NS];
+    load(ba, 0);
+    for (int e0 = 0; e0 < g.en0; e0 += 2) {
+        load(bb, e0 + 1);
+        use(ba, e0);
+        load(ba, min(e0 + 2, g.en0 - 1));
+        use(bb, e0 + 1);
+    }
+    // D[ctx][line]: lane holds contexts 16 kb + 4 lg + v of line n = li
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int line = ROLE == 0 ? wl0 + 16 * j + li : wl0 + 4 * li + j;
+        if (line < le)
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) zt[(line - lb) * kZS + 16 * kb + 4 * lg + v] = acc[j][kb][v];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void split_lik_kernel(StreamArgs a, const float *__restrict__ q,
+                                                             float *__restrict__ part)
+{
+    extern __shared__ float sh[];
+    __shared__ int ctxs[kCtx];
+    // decode (modality, outcome, role, tile): the two roles of a modality share
+    // its workgroup range, outcome-major, so both roles of a slice run together
+    const int wg = blockIdx.x;
+    int m = 0;
+    while (m + 1 < a.M && a.task[2 * (m + 1)].wg0 <= wg) ++m;
+    const SpTask t0 = a.task[2 * m], t1 = a.task[2 * m + 1];
+    const int per_o = t0.tiles + t1.tiles;
+    const int local = wg - t0.wg0;
+    const int o = local / per_o, r = local - o * per_o;
+    const int role = r < t0.tiles ? 0 : 1;
+    const int tile = role ? r - t0.tiles : r;
+    const SpTask tk = role ? t1 : t0;
+    const ModDesc &md = a.mods[m];
+    const Geo g = geo_of(md, role);
+    const int32_t *start = a.bstart + a.sm[m].bofs;
+    const int b0 = start[o], J = start[o + 1] - b0;
+    if (J == 0) return;
+    const int G = tk.G;
+    const int gs = tile * G, ng = min(G, g.ln0 - gs);
+    const int lb = gs * g.ln1, le = (gs + ng) * g.ln1;
+    const float *X = reinterpret_cast<const float *>(a.base + md.la32_off) + (int64_t)o * md.slice;
+    float *qe0 = sh;                      // [kCtx][32]: marginals of the entry side's first factor
+    float *qe1 = qe0 + kCtx * 32;         // [kCtx][32]: second factor
+    float *zt = qe1 + kCtx * kMaxT * 4;   // [tile lines][kZS]
+    const int tid = threadIdx.x;
+    const int off_e0 = a.facs[g.ef0].q_off, off_e1 = a.facs[g.ef1].q_off;
+    const int off_l0 = a.facs[g.lf0].q_off, off_l1 = a.facs[g.lf1].q_off;
+
+    for (int c0 = 0; c0 < J; c0 += kCtx) {
+        const int jc = min(kCtx, J - c0);
+        if (tid < kCtx) ctxs[tid] = tid < jc ? a.bctx[(int64_t)m * a.nctx + b0 + c0 + tid] : -1;
+        __syncthreads();
+        for (int i = tid; i < kCtx * 64; i += kThreads) {
+            const int c = i >> 6, s = i & 63;
+            const int ctx = ctxs[c];
+            float v = 0.0f;
+            if (s < 32) {
+                if (ctx >= 0 && s < g.en0) v = q[(int64_t)ctx * a.ntot + off_e0 + s];
+                qe0[c * 32 + s] = v;
+            } else {
+                if (ctx >= 0 && s - 32 < g.en1) v = q[(int64_t)ctx * a.ntot + off_e1 + s - 32];
+                qe1[c * 32 + s - 32] = v;
+            }
+        }
+        __syncthreads();
+        const int nkb = (jc + 15) >> 4;
+        const int nt = g.en1 >> 2;
+        // dispatch on (role, context blocks, k-steps per state); eligibility
+        // admits second factors of 16 or 32 states
+#define BI_SPLIT_TILE(R, K, T) split_tile<K, R, T>(a, g, X, md.Cp, lb, le, qe0, qe1, zt)
+#define BI_SPLIT_NT(R, K) \
+    if (nt == 8) BI_SPLIT_TILE(R, K, 8); \
+    else BI_SPLIT_TILE(R, K, 4)
+#define BI_SPLIT_KB(R) \
+    if (nkb == 1) { BI_SPLIT_NT(R, 1); } \
+    else if (nkb == 2) { BI_SPLIT_NT(R, 2); } \
+    else { BI_SPLIT_NT(R, 3); }
+        if (role == 0) {
+            BI_SPLIT_KB(0)
+        } else {
+            BI_SPLIT_KB(1)
+        }
+#undef BI_SPLIT_KB
+#undef BI_SPLIT_NT
+#undef BI_SPLIT_TILE
+        __syncthreads();
+        // fold: first line factor per (context, group) over l1; second line
+        // factor per (context, l1) over the tile's groups
+        const int64_t ps = a.pstride;
+        const int ln1 = g.ln1;
+        for (int i = tid; i < jc * ng; i += kThreads) {
+            const int c = i / ng, gg = i - c * ng;
+            const float *qc = q + (int64_t)ctxs[c] * a.ntot + off_l1;
+            const float *z = zt + gg * ln1 * kZS + c;
+            float acc = 0.0f;
+            for (int l1 = 0; l1 < ln1; ++l1) acc = fmaf(z[l1 * kZS], qc[l1], acc);
+            part[(int64_t)ctxs[c] * ps + tk.so + gs + gg] = acc;
+        }
+        for (int i = tid; i < jc * ln1; i += kThreads) {
+            const int c = i / ln1, l1 = i - c * ln1;
+            const float *qc = q + (int64_t)ctxs[c] * a.ntot + off_l0 + gs;
+            const float *z = zt + l1 * kZS + c;
+            float acc = 0.0f;
+            for (int gg = 0; gg < ng; ++gg) acc = fmaf(z[gg * ln1 * kZS], qc[gg], acc);
+            part[(int64_t)ctxs[c] * ps + tk.so + g.ln0 + (int64_t)tile * ln1 + l1] = acc;
+        }
+        __syncthreads();
+    }
+}
+
+size_t lds_bytes(const bi_model *m)
+{
+    size_t most = 0;
+    for (const ModDesc &md : m->mods)
+        for (int role = 0; role < 2; ++role) {
+            const Geo g = geo_of(md, role);
+            const size_t lines = (size_t)std::min(split_groups(g), g.ln0) * g.ln1;
+            most = std::max(most, sizeof(float) * ((size_t)kCtx * 64 + lines * kZS));
+        }
+    return most;
+}
+
+}  // namespace
+
+bool split_eligible(const bi_model *m)
+{
+    if (m->M > kStreamMaxM) return false;
+    int64_t pstride = 0;
+    for (const ModDesc &md : m->mods) {
+        if (md.la32_off < 0 || md.nrow != 2 || md.ncol != 2 || md.Cp != md.C) return false;
+        if (4 * (int64_t)md.R * md.Cp >= INT32_MAX) return false;   // 32-bit byte offsets inside a slice
+        for (int role = 0; role < 2; ++role) {
+            const Geo g = geo_of(md, role);
+            // 4 or 8 k-steps per first-factor state (16 or 32 states)
+            if ((g.en1 != 16 && g.en1 != 32) || g.en0 > 32 || g.en0 % 2 != 0 || g.ln1 > kTileLines || g.ln1 % 4 != 0)
+                return false;
+            const int G = split_groups(g);
+            pstride += g.ln0 + (int64_t)((g.ln0 + G - 1) / G) * g.ln1;
+        }
+        if (md.K > kStreamMaxK) return false;
+    }
+    return lds_bytes(m) <= 64 * 1024 && pstride < (int64_t)1 << 30;
+}
+
+int64_t split_plan(const bi_model *m, StreamArgs *a)
+{
+    int wg = 0;
+    int64_t so = 0;
+    a->ntask = 0;
+    a->nmsg = 0;
+    for (int i = 0; i < m->M; ++i) {
+        const ModDesc &md = m->mods[i];
+        const int wg0 = wg;
+        for (int role = 0; role < 2; ++role) {
+            const Geo g = geo_of(md, role);
+            SpTask &tk = a->task[a->ntask++];
+            tk.m = (int8_t)i;
+            tk.role = (int8_t)role;
+            const int G = split_groups(g);
+            tk.G = (int16_t)G;
+            tk.tiles = (g.ln0 + G - 1) / G;
+            tk.wg0 = wg0;
+            wg += md.K * tk.tiles;
+            tk.so = (int32_t)so;
+            MsgSrc &m0 = a->msg[a->nmsg++];
+            m0.f = g.lf0;
+            m0.copies = 1;
+            m0.stride = 0;
+            m0.off = (int32_t)so;
+            MsgSrc &m1 = a->msg[a->nmsg++];
+            m1.f = g.lf1;
+            m1.copies = tk.tiles;
+            m1.stride = g.ln1;
+            m1.off = (int32_t)(so + g.ln0);
+            so += g.ln0 + (int64_t)tk.tiles * g.ln1;
+        }
+    }
+    a->nwg = wg;
+    return so;
+}
+
+size_t split_lds_bytes(const bi_model *m) { return lds_bytes(m); }
+
+void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream)
+{
+    hipLaunchKernelGGL(split_lik_kernel, dim3(a.nwg), dim3(kThreads), lds_bytes(m), stream, a, q, part);
+}
+
+}  // namespace bi

@@ -76,6 +76,15 @@ size_t stream_workspace(const bi_model *m, int b, int T, bool sparse);
 int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
                   float *q, void *ws, hipStream_t stream, bool sparse);
 
+// Dense likelihood kernel with one contraction per workgroup (split.hip), for
+// models whose modalities all have two factors per side (second factors of
+// 16 or 32 states, first factors of at most 32): eligibility, planning (tasks and message sources; returns the
+// values of partial messages per context) and one launch.
+bool split_eligible(const bi_model *m);
+int64_t split_plan(const bi_model *m, StreamArgs *a);
+size_t split_lds_bytes(const bi_model *m);
+void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream);
+
 // Sparse likelihood kernel (sparse.hip): task planning and one launch.
 // sparse_plan fills a->task / a->ntask / a->nwg and the message sources,
 // and returns the values of partial messages per context.

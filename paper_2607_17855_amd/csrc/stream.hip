@@ -573,7 +573,7 @@ static void plan_ws(const bi_model *m, int b, int T, bool sparse, StreamArgs *a,
         sm.fofs = fofs;
         fofs += sm.K;
     }
-    a->pstride = sparse ? sparse_plan(m, a) : dense_plan(m, a);
+    a->pstride = sparse ? sparse_plan(m, a) : split_eligible(m) ? split_plan(m, a) : dense_plan(m, a);
     const int64_t es = sparse ? 8 : 4;
     int64_t off = 0;
     offs[0] = off;  off = align_up(off + 4 * (int64_t)bofs, kAlign);
@@ -597,14 +597,17 @@ template <typename QT>
 static void run_iterations(const bi_model *m, int algo, int iters, const StreamArgs &a, char *part, QT *qa, QT *qb,
                            float *q, size_t lik_lds, size_t upd_lds, hipStream_t stream, bool sparse)
 {
+    const bool split = !sparse && split_eligible(m);
     QT *cur = qa, *nxt = qb;
     using PT = QT;
     for (int k = 0; k < iters; ++k) {
         {
-            ProfScope p(sparse ? "lik_sparse" : "lik", stream);
+            ProfScope p(sparse ? "lik_sparse" : split ? "lik_split" : "lik", stream);
             if (sparse)
                 sparse_lik_launch(m, a, reinterpret_cast<const double *>(cur), reinterpret_cast<double *>(part),
                                   stream);
+            else if (split)
+                split_lik_launch(m, a, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream);
             else
                 hipLaunchKernelGGL(lik_kernel, dim3(a.nwg), dim3(kThreads), lik_lds, stream, a,
                                    reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part));
@@ -647,6 +650,8 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     size_t lik_lds = 0;
     if (sparse) {
         lik_lds = sparse_lds_bytes(m);
+    } else if (split_eligible(m)) {
+        lik_lds = split_lds_bytes(m);
     } else {
         int ncs_max = 1;
         for (const ModDesc &md : m->mods)
@@ -658,7 +663,7 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     if (sparse) {
         const int rc = sparse_prepare(m);
         if (rc != BI_OK) return rc;
-    } else {
+    } else if (!split_eligible(m)) {
         const hipError_t e = hipFuncSetAttribute((const void *)lik_kernel,
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lik_lds);
         if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));

@@ -62,6 +62,35 @@ def test_stream_small_vs_oracle_and_agent(case, iters, force_stream):
         pm.close()
 
 
+# shapes taken by the split matrix-core kernel (two factors per side, second
+# factors of 16 or 32 states, even first factors): ragged row and column
+# tiles, 4 and 8 k-steps per state, two modalities, several column tiles and
+# a bucket of more than 48 contexts
+SPLIT_CASES = [
+    ([6, 16, 4, 32], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], 24, 5),
+    ([2, 32, 10, 16], [1, 2, 1, 2], [4, 2], [[0, 1, 2, 3], [0, 1, 2, 3]], 40, 4),
+    ([4, 32, 32, 16], [2, 2, 1, 1], [2], [[0, 1, 2, 3]], 60, 2),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SPLIT_CASES)))
+def test_split_kernel_vs_oracle_and_agent(case, force_stream):
+    n, U, K, deps, b, T = SPLIT_CASES[case]
+    w = _shared_model(80 + case, n, U, K, deps, b, T, iters=2)
+    for algo in ("vmp", "mmp"):
+        q, pm = run_gpu(w, algo, flags=bi.BI_DENSE_A | bi.BI_FAST_F32)
+        check_invariants(w, q)
+        ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters)
+        err = float(np.abs(q - ref).max())
+        print(f"[gpu]   split stream vs oracle {err:.3e}", flush=True)
+        assert err <= TOL
+        os.environ["BI_FORCE_PATH"] = "agent"
+        qa, _ = run_gpu(w, algo, pm=pm)
+        os.environ["BI_FORCE_PATH"] = "stream"
+        assert float(np.abs(q - qa).max()) <= TOL
+        pm.close()
+
+
 @functools.lru_cache(maxsize=None)
 def cfg5():
     return synth.config5()

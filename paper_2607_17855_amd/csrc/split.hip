@@ -134,13 +134,19 @@ __device__ void split_tile(const StreamArgs &a, const Geo &g, const float *__res
     };
     // ping-pong: the loads of state e0 + 1 are in flight while state e0 is used
     // (en0 is even; the last round re-reads the last state, unused)
+    // (the scheduling barriers keep each batch of loads ahead of the MFMAs
+    // that do not need it; left alone, the compiler sinks them to their use)
     f4 ba[NS], bb[NS];
     load(ba, 0);
     for (int e0 = 0; e0 < g.en0; e0 += 2) {
         load(bb, e0 + 1);
+        __builtin_amdgcn_sched_barrier(0);
         use(ba, e0);
+        __builtin_amdgcn_sched_barrier(0);
         load(ba, min(e0 + 2, g.en0 - 1));
+        __builtin_amdgcn_sched_barrier(0);
         use(bb, e0 + 1);
+        __builtin_amdgcn_sched_barrier(0);
     }
     // D[ctx][line]: lane holds contexts 16 kb + 4 lg + v of line n = li
 #pragma unroll
@@ -154,7 +160,7 @@ __device__ void split_tile(const StreamArgs &a, const Geo &g, const float *__res
     }
 }
 
-__global__ __launch_bounds__(kThreads) void split_lik_kernel(StreamArgs a, const float *__restrict__ q,
+__global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, const float *__restrict__ q,
                                                              float *__restrict__ part)
 {
     extern __shared__ float sh[];

@@ -33,7 +33,8 @@ PEAK_HBM_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cfg5.json")
 CSRC = os.path.join(ROOT, "paper_2607_17855_amd", "csrc")
 # likelihood kernels: profile class -> (kernel symbol, source file)
-LIK = {"lik": ("lik_kernel", "stream.hip"), "lik_sparse": ("sparse_lik_kernel", "sparse.hip")}
+LIK = {"lik": ("lik_kernel", "stream.hip"), "lik_split": ("split_lik_kernel", "split.hip"),
+       "lik_sparse": ("sparse_lik_kernel", "sparse.hip")}
 LAYOUTS = ("dense", "sparse")
 ALGOS = ("vmp", "mmp")
 
@@ -55,9 +56,10 @@ def slice_sizes(model):
 
 def dense_lik_work(model, obs):
     """Algorithmic flops and HBM bytes of one dense likelihood launch: per
-    context and modality the two passes Z = X t and V = s X over the slice,
-    one FMA (2 flops) per slice entry each (16.8 MFLOP per belief update);
-    every slice observed by at least one context is read once in fp32."""
+    context and modality the two contractions of the slice (towards its rows
+    and towards its columns), one FMA (2 flops) per slice entry each
+    (16.8 MFLOP per belief update); every slice observed by at least one
+    context is read once in fp32."""
     import numpy as np
     nctx = obs.shape[0] * obs.shape[1]
     flops = sum(2 * 2 * P for P in slice_sizes(model)) * nctx
@@ -181,7 +183,8 @@ def main():
     value = bu_per_step / (ms_step / 1e3)
 
     traffic = load_traffic()
-    work = {"lik": dense_lik_work(w.model, w.obs), "lik_sparse": sparse_lik_work(w.model, w.obs)}
+    dense_work = dense_lik_work(w.model, w.obs)
+    work = {"lik": dense_work, "lik_split": dense_work, "lik_sparse": sparse_lik_work(w.model, w.obs)}
     rooflines = {}
     for cls, (kname, src) in LIK.items():
         if cls not in prof:
@@ -191,7 +194,7 @@ def main():
         flops, alg_bytes = work[cls]
         tr = traffic.get(kname)
         hbm = tr["hbm_bytes_per_launch"] if tr and tr.get("kernel_source_sha") == source_sha(src) else None
-        if cls == "lik":
+        if cls in ("lik", "lik_split"):
             bound, peak = "mfma", PEAK_FP32_MFMA_TFLOPS
         else:
             bound, peak = "alu", PEAK_FP64_VALU_TFLOPS

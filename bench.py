@@ -15,6 +15,12 @@ outside the timed region (the one-time layout step).
 Prints one JSON line.  value = belief updates per second over the whole job,
 one belief update being one (agent, time step, iteration) of one algorithm
 on one layout.
+
+--workload picks another workload for measurement (agent-resident fp64
+kernels, one model per agent): vmp_2f (F=2 factors of 8 and 6 states, M=3
+modalities on both, T=10, b=1024, VMP), mmp_3f (F=3 of 12/10/8 states, M=4 x
+16 outcomes on random factor subsets, T=20, b=4096, MMP), fpi_hmm (one
+4-state factor, T=8, b=1, FPI).
 """
 import argparse
 import hashlib
@@ -85,6 +91,21 @@ def sparse_lik_work(model, obs):
     return flops, nbytes
 
 
+def agent_work(model, T, algo):
+    """Algorithmic flops and bytes of one belief update on the agent-resident
+    path: the two contractions of every observed slice (one FMA per entry
+    each), the transition messages (two n x n products per factor; FPI: one,
+    once per time step, counted per update), and one read of the observed
+    fp64 slices."""
+    lik = sum(4 * P for P in slice_sizes(model))
+    trans = sum((2 if algo == "fpi" else 4) * n * n for n in model.n)
+    nbytes = sum(8.0 * P for P in slice_sizes(model))
+    return float(lik + trans), nbytes
+
+
+AGENT_WORKLOADS = {"vmp_2f": ("config2", "vmp"), "mmp_3f": ("config3", "mmp"), "fpi_hmm": ("config1", "fpi")}
+
+
 def cpu_baseline(w, algos, budget_s: float = 25.0):
     import numpy as np
     import oracle
@@ -121,6 +142,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layouts", default=",".join(LAYOUTS), help="comma list of A layouts in a step")
+    ap.add_argument("--workload", default="large", choices=["large"] + list(AGENT_WORKLOADS))
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a device-to-device copy of MIB MiB (reference kernel for HBM byte counters)")
     args = ap.parse_args()
@@ -137,6 +159,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.workload != "large":
+        return bench_agent(args, bi, synth, torch, dev)
     w = synth.config5()
     flags = {"dense": bi.BI_DENSE_A | bi.BI_FAST_F32, "sparse": bi.BI_SPARSE_A}
     pms = {lay: bi.PackedModel(w.model, flags=flags[lay], device=dev) for lay in layouts}
@@ -235,6 +259,60 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, list(ALGOS))
+    print(json.dumps(out), flush=True)
+
+
+def bench_agent(args, bi, synth, torch, dev):
+    """One step = one call of the workload's algorithm over its whole batch."""
+    cfg, algo = AGENT_WORKLOADS[args.workload]
+    w = getattr(synth, cfg)()
+    pm = bi.PackedModel(w.model, flags=bi.BI_DENSE_A, device=dev)
+    obs = torch.from_numpy(w.obs).to(dev)
+    act = torch.from_numpy(w.act).to(dev)
+    q = torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    assert pm.workspace(w.b, w.T, algo) is None, "per-agent workloads run on the agent-resident kernels"
+
+    def step():
+        pm.infer(algo, obs, act, w.iters, q=q, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    bi.bi_profile_begin()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    prof = bi.bi_profile_end()
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    bu = w.b * w.T * w.iters
+    cls = "agent_filter" if algo == "fpi" else "agent_window"
+    launches, total_ms = prof[cls]
+    avg_ms = total_ms / max(launches, 1)
+    fl, nb = agent_work(w.model, w.T, algo)
+    flops = fl * bu
+    achieved = flops / (avg_ms / 1e3) / 1e12
+    out = {
+        "metric": METRIC, "value": bu / (ms_step / 1e3), "unit": "belief_updates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"{w.name}: per-agent models, {algo.upper()} x{w.iters}", "b": w.b, "T": w.T,
+                   "iters": w.iters, "algos": [algo]},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP64_VALU_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_FP64_VALU_TFLOPS, "traffic": None, "kernel": cls + "_kernel",
+                     "avg_launch_ms": avg_ms, "launches": launches, "algorithmic_flops_per_launch": flops,
+                     "algorithmic_bytes_per_launch": nb * w.b * w.T},
+        "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, [algo])
     print(json.dumps(out), flush=True)
 
 

@@ -21,6 +21,8 @@
 // fp32 FMA, so this path pays only in LDS footprint.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "internal.h"
 #include "profile.h"
 
@@ -29,12 +31,22 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kStageMaxM = 16;
+
+// Observed slices staged in LDS: a context's block holds modality m's slice at
+// po[m] with rows padded to Cp + 1 values (conflict-free row and column
+// reads); pr[m] is the slice's offset in the unpadded concatenation.
+enum StageMode { kStageNone = 0, kStageChunk = 1, kStageWindow = 2 };
+
 struct AgentArgs {
     const char *base;      // packed buffer
     const ModDesc *mods;   // device descriptor tables (inside the packed buffer)
     const FacDesc *facs;
     int F, M, shared;      // shared: one model for every agent
     int T, iters, ntot, zvpc, nc;  // nc: contexts per Z/V chunk
+    int stage;             // StageMode
+    int sctx, sraw;        // staged values per context (padded), unpadded values per context
+    int po[kStageMaxM + 1], pr[kStageMaxM + 1];
     const int32_t *obs;
     const int32_t *act;
     float *q;
@@ -60,9 +72,91 @@ __device__ inline double wave_sum(double v)
     return v;
 }
 
+// One Z or V output of an observed slice X (row stride xs) for the marginals
+// qt: j < R gives Z[j], j = R + col gives V[col].
+__device__ inline double zv_one(const AgentArgs &a, const ModDesc &md, const double *X, int64_t xs,
+                                const double *qt, int j)
+{
+    const int R = md.R;
+    double acc = 0.0;
+    if (j < R) {  // Z[r] = sum_c X[r][c] t[c]
+        if (md.nrow > 0) {  // (Z of a rank-0 row side feeds no message)
+            const double *row = X + (int64_t)j * xs;
+            const double *q0 = qt + a.facs[md.cf[0]].q_off;
+            if (md.ncol == 1) {
+                for (int cc = 0; cc < md.C; ++cc) acc = fma(row[cc], q0[cc], acc);
+            } else {
+                const double *q1 = qt + a.facs[md.cf[1]].q_off;
+                const int n0 = md.cn[0], n1 = md.cn[1];
+                for (int c0 = 0; c0 < n0; ++c0) {
+                    double in = 0.0;
+                    const double *rr = row + c0 * n1;
+                    for (int c1 = 0; c1 < n1; ++c1) in = fma(rr[c1], q1[c1], in);
+                    acc = fma(q0[c0], in, acc);
+                }
+            }
+        }
+    } else {  // V[c] = sum_r s[r] X[r][c]
+        const int col = j - R;
+        if (md.nrow == 0) {
+            acc = X[col];
+        } else if (md.nrow == 1) {
+            const double *q0 = qt + a.facs[md.rf[0]].q_off;
+            for (int r = 0; r < R; ++r) acc = fma(q0[r], X[(int64_t)r * xs + col], acc);
+        } else {
+            const double *q0 = qt + a.facs[md.rf[0]].q_off;
+            const double *q1 = qt + a.facs[md.rf[1]].q_off;
+            const int n0 = md.rn[0], n1 = md.rn[1];
+            for (int r0 = 0; r0 < n0; ++r0) {
+                double in = 0.0;
+                const double *xc = X + (int64_t)r0 * n1 * xs + col;
+                for (int r1 = 0; r1 < n1; ++r1) in = fma(q1[r1], xc[(int64_t)r1 * xs], in);
+                acc = fma(q0[r0], in, acc);
+            }
+        }
+    }
+    return acc;
+}
+
+// Copy the observed slices of contexts [t0, t0 + nc) into stg (one block of
+// sctx values per context): every thread issues its loads before any store,
+// so the workgroup pays one memory round trip for the whole chunk.
+__device__ void stage_slices(const AgentArgs &a, int agent, int t0, int nc, double *stg)
+{
+    const int total = nc * a.sraw;
+    for (int i0 = 0; i0 < total; i0 += 8 * kThreads) {
+        double v[8];
+        int dst[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * kThreads + (int)threadIdx.x;
+            dst[u] = -1;
+            v[u] = 0.0;
+            if (i < total) {
+                const int c = i / a.sraw, rem = i - c * a.sraw;
+                int m = 0;
+                while (m + 1 < a.M && a.pr[m + 1] <= rem) ++m;
+                const ModDesc &md = a.mods[m];
+                const int e = rem - a.pr[m], r = e / md.Cp, col = e - r * md.Cp;
+                const int o = a.obs[((int64_t)agent * a.T + t0 + c) * a.M + m];
+                const double *X = at<double>(a.base, md.la_off) + (a.shared ? 0 : (int64_t)agent * md.la_agent) +
+                                  (int64_t)o * md.slice;
+                v[u] = X[e];
+                dst[u] = c * a.sctx + a.po[m] + r * (md.Cp + 1) + col;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (dst[u] >= 0) stg[dst[u]] = v[u];
+    }
+}
+
 // Phase 1: Z/V of contexts [t0, t0 + nc) into zv[c][zvpc].
-// q: marginals of context t at q + t * ntot.
-__device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv)
+// q: marginals of context t at q + t * ntot.  With staged slices, X of
+// context t0 + c comes from stg + (sc0 + c) * sctx (LDS); otherwise from the
+// packed buffer.
+__device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv,
+                         const double *stg, int sc0)
 {
     const int tid = threadIdx.x;
     int base = 0;
@@ -77,45 +171,13 @@ __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const do
         for (; i < cnt; i += kThreads) {
             const int c = i / per, j = i - c * per;
             const int t = t0 + c;
-            const int o = a.obs[((int64_t)agent * a.T + t) * a.M + m];
-            const double *X = la + (int64_t)o * md.slice;
             const double *qt = q + t * a.ntot;
-            double acc = 0.0;
-            if (j < R) {  // Z[r] = sum_c X[r][c] t[c]
-                if (md.nrow > 0) {  // (Z of a rank-0 row side feeds no message)
-                    const double *row = X + (int64_t)j * Cp;
-                    const double *q0 = qt + a.facs[md.cf[0]].q_off;
-                    if (md.ncol == 1) {
-                        for (int cc = 0; cc < C; ++cc) acc = fma(row[cc], q0[cc], acc);
-                    } else {
-                        const double *q1 = qt + a.facs[md.cf[1]].q_off;
-                        const int n0 = md.cn[0], n1 = md.cn[1];
-                        for (int c0 = 0; c0 < n0; ++c0) {
-                            double in = 0.0;
-                            const double *rr = row + c0 * n1;
-                            for (int c1 = 0; c1 < n1; ++c1) in = fma(rr[c1], q1[c1], in);
-                            acc = fma(q0[c0], in, acc);
-                        }
-                    }
-                }
-            } else {  // V[c] = sum_r s[r] X[r][c]
-                const int col = j - R;
-                if (md.nrow == 0) {
-                    acc = X[col];
-                } else if (md.nrow == 1) {
-                    const double *q0 = qt + a.facs[md.rf[0]].q_off;
-                    for (int r = 0; r < R; ++r) acc = fma(q0[r], X[(int64_t)r * Cp + col], acc);
-                } else {
-                    const double *q0 = qt + a.facs[md.rf[0]].q_off;
-                    const double *q1 = qt + a.facs[md.rf[1]].q_off;
-                    const int n0 = md.rn[0], n1 = md.rn[1];
-                    for (int r0 = 0; r0 < n0; ++r0) {
-                        double in = 0.0;
-                        const double *xc = X + (int64_t)r0 * n1 * Cp + col;
-                        for (int r1 = 0; r1 < n1; ++r1) in = fma(q1[r1], xc[(int64_t)r1 * Cp], in);
-                        acc = fma(q0[r0], in, acc);
-                    }
-                }
+            double acc;
+            if (stg) {
+                acc = zv_one(a, md, stg + (int64_t)(sc0 + c) * a.sctx + a.po[m], Cp + 1, qt, j);
+            } else {
+                const int o = a.obs[((int64_t)agent * a.T + t) * a.M + m];
+                acc = zv_one(a, md, la + (int64_t)o * md.slice, Cp, qt, j);
             }
             zv[c * a.zvpc + md.zv_off + j] = acc;
         }
@@ -191,12 +253,19 @@ __device__ void wave_softmax(double *v, int n, int lane)
     for (int s = lane; s < n; s += 64) v[s] = v[s] / sum;
 }
 
-// lam for every context of the window (phases 1 and 2 over context chunks).
-__device__ void window_lam(const AgentArgs &a, int agent, const double *q, double *zv, const int *sfac, double *lam)
+// lam for every context of the window (phases 1 and 2 over context chunks;
+// staged chunks are copied to LDS first unless the whole window is resident).
+__device__ void window_lam(const AgentArgs &a, int agent, const double *q, double *zv, double *stg, const int *sfac,
+                           double *lam)
 {
     for (int t0 = 0; t0 < a.T; t0 += a.nc) {
         const int nc = min(a.nc, a.T - t0);
-        phase_zv(a, agent, t0, nc, q, zv);
+        if (a.stage == kStageChunk) {
+            stage_slices(a, agent, t0, nc, stg);
+            __syncthreads();
+        }
+        phase_zv(a, agent, t0, nc, q, zv, a.stage == kStageNone ? nullptr : stg,
+                 a.stage == kStageWindow ? t0 : 0);
         __syncthreads();
         phase_lam(a, t0, nc, q, zv, sfac, lam);
         __syncthreads();
@@ -218,9 +287,11 @@ __global__ __launch_bounds__(kThreads) void agent_window_kernel(AgentArgs a)
     extern __shared__ double smem[];
     const int agent = blockIdx.x;
     const int TN = a.T * a.ntot;
-    double *qa = smem, *qb = qa + TN, *lam = qb + TN, *zv = lam + TN;
-    int *sfac = reinterpret_cast<int *>(zv + a.nc * a.zvpc);
+    double *qa = smem, *qb = qa + TN, *lam = qb + TN, *zv = lam + TN, *stg = zv + a.nc * a.zvpc;
+    const int nstg = a.stage == kStageWindow ? a.T : a.stage == kStageChunk ? a.nc : 0;
+    int *sfac = reinterpret_cast<int *>(stg + (int64_t)nstg * a.sctx);
     init_tables(a, sfac);
+    if (a.stage == kStageWindow) stage_slices(a, agent, 0, a.T, stg);   // every iteration reads them from LDS
     __syncthreads();
     for (int i = threadIdx.x; i < TN; i += kThreads) qa[i] = 1.0 / a.facs[sfac[i % a.ntot]].n;
     __syncthreads();
@@ -228,7 +299,7 @@ __global__ __launch_bounds__(kThreads) void agent_window_kernel(AgentArgs a)
     const int64_t am = a.shared ? 0 : agent;
     double *cur = qa, *nxt = qb;
     for (int k = 0; k < a.iters; ++k) {
-        window_lam(a, agent, cur, zv, sfac, lam);
+        window_lam(a, agent, cur, zv, stg, sfac, lam);
         for (int p = wave; p < a.T * a.F; p += kWaves) {
             const int t = p / a.F, f = p - t * a.F;
             const FacDesc &fd = a.facs[f];
@@ -295,8 +366,11 @@ __global__ __launch_bounds__(kThreads) void agent_filter_kernel(AgentArgs a)
     // placed at row t of a [T][ntot] view so phase_zv / phase_lam index it
     // like the window kernel
     double *qfin = smem, *cur = qfin + TN, *lam = cur + TN, *zv = lam + TN, *logp = zv + a.zvpc;
-    int *sfac = reinterpret_cast<int *>(logp + a.ntot);
+    double *stg = logp + a.ntot;
+    const int nstg = a.stage == kStageWindow ? a.T : a.stage == kStageChunk ? 1 : 0;
+    int *sfac = reinterpret_cast<int *>(stg + (int64_t)nstg * a.sctx);
     init_tables(a, sfac);
+    if (a.stage == kStageWindow) stage_slices(a, agent, 0, a.T, stg);
     __syncthreads();
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
     const int64_t am = a.shared ? 0 : agent;
@@ -322,9 +396,11 @@ __global__ __launch_bounds__(kThreads) void agent_filter_kernel(AgentArgs a)
         }
         double *qt = cur + t * a.ntot;
         for (int j = threadIdx.x; j < a.ntot; j += kThreads) qt[j] = 1.0 / a.facs[sfac[j]].n;
+        if (a.stage == kStageChunk) stage_slices(a, agent, t, 1, stg);   // step t's slices, for all its iterations
         __syncthreads();
         for (int k = 0; k < a.iters; ++k) {
-            phase_zv(a, agent, t, 1, cur, zv);
+            phase_zv(a, agent, t, 1, cur, zv, a.stage == kStageNone ? nullptr : stg,
+                     a.stage == kStageWindow ? t : 0);
             __syncthreads();
             phase_lam(a, t, 1, cur, zv, sfac, lam);
             __syncthreads();
@@ -368,20 +444,54 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     a.act = act;
     a.q = q;
     const size_t TN = (size_t)T * m->ntot;
-    size_t fixed, per_ctx = (size_t)m->zvpc * 8;
+    // staged slice layout (see AgentArgs)
+    int64_t sctx = 0, sraw = 0;
+    bool can_stage = m->M <= kStageMaxM;
+    for (int i = 0; i < m->M && can_stage; ++i) {
+        const ModDesc &md = m->mods[i];
+        a.po[i] = (int)sctx;
+        a.pr[i] = (int)sraw;
+        sctx += (int64_t)md.R * (md.Cp + 1);
+        sraw += (int64_t)md.R * md.Cp;
+        if (sctx > (int64_t)kLdsMax / 8) can_stage = false;
+    }
+    if (can_stage) {
+        a.po[m->M] = (int)sctx;
+        a.pr[m->M] = (int)sraw;
+    }
+    a.sctx = (int)sctx;
+    a.sraw = (int)sraw;
+    const size_t sb = 8 * (size_t)sctx;   // staged bytes per context
+    const size_t budget2 = 80 * 1024;    // two workgroups per CU
+    size_t fixed, per_ctx = (size_t)m->zvpc * 8, lds;
+    a.stage = kStageNone;
     if (algo == BI_ALGO_FPI) {
-        fixed = (3 * TN + m->ntot) * 8 + (size_t)m->ntot * 4;
+        fixed = (3 * TN + m->ntot) * 8 + (size_t)m->ntot * 4 + per_ctx;
         a.nc = 1;
+        if (can_stage && fixed + T * sb <= budget2)
+            a.stage = kStageWindow;
+        else if (can_stage && fixed + sb <= kLdsMax)
+            a.stage = kStageChunk;
+        lds = fixed + (a.stage == kStageWindow ? T * sb : a.stage == kStageChunk ? sb : 0);
     } else {
         fixed = 3 * TN * 8 + (size_t)m->ntot * 4;
-        // whole window in one chunk when it fits in 80 KB (two workgroups per
-        // CU), otherwise as many contexts as 160 KB allow
-        size_t nc = T;
-        if (fixed + nc * per_ctx > 80 * 1024) nc = fixed < kLdsMax ? (kLdsMax - fixed) / per_ctx : 0;
-        if (nc > (size_t)T) nc = T;
-        a.nc = (int)nc;
+        if (can_stage && fixed + T * (per_ctx + sb) <= budget2) {
+            // the whole window's slices stay in LDS for every iteration
+            a.stage = kStageWindow;
+            a.nc = T;
+            lds = fixed + T * (per_ctx + sb);
+        } else {
+            // slices read from the packed buffer: whole window in one chunk
+            // when it fits in 80 KB, otherwise as many contexts as 160 KB allow.
+            // (Copying each chunk's slices to LDS first measured slower here:
+            // the extra barriers per chunk cost more than the saved reads.)
+            size_t nc = T;
+            if (fixed + nc * per_ctx > budget2) nc = fixed < kLdsMax ? (kLdsMax - fixed) / per_ctx : 0;
+            if (nc > (size_t)T) nc = T;
+            a.nc = (int)nc;
+            lds = fixed + (size_t)a.nc * per_ctx;
+        }
     }
-    const size_t lds = fixed + (size_t)a.nc * per_ctx;
     if (a.nc < 1 || lds > kLdsMax)
         return fail(BI_ERR_UNSUPPORTED, "agent working set (%zu bytes of LDS) exceeds the 160 KB budget", lds);
     hipError_t e;

@@ -43,6 +43,10 @@
  *        bwd = LN(B_f[:,:,u_t]^T q_{t+1,f}) (t < T-1),
  *        q_{t,f} = softmax(lam + mean of the temporal messages present at t):
  *        (fwd + bwd)/2 for t < T-1, fwd alone at t = T-1.
+ *   Rolling inference (the window of Sec. III-B is the current step and the
+ *   h steps before it): a caller may replace D_f by its own prior over the
+ *   window's first step (every LN(D_f) above becomes LN(prior_f)), typically
+ *   the predictive prior B_f[:,:,u] q_f of an earlier marginal (orc_predict).
  */
 #include <math.h>
 #include <omp.h>
@@ -131,16 +135,23 @@ static double Bv(const orc_model *md, const double *Bf, int f, int i, int j, int
     return Bf[((size_t)i * md->n[f] + j) * md->U[f] + u];
 }
 
+/* p(s_1) of agent a: the caller's prior (prior: [b][ntot]) or D_f */
+static const double *first_prior(const orc_model *md, const double *prior, int f, int a, const int *qoff, int ntot)
+{
+    if (prior) return prior + (size_t)a * ntot + qoff[f];
+    return md->D[f] + (size_t)(md->mb == 1 ? 0 : a) * md->n[f];
+}
+
 static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int *act, int iters, double *q,
-                    const int *qoff, int ntot, double *work)
+                    const int *qoff, int ntot, double *work, const double *prior)
 {
     double *cur = work, *lam = work + ntot, *logp = work + 2 * ntot;
     for (int t = 0; t < T; ++t) {
         for (int f = 0; f < md->F; ++f) {
             const int nf = md->n[f];
             if (t == 0) {
-                const double *Df = md->D[f] + (size_t)(md->mb == 1 ? 0 : a) * nf;
-                for (int s = 0; s < nf; ++s) logp[qoff[f] + s] = LN(Df[s]);
+                const double *p0 = first_prior(md, prior, f, a, qoff, ntot);
+                for (int s = 0; s < nf; ++s) logp[qoff[f] + s] = LN(p0[s]);
             } else {
                 const double *Bf = B_at(md, f, a);
                 const int u = act[(size_t)(t - 1) * md->F + f];
@@ -166,7 +177,7 @@ static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int
 }
 
 static void run_window(const orc_model *md, int algo, int a, int T, const int *obs, const int *act, int iters,
-                       double *q, const int *qoff, int ntot, double *work)
+                       double *q, const int *qoff, int ntot, double *work, const double *prior)
 {
     double *qn = work;                               /* [T][ntot] next iterate */
     double *lam = work + (size_t)T * ntot;            /* [T][ntot] */
@@ -181,7 +192,7 @@ static void run_window(const orc_model *md, int algo, int a, int T, const int *o
             for (int f = 0; f < md->F; ++f) {
                 const int nf = md->n[f];
                 const double *Bf = B_at(md, f, a);
-                const double *Df = md->D[f] + (size_t)(md->mb == 1 ? 0 : a) * nf;
+                const double *p0 = first_prior(md, prior, f, a, qoff, ntot);
                 const double *qprev = t > 0 ? q + (size_t)(t - 1) * ntot + qoff[f] : NULL;
                 const double *qnext = t + 1 < T ? q + (size_t)(t + 1) * ntot + qoff[f] : NULL;
                 const int uprev = t > 0 ? act[(size_t)(t - 1) * md->F + f] : 0;
@@ -191,7 +202,7 @@ static void run_window(const orc_model *md, int algo, int a, int T, const int *o
                     double fwd, bwd = 0.0;
                     if (algo == ORC_VMP) {
                         if (t == 0) {
-                            fwd = LN(Df[s]);
+                            fwd = LN(p0[s]);
                         } else {
                             fwd = 0.0;
                             for (int sp = 0; sp < nf; ++sp) fwd += LN(Bv(md, Bf, f, s, sp, uprev)) * qprev[sp];
@@ -201,7 +212,7 @@ static void run_window(const orc_model *md, int algo, int a, int T, const int *o
                         v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd + bwd;
                     } else { /* MMP */
                         if (t == 0) {
-                            fwd = LN(Df[s]);
+                            fwd = LN(p0[s]);
                         } else {
                             double p = 0.0;
                             for (int sp = 0; sp < nf; ++sp) p += Bv(md, Bf, f, s, sp, uprev) * qprev[sp];
@@ -225,12 +236,15 @@ static void run_window(const orc_model *md, int algo, int a, int T, const int *o
 }
 
 /*
- * Run `algo` (0 FPI, 1 VMP, 2 MMP) for b agents.  Returns 0, or -1 on an
- * invalid argument.  nthreads <= 0 uses the OpenMP default.
+ * Run `algo` (0 FPI, 1 VMP, 2 MMP) for b agents.  prior: NULL (p(s_1) = D)
+ * or [b][sum n_f], each factor's block a distribution over its states.
+ * Returns 0, or -1 on an invalid argument.  nthreads <= 0 uses the OpenMP
+ * default.
  */
-int orc_infer(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
-              const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
-              int b, int T, const int *obs, const int *act, int iters, double *q, int nthreads)
+int orc_infer_prior(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
+                    const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
+                    int b, int T, const int *obs, const int *act, const double *prior, int iters, double *q,
+                    int nthreads)
 {
     if (algo < 0 || algo > 2 || F < 1 || M < 1 || b < 1 || T < 1 || iters < 1) return -1;
     if (mb != 1 && mb != b) return -1;
@@ -262,13 +276,52 @@ int orc_infer(int algo, int F, const int *n, const int *U, int M, const int *K, 
         const int *ua = T > 1 ? act + (size_t)a * (T - 1) * F : NULL;
         double *qa = q + (size_t)a * T * ntot;
         if (algo == ORC_FPI)
-            run_fpi(&md, a, T, oa, ua, iters, qa, qoff, ntot, work);
+            run_fpi(&md, a, T, oa, ua, iters, qa, qoff, ntot, work, prior);
         else
-            run_window(&md, algo, a, T, oa, ua, iters, qa, qoff, ntot, work);
+            run_window(&md, algo, a, T, oa, ua, iters, qa, qoff, ntot, work, prior);
         free(work);
     }
     free(qoff);
     return bad ? -1 : 0;
+}
+
+int orc_infer(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
+              const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
+              int b, int T, const int *obs, const int *act, int iters, double *q, int nthreads)
+{
+    return orc_infer_prior(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, b, T, obs, act, NULL, iters, q,
+                           nthreads);
+}
+
+/*
+ * Predictive prior of the next step (the same product as FPI's prior):
+ *   out[a][f](i) = sum_j B_f[i][j][u_{a,f}] q[a][f](j)
+ * q: [b][sum n_f] marginals, act: [b][F], out: [b][sum n_f].  Returns 0 or -1.
+ */
+int orc_predict(int F, const int *n, const int *U, int mb, const double *const *B, int b, const double *q,
+                const int *act, double *out)
+{
+    if (F < 1 || b < 1 || (mb != 1 && mb != b) || !n || !U || !B || !q || !act || !out) return -1;
+    int ntot = 0;
+    for (int f = 0; f < F; ++f) {
+        if (n[f] < 1 || U[f] < 1) return -1;
+        ntot += n[f];
+    }
+    for (int a = 0; a < b; ++a) {
+        int off = 0;
+        for (int f = 0; f < F; ++f) {
+            const int nf = n[f], u = act[(size_t)a * F + f];
+            if (u < 0 || u >= U[f]) return -1;
+            const double *Bf = B[f] + (size_t)(mb == 1 ? 0 : a) * nf * nf * U[f];
+            for (int i = 0; i < nf; ++i) {
+                double p = 0.0;
+                for (int j = 0; j < nf; ++j) p += Bf[((size_t)i * nf + j) * U[f] + u] * q[(size_t)a * ntot + off + j];
+                out[(size_t)a * ntot + off + i] = p;
+            }
+            off += nf;
+        }
+    }
+    return 0;
 }
 
 /* Number of OpenMP threads orc_infer uses when nthreads <= 0. */

@@ -1,7 +1,9 @@
 """ctypes front end of ``bi_oracle.c`` (test infrastructure only).
 
 ``infer(algo, model, obs, act, iters)`` converts the float32 model arrays of a
-:class:`paper_2607_17855_amd.synth.Model` to float64 and runs the C oracle.
+:class:`paper_2607_17855_amd.synth.Model` to float64 and runs the C oracle;
+``prior=`` replaces p(s_1) = D by the caller's prior (rolling inference), and
+``predict(model, q, act)`` gives the predictive prior B q of the next step.
 """
 from __future__ import annotations
 
@@ -42,6 +44,15 @@ def load_library(path: str):
                               P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p), ctypes.c_int,
                               ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
                               P(ctypes.c_double), ctypes.c_int]
+    lib.orc_infer_prior.restype = ctypes.c_int
+    lib.orc_infer_prior.argtypes = [ctypes.c_int, ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                    P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                    P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p), ctypes.c_int,
+                                    ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_double),
+                                    ctypes.c_int, P(ctypes.c_double), ctypes.c_int]
+    lib.orc_predict.restype = ctypes.c_int
+    lib.orc_predict.argtypes = [ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int, P(ctypes.c_void_p),
+                                ctypes.c_int, P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double)]
     lib.orc_default_threads.restype = ctypes.c_int
     return lib
 
@@ -64,9 +75,11 @@ def _i32(x) -> np.ndarray:
 
 
 def infer(algo: str, model, obs: np.ndarray, act: np.ndarray, iters: int,
-          agents: Optional[Sequence[int]] = None, threads: int = 0, lib=None) -> np.ndarray:
+          agents: Optional[Sequence[int]] = None, threads: int = 0, lib=None,
+          prior: Optional[np.ndarray] = None) -> np.ndarray:
     """Posterior marginals q [b][T][sum n] (float64) of ``algo`` for every agent,
-    or for the listed ``agents`` only (agents are independent)."""
+    or for the listed ``agents`` only (agents are independent).  ``prior``:
+    [b][sum n] distributions over the first step, replacing D."""
     if lib is None:
         lib = _load()
     if agents is not None:
@@ -74,6 +87,8 @@ def infer(algo: str, model, obs: np.ndarray, act: np.ndarray, iters: int,
         model = model.agent_slice(agents)
         obs = obs[agents]
         act = act[agents]
+        if prior is not None:
+            prior = np.asarray(prior)[agents]
     b, T, M = obs.shape
     F = len(model.n)
     n, U, K = _i32(model.n), _i32(model.U), _i32(model.K)
@@ -87,9 +102,37 @@ def infer(algo: str, model, obs: np.ndarray, act: np.ndarray, iters: int,
     act_c = _i32(act) if T > 1 else _i32(np.zeros((b, 1, F)))
     q = np.zeros((b, T, int(sum(model.n))), dtype=np.float64)
     ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))  # noqa: E731
-    rc = lib.orc_infer(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
-                       ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c), int(iters),
-                       q.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(threads))
+    dp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))  # noqa: E731
+    if prior is None:
+        rc = lib.orc_infer(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
+                           ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c), int(iters), dp(q), int(threads))
+    else:
+        pr = np.ascontiguousarray(prior, dtype=np.float64).reshape(b, int(sum(model.n)))
+        rc = lib.orc_infer_prior(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
+                                 ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c), dp(pr), int(iters), dp(q),
+                                 int(threads))
     if rc != 0:
         raise ValueError(f"oracle rejected the arguments (rc={rc})")
     return q
+
+
+def predict(model, q: np.ndarray, act: np.ndarray, lib=None) -> np.ndarray:
+    """Predictive prior [b][sum n] (float64) of the next step: for every agent
+    and factor f, B_f[:, :, u_f] q_f, with q [b][sum n] and act [b][F]."""
+    if lib is None:
+        lib = _load()
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    b = q.shape[0]
+    F = len(model.n)
+    n, U = _i32(model.n), _i32(model.U)
+    B = [np.ascontiguousarray(x, dtype=np.float64) for x in model.B]
+    ptrs = lambda arrs: (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])  # noqa: E731
+    ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))  # noqa: E731
+    act_c = _i32(np.asarray(act).reshape(b, F))
+    out = np.zeros((b, int(sum(model.n))), dtype=np.float64)
+    rc = lib.orc_predict(F, ip(n), ip(U), int(model.mb), ptrs(B), b,
+                         q.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), ip(act_c),
+                         out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    if rc != 0:
+        raise ValueError(f"oracle rejected the arguments (rc={rc})")
+    return out

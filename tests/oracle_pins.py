@@ -3,6 +3,8 @@
 Each ``pin_*`` takes an ``infer(algo, model, obs, act, iters)`` callable (the
 oracle, or a deliberately broken copy of it in the mutation tests) and returns
 the largest absolute deviation from the independently computed expectation.
+Pins of the rolling-inference entry points also use the predictive prior of
+the same oracle library (``_predict_of(infer)``).
 """
 from __future__ import annotations
 
@@ -266,6 +268,64 @@ def pin_invariants(infer):
     return worst
 
 
+def _predict_of(infer):
+    """The oracle's predict() on the library that ``infer`` runs."""
+    import oracle
+    lib = getattr(infer, "keywords", {}).get("lib")
+    return lambda model, q, act: oracle.predict(model, q, act, lib=lib)
+
+
+def pin_online_filter(infer):
+    """Rolling inference: FPI is causal, so filtering a window in one call must
+    equal filtering it one step per call, each step's prior being the
+    predictive prior B q of the previous step's posterior (Sec. III-B: the
+    window is the current step plus the steps before it).  The first call
+    passes D explicitly as the prior."""
+    predict = _predict_of(infer)
+    err = 0.0
+    for seed in range(4):
+        w = synth.random_small(300 + seed, F_max=3, n_max=5, M_max=3, K_max=4, T_max=5, b=3)
+        full = infer("fpi", w.model, w.obs, w.act, w.iters)
+        offs = np.cumsum([0] + list(w.model.n))
+        prior = np.concatenate([np.broadcast_to(np.float64(d[0] if w.model.mb == 1 else d), (w.b, len(d[0])))
+                                if w.model.mb == 1 else np.float64(d) for d in w.model.D], axis=1)
+        for t in range(w.T):
+            step = infer("fpi", w.model, w.obs[:, t:t + 1], w.act[:, :0], w.iters, prior=prior)
+            err = max(err, float(np.abs(step[:, 0] - full[:, t]).max()))
+            if t + 1 < w.T:
+                prior = predict(w.model, step[:, 0], w.act[:, t])
+        assert offs[-1] == full.shape[-1]
+    return err
+
+
+def pin_prior_t1(infer):
+    """A caller's prior p over a single step: the three schemes coincide (no
+    temporal messages besides the prior) and, with one factor, equal Bayes'
+    rule A[o] * p / Z for any p."""
+    err = 0.0
+    for seed in range(3):
+        w = synth.random_small(320 + seed, F_max=3, n_max=5, M_max=3, K_max=4, T_max=1, b=3)
+        rng = np.random.Generator(np.random.PCG64(seed))
+        prior = np.concatenate([rng.dirichlet(np.ones(n), size=w.b) for n in w.model.n], axis=1)
+        ref = infer("fpi", w.model, w.obs[:, :1], w.act[:, :0], w.iters, prior=prior)
+        for algo in ("vmp", "mmp"):
+            q = infer(algo, w.model, w.obs[:, :1], w.act[:, :0], w.iters, prior=prior)
+            err = max(err, float(np.abs(q - ref).max()))
+    for seed, K in [(11, (3,)), (12, (4, 2))]:
+        model, obs, act = _hmm(seed, n=5, K=K, T=1, b=3)
+        rng = np.random.Generator(np.random.PCG64(seed))
+        prior = rng.dirichlet(np.ones(5), size=3)
+        prior[0, 1] = 0.0   # a zero prior state stays at zero
+        prior[0] /= prior[0].sum()
+        q = infer("fpi", model, obs, act, 2, prior=prior)
+        for a in range(3):
+            post = prior[a].copy()
+            for m, A in enumerate(model.A):
+                post = post * np.float64(A[a][obs[a, 0, m]])
+            err = max(err, float(np.abs(q[a, 0] - post / post.sum()).max()))
+    return err
+
+
 ALL_PINS = {
     "bayes_filter": (pin_bayes_filter, 1e-12),
     "golden_hmm2": (pin_golden_hmm2, 1e-7),
@@ -276,4 +336,6 @@ ALL_PINS = {
     "iid_closed_forms": (pin_iid_closed_forms, 1e-12),
     "mmp_permutation_smoothing": (pin_mmp_permutation_smoothing, 1e-10),
     "invariants": (pin_invariants, 1e-12),
+    "online_filter": (pin_online_filter, 1e-12),
+    "prior_t1": (pin_prior_t1, 1e-12),
 }

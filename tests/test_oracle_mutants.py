@@ -29,7 +29,10 @@ MUTANTS = [
     ("lik_keeps_own_factor", "if (j != i) w *= q[qoff[d[j]] + idx[j]];", "w *= q[qoff[d[j]] + idx[j]];", 1),
     ("lik_axis_order", "for (int i = k - 1; i >= 0; --i) {\n                if (++idx[i]",
      "for (int i = 0; i < k; ++i) {\n                if (++idx[i]", 1),
-    ("vmp_drops_prior", "fwd = LN(Df[s]);", "fwd = 0.0;", 1),
+    ("vmp_drops_prior", "fwd = LN(p0[s]);", "fwd = 0.0;", 1),
+    ("caller_prior_ignored", "if (prior) return prior + (size_t)a * ntot + qoff[f];", "", 1),
+    ("predict_transposed", "p += Bf[((size_t)i * nf + j) * U[f] + u] * q[(size_t)a * ntot + off + j];",
+     "p += Bf[((size_t)j * nf + i) * U[f] + u] * q[(size_t)a * ntot + off + j];", 1),
     ("softmax_sign", "v[i] = exp(v[i] - mx);", "v[i] = exp(mx - v[i]);", 1),
     ("no_log_clamp", "return log(x > ORC_EPS ? x : ORC_EPS);", "return log(x > 0 ? x : 1e-300);", 1),
 ]

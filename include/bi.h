@@ -200,6 +200,48 @@ int bi_vmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, 
 int bi_mmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
            int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream);
 
+/*
+ * Rolling (online) inference.  The window of Sec. III-B is the current step
+ * and the h steps before it; when it slides, the belief about its first step
+ * comes from what was inferred before rather than from D.  These three calls
+ * are bi_vfilter / bi_vmp / bi_mmp with p(s_1) = D replaced by the caller's
+ * prior over the window's first step:
+ *   prior_dev: device fp32 [b][sum_f n_f], factor f's block at sum_{g<f} n_g,
+ *              each block a distribution over the factor's states (zeros
+ *              allowed: their logarithm is clamped to log(1e-16)); read only,
+ *              must stay valid until the stream work completes; NULL is
+ *              BI_ERR_INVALID_ARG.
+ * Every other argument, the workspace and the errors are those of the call
+ * without a prior.  Typical use: prior = bi_predict of an earlier marginal.
+ */
+int bi_vfilter_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+                     const float *prior_dev, int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes,
+                     void *hip_stream);
+int bi_vmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+                 const float *prior_dev, int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes,
+                 void *hip_stream);
+int bi_mmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+                 const float *prior_dev, int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes,
+                 void *hip_stream);
+
+/*
+ * Predictive prior of the next step (the product FPI uses between steps,
+ * Sec. III-B transition model): for every agent a and factor f
+ *   out[a][f](i) = sum_j B_f[i][j][u_{a,f}] q[a][f](j)      (fp64 sums)
+ *   q_dev:    device fp32 marginals of agent a at q_dev + a * q_stride
+ *             (q_stride >= sum_f n_f floats; e.g. one step of a bi_vfilter
+ *             output with q_stride = T * sum_f n_f);
+ *   act_dev:  device int32 actions of agent a at act_dev + a * act_stride
+ *             (act_stride >= F), u_{a,f} in [0, U_f);
+ *   out_dev:  device fp32 [b][sum_f n_f], written.
+ * b must equal the model's agent count when the model is per-agent.  Errors:
+ * BI_ERR_INVALID_ARG (NULL pointers, b < 1, strides too small),
+ * BI_ERR_SHAPE (b versus model_batch).  Asynchronous on hip_stream; allocates
+ * nothing.
+ */
+int bi_predict(const bi_model *model, int32_t b, const float *q_dev, int64_t q_stride, const int32_t *act_dev,
+               int64_t act_stride, float *out_dev, void *hip_stream);
+
 /* Free the host metadata of a packed model (not the caller's device buffer).
  * NULL is ignored. */
 void bi_free_model(bi_model *model);

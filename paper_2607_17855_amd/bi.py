@@ -29,7 +29,8 @@ BI_ALGO_FPI, BI_ALGO_VMP, BI_ALGO_MMP = 0, 1, 2
 ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
 
 EXPORTS = ("bi_last_error", "bi_plan_model", "bi_plan_model_exact", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
-           "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_free_model",
+           "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_vfilter_prior",
+           "bi_vmp_prior", "bi_mmp_prior", "bi_predict", "bi_free_model",
            "bi_profile_begin", "bi_profile_end")
 
 
@@ -79,6 +80,9 @@ def load(path: str = LIB_PATH):
     lib.bi_workspace_size.argtypes = [vp, i32, i32, i32, P(sz)]
     for name in ("bi_vfilter", "bi_vmp", "bi_mmp"):
         getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, sz, vp]
+    for name in ("bi_vfilter_prior", "bi_vmp_prior", "bi_mmp_prior"):
+        getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, sz, vp]
+    lib.bi_predict.argtypes = [vp, i32, vp, ctypes.c_int64, vp, ctypes.c_int64, vp, vp]
     lib.bi_free_model.argtypes = [vp]
     lib.bi_free_model.restype = None
     lib.bi_profile_begin.argtypes = []
@@ -195,13 +199,15 @@ def bi_workspace_size(handle: int, b: int, T: int, algo: int) -> int:
     return int(out.value)
 
 
-def _infer(fn_name, handle, b, T, obs, act, iters, q, ws, stream):
+def _infer(fn_name, handle, b, T, obs, act, iters, q, ws, stream, prior=None):
     ws_ptr = ws.data_ptr() if ws is not None else 0
     ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
     act_ptr = act.data_ptr() if act is not None and act.numel() > 0 else 0
-    _check(getattr(load(), fn_name)(ctypes.c_void_p(handle), int(b), int(T), ctypes.c_void_p(obs.data_ptr()),
-                                    ctypes.c_void_p(act_ptr), int(iters), ctypes.c_void_p(q.data_ptr()),
-                                    ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(_stream_ptr(stream))))
+    head = (ctypes.c_void_p(handle), int(b), int(T), ctypes.c_void_p(obs.data_ptr()), ctypes.c_void_p(act_ptr))
+    if fn_name.endswith("_prior"):
+        head += (ctypes.c_void_p(prior.data_ptr() if prior is not None else 0),)
+    _check(getattr(load(), fn_name)(*head, int(iters), ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(ws_ptr),
+                                    ws_bytes, ctypes.c_void_p(_stream_ptr(stream))))
 
 
 def bi_vfilter(handle, b, T, obs, act, iters, q, ws=None, stream=None):
@@ -214,6 +220,25 @@ def bi_vmp(handle, b, T, obs, act, iters, q, ws=None, stream=None):
 
 def bi_mmp(handle, b, T, obs, act, iters, q, ws=None, stream=None):
     _infer("bi_mmp", handle, b, T, obs, act, iters, q, ws, stream)
+
+
+def bi_vfilter_prior(handle, b, T, obs, act, prior, iters, q, ws=None, stream=None):
+    _infer("bi_vfilter_prior", handle, b, T, obs, act, iters, q, ws, stream, prior)
+
+
+def bi_vmp_prior(handle, b, T, obs, act, prior, iters, q, ws=None, stream=None):
+    _infer("bi_vmp_prior", handle, b, T, obs, act, iters, q, ws, stream, prior)
+
+
+def bi_mmp_prior(handle, b, T, obs, act, prior, iters, q, ws=None, stream=None):
+    _infer("bi_mmp_prior", handle, b, T, obs, act, iters, q, ws, stream, prior)
+
+
+def bi_predict(handle, b, q, q_stride, act, act_stride, out, stream=None):
+    """out[a] = B[:, :, act[a]] q[a] per factor; q / act rows at a * q_stride / a * act_stride elements."""
+    _check(load().bi_predict(ctypes.c_void_p(handle), int(b), ctypes.c_void_p(q.data_ptr()), int(q_stride),
+                             ctypes.c_void_p(act.data_ptr()), int(act_stride), ctypes.c_void_p(out.data_ptr()),
+                             ctypes.c_void_p(_stream_ptr(stream))))
 
 
 def bi_free_model(handle: int):
@@ -234,6 +259,7 @@ def bi_profile_end() -> dict:
 
 
 _ENTRY = {"fpi": bi_vfilter, "vmp": bi_vmp, "mmp": bi_mmp}
+_ENTRY_PRIOR = {"fpi": bi_vfilter_prior, "vmp": bi_vmp_prior, "mmp": bi_mmp_prior}
 
 
 class PackedModel:
@@ -256,16 +282,34 @@ class PackedModel:
         nb = bi_workspace_size(self.handle, b, T, ALGO_IDS[algo])
         return torch.empty(nb, dtype=torch.uint8, device=self.buf.device) if nb else None
 
-    def infer(self, algo: str, obs, act, iters: int, q=None, ws=None, stream=None):
-        """obs [b][T][M] / act [b][T-1][F] int32 device tensors -> q [b][T][sum n] float32."""
+    def infer(self, algo: str, obs, act, iters: int, q=None, ws=None, stream=None, prior=None):
+        """obs [b][T][M] / act [b][T-1][F] int32 device tensors -> q [b][T][sum n] float32.
+
+        prior: optional float32 device tensor [b][sum n], the first step's prior in place of D."""
         import torch
         b, T = int(obs.shape[0]), int(obs.shape[1])
         if q is None:
             q = torch.empty((b, T, sum(self.model.n)), dtype=torch.float32, device=self.buf.device)
         if ws is None:
             ws = self.workspace(b, T, algo)
-        _ENTRY[algo](self.handle, b, T, obs, act, iters, q, ws, stream)
+        if prior is None:
+            _ENTRY[algo](self.handle, b, T, obs, act, iters, q, ws, stream)
+        else:
+            _ENTRY_PRIOR[algo](self.handle, b, T, obs, act, prior, iters, q, ws, stream)
         return q
+
+    def predict(self, q, act, out=None, stream=None):
+        """Predictive prior of the next step: q [b][..][sum n] marginals of the step to carry (the
+        last dimension holds one step; other rows are skipped by the stride) and act [b][F] int32
+        -> out [b][sum n] float32."""
+        import torch
+        b, ntot = int(q.shape[0]), sum(self.model.n)
+        if q.stride(-1) != 1 or act.stride(-1) != 1:
+            raise ValueError("q and act must be contiguous in their last dimension")
+        if out is None:
+            out = torch.empty((b, ntot), dtype=torch.float32, device=self.buf.device)
+        bi_predict(self.handle, b, q, q.stride(0), act, act.stride(0), out, stream)
+        return out
 
     def close(self):
         if getattr(self, "handle", 0):

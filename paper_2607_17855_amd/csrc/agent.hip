@@ -49,6 +49,7 @@ struct AgentArgs {
     int po[kStageMaxM + 1], pr[kStageMaxM + 1];
     const int32_t *obs;
     const int32_t *act;
+    const float *prior;    // optional [agent][ntot] prior of the first step (replaces D)
     float *q;
 };
 
@@ -319,7 +320,7 @@ __global__ __launch_bounds__(kThreads) void agent_window_kernel(AgentArgs a)
             for (int s = lane; s < n; s += 64) {
                 double fwd, bwd = 0.0;
                 if (t == 0) {
-                    fwd = ld[s];
+                    fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + fd.q_off + s]) : ld[s];
                 } else if (ALGO == BI_ALGO_VMP) {
                     double acc = 0.0;
                     for (int j = 0; j < n; ++j) acc = fma(LBp[s * n + j], qprev[j], acc);
@@ -382,7 +383,12 @@ __global__ __launch_bounds__(kThreads) void agent_filter_kernel(AgentArgs a)
             double *lp = logp + fd.q_off;
             if (t == 0) {
                 const double *ld = at<double>(a.base, fd.ld_off) + am * fd.ld_agent;
-                for (int s = lane; s < n; s += 64) lp[s] = ld[s];
+                if (a.prior) {
+                    const float *pr = a.prior + (int64_t)agent * a.ntot + fd.q_off;
+                    for (int s = lane; s < n; s += 64) lp[s] = ln_clamped((double)pr[s]);
+                } else {
+                    for (int s = lane; s < n; s += 64) lp[s] = ld[s];
+                }
             } else {
                 const int u = a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f];
                 const float *Bp = at<float>(a.base, fd.b_off) + am * fd.b_agent + (int64_t)u * n * n;
@@ -426,8 +432,8 @@ constexpr size_t kLdsMax = 160 * 1024;
 
 }  // namespace
 
-int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
-                 float *q, hipStream_t stream)
+int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
+                 const float *prior, int iters, float *q, hipStream_t stream)
 {
     AgentArgs a;
     a.base = m->dev;
@@ -442,6 +448,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     a.zvpc = m->zvpc;
     a.obs = obs;
     a.act = act;
+    a.prior = prior;
     a.q = q;
     const size_t TN = (size_t)T * m->ntot;
     // staged slice layout (see AgentArgs)

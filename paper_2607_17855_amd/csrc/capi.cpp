@@ -209,7 +209,7 @@ int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo,
 }
 
 static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const int32_t *obs, const int32_t *act,
-                 int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream)
+                 const float *prior, int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream)
 {
     try {
         if (!model) return fail(BI_ERR_INVALID_ARG, "model is NULL");
@@ -228,8 +228,9 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
             return fail(BI_ERR_INVALID_ARG, "ws must be %d-byte aligned", bi::kAlign);
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
         const Path p = choose_path(model, algo);
-        if (p != Path::Agent) return bi::launch_stream(model, algo, b, T, obs, act, iters, q, ws, s, p == Path::Sparse);
-        return bi::launch_agent(model, algo, b, T, obs, act, iters, q, s);
+        if (p != Path::Agent)
+            return bi::launch_stream(model, algo, b, T, obs, act, prior, iters, q, ws, s, p == Path::Sparse);
+        return bi::launch_agent(model, algo, b, T, obs, act, prior, iters, q, s);
     } catch (...) {
         return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
     }
@@ -238,19 +239,64 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
 int bi_vfilter(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
                int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, nullptr, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_vmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
            int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, nullptr, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_mmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
            int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, nullptr, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_vfilter_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+                     const float *prior_dev, int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes,
+                     void *hip_stream)
+{
+    if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
+    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, prior_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_vmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+                 const float *prior_dev, int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes,
+                 void *hip_stream)
+{
+    if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
+    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, prior_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_mmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
+                 const float *prior_dev, int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes,
+                 void *hip_stream)
+{
+    if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
+    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, prior_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_predict(const bi_model *model, int32_t b, const float *q_dev, int64_t q_stride, const int32_t *act_dev,
+               int64_t act_stride, float *out_dev, void *hip_stream)
+{
+    try {
+        if (!model) return fail(BI_ERR_INVALID_ARG, "model is NULL");
+        if (!model->dev) return fail(BI_ERR_INVALID_ARG, "model has no device buffer (bi_attach_device_buffer)");
+        if (b < 1) return fail(BI_ERR_INVALID_ARG, "b must be >= 1");
+        if (model->mb != 1 && model->mb != b)
+            return fail(BI_ERR_SHAPE, "b=%d but the model holds %d agents", b, model->mb);
+        if (!q_dev || !act_dev || !out_dev) return fail(BI_ERR_INVALID_ARG, "q, act and out must be non-NULL");
+        if (q_stride < model->ntot)
+            return fail(BI_ERR_INVALID_ARG, "q_stride %lld < %d states", (long long)q_stride, model->ntot);
+        if (act_stride < model->F)
+            return fail(BI_ERR_INVALID_ARG, "act_stride %lld < %d factors", (long long)act_stride, model->F);
+        return bi::launch_predict(model, b, q_dev, q_stride, act_dev, act_stride, out_dev,
+                                  reinterpret_cast<hipStream_t>(hip_stream));
+    } catch (...) {
+        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
+    }
 }
 
 void bi_free_model(bi_model *model) { delete model; }

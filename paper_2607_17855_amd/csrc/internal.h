@@ -38,7 +38,12 @@ int plan(const bi_model_desc *desc, bi_model *m, const float *const *A = nullptr
 
 // Agent-resident launches (one workgroup per agent, every iteration in-kernel).
 // Returns BI_OK or an error code.
-int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
-                 float *q, hipStream_t stream);
+// `prior` (nullable, device fp32 [b][ntot]) replaces D at the first step.
+int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
+                 const float *prior, int iters, float *q, hipStream_t stream);
+
+// Predictive prior B_f[:, :, u] q for every agent and factor (predict.hip).
+int launch_predict(const bi_model *m, int b, const float *q, int64_t q_stride, const int32_t *act,
+                   int64_t act_stride, float *out, hipStream_t stream);
 
 }  // namespace bi

@@ -59,6 +59,7 @@ struct StreamArgs {
     int64_t pstride;            // values of partial messages per context
     const int32_t *obs;
     const int32_t *act;
+    const float *prior;         // optional [agent][ntot] prior of the first step (replaces D)
     int32_t *bstart, *bctx;
     int nmsg, ntask;
     StreamMod sm[kStreamMaxM];
@@ -73,8 +74,8 @@ bool sparse_eligible(const bi_model *m, int algo);
 // Workspace bytes of a streaming call with b agents and window T.
 size_t stream_workspace(const bi_model *m, int b, int T, bool sparse);
 // Enqueue a streaming VMP / MMP call (dense or sparse likelihood kernels).
-int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
-                  float *q, void *ws, hipStream_t stream, bool sparse);
+int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
+                  const float *prior, int iters, float *q, void *ws, hipStream_t stream, bool sparse);
 
 // Dense likelihood kernel with one contraction per workgroup (split.hip), for
 // models whose modalities all have two factors per side (second factors of

@@ -456,7 +456,7 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *par
             }
             double fwd, bwd = 0.0;
             if (t == 0) {
-                fwd = ld[s];
+                fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + fd.q_off + s]) : ld[s];
             } else if (ALGO == BI_ALGO_VMP) {
                 double acc = 0.0;
                 for (int j = 0; j < n; ++j) acc = fma(LBp[s * n + j], (double)qprev[j], acc);
@@ -626,8 +626,8 @@ static void run_iterations(const bi_model *m, int algo, int iters, const StreamA
     }
 }
 
-int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act, int iters,
-                  float *q, void *ws, hipStream_t stream, bool sparse)
+int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
+                  const float *prior, int iters, float *q, void *ws, hipStream_t stream, bool sparse)
 {
     StreamArgs a{};
     int64_t offs[6], total;
@@ -643,6 +643,7 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.ntot = m->ntot;
     a.obs = obs;
     a.act = act;
+    a.prior = prior;
     a.bstart = reinterpret_cast<int32_t *>(w + offs[0]);
     a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
     char *part = w + offs[3];

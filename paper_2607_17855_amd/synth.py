@@ -180,6 +180,25 @@ def sample_sequences(rng: np.random.Generator, model: Model, b: int, T: int):
     return obs, act
 
 
+def random_prior(rng: np.random.Generator, n: Sequence[int], b: int, alpha: float = 1.0,
+                 p_zero: float = 0.0) -> np.ndarray:
+    """A first-step belief per agent, float32 [b][sum n]: each factor's block a
+    Dirichlet(alpha) draw, with states set to zero at rate p_zero (one state
+    of every block kept) and the block renormalised."""
+    out = np.zeros((b, int(sum(n))), dtype=np.float32)
+    off = 0
+    for nf in n:
+        p = rng.dirichlet(np.full(nf, alpha), size=b)
+        if p_zero > 0.0:
+            zero = rng.random((b, nf)) < p_zero
+            zero[np.arange(b), rng.integers(0, nf, size=b)] = False
+            p = np.where(zero, 0.0, p)
+            p /= p.sum(axis=1, keepdims=True)
+        out[:, off:off + nf] = p.astype(np.float32)
+        off += nf
+    return out
+
+
 def _gather_col(a: np.ndarray, ai: np.ndarray, coords) -> np.ndarray:
     """a[ai[i], :, coords[0][i], coords[1][i], ...] for every i -> [b][K]."""
     k = a.shape[1]

@@ -165,6 +165,21 @@ def test_inference_validates_on_host_before_launch():
             assert fn(ctypes.c_void_p(h), 2, 2, fake, None, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
             assert fn(ctypes.c_void_p(h), 2, 2, None, fake, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
             assert fn(ctypes.c_void_p(h), 2, 2, fake, fake, 3, None, None, 0, None) == bi.BI_ERR_INVALID_ARG
+        for fn in (lib.bi_vfilter_prior, lib.bi_vmp_prior, lib.bi_mmp_prior):
+            # the prior is required; the other checks are those of the call without it
+            assert fn(ctypes.c_void_p(h), 2, 2, fake, fake, None, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+            assert fn(ctypes.c_void_p(h), 3, 2, fake, fake, fake, 3, fake, None, 0, None) == bi.BI_ERR_SHAPE
+            assert fn(ctypes.c_void_p(h), 2, 2, fake, fake, fake, 0, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+        ntot, F = sum(m.n), m.F
+        pr = lib.bi_predict
+        assert pr(None, 2, fake, ntot, fake, F, fake, None) == bi.BI_ERR_INVALID_ARG
+        assert pr(ctypes.c_void_p(h), 3, fake, ntot, fake, F, fake, None) == bi.BI_ERR_SHAPE
+        assert pr(ctypes.c_void_p(h), 0, fake, ntot, fake, F, fake, None) == bi.BI_ERR_INVALID_ARG
+        assert pr(ctypes.c_void_p(h), 2, None, ntot, fake, F, fake, None) == bi.BI_ERR_INVALID_ARG
+        assert pr(ctypes.c_void_p(h), 2, fake, ntot, None, F, fake, None) == bi.BI_ERR_INVALID_ARG
+        assert pr(ctypes.c_void_p(h), 2, fake, ntot, fake, F, None, None) == bi.BI_ERR_INVALID_ARG
+        assert pr(ctypes.c_void_p(h), 2, fake, ntot - 1, fake, F, fake, None) == bi.BI_ERR_INVALID_ARG
+        assert pr(ctypes.c_void_p(h), 2, fake, ntot, fake, F - 1, fake, None) == bi.BI_ERR_INVALID_ARG
         sz = ctypes.c_size_t(0)
         assert lib.bi_workspace_size(ctypes.c_void_p(h), 2, 2, 9, ctypes.byref(sz)) == bi.BI_ERR_INVALID_ARG
     finally:

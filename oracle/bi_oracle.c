@@ -26,7 +26,7 @@
  *   LN(x) = log(max(x, 1e-16))  (log of zero is clamped, never -inf)
  *   q initialised uniform; fixed iteration count; Jacobi schedule (every
  *   marginal of iteration k is computed from the marginals of iteration k-1);
- *   no damping.
+ *   no damping unless asked for (below).
  *   Likelihood message (Sec. IV: marginalisation of the log-likelihood under
  *   the other factors' marginals, summed over the Markov blanket):
  *     lam_{t,f}(s) = sum_{m: f in dep(m)} sum_{s_dep: s_f = s}
@@ -47,6 +47,10 @@
  *   h steps before it): a caller may replace D_f by its own prior over the
  *   window's first step (every LN(D_f) above becomes LN(prior_f)), typically
  *   the predictive prior B_f[:,:,u] q_f of an earlier marginal (orc_predict).
+ *   Damping (optional, step size tau in (0, 1]): every sweep mixes the new
+ *   marginal with the current one, q <- (1 - tau) q + tau q_new, where q_new
+ *   is the softmax above computed from the current q; tau = 1 is the plain
+ *   update.  A fixed point of the plain update is one of the damped update.
  */
 #include <math.h>
 #include <omp.h>
@@ -142,10 +146,16 @@ static const double *first_prior(const orc_model *md, const double *prior, int f
     return md->D[f] + (size_t)(md->mb == 1 ? 0 : a) * md->n[f];
 }
 
-static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int *act, int iters, double *q,
-                    const int *qoff, int ntot, double *work, const double *prior)
+/* q <- (1 - tau) q + tau q_new over n values (tau = 1: plain replacement). */
+static void damp(double *q, const double *q_new, int n, double tau)
 {
-    double *cur = work, *lam = work + ntot, *logp = work + 2 * ntot;
+    for (int s = 0; s < n; ++s) q[s] = tau == 1.0 ? q_new[s] : (1.0 - tau) * q[s] + tau * q_new[s];
+}
+
+static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int *act, int iters, double *q,
+                    const int *qoff, int ntot, double *work, const double *prior, double tau)
+{
+    double *cur = work, *lam = work + ntot, *logp = work + 2 * ntot, *v = work + 3 * ntot;
     for (int t = 0; t < T; ++t) {
         for (int f = 0; f < md->F; ++f) {
             const int nf = md->n[f];
@@ -167,9 +177,9 @@ static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int
         for (int k = 0; k < iters; ++k) {
             likelihood_messages(md, a, obs + (size_t)t * md->M, cur, qoff, ntot, lam);
             for (int f = 0; f < md->F; ++f) {
-                double *v = cur + qoff[f];
                 for (int s = 0; s < md->n[f]; ++s) v[s] = lam[qoff[f] + s] + logp[qoff[f] + s];
                 softmax(v, md->n[f]);
+                damp(cur + qoff[f], v, md->n[f], tau);
             }
         }
         memcpy(q + (size_t)t * ntot, cur, sizeof(double) * (size_t)ntot);
@@ -177,7 +187,7 @@ static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int
 }
 
 static void run_window(const orc_model *md, int algo, int a, int T, const int *obs, const int *act, int iters,
-                       double *q, const int *qoff, int ntot, double *work, const double *prior)
+                       double *q, const int *qoff, int ntot, double *work, const double *prior, double tau)
 {
     double *qn = work;                               /* [T][ntot] next iterate */
     double *lam = work + (size_t)T * ntot;            /* [T][ntot] */
@@ -231,22 +241,23 @@ static void run_window(const orc_model *md, int algo, int a, int T, const int *o
                 softmax(v, nf);
             }
         }
-        memcpy(q, qn, sizeof(double) * (size_t)T * ntot);
+        damp(q, qn, T * ntot, tau);
     }
 }
 
 /*
  * Run `algo` (0 FPI, 1 VMP, 2 MMP) for b agents.  prior: NULL (p(s_1) = D)
- * or [b][sum n_f], each factor's block a distribution over its states.
- * Returns 0, or -1 on an invalid argument.  nthreads <= 0 uses the OpenMP
- * default.
+ * or [b][sum n_f], each factor's block a distribution over its states; tau:
+ * damping step in (0, 1].  Returns 0, or -1 on an invalid argument.
+ * nthreads <= 0 uses the OpenMP default.
  */
-int orc_infer_prior(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
-                    const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
-                    int b, int T, const int *obs, const int *act, const double *prior, int iters, double *q,
-                    int nthreads)
+int orc_infer_ex(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
+                 const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
+                 int b, int T, const int *obs, const int *act, const double *prior, double tau, int iters,
+                 double *q, int nthreads)
 {
     if (algo < 0 || algo > 2 || F < 1 || M < 1 || b < 1 || T < 1 || iters < 1) return -1;
+    if (!(tau > 0.0 && tau <= 1.0)) return -1;
     if (mb != 1 && mb != b) return -1;
     if (!n || !U || !K || !dep_off || !dep || !A || !B || !D || !obs || !q) return -1;
     if (T > 1 && !act) return -1;
@@ -265,7 +276,7 @@ int orc_infer_prior(int algo, int F, const int *n, const int *U, int M, const in
             if (dep[i] < 0 || dep[i] >= F) { free(qoff); return -1; }
     }
     orc_model md = {F, M, mb, n, U, K, dep_off, dep, A, B, D};
-    const size_t work_per = (size_t)(3 + 2 * T) * (size_t)ntot;
+    const size_t work_per = (size_t)(4 + 2 * T) * (size_t)ntot;
     int bad = 0;
     const int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
 #pragma omp parallel for schedule(dynamic, 1) num_threads(nt) reduction(| : bad)
@@ -276,13 +287,22 @@ int orc_infer_prior(int algo, int F, const int *n, const int *U, int M, const in
         const int *ua = T > 1 ? act + (size_t)a * (T - 1) * F : NULL;
         double *qa = q + (size_t)a * T * ntot;
         if (algo == ORC_FPI)
-            run_fpi(&md, a, T, oa, ua, iters, qa, qoff, ntot, work, prior);
+            run_fpi(&md, a, T, oa, ua, iters, qa, qoff, ntot, work, prior, tau);
         else
-            run_window(&md, algo, a, T, oa, ua, iters, qa, qoff, ntot, work, prior);
+            run_window(&md, algo, a, T, oa, ua, iters, qa, qoff, ntot, work, prior, tau);
         free(work);
     }
     free(qoff);
     return bad ? -1 : 0;
+}
+
+int orc_infer_prior(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
+                    const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
+                    int b, int T, const int *obs, const int *act, const double *prior, int iters, double *q,
+                    int nthreads)
+{
+    return orc_infer_ex(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, b, T, obs, act, prior, 1.0, iters, q,
+                        nthreads);
 }
 
 int orc_infer(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,

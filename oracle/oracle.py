@@ -50,6 +50,12 @@ def load_library(path: str):
                                     P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p), ctypes.c_int,
                                     ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_double),
                                     ctypes.c_int, P(ctypes.c_double), ctypes.c_int]
+    lib.orc_infer_ex.restype = ctypes.c_int
+    lib.orc_infer_ex.argtypes = [ctypes.c_int, ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                 P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                 P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p), ctypes.c_int,
+                                 ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_double),
+                                 ctypes.c_double, ctypes.c_int, P(ctypes.c_double), ctypes.c_int]
     lib.orc_predict.restype = ctypes.c_int
     lib.orc_predict.argtypes = [ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int, P(ctypes.c_void_p),
                                 ctypes.c_int, P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double)]
@@ -76,10 +82,11 @@ def _i32(x) -> np.ndarray:
 
 def infer(algo: str, model, obs: np.ndarray, act: np.ndarray, iters: int,
           agents: Optional[Sequence[int]] = None, threads: int = 0, lib=None,
-          prior: Optional[np.ndarray] = None) -> np.ndarray:
+          prior: Optional[np.ndarray] = None, damping: float = 1.0) -> np.ndarray:
     """Posterior marginals q [b][T][sum n] (float64) of ``algo`` for every agent,
     or for the listed ``agents`` only (agents are independent).  ``prior``:
-    [b][sum n] distributions over the first step, replacing D."""
+    [b][sum n] distributions over the first step, replacing D.  ``damping``:
+    step tau in (0, 1] of q <- (1 - tau) q + tau q_new (1 = plain update)."""
     if lib is None:
         lib = _load()
     if agents is not None:
@@ -103,14 +110,14 @@ def infer(algo: str, model, obs: np.ndarray, act: np.ndarray, iters: int,
     q = np.zeros((b, T, int(sum(model.n))), dtype=np.float64)
     ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))  # noqa: E731
     dp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))  # noqa: E731
-    if prior is None:
+    if prior is None and damping == 1.0:
         rc = lib.orc_infer(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
                            ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c), int(iters), dp(q), int(threads))
     else:
-        pr = np.ascontiguousarray(prior, dtype=np.float64).reshape(b, int(sum(model.n)))
-        rc = lib.orc_infer_prior(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
-                                 ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c), dp(pr), int(iters), dp(q),
-                                 int(threads))
+        pr = None if prior is None else np.ascontiguousarray(prior, dtype=np.float64).reshape(b, int(sum(model.n)))
+        rc = lib.orc_infer_ex(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
+                              ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c),
+                              None if pr is None else dp(pr), float(damping), int(iters), dp(q), int(threads))
     if rc != 0:
         raise ValueError(f"oracle rejected the arguments (rc={rc})")
     return q

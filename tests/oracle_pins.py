@@ -326,6 +326,75 @@ def pin_prior_t1(infer):
     return err
 
 
+def pin_damped_filter(infer):
+    """Damping q <- (1 - tau) q + tau q_new with one factor: FPI's target at
+    step t, Bayes' rule A[o_t] * prior_t / Z, does not depend on the current
+    iterate, so K sweeps from the uniform start leave
+    q_t = target + (1 - tau)^K (uniform - target) exactly, and the next
+    step's prior is B q_t of that (not yet converged) marginal."""
+    err = 0.0
+    for seed, K, iters, tau in [(21, (3,), 1, 0.3), (22, (5, 2), 4, 0.7), (23, (2, 2, 4), 3, 0.5)]:
+        model, obs, act = _hmm(seed, n=5, K=K, T=6, b=3)
+        q = infer("fpi", model, obs, act, iters, damping=tau)
+        n = model.n[0]
+        for a in range(obs.shape[0]):
+            B = np.float64(model.B[0][a])
+            pred = np.float64(model.D[0][a])
+            for t in range(obs.shape[1]):
+                lik = np.ones(n)
+                for m, A in enumerate(model.A):
+                    lik = lik * np.float64(A[a][obs[a, t, m]])
+                target = lik * pred / (lik * pred).sum()
+                want = target + (1.0 - tau) ** iters * (np.full(n, 1.0 / n) - target)
+                err = max(err, float(np.abs(q[a, t] - want).max()))
+                if t + 1 < obs.shape[1]:
+                    pred = B[:, :, act[a, t, 0]] @ want
+    return err
+
+
+def pin_damped_iid(infer):
+    """Damping with transitions that ignore the previous state: the VMP and
+    MMP targets (the closed forms of pin_iid_closed_forms) do not depend on
+    the iterate, so K damped sweeps give target + (1 - tau)^K (uniform - target)."""
+    err = 0.0
+    for seed, T, iters, tau in [(31, 5, 3, 0.4), (32, 2, 1, 0.8), (33, 4, 6, 0.25)]:
+        model, obs, act = _iid_model(seed, T=T)
+        b, n = obs.shape[0], model.n[0]
+        qv = infer("vmp", model, obs, act, iters, damping=tau)
+        qm = infer("mmp", model, obs, act, iters, damping=tau)
+        shrink = (1.0 - tau) ** iters
+        for a in range(b):
+            B = np.float64(model.B[0][a])
+            D = np.float64(model.D[0][a])
+            for t in range(T):
+                L = np.ones(n)
+                for m in range(model.M):
+                    L = L * np.float64(model.A[m][a][obs[a, t, m]])
+                prior = D if t == 0 else B[:, 0, act[a, t - 1, 0]]
+                for q, tgt in ((qv, L * prior), (qm, L * (prior if t == T - 1 else np.sqrt(prior)))):
+                    tgt = tgt / tgt.sum()
+                    err = max(err, float(np.abs(q[a, t] - (tgt + shrink * (1.0 / n - tgt))).max()))
+    return err
+
+
+def pin_damped_fixed_point(infer):
+    """A fixed point of the plain update is a fixed point of the damped one:
+    on models where the plain Jacobi iteration converges, the damped
+    iteration converges to the same marginals (VMP and MMP, several factors,
+    a window of several steps).  Convergence of each run is checked too."""
+    err = 0.0
+    for seed in (41, 42, 43):
+        w = synth.random_small(seed, F_max=3, n_max=4, M_max=3, K_max=3, T_max=4, b=2)
+        for algo in ("vmp", "mmp"):
+            plain = infer(algo, w.model, w.obs, w.act, 300)
+            plain1 = infer(algo, w.model, w.obs, w.act, 301)
+            damped = infer(algo, w.model, w.obs, w.act, 600, damping=0.5)
+            damped1 = infer(algo, w.model, w.obs, w.act, 601, damping=0.5)
+            err = max(err, float(np.abs(plain - plain1).max()), float(np.abs(damped - damped1).max()),
+                      float(np.abs(plain - damped).max()))
+    return err
+
+
 ALL_PINS = {
     "bayes_filter": (pin_bayes_filter, 1e-12),
     "golden_hmm2": (pin_golden_hmm2, 1e-7),
@@ -338,4 +407,7 @@ ALL_PINS = {
     "invariants": (pin_invariants, 1e-12),
     "online_filter": (pin_online_filter, 1e-12),
     "prior_t1": (pin_prior_t1, 1e-12),
+    "damped_filter": (pin_damped_filter, 1e-12),
+    "damped_iid": (pin_damped_iid, 1e-12),
+    "damped_fixed_point": (pin_damped_fixed_point, 1e-10),
 }

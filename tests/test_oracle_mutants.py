@@ -33,6 +33,8 @@ MUTANTS = [
     ("caller_prior_ignored", "if (prior) return prior + (size_t)a * ntot + qoff[f];", "", 1),
     ("predict_transposed", "p += Bf[((size_t)i * nf + j) * U[f] + u] * q[(size_t)a * ntot + off + j];",
      "p += Bf[((size_t)j * nf + i) * U[f] + u] * q[(size_t)a * ntot + off + j];", 1),
+    ("damping_swapped", "(1.0 - tau) * q[s] + tau * q_new[s]", "tau * q[s] + (1.0 - tau) * q_new[s]", 1),
+    ("damping_ignored", "q[s] = tau == 1.0 ? q_new[s] :", "q[s] = 1 ? q_new[s] :", 1),
     ("softmax_sign", "v[i] = exp(v[i] - mx);", "v[i] = exp(mx - v[i]);", 1),
     ("no_log_clamp", "return log(x > ORC_EPS ? x : ORC_EPS);", "return log(x > 0 ? x : 1e-300);", 1),
 ]

@@ -23,3 +23,6 @@ def test_rejects_bad_arguments():
     with pytest.raises(ValueError):
         oracle.infer("vmp", bad, w.obs, w.act, 2)
     assert np.all(np.isfinite(oracle.infer("mmp", w.model, w.obs, w.act, 2)))
+    for tau in (0.0, -0.5, 1.5):
+        with pytest.raises(ValueError):
+            oracle.infer("vmp", w.model, w.obs, w.act, 2, damping=tau)

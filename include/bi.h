@@ -225,6 +225,32 @@ int bi_mmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs
                  void *hip_stream);
 
 /*
+ * Options of bi_infer (all calls above are bi_infer with some of them fixed).
+ *   prior_dev: NULL (the first step's prior is D) or as for bi_vfilter_prior.
+ *   damping:   step tau in (0, 1] of a damped update: every sweep (every
+ *              iteration of FPI at a step; every Jacobi sweep of VMP / MMP)
+ *              mixes the new marginal with the current one,
+ *                q <- (1 - tau) q + tau q_new,
+ *              q_new being the update stated above for that algorithm.
+ *              1 is the plain update; a fixed point of the plain update is
+ *              one of the damped update, which oscillates less.
+ */
+typedef struct bi_infer_opts {
+    const float *prior_dev;
+    double damping;
+} bi_infer_opts;
+
+/*
+ * Inference with options: algo is BI_ALGO_FPI / _VMP / _MMP; opts NULL means
+ * { NULL, 1.0 }.  Other arguments, the workspace (bi_workspace_size for the
+ * same algo) and the errors are those of bi_vfilter; a damping outside
+ * (0, 1] (or NaN) is BI_ERR_INVALID_ARG, as is an unknown algo.
+ */
+int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const int32_t *obs_dev,
+             const int32_t *act_dev, int32_t iters, const bi_infer_opts *opts, float *q_dev, void *ws_dev,
+             size_t ws_bytes, void *hip_stream);
+
+/*
  * Predictive prior of the next step (the product FPI uses between steps,
  * Sec. III-B transition model): for every agent a and factor f
  *   out[a][f](i) = sum_j B_f[i][j][u_{a,f}] q[a][f](j)      (fp64 sums)

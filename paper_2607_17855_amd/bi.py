@@ -30,7 +30,7 @@ ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
 
 EXPORTS = ("bi_last_error", "bi_plan_model", "bi_plan_model_exact", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
            "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_vfilter_prior",
-           "bi_vmp_prior", "bi_mmp_prior", "bi_predict", "bi_free_model",
+           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_predict", "bi_free_model",
            "bi_profile_begin", "bi_profile_end")
 
 
@@ -54,6 +54,10 @@ class bi_profile_entry(ctypes.Structure):
 class bi_model_stats(ctypes.Structure):
     _fields_ = [("a_raw", ctypes.c_int64), ("a_stored", ctypes.c_int64), ("a_nnz", ctypes.c_int64),
                 ("device_bytes", ctypes.c_int64)]
+
+
+class bi_infer_opts(ctypes.Structure):
+    _fields_ = [("prior_dev", ctypes.c_void_p), ("damping", ctypes.c_double)]
 
 
 _lib = None
@@ -82,6 +86,7 @@ def load(path: str = LIB_PATH):
         getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, sz, vp]
     for name in ("bi_vfilter_prior", "bi_vmp_prior", "bi_mmp_prior"):
         getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, sz, vp]
+    lib.bi_infer.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp, sz, vp]
     lib.bi_predict.argtypes = [vp, i32, vp, ctypes.c_int64, vp, ctypes.c_int64, vp, vp]
     lib.bi_free_model.argtypes = [vp]
     lib.bi_free_model.restype = None
@@ -234,6 +239,17 @@ def bi_mmp_prior(handle, b, T, obs, act, prior, iters, q, ws=None, stream=None):
     _infer("bi_mmp_prior", handle, b, T, obs, act, iters, q, ws, stream, prior)
 
 
+def bi_infer(handle, algo: int, b, T, obs, act, iters, q, ws=None, stream=None, prior=None, damping: float = 1.0):
+    """The general entry point: any algorithm, optional first-step prior and damping."""
+    ws_ptr = ws.data_ptr() if ws is not None else 0
+    ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    act_ptr = act.data_ptr() if act is not None and act.numel() > 0 else 0
+    opts = bi_infer_opts(ctypes.c_void_p(prior.data_ptr() if prior is not None else 0), float(damping))
+    _check(load().bi_infer(ctypes.c_void_p(handle), int(algo), int(b), int(T), ctypes.c_void_p(obs.data_ptr()),
+                           ctypes.c_void_p(act_ptr), int(iters), ctypes.byref(opts), ctypes.c_void_p(q.data_ptr()),
+                           ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(_stream_ptr(stream))))
+
+
 def bi_predict(handle, b, q, q_stride, act, act_stride, out, stream=None):
     """out[a] = B[:, :, act[a]] q[a] per factor; q / act rows at a * q_stride / a * act_stride elements."""
     _check(load().bi_predict(ctypes.c_void_p(handle), int(b), ctypes.c_void_p(q.data_ptr()), int(q_stride),
@@ -282,17 +298,21 @@ class PackedModel:
         nb = bi_workspace_size(self.handle, b, T, ALGO_IDS[algo])
         return torch.empty(nb, dtype=torch.uint8, device=self.buf.device) if nb else None
 
-    def infer(self, algo: str, obs, act, iters: int, q=None, ws=None, stream=None, prior=None):
+    def infer(self, algo: str, obs, act, iters: int, q=None, ws=None, stream=None, prior=None,
+              damping: float = 1.0):
         """obs [b][T][M] / act [b][T-1][F] int32 device tensors -> q [b][T][sum n] float32.
 
-        prior: optional float32 device tensor [b][sum n], the first step's prior in place of D."""
+        prior: optional float32 device tensor [b][sum n], the first step's prior in place of D.
+        damping: step tau in (0, 1] of q <- (1 - tau) q + tau q_new (1 = plain update)."""
         import torch
         b, T = int(obs.shape[0]), int(obs.shape[1])
         if q is None:
             q = torch.empty((b, T, sum(self.model.n)), dtype=torch.float32, device=self.buf.device)
         if ws is None:
             ws = self.workspace(b, T, algo)
-        if prior is None:
+        if damping != 1.0:
+            bi_infer(self.handle, ALGO_IDS[algo], b, T, obs, act, iters, q, ws, stream, prior, damping)
+        elif prior is None:
             _ENTRY[algo](self.handle, b, T, obs, act, iters, q, ws, stream)
         else:
             _ENTRY_PRIOR[algo](self.handle, b, T, obs, act, prior, iters, q, ws, stream)

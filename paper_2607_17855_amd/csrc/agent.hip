@@ -50,6 +50,7 @@ struct AgentArgs {
     const int32_t *obs;
     const int32_t *act;
     const float *prior;    // optional [agent][ntot] prior of the first step (replaces D)
+    double tau;            // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
     float *q;
 };
 
@@ -348,6 +349,10 @@ __global__ __launch_bounds__(kThreads) void agent_window_kernel(AgentArgs a)
                 v[s] = val;
             }
             wave_softmax(v, n, lane);
+            if (a.tau != 1.0) {
+                const double *old = cur + t * a.ntot + fd.q_off;
+                for (int s = lane; s < n; s += 64) v[s] = (1.0 - a.tau) * old[s] + a.tau * v[s];
+            }
         }
         __syncthreads();
         double *tmp = cur;
@@ -411,13 +416,19 @@ __global__ __launch_bounds__(kThreads) void agent_filter_kernel(AgentArgs a)
             phase_lam(a, t, 1, cur, zv, sfac, lam);
             __syncthreads();
             // Jacobi: lam holds every factor's message from the previous iterate
+            // (damped: the new marginal is formed in lam's row, then mixed
+            // into the current one; each lane owns the same states throughout)
             for (int f = wave; f < a.F; f += kWaves) {
                 const FacDesc &fd = a.facs[f];
-                double *v = qt + fd.q_off;
-                const double *lm = lam + t * a.ntot + fd.q_off;
+                double *lm = lam + t * a.ntot + fd.q_off;
+                double *v = a.tau != 1.0 ? lm : qt + fd.q_off;
                 const double *lp = logp + fd.q_off;
                 for (int s = lane; s < fd.n; s += 64) v[s] = lm[s] + lp[s];
                 wave_softmax(v, fd.n, lane);
+                if (a.tau != 1.0) {
+                    double *qf = qt + fd.q_off;
+                    for (int s = lane; s < fd.n; s += 64) qf[s] = (1.0 - a.tau) * qf[s] + a.tau * v[s];
+                }
             }
             __syncthreads();
         }
@@ -433,7 +444,7 @@ constexpr size_t kLdsMax = 160 * 1024;
 }  // namespace
 
 int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
-                 const float *prior, int iters, float *q, hipStream_t stream)
+                 const float *prior, double tau, int iters, float *q, hipStream_t stream)
 {
     AgentArgs a;
     a.base = m->dev;
@@ -449,6 +460,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     a.obs = obs;
     a.act = act;
     a.prior = prior;
+    a.tau = tau;
     a.q = q;
     const size_t TN = (size_t)T * m->ntot;
     // staged slice layout (see AgentArgs)

@@ -209,7 +209,7 @@ int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo,
 }
 
 static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const int32_t *obs, const int32_t *act,
-                 const float *prior, int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream)
+                 const float *prior, double tau, int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream)
 {
     try {
         if (!model) return fail(BI_ERR_INVALID_ARG, "model is NULL");
@@ -219,6 +219,7 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
             return fail(BI_ERR_SHAPE, "b=%d but the model holds %d agents", b, model->mb);
         if (!obs || !q) return fail(BI_ERR_INVALID_ARG, "obs and q must be non-NULL");
         if (T > 1 && !act) return fail(BI_ERR_INVALID_ARG, "act must be non-NULL when T > 1");
+        if (!(tau > 0.0 && tau <= 1.0)) return fail(BI_ERR_INVALID_ARG, "damping %g is not in (0, 1]", tau);
         size_t need = 0;
         int rc = bi_workspace_size(model, b, T, algo, &need);
         if (rc != BI_OK) return rc;
@@ -229,8 +230,8 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
         const Path p = choose_path(model, algo);
         if (p != Path::Agent)
-            return bi::launch_stream(model, algo, b, T, obs, act, prior, iters, q, ws, s, p == Path::Sparse);
-        return bi::launch_agent(model, algo, b, T, obs, act, prior, iters, q, s);
+            return bi::launch_stream(model, algo, b, T, obs, act, prior, tau, iters, q, ws, s, p == Path::Sparse);
+        return bi::launch_agent(model, algo, b, T, obs, act, prior, tau, iters, q, s);
     } catch (...) {
         return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
     }
@@ -239,19 +240,19 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
 int bi_vfilter(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
                int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, nullptr, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_vmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
            int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, nullptr, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_mmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
            int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, nullptr, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_vfilter_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
@@ -259,7 +260,7 @@ int bi_vfilter_prior(const bi_model *model, int32_t b, int32_t T, const int32_t 
                      void *hip_stream)
 {
     if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
-    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, prior_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_vmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
@@ -267,7 +268,7 @@ int bi_vmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs
                  void *hip_stream)
 {
     if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
-    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, prior_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_mmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
@@ -275,7 +276,17 @@ int bi_mmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs
                  void *hip_stream)
 {
     if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
-    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, prior_dev, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const int32_t *obs_dev,
+             const int32_t *act_dev, int32_t iters, const bi_infer_opts *opts, float *q_dev, void *ws_dev,
+             size_t ws_bytes, void *hip_stream)
+{
+    if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
+    const float *prior = opts ? opts->prior_dev : nullptr;
+    const double tau = opts ? opts->damping : 1.0;
+    return infer(algo, model, b, T, obs_dev, act_dev, prior, tau, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_predict(const bi_model *model, int32_t b, const float *q_dev, int64_t q_stride, const int32_t *act_dev,

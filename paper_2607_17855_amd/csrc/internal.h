@@ -38,9 +38,10 @@ int plan(const bi_model_desc *desc, bi_model *m, const float *const *A = nullptr
 
 // Agent-resident launches (one workgroup per agent, every iteration in-kernel).
 // Returns BI_OK or an error code.
-// `prior` (nullable, device fp32 [b][ntot]) replaces D at the first step.
+// `prior` (nullable, device fp32 [b][ntot]) replaces D at the first step;
+// `tau` in (0, 1] damps every update: q <- (1 - tau) q + tau q_new.
 int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
-                 const float *prior, int iters, float *q, hipStream_t stream);
+                 const float *prior, double tau, int iters, float *q, hipStream_t stream);
 
 // Predictive prior B_f[:, :, u] q for every agent and factor (predict.hip).
 int launch_predict(const bi_model *m, int b, const float *q, int64_t q_stride, const int32_t *act,

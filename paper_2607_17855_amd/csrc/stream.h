@@ -60,6 +60,7 @@ struct StreamArgs {
     const int32_t *obs;
     const int32_t *act;
     const float *prior;         // optional [agent][ntot] prior of the first step (replaces D)
+    double tau;                 // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
     int32_t *bstart, *bctx;
     int nmsg, ntask;
     StreamMod sm[kStreamMaxM];
@@ -75,7 +76,7 @@ bool sparse_eligible(const bi_model *m, int algo);
 size_t stream_workspace(const bi_model *m, int b, int T, bool sparse);
 // Enqueue a streaming VMP / MMP call (dense or sparse likelihood kernels).
 int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
-                  const float *prior, int iters, float *q, void *ws, hipStream_t stream, bool sparse);
+                  const float *prior, double tau, int iters, float *q, void *ws, hipStream_t stream, bool sparse);
 
 // Dense likelihood kernel with one contraction per workgroup (split.hip), for
 // models whose modalities all have two factors per side (second factors of

@@ -492,7 +492,12 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *par
         }
         sum = wave_sum(sum);
         OT *out = qout + (int64_t)ctx * a.ntot + fd.q_off;
-        for (int s = lane; s < n; s += 64) out[s] = (OT)(v[s] / sum);
+        if (a.tau != 1.0) {
+            const QT *old = qin + (int64_t)ctx * a.ntot + fd.q_off;
+            for (int s = lane; s < n; s += 64) out[s] = (OT)((1.0 - a.tau) * (double)old[s] + a.tau * (v[s] / sum));
+        } else {
+            for (int s = lane; s < n; s += 64) out[s] = (OT)(v[s] / sum);
+        }
     }
 }
 
@@ -627,7 +632,7 @@ static void run_iterations(const bi_model *m, int algo, int iters, const StreamA
 }
 
 int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
-                  const float *prior, int iters, float *q, void *ws, hipStream_t stream, bool sparse)
+                  const float *prior, double tau, int iters, float *q, void *ws, hipStream_t stream, bool sparse)
 {
     StreamArgs a{};
     int64_t offs[6], total;
@@ -644,6 +649,7 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.obs = obs;
     a.act = act;
     a.prior = prior;
+    a.tau = tau;
     a.bstart = reinterpret_cast<int32_t *>(w + offs[0]);
     a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
     char *part = w + offs[3];

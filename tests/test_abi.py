@@ -170,6 +170,17 @@ def test_inference_validates_on_host_before_launch():
             assert fn(ctypes.c_void_p(h), 2, 2, fake, fake, None, 3, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
             assert fn(ctypes.c_void_p(h), 3, 2, fake, fake, fake, 3, fake, None, 0, None) == bi.BI_ERR_SHAPE
             assert fn(ctypes.c_void_p(h), 2, 2, fake, fake, fake, 0, fake, None, 0, None) == bi.BI_ERR_INVALID_ARG
+        bi_ = lib.bi_infer
+        for tau in (0.0, -1.0, 1.5, float("nan")):
+            opts = bi.bi_infer_opts(None, tau)
+            assert bi_(ctypes.c_void_p(h), 1, 2, 2, fake, fake, 3, ctypes.byref(opts), fake, None, 0, None) == \
+                bi.BI_ERR_INVALID_ARG
+        opts = bi.bi_infer_opts(None, 0.5)
+        assert bi_(ctypes.c_void_p(h), 3, 2, 2, fake, fake, 3, ctypes.byref(opts), fake, None, 0, None) == \
+            bi.BI_ERR_INVALID_ARG   # unknown algorithm
+        assert bi_(ctypes.c_void_p(h), 1, 3, 2, fake, fake, 3, ctypes.byref(opts), fake, None, 0, None) == \
+            bi.BI_ERR_SHAPE
+        assert bi_(ctypes.c_void_p(h), 1, 2, 2, fake, fake, 3, None, None, None, 0, None) == bi.BI_ERR_INVALID_ARG
         ntot, F = sum(m.n), m.F
         pr = lib.bi_predict
         assert pr(None, 2, fake, ntot, fake, F, fake, None) == bi.BI_ERR_INVALID_ARG

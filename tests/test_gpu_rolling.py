@@ -169,3 +169,42 @@ def test_online_filter_matches_full_window(seed):
         assert err <= TOL
     finally:
         pm.close()
+
+
+def _check_damped(w, algo, flags, path, seed, tau, with_prior):
+    """bi_infer with damping (and optionally a prior) vs the oracle."""
+    torch = _torch()
+    pm = bi.PackedModel(w.model, flags)
+    try:
+        with _ForcePath(path):
+            prior = _prior(seed, w) if with_prior else None
+            print(f"[gpu] {w.name} {algo} b={w.b} T={w.T} iters={w.iters} flags={flags} damping={tau} "
+                  f"prior={with_prior}", flush=True)
+            q = pm.infer(algo, _dev(w.obs), _dev(w.act), w.iters, prior=None if prior is None else _dev(prior),
+                         damping=tau)
+            torch.cuda.synchronize()
+            q = q.cpu().numpy()
+            check_invariants(w, q)
+            ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters,
+                               prior=None if prior is None else prior.astype(np.float64), damping=tau)
+            err = float(np.abs(q - ref).max())
+            print(f"[gpu]   {algo} damped vs oracle {err:.3e}", flush=True)
+            assert err <= TOL
+    finally:
+        pm.close()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_damping_agent_path(seed):
+    w = synth.random_small(340 + seed, b=4, T_max=5, per_agent=bool(seed % 2))
+    for algo in ("fpi", "vmp", "mmp"):
+        _check_damped(w, algo, bi.BI_DENSE_A, "agent", 540 + seed, (0.3, 0.5, 0.8, 0.65)[seed], seed >= 2)
+
+
+@pytest.mark.parametrize("case", range(len(SHARED)))
+def test_damping_stream_and_sparse_paths(case):
+    w = _shared_model(640 + case, *SHARED[case], iters=3)
+    ws = _shared_model(660 + case, *SHARED[case], sparsity=0.6, iters=3)
+    for algo in ("vmp", "mmp"):
+        _check_damped(w, algo, bi.BI_DENSE_A | bi.BI_FAST_F32, "stream", 740 + case, 0.45, case == 1)
+        _check_damped(ws, algo, bi.BI_SPARSE_A, None, 760 + case, 0.7, case != 1)

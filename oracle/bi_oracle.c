@@ -47,6 +47,10 @@
  *   h steps before it): a caller may replace D_f by its own prior over the
  *   window's first step (every LN(D_f) above becomes LN(prior_f)), typically
  *   the predictive prior B_f[:,:,u] q_f of an earlier marginal (orc_predict).
+ *   Soft observations (orc_infer_soft): o_{t,m} is a vector over the K_m
+ *   outcomes and every LN(A_m[o_{t,m}, s_dep]) above becomes the expected
+ *   log-likelihood sum_o o_{t,m}[o] LN(A_m[o, s_dep]) (the log(A) . o
+ *   contraction of Sec. III-C); an integer outcome is the one-hot vector.
  *   Damping (optional, step size tau in (0, 1]): every sweep mixes the new
  *   marginal with the current one, q <- (1 - tau) q + tau q_new, where q_new
  *   is the softmax above computed from the current q; tau = 1 is the plain
@@ -94,23 +98,59 @@ static size_t slice_size(const orc_model *md, int m)
     return p;
 }
 
-/* Likelihood messages of one context (agent a, one time step).
- * o: [M] observed outcomes; q: [sum n] marginals of the context;
- * lam: [sum n] output.  qoff[f] is the offset of factor f in q / lam. */
-static void likelihood_messages(const orc_model *md, int a, const int *o, const double *q, const int *qoff,
-                                int ntot, double *lam)
+/* Observations of one agent: integer outcomes hard[T][M], or soft ones,
+ * soft[T][sum K] (a distribution over modality m's outcomes at koff[m]). */
+typedef struct {
+    const int *hard;
+    const double *soft;
+    const int *koff;
+    int ksum;
+} orc_obs;
+
+/* Log-likelihood tensors of context t, concatenated over the modalities
+ * (modality m's values at poff[m], row-major over s_dep like A):
+ *   integer outcome o:    ll_m(s_dep) = LN(A_m[o, s_dep]);
+ *   soft observation o_m: ll_m(s_dep) = sum_o o_m[o] LN(A_m[o, s_dep]),
+ * i.e. the product log(A_block) . o_concat of the block-diagonal merge
+ * (Sec. III-C and Appendix: each A_m reshaped to p_m x K_m, the blocks on
+ * the diagonal, the observation vectors concatenated). */
+static void context_loglik(const orc_model *md, int a, const orc_obs *ob, int t, const size_t *poff, double *ll)
 {
     int am = md->mb == 1 ? 0 : a;
+    for (int m = 0; m < md->M; ++m) {
+        const size_t P = slice_size(md, m);
+        const double *Am = md->A[m] + (size_t)am * md->K[m] * P;   /* [K_m][P] */
+        double *out = ll + poff[m];
+        if (ob->hard) {
+            const double *slice = Am + (size_t)ob->hard[(size_t)t * md->M + m] * P;
+            for (size_t e = 0; e < P; ++e) out[e] = LN(slice[e]);
+        } else {
+            const double *om = ob->soft + (size_t)t * ob->ksum + ob->koff[m];
+            for (size_t e = 0; e < P; ++e) {
+                double v = 0.0;
+                for (int o = 0; o < md->K[m]; ++o) v += om[o] * LN(Am[(size_t)o * P + e]);
+                out[e] = v;
+            }
+        }
+    }
+}
+
+/* Likelihood messages of one context from its log-likelihood tensors ll
+ * (context_loglik).  q: [sum n] marginals of the context; lam: [sum n]
+ * output.  qoff[f] is the offset of factor f in q / lam. */
+static void likelihood_messages(const orc_model *md, const double *lls, const size_t *poff, const double *q,
+                                const int *qoff, int ntot, double *lam)
+{
     for (int i = 0; i < ntot; ++i) lam[i] = 0.0;
     for (int m = 0; m < md->M; ++m) {
         const int k = md->dep_off[m + 1] - md->dep_off[m];
         const int *d = md->dep + md->dep_off[m];
         const size_t P = slice_size(md, m);
-        const double *slice = md->A[m] + ((size_t)am * md->K[m] + (size_t)o[m]) * P;
+        const double *llm = lls + poff[m];
         int idx[ORC_MAX_RANK];
         for (int i = 0; i < k; ++i) idx[i] = 0;
         for (size_t e = 0; e < P; ++e) {
-            const double ll = LN(slice[e]);
+            const double ll = llm[e];
             for (int i = 0; i < k; ++i) {
                 double w = 1.0;
                 for (int j = 0; j < k; ++j)
@@ -152,8 +192,9 @@ static void damp(double *q, const double *q_new, int n, double tau)
     for (int s = 0; s < n; ++s) q[s] = tau == 1.0 ? q_new[s] : (1.0 - tau) * q[s] + tau * q_new[s];
 }
 
-static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int *act, int iters, double *q,
-                    const int *qoff, int ntot, double *work, const double *prior, double tau)
+static void run_fpi(const orc_model *md, int a, int T, const orc_obs *obs, const int *act, int iters, double *q,
+                    const int *qoff, int ntot, double *work, const double *prior, double tau, const size_t *poff,
+                    double *lls)
 {
     double *cur = work, *lam = work + ntot, *logp = work + 2 * ntot, *v = work + 3 * ntot;
     for (int t = 0; t < T; ++t) {
@@ -175,7 +216,8 @@ static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int
             for (int s = 0; s < nf; ++s) cur[qoff[f] + s] = 1.0 / nf;
         }
         for (int k = 0; k < iters; ++k) {
-            likelihood_messages(md, a, obs + (size_t)t * md->M, cur, qoff, ntot, lam);
+            context_loglik(md, a, obs, t, poff, lls);
+            likelihood_messages(md, lls, poff, cur, qoff, ntot, lam);
             for (int f = 0; f < md->F; ++f) {
                 for (int s = 0; s < md->n[f]; ++s) v[s] = lam[qoff[f] + s] + logp[qoff[f] + s];
                 softmax(v, md->n[f]);
@@ -186,8 +228,9 @@ static void run_fpi(const orc_model *md, int a, int T, const int *obs, const int
     }
 }
 
-static void run_window(const orc_model *md, int algo, int a, int T, const int *obs, const int *act, int iters,
-                       double *q, const int *qoff, int ntot, double *work, const double *prior, double tau)
+static void run_window(const orc_model *md, int algo, int a, int T, const orc_obs *obs, const int *act, int iters,
+                       double *q, const int *qoff, int ntot, double *work, const double *prior, double tau,
+                       const size_t *poff, double *lls)
 {
     double *qn = work;                               /* [T][ntot] next iterate */
     double *lam = work + (size_t)T * ntot;            /* [T][ntot] */
@@ -196,8 +239,10 @@ static void run_window(const orc_model *md, int algo, int a, int T, const int *o
             for (int s = 0; s < md->n[f]; ++s) q[(size_t)t * ntot + qoff[f] + s] = 1.0 / md->n[f];
     for (int k = 0; k < iters; ++k) {
         for (int t = 0; t < T; ++t)
-            likelihood_messages(md, a, obs + (size_t)t * md->M, q + (size_t)t * ntot, qoff, ntot,
-                                lam + (size_t)t * ntot);
+        {
+            context_loglik(md, a, obs, t, poff, lls);
+            likelihood_messages(md, lls, poff, q + (size_t)t * ntot, qoff, ntot, lam + (size_t)t * ntot);
+        }
         for (int t = 0; t < T; ++t) {
             for (int f = 0; f < md->F; ++f) {
                 const int nf = md->n[f];
@@ -245,6 +290,64 @@ static void run_window(const orc_model *md, int algo, int a, int T, const int *o
     }
 }
 
+/* Shared driver of orc_infer_ex and orc_infer_soft: exactly one of hard
+ * ([b][T][M] outcomes) and soft ([b][T][sum K] observation vectors) is set. */
+static int run_all(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
+                   const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
+                   int b, int T, const int *hard, const double *soft, const int *act, const double *prior,
+                   double tau, int iters, double *q, int nthreads)
+{
+    if (algo < 0 || algo > 2 || F < 1 || M < 1 || b < 1 || T < 1 || iters < 1) return -1;
+    if (!(tau > 0.0 && tau <= 1.0)) return -1;
+    if (mb != 1 && mb != b) return -1;
+    if (!n || !U || !K || !dep_off || !dep || !A || !B || !D || !(hard || soft) || !q) return -1;
+    if (T > 1 && !act) return -1;
+    int ntot = 0;
+    int *qoff = (int *)malloc(sizeof(int) * (size_t)F);
+    int *koff = (int *)malloc(sizeof(int) * (size_t)M);
+    size_t *poff = (size_t *)malloc(sizeof(size_t) * (size_t)(M + 1));
+    if (!qoff || !koff || !poff) { free(qoff); free(koff); free(poff); return -1; }
+    int bad = 0, ksum = 0;
+    for (int f = 0; f < F; ++f) {
+        if (n[f] < 1 || U[f] < 1) bad = 1;
+        qoff[f] = ntot;
+        ntot += n[f];
+    }
+    orc_model md = {F, M, mb, n, U, K, dep_off, dep, A, B, D};
+    poff[0] = 0;
+    for (int m = 0; m < M && !bad; ++m) {
+        int k = dep_off[m + 1] - dep_off[m];
+        if (k < 1 || k > ORC_MAX_RANK || K[m] < 1) { bad = 1; break; }
+        for (int i = dep_off[m]; i < dep_off[m + 1]; ++i)
+            if (dep[i] < 0 || dep[i] >= F) bad = 1;
+        if (bad) break;
+        koff[m] = ksum;
+        ksum += K[m];
+        poff[m + 1] = poff[m] + slice_size(&md, m);
+    }
+    if (bad) { free(qoff); free(koff); free(poff); return -1; }
+    const size_t work_per = (size_t)(4 + 2 * T) * (size_t)ntot + poff[M];
+    const int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nt) reduction(| : bad)
+    for (int a = 0; a < b; ++a) {
+        double *work = (double *)malloc(sizeof(double) * work_per);
+        if (!work) { bad = 1; continue; }
+        double *lls = work + (size_t)(4 + 2 * T) * (size_t)ntot;
+        orc_obs ob = {hard ? hard + (size_t)a * T * M : NULL, soft ? soft + (size_t)a * T * ksum : NULL, koff, ksum};
+        const int *ua = T > 1 ? act + (size_t)a * (T - 1) * F : NULL;
+        double *qa = q + (size_t)a * T * ntot;
+        if (algo == ORC_FPI)
+            run_fpi(&md, a, T, &ob, ua, iters, qa, qoff, ntot, work, prior, tau, poff, lls);
+        else
+            run_window(&md, algo, a, T, &ob, ua, iters, qa, qoff, ntot, work, prior, tau, poff, lls);
+        free(work);
+    }
+    free(qoff);
+    free(koff);
+    free(poff);
+    return bad ? -1 : 0;
+}
+
 /*
  * Run `algo` (0 FPI, 1 VMP, 2 MMP) for b agents.  prior: NULL (p(s_1) = D)
  * or [b][sum n_f], each factor's block a distribution over its states; tau:
@@ -256,44 +359,24 @@ int orc_infer_ex(int algo, int F, const int *n, const int *U, int M, const int *
                  int b, int T, const int *obs, const int *act, const double *prior, double tau, int iters,
                  double *q, int nthreads)
 {
-    if (algo < 0 || algo > 2 || F < 1 || M < 1 || b < 1 || T < 1 || iters < 1) return -1;
-    if (!(tau > 0.0 && tau <= 1.0)) return -1;
-    if (mb != 1 && mb != b) return -1;
-    if (!n || !U || !K || !dep_off || !dep || !A || !B || !D || !obs || !q) return -1;
-    if (T > 1 && !act) return -1;
-    int ntot = 0;
-    int *qoff = (int *)malloc(sizeof(int) * (size_t)F);
-    if (!qoff) return -1;
-    for (int f = 0; f < F; ++f) {
-        if (n[f] < 1 || U[f] < 1) { free(qoff); return -1; }
-        qoff[f] = ntot;
-        ntot += n[f];
-    }
-    for (int m = 0; m < M; ++m) {
-        int k = dep_off[m + 1] - dep_off[m];
-        if (k < 1 || k > ORC_MAX_RANK || K[m] < 1) { free(qoff); return -1; }
-        for (int i = dep_off[m]; i < dep_off[m + 1]; ++i)
-            if (dep[i] < 0 || dep[i] >= F) { free(qoff); return -1; }
-    }
-    orc_model md = {F, M, mb, n, U, K, dep_off, dep, A, B, D};
-    const size_t work_per = (size_t)(4 + 2 * T) * (size_t)ntot;
-    int bad = 0;
-    const int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
-#pragma omp parallel for schedule(dynamic, 1) num_threads(nt) reduction(| : bad)
-    for (int a = 0; a < b; ++a) {
-        double *work = (double *)malloc(sizeof(double) * work_per);
-        if (!work) { bad = 1; continue; }
-        const int *oa = obs + (size_t)a * T * M;
-        const int *ua = T > 1 ? act + (size_t)a * (T - 1) * F : NULL;
-        double *qa = q + (size_t)a * T * ntot;
-        if (algo == ORC_FPI)
-            run_fpi(&md, a, T, oa, ua, iters, qa, qoff, ntot, work, prior, tau);
-        else
-            run_window(&md, algo, a, T, oa, ua, iters, qa, qoff, ntot, work, prior, tau);
-        free(work);
-    }
-    free(qoff);
-    return bad ? -1 : 0;
+    if (!obs) return -1;
+    return run_all(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, b, T, obs, NULL, act, prior, tau, iters, q,
+                   nthreads);
+}
+
+/*
+ * As orc_infer_ex with soft observations: obs_soft [b][T][sum K], the
+ * observation vector of modality m (a distribution over its K_m outcomes,
+ * one-hot for an integer outcome) at offset sum_{m' < m} K_m'.
+ */
+int orc_infer_soft(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
+                   const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
+                   int b, int T, const double *obs_soft, const int *act, const double *prior, double tau,
+                   int iters, double *q, int nthreads)
+{
+    if (!obs_soft) return -1;
+    return run_all(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, b, T, NULL, obs_soft, act, prior, tau, iters,
+                   q, nthreads);
 }
 
 int orc_infer_prior(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,

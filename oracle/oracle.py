@@ -56,6 +56,12 @@ def load_library(path: str):
                                  P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p), ctypes.c_int,
                                  ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_double),
                                  ctypes.c_double, ctypes.c_int, P(ctypes.c_double), ctypes.c_int]
+    lib.orc_infer_soft.restype = ctypes.c_int
+    lib.orc_infer_soft.argtypes = [ctypes.c_int, ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                   P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                   P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p), ctypes.c_int,
+                                   ctypes.c_int, P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double),
+                                   ctypes.c_double, ctypes.c_int, P(ctypes.c_double), ctypes.c_int]
     lib.orc_predict.restype = ctypes.c_int
     lib.orc_predict.argtypes = [ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int, P(ctypes.c_void_p),
                                 ctypes.c_int, P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double)]
@@ -84,19 +90,37 @@ def infer(algo: str, model, obs: np.ndarray, act: np.ndarray, iters: int,
           agents: Optional[Sequence[int]] = None, threads: int = 0, lib=None,
           prior: Optional[np.ndarray] = None, damping: float = 1.0) -> np.ndarray:
     """Posterior marginals q [b][T][sum n] (float64) of ``algo`` for every agent,
-    or for the listed ``agents`` only (agents are independent).  ``prior``:
-    [b][sum n] distributions over the first step, replacing D.  ``damping``:
-    step tau in (0, 1] of q <- (1 - tau) q + tau q_new (1 = plain update)."""
+    or for the listed ``agents`` only (agents are independent).  ``obs``: int
+    outcomes [b][T][M].  ``prior``: [b][sum n] distributions over the first
+    step, replacing D.  ``damping``: step tau in (0, 1] of
+    q <- (1 - tau) q + tau q_new (1 = plain update)."""
+    return _run(algo, model, obs, None, act, iters, agents, threads, lib, prior, damping)
+
+
+def infer_soft(algo: str, model, obs_soft: np.ndarray, act: np.ndarray, iters: int,
+               agents: Optional[Sequence[int]] = None, threads: int = 0, lib=None,
+               prior: Optional[np.ndarray] = None, damping: float = 1.0) -> np.ndarray:
+    """As ``infer`` with soft observations ``obs_soft`` [b][T][sum K]: modality
+    m's observation vector (a distribution over its outcomes) at offset
+    sum_{m' < m} K_m'."""
+    return _run(algo, model, None, obs_soft, act, iters, agents, threads, lib, prior, damping)
+
+
+def _run(algo, model, obs, obs_soft, act, iters, agents, threads, lib, prior, damping):
     if lib is None:
         lib = _load()
     if agents is not None:
         agents = list(agents)
         model = model.agent_slice(agents)
-        obs = obs[agents]
+        if obs is not None:
+            obs = obs[agents]
+        else:
+            obs_soft = obs_soft[agents]
         act = act[agents]
         if prior is not None:
             prior = np.asarray(prior)[agents]
-    b, T, M = obs.shape
+    b, T = (obs if obs is not None else obs_soft).shape[:2]
+    M = len(model.K)
     F = len(model.n)
     n, U, K = _i32(model.n), _i32(model.U), _i32(model.K)
     dep_off = _i32(np.cumsum([0] + [len(d) for d in model.deps]))
@@ -105,16 +129,24 @@ def infer(algo: str, model, obs: np.ndarray, act: np.ndarray, iters: int,
     B = [np.ascontiguousarray(x, dtype=np.float64) for x in model.B]
     D = [np.ascontiguousarray(x, dtype=np.float64) for x in model.D]
     ptrs = lambda arrs: (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])  # noqa: E731
-    obs_c = _i32(obs)
     act_c = _i32(act) if T > 1 else _i32(np.zeros((b, 1, F)))
     q = np.zeros((b, T, int(sum(model.n))), dtype=np.float64)
     ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))  # noqa: E731
     dp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))  # noqa: E731
-    if prior is None and damping == 1.0:
+    pr = None if prior is None else np.ascontiguousarray(prior, dtype=np.float64).reshape(b, int(sum(model.n)))
+    if obs_soft is not None:
+        os_c = np.ascontiguousarray(obs_soft, dtype=np.float64)
+        if os_c.shape != (b, T, int(sum(model.K))):
+            raise ValueError(f"soft observations of shape {os_c.shape}, expected {(b, T, int(sum(model.K)))}")
+        rc = lib.orc_infer_soft(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
+                                ptrs(A), ptrs(B), ptrs(D), b, T, dp(os_c), ip(act_c),
+                                None if pr is None else dp(pr), float(damping), int(iters), dp(q), int(threads))
+    elif prior is None and damping == 1.0:
+        obs_c = _i32(obs)
         rc = lib.orc_infer(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
                            ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c), int(iters), dp(q), int(threads))
     else:
-        pr = None if prior is None else np.ascontiguousarray(prior, dtype=np.float64).reshape(b, int(sum(model.n)))
+        obs_c = _i32(obs)
         rc = lib.orc_infer_ex(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
                               ptrs(A), ptrs(B), ptrs(D), b, T, ip(obs_c), ip(act_c),
                               None if pr is None else dp(pr), float(damping), int(iters), dp(q), int(threads))

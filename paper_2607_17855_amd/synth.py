@@ -199,6 +199,38 @@ def random_prior(rng: np.random.Generator, n: Sequence[int], b: int, alpha: floa
     return out
 
 
+def one_hot_obs(obs: np.ndarray, K: Sequence[int]) -> np.ndarray:
+    """Integer outcomes [b][T][M] as soft observation vectors, float32
+    [b][T][sum K] (modality m's one-hot block at sum_{m' < m} K_m')."""
+    b, T, M = obs.shape
+    out = np.zeros((b, T, int(sum(K))), dtype=np.float32)
+    k0 = 0
+    for m in range(M):
+        np.put_along_axis(out[:, :, k0:k0 + K[m]], obs[:, :, m:m + 1].astype(np.int64), 1.0, axis=2)
+        k0 += K[m]
+    return out
+
+
+def soft_obs(rng: np.random.Generator, obs: np.ndarray, K: Sequence[int], confidence: float = 0.7,
+             alpha: float = 1.0, p_hard: float = 0.0) -> np.ndarray:
+    """Soft observation vectors float32 [b][T][sum K] around integer outcomes:
+    each block puts `confidence` on the drawn outcome and spreads the rest as a
+    Dirichlet(alpha) draw over all outcomes (a noisy sensor's output); blocks
+    are one-hot at rate p_hard."""
+    b, T, M = obs.shape
+    hard = one_hot_obs(obs, K).astype(np.float64)
+    out = np.zeros_like(hard)
+    k0 = 0
+    for m in range(M):
+        km = K[m]
+        noise = rng.dirichlet(np.full(km, alpha), size=(b, T))
+        blk = confidence * hard[:, :, k0:k0 + km] + (1.0 - confidence) * noise
+        keep = rng.random((b, T, 1)) < p_hard
+        out[:, :, k0:k0 + km] = np.where(keep, hard[:, :, k0:k0 + km], blk)
+        k0 += km
+    return out.astype(np.float32)
+
+
 def _gather_col(a: np.ndarray, ai: np.ndarray, coords) -> np.ndarray:
     """a[ai[i], :, coords[0][i], coords[1][i], ...] for every i -> [b][K]."""
     k = a.shape[1]

@@ -25,9 +25,22 @@ def _agent(arr, mb, a):
     return np.asarray(arr[0 if mb == 1 else a], dtype=np.float64)
 
 
-def window_log_joint(model, obs_a, act_a, a):
+def obs_loglik(model, a, m, obs_t, soft=False):
+    """Observation term of modality m at one step, an array over s_dep:
+    log A_m[o] for an integer outcome, or for a soft observation (obs_t the
+    concatenated vectors [sum K]) its expectation sum_o w[o] log A_m[o]."""
+    LA = LN(_agent(model.A[m], model.mb, a))                   # [K][s_d1]..[s_dk]
+    if not soft:
+        return LA[obs_t[m]]
+    k0 = int(sum(model.K[:m]))
+    w = np.asarray(obs_t[k0:k0 + model.K[m]], dtype=np.float64)
+    return np.tensordot(w, LA, axes=(0, 0))
+
+
+def window_log_joint(model, obs_a, act_a, a, soft=False):
     """log p(o_{0:T-1}, s_{0:T-1} | u) of one agent as a dense array with one
-    axis per hidden variable (t, f), ordered t-major."""
+    axis per hidden variable (t, f), ordered t-major (with soft observations
+    obs_a is [T][sum K] and each observation term is obs_loglik's expectation)."""
     T = obs_a.shape[0]
     F = len(model.n)
     shape = [model.n[f] for t in range(T) for f in range(F)]
@@ -54,8 +67,7 @@ def window_log_joint(model, obs_a, act_a, a):
             lp = add(LN(Bf), [ax(t, f), ax(t - 1, f)])
     for t in range(T):
         for m, d in enumerate(model.deps):
-            Am = _agent(model.A[m], model.mb, a)[obs_a[t, m]]             # [s_d1]..[s_dk]
-            lp = add(LN(Am), [ax(t, f) for f in d])
+            lp = add(obs_loglik(model, a, m, obs_a[t], soft), [ax(t, f) for f in d])
     return lp
 
 
@@ -80,14 +92,14 @@ def softmax(v):
     return e / e.sum()
 
 
-def vmp_bruteforce(model, obs, act, iters):
+def vmp_bruteforce(model, obs, act, iters, soft=False):
     """Mean-field (Jacobi) coordinate updates over the enumerated window joint."""
     b, T, _ = obs.shape
     F = len(model.n)
     out = np.zeros((b, T, sum(model.n)))
     offs = np.cumsum([0] + list(model.n))
     for a in range(b):
-        lp = window_log_joint(model, obs[a], act[a] if T > 1 else None, a)
+        lp = window_log_joint(model, obs[a], act[a] if T > 1 else None, a, soft)
         q = [np.full(model.n[f], 1.0 / model.n[f]) for t in range(T) for f in range(F)]
         for _ in range(iters):
             q = [softmax(expected_given(lp, q, v)) for v in range(T * F)]
@@ -97,7 +109,7 @@ def vmp_bruteforce(model, obs, act, iters):
     return out
 
 
-def fpi_bruteforce(model, obs, act, iters):
+def fpi_bruteforce(model, obs, act, iters, soft=False):
     """Variational filtering: per time step, mean-field updates over the
     enumerated single-step joint  p(o_t | s_t) prod_f p_{t,f}(s_t^f), with the
     predictive prior p_{t,f} = B_f[u_{t-1}] q_{t-1,f} (D at t = 0)."""
@@ -119,7 +131,7 @@ def fpi_bruteforce(model, obs, act, iters):
                 view[f] = model.n[f]
                 lp = lp + LN(prior).reshape(view)
             for m, d in enumerate(model.deps):
-                Am = LN(_agent(model.A[m], model.mb, a)[obs[a, t, m]])
+                Am = obs_loglik(model, a, m, obs[a, t], soft)
                 view = [1] * F
                 for f in d:
                     view[f] = model.n[f]

@@ -395,6 +395,78 @@ def pin_damped_fixed_point(infer):
     return err
 
 
+def _soft_of(infer):
+    """The oracle's infer_soft() on the library that ``infer`` runs."""
+    import oracle
+    lib = getattr(infer, "keywords", {}).get("lib")
+    return lambda *args, **kw: oracle.infer_soft(*args, lib=lib, **kw)
+
+
+def pin_soft_onehot(infer):
+    """One-hot observation vectors are integer observations: the merged
+    log-likelihood sum_o o[o] log A[o] picks one slice (Sec. III-C, the
+    observation vector of the running example), so every algorithm must give
+    the integer-observation result exactly, on the same oracle."""
+    infer_soft = _soft_of(infer)
+    err = 0.0
+    for seed in range(4):
+        w = synth.random_small(400 + seed, F_max=3, n_max=4, M_max=3, K_max=4, T_max=4, b=3)
+        oh = synth.one_hot_obs(w.obs, w.model.K)
+        for algo in ("fpi", "vmp", "mmp"):
+            err = max(err, float(np.abs(infer_soft(algo, w.model, oh, w.act, w.iters) -
+                                        infer(algo, w.model, w.obs, w.act, w.iters)).max()))
+    return err
+
+
+def pin_soft_bruteforce(infer):
+    """Soft observations against enumeration: the observation term of the
+    joint becomes the expected log-likelihood sum_o w[o] log A[o, s_dep]
+    (computed by tensordot in the checker), and VMP / FPI are the mean-field
+    updates over that enumerated joint; MMP equals them for a single step."""
+    infer_soft = _soft_of(infer)
+    err = 0.0
+    for seed in range(6):
+        w = synth.random_small(420 + seed, F_max=3, n_max=4, M_max=3, K_max=4, T_max=3, b=2)
+        rng = np.random.Generator(np.random.PCG64(seed))
+        so = synth.soft_obs(rng, w.obs, w.model.K, confidence=0.5, p_hard=0.2).astype(np.float64)
+        err = max(err, float(np.abs(infer_soft("vmp", w.model, so, w.act, w.iters) -
+                                    bf.vmp_bruteforce(w.model, so, w.act, w.iters, soft=True)).max()))
+        err = max(err, float(np.abs(infer_soft("fpi", w.model, so, w.act, w.iters) -
+                                    bf.fpi_bruteforce(w.model, so, w.act, w.iters, soft=True)).max()))
+        ref1 = bf.vmp_bruteforce(w.model, so[:, :1], w.act[:, :0], w.iters, soft=True)
+        err = max(err, float(np.abs(infer_soft("mmp", w.model, so[:, :1], w.act[:, :0], w.iters) - ref1).max()))
+    return err
+
+
+def pin_soft_filter(infer):
+    """One factor with soft evidence: FPI is exact filtering with the
+    geometric likelihood L_t(s) = prod_m prod_o A_m[o, s]^(w_{t,m}[o])
+    (the exponential of the expected log-likelihood)."""
+    infer_soft = _soft_of(infer)
+    err = 0.0
+    for seed, K in [(51, (3,)), (52, (4, 2)), (53, (2, 5, 3))]:
+        model, obs, act = _hmm(seed, n=5, K=K, T=6, b=3)
+        rng = np.random.Generator(np.random.PCG64(seed))
+        so = synth.soft_obs(rng, obs, model.K, confidence=0.4).astype(np.float64)
+        q = infer_soft("fpi", model, so, act, 2)
+        for a in range(obs.shape[0]):
+            B = np.float64(model.B[0][a])
+            pred = np.float64(model.D[0][a])
+            for t in range(obs.shape[1]):
+                lik = np.ones(5)
+                k0 = 0
+                for m, A in enumerate(model.A):
+                    Aa = np.float64(A[a])                        # [K][n]
+                    wv = so[a, t, k0:k0 + model.K[m]]
+                    lik = lik * np.prod(Aa ** wv[:, None], axis=0)
+                    k0 += model.K[m]
+                post = lik * pred / (lik * pred).sum()
+                err = max(err, float(np.abs(q[a, t] - post).max()))
+                if t + 1 < obs.shape[1]:
+                    pred = B[:, :, act[a, t, 0]] @ post
+    return err
+
+
 ALL_PINS = {
     "bayes_filter": (pin_bayes_filter, 1e-12),
     "golden_hmm2": (pin_golden_hmm2, 1e-7),
@@ -410,4 +482,7 @@ ALL_PINS = {
     "damped_filter": (pin_damped_filter, 1e-12),
     "damped_iid": (pin_damped_iid, 1e-12),
     "damped_fixed_point": (pin_damped_fixed_point, 1e-10),
+    "soft_onehot": (pin_soft_onehot, 0.0),
+    "soft_bruteforce": (pin_soft_bruteforce, 1e-12),
+    "soft_filter": (pin_soft_filter, 1e-12),
 }

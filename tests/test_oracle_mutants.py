@@ -35,6 +35,10 @@ MUTANTS = [
      "p += Bf[((size_t)j * nf + i) * U[f] + u] * q[(size_t)a * ntot + off + j];", 1),
     ("damping_swapped", "(1.0 - tau) * q[s] + tau * q_new[s]", "tau * q[s] + (1.0 - tau) * q_new[s]", 1),
     ("damping_ignored", "q[s] = tau == 1.0 ? q_new[s] :", "q[s] = 1 ? q_new[s] :", 1),
+    ("soft_weight_dropped", "v += om[o] * LN(Am[(size_t)o * P + e]);", "v += LN(Am[(size_t)o * P + e]);", 1),
+    ("soft_block_offset", "ob->soft + (size_t)t * ob->ksum + ob->koff[m];", "ob->soft + (size_t)t * ob->ksum;", 1),
+    ("soft_outcome_axis", "v += om[o] * LN(Am[(size_t)o * P + e]);", "v += om[o] * LN(Am[(size_t)o + e * md->K[m]]);",
+     1),
     ("softmax_sign", "v[i] = exp(v[i] - mx);", "v[i] = exp(mx - v[i]);", 1),
     ("no_log_clamp", "return log(x > ORC_EPS ? x : ORC_EPS);", "return log(x > 0 ? x : 1e-300);", 1),
 ]

@@ -251,6 +251,27 @@ int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const in
              size_t ws_bytes, void *hip_stream);
 
 /*
+ * Soft observations (Sec. III-C: the log-likelihood of a modality is the
+ * contraction log(A_m) . o_m of its A-array with an observation vector).
+ * Instead of integer outcomes, every context carries one vector per modality:
+ *   obs_dev: device fp32 [b][T][sum_m K_m], modality m's vector over its K_m
+ *            outcomes at offset sum_{m' < m} K_m' (a distribution, e.g. a
+ *            noisy sensor's output; one-hot reproduces the integer call).
+ * Every log A_m[o_{t,m}, s_dep] in the updates above becomes the expected
+ * log-likelihood sum_o o_{t,m}[o] log A_m[o, s_dep], formed once per call
+ * (before the iterations) in the workspace:
+ *   ws_bytes >= bi_workspace_size_soft(model, b, T, algo), 256-byte aligned
+ *   (b * T * sum_m prod_{f in dep(m)} n_f doubles, the slices padded as in
+ *   the packed model).
+ * algo, opts and the other arguments are those of bi_infer; the same errors.
+ * Any packed layout works (the dense fp64 planes are used).
+ */
+int bi_workspace_size_soft(const bi_model *model, int32_t b, int32_t T, int32_t algo, size_t *bytes);
+int bi_infer_soft(const bi_model *model, int32_t algo, int32_t b, int32_t T, const float *obs_dev,
+                  const int32_t *act_dev, int32_t iters, const bi_infer_opts *opts, float *q_dev, void *ws_dev,
+                  size_t ws_bytes, void *hip_stream);
+
+/*
  * Predictive prior of the next step (the product FPI uses between steps,
  * Sec. III-B transition model): for every agent a and factor f
  *   out[a][f](i) = sum_j B_f[i][j][u_{a,f}] q[a][f](j)      (fp64 sums)

@@ -30,7 +30,7 @@ ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
 
 EXPORTS = ("bi_last_error", "bi_plan_model", "bi_plan_model_exact", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
            "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_vfilter_prior",
-           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_predict", "bi_free_model",
+           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_workspace_size_soft", "bi_infer_soft", "bi_predict", "bi_free_model",
            "bi_profile_begin", "bi_profile_end")
 
 
@@ -87,6 +87,8 @@ def load(path: str = LIB_PATH):
     for name in ("bi_vfilter_prior", "bi_vmp_prior", "bi_mmp_prior"):
         getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, sz, vp]
     lib.bi_infer.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp, sz, vp]
+    lib.bi_workspace_size_soft.argtypes = [vp, i32, i32, i32, P(sz)]
+    lib.bi_infer_soft.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp, sz, vp]
     lib.bi_predict.argtypes = [vp, i32, vp, ctypes.c_int64, vp, ctypes.c_int64, vp, vp]
     lib.bi_free_model.argtypes = [vp]
     lib.bi_free_model.restype = None
@@ -250,6 +252,25 @@ def bi_infer(handle, algo: int, b, T, obs, act, iters, q, ws=None, stream=None, 
                            ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(_stream_ptr(stream))))
 
 
+def bi_workspace_size_soft(handle: int, b: int, T: int, algo: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().bi_workspace_size_soft(ctypes.c_void_p(handle), int(b), int(T), int(algo), ctypes.byref(out)))
+    return int(out.value)
+
+
+def bi_infer_soft(handle, algo: int, b, T, obs_soft, act, iters, q, ws, stream=None, prior=None,
+                  damping: float = 1.0):
+    """Soft observations obs_soft [b][T][sum K] float32 (device)."""
+    ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    act_ptr = act.data_ptr() if act is not None and act.numel() > 0 else 0
+    opts = bi_infer_opts(ctypes.c_void_p(prior.data_ptr() if prior is not None else 0), float(damping))
+    _check(load().bi_infer_soft(ctypes.c_void_p(handle), int(algo), int(b), int(T),
+                                ctypes.c_void_p(obs_soft.data_ptr()), ctypes.c_void_p(act_ptr), int(iters),
+                                ctypes.byref(opts), ctypes.c_void_p(q.data_ptr()),
+                                ctypes.c_void_p(ws.data_ptr() if ws is not None else 0), ws_bytes,
+                                ctypes.c_void_p(_stream_ptr(stream))))
+
+
 def bi_predict(handle, b, q, q_stride, act, act_stride, out, stream=None):
     """out[a] = B[:, :, act[a]] q[a] per factor; q / act rows at a * q_stride / a * act_stride elements."""
     _check(load().bi_predict(ctypes.c_void_p(handle), int(b), ctypes.c_void_p(q.data_ptr()), int(q_stride),
@@ -316,6 +337,27 @@ class PackedModel:
             _ENTRY[algo](self.handle, b, T, obs, act, iters, q, ws, stream)
         else:
             _ENTRY_PRIOR[algo](self.handle, b, T, obs, act, prior, iters, q, ws, stream)
+        return q
+
+    def workspace_soft(self, b: int, T: int, algo: str):
+        import torch
+        nb = bi_workspace_size_soft(self.handle, b, T, ALGO_IDS[algo])
+        return torch.empty(nb, dtype=torch.uint8, device=self.buf.device)
+
+    def infer_soft(self, algo: str, obs_soft, act, iters: int, q=None, ws=None, stream=None, prior=None,
+                   damping: float = 1.0):
+        """obs_soft [b][T][sum K] float32 / act [b][T-1][F] int32 device tensors -> q [b][T][sum n]."""
+        import torch
+        b, T = int(obs_soft.shape[0]), int(obs_soft.shape[1])
+        if obs_soft.dtype != torch.float32 or not obs_soft.is_contiguous():
+            raise ValueError("obs_soft must be a contiguous float32 tensor")
+        if int(obs_soft.shape[2]) != sum(self.model.K):
+            raise ValueError(f"obs_soft has {int(obs_soft.shape[2])} values per step, expected {sum(self.model.K)}")
+        if q is None:
+            q = torch.empty((b, T, sum(self.model.n)), dtype=torch.float32, device=self.buf.device)
+        if ws is None:
+            ws = self.workspace_soft(b, T, algo)
+        bi_infer_soft(self.handle, ALGO_IDS[algo], b, T, obs_soft, act, iters, q, ws, stream, prior, damping)
         return q
 
     def predict(self, q, act, out=None, stream=None):

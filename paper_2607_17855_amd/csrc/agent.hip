@@ -47,7 +47,9 @@ struct AgentArgs {
     int stage;             // StageMode
     int sctx, sraw;        // staged values per context (padded), unpadded values per context
     int po[kStageMaxM + 1], pr[kStageMaxM + 1];
-    const int32_t *obs;
+    const int32_t *obs;    // integer outcomes [agent][T][M], or NULL with ll
+    const double *ll;      // soft observations: log-likelihood tensors [agent][T][llpc] (soft.hip)
+    int64_t llpc;
     const int32_t *act;
     const float *prior;    // optional [agent][ntot] prior of the first step (replaces D)
     double tau;            // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
@@ -140,9 +142,15 @@ __device__ void stage_slices(const AgentArgs &a, int agent, int t0, int nc, doub
                 while (m + 1 < a.M && a.pr[m + 1] <= rem) ++m;
                 const ModDesc &md = a.mods[m];
                 const int e = rem - a.pr[m], r = e / md.Cp, col = e - r * md.Cp;
-                const int o = a.obs[((int64_t)agent * a.T + t0 + c) * a.M + m];
-                const double *X = at<double>(a.base, md.la_off) + (a.shared ? 0 : (int64_t)agent * md.la_agent) +
-                                  (int64_t)o * md.slice;
+                const int64_t ctx = (int64_t)agent * a.T + t0 + c;
+                const double *X;
+                if (a.ll) {
+                    X = a.ll + ctx * a.llpc + a.pr[m];
+                } else {
+                    const int o = a.obs[ctx * a.M + m];
+                    X = at<double>(a.base, md.la_off) + (a.shared ? 0 : (int64_t)agent * md.la_agent) +
+                        (int64_t)o * md.slice;
+                }
                 v[u] = X[e];
                 dst[u] = c * a.sctx + a.po[m] + r * (md.Cp + 1) + col;
             }
@@ -162,6 +170,7 @@ __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const do
 {
     const int tid = threadIdx.x;
     int base = 0;
+    int64_t llo = 0;   // offset of modality m in a context's log-likelihood tensors
     for (int m = 0; m < a.M; ++m) {
         const ModDesc &md = a.mods[m];
         const int R = md.R, C = md.C, Cp = md.Cp;
@@ -177,6 +186,8 @@ __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const do
             double acc;
             if (stg) {
                 acc = zv_one(a, md, stg + (int64_t)(sc0 + c) * a.sctx + a.po[m], Cp + 1, qt, j);
+            } else if (a.ll) {
+                acc = zv_one(a, md, a.ll + ((int64_t)agent * a.T + t) * a.llpc + llo, Cp, qt, j);
             } else {
                 const int o = a.obs[((int64_t)agent * a.T + t) * a.M + m];
                 acc = zv_one(a, md, la + (int64_t)o * md.slice, Cp, qt, j);
@@ -184,6 +195,7 @@ __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const do
             zv[c * a.zvpc + md.zv_off + j] = acc;
         }
         base += cnt;
+        llo += md.slice;
     }
 }
 
@@ -443,8 +455,8 @@ constexpr size_t kLdsMax = 160 * 1024;
 
 }  // namespace
 
-int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
-                 const float *prior, double tau, int iters, float *q, hipStream_t stream)
+int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const double *ll,
+                 const int32_t *act, const float *prior, double tau, int iters, float *q, hipStream_t stream)
 {
     AgentArgs a;
     a.base = m->dev;
@@ -458,6 +470,9 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     a.ntot = m->ntot;
     a.zvpc = m->zvpc;
     a.obs = obs;
+    a.ll = ll;
+    a.llpc = 0;
+    for (const ModDesc &md : m->mods) a.llpc += md.slice;
     a.act = act;
     a.prior = prior;
     a.tau = tau;

@@ -231,7 +231,7 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
         const Path p = choose_path(model, algo);
         if (p != Path::Agent)
             return bi::launch_stream(model, algo, b, T, obs, act, prior, tau, iters, q, ws, s, p == Path::Sparse);
-        return bi::launch_agent(model, algo, b, T, obs, act, prior, tau, iters, q, s);
+        return bi::launch_agent(model, algo, b, T, obs, nullptr, act, prior, tau, iters, q, s);
     } catch (...) {
         return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
     }
@@ -287,6 +287,51 @@ int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const in
     const float *prior = opts ? opts->prior_dev : nullptr;
     const double tau = opts ? opts->damping : 1.0;
     return infer(algo, model, b, T, obs_dev, act_dev, prior, tau, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_workspace_size_soft(const bi_model *model, int32_t b, int32_t T, int32_t algo, size_t *bytes)
+{
+    if (!model || !bytes) return fail(BI_ERR_INVALID_ARG, "model and bytes must be non-NULL");
+    if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
+    if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
+    const int64_t vals = bi::soft_values_per_context(model);
+    if (vals > (INT64_MAX / 8) / ((int64_t)b * T))
+        return fail(BI_ERR_UNSUPPORTED, "soft log-likelihood tensors of b=%d T=%d overflow", b, T);
+    *bytes = (size_t)bi::align_up((int64_t)b * T * vals * 8, bi::kAlign);
+    return BI_OK;
+}
+
+int bi_infer_soft(const bi_model *model, int32_t algo, int32_t b, int32_t T, const float *obs_dev,
+                  const int32_t *act_dev, int32_t iters, const bi_infer_opts *opts, float *q_dev, void *ws_dev,
+                  size_t ws_bytes, void *hip_stream)
+{
+    try {
+        if (!model) return fail(BI_ERR_INVALID_ARG, "model is NULL");
+        if (!model->dev) return fail(BI_ERR_INVALID_ARG, "model has no device buffer (bi_attach_device_buffer)");
+        if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
+        if (b < 1 || T < 1 || iters < 1) return fail(BI_ERR_INVALID_ARG, "b, T and iters must be >= 1");
+        if (model->mb != 1 && model->mb != b)
+            return fail(BI_ERR_SHAPE, "b=%d but the model holds %d agents", b, model->mb);
+        if (!obs_dev || !q_dev) return fail(BI_ERR_INVALID_ARG, "obs and q must be non-NULL");
+        if (T > 1 && !act_dev) return fail(BI_ERR_INVALID_ARG, "act must be non-NULL when T > 1");
+        const float *prior = opts ? opts->prior_dev : nullptr;
+        const double tau = opts ? opts->damping : 1.0;
+        if (!(tau > 0.0 && tau <= 1.0)) return fail(BI_ERR_INVALID_ARG, "damping %g is not in (0, 1]", tau);
+        size_t need = 0;
+        int rc = bi_workspace_size_soft(model, b, T, algo, &need);
+        if (rc != BI_OK) return rc;
+        if (ws_bytes < need) return fail(BI_ERR_BUFFER_TOO_SMALL, "ws_bytes %zu < %zu required", ws_bytes, need);
+        if (!ws_dev) return fail(BI_ERR_INVALID_ARG, "ws is NULL");
+        if (reinterpret_cast<uintptr_t>(ws_dev) % bi::kAlign)
+            return fail(BI_ERR_INVALID_ARG, "ws must be %d-byte aligned", bi::kAlign);
+        hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+        double *ll = reinterpret_cast<double *>(ws_dev);
+        rc = bi::launch_soft_ll(model, b, T, obs_dev, ll, s);
+        if (rc != BI_OK) return rc;
+        return bi::launch_agent(model, algo, b, T, nullptr, ll, act_dev, prior, tau, iters, q_dev, s);
+    } catch (...) {
+        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
+    }
 }
 
 int bi_predict(const bi_model *model, int32_t b, const float *q_dev, int64_t q_stride, const int32_t *act_dev,

@@ -39,9 +39,16 @@ int plan(const bi_model_desc *desc, bi_model *m, const float *const *A = nullptr
 // Agent-resident launches (one workgroup per agent, every iteration in-kernel).
 // Returns BI_OK or an error code.
 // `prior` (nullable, device fp32 [b][ntot]) replaces D at the first step;
-// `tau` in (0, 1] damps every update: q <- (1 - tau) q + tau q_new.
-int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
-                 const float *prior, double tau, int iters, float *q, hipStream_t stream);
+// `tau` in (0, 1] damps every update: q <- (1 - tau) q + tau q_new.  With
+// soft observations obs is NULL and ll holds every context's log-likelihood
+// tensors (launch_soft_ll).
+int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const double *ll,
+                 const int32_t *act, const float *prior, double tau, int iters, float *q, hipStream_t stream);
+
+// Soft observations (soft.hip): values per context of the log-likelihood
+// tensors, and the launch that forms them from w [b][T][sum K].
+int64_t soft_values_per_context(const bi_model *m);
+int launch_soft_ll(const bi_model *m, int b, int T, const float *w, double *ll, hipStream_t stream);
 
 // Predictive prior B_f[:, :, u] q for every agent and factor (predict.hip).
 int launch_predict(const bi_model *m, int b, const float *q, int64_t q_stride, const int32_t *act,

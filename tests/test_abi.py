@@ -181,6 +181,25 @@ def test_inference_validates_on_host_before_launch():
         assert bi_(ctypes.c_void_p(h), 1, 3, 2, fake, fake, 3, ctypes.byref(opts), fake, None, 0, None) == \
             bi.BI_ERR_SHAPE
         assert bi_(ctypes.c_void_p(h), 1, 2, 2, fake, fake, 3, None, None, None, 0, None) == bi.BI_ERR_INVALID_ARG
+        # soft observations: same argument checks, own workspace size
+        si = lib.bi_infer_soft
+        assert si(ctypes.c_void_p(h), 1, 3, 2, fake, fake, 3, None, fake, fake, 1 << 30, None) == bi.BI_ERR_SHAPE
+        assert si(ctypes.c_void_p(h), 5, 2, 2, fake, fake, 3, None, fake, fake, 1 << 30, None) == \
+            bi.BI_ERR_INVALID_ARG
+        assert si(ctypes.c_void_p(h), 1, 2, 2, None, fake, 3, None, fake, fake, 1 << 30, None) == \
+            bi.BI_ERR_INVALID_ARG
+        assert si(ctypes.c_void_p(h), 1, 2, 2, fake, None, 3, None, fake, fake, 1 << 30, None) == \
+            bi.BI_ERR_INVALID_ARG
+        assert si(ctypes.c_void_p(h), 1, 2, 2, fake, fake, 3, None, fake, fake, 16, None) == \
+            bi.BI_ERR_BUFFER_TOO_SMALL
+        assert si(ctypes.c_void_p(h), 1, 2, 2, fake, fake, 3, None, fake, None, 1 << 30, None) == \
+            bi.BI_ERR_INVALID_ARG
+        opts = bi.bi_infer_opts(None, 2.0)
+        assert si(ctypes.c_void_p(h), 1, 2, 2, fake, fake, 3, ctypes.byref(opts), fake, fake, 1 << 30, None) == \
+            bi.BI_ERR_INVALID_ARG
+        mods, _ = _descs(img, m.M, m.F)
+        per_ctx = sum(int(mods[i].slice) for i in range(m.M))
+        assert bi.bi_workspace_size_soft(h, 2, 3, 0) == -(-2 * 3 * per_ctx * 8 // 256) * 256
         ntot, F = sum(m.n), m.F
         pr = lib.bi_predict
         assert pr(None, 2, fake, ntot, fake, F, fake, None) == bi.BI_ERR_INVALID_ARG

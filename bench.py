@@ -20,7 +20,9 @@ on one layout.
 kernels, one model per agent): vmp_2f (F=2 factors of 8 and 6 states, M=3
 modalities on both, T=10, b=1024, VMP), mmp_3f (F=3 of 12/10/8 states, M=4 x
 16 outcomes on random factor subsets, T=20, b=4096, MMP), fpi_hmm (one
-4-state factor, T=8, b=1, FPI).
+4-state factor, T=8, b=1, FPI).  --soft runs such a workload with soft
+observation vectors (each puts 0.7 on the sampled outcome and spreads the
+rest as a Dirichlet(1) draw) through bi_infer_soft.
 """
 import argparse
 import hashlib
@@ -106,7 +108,16 @@ def agent_work(model, T, algo):
 AGENT_WORKLOADS = {"vmp_2f": ("config2", "vmp"), "mmp_3f": ("config3", "mmp"), "fpi_hmm": ("config1", "fpi")}
 
 
-def cpu_baseline(w, algos, budget_s: float = 25.0):
+def soft_ll_bytes(model, b, T):
+    """Algorithmic HBM bytes of one soft log-likelihood launch: the fp64
+    slices of every outcome read once per agent (once in all for a shared
+    model) and T expected log-likelihood tensors written per agent."""
+    P = slice_sizes(model)
+    reads = sum(8.0 * k * p for k, p in zip(model.K, P)) * (1 if model.mb == 1 else b)
+    return reads + 8.0 * b * T * sum(P)
+
+
+def cpu_baseline(w, algos, budget_s: float = 25.0, soft=None):
     import numpy as np
     import oracle
     threads = oracle.default_threads()
@@ -116,7 +127,10 @@ def cpu_baseline(w, algos, budget_s: float = 25.0):
     done_bu = 0
     calls = 0
     for algo in algos:
-        oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=agents)
+        if soft is None:
+            oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=agents)
+        else:
+            oracle.infer_soft(algo, w.model, soft, w.act, w.iters, agents=agents)
         done_bu += len(agents) * w.T * w.iters
         calls += 1
         if time.perf_counter() - t0 > budget_s:
@@ -125,7 +139,8 @@ def cpu_baseline(w, algos, budget_s: float = 25.0):
     return {"value": done_bu / dt, "unit": "belief_updates/s", "cores": min(threads, len(agents)),
             "kind": "oracle",
             "sample": f"{len(agents)} of {w.b} agents x T={w.T} x {w.iters} iters, "
-                      f"{'+'.join(algos[:calls])}, fp64 looped oracle (layout-independent), {dt:.1f} s wall"}
+                      f"{'+'.join(algos[:calls])}{' (soft observations)' if soft is not None else ''}, "
+                      f"fp64 looped oracle (layout-independent), {dt:.1f} s wall"}
 
 
 def load_traffic():
@@ -143,6 +158,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layouts", default=",".join(LAYOUTS), help="comma list of A layouts in a step")
     ap.add_argument("--workload", default="large", choices=["large"] + list(AGENT_WORKLOADS))
+    ap.add_argument("--soft", action="store_true", help="soft observation vectors (per-agent workloads)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a device-to-device copy of MIB MiB (reference kernel for HBM byte counters)")
     args = ap.parse_args()
@@ -161,6 +177,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.workload != "large":
         return bench_agent(args, bi, synth, torch, dev)
+    if args.soft:
+        print("bench.py: --soft applies to the per-agent workloads (--workload)", file=sys.stderr)
+        sys.exit(2)
     w = synth.config5()
     flags = {"dense": bi.BI_DENSE_A | bi.BI_FAST_F32, "sparse": bi.BI_SPARSE_A}
     pms = {lay: bi.PackedModel(w.model, flags=flags[lay], device=dev) for lay in layouts}
@@ -272,9 +291,18 @@ def bench_agent(args, bi, synth, torch, dev):
     q = torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
     assert pm.workspace(w.b, w.T, algo) is None, "per-agent workloads run on the agent-resident kernels"
+    soft_np = None
+    if args.soft:
+        import numpy as np
+        soft_np = synth.soft_obs(np.random.Generator(np.random.PCG64(17855)), w.obs, w.model.K, confidence=0.7)
+        soft_dev = torch.from_numpy(soft_np).to(dev)
+        ws = pm.workspace_soft(w.b, w.T, algo)
 
     def step():
-        pm.infer(algo, obs, act, w.iters, q=q, stream=stream)
+        if soft_np is not None:
+            pm.infer_soft(algo, soft_dev, act, w.iters, q=q, ws=ws, stream=stream)
+        else:
+            pm.infer(algo, obs, act, w.iters, q=q, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -302,8 +330,9 @@ def bench_agent(args, bi, synth, torch, dev):
         "metric": METRIC, "value": bu / (ms_step / 1e3), "unit": "belief_updates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
-        "config": {"workload": f"{w.name}: per-agent models, {algo.upper()} x{w.iters}", "b": w.b, "T": w.T,
-                   "iters": w.iters, "algos": [algo]},
+        "config": {"workload": f"{w.name}: per-agent models, {algo.upper()} x{w.iters}"
+                               + (", soft observations" if soft_np is not None else ""),
+                   "b": w.b, "T": w.T, "iters": w.iters, "algos": [algo], "soft": soft_np is not None},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP64_VALU_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP64_VALU_TFLOPS, "traffic": None, "kernel": cls + "_kernel",
                      "avg_launch_ms": avg_ms, "launches": launches, "algorithmic_flops_per_launch": flops,
@@ -311,8 +340,20 @@ def bench_agent(args, bi, synth, torch, dev):
         "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
         "wall_s_timed": wall,
     }
+    if soft_np is not None:
+        sl, sms = prof["soft_ll"]
+        s_avg = sms / max(sl, 1)
+        s_bytes = soft_ll_bytes(w.model, w.b, w.T)
+        s_ach = s_bytes / (s_avg / 1e3) / 1e9
+        out["roofline_all"] = {
+            cls: dict(out["roofline"]),
+            "soft_ll": {"bound": "hbm", "achieved": s_ach, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                        "frac": s_ach / PEAK_HBM_GBPS, "traffic": None, "kernel": "soft_ll_kernel",
+                        "avg_launch_ms": s_avg, "launches": sl, "algorithmic_bytes_per_launch": s_bytes}}
+        if s_avg > avg_ms:
+            out["roofline"] = out["roofline_all"]["soft_ll"]
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, [algo])
+        out["cpu_baseline"] = cpu_baseline(w, [algo], soft=soft_np)
     print(json.dumps(out), flush=True)
 
 

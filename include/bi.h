@@ -57,6 +57,14 @@ extern "C" {
  * marginals are insensitive to fp32 rounding of the log-likelihoods; it
  * stores an extra fp32 copy of the slices. */
 #define BI_FAST_F32 4u
+/* Input checking.  Out-of-range observations or actions are undefined
+ * behaviour by default.  With BI_CHECK every inference call first scans obs
+ * and act on the device, synchronises its stream and returns
+ * BI_ERR_INVALID_ARG (naming the first bad entry, bi_last_error) before any
+ * inference kernel runs; the workspace sizes grow by 256 bytes for the check's
+ * status words, and such calls cannot be captured in a HIP graph.
+ * bi_predict is not checked. */
+#define BI_CHECK 8u
 
 /* Algorithm ids (bi_workspace_size). */
 #define BI_ALGO_FPI 0

@@ -19,6 +19,9 @@ namespace {
 
 enum class Path { Agent, Stream, Sparse };
 
+// BI_CHECK: status words of the input check, after the call's own workspace
+constexpr size_t kStatusBytes = 256;
+
 // Dispatch: a model packed with the sparse layout (shared by every agent)
 // runs VMP / MMP on the sparse streaming kernels; the dense streaming kernels
 // serve large shared models when the caller opted into fp32 contractions;
@@ -205,6 +208,7 @@ int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo,
     if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
     const Path p = choose_path(model, algo);
     *bytes = p == Path::Agent ? 0 : bi::stream_workspace(model, b, T, p == Path::Sparse);
+    if (model->flags & BI_CHECK) *bytes = (size_t)bi::align_up((int64_t)*bytes, bi::kAlign) + kStatusBytes;
     return BI_OK;
 }
 
@@ -228,6 +232,11 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
         if (need > 0 && reinterpret_cast<uintptr_t>(ws) % bi::kAlign)
             return fail(BI_ERR_INVALID_ARG, "ws must be %d-byte aligned", bi::kAlign);
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        if (model->flags & BI_CHECK) {
+            rc = bi::check_inputs(model, b, T, obs, act,
+                                  reinterpret_cast<int32_t *>(static_cast<char *>(ws) + need - kStatusBytes), s);
+            if (rc != BI_OK) return rc;
+        }
         const Path p = choose_path(model, algo);
         if (p != Path::Agent)
             return bi::launch_stream(model, algo, b, T, obs, act, prior, tau, iters, q, ws, s, p == Path::Sparse);
@@ -298,6 +307,7 @@ int bi_workspace_size_soft(const bi_model *model, int32_t b, int32_t T, int32_t 
     if (vals > (INT64_MAX / 8) / ((int64_t)b * T))
         return fail(BI_ERR_UNSUPPORTED, "soft log-likelihood tensors of b=%d T=%d overflow", b, T);
     *bytes = (size_t)bi::align_up((int64_t)b * T * vals * 8, bi::kAlign);
+    if (model->flags & BI_CHECK) *bytes += kStatusBytes;
     return BI_OK;
 }
 
@@ -325,6 +335,11 @@ int bi_infer_soft(const bi_model *model, int32_t algo, int32_t b, int32_t T, con
         if (reinterpret_cast<uintptr_t>(ws_dev) % bi::kAlign)
             return fail(BI_ERR_INVALID_ARG, "ws must be %d-byte aligned", bi::kAlign);
         hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+        if (model->flags & BI_CHECK) {
+            rc = bi::check_inputs(model, b, T, nullptr, act_dev,
+                                  reinterpret_cast<int32_t *>(static_cast<char *>(ws_dev) + need - kStatusBytes), s);
+            if (rc != BI_OK) return rc;
+        }
         double *ll = reinterpret_cast<double *>(ws_dev);
         rc = bi::launch_soft_ll(model, b, T, obs_dev, ll, s);
         if (rc != BI_OK) return rc;

@@ -50,6 +50,12 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
 int64_t soft_values_per_context(const bi_model *m);
 int launch_soft_ll(const bi_model *m, int b, int T, const float *w, double *ll, hipStream_t stream);
 
+// BI_CHECK (check.hip): scan obs (may be NULL) and act for out-of-range
+// values, using 3 int32 status words of device memory; synchronises `stream`.
+// Returns BI_OK or BI_ERR_INVALID_ARG naming the first offending entry.
+int check_inputs(const bi_model *m, int b, int T, const int32_t *obs, const int32_t *act, int32_t *status,
+                 hipStream_t stream);
+
 // Predictive prior B_f[:, :, u] q for every agent and factor (predict.hip).
 int launch_predict(const bi_model *m, int b, const float *q, int64_t q_stride, const int32_t *act,
                    int64_t act_stride, float *out, hipStream_t stream);

@@ -46,7 +46,7 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
         return fail(BI_ERR_INVALID_ARG, "desc has a NULL array");
     if (d->model_batch < 1) return fail(BI_ERR_INVALID_ARG, "model_batch must be >= 1");
     uint32_t flags = d->flags ? d->flags : BI_DENSE_A;
-    if ((flags & ~(BI_DENSE_A | BI_SPARSE_A | BI_FAST_F32)) != 0)
+    if ((flags & ~(BI_DENSE_A | BI_SPARSE_A | BI_FAST_F32 | BI_CHECK)) != 0)
         return fail(BI_ERR_INVALID_ARG, "unknown bits in flags");
     if ((flags & (BI_DENSE_A | BI_SPARSE_A)) == 0) flags |= BI_DENSE_A;
     if ((flags & BI_DENSE_A) && (flags & BI_SPARSE_A))

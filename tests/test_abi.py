@@ -278,6 +278,33 @@ def test_host_pack_sparse_planes(seed):
         bi.bi_free_model(h)
 
 
+def test_check_flag_adds_status_words_to_every_workspace():
+    w = synth.random_small(7, b=2, per_agent=True)
+    m = w.model
+    h0, _ = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, m.mb, m.A, m.B, m.D)
+    h1, _ = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, m.mb, m.A, m.B, m.D, flags=bi.BI_DENSE_A | bi.BI_CHECK)
+    try:
+        for algo in range(3):
+            assert bi.bi_workspace_size(h0, 2, 3, algo) == 0            # agent-resident: none
+            assert bi.bi_workspace_size(h1, 2, 3, algo) == 256          # the check's status words
+            assert bi.bi_workspace_size_soft(h1, 2, 3, algo) == bi.bi_workspace_size_soft(h0, 2, 3, algo) + 256
+    finally:
+        bi.bi_free_model(h0)
+        bi.bi_free_model(h1)
+    # a shared model on the streaming kernels: its workspace plus the status words
+    ms = synth.make_model(np.random.Generator(np.random.PCG64(8)), [32, 32, 16], [1, 1, 1], [3], [[0, 1, 2]], 1)
+    fl = bi.BI_DENSE_A | bi.BI_FAST_F32
+    h0, _ = bi.bi_pack_model_host(ms.n, ms.U, ms.K, ms.deps, 1, ms.A, ms.B, ms.D, flags=fl)
+    h1, _ = bi.bi_pack_model_host(ms.n, ms.U, ms.K, ms.deps, 1, ms.A, ms.B, ms.D, flags=fl | bi.BI_CHECK)
+    try:
+        n0 = bi.bi_workspace_size(h0, 4, 3, 1)
+        assert n0 > 0
+        assert bi.bi_workspace_size(h1, 4, 3, 1) == -(-n0 // 256) * 256 + 256
+    finally:
+        bi.bi_free_model(h0)
+        bi.bi_free_model(h1)
+
+
 def test_sparse_layout_needs_a_shared_model():
     with pytest.raises(bi.BiError) as ei:
         bi.bi_plan_model([3], [1], [2], [[0]], 2, bi.BI_SPARSE_A)

@@ -419,6 +419,27 @@ __global__ __launch_bounds__(kThreads, 1) void lik_kernel(StreamArgs a, const fl
     }
 }
 
+// sum_j M[j * ms] * x[j] over j < n in order (fp64), loads issued 8 at a time
+template <typename MT, typename XT>
+__device__ inline double dot_strided(const MT *M, int64_t ms, const XT *x, int n)
+{
+    double acc = 0.0;
+    int j = 0;
+    for (; j + 8 <= n; j += 8) {
+        MT mv[8];
+        XT xv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            mv[u] = M[(int64_t)(j + u) * ms];
+            xv[u] = x[j + u];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc = fma((double)mv[u], (double)xv[u], acc);
+    }
+    for (; j < n; ++j) acc = fma((double)M[(int64_t)j * ms], (double)x[j], acc);
+    return acc;
+}
+
 // ---------------------------------------------------------------------------
 // update: messages summed over their partial vectors (fp64, fixed order),
 // transition messages, masked softmax; one workgroup per context, one wave
@@ -452,29 +473,29 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *par
                 const MsgSrc src = a.msg[i];
                 if (src.f != f) continue;
                 const PT *pp = pc + src.off + s;
-                for (int k = 0; k < src.copies; ++k) lam += (double)pp[(int64_t)k * src.stride];
+                int k = 0;
+                for (; k + 8 <= src.copies; k += 8) {   // loads first, then the sums in order
+                    PT pv[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) pv[u] = pp[(int64_t)(k + u) * src.stride];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) lam += (double)pv[u];
+                }
+                for (; k < src.copies; ++k) lam += (double)pp[(int64_t)k * src.stride];
             }
             double fwd, bwd = 0.0;
             if (t == 0) {
                 fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + fd.q_off + s]) : ld[s];
             } else if (ALGO == BI_ALGO_VMP) {
-                double acc = 0.0;
-                for (int j = 0; j < n; ++j) acc = fma(LBp[s * n + j], (double)qprev[j], acc);
-                fwd = acc;
+                fwd = dot_strided(LBp + s * n, 1, qprev, n);
             } else {
-                double acc = 0.0;
-                for (int j = 0; j < n; ++j) acc = fma((double)Bp[s * n + j], (double)qprev[j], acc);
-                fwd = ln_clamped(acc);
+                fwd = ln_clamped(dot_strided(Bp + s * n, 1, qprev, n));
             }
             if (qnext) {
-                double acc = 0.0;
-                if (ALGO == BI_ALGO_VMP) {
-                    for (int i = 0; i < n; ++i) acc = fma((double)qnext[i], LBn[i * n + s], acc);
-                    bwd = acc;
-                } else {
-                    for (int i = 0; i < n; ++i) acc = fma((double)qnext[i], (double)Bn[i * n + s], acc);
-                    bwd = ln_clamped(acc);
-                }
+                if (ALGO == BI_ALGO_VMP)
+                    bwd = dot_strided(LBn + s, n, qnext, n);
+                else
+                    bwd = ln_clamped(dot_strided(Bn + s, n, qnext, n));
             }
             if (ALGO == BI_ALGO_VMP)
                 v[s] = lam + fwd + bwd;

@@ -32,6 +32,8 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kStageMaxM = 16;
+constexpr int kStageMaxF = 16;
+constexpr size_t kBStageMax = 32 * 1024;   // bytes of B / log B staged per workgroup
 
 // Observed slices staged in LDS: a context's block holds modality m's slice at
 // po[m] with rows padded to Cp + 1 values (conflict-free row and column
@@ -52,6 +54,11 @@ struct AgentArgs {
     int64_t llpc;
     const int32_t *act;
     const float *prior;    // optional [agent][ntot] prior of the first step (replaces D)
+    // The agent's transition tables staged in LDS once per launch when they
+    // fit (bst): log B (fp64) for VMP, B (fp32) for MMP and FPI; factor f's
+    // [u][i][j] block at element bo[f].  bdoubles: LDS doubles of the table.
+    int bst, bdoubles;
+    int bo[kStageMaxF + 1];
     double tau;            // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
     float *q;
 };
@@ -76,9 +83,64 @@ __device__ inline double wave_sum(double v)
     return v;
 }
 
+// sum_{i < len} x[i * stride] w(i) with the outer-product weight
+// w(i) = q0[i / n1] q1[i % n1] (q1 == nullptr, n1 == 1: w(i) = q0[i]); the
+// values of x are loaded 8 at a time, so a long dot product costs one
+// memory round trip per 8 terms.
+__device__ inline double outer_dot(const double *x, int64_t stride, int len, const double *q0, const double *q1,
+                                   int n1)
+{
+    double acc = 0.0;
+    int i0 = 0, i1 = 0;   // i = i0 * n1 + i1
+    int i = 0;
+    for (; i + 8 <= len; i += 8) {
+        double xv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) xv[u] = x[(int64_t)(i + u) * stride];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const double w = q1 ? q0[i0] * q1[i1] : q0[i0];
+            acc = fma(xv[u], w, acc);
+            if (++i1 == n1) {
+                i1 = 0;
+                ++i0;
+            }
+        }
+    }
+    for (; i < len; ++i) {
+        const double w = q1 ? q0[i0] * q1[i1] : q0[i0];
+        acc = fma(x[(int64_t)i * stride], w, acc);
+        if (++i1 == n1) {
+            i1 = 0;
+            ++i0;
+        }
+    }
+    return acc;
+}
+
 // One Z or V output of an observed slice X (row stride xs) for the marginals
-// qt: j < R gives Z[j], j = R + col gives V[col].
+// qt: j < R gives Z[j] = sum_c X[j][c] t[c], j = R + col gives
+// V[col] = sum_r s[r] X[r][col] (t, s: outer products of the column and row
+// factors' marginals).
 __device__ inline double zv_one(const AgentArgs &a, const ModDesc &md, const double *X, int64_t xs,
+                                const double *qt, int j)
+{
+    const int R = md.R;
+    if (j < R) {
+        if (md.nrow == 0) return 0.0;   // Z of a rank-0 row side feeds no message
+        const double *q1 = md.ncol == 2 ? qt + a.facs[md.cf[1]].q_off : nullptr;
+        return outer_dot(X + (int64_t)j * xs, 1, md.C, qt + a.facs[md.cf[0]].q_off, q1,
+                         md.ncol == 2 ? md.cn[1] : 1);
+    }
+    const int col = j - R;
+    if (md.nrow == 0) return X[col];
+    const double *q1 = md.nrow == 2 ? qt + a.facs[md.rf[1]].q_off : nullptr;
+    return outer_dot(X + col, xs, R, qt + a.facs[md.rf[0]].q_off, q1, md.nrow == 2 ? md.rn[1] : 1);
+}
+
+// The same output with the nested loops of the two-sided view, for slices
+// staged in LDS (short latency: no batching, fewer registers).
+__device__ inline double zv_one_lds(const AgentArgs &a, const ModDesc &md, const double *X, int64_t xs,
                                 const double *qt, int j)
 {
     const int R = md.R;
@@ -165,6 +227,7 @@ __device__ void stage_slices(const AgentArgs &a, int agent, int t0, int nc, doub
 // q: marginals of context t at q + t * ntot.  With staged slices, X of
 // context t0 + c comes from stg + (sc0 + c) * sctx (LDS); otherwise from the
 // packed buffer.
+template <bool GX>   // GX: slices read from global memory (batched loads); else staged in LDS
 __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv,
                          const double *stg, int sc0)
 {
@@ -184,8 +247,8 @@ __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const do
             const int t = t0 + c;
             const double *qt = q + t * a.ntot;
             double acc;
-            if (stg) {
-                acc = zv_one(a, md, stg + (int64_t)(sc0 + c) * a.sctx + a.po[m], Cp + 1, qt, j);
+            if (!GX) {
+                acc = zv_one_lds(a, md, stg + (int64_t)(sc0 + c) * a.sctx + a.po[m], Cp + 1, qt, j);
             } else if (a.ll) {
                 acc = zv_one(a, md, a.ll + ((int64_t)agent * a.T + t) * a.llpc + llo, Cp, qt, j);
             } else {
@@ -269,6 +332,7 @@ __device__ void wave_softmax(double *v, int n, int lane)
 
 // lam for every context of the window (phases 1 and 2 over context chunks;
 // staged chunks are copied to LDS first unless the whole window is resident).
+template <bool GX>
 __device__ void window_lam(const AgentArgs &a, int agent, const double *q, double *zv, double *stg, const int *sfac,
                            double *lam)
 {
@@ -278,11 +342,28 @@ __device__ void window_lam(const AgentArgs &a, int agent, const double *q, doubl
             stage_slices(a, agent, t0, nc, stg);
             __syncthreads();
         }
-        phase_zv(a, agent, t0, nc, q, zv, a.stage == kStageNone ? nullptr : stg,
-                 a.stage == kStageWindow ? t0 : 0);
+        phase_zv<GX>(a, agent, t0, nc, q, zv, stg, a.stage == kStageWindow ? t0 : 0);
         __syncthreads();
         phase_lam(a, t0, nc, q, zv, sfac, lam);
         __syncthreads();
+    }
+}
+
+// Copy the agent's B (fp32) or log B (fp64, lb) of every factor into tab.
+__device__ void stage_b(const AgentArgs &a, int agent, bool lb, double *tab)
+{
+    const int64_t am = a.shared ? 0 : agent;
+    for (int f = 0; f < a.F; ++f) {
+        const FacDesc &fd = a.facs[f];
+        const int cnt = fd.U * fd.n * fd.n;
+        if (lb) {
+            const double *src = at<double>(a.base, fd.lb_off) + am * fd.b_agent;
+            for (int i = threadIdx.x; i < cnt; i += kThreads) tab[a.bo[f] + i] = src[i];
+        } else {
+            const float *src = at<float>(a.base, fd.b_off) + am * fd.b_agent;
+            float *dst = reinterpret_cast<float *>(tab) + a.bo[f];
+            for (int i = threadIdx.x; i < cnt; i += kThreads) dst[i] = src[i];
+        }
     }
 }
 
@@ -295,78 +376,107 @@ __device__ void init_tables(const AgentArgs &a, int *sfac)
     }
 }
 
-template <int ALGO>  // BI_ALGO_VMP or BI_ALGO_MMP
-__global__ __launch_bounds__(kThreads) void agent_window_kernel(AgentArgs a)
+// Segmented softmax over the window: logits v[t][j] of every (step, state)
+// are in LDS; each thread owns states i = threadIdx.x + k * kThreads and
+// reads its (t, f) segment for the max and, after the exponentials are
+// written to e, for the sum.  Every lane works whatever the factor sizes
+// (a wave per (t, f) would leave 64 - n_f lanes idle).  Writes out (damped
+// towards cur when tau != 1).  Three barriers.
+__device__ void window_softmax(const AgentArgs &a, const int *sfac, const double *v, double *e, const double *cur,
+                               double *out)
+{
+    const int TN = a.T * a.ntot;
+    for (int i = threadIdx.x; i < TN; i += kThreads) {
+        const int t = i / a.ntot, j = i - t * a.ntot;
+        const FacDesc &fd = a.facs[sfac[j]];
+        const double *seg = v + t * a.ntot + fd.q_off;
+        double mx = seg[0];
+        for (int s = 1; s < fd.n; ++s) mx = fmax(mx, seg[s]);
+        e[i] = exp(v[i] - mx);
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < TN; i += kThreads) {
+        const int t = i / a.ntot, j = i - t * a.ntot;
+        const FacDesc &fd = a.facs[sfac[j]];
+        const double *seg = e + t * a.ntot + fd.q_off;
+        double sum = 0.0;
+        for (int s = 0; s < fd.n; ++s) sum += seg[s];
+        const double qn = e[i] / sum;
+        out[i] = a.tau != 1.0 ? (1.0 - a.tau) * cur[i] + a.tau * qn : qn;
+    }
+    __syncthreads();
+}
+
+template <int ALGO, bool GX>  // ALGO: BI_ALGO_VMP or BI_ALGO_MMP; GX: slices read from global memory
+__global__ __launch_bounds__(kThreads, 4) void agent_window_kernel(AgentArgs a)
 {
     extern __shared__ double smem[];
     const int agent = blockIdx.x;
     const int TN = a.T * a.ntot;
     double *qa = smem, *qb = qa + TN, *lam = qb + TN, *zv = lam + TN, *stg = zv + a.nc * a.zvpc;
     const int nstg = a.stage == kStageWindow ? a.T : a.stage == kStageChunk ? a.nc : 0;
-    int *sfac = reinterpret_cast<int *>(stg + (int64_t)nstg * a.sctx);
+    double *btab = stg + (int64_t)nstg * a.sctx;
+    int *sfac = reinterpret_cast<int *>(btab + a.bdoubles);
     init_tables(a, sfac);
+    if (a.bst) stage_b(a, agent, ALGO == BI_ALGO_VMP, btab);
     if (a.stage == kStageWindow) stage_slices(a, agent, 0, a.T, stg);   // every iteration reads them from LDS
     __syncthreads();
     for (int i = threadIdx.x; i < TN; i += kThreads) qa[i] = 1.0 / a.facs[sfac[i % a.ntot]].n;
     __syncthreads();
-    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
     const int64_t am = a.shared ? 0 : agent;
     double *cur = qa, *nxt = qb;
     for (int k = 0; k < a.iters; ++k) {
-        window_lam(a, agent, cur, zv, stg, sfac, lam);
-        for (int p = wave; p < a.T * a.F; p += kWaves) {
-            const int t = p / a.F, f = p - t * a.F;
+        window_lam<GX>(a, agent, cur, zv, stg, sfac, lam);
+        // logits of every (t, state) into nxt, one thread per state
+        for (int i = threadIdx.x; i < TN; i += kThreads) {
+            const int t = i / a.ntot, j = i - t * a.ntot;
+            const int f = sfac[j];
             const FacDesc &fd = a.facs[f];
-            const int n = fd.n;
+            const int n = fd.n, s = j - fd.q_off;
             const double *qprev = t > 0 ? cur + (t - 1) * a.ntot + fd.q_off : nullptr;
             const double *qnext = t + 1 < a.T ? cur + (t + 1) * a.ntot + fd.q_off : nullptr;
             const int up = t > 0 ? a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f] : 0;
             const int un = t + 1 < a.T ? a.act[((int64_t)agent * (a.T - 1) + t) * a.F + f] : 0;
             // VMP uses log B, MMP the linear B (log taken after the product)
-            const double *LBp = at<double>(a.base, fd.lb_off) + am * fd.b_agent + (int64_t)up * n * n;  // [i][j]
-            const double *LBn = at<double>(a.base, fd.lb_off) + am * fd.b_agent + (int64_t)un * n * n;
-            const float *Bp = at<float>(a.base, fd.b_off) + am * fd.b_agent + (int64_t)up * n * n;
-            const float *Bn = at<float>(a.base, fd.b_off) + am * fd.b_agent + (int64_t)un * n * n;
-            const double *ld = at<double>(a.base, fd.ld_off) + am * fd.ld_agent;
-            double *v = nxt + t * a.ntot + fd.q_off;
-            const double *lm = lam + t * a.ntot + fd.q_off;
-            for (int s = lane; s < n; s += 64) {
-                double fwd, bwd = 0.0;
-                if (t == 0) {
-                    fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + fd.q_off + s]) : ld[s];
-                } else if (ALGO == BI_ALGO_VMP) {
-                    double acc = 0.0;
-                    for (int j = 0; j < n; ++j) acc = fma(LBp[s * n + j], qprev[j], acc);
-                    fwd = acc;
+            const double *LB = a.bst ? btab + a.bo[f] : at<double>(a.base, fd.lb_off) + am * fd.b_agent;
+            const float *Bf = a.bst ? reinterpret_cast<const float *>(btab) + a.bo[f]
+                                    : at<float>(a.base, fd.b_off) + am * fd.b_agent;
+            double fwd, bwd = 0.0;
+            if (t == 0) {
+                fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + j])
+                              : at<double>(a.base, fd.ld_off)[am * fd.ld_agent + s];
+            } else if (ALGO == BI_ALGO_VMP) {
+                const double *row = LB + (int64_t)up * n * n + s * n;   // [i][j]
+                double acc = 0.0;
+                for (int jj = 0; jj < n; ++jj) acc = fma(row[jj], qprev[jj], acc);
+                fwd = acc;
+            } else {
+                const float *row = Bf + (int64_t)up * n * n + s * n;
+                double acc = 0.0;
+                for (int jj = 0; jj < n; ++jj) acc = fma((double)row[jj], qprev[jj], acc);
+                fwd = ln_clamped(acc);
+            }
+            if (qnext) {
+                double acc = 0.0;
+                if (ALGO == BI_ALGO_VMP) {
+                    const double *col = LB + (int64_t)un * n * n + s;
+                    for (int ii = 0; ii < n; ++ii) acc = fma(qnext[ii], col[ii * n], acc);
+                    bwd = acc;
                 } else {
-                    double acc = 0.0;
-                    for (int j = 0; j < n; ++j) acc = fma((double)Bp[s * n + j], qprev[j], acc);
-                    fwd = ln_clamped(acc);
+                    const float *col = Bf + (int64_t)un * n * n + s;
+                    for (int ii = 0; ii < n; ++ii) acc = fma(qnext[ii], (double)col[ii * n], acc);
+                    bwd = ln_clamped(acc);
                 }
-                if (qnext) {
-                    double acc = 0.0;
-                    if (ALGO == BI_ALGO_VMP) {
-                        for (int i = 0; i < n; ++i) acc = fma(qnext[i], LBn[i * n + s], acc);
-                        bwd = acc;
-                    } else {
-                        for (int i = 0; i < n; ++i) acc = fma(qnext[i], (double)Bn[i * n + s], acc);
-                        bwd = ln_clamped(acc);
-                    }
-                }
-                double val;
-                if (ALGO == BI_ALGO_VMP)
-                    val = lm[s] + fwd + bwd;
-                else
-                    val = qnext ? lm[s] + 0.5 * (fwd + bwd) : lm[s] + fwd;
-                v[s] = val;
             }
-            wave_softmax(v, n, lane);
-            if (a.tau != 1.0) {
-                const double *old = cur + t * a.ntot + fd.q_off;
-                for (int s = lane; s < n; s += 64) v[s] = (1.0 - a.tau) * old[s] + a.tau * v[s];
-            }
+            const double lm = lam[i];
+            if (ALGO == BI_ALGO_VMP)
+                nxt[i] = lm + fwd + bwd;
+            else
+                nxt[i] = qnext ? lm + 0.5 * (fwd + bwd) : lm + fwd;
         }
         __syncthreads();
+        // lam is free again: it takes the exponentials
+        window_softmax(a, sfac, nxt, lam, cur, nxt);
         double *tmp = cur;
         cur = nxt;
         nxt = tmp;
@@ -375,7 +485,8 @@ __global__ __launch_bounds__(kThreads) void agent_window_kernel(AgentArgs a)
     for (int i = threadIdx.x; i < TN; i += kThreads) out[i] = (float)cur[i];
 }
 
-__global__ __launch_bounds__(kThreads) void agent_filter_kernel(AgentArgs a)
+template <bool GX>   // slices read from global memory
+__global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
 {
     extern __shared__ double smem[];
     const int agent = blockIdx.x;
@@ -386,8 +497,10 @@ __global__ __launch_bounds__(kThreads) void agent_filter_kernel(AgentArgs a)
     double *qfin = smem, *cur = qfin + TN, *lam = cur + TN, *zv = lam + TN, *logp = zv + a.zvpc;
     double *stg = logp + a.ntot;
     const int nstg = a.stage == kStageWindow ? a.T : a.stage == kStageChunk ? 1 : 0;
-    int *sfac = reinterpret_cast<int *>(stg + (int64_t)nstg * a.sctx);
+    double *btab = stg + (int64_t)nstg * a.sctx;
+    int *sfac = reinterpret_cast<int *>(btab + a.bdoubles);
     init_tables(a, sfac);
+    if (a.bst) stage_b(a, agent, false, btab);
     if (a.stage == kStageWindow) stage_slices(a, agent, 0, a.T, stg);
     __syncthreads();
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
@@ -408,7 +521,8 @@ __global__ __launch_bounds__(kThreads) void agent_filter_kernel(AgentArgs a)
                 }
             } else {
                 const int u = a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f];
-                const float *Bp = at<float>(a.base, fd.b_off) + am * fd.b_agent + (int64_t)u * n * n;
+                const float *Bp = (a.bst ? reinterpret_cast<const float *>(btab) + a.bo[f]
+                                         : at<float>(a.base, fd.b_off) + am * fd.b_agent) + (int64_t)u * n * n;
                 const double *qp = qfin + (t - 1) * a.ntot + fd.q_off;
                 for (int s = lane; s < n; s += 64) {
                     double acc = 0.0;
@@ -422,7 +536,7 @@ __global__ __launch_bounds__(kThreads) void agent_filter_kernel(AgentArgs a)
         if (a.stage == kStageChunk) stage_slices(a, agent, t, 1, stg);   // step t's slices, for all its iterations
         __syncthreads();
         for (int k = 0; k < a.iters; ++k) {
-            phase_zv(a, agent, t, 1, cur, zv, a.stage == kStageNone ? nullptr : stg,
+            phase_zv<GX>(a, agent, t, 1, cur, zv, stg,
                      a.stage == kStageWindow ? t : 0);
             __syncthreads();
             phase_lam(a, t, 1, cur, zv, sfac, lam);
@@ -497,10 +611,22 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     a.sraw = (int)sraw;
     const size_t sb = 8 * (size_t)sctx;   // staged bytes per context
     const size_t budget2 = 80 * 1024;    // two workgroups per CU
+    // transition tables: staged when they fit kBStageMax
+    {
+        int64_t elems = 0;
+        for (int f = 0; f < m->F && f <= kStageMaxF; ++f) {
+            if (f < kStageMaxF) a.bo[f] = (int)elems;
+            elems += (int64_t)m->facs[f].U * m->facs[f].n * m->facs[f].n;
+        }
+        const size_t bytes = (size_t)elems * (algo == BI_ALGO_VMP ? 8 : 4);
+        a.bst = m->F <= kStageMaxF && bytes <= kBStageMax;
+        a.bdoubles = a.bst ? (int)((bytes + 7) / 8) : 0;
+    }
+    const size_t bt = 8 * (size_t)a.bdoubles;
     size_t fixed, per_ctx = (size_t)m->zvpc * 8, lds;
     a.stage = kStageNone;
     if (algo == BI_ALGO_FPI) {
-        fixed = (3 * TN + m->ntot) * 8 + (size_t)m->ntot * 4 + per_ctx;
+        fixed = (3 * TN + m->ntot) * 8 + (size_t)m->ntot * 4 + per_ctx + bt;
         a.nc = 1;
         if (can_stage && fixed + T * sb <= budget2)
             a.stage = kStageWindow;
@@ -508,7 +634,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
             a.stage = kStageChunk;
         lds = fixed + (a.stage == kStageWindow ? T * sb : a.stage == kStageChunk ? sb : 0);
     } else {
-        fixed = 3 * TN * 8 + (size_t)m->ntot * 4;
+        fixed = 3 * TN * 8 + (size_t)m->ntot * 4 + bt;
         if (can_stage && fixed + T * (per_ctx + sb) <= budget2) {
             // the whole window's slices stay in LDS for every iteration
             a.stage = kStageWindow;
@@ -528,31 +654,21 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     }
     if (a.nc < 1 || lds > kLdsMax)
         return fail(BI_ERR_UNSUPPORTED, "agent working set (%zu bytes of LDS) exceeds the 160 KB budget", lds);
-    hipError_t e;
-    if (algo == BI_ALGO_FPI) {
-        e = hipFuncSetAttribute((const void *)agent_filter_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)kLdsMax);
-        if (e == hipSuccess) {
-            ProfScope p("agent_filter", stream);
-            hipLaunchKernelGGL(agent_filter_kernel, dim3(b), dim3(kThreads), lds, stream, a);
-            e = hipGetLastError();
-        }
-    } else if (algo == BI_ALGO_VMP) {
-        e = hipFuncSetAttribute((const void *)agent_window_kernel<BI_ALGO_VMP>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
-        if (e == hipSuccess) {
-            ProfScope p("agent_window", stream);
-            hipLaunchKernelGGL(agent_window_kernel<BI_ALGO_VMP>, dim3(b), dim3(kThreads), lds, stream, a);
-            e = hipGetLastError();
-        }
-    } else {
-        e = hipFuncSetAttribute((const void *)agent_window_kernel<BI_ALGO_MMP>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
-        if (e == hipSuccess) {
-            ProfScope p("agent_window", stream);
-            hipLaunchKernelGGL(agent_window_kernel<BI_ALGO_MMP>, dim3(b), dim3(kThreads), lds, stream, a);
-            e = hipGetLastError();
-        }
+    const bool gx = a.stage == kStageNone;
+    const void *fn;
+    if (algo == BI_ALGO_FPI)
+        fn = gx ? (const void *)agent_filter_kernel<true> : (const void *)agent_filter_kernel<false>;
+    else if (algo == BI_ALGO_VMP)
+        fn = gx ? (const void *)agent_window_kernel<BI_ALGO_VMP, true>
+                : (const void *)agent_window_kernel<BI_ALGO_VMP, false>;
+    else
+        fn = gx ? (const void *)agent_window_kernel<BI_ALGO_MMP, true>
+                : (const void *)agent_window_kernel<BI_ALGO_MMP, false>;
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
+    if (e == hipSuccess) {
+        ProfScope p(algo == BI_ALGO_FPI ? "agent_filter" : "agent_window", stream);
+        void *args[] = {&a};
+        e = hipLaunchKernel(fn, dim3(b), dim3(kThreads), args, lds, stream);
     }
     if (e != hipSuccess) return fail(BI_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
     return BI_OK;

@@ -66,6 +66,11 @@ extern "C" {
  * bi_predict is not checked. */
 #define BI_CHECK 8u
 
+/* Kernel families (bi_query_path). */
+#define BI_PATH_AGENT 0  /* agent-resident fp64 kernels: one workgroup per agent, all iterations in-kernel */
+#define BI_PATH_STREAM 1 /* dense streaming kernels: fp32 matrix-core contractions (shared model, BI_FAST_F32) */
+#define BI_PATH_SPARSE 2 /* sparse streaming kernels: fp64 gathers over the nonzeros (shared model, BI_SPARSE_A) */
+
 /* Algorithm ids (bi_workspace_size). */
 #define BI_ALGO_FPI 0
 #define BI_ALGO_VMP 1
@@ -257,6 +262,16 @@ typedef struct bi_infer_opts {
 int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const int32_t *obs_dev,
              const int32_t *act_dev, int32_t iters, const bi_infer_opts *opts, float *q_dev, void *ws_dev,
              size_t ws_bytes, void *hip_stream);
+
+/*
+ * The kernel family a call with these sizes will run (BI_PATH_*).  FPI always
+ * runs agent-resident.  VMP and MMP on a model shared by every agent may
+ * also run the dense streaming kernels (packed with BI_FAST_F32) or the
+ * sparse ones (packed with BI_SPARSE_A); among the families the packing
+ * allows, a selector fitted to timings of seeded sweep models on MI355X
+ * picks the one expected to be fastest for (model, algo, b, T).  Host only.
+ */
+int bi_query_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, int32_t *path);
 
 /*
  * Soft observations (Sec. III-C: the log-likelihood of a modality is the

@@ -31,7 +31,7 @@ ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
 
 EXPORTS = ("bi_last_error", "bi_plan_model", "bi_plan_model_exact", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
            "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_vfilter_prior",
-           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_workspace_size_soft", "bi_infer_soft", "bi_predict", "bi_free_model",
+           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_query_path", "bi_workspace_size_soft", "bi_infer_soft", "bi_predict", "bi_free_model",
            "bi_profile_begin", "bi_profile_end")
 
 
@@ -89,6 +89,7 @@ def load(path: str = LIB_PATH):
         getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, sz, vp]
     lib.bi_infer.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp, sz, vp]
     lib.bi_workspace_size_soft.argtypes = [vp, i32, i32, i32, P(sz)]
+    lib.bi_query_path.argtypes = [vp, i32, i32, i32, P(i32)]
     lib.bi_infer_soft.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp, sz, vp]
     lib.bi_predict.argtypes = [vp, i32, vp, ctypes.c_int64, vp, ctypes.c_int64, vp, vp]
     lib.bi_free_model.argtypes = [vp]
@@ -253,6 +254,16 @@ def bi_infer(handle, algo: int, b, T, obs, act, iters, q, ws=None, stream=None, 
                            ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(_stream_ptr(stream))))
 
 
+BI_PATH_AGENT, BI_PATH_STREAM, BI_PATH_SPARSE = 0, 1, 2
+PATH_NAMES = {BI_PATH_AGENT: "agent", BI_PATH_STREAM: "stream", BI_PATH_SPARSE: "sparse"}
+
+
+def bi_query_path(handle: int, b: int, T: int, algo: int) -> int:
+    out = ctypes.c_int32(-1)
+    _check(load().bi_query_path(ctypes.c_void_p(handle), int(b), int(T), int(algo), ctypes.byref(out)))
+    return int(out.value)
+
+
 def bi_workspace_size_soft(handle: int, b: int, T: int, algo: int) -> int:
     out = ctypes.c_size_t(0)
     _check(load().bi_workspace_size_soft(ctypes.c_void_p(handle), int(b), int(T), int(algo), ctypes.byref(out)))
@@ -314,6 +325,10 @@ class PackedModel:
 
     def stats(self) -> dict:
         return bi_get_model_stats(self.handle)
+
+    def path(self, b: int, T: int, algo: str) -> str:
+        """The kernel family ("agent", "stream" or "sparse") a call with these sizes runs."""
+        return PATH_NAMES[bi_query_path(self.handle, b, T, ALGO_IDS[algo])]
 
     def workspace(self, b: int, T: int, algo: str):
         import torch

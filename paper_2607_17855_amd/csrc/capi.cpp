@@ -17,27 +17,29 @@ using bi::fail;
 
 namespace {
 
-enum class Path { Agent, Stream, Sparse };
+enum class Path { Agent = BI_PATH_AGENT, Stream = BI_PATH_STREAM, Sparse = BI_PATH_SPARSE };
 
 // BI_CHECK: status words of the input check, after the call's own workspace
 constexpr size_t kStatusBytes = 256;
 
-// Dispatch: a model packed with the sparse layout (shared by every agent)
-// runs VMP / MMP on the sparse streaming kernels; the dense streaming kernels
-// serve large shared models when the caller opted into fp32 contractions;
-// everything else runs the agent-resident fp64 kernels.
-// BI_FORCE_PATH=agent|stream overrides these rules (tests), never the
-// eligibility.
-Path choose_path(const bi_model *m, int algo)
+// Dispatch among the kernel families the packed model is eligible for: the
+// agent-resident fp64 kernels (always), the dense streaming kernels (shared
+// model, BI_FAST_F32: the caller opted into fp32 contractions) and the
+// sparse streaming kernels (shared model, BI_SPARSE_A).  With more than one
+// eligible, the measured selector decides (selector.cpp).
+// BI_FORCE_PATH=agent|stream|sparse overrides the choice (tests, timing
+// sweeps), never the eligibility.
+Path choose_path(const bi_model *m, int algo, int b, int T)
 {
+    const bool stream = bi::stream_eligible(m, algo), sparse = bi::sparse_eligible(m, algo);
     const char *env = std::getenv("BI_FORCE_PATH");
-    const bool force_agent = env && std::strcmp(env, "agent") == 0;
-    if (bi::sparse_eligible(m, algo) && !force_agent) return Path::Sparse;
-    if (!bi::stream_eligible(m, algo) || force_agent) return Path::Agent;
-    if (env && std::strcmp(env, "stream") == 0) return Path::Stream;
-    int64_t biggest = 0;
-    for (const bi::ModDesc &md : m->mods) biggest = std::max<int64_t>(biggest, (int64_t)md.R * md.C);
-    return biggest >= 16384 ? Path::Stream : Path::Agent;
+    if (env) {
+        if (std::strcmp(env, "agent") == 0) return Path::Agent;
+        if (std::strcmp(env, "stream") == 0 && stream) return Path::Stream;
+        if (std::strcmp(env, "sparse") == 0 && sparse) return Path::Sparse;
+    }
+    if (!stream && !sparse) return Path::Agent;
+    return static_cast<Path>(bi::select_path(m, algo, b, T, stream, sparse));
 }
 
 }  // namespace
@@ -206,7 +208,7 @@ int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo,
     if (!model || !bytes) return fail(BI_ERR_INVALID_ARG, "model and bytes must be non-NULL");
     if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
     if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
-    const Path p = choose_path(model, algo);
+    const Path p = choose_path(model, algo, b, T);
     *bytes = p == Path::Agent ? 0 : bi::stream_workspace(model, b, T, p == Path::Sparse);
     if (model->flags & BI_CHECK) *bytes = (size_t)bi::align_up((int64_t)*bytes, bi::kAlign) + kStatusBytes;
     return BI_OK;
@@ -237,7 +239,7 @@ static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const in
                                   reinterpret_cast<int32_t *>(static_cast<char *>(ws) + need - kStatusBytes), s);
             if (rc != BI_OK) return rc;
         }
-        const Path p = choose_path(model, algo);
+        const Path p = choose_path(model, algo, b, T);
         if (p != Path::Agent)
             return bi::launch_stream(model, algo, b, T, obs, act, prior, tau, iters, q, ws, s, p == Path::Sparse);
         return bi::launch_agent(model, algo, b, T, obs, nullptr, act, prior, tau, iters, q, s);
@@ -296,6 +298,15 @@ int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const in
     const float *prior = opts ? opts->prior_dev : nullptr;
     const double tau = opts ? opts->damping : 1.0;
     return infer(algo, model, b, T, obs_dev, act_dev, prior, tau, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+}
+
+int bi_query_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, int32_t *path)
+{
+    if (!model || !path) return fail(BI_ERR_INVALID_ARG, "model and path must be non-NULL");
+    if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
+    if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
+    *path = static_cast<int32_t>(choose_path(model, algo, b, T));
+    return BI_OK;
 }
 
 int bi_workspace_size_soft(const bi_model *model, int32_t b, int32_t T, int32_t algo, size_t *bytes)

@@ -56,6 +56,11 @@ int launch_soft_ll(const bi_model *m, int b, int T, const float *w, double *ll, 
 int check_inputs(const bi_model *m, int b, int T, const int32_t *obs, const int32_t *act, int32_t *status,
                  hipStream_t stream);
 
+// Kernel-family selector (selector.cpp): one of BI_PATH_* among the eligible
+// ones (agent always; stream / sparse as flagged), for algo over b agents and
+// a window of T steps.
+int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool sparse);
+
 // Predictive prior B_f[:, :, u] q for every agent and factor (predict.hip).
 int launch_predict(const bi_model *m, int b, const float *q, int64_t q_stride, const int32_t *act,
                    int64_t act_stride, float *out, hipStream_t stream);

@@ -296,14 +296,39 @@ class SweepSpec:
         return int(sum(k * int(np.prod([self.n[f] for f in d])) for k, d in zip(self.K, self.deps)))
 
 
-def config4_spec(case: int) -> SweepSpec:
-    """One of the 770 sweep POMDP specifications (case = 0..769)."""
-    rd = _rng(4, case, 2)
+# seed family of the skewed-regime sweep (the uniform sweep uses 4)
+SKEWED_CFG = 46
+
+
+def _skewed_dims(rd: np.random.Generator, count: int, lo: int = 2, hi: int = 32) -> List[int]:
+    """Sizes of the skewed regime (Sec. V-A, fine-grained dimensionality
+    sampling): each size comes from the top 10% of [lo, hi] with probability
+    1/5, otherwise from the bottom 10%, giving strongly imbalanced shapes."""
+    band = max(1, int(round(0.1 * (hi - lo))))
+    top = rd.random(count) < 0.2
+    high = rd.integers(hi - band, hi + 1, size=count)
+    low = rd.integers(lo, lo + band + 1, size=count)
+    return [int(h) if t else int(x) for t, h, x in zip(top, high, low)]
+
+
+def config4_spec(case: int, regime: str = "uniform") -> SweepSpec:
+    """One of the sweep POMDP specifications (case = 0..769).  regime
+    "uniform" draws every state and outcome count uniformly from 2..32;
+    "skewed" draws them from the extremes of that range (_skewed_dims)."""
+    if regime not in ("uniform", "skewed"):
+        raise ValueError(f"unknown regime {regime!r}")
+    rd = _rng(4 if regime == "uniform" else SKEWED_CFG, case, 2)
     F = int(rd.integers(1, 5))
-    n = [int(x) for x in rd.integers(2, 33, size=F)]
+    if regime == "uniform":
+        n = [int(x) for x in rd.integers(2, 33, size=F)]
+    else:
+        n = _skewed_dims(rd, F)
     U = [int(x) for x in rd.integers(1, 6, size=F)]
     M = int(rd.integers(1, 6))
-    K = [int(x) for x in rd.integers(2, 33, size=M)]
+    if regime == "uniform":
+        K = [int(x) for x in rd.integers(2, 33, size=M)]
+    else:
+        K = _skewed_dims(rd, M)
     deps = [_random_subset(rd, F) for _ in range(M)]
     T = int(rd.integers(1, 21))
     return SweepSpec(n, U, K, deps, T)
@@ -312,13 +337,15 @@ def config4_spec(case: int) -> SweepSpec:
 N_SWEEP = 770
 
 
-def config4(case: int, b: int = 256) -> Workload:
+def config4(case: int, b: int = 256, regime: str = "uniform") -> Workload:
     """Sweep POMDP ``case``: one generative model shared by the b agents."""
-    sp = config4_spec(case)
-    rm, rs = _rng(4, case, 0), _rng(4, case, 1)
+    sp = config4_spec(case, regime)
+    cfg = 4 if regime == "uniform" else SKEWED_CFG
+    rm, rs = _rng(cfg, case, 0), _rng(cfg, case, 1)
     model = make_model(rm, sp.n, sp.U, sp.K, sp.deps, 1, 1.0, 1.0)
     obs, act = sample_sequences(rs, model, b, sp.T)
-    return Workload(f"cfg4_case{case}_b{b}", ["fpi", "vmp", "mmp"], model, obs, act, 16)
+    tag = "cfg4" if regime == "uniform" else "cfg4skew"
+    return Workload(f"{tag}_case{case}_b{b}", ["fpi", "vmp", "mmp"], model, obs, act, 16)
 
 
 def config5(case: int = 0, b: int = 64, n: int = 32, F: int = 4, M: int = 4, K: int = 32, T: int = 16) -> Workload:

@@ -296,11 +296,17 @@ def test_check_flag_adds_status_words_to_every_workspace():
     fl = bi.BI_DENSE_A | bi.BI_FAST_F32
     h0, _ = bi.bi_pack_model_host(ms.n, ms.U, ms.K, ms.deps, 1, ms.A, ms.B, ms.D, flags=fl)
     h1, _ = bi.bi_pack_model_host(ms.n, ms.U, ms.K, ms.deps, 1, ms.A, ms.B, ms.D, flags=fl | bi.BI_CHECK)
+    old = os.environ.get("BI_FORCE_PATH")
+    os.environ["BI_FORCE_PATH"] = "stream"   # the selector would run this small batch agent-resident
     try:
         n0 = bi.bi_workspace_size(h0, 4, 3, 1)
         assert n0 > 0
         assert bi.bi_workspace_size(h1, 4, 3, 1) == -(-n0 // 256) * 256 + 256
     finally:
+        if old is None:
+            os.environ.pop("BI_FORCE_PATH", None)
+        else:
+            os.environ["BI_FORCE_PATH"] = old
         bi.bi_free_model(h0)
         bi.bi_free_model(h1)
 
@@ -313,3 +319,74 @@ def test_sparse_layout_needs_a_shared_model():
     out = ctypes.c_size_t(0)
     d = bi._Desc([3], [1], [2], [[0]], 1, bi.BI_SPARSE_A)
     assert lib.bi_plan_model_exact(ctypes.byref(d.c), None, ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG
+
+
+def test_query_path_follows_eligibility_and_forcing():
+    lib_models = []
+    try:
+        w = synth.random_small(9, b=3, per_agent=True)
+        m = w.model
+        h, _ = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, m.mb, m.A, m.B, m.D, flags=bi.BI_DENSE_A | bi.BI_FAST_F32)
+        lib_models.append(h)
+        for algo in range(3):   # per-agent models: agent-resident only, whatever is forced
+            assert bi.bi_query_path(h, 3, 4, algo) == bi.BI_PATH_AGENT
+        ms = synth.make_model(np.random.Generator(np.random.PCG64(3)), [9, 7, 5], [2, 1, 3], [3, 2],
+                              [[0, 1, 2], [1]], 1)
+        hs, _ = bi.bi_pack_model_host(ms.n, ms.U, ms.K, ms.deps, 1, ms.A, ms.B, ms.D, flags=bi.BI_SPARSE_A)
+        lib_models.append(hs)
+        assert bi.bi_query_path(hs, 8, 4, bi.BI_ALGO_FPI) == bi.BI_PATH_AGENT
+        old = os.environ.get("BI_FORCE_PATH")
+        try:
+            os.environ["BI_FORCE_PATH"] = "sparse"
+            assert bi.bi_query_path(hs, 8, 4, bi.BI_ALGO_VMP) == bi.BI_PATH_SPARSE
+            assert bi.bi_query_path(hs, 8, 4, bi.BI_ALGO_FPI) == bi.BI_PATH_AGENT   # not eligible
+            os.environ["BI_FORCE_PATH"] = "stream"                                 # not packed for it
+            assert bi.bi_query_path(hs, 8, 4, bi.BI_ALGO_VMP) in (bi.BI_PATH_AGENT, bi.BI_PATH_SPARSE)
+            os.environ["BI_FORCE_PATH"] = "agent"
+            assert bi.bi_query_path(hs, 8, 4, bi.BI_ALGO_MMP) == bi.BI_PATH_AGENT
+        finally:
+            if old is None:
+                os.environ.pop("BI_FORCE_PATH", None)
+            else:
+                os.environ["BI_FORCE_PATH"] = old
+        out = ctypes.c_int32(0)
+        assert bi.load().bi_query_path(ctypes.c_void_p(hs), 0, 4, 1, ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG
+        assert bi.load().bi_query_path(ctypes.c_void_p(hs), 8, 4, 7, ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG
+    finally:
+        for h in lib_models:
+            bi.bi_free_model(h)
+
+
+@pytest.mark.parametrize("regime", ["uniform", "skewed"])
+def test_selector_table_matches_the_fitted_trees(regime):
+    """The C selector (through bi_query_path on host-packed sweep models)
+    makes the choice of the decision trees the fit produced, for every
+    candidate set and algorithm, on a sample of the sweep models."""
+    from paper_2607_17855_amd.selector import fit
+    data = fit.load()
+    flags = {1: bi.BI_DENSE_A | bi.BI_FAST_F32, 2: bi.BI_SPARSE_A, 3: bi.BI_SPARSE_A | bi.BI_FAST_F32}
+    trees = {}
+    for cset, cands in fit.SETS.items():
+        for algo in ("vmp", "mmp"):
+            X, y, wt, _ = fit.dataset(data, algo, cands)
+            trees[(cset, algo)] = (fit.fit_tree(X, y, wt), cands)
+    rng = np.random.Generator(np.random.PCG64(7))
+    cases = sorted(set(int(c) for c in rng.choice(770, size=40, replace=False)))
+    checked = 0
+    for case in cases:
+        sp = synth.config4_spec(case, regime)
+        model = synth.make_model(np.random.Generator(np.random.PCG64(case)), sp.n, sp.U, sp.K, sp.deps, 1)
+        for cset, fl in flags.items():
+            h, _ = bi.bi_pack_model_host(model.n, model.U, model.K, model.deps, 1, model.A, model.B, model.D,
+                                         flags=fl)
+            try:
+                for algo in ("vmp", "mmp"):
+                    tree, cands = trees[(cset, algo)]
+                    want = cands[int(tree.predict(np.array([fit.features(sp, 256)]))[0])]
+                    got = bi.PATH_NAMES[bi.bi_query_path(h, 256, sp.T, bi.ALGO_IDS[algo])]
+                    # a family the model is not eligible for falls back; the sweep models are all eligible
+                    assert got == want, (regime, case, cset, algo, got, want)
+                    checked += 1
+            finally:
+                bi.bi_free_model(h)
+    assert checked == len(cases) * 6

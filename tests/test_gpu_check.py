@@ -1,6 +1,8 @@
 """BI_CHECK: out-of-range observations and actions are reported by the input
 check (a device scan plus a stream sync) before any inference kernel runs;
 valid inputs give the same marginals as a model packed without the flag."""
+import os
+
 import numpy as np
 import pytest
 
@@ -27,17 +29,30 @@ def _shared_big(seed, b=8, T=4):
 
 
 CASES = [
-    # (workload maker, flags, algos): agent-resident, dense streaming, sparse streaming
-    (lambda: synth.random_small(610, b=4, T_max=5, per_agent=True), bi.BI_DENSE_A, ("fpi", "vmp", "mmp")),
-    (lambda: _shared_big(611), bi.BI_DENSE_A | bi.BI_FAST_F32, ("vmp", "mmp")),
-    (lambda: _shared_big(612), bi.BI_SPARSE_A, ("vmp", "mmp")),
+    # (workload maker, flags, algos, family): agent-resident, dense streaming, sparse streaming
+    (lambda: synth.random_small(610, b=4, T_max=5, per_agent=True), bi.BI_DENSE_A, ("fpi", "vmp", "mmp"), "agent"),
+    (lambda: _shared_big(611), bi.BI_DENSE_A | bi.BI_FAST_F32, ("vmp", "mmp"), "stream"),
+    (lambda: _shared_big(612), bi.BI_SPARSE_A, ("vmp", "mmp"), "sparse"),
 ]
 
 
+@pytest.fixture
+def family(request):
+    """Force the case's kernel family (the selector would pick by size)."""
+    fam = CASES[request.node.callspec.params["case"]][3]
+    old = os.environ.get("BI_FORCE_PATH")
+    os.environ["BI_FORCE_PATH"] = fam
+    yield fam
+    if old is None:
+        os.environ.pop("BI_FORCE_PATH", None)
+    else:
+        os.environ["BI_FORCE_PATH"] = old
+
+
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_check_passes_valid_inputs_unchanged(case):
+def test_check_passes_valid_inputs_unchanged(case, family):
     torch = _torch()
-    make, flags, algos = CASES[case]
+    make, flags, algos, _ = CASES[case]
     w = make()
     p0 = bi.PackedModel(w.model, flags)
     p1 = bi.PackedModel(w.model, flags | bi.BI_CHECK)
@@ -45,6 +60,7 @@ def test_check_passes_valid_inputs_unchanged(case):
         obs, act = _dev(w.obs), _dev(w.act)
         for algo in algos:
             print(f"[gpu] {w.name} {algo} flags={flags} check", flush=True)
+            assert p1.path(w.b, w.T, algo) == family
             q0 = p0.infer(algo, obs, act, w.iters)
             q1 = p1.infer(algo, obs, act, w.iters)
             torch.cuda.synchronize()
@@ -55,9 +71,9 @@ def test_check_passes_valid_inputs_unchanged(case):
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_check_reports_the_first_bad_entry(case):
+def test_check_reports_the_first_bad_entry(case, family):
     torch = _torch()
-    make, flags, algos = CASES[case]
+    make, flags, algos, _ = CASES[case]
     w = make()
     if w.T < 2:
         pytest.skip("needs actions")

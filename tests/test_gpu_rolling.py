@@ -118,7 +118,7 @@ def test_prior_stream_path(case):
 def test_prior_sparse_path(case):
     w = _shared_model(620 + case, *SHARED[case], sparsity=0.6)
     for algo in ("vmp", "mmp"):
-        _check_prior(w, algo, bi.BI_SPARSE_A, None, 720 + case)
+        _check_prior(w, algo, bi.BI_SPARSE_A, "sparse", 720 + case)
 
 
 @pytest.mark.parametrize("seed", range(4))
@@ -207,4 +207,4 @@ def test_damping_stream_and_sparse_paths(case):
     ws = _shared_model(660 + case, *SHARED[case], sparsity=0.6, iters=3)
     for algo in ("vmp", "mmp"):
         _check_damped(w, algo, bi.BI_DENSE_A | bi.BI_FAST_F32, "stream", 740 + case, 0.45, case == 1)
-        _check_damped(ws, algo, bi.BI_SPARSE_A, None, 760 + case, 0.7, case != 1)
+        _check_damped(ws, algo, bi.BI_SPARSE_A, "sparse", 760 + case, 0.7, case != 1)

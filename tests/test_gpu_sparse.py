@@ -37,14 +37,27 @@ CASES = [
 ]
 
 
+@pytest.fixture
+def force_sparse():
+    # small models would run agent-resident under the selector: force the
+    # sparse kernels, which are what these cases test
+    old = os.environ.get("BI_FORCE_PATH")
+    os.environ["BI_FORCE_PATH"] = "sparse"
+    yield
+    if old is None:
+        os.environ.pop("BI_FORCE_PATH", None)
+    else:
+        os.environ["BI_FORCE_PATH"] = old
+
+
 @pytest.mark.parametrize("case", range(len(CASES)))
 @pytest.mark.parametrize("iters", [1, 3])
-def test_sparse_small_vs_oracle_and_agent(case, iters):
+def test_sparse_small_vs_oracle_and_agent(case, iters, force_sparse):
     n, U, K, deps, b, T, sp = CASES[case]
     w = _shared_model(70 + case, n, U, K, deps, b, T, sp, iters=iters)
     for algo in ("vmp", "mmp"):
         q, pm = run_gpu(w, algo, flags=bi.BI_SPARSE_A)
-        assert pm.workspace(w.b, w.T, algo) is not None, "sparse layout must take the sparse kernels"
+        assert pm.path(w.b, w.T, algo) == "sparse", "the forced sparse kernels must run"
         check_invariants(w, q)
         ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters)
         err = float(np.abs(q - ref).max())
@@ -55,14 +68,11 @@ def test_sparse_small_vs_oracle_and_agent(case, iters):
         try:
             qa, _ = run_gpu(w, algo, pm=pm)
         finally:
-            if old is None:
-                os.environ.pop("BI_FORCE_PATH", None)
-            else:
-                os.environ["BI_FORCE_PATH"] = old
+            os.environ["BI_FORCE_PATH"] = old
         assert float(np.abs(q - qa).max()) <= TOL
         # FPI has no sparse kernel: the same packed model runs it agent-resident
         if algo == "vmp":
-            assert pm.workspace(w.b, w.T, "fpi") is None
+            assert pm.path(w.b, w.T, "fpi") == "agent"
         pm.close()
 
 
@@ -87,6 +97,7 @@ CFG5_AGENTS = [0, 21, 42, 63]
 def test_config5_sparse(algo):
     w = cfg5()
     q, pm = run_gpu(w, algo, flags=bi.BI_SPARSE_A)
+    assert pm.path(w.b, w.T, algo) == "sparse", "the selector must send the large model to the sparse kernels"
     st = pm.stats()
     print(f"[gpu]   config 5 sparse: nnz {st['a_nnz']} device bytes {st['device_bytes']}", flush=True)
     check_invariants(w, q)

@@ -103,6 +103,7 @@ CFG5_AGENTS = [0, 21, 42, 63]
 def test_config5_stream(algo):
     w = cfg5()
     q, pm = run_gpu(w, algo, flags=bi.BI_DENSE_A | bi.BI_FAST_F32)
+    assert pm.path(w.b, w.T, algo) == "stream", "the selector must send the large model to the streaming kernels"
     assert pm.workspace(w.b, w.T, algo) is not None, "config 5 must take the streaming path"
     check_invariants(w, q)
     q2, _ = run_gpu(w, algo, pm=pm)

@@ -47,6 +47,16 @@
  *   h steps before it): a caller may replace D_f by its own prior over the
  *   window's first step (every LN(D_f) above becomes LN(prior_f)), typically
  *   the predictive prior B_f[:,:,u] q_f of an earlier marginal (orc_predict).
+ *   B-dependencies (orc_infer_general): B_f may condition s_{t+1}^f on a
+ *   list of factors g_1 < .. < g_k at t (the general transition model of
+ *   Sec. III-B; the list {f} is the trivial case above).  Then, with
+ *   E[.] the expectation under the factorised q of the step named,
+ *     VMP fwd_{t,f}(s) = E_{q_{t-1}}[LN B_f[s][s_dep]],
+ *         bwd_{t,f}(s) = sum over the factors j whose list holds f of
+ *                        E_{q_{t+1,j}, q_{t,dep(j) \ f}}[LN B_j[s''][s_dep, s_f = s]];
+ *     MMP uses the logs of the same expectations of B (not of LN B) and the
+ *         mean of the forward message and of the backward messages present;
+ *     FPI's prior is the predictive marginal E_{q_{t-1}}[B_f[s][s_dep]].
  *   Soft observations (orc_infer_soft): o_{t,m} is a vector over the K_m
  *   outcomes and every LN(A_m[o_{t,m}, s_dep]) above becomes the expected
  *   log-likelihood sum_o o_{t,m}[o] LN(A_m[o, s_dep]) (the log(A) . o
@@ -73,7 +83,19 @@ typedef struct {
     const double *const *A;
     const double *const *B;
     const double *const *D;
+    const int *bdep_off, *bdep;   /* B-dependency lists; NULL: bdep(f) = {f} */
 } orc_model;
+
+/* B-dependency list of factor f: *k entries */
+static const int *bdeps_of(const orc_model *md, int f, int *k)
+{
+    if (md->bdep_off) {
+        *k = md->bdep_off[f + 1] - md->bdep_off[f];
+        return md->bdep + md->bdep_off[f];
+    }
+    *k = 1;
+    return NULL;   /* trivial: the list is {f} */
+}
 
 static double LN(double x) { return log(x > ORC_EPS ? x : ORC_EPS); }
 
@@ -166,17 +188,74 @@ static void likelihood_messages(const orc_model *md, const double *lls, const si
     }
 }
 
+/* states of the B-dependencies of f taken together (prod of their n) */
+static size_t bdep_states(const orc_model *md, int f)
+{
+    int k;
+    const int *d = bdeps_of(md, f, &k);
+    if (!d) return (size_t)md->n[f];
+    size_t p = 1;
+    for (int i = 0; i < k; ++i) p *= (size_t)md->n[d[i]];
+    return p;
+}
+
 static const double *B_at(const orc_model *md, int f, int a)
 {
     int am = md->mb == 1 ? 0 : a;
-    size_t nf = (size_t)md->n[f];
-    return md->B[f] + (size_t)am * nf * nf * (size_t)md->U[f];
+    return md->B[f] + (size_t)am * (size_t)md->n[f] * bdep_states(md, f) * (size_t)md->U[f];
 }
 
-/* B_f[i][j][u] */
-static double Bv(const orc_model *md, const double *Bf, int f, int i, int j, int u)
+/*
+ * Contraction of B_f over its B-dependencies (Sec. III-B transition model,
+ * B_f[i][s_{g_1}]..[s_{g_k}][u], row-major over the list):
+ *   sum_{s_dep} val(B_f[i][s_dep][u]) prod_{g in dep, g != skip} q[qoff[g] + s_g]
+ * with val = LN when logB, the identity otherwise; the dependency at list
+ * position `skip` (-1: none) is held at state `fixv` and not weighted.
+ * q holds the marginals of one step of one agent ([sum n]).
+ */
+static double b_contract(const orc_model *md, const double *Bf, int f, int i, int u, const double *q,
+                         const int *qoff, int skip, int fixv, int logB)
 {
-    return Bf[((size_t)i * md->n[f] + j) * md->U[f] + u];
+    int k;
+    const int *d = bdeps_of(md, f, &k);
+    int dl[ORC_MAX_RANK], idx[ORC_MAX_RANK];
+    for (int j = 0; j < k; ++j) {
+        dl[j] = d ? d[j] : f;
+        idx[j] = j == skip ? fixv : 0;
+    }
+    const size_t P = bdep_states(md, f);
+    const int U = md->U[f];
+    double acc = 0.0;
+    for (;;) {
+        size_t flat = 0;
+        double w = 1.0;
+        for (int j = 0; j < k; ++j) {
+            flat = flat * (size_t)md->n[dl[j]] + (size_t)idx[j];
+            if (j != skip) w *= q[qoff[dl[j]] + idx[j]];
+        }
+        const double b = Bf[((size_t)i * P + flat) * U + u];
+        acc += (logB ? LN(b) : b) * w;
+        /* odometer over the free positions, last fastest */
+        int j = k - 1;
+        for (; j >= 0; --j) {
+            if (j == skip) continue;
+            if (++idx[j] < md->n[dl[j]]) break;
+            idx[j] = 0;
+        }
+        if (j < 0) break;
+    }
+    return acc;
+}
+
+/* Position of factor f in the B-dependency list of j, or -1. */
+static int bdep_pos(const orc_model *md, int j, int f)
+{
+    int k;
+    const int *d = bdeps_of(md, j, &k);
+    if (!d) return j == f ? 0 : -1;
+    for (int i = 0; i < k; ++i)
+        if (d[i] == f) return i;
+    return -1;
 }
 
 /* p(s_1) of agent a: the caller's prior (prior: [b][ntot]) or D_f */
@@ -204,14 +283,11 @@ static void run_fpi(const orc_model *md, int a, int T, const orc_obs *obs, const
                 const double *p0 = first_prior(md, prior, f, a, qoff, ntot);
                 for (int s = 0; s < nf; ++s) logp[qoff[f] + s] = LN(p0[s]);
             } else {
+                /* predictive marginal of s_t^f under the factorised q_{t-1} */
                 const double *Bf = B_at(md, f, a);
                 const int u = act[(size_t)(t - 1) * md->F + f];
-                const double *qp = q + (size_t)(t - 1) * ntot + qoff[f];
-                for (int i = 0; i < nf; ++i) {
-                    double p = 0.0;
-                    for (int j = 0; j < nf; ++j) p += Bv(md, Bf, f, i, j, u) * qp[j];
-                    logp[qoff[f] + i] = LN(p);
-                }
+                const double *qp = q + (size_t)(t - 1) * ntot;
+                for (int i = 0; i < nf; ++i) logp[qoff[f] + i] = LN(b_contract(md, Bf, f, i, u, qp, qoff, -1, 0, 0));
             }
             for (int s = 0; s < nf; ++s) cur[qoff[f] + s] = 1.0 / nf;
         }
@@ -244,44 +320,51 @@ static void run_window(const orc_model *md, int algo, int a, int T, const orc_ob
             likelihood_messages(md, lls, poff, q + (size_t)t * ntot, qoff, ntot, lam + (size_t)t * ntot);
         }
         for (int t = 0; t < T; ++t) {
+            /* Transition messages (Sec. III-B joint): the forward one from
+             * B_f given the factors it depends on at t-1, and one backward
+             * message from every factor j whose B-dependencies contain f
+             * (its "children"), given s_{t+1}^j and the other dependencies
+             * of j at t.  With trivial lists: B_f[s][s'] q_{t-1,f}(s') and
+             * q_{t+1,f}(s'') B_f[s''][s]. */
+            const double *qprev = t > 0 ? q + (size_t)(t - 1) * ntot : NULL;
+            const double *qcur = q + (size_t)t * ntot;
+            const double *qnext = t + 1 < T ? q + (size_t)(t + 1) * ntot : NULL;
             for (int f = 0; f < md->F; ++f) {
                 const int nf = md->n[f];
                 const double *Bf = B_at(md, f, a);
                 const double *p0 = first_prior(md, prior, f, a, qoff, ntot);
-                const double *qprev = t > 0 ? q + (size_t)(t - 1) * ntot + qoff[f] : NULL;
-                const double *qnext = t + 1 < T ? q + (size_t)(t + 1) * ntot + qoff[f] : NULL;
                 const int uprev = t > 0 ? act[(size_t)(t - 1) * md->F + f] : 0;
-                const int unext = t + 1 < T ? act[(size_t)t * md->F + f] : 0;
                 double *v = qn + (size_t)t * ntot + qoff[f];
                 for (int s = 0; s < nf; ++s) {
-                    double fwd, bwd = 0.0;
-                    if (algo == ORC_VMP) {
-                        if (t == 0) {
-                            fwd = LN(p0[s]);
-                        } else {
-                            fwd = 0.0;
-                            for (int sp = 0; sp < nf; ++sp) fwd += LN(Bv(md, Bf, f, s, sp, uprev)) * qprev[sp];
-                        }
-                        if (qnext)
-                            for (int sn = 0; sn < nf; ++sn) bwd += qnext[sn] * LN(Bv(md, Bf, f, sn, s, unext));
-                        v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd + bwd;
-                    } else { /* MMP */
-                        if (t == 0) {
-                            fwd = LN(p0[s]);
-                        } else {
-                            double p = 0.0;
-                            for (int sp = 0; sp < nf; ++sp) p += Bv(md, Bf, f, s, sp, uprev) * qprev[sp];
-                            fwd = LN(p);
-                        }
-                        if (qnext) {
-                            double p = 0.0;
-                            for (int sn = 0; sn < nf; ++sn) p += Bv(md, Bf, f, sn, s, unext) * qnext[sn];
-                            bwd = LN(p);
-                            v[s] = lam[(size_t)t * ntot + qoff[f] + s] + 0.5 * (fwd + bwd);
-                        } else {
-                            v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd;
+                    double fwd;
+                    if (t == 0)
+                        fwd = LN(p0[s]);
+                    else if (algo == ORC_VMP)
+                        fwd = b_contract(md, Bf, f, s, uprev, qprev, qoff, -1, 0, 1);
+                    else
+                        fwd = LN(b_contract(md, Bf, f, s, uprev, qprev, qoff, -1, 0, 0));
+                    double bwd = 0.0;   /* VMP: sum of the backward messages; MMP: sum of their logs */
+                    int children = 0;
+                    if (qnext) {
+                        for (int j = 0; j < md->F; ++j) {
+                            const int pos = bdep_pos(md, j, f);
+                            if (pos < 0) continue;
+                            const double *Bj = B_at(md, j, a);
+                            const int unext = act[(size_t)t * md->F + j];
+                            double m = 0.0;
+                            for (int sn = 0; sn < md->n[j]; ++sn)
+                                m += qnext[qoff[j] + sn] *
+                                     b_contract(md, Bj, j, sn, unext, qcur, qoff, pos, s, algo == ORC_VMP);
+                            bwd += algo == ORC_VMP ? m : LN(m);
+                            ++children;
                         }
                     }
+                    if (algo == ORC_VMP)
+                        v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd + bwd;
+                    else if (children > 0)   /* mean of the messages present */
+                        v[s] = lam[(size_t)t * ntot + qoff[f] + s] + (fwd + bwd) / (double)(1 + children);
+                    else
+                        v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd;
                 }
                 softmax(v, nf);
             }
@@ -292,11 +375,28 @@ static void run_window(const orc_model *md, int algo, int a, int T, const orc_ob
 
 /* Shared driver of orc_infer_ex and orc_infer_soft: exactly one of hard
  * ([b][T][M] outcomes) and soft ([b][T][sum K] observation vectors) is set. */
+/* Checks B-dependency lists (NULL: trivial): non-empty, ascending, in range. */
+static int bdeps_ok(int F, const int *bdep_off, const int *bdep)
+{
+    if (!bdep_off) return 1;
+    if (!bdep || bdep_off[0] != 0) return 0;
+    for (int f = 0; f < F; ++f) {
+        const int k = bdep_off[f + 1] - bdep_off[f];
+        if (k < 1 || k > ORC_MAX_RANK) return 0;
+        for (int i = bdep_off[f]; i < bdep_off[f + 1]; ++i) {
+            if (bdep[i] < 0 || bdep[i] >= F) return 0;
+            if (i > bdep_off[f] && bdep[i] <= bdep[i - 1]) return 0;
+        }
+    }
+    return 1;
+}
+
 static int run_all(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
                    const int *dep, int mb, const double *const *A, const double *const *B, const double *const *D,
-                   int b, int T, const int *hard, const double *soft, const int *act, const double *prior,
-                   double tau, int iters, double *q, int nthreads)
+                   const int *bdep_off, const int *bdep, int b, int T, const int *hard, const double *soft,
+                   const int *act, const double *prior, double tau, int iters, double *q, int nthreads)
 {
+    if (F < 1 || !bdeps_ok(F, bdep_off, bdep)) return -1;
     if (algo < 0 || algo > 2 || F < 1 || M < 1 || b < 1 || T < 1 || iters < 1) return -1;
     if (!(tau > 0.0 && tau <= 1.0)) return -1;
     if (mb != 1 && mb != b) return -1;
@@ -313,7 +413,7 @@ static int run_all(int algo, int F, const int *n, const int *U, int M, const int
         qoff[f] = ntot;
         ntot += n[f];
     }
-    orc_model md = {F, M, mb, n, U, K, dep_off, dep, A, B, D};
+    orc_model md = {F, M, mb, n, U, K, dep_off, dep, A, B, D, bdep_off, bdep};
     poff[0] = 0;
     for (int m = 0; m < M && !bad; ++m) {
         int k = dep_off[m + 1] - dep_off[m];
@@ -360,8 +460,8 @@ int orc_infer_ex(int algo, int F, const int *n, const int *U, int M, const int *
                  double *q, int nthreads)
 {
     if (!obs) return -1;
-    return run_all(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, b, T, obs, NULL, act, prior, tau, iters, q,
-                   nthreads);
+    return run_all(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, NULL, NULL, b, T, obs, NULL, act, prior, tau,
+                   iters, q, nthreads);
 }
 
 /*
@@ -375,8 +475,24 @@ int orc_infer_soft(int algo, int F, const int *n, const int *U, int M, const int
                    int iters, double *q, int nthreads)
 {
     if (!obs_soft) return -1;
-    return run_all(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, b, T, NULL, obs_soft, act, prior, tau, iters,
-                   q, nthreads);
+    return run_all(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, NULL, NULL, b, T, NULL, obs_soft, act, prior, tau,
+                   iters, q, nthreads);
+}
+
+/*
+ * The general entry point: B-dependency lists bdep_off [F+1] / bdep (B_f of
+ * shape [mb][n_f][n_{g_1}]..[n_{g_k}][U_f]; NULL: every list is {f}), and
+ * either integer observations (obs) or soft ones (obs_soft), the other NULL.
+ */
+int orc_infer_general(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
+                      const int *dep, int mb, const double *const *A, const double *const *B,
+                      const double *const *D, const int *bdep_off, const int *bdep, int b, int T, const int *obs,
+                      const double *obs_soft, const int *act, const double *prior, double tau, int iters, double *q,
+                      int nthreads)
+{
+    if ((obs == NULL) == (obs_soft == NULL)) return -1;
+    return run_all(algo, F, n, U, M, K, dep_off, dep, mb, A, B, D, bdep_off, bdep, b, T, obs, obs_soft, act, prior,
+                   tau, iters, q, nthreads);
 }
 
 int orc_infer_prior(int algo, int F, const int *n, const int *U, int M, const int *K, const int *dep_off,
@@ -425,6 +541,39 @@ int orc_predict(int F, const int *n, const int *U, int mb, const double *const *
         }
     }
     return 0;
+}
+
+/*
+ * Predictive prior with B-dependency lists (NULL: trivial, as orc_predict):
+ *   out[a][f](i) = sum_{s_dep} B_f[i][s_dep][u_{a,f}] prod_{g in dep(f)} q[a][g](s_g)
+ * the predictive marginal of s_{t+1}^f under the factorised q.
+ */
+int orc_predict_general(int F, const int *n, const int *U, int mb, const double *const *B, const int *bdep_off,
+                        const int *bdep, int b, const double *q, const int *act, double *out)
+{
+    if (F < 1 || b < 1 || (mb != 1 && mb != b) || !n || !U || !B || !q || !act || !out) return -1;
+    if (!bdeps_ok(F, bdep_off, bdep)) return -1;
+    int *qoff = (int *)malloc(sizeof(int) * (size_t)F);
+    if (!qoff) return -1;
+    int ntot = 0;
+    for (int f = 0; f < F; ++f) {
+        if (n[f] < 1 || U[f] < 1) { free(qoff); return -1; }
+        qoff[f] = ntot;
+        ntot += n[f];
+    }
+    orc_model md = {F, 0, mb, n, U, NULL, NULL, NULL, NULL, B, NULL, bdep_off, bdep};
+    int bad = 0;
+    for (int a = 0; a < b && !bad; ++a) {
+        for (int f = 0; f < F; ++f) {
+            const int u = act[(size_t)a * F + f];
+            if (u < 0 || u >= U[f]) { bad = 1; break; }
+            const double *Bf = B_at(&md, f, a);
+            for (int i = 0; i < n[f]; ++i)
+                out[(size_t)a * ntot + qoff[f] + i] = b_contract(&md, Bf, f, i, u, q + (size_t)a * ntot, qoff, -1, 0, 0);
+        }
+    }
+    free(qoff);
+    return bad ? -1 : 0;
 }
 
 /* Number of OpenMP threads orc_infer uses when nthreads <= 0. */

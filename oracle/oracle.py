@@ -62,6 +62,17 @@ def load_library(path: str):
                                    P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p), ctypes.c_int,
                                    ctypes.c_int, P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double),
                                    ctypes.c_double, ctypes.c_int, P(ctypes.c_double), ctypes.c_int]
+    lib.orc_infer_general.restype = ctypes.c_int
+    lib.orc_infer_general.argtypes = [ctypes.c_int, ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                      P(ctypes.c_int), P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                      P(ctypes.c_void_p), P(ctypes.c_void_p), P(ctypes.c_void_p),
+                                      P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int, ctypes.c_int,
+                                      P(ctypes.c_int), P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double),
+                                      ctypes.c_double, ctypes.c_int, P(ctypes.c_double), ctypes.c_int]
+    lib.orc_predict_general.restype = ctypes.c_int
+    lib.orc_predict_general.argtypes = [ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                        P(ctypes.c_void_p), P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int,
+                                        P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double)]
     lib.orc_predict.restype = ctypes.c_int
     lib.orc_predict.argtypes = [ctypes.c_int, P(ctypes.c_int), P(ctypes.c_int), ctypes.c_int, P(ctypes.c_void_p),
                                 ctypes.c_int, P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double)]
@@ -134,7 +145,21 @@ def _run(algo, model, obs, obs_soft, act, iters, agents, threads, lib, prior, da
     ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))  # noqa: E731
     dp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))  # noqa: E731
     pr = None if prior is None else np.ascontiguousarray(prior, dtype=np.float64).reshape(b, int(sum(model.n)))
-    if obs_soft is not None:
+    bdeps = getattr(model, "bdeps", None)
+    if bdeps is not None:
+        # B-dependency lists (general transition model)
+        bd_off = _i32(np.cumsum([0] + [len(d) for d in bdeps]))
+        bd = _i32([g for d in bdeps for g in d])
+        os_c = None if obs_soft is None else np.ascontiguousarray(obs_soft, dtype=np.float64)
+        obs_c = None if obs is None else _i32(obs)
+        if os_c is not None and os_c.shape != (b, T, int(sum(model.K))):
+            raise ValueError(f"soft observations of shape {os_c.shape}, expected {(b, T, int(sum(model.K)))}")
+        rc = lib.orc_infer_general(ALGOS[algo], F, ip(n), ip(U), M, ip(K), ip(dep_off), ip(dep), int(model.mb),
+                                   ptrs(A), ptrs(B), ptrs(D), ip(bd_off), ip(bd), b, T,
+                                   None if obs_c is None else ip(obs_c), None if os_c is None else dp(os_c),
+                                   ip(act_c), None if pr is None else dp(pr), float(damping), int(iters), dp(q),
+                                   int(threads))
+    elif obs_soft is not None:
         os_c = np.ascontiguousarray(obs_soft, dtype=np.float64)
         if os_c.shape != (b, T, int(sum(model.K))):
             raise ValueError(f"soft observations of shape {os_c.shape}, expected {(b, T, int(sum(model.K)))}")
@@ -157,7 +182,8 @@ def _run(algo, model, obs, obs_soft, act, iters, agents, threads, lib, prior, da
 
 def predict(model, q: np.ndarray, act: np.ndarray, lib=None) -> np.ndarray:
     """Predictive prior [b][sum n] (float64) of the next step: for every agent
-    and factor f, B_f[:, :, u_f] q_f, with q [b][sum n] and act [b][F]."""
+    and factor f, B_f[:, :, u_f] q_f, with q [b][sum n] and act [b][F] (with
+    B-dependency lists: B_f contracted with the marginals of its list)."""
     if lib is None:
         lib = _load()
     q = np.ascontiguousarray(q, dtype=np.float64)
@@ -169,9 +195,17 @@ def predict(model, q: np.ndarray, act: np.ndarray, lib=None) -> np.ndarray:
     ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))  # noqa: E731
     act_c = _i32(np.asarray(act).reshape(b, F))
     out = np.zeros((b, int(sum(model.n))), dtype=np.float64)
-    rc = lib.orc_predict(F, ip(n), ip(U), int(model.mb), ptrs(B), b,
-                         q.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), ip(act_c),
-                         out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    bdeps = getattr(model, "bdeps", None)
+    if bdeps is not None:
+        bd_off = _i32(np.cumsum([0] + [len(d) for d in bdeps]))
+        bd = _i32([g for d in bdeps for g in d])
+        rc = lib.orc_predict_general(F, ip(n), ip(U), int(model.mb), ptrs(B), ip(bd_off), ip(bd), b,
+                                     q.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), ip(act_c),
+                                     out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    else:
+        rc = lib.orc_predict(F, ip(n), ip(U), int(model.mb), ptrs(B), b,
+                             q.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), ip(act_c),
+                             out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
     if rc != 0:
         raise ValueError(f"oracle rejected the arguments (rc={rc})")
     return out

@@ -11,7 +11,12 @@ notation"):
   < d_k)``; ``A[m][a, o, s...] = P(o^m = o | s^{d_1}, ..., s^{d_k})`` (the outcome
   axis first, then the dependency axes in list order).
 * ``B[f]``: float32 ``[mb][n_f][n_f][U_f]``; ``B[f][a, i, j, u] = P(s_{t+1}^f = i |
-  s_t^f = j, u_t^f = u)`` (trivial B-dependencies only, as in Sec. III-B).
+  s_t^f = j, u_t^f = u)`` (trivial B-dependencies, the case the paper's
+  layouts support, Sec. III-B).  With B-dependency lists ``bdeps[f] =
+  (g_1 < ... < g_k)`` (the general transition model of Sec. III-B),
+  ``B[f]`` is ``[mb][n_f][n_{g_1}]...[n_{g_k}][U_f]`` with
+  ``B[f][a, i, j_1, ..., j_k, u] = P(s_{t+1}^f = i | s_t^{g_1} = j_1, ..., u_t^f = u)``;
+  ``bdeps = None`` means ``bdeps[f] = [f]``.
 * ``D[f]``: float32 ``[mb][n_f]``, the prior ``p(s_1^f)``.
 * ``mb`` is 1 for a model shared by every agent, else the number of agents.
 
@@ -46,6 +51,15 @@ class Model:
     A: List[np.ndarray]          # see module docstring
     B: List[np.ndarray]
     D: List[np.ndarray]
+    bdeps: Optional[List[List[int]]] = None   # B-dependency lists (None: trivial)
+
+    def bdep(self, f: int) -> List[int]:
+        """Factors whose current states condition the next state of f."""
+        return list(self.bdeps[f]) if self.bdeps is not None else [f]
+
+    @property
+    def trivial_bdeps(self) -> bool:
+        return self.bdeps is None or all(list(d) == [f] for f, d in enumerate(self.bdeps))
 
     @property
     def F(self) -> int:
@@ -67,7 +81,8 @@ class Model:
         return Model(list(self.n), list(self.U), list(self.K), [list(d) for d in self.deps], len(idx),
                      [np.ascontiguousarray(a[idx]) for a in self.A],
                      [np.ascontiguousarray(b[idx]) for b in self.B],
-                     [np.ascontiguousarray(d[idx]) for d in self.D])
+                     [np.ascontiguousarray(d[idx]) for d in self.D],
+                     None if self.bdeps is None else [list(d) for d in self.bdeps])
 
 
 @dataclasses.dataclass
@@ -122,7 +137,7 @@ def _sparsify_columns(rng: np.random.Generator, a: np.ndarray, axis: int, p_zero
 
 
 def make_model(rng: np.random.Generator, n, U, K, deps, mb: int, alpha_A: float = 1.0, alpha_B: float = 1.0,
-               sparsity: float = 0.0, uniform_D: bool = True) -> Model:
+               sparsity: float = 0.0, uniform_D: bool = True, bdeps=None) -> Model:
     n = [int(x) for x in n]
     U = [int(x) for x in U]
     K = [int(x) for x in K]
@@ -134,9 +149,12 @@ def make_model(rng: np.random.Generator, n, U, K, deps, mb: int, alpha_A: float 
         if sparsity > 0:
             a = _sparsify_columns(rng, a, 1, sparsity)
         A.append(np.ascontiguousarray(a, dtype=np.float32))
+    if bdeps is not None:
+        bdeps = [sorted(int(g) for g in d) for d in bdeps]
     B = []
     for f in range(len(n)):
-        b = _dirichlet_columns(rng, alpha_B, (mb,), n[f], (n[f], U[f]))
+        cond = [n[g] for g in bdeps[f]] if bdeps is not None else [n[f]]
+        b = _dirichlet_columns(rng, alpha_B, (mb,), n[f], tuple(cond) + (U[f],))
         B.append(np.ascontiguousarray(b, dtype=np.float32))
     D = []
     for f in range(len(n)):
@@ -145,7 +163,7 @@ def make_model(rng: np.random.Generator, n, U, K, deps, mb: int, alpha_A: float 
         else:
             d = _dirichlet_columns(rng, 1.0, (mb,), n[f], ())
         D.append(np.ascontiguousarray(d, dtype=np.float32))
-    return Model(n, U, K, deps, mb, A, B, D)
+    return Model(n, U, K, deps, mb, A, B, D, bdeps)
 
 
 def _sample_cat(rng: np.random.Generator, p: np.ndarray) -> np.ndarray:
@@ -172,10 +190,11 @@ def sample_sequences(rng: np.random.Generator, model: Model, b: int, T: int):
             col = _gather_col(model.A[m], ai, [s[:, f] for f in model.deps[m]])
             obs[:, t, m] = _sample_cat(rng, col)
         if t + 1 < T:
+            prev = s.copy()                                  # every factor moves from the same s_t
             for f in range(F):
                 u = rng.integers(0, model.U[f], size=b)
                 act[:, t, f] = u
-                col = model.B[f][ai, :, s[:, f], u]          # [b][n_f]
+                col = model.B[f][(ai, slice(None)) + tuple(prev[:, g] for g in model.bdep(f)) + (u,)]   # [b][n_f]
                 s[:, f] = _sample_cat(rng, col)
     return obs, act
 

@@ -21,6 +21,11 @@ def LN(x):
     return np.log(np.maximum(np.asarray(x, dtype=np.float64), EPS))
 
 
+def _bdep(model, f):
+    bd = getattr(model, "bdeps", None)
+    return list(bd[f]) if bd is not None else [f]
+
+
 def _agent(arr, mb, a):
     return np.asarray(arr[0 if mb == 1 else a], dtype=np.float64)
 
@@ -63,8 +68,9 @@ def window_log_joint(model, obs_a, act_a, a, soft=False):
         lp = add(LN(_agent(model.D[f], model.mb, a)), [ax(0, f)])
     for t in range(1, T):
         for f in range(F):
-            Bf = _agent(model.B[f], model.mb, a)[:, :, act_a[t - 1, f]]   # [s_t][s_{t-1}]
-            lp = add(LN(Bf), [ax(t, f), ax(t - 1, f)])
+            # B_f[s_t^f][s_{t-1}^{g_1}]..[s_{t-1}^{g_k}] (g: B-dependency list, {f} if trivial)
+            Bf = _agent(model.B[f], model.mb, a)[..., act_a[t - 1, f]]
+            lp = add(LN(Bf), [ax(t, f)] + [ax(t - 1, g) for g in _bdep(model, f)])
     for t in range(T):
         for m, d in enumerate(model.deps):
             lp = add(obs_loglik(model, a, m, obs_a[t], soft), [ax(t, f) for f in d])
@@ -125,8 +131,13 @@ def fpi_bruteforce(model, obs, act, iters, soft=False):
                 if t == 0:
                     prior = _agent(model.D[f], model.mb, a)
                 else:
-                    Bf = _agent(model.B[f], model.mb, a)[:, :, act[a, t - 1, f]]
-                    prior = Bf @ prev[f]
+                    # predictive marginal: B_f contracted with the previous step's
+                    # marginals of its B-dependencies
+                    Bf = _agent(model.B[f], model.mb, a)[..., act[a, t - 1, f]]
+                    dl = _bdep(model, f)
+                    letters = string.ascii_letters[1:1 + len(dl)]
+                    prior = np.einsum("a" + letters + "," + ",".join(letters) + "->a", Bf,
+                                      *[prev[g] for g in dl])
                 view = [1] * F
                 view[f] = model.n[f]
                 lp = lp + LN(prior).reshape(view)

@@ -467,6 +467,95 @@ def pin_soft_filter(infer):
     return err
 
 
+def _bdep_model(seed, F, n_max=4, M_max=3, K_max=3, T=4, b=2, singleton_A=False, lists=None):
+    """Small model with random B-dependency lists (random non-empty subsets)."""
+    rd = np.random.Generator(np.random.PCG64(seed))
+    n = [int(x) for x in rd.integers(2, n_max + 1, size=F)]
+    U = [int(x) for x in rd.integers(1, 3, size=F)]
+    if singleton_A:
+        deps = [[f] for f in range(F)]
+    else:
+        deps = [sorted(set(int(g) for g in rd.choice(F, size=int(rd.integers(1, F + 1)), replace=False)))
+                for _ in range(int(rd.integers(1, M_max + 1)))]
+    K = [int(x) for x in rd.integers(2, K_max + 1, size=len(deps))]
+    if lists is None:
+        lists = [sorted(set(int(g) for g in rd.choice(F, size=int(rd.integers(1, F + 1)), replace=False)))
+                 for _ in range(F)]
+    model = synth.make_model(rd, n, U, K, deps, b, 1.0, 1.0, uniform_D=False, bdeps=lists)
+    obs, act = synth.sample_sequences(rd, model, b, T)
+    return model, obs, act
+
+
+def pin_bdeps_trivial_lists(infer):
+    """Listing every factor's own previous state ({f}) through the general
+    B-dependency path is the trivial model, result for result."""
+    err = 0.0
+    for seed in range(4):
+        w = synth.random_small(500 + seed, F_max=3, n_max=4, T_max=5, b=3)
+        m = w.model
+        mg = synth.Model(m.n, m.U, m.K, m.deps, m.mb, m.A, m.B, m.D, [[f] for f in range(m.F)])
+        for algo in ("fpi", "vmp", "mmp"):
+            err = max(err, float(np.abs(infer(algo, mg, w.obs, w.act, w.iters) -
+                                        infer(algo, m, w.obs, w.act, w.iters)).max()))
+    return err
+
+
+def pin_bdeps_bruteforce(infer):
+    """General B-dependencies against enumeration: the transition terms of
+    the joint become log B_f[s_t^f][s_{t-1}^{dep(f)}] (Sec. III-B), VMP is the
+    mean-field update over that joint, and FPI uses the predictive marginal
+    of the enumerated previous-step posterior."""
+    err = 0.0
+    for seed in range(8):
+        model, obs, act = _bdep_model(600 + seed, F=2 + seed % 2, T=3 if seed % 2 else 4)
+        err = max(err, float(np.abs(infer("vmp", model, obs, act, 5) -
+                                    bf.vmp_bruteforce(model, obs, act, 5)).max()))
+        err = max(err, float(np.abs(infer("fpi", model, obs, act, 4) -
+                                    bf.fpi_bruteforce(model, obs, act, 4)).max()))
+    return err
+
+
+def pin_bdeps_uninformative_transitions(infer):
+    """Transitions that ignore every dependency (B_f[s][s_dep][u] = p_u(s))
+    with a factorised likelihood (one modality per factor): every backward
+    message is constant in s and cancels, so
+      VMP: q_{t,f} ~ L_{t,f} p_f  (D_f at t = 0);
+      MMP: q_{t,f} ~ L_{t,f} p_f^(1 / (1 + c_f)) inside the window, with c_f
+           the number of factors whose B-dependency list holds f (the mean
+           of the forward message and the c_f backward ones), L p at t = T-1."""
+    err = 0.0
+    for seed, lists in [(31, [[0, 1], [0, 1], [1, 2]]), (32, [[1], [0, 1, 2], [0, 1]]), (33, [[0, 1], [0]])]:
+        F = len(lists)
+        model, obs, act = _bdep_model(seed, F=F, T=5, b=2, singleton_A=True, lists=lists)
+        rd = np.random.Generator(np.random.PCG64(seed + 100))
+        for f in range(F):   # B_f constant over the dependency states
+            shp = model.B[f].shape
+            p = rd.dirichlet(np.ones(shp[1]), size=(shp[0], shp[-1]))       # [mb][U][n_f]
+            p = np.transpose(p, (0, 2, 1)).reshape(shp[0], shp[1], *([1] * (len(shp) - 3)), shp[-1])
+            model.B[f] = np.ascontiguousarray(np.broadcast_to(p, shp), dtype=np.float32)
+        obs, act = synth.sample_sequences(rd, model, 2, 5)
+        children = [sum(f in d for d in lists) for f in range(F)]
+        qv = infer("vmp", model, obs, act, 3)
+        qm = infer("mmp", model, obs, act, 3)
+        offs = np.cumsum([0] + list(model.n))
+        T = obs.shape[1]
+        for a in range(obs.shape[0]):
+            for t in range(T):
+                for f in range(F):
+                    L = np.float64(model.A[f][a][obs[a, t, f]])
+                    if t == 0:
+                        prior = np.float64(model.D[f][a])
+                    else:
+                        prior = np.float64(model.B[f][a][(slice(None),) + (0,) * (model.B[f].ndim - 3) +
+                                                        (act[a, t - 1, f],)])
+                    v = L * prior
+                    err = max(err, float(np.abs(qv[a, t, offs[f]:offs[f + 1]] - v / v.sum()).max()))
+                    c = children[f] if t + 1 < T else 0
+                    wm = L * prior ** (1.0 / (1 + c))
+                    err = max(err, float(np.abs(qm[a, t, offs[f]:offs[f + 1]] - wm / wm.sum()).max()))
+    return err
+
+
 ALL_PINS = {
     "bayes_filter": (pin_bayes_filter, 1e-12),
     "golden_hmm2": (pin_golden_hmm2, 1e-7),
@@ -485,4 +574,7 @@ ALL_PINS = {
     "soft_onehot": (pin_soft_onehot, 0.0),
     "soft_bruteforce": (pin_soft_bruteforce, 1e-12),
     "soft_filter": (pin_soft_filter, 1e-12),
+    "bdeps_trivial_lists": (pin_bdeps_trivial_lists, 0.0),
+    "bdeps_bruteforce": (pin_bdeps_bruteforce, 1e-12),
+    "bdeps_uninformative_transitions": (pin_bdeps_uninformative_transitions, 1e-12),
 }

@@ -14,18 +14,20 @@ SRC = os.path.join(os.path.dirname(orc_mod.__file__), "bi_oracle.c")
 
 # (name, text in bi_oracle.c, replacement, count)
 MUTANTS = [
-    ("vmp_fwd_transposed", "fwd += LN(Bv(md, Bf, f, s, sp, uprev)) * qprev[sp];",
-     "fwd += LN(Bv(md, Bf, f, sp, s, uprev)) * qprev[sp];", 1),
-    ("vmp_bwd_transposed", "bwd += qnext[sn] * LN(Bv(md, Bf, f, sn, s, unext));",
-     "bwd += qnext[sn] * LN(Bv(md, Bf, f, s, sn, unext));", 1),
-    ("mmp_fwd_transposed", "p += Bv(md, Bf, f, s, sp, uprev) * qprev[sp];",
-     "p += Bv(md, Bf, f, sp, s, uprev) * qprev[sp];", 1),
-    ("mmp_bwd_transposed", "p += Bv(md, Bf, f, sn, s, unext) * qnext[sn];",
-     "p += Bv(md, Bf, f, s, sn, unext) * qnext[sn];", 1),
-    ("mmp_no_half", "0.5 * (fwd + bwd)", "(fwd + bwd)", 1),
+    ("b_axis_swapped", "const double b = Bf[((size_t)i * P + flat) * U + u];",
+     "const double b = Bf[((size_t)(flat % md->n[f]) * P + (i + flat / md->n[f]) % P) * U + u];", 1),
+    ("b_fixed_state_weighted", "if (j != skip) w *= q[qoff[dl[j]] + idx[j]];", "w *= q[qoff[dl[j]] + idx[j]];", 1),
+    ("vmp_linear_b", "acc += (logB ? LN(b) : b) * w;", "acc += b * w;", 1),
+    ("fwd_from_same_step", "fwd = b_contract(md, Bf, f, s, uprev, qprev, qoff, -1, 0, 1);",
+     "fwd = b_contract(md, Bf, f, s, uprev, qcur, qoff, -1, 0, 1);", 1),
+    ("mmp_bwd_from_same_step", "m += qnext[qoff[j] + sn] *", "m += qcur[qoff[j] + sn] *", 1),
+    ("only_self_children", "if (pos < 0) continue;", "if (pos < 0 || j != f) continue;", 1),
+    ("mmp_mean_of_two", "(fwd + bwd) / (double)(1 + children)", "0.5 * (fwd + bwd)", 1),
+    ("fpi_prior_expected_log", "LN(b_contract(md, Bf, f, i, u, qp, qoff, -1, 0, 0))",
+     "b_contract(md, Bf, f, i, u, qp, qoff, -1, 0, 1)", 1),
+    ("mmp_no_half", "(fwd + bwd) / (double)(1 + children)", "(fwd + bwd)", 1),
     ("mmp_last_half", "v[s] = lam[(size_t)t * ntot + qoff[f] + s] + fwd;",
      "v[s] = lam[(size_t)t * ntot + qoff[f] + s] + 0.5 * fwd;", 1),
-    ("fpi_prior_transposed", "p += Bv(md, Bf, f, i, j, u) * qp[j];", "p += Bv(md, Bf, f, j, i, u) * qp[j];", 1),
     ("lik_keeps_own_factor", "if (j != i) w *= q[qoff[d[j]] + idx[j]];", "w *= q[qoff[d[j]] + idx[j]];", 1),
     ("lik_axis_order", "for (int i = k - 1; i >= 0; --i) {\n                if (++idx[i]",
      "for (int i = 0; i < k; ++i) {\n                if (++idx[i]", 1),

@@ -96,6 +96,14 @@ typedef struct bi_model_desc {
     const int32_t *dep;     /* [dep_off[M]] host */
     int32_t model_batch;
     uint32_t flags;
+    /* B-dependency lists (Sec. III-B, transition model): factor f's next state
+     * depends on the current states of bdep[bdep_off[f] .. bdep_off[f+1]),
+     * ascending, 1 to 4 factors, each factor in at most 8 lists; B[f] is then
+     * [model_batch][n_f][n_{g_1}]..[n_{g_k}][U_f].  NULL (both): every list is
+     * {f}, B[f] = [model_batch][n_f][n_f][U_f].  Models with other lists run
+     * agent-resident (the streaming kernels take trivial lists only). */
+    const int32_t *bdep_off;
+    const int32_t *bdep;
 } bi_model_desc;
 
 /* Opaque handle: host-side metadata of a packed model (the packed tensors

@@ -45,7 +45,8 @@ class bi_model_desc(ctypes.Structure):
     _fields_ = [("F", ctypes.c_int32), ("n", ctypes.POINTER(ctypes.c_int32)), ("U", ctypes.POINTER(ctypes.c_int32)),
                 ("M", ctypes.c_int32), ("K", ctypes.POINTER(ctypes.c_int32)),
                 ("dep_off", ctypes.POINTER(ctypes.c_int32)), ("dep", ctypes.POINTER(ctypes.c_int32)),
-                ("model_batch", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+                ("model_batch", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("bdep_off", ctypes.POINTER(ctypes.c_int32)), ("bdep", ctypes.POINTER(ctypes.c_int32))]
 
 
 class bi_profile_entry(ctypes.Structure):
@@ -115,7 +116,7 @@ def _check(rc: int):
 class _Desc:
     """Keeps the int32 arrays of a bi_model_desc alive."""
 
-    def __init__(self, n, U, K, deps, model_batch: int, flags: int):
+    def __init__(self, n, U, K, deps, model_batch: int, flags: int, bdeps=None):
         self.n = np.ascontiguousarray(n, dtype=np.int32)
         self.U = np.ascontiguousarray(U, dtype=np.int32)
         self.K = np.ascontiguousarray(K, dtype=np.int32)
@@ -124,12 +125,18 @@ class _Desc:
         if self.dep.size == 0:
             self.dep = np.zeros(1, dtype=np.int32)
         ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))  # noqa: E731
+        if bdeps is None:
+            bo = bd = None
+        else:
+            self.bdep_off = np.ascontiguousarray(np.cumsum([0] + [len(d) for d in bdeps]), dtype=np.int32)
+            self.bdep = np.ascontiguousarray([g for d in bdeps for g in d] or [0], dtype=np.int32)
+            bo, bd = ip(self.bdep_off), ip(self.bdep)
         self.c = bi_model_desc(len(self.n), ip(self.n), ip(self.U), len(self.K), ip(self.K), ip(self.dep_off),
-                               ip(self.dep), int(model_batch), int(flags))
+                               ip(self.dep), int(model_batch), int(flags), bo, bd)
 
 
-def bi_plan_model(n, U, K, deps, model_batch: int, flags: int = BI_DENSE_A) -> int:
-    d = _Desc(n, U, K, deps, model_batch, flags)
+def bi_plan_model(n, U, K, deps, model_batch: int, flags: int = BI_DENSE_A, bdeps=None) -> int:
+    d = _Desc(n, U, K, deps, model_batch, flags, bdeps)
     out = ctypes.c_size_t(0)
     _check(load().bi_plan_model(ctypes.byref(d.c), ctypes.byref(out)))
     return int(out.value)
@@ -143,9 +150,9 @@ def _ptrs(arrs):
     return (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])
 
 
-def bi_plan_model_exact(n, U, K, deps, model_batch: int, A, flags: int = BI_DENSE_A) -> int:
+def bi_plan_model_exact(n, U, K, deps, model_batch: int, A, flags: int = BI_DENSE_A, bdeps=None) -> int:
     """Exact packed size for these A tensors (differs from bi_plan_model for BI_SPARSE_A)."""
-    d = _Desc(n, U, K, deps, model_batch, flags)
+    d = _Desc(n, U, K, deps, model_batch, flags, bdeps)
     A = _f32_list(A)
     out = ctypes.c_size_t(0)
     _check(load().bi_plan_model_exact(ctypes.byref(d.c), _ptrs(A), ctypes.byref(out)))
@@ -160,9 +167,9 @@ def _stream_ptr(stream) -> Optional[int]:
 
 
 def bi_pack_model(n, U, K, deps, model_batch: int, A: Sequence[np.ndarray], B: Sequence[np.ndarray],
-                  D: Sequence[np.ndarray], dev_buf, flags: int = BI_DENSE_A, stream=None) -> int:
+                  D: Sequence[np.ndarray], dev_buf, flags: int = BI_DENSE_A, stream=None, bdeps=None) -> int:
     """Pack host float32 A/B/D into the device tensor ``dev_buf``; returns the handle."""
-    d = _Desc(n, U, K, deps, model_batch, flags)
+    d = _Desc(n, U, K, deps, model_batch, flags, bdeps)
     A = [np.ascontiguousarray(a, dtype=np.float32) for a in A]
     B = [np.ascontiguousarray(b, dtype=np.float32) for b in B]
     D = [np.ascontiguousarray(x, dtype=np.float32) for x in D]
@@ -174,10 +181,10 @@ def bi_pack_model(n, U, K, deps, model_batch: int, A: Sequence[np.ndarray], B: S
     return int(out.value)
 
 
-def bi_pack_model_host(n, U, K, deps, model_batch: int, A, B, D, flags: int = BI_DENSE_A):
+def bi_pack_model_host(n, U, K, deps, model_batch: int, A, B, D, flags: int = BI_DENSE_A, bdeps=None):
     """Pack into host memory; returns (handle, uint8 numpy image)."""
-    d = _Desc(n, U, K, deps, model_batch, flags)
-    nbytes = bi_plan_model_exact(n, U, K, deps, model_batch, A, flags)
+    d = _Desc(n, U, K, deps, model_batch, flags, bdeps)
+    nbytes = bi_plan_model_exact(n, U, K, deps, model_batch, A, flags, bdeps)
     raw = np.zeros(nbytes + 512, dtype=np.uint8)
     start = (-raw.ctypes.data) % 256
     img = raw[start:start + nbytes]
@@ -317,10 +324,11 @@ class PackedModel:
     def __init__(self, model, flags: int = BI_DENSE_A, device=None, stream=None):
         import torch
         self.model = model
-        nbytes = bi_plan_model_exact(model.n, model.U, model.K, model.deps, model.mb, model.A, flags)
+        bdeps = getattr(model, "bdeps", None)
+        nbytes = bi_plan_model_exact(model.n, model.U, model.K, model.deps, model.mb, model.A, flags, bdeps)
         self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device or "cuda")
         self.handle = bi_pack_model(model.n, model.U, model.K, model.deps, model.mb, model.A, model.B, model.D,
-                                    self.buf, flags, stream)
+                                    self.buf, flags, stream, bdeps)
         self.flags = flags
 
     def stats(self) -> dict:

@@ -25,6 +25,7 @@
 
 #include "internal.h"
 #include "profile.h"
+#include "transition.h"
 
 namespace bi {
 namespace {
@@ -59,6 +60,7 @@ struct AgentArgs {
     // [u][i][j] block at element bo[f].  bdoubles: LDS doubles of the table.
     int bst, bdoubles;
     int bo[kStageMaxF + 1];
+    int trivb;             // every B-dependency list is {f} (the dedicated transition code)
     double tau;            // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
     float *q;
 };
@@ -355,7 +357,7 @@ __device__ void stage_b(const AgentArgs &a, int agent, bool lb, double *tab)
     const int64_t am = a.shared ? 0 : agent;
     for (int f = 0; f < a.F; ++f) {
         const FacDesc &fd = a.facs[f];
-        const int cnt = fd.U * fd.n * fd.n;
+        const int cnt = fd.U * fd.n * fd.bstates;
         if (lb) {
             const double *src = at<double>(a.base, fd.lb_off) + am * fd.b_agent;
             for (int i = threadIdx.x; i < cnt; i += kThreads) tab[a.bo[f] + i] = src[i];
@@ -442,6 +444,49 @@ __global__ __launch_bounds__(kThreads, 4) void agent_window_kernel(AgentArgs a)
             const float *Bf = a.bst ? reinterpret_cast<const float *>(btab) + a.bo[f]
                                     : at<float>(a.base, fd.b_off) + am * fd.b_agent;
             double fwd, bwd = 0.0;
+            if (!a.trivb) {
+                // general B-dependencies: forward message from the factors f
+                // depends on, one backward message per child j of f
+                const int bs = fd.bstates;
+                if (t == 0)
+                    fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + j])
+                                  : at<double>(a.base, fd.ld_off)[am * fd.ld_agent + s];
+                else if (ALGO == BI_ALGO_VMP)
+                    fwd = bdep_sum(a.facs, fd, LB + (int64_t)up * n * bs, s, cur + (t - 1) * a.ntot, -1, 0);
+                else
+                    fwd = ln_clamped(bdep_sum(a.facs, fd, Bf + (int64_t)up * n * bs, s, cur + (t - 1) * a.ntot, -1, 0));
+                int children = 0;
+                if (t + 1 < a.T) {
+                    for (int c = 0; c < fd.nch; ++c) {
+                        const int jf = fd.ch[c], pos = fd.chpos[c];
+                        const FacDesc &fj = a.facs[jf];
+                        const int uj = a.act[((int64_t)agent * (a.T - 1) + t) * a.F + jf];
+                        const int64_t tab = (int64_t)uj * fj.n * fj.bstates;
+                        const double *qn = cur + (t + 1) * a.ntot + fj.q_off;
+                        double msg = 0.0;
+                        if (ALGO == BI_ALGO_VMP) {
+                            const double *LBj =
+                                (a.bst ? btab + a.bo[jf] : at<double>(a.base, fj.lb_off) + am * fj.b_agent) + tab;
+                            for (int sn = 0; sn < fj.n; ++sn)
+                                msg = fma(qn[sn], bdep_sum(a.facs, fj, LBj, sn, cur + t * a.ntot, pos, s), msg);
+                            bwd += msg;
+                        } else {
+                            const float *Bj = (a.bst ? reinterpret_cast<const float *>(btab) + a.bo[jf]
+                                                     : at<float>(a.base, fj.b_off) + am * fj.b_agent) + tab;
+                            for (int sn = 0; sn < fj.n; ++sn)
+                                msg = fma(qn[sn], bdep_sum(a.facs, fj, Bj, sn, cur + t * a.ntot, pos, s), msg);
+                            bwd += ln_clamped(msg);
+                        }
+                        ++children;
+                    }
+                }
+                const double lm = lam[i];
+                if (ALGO == BI_ALGO_VMP)
+                    nxt[i] = lm + fwd + bwd;
+                else
+                    nxt[i] = children > 0 ? lm + (fwd + bwd) / (double)(1 + children) : lm + fwd;
+                continue;
+            }
             if (t == 0) {
                 fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + j])
                               : at<double>(a.base, fd.ld_off)[am * fd.ld_agent + s];
@@ -522,12 +567,18 @@ __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
             } else {
                 const int u = a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f];
                 const float *Bp = (a.bst ? reinterpret_cast<const float *>(btab) + a.bo[f]
-                                         : at<float>(a.base, fd.b_off) + am * fd.b_agent) + (int64_t)u * n * n;
-                const double *qp = qfin + (t - 1) * a.ntot + fd.q_off;
-                for (int s = lane; s < n; s += 64) {
-                    double acc = 0.0;
-                    for (int j = 0; j < n; ++j) acc = fma((double)Bp[s * n + j], qp[j], acc);
-                    lp[s] = ln_clamped(acc);
+                                         : at<float>(a.base, fd.b_off) + am * fd.b_agent) +
+                                  (int64_t)u * n * fd.bstates;
+                if (a.trivb) {
+                    const double *qp = qfin + (t - 1) * a.ntot + fd.q_off;
+                    for (int s = lane; s < n; s += 64) {
+                        double acc = 0.0;
+                        for (int j = 0; j < n; ++j) acc = fma((double)Bp[s * n + j], qp[j], acc);
+                        lp[s] = ln_clamped(acc);
+                    }
+                } else {   // predictive marginal under the factorised q_{t-1}
+                    for (int s = lane; s < n; s += 64)
+                        lp[s] = ln_clamped(bdep_sum(a.facs, fd, Bp, s, qfin + (t - 1) * a.ntot, -1, 0));
                 }
             }
         }
@@ -589,6 +640,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     for (const ModDesc &md : m->mods) a.llpc += md.slice;
     a.act = act;
     a.prior = prior;
+    a.trivb = m->trivial_b;
     a.tau = tau;
     a.q = q;
     const size_t TN = (size_t)T * m->ntot;
@@ -616,7 +668,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
         int64_t elems = 0;
         for (int f = 0; f < m->F && f <= kStageMaxF; ++f) {
             if (f < kStageMaxF) a.bo[f] = (int)elems;
-            elems += (int64_t)m->facs[f].U * m->facs[f].n * m->facs[f].n;
+            elems += (int64_t)m->facs[f].U * m->facs[f].n * m->facs[f].bstates;
         }
         const size_t bytes = (size_t)elems * (algo == BI_ALGO_VMP ? 8 : 4);
         a.bst = m->F <= kStageMaxF && bytes <= kBStageMax;

@@ -14,6 +14,8 @@ struct bi_model {
     int32_t F = 0, M = 0, mb = 1;
     uint32_t flags = BI_DENSE_A;
     std::vector<int32_t> n, U, K, dep_off, dep;
+    std::vector<int32_t> bdep_off, bdep;   // B-dependency lists ({f} each when trivial)
+    bool trivial_b = true;   // every B-dependency list is {f}
     std::vector<bi::ModDesc> mods;
     std::vector<bi::FacDesc> facs;
     int32_t ntot = 0;      // sum of n

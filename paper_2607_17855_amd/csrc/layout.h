@@ -68,14 +68,24 @@ struct ModDesc {
     int64_t nnz;                        // entries of the modality (each stored twice)
 };
 
+constexpr int kMaxBDep = 4;   // B-dependencies per factor
+constexpr int kMaxCh = 8;     // factors whose B-dependencies hold a given factor
+
 struct FacDesc {
-    int64_t b_off;    // byte offset of fp32 B as [agent][u][i][j] = P(s'=i | s=j, u)
+    int64_t b_off;    // byte offset of fp32 B as [agent][u][i][j] = P(s'=i | s_dep=j, u), j the
+                      // dependency states flattened (row-major over bd); trivial: j = s^f
     int64_t lb_off;   // byte offset of fp64 log B, same layout
     int64_t ld_off;   // byte offset of fp64 log D as [agent][n]
     int64_t b_agent;  // elements per agent of B / LB (0 when shared)
     int32_t ld_agent; // elements per agent of LD (0 when shared)
     int32_t n, U;
     int32_t q_off;    // offset of this factor in a context's marginal vector
+    int32_t nbd;                  // B-dependencies (factors whose states at t condition s_{t+1}^f)
+    int32_t bd[kMaxBDep];         // ascending; trivial: {f}
+    int32_t bdn[kMaxBDep];        // their state counts
+    int32_t bstates;              // prod of bdn (B_f is [u][n][bstates])
+    int32_t nch;                  // children: factors j with f in bd(j)
+    int32_t ch[kMaxCh], chpos[kMaxCh];   // the children and the position of f in their lists
 };
 
 struct SpEntry {

@@ -81,6 +81,34 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
                         2 * kMaxSide);
     }
     m->dep.assign(d->dep, d->dep + d->dep_off[d->M]);
+    // B-dependency lists (NULL: trivial)
+    if ((d->bdep_off == nullptr) != (d->bdep == nullptr))
+        return fail(BI_ERR_INVALID_ARG, "bdep_off and bdep must both be set or both be NULL");
+    m->bdep_off.clear();
+    m->bdep.clear();
+    for (int f = 0; f <= d->F; ++f) m->bdep_off.push_back(f);
+    for (int f = 0; f < d->F; ++f) m->bdep.push_back(f);
+    if (d->bdep_off) {
+        if (d->bdep_off[0] != 0) return fail(BI_ERR_SHAPE, "bdep_off[0] must be 0");
+        for (int f = 0; f < d->F; ++f) {
+            const int k = d->bdep_off[f + 1] - d->bdep_off[f];
+            if (k < 1) return fail(BI_ERR_SHAPE, "factor %d: empty B-dependency list", f);
+            if (k > kMaxBDep)
+                return fail(BI_ERR_UNSUPPORTED, "factor %d: %d B-dependencies; this build handles up to %d", f, k,
+                            kMaxBDep);
+            for (int i = d->bdep_off[f]; i < d->bdep_off[f + 1]; ++i) {
+                if (d->bdep[i] < 0 || d->bdep[i] >= d->F)
+                    return fail(BI_ERR_SHAPE, "factor %d: B-dependency %d out of range", f, d->bdep[i]);
+                if (i > d->bdep_off[f] && d->bdep[i] <= d->bdep[i - 1])
+                    return fail(BI_ERR_SHAPE, "factor %d: B-dependency list not strictly ascending", f);
+            }
+        }
+        m->bdep_off.assign(d->bdep_off, d->bdep_off + d->F + 1);
+        m->bdep.assign(d->bdep, d->bdep + d->bdep_off[d->F]);
+    }
+    m->trivial_b = true;
+    for (int f = 0; f < d->F; ++f)
+        if (m->bdep_off[f + 1] - m->bdep_off[f] != 1 || m->bdep[m->bdep_off[f]] != f) m->trivial_b = false;
 
     // descriptor tables first
     int64_t off = 0;
@@ -93,12 +121,34 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
     m->facs.assign(m->F, FacDesc{});
     int32_t qoff = 0;
     for (int f = 0; f < m->F; ++f) {
-        m->facs[f].n = m->n[f];
-        m->facs[f].U = m->U[f];
-        m->facs[f].q_off = qoff;
+        FacDesc &fd = m->facs[f];
+        fd.n = m->n[f];
+        fd.U = m->U[f];
+        fd.q_off = qoff;
         qoff += m->n[f];
+        fd.nbd = m->bdep_off[f + 1] - m->bdep_off[f];
+        int64_t bs = 1;
+        for (int i = 0; i < kMaxBDep; ++i) {
+            fd.bd[i] = i < fd.nbd ? m->bdep[m->bdep_off[f] + i] : -1;
+            fd.bdn[i] = i < fd.nbd ? m->n[fd.bd[i]] : 1;
+            bs *= fd.bdn[i];
+        }
+        if (bs * fd.n * fd.U > INT32_MAX / 2) return fail(BI_ERR_UNSUPPORTED, "factor %d: B too large", f);
+        fd.bstates = (int32_t)bs;
+        fd.nch = 0;
+        for (int i = 0; i < kMaxCh; ++i) fd.ch[i] = fd.chpos[i] = -1;
     }
     m->ntot = qoff;
+    for (int j = 0; j < m->F; ++j)   // children: j is a child of every factor on its list
+        for (int p = 0; p < m->facs[j].nbd; ++p) {
+            FacDesc &fd = m->facs[m->facs[j].bd[p]];
+            if (fd.nch == kMaxCh)
+                return fail(BI_ERR_UNSUPPORTED, "factor %d is on more than %d B-dependency lists", m->facs[j].bd[p],
+                            kMaxCh);
+            fd.ch[fd.nch] = j;
+            fd.chpos[fd.nch] = p;
+            ++fd.nch;
+        }
 
     int64_t a_raw = 0, a_stored = 0;
     int32_t zv = 0;
@@ -178,7 +228,7 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
     m->zvpc = zv;
     for (int f = 0; f < m->F; ++f) {
         FacDesc &fd = m->facs[f];
-        const int64_t per = (int64_t)fd.U * fd.n * fd.n;
+        const int64_t per = (int64_t)fd.U * fd.n * fd.bstates;
         fd.b_agent = m->mb == 1 ? 0 : per;
         fd.b_off = off;
         off = align_up(off + 4 * per * m->mb, kAlign);
@@ -292,17 +342,17 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
     }
     for (int f = 0; f < m->F; ++f) {
         const FacDesc &fd = m->facs[f];
-        const int n = fd.n, U = fd.U;
+        const int n = fd.n, U = fd.U, bs = fd.bstates;
         for (int a = 0; a < m->mb; ++a) {
-            const float *src = B[f] + (int64_t)a * n * n * U;          // [i][j][u]
-            float *b = reinterpret_cast<float *>(host + fd.b_off) + (int64_t)a * U * n * n;   // [u][i][j]
-            double *lb = reinterpret_cast<double *>(host + fd.lb_off) + (int64_t)a * U * n * n;
+            const float *src = B[f] + (int64_t)a * n * bs * U;          // [i][j][u], j over the dependency states
+            float *b = reinterpret_cast<float *>(host + fd.b_off) + (int64_t)a * U * n * bs;   // [u][i][j]
+            double *lb = reinterpret_cast<double *>(host + fd.lb_off) + (int64_t)a * U * n * bs;
             for (int u = 0; u < U; ++u)
                 for (int i = 0; i < n; ++i)
-                    for (int j = 0; j < n; ++j) {
-                        const float v = src[((int64_t)i * n + j) * U + u];
-                        b[((int64_t)u * n + i) * n + j] = v;
-                        lb[((int64_t)u * n + i) * n + j] = ln_clamped((double)v);
+                    for (int j = 0; j < bs; ++j) {
+                        const float v = src[((int64_t)i * bs + j) * U + u];
+                        b[((int64_t)u * n + i) * bs + j] = v;
+                        lb[((int64_t)u * n + i) * bs + j] = ln_clamped((double)v);
                     }
             const float *dsrc = D[f] + (int64_t)a * n;
             double *ld = reinterpret_cast<double *>(host + fd.ld_off) + (int64_t)a * n;

@@ -12,6 +12,7 @@
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
+#include "transition.h"
 
 namespace bi {
 
@@ -20,7 +21,7 @@ namespace {
 struct PredictArgs {
     const char *base;
     const FacDesc *facs;
-    int F, ntot;
+    int F, ntot, trivb;
     const float *q;
     int64_t q_stride;
     const int32_t *act;
@@ -40,7 +41,11 @@ __global__ __launch_bounds__(256) void predict_kernel(PredictArgs a)
         const int n = fd.n;
         const int u = ua[f];
         const float *B = reinterpret_cast<const float *>(a.base + fd.b_off) + (int64_t)agent * fd.b_agent +
-                         (int64_t)u * n * n;
+                         (int64_t)u * n * fd.bstates;
+        if (!a.trivb) {   // B-dependency lists: the predictive marginal under the factorised q
+            for (int i = lane; i < n; i += 64) oa[fd.q_off + i] = (float)bdep_sum(a.facs, fd, B, i, qa, -1, 0);
+            continue;
+        }
         const float *qf = qa + fd.q_off;
         for (int i = lane; i < n; i += 64) {
             const float *row = B + (int64_t)i * n;
@@ -61,6 +66,7 @@ int launch_predict(const bi_model *m, int b, const float *q, int64_t q_stride, c
     a.facs = reinterpret_cast<const FacDesc *>(m->dev + align_up((int64_t)sizeof(ModDesc) * m->M, kAlign));
     a.F = m->F;
     a.ntot = m->ntot;
+    a.trivb = m->trivial_b;
     a.q = q;
     a.q_stride = q_stride;
     a.act = act;

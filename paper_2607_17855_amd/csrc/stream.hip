@@ -538,7 +538,7 @@ void launch_update(int algo, const StreamArgs &a, size_t lds, hipStream_t stream
 
 bool stream_eligible(const bi_model *m, int algo)
 {
-    if (!(m->flags & BI_FAST_F32) || m->mb != 1 || algo == BI_ALGO_FPI) return false;
+    if (!(m->flags & BI_FAST_F32) || m->mb != 1 || algo == BI_ALGO_FPI || !m->trivial_b) return false;
     if (m->M > kStreamMaxM) return false;
     for (const ModDesc &md : m->mods) {
         if (md.la32_off < 0) return false;

@@ -48,7 +48,9 @@ SpEntry = np.dtype([("v", np.float64), ("a", np.uint32), ("b", np.uint32)])
 class FacDesc(ctypes.Structure):
     _fields_ = [("b_off", ctypes.c_int64), ("lb_off", ctypes.c_int64), ("ld_off", ctypes.c_int64),
                 ("b_agent", ctypes.c_int64), ("ld_agent", ctypes.c_int32), ("n", ctypes.c_int32),
-                ("U", ctypes.c_int32), ("q_off", ctypes.c_int32)]
+                ("U", ctypes.c_int32), ("q_off", ctypes.c_int32), ("nbd", ctypes.c_int32),
+                ("bd", ctypes.c_int32 * 4), ("bdn", ctypes.c_int32 * 4), ("bstates", ctypes.c_int32),
+                ("nch", ctypes.c_int32), ("ch", ctypes.c_int32 * 8), ("chpos", ctypes.c_int32 * 8)]
 
 
 def _descs(img, M, F):
@@ -390,3 +392,80 @@ def test_selector_table_matches_the_fitted_trees(regime):
             finally:
                 bi.bi_free_model(h)
     assert checked == len(cases) * 6
+
+
+def _bdep_model(seed, lists, mb=2, n=(3, 4, 2)):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return synth.make_model(rng, list(n), [2, 1, 3], [3, 2], [[0, 1], [2]], mb, bdeps=lists)
+
+
+def test_bdeps_host_pack_layout():
+    lists = [[0, 2], [1], [0, 1, 2]]
+    m = _bdep_model(41, lists)
+    h, img = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, m.mb, m.A, m.B, m.D, bdeps=m.bdeps)
+    try:
+        _, facs = _descs(img, m.M, m.F)
+        for f in range(m.F):
+            fd = facs[f]
+            assert fd.nbd == len(lists[f]) and [fd.bd[i] for i in range(fd.nbd)] == lists[f]
+            assert [fd.bdn[i] for i in range(fd.nbd)] == [m.n[g] for g in lists[f]]
+            assert fd.bstates == int(np.prod([m.n[g] for g in lists[f]]))
+            kids = sorted((j, lists[j].index(f)) for j in range(m.F) if f in lists[j])
+            assert sorted((fd.ch[i], fd.chpos[i]) for i in range(fd.nch)) == kids
+            n, U, bs = m.n[f], m.U[f], fd.bstates
+            for a in range(m.mb):
+                b = img[fd.b_off + 4 * a * fd.b_agent:fd.b_off + 4 * (a + 1) * fd.b_agent].view(np.float32)
+                want = np.transpose(m.B[f][a].reshape(n, bs, U), (2, 0, 1)).ravel()   # [u][i][flat]
+                assert np.array_equal(b, want)
+                lb = img[fd.lb_off + 8 * a * fd.b_agent:fd.lb_off + 8 * (a + 1) * fd.b_agent].view(np.float64)
+                assert np.allclose(lb, np.log(np.maximum(want.astype(np.float64), 1e-16)), rtol=0, atol=1e-12)
+    finally:
+        bi.bi_free_model(h)
+    # the explicit trivial lists pack exactly like no lists
+    t = _bdep_model(42, None)
+    h0, i0 = bi.bi_pack_model_host(t.n, t.U, t.K, t.deps, t.mb, t.A, t.B, t.D)
+    h1, i1 = bi.bi_pack_model_host(t.n, t.U, t.K, t.deps, t.mb, t.A, t.B, t.D, bdeps=[[0], [1], [2]])
+    try:
+        assert np.array_equal(i0, i1)
+    finally:
+        bi.bi_free_model(h0)
+        bi.bi_free_model(h1)
+
+
+def test_bdeps_validation_and_dispatch():
+    m = _bdep_model(43, [[0, 2], [1], [0, 1, 2]], mb=1)
+    def err(lists):
+        try:
+            h, _ = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, 1, m.A, m.B, m.D, bdeps=lists)
+        except bi.BiError as e:
+            return e.code
+        bi.bi_free_model(h)
+        return bi.BI_OK
+    assert err([[0], [], [2]]) == bi.BI_ERR_SHAPE                # empty list
+    assert err([[0], [1], [2, 0]]) == bi.BI_ERR_SHAPE            # not ascending
+    assert err([[0], [1], [3]]) == bi.BI_ERR_SHAPE               # out of range
+    d = bi._Desc(m.n, m.U, m.K, m.deps, 1, bi.BI_DENSE_A, [[0], [1], [2]])
+    d.c.bdep = None                                               # one of the two arrays missing
+    out = ctypes.c_size_t(0)
+    assert bi.load().bi_plan_model(ctypes.byref(d.c), ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG
+    # five dependencies, and a factor on nine lists: beyond this build
+    big = synth.make_model(np.random.Generator(np.random.PCG64(1)), [2] * 9, [1] * 9, [2], [[0]], 1)
+    bd = bi._Desc(big.n, big.U, big.K, big.deps, 1, bi.BI_DENSE_A, [[0, 1, 2, 3, 4]] + [[f] for f in range(1, 9)])
+    assert bi.load().bi_plan_model(ctypes.byref(bd.c), ctypes.byref(out)) == bi.BI_ERR_UNSUPPORTED
+    bd = bi._Desc(big.n, big.U, big.K, big.deps, 1, bi.BI_DENSE_A, [[0, f] if f else [0] for f in range(9)])
+    assert bi.load().bi_plan_model(ctypes.byref(bd.c), ctypes.byref(out)) == bi.BI_ERR_UNSUPPORTED
+    # non-trivial lists run agent-resident whatever the packing allows
+    for fl in (bi.BI_DENSE_A | bi.BI_FAST_F32, bi.BI_SPARSE_A):
+        h, _ = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, 1, m.A, m.B, m.D, flags=fl, bdeps=m.bdeps)
+        old = os.environ.get("BI_FORCE_PATH")
+        try:
+            for force in ("stream", "sparse"):
+                os.environ["BI_FORCE_PATH"] = force
+                for algo in range(3):
+                    assert bi.bi_query_path(h, 8, 4, algo) == bi.BI_PATH_AGENT
+        finally:
+            if old is None:
+                os.environ.pop("BI_FORCE_PATH", None)
+            else:
+                os.environ["BI_FORCE_PATH"] = old
+            bi.bi_free_model(h)

@@ -20,7 +20,11 @@ on one layout.
 kernels, one model per agent): vmp_2f (F=2 factors of 8 and 6 states, M=3
 modalities on both, T=10, b=1024, VMP), mmp_3f (F=3 of 12/10/8 states, M=4 x
 16 outcomes on random factor subsets, T=20, b=4096, MMP), fpi_hmm (one
-4-state factor, T=8, b=1, FPI).  --soft runs such a workload with soft
+4-state factor, T=8, b=1, FPI), fpi_2f (FPI on the F=2 models), fpi_2f_rolling
+(the same, online: T calls of one step, each carrying the predictive prior of
+the step before through bi_predict), mmp_3f_bdeps (the F=3 structure with
+every factor's transition conditioned on itself and one other factor).  --soft
+runs such a workload with soft
 observation vectors (each puts 0.7 on the sampled outcome and spreads the
 rest as a Dirichlet(1) draw) through bi_infer_soft.
 """
@@ -50,6 +54,9 @@ ALGOS = ("vmp", "mmp")
 def source_sha(fname: str) -> str:
     with open(os.path.join(CSRC, fname), "rb") as fh:
         return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+import numpy as np   # noqa: E402  (host-side arithmetic of the work counts)
 
 
 def slice_sizes(model):
@@ -96,16 +103,35 @@ def sparse_lik_work(model, obs):
 def agent_work(model, T, algo):
     """Algorithmic flops and bytes of one belief update on the agent-resident
     path: the two contractions of every observed slice (one FMA per entry
-    each), the transition messages (two n x n products per factor; FPI: one,
-    once per time step, counted per update), and one read of the observed
-    fp64 slices."""
+    each), the transition messages (per state of f: the forward contraction
+    over the states of f's B-dependency list, and for every factor j whose
+    list holds f the backward one over s_{t+1}^j and j's other listed
+    factors; two n x n products per factor for trivial lists; FPI: the
+    forward one only, once per time step, counted per update), and one read
+    of the observed fp64 slices."""
     lik = sum(4 * P for P in slice_sizes(model))
-    trans = sum((2 if algo == "fpi" else 4) * n * n for n in model.n)
+    bstates = [int(np.prod([model.n[g] for g in model.bdep(f)])) for f in range(model.F)]
+    trans = 0
+    for f, n in enumerate(model.n):
+        fwd = n * bstates[f]
+        bwd = sum(model.n[j] * bstates[j] for j in range(model.F) if f in model.bdep(j))   # n states x n_j x others
+        trans += 2 * (fwd if algo == "fpi" else fwd + bwd)
     nbytes = sum(8.0 * P for P in slice_sizes(model))
     return float(lik + trans), nbytes
 
 
-AGENT_WORKLOADS = {"vmp_2f": ("config2", "vmp"), "mmp_3f": ("config3", "mmp"), "fpi_hmm": ("config1", "fpi")}
+# per-agent workloads: name -> (generator, algorithm, options)
+AGENT_WORKLOADS = {
+    "vmp_2f": ("config2", "vmp", {}),
+    "mmp_3f": ("config3", "mmp", {}),
+    "fpi_hmm": ("config1", "fpi", {}),
+    # the F=2 models filtered over the whole window, and online: one step per
+    # call, each carrying the predictive prior of the step before (bi_predict)
+    "fpi_2f": ("config2", "fpi", {}),
+    "fpi_2f_rolling": ("config2", "fpi", {"rolling": True}),
+    # the F=3 structure with coupled transitions (B-dependency lists)
+    "mmp_3f_bdeps": ("config3", "mmp", {"bdeps": True}),
+}
 
 
 def soft_ll_bytes(model, b, T):
@@ -282,9 +308,15 @@ def main():
 
 
 def bench_agent(args, bi, synth, torch, dev):
-    """One step = one call of the workload's algorithm over its whole batch."""
-    cfg, algo = AGENT_WORKLOADS[args.workload]
-    w = getattr(synth, cfg)()
+    """One step = one call of the workload's algorithm over its whole batch
+    (online workloads: T one-step calls and T - 1 predictive priors)."""
+    import numpy as np
+    cfg, algo, opts = AGENT_WORKLOADS[args.workload]
+    w = getattr(synth, cfg)(bdeps=synth.CONFIG3_BDEPS) if opts.get("bdeps") else getattr(synth, cfg)()
+    rolling = bool(opts.get("rolling"))
+    if rolling and args.soft:
+        print("bench.py: --soft is not combined with the online workload", file=sys.stderr)
+        sys.exit(2)
     pm = bi.PackedModel(w.model, flags=bi.BI_DENSE_A, device=dev)
     obs = torch.from_numpy(w.obs).to(dev)
     act = torch.from_numpy(w.act).to(dev)
@@ -298,8 +330,21 @@ def bench_agent(args, bi, synth, torch, dev):
         soft_dev = torch.from_numpy(soft_np).to(dev)
         ws = pm.workspace_soft(w.b, w.T, algo)
 
+    if rolling:
+        # per step t: its observations, its own output, the prior of step t + 1
+        obs_t = [obs[:, t:t + 1].contiguous() for t in range(w.T)]
+        act_t = [act[:, t].contiguous() for t in range(w.T - 1)]
+        q_t = [torch.empty((w.b, 1, w.model.n_total), dtype=torch.float32, device=dev) for _ in range(w.T)]
+        priors = [torch.empty((w.b, w.model.n_total), dtype=torch.float32, device=dev) for _ in range(2)]
+
     def step():
-        if soft_np is not None:
+        if rolling:
+            prior = None   # step 0: D of the packed model
+            for t in range(w.T):
+                pm.infer(algo, obs_t[t], None, w.iters, q=q_t[t], stream=stream, prior=prior)
+                if t + 1 < w.T:
+                    prior = pm.predict(q_t[t][:, 0], act_t[t], out=priors[t % 2], stream=stream)
+        elif soft_np is not None:
             pm.infer_soft(algo, soft_dev, act, w.iters, q=q, ws=ws, stream=stream)
         else:
             pm.infer(algo, obs, act, w.iters, q=q, stream=stream)
@@ -324,19 +369,23 @@ def bench_agent(args, bi, synth, torch, dev):
     launches, total_ms = prof[cls]
     avg_ms = total_ms / max(launches, 1)
     fl, nb = agent_work(w.model, w.T, algo)
-    flops = fl * bu
+    t_launch = 1 if rolling else w.T   # steps per launch
+    flops = fl * w.b * t_launch * w.iters
     achieved = flops / (avg_ms / 1e3) / 1e12
     out = {
         "metric": METRIC, "value": bu / (ms_step / 1e3), "unit": "belief_updates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": {"workload": f"{w.name}: per-agent models, {algo.upper()} x{w.iters}"
-                               + (", soft observations" if soft_np is not None else ""),
-                   "b": w.b, "T": w.T, "iters": w.iters, "algos": [algo], "soft": soft_np is not None},
+                               + (", soft observations" if soft_np is not None else "")
+                               + (", online (one step per call, predictive prior carried)" if rolling else "")
+                               + (f", B-dependency lists {w.model.bdeps}" if w.model.bdeps else ""),
+                   "b": w.b, "T": w.T, "iters": w.iters, "algos": [algo], "soft": soft_np is not None,
+                   "rolling": rolling},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP64_VALU_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP64_VALU_TFLOPS, "traffic": None, "kernel": cls + "_kernel",
                      "avg_launch_ms": avg_ms, "launches": launches, "algorithmic_flops_per_launch": flops,
-                     "algorithmic_bytes_per_launch": nb * w.b * w.T},
+                     "algorithmic_bytes_per_launch": nb * w.b * t_launch},
         "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
         "wall_s_timed": wall,
     }

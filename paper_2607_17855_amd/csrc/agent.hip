@@ -34,7 +34,7 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kStageMaxM = 16;
 constexpr int kStageMaxF = 16;
-constexpr size_t kBStageMax = 32 * 1024;   // bytes of B / log B staged per workgroup
+constexpr size_t kBStageMax = 64 * 1024;   // bytes of B / log B staged per workgroup
 
 // Observed slices staged in LDS: a context's block holds modality m's slice at
 // po[m] with rows padded to Cp + 1 values (conflict-free row and column
@@ -60,7 +60,6 @@ struct AgentArgs {
     // [u][i][j] block at element bo[f].  bdoubles: LDS doubles of the table.
     int bst, bdoubles;
     int bo[kStageMaxF + 1];
-    int trivb;             // every B-dependency list is {f} (the dedicated transition code)
     double tau;            // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
     float *q;
 };
@@ -409,7 +408,10 @@ __device__ void window_softmax(const AgentArgs &a, const int *sfac, const double
     __syncthreads();
 }
 
-template <int ALGO, bool GX>  // ALGO: BI_ALGO_VMP or BI_ALGO_MMP; GX: slices read from global memory
+// ALGO: BI_ALGO_VMP or BI_ALGO_MMP; GX: slices read from global memory; TB:
+// every B-dependency list is {f} (the row / column transition products;
+// otherwise the general contractions of transition.h)
+template <int ALGO, bool GX, bool TB>
 __global__ __launch_bounds__(kThreads, 4) void agent_window_kernel(AgentArgs a)
 {
     extern __shared__ double smem[];
@@ -444,37 +446,42 @@ __global__ __launch_bounds__(kThreads, 4) void agent_window_kernel(AgentArgs a)
             const float *Bf = a.bst ? reinterpret_cast<const float *>(btab) + a.bo[f]
                                     : at<float>(a.base, fd.b_off) + am * fd.b_agent;
             double fwd, bwd = 0.0;
-            if (!a.trivb) {
+            if (!TB) {
                 // general B-dependencies: forward message from the factors f
                 // depends on, one backward message per child j of f
-                const int bs = fd.bstates;
+                const BDep df = bdep_of(a.facs, fd);
+                const int bs = df.bs;
                 if (t == 0)
                     fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + j])
                                   : at<double>(a.base, fd.ld_off)[am * fd.ld_agent + s];
                 else if (ALGO == BI_ALGO_VMP)
-                    fwd = bdep_sum(a.facs, fd, LB + (int64_t)up * n * bs, s, cur + (t - 1) * a.ntot, -1, 0);
+                    fwd = bdep_row(df, LB + ((int64_t)up * n + s) * bs, cur + (t - 1) * a.ntot, -1, 0);
                 else
-                    fwd = ln_clamped(bdep_sum(a.facs, fd, Bf + (int64_t)up * n * bs, s, cur + (t - 1) * a.ntot, -1, 0));
+                    fwd = ln_clamped(bdep_row(df, Bf + ((int64_t)up * n + s) * bs, cur + (t - 1) * a.ntot, -1, 0));
                 int children = 0;
                 if (t + 1 < a.T) {
                     for (int c = 0; c < fd.nch; ++c) {
                         const int jf = fd.ch[c], pos = fd.chpos[c];
                         const FacDesc &fj = a.facs[jf];
+                        const BDep dj = bdep_of(a.facs, fj);
+                        const int nj = fj.n;
                         const int uj = a.act[((int64_t)agent * (a.T - 1) + t) * a.F + jf];
-                        const int64_t tab = (int64_t)uj * fj.n * fj.bstates;
+                        const int64_t tab = (int64_t)uj * nj * dj.bs;
                         const double *qn = cur + (t + 1) * a.ntot + fj.q_off;
                         double msg = 0.0;
                         if (ALGO == BI_ALGO_VMP) {
                             const double *LBj =
                                 (a.bst ? btab + a.bo[jf] : at<double>(a.base, fj.lb_off) + am * fj.b_agent) + tab;
-                            for (int sn = 0; sn < fj.n; ++sn)
-                                msg = fma(qn[sn], bdep_sum(a.facs, fj, LBj, sn, cur + t * a.ntot, pos, s), msg);
+                            for (int sn = 0; sn < nj; ++sn)
+                                msg = fma(qn[sn], bdep_row(dj, LBj + (int64_t)sn * dj.bs, cur + t * a.ntot, pos, s),
+                                          msg);
                             bwd += msg;
                         } else {
                             const float *Bj = (a.bst ? reinterpret_cast<const float *>(btab) + a.bo[jf]
                                                      : at<float>(a.base, fj.b_off) + am * fj.b_agent) + tab;
-                            for (int sn = 0; sn < fj.n; ++sn)
-                                msg = fma(qn[sn], bdep_sum(a.facs, fj, Bj, sn, cur + t * a.ntot, pos, s), msg);
+                            for (int sn = 0; sn < nj; ++sn)
+                                msg = fma(qn[sn], bdep_row(dj, Bj + (int64_t)sn * dj.bs, cur + t * a.ntot, pos, s),
+                                          msg);
                             bwd += ln_clamped(msg);
                         }
                         ++children;
@@ -530,7 +537,7 @@ __global__ __launch_bounds__(kThreads, 4) void agent_window_kernel(AgentArgs a)
     for (int i = threadIdx.x; i < TN; i += kThreads) out[i] = (float)cur[i];
 }
 
-template <bool GX>   // slices read from global memory
+template <bool GX, bool TB>   // slices read from global memory; trivial B-dependency lists
 __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
 {
     extern __shared__ double smem[];
@@ -569,7 +576,7 @@ __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
                 const float *Bp = (a.bst ? reinterpret_cast<const float *>(btab) + a.bo[f]
                                          : at<float>(a.base, fd.b_off) + am * fd.b_agent) +
                                   (int64_t)u * n * fd.bstates;
-                if (a.trivb) {
+                if (TB) {
                     const double *qp = qfin + (t - 1) * a.ntot + fd.q_off;
                     for (int s = lane; s < n; s += 64) {
                         double acc = 0.0;
@@ -577,8 +584,9 @@ __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
                         lp[s] = ln_clamped(acc);
                     }
                 } else {   // predictive marginal under the factorised q_{t-1}
+                    const BDep df = bdep_of(a.facs, fd);
                     for (int s = lane; s < n; s += 64)
-                        lp[s] = ln_clamped(bdep_sum(a.facs, fd, Bp, s, qfin + (t - 1) * a.ntot, -1, 0));
+                        lp[s] = ln_clamped(bdep_row(df, Bp + (int64_t)s * df.bs, qfin + (t - 1) * a.ntot, -1, 0));
                 }
             }
         }
@@ -640,7 +648,6 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     for (const ModDesc &md : m->mods) a.llpc += md.slice;
     a.act = act;
     a.prior = prior;
-    a.trivb = m->trivial_b;
     a.tau = tau;
     a.q = q;
     const size_t TN = (size_t)T * m->ntot;
@@ -706,16 +713,22 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     }
     if (a.nc < 1 || lds > kLdsMax)
         return fail(BI_ERR_UNSUPPORTED, "agent working set (%zu bytes of LDS) exceeds the 160 KB budget", lds);
-    const bool gx = a.stage == kStageNone;
-    const void *fn;
-    if (algo == BI_ALGO_FPI)
-        fn = gx ? (const void *)agent_filter_kernel<true> : (const void *)agent_filter_kernel<false>;
-    else if (algo == BI_ALGO_VMP)
-        fn = gx ? (const void *)agent_window_kernel<BI_ALGO_VMP, true>
-                : (const void *)agent_window_kernel<BI_ALGO_VMP, false>;
-    else
-        fn = gx ? (const void *)agent_window_kernel<BI_ALGO_MMP, true>
-                : (const void *)agent_window_kernel<BI_ALGO_MMP, false>;
+    const bool gx = a.stage == kStageNone, tb = m->trivial_b;
+    // instantiation table [algo][gx][tb]
+    static const void *const kFilter[2][2] = {
+        {(const void *)agent_filter_kernel<false, false>, (const void *)agent_filter_kernel<false, true>},
+        {(const void *)agent_filter_kernel<true, false>, (const void *)agent_filter_kernel<true, true>}};
+    static const void *const kVmp[2][2] = {
+        {(const void *)agent_window_kernel<BI_ALGO_VMP, false, false>,
+         (const void *)agent_window_kernel<BI_ALGO_VMP, false, true>},
+        {(const void *)agent_window_kernel<BI_ALGO_VMP, true, false>,
+         (const void *)agent_window_kernel<BI_ALGO_VMP, true, true>}};
+    static const void *const kMmp[2][2] = {
+        {(const void *)agent_window_kernel<BI_ALGO_MMP, false, false>,
+         (const void *)agent_window_kernel<BI_ALGO_MMP, false, true>},
+        {(const void *)agent_window_kernel<BI_ALGO_MMP, true, false>,
+         (const void *)agent_window_kernel<BI_ALGO_MMP, true, true>}};
+    const void *fn = algo == BI_ALGO_FPI ? kFilter[gx][tb] : algo == BI_ALGO_VMP ? kVmp[gx][tb] : kMmp[gx][tb];
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     if (e == hipSuccess) {
         ProfScope p(algo == BI_ALGO_FPI ? "agent_filter" : "agent_window", stream);

@@ -43,7 +43,8 @@ __global__ __launch_bounds__(256) void predict_kernel(PredictArgs a)
         const float *B = reinterpret_cast<const float *>(a.base + fd.b_off) + (int64_t)agent * fd.b_agent +
                          (int64_t)u * n * fd.bstates;
         if (!a.trivb) {   // B-dependency lists: the predictive marginal under the factorised q
-            for (int i = lane; i < n; i += 64) oa[fd.q_off + i] = (float)bdep_sum(a.facs, fd, B, i, qa, -1, 0);
+            const BDep d = bdep_of(a.facs, fd);
+            for (int i = lane; i < n; i += 64) oa[fd.q_off + i] = (float)bdep_row(d, B + (int64_t)i * d.bs, qa, -1, 0);
             continue;
         }
         const float *qf = qa + fd.q_off;

@@ -293,14 +293,21 @@ def config3_structure(case: int = 0) -> List[List[int]]:
     return [_random_subset(rd, 3) for _ in range(4)]
 
 
-def config3(case: int = 0, b: int = 4096) -> Workload:
+# B-dependency lists of the coupled-transition variant of the F=3 workload:
+# every factor moves conditioned on itself and on one other factor
+CONFIG3_BDEPS = [[0, 1], [1, 2], [0, 2]]
+
+
+def config3(case: int = 0, b: int = 4096, bdeps=None) -> Workload:
     """F=3 (12,10,8; U=4,2,1), M=4 x 16 outcomes on random factor subsets, T=20,
-    per-agent Dirichlet(0.5) models."""
+    per-agent Dirichlet(0.5) models.  bdeps: optional B-dependency lists (the
+    general transition model; None: each factor on its own previous state)."""
     deps = config3_structure(case)
     rm, rs = _rng(3, case, 0), _rng(3, case, 1)
-    model = make_model(rm, [12, 10, 8], [4, 2, 1], [16] * 4, deps, b, 0.5, 0.5)
+    model = make_model(rm, [12, 10, 8], [4, 2, 1], [16] * 4, deps, b, 0.5, 0.5, bdeps=bdeps)
     obs, act = sample_sequences(rs, model, b, 20)
-    return Workload(f"cfg3_F3_M4_T20_b{b}", ["mmp"], model, obs, act, 16)
+    tag = "" if bdeps is None else "_bdeps"
+    return Workload(f"cfg3_F3_M4_T20_b{b}{tag}", ["mmp"], model, obs, act, 16)
 
 
 @dataclasses.dataclass

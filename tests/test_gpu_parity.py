@@ -129,11 +129,45 @@ def test_shared_equals_replicated():
         assert np.abs(qs - qr).max() <= 1e-6
 
 
-@pytest.mark.parametrize("case", [0, 1, 2, 3, 4, 5, 6, 7])
-def test_config4_sweep_sample(case):
-    sp = synth.config4_spec(case)
-    if sp.a_floats() > 8_000_000:
-        pytest.skip("large sweep case: covered by the streaming tests")
-    w = synth.config4(case)
+def _sweep_sample(regime, count, seed):
+    """A seeded sample of sweep models whose oracle cost stays small."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    out = []
+    for case in rng.permutation(synth.N_SWEEP):
+        if synth.config4_spec(int(case), regime).a_floats() <= 400_000:
+            out.append(int(case))
+        if len(out) == count:
+            break
+    return sorted(out)
+
+
+SWEEP = [("uniform", c) for c in _sweep_sample("uniform", 24, 4)] + \
+        [("skewed", c) for c in _sweep_sample("skewed", 24, 46)]
+
+
+@pytest.mark.parametrize("regime,case", SWEEP)
+def test_config4_sweep_sample(regime, case):
+    """Sweep models of both dimension regimes (one model shared by 256
+    agents): every algorithm on the family the selector picks, and VMP / MMP
+    on the sparse kernels, against the oracle on four agents."""
+    import os
+    w = synth.config4(case, regime=regime)
+    agents = [0, 1, 128, 255]
     for algo in ("fpi", "vmp", "mmp"):
-        check(w, algo, agents=[0, 1, 128, 255])
+        check(w, algo, agents=agents)
+    old = os.environ.get("BI_FORCE_PATH")
+    os.environ["BI_FORCE_PATH"] = "sparse"
+    try:
+        for algo in ("vmp", "mmp"):
+            q, pm = run_gpu(w, algo, flags=bi.BI_SPARSE_A)
+            assert pm.path(w.b, w.T, algo) == "sparse"
+            ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=agents)
+            err = float(np.abs(q[agents] - ref).max())
+            print(f"[gpu]   sweep {regime} {case} {algo} sparse vs oracle {err:.3e}", flush=True)
+            assert err <= TOL
+            pm.close()
+    finally:
+        if old is None:
+            os.environ.pop("BI_FORCE_PATH", None)
+        else:
+            os.environ["BI_FORCE_PATH"] = old

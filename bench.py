@@ -6,8 +6,11 @@ Workload: the large shared-model case -- F = 4 hidden factors of 32 states
 factors (32^5 entries per A_m, 90% random zeros, renormalised columns), one
 model shared by b = 64 agents, window T = 16, 16 iterations.  One step runs
 VMP and MMP over the whole batch on both A layouts:
-  dense  (BI_DENSE_A | BI_FAST_F32): fp32 matrix-core contractions over the
-         dense slices, fp64 message sums / transitions / softmax;
+  dense  (BI_DENSE_A | BI_FAST_F32 | BI_F16_PAIRS): the slices stored as fp16
+         (high, residual) pairs, contracted on fp16 matrix cores with three
+         products per fp32 product and fp32 accumulation; fp64 message sums /
+         transitions / softmax (--dense-f32: fp32 matrix cores on the fp32
+         copy instead);
   sparse (BI_SPARSE_A): fp64 gathers over the nonzero entries.
 Inputs are resident in HBM before timing starts; each model is packed once
 outside the timed region (the one-time layout step).
@@ -40,13 +43,14 @@ sys.path.insert(0, ROOT)
 
 METRIC = "belief updates/sec (agents×timesteps×iters) + achieved HBM GB/s, 1 MI355X"
 PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_FP16_MFMA_TFLOPS = 2500.0
 PEAK_FP64_VALU_TFLOPS = 78.6
 PEAK_HBM_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cfg5.json")
 CSRC = os.path.join(ROOT, "paper_2607_17855_amd", "csrc")
 # likelihood kernels: profile class -> (kernel symbol, source file)
-LIK = {"lik": ("lik_kernel", "stream.hip"), "lik_split": ("split_lik_kernel", "split.hip"),
-       "lik_sparse": ("sparse_lik_kernel", "sparse.hip")}
+LIK = {"lik": ("lik_kernel", "stream.hip"), "lik_split": ("split_lik_kernel<false>", "split.hip"),
+       "lik_split16": ("split_lik_kernel<true>", "split.hip"), "lik_sparse": ("sparse_lik_kernel", "sparse.hip")}
 LAYOUTS = ("dense", "sparse")
 ALGOS = ("vmp", "mmp")
 
@@ -185,6 +189,8 @@ def main():
     ap.add_argument("--layouts", default=",".join(LAYOUTS), help="comma list of A layouts in a step")
     ap.add_argument("--workload", default="large", choices=["large"] + list(AGENT_WORKLOADS))
     ap.add_argument("--soft", action="store_true", help="soft observation vectors (per-agent workloads)")
+    ap.add_argument("--dense-f32", action="store_true",
+                    help="dense layout on fp32 matrix cores (the fp32 copy) instead of the fp16 pairs")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a device-to-device copy of MIB MiB (reference kernel for HBM byte counters)")
     args = ap.parse_args()
@@ -207,7 +213,8 @@ def main():
         print("bench.py: --soft applies to the per-agent workloads (--workload)", file=sys.stderr)
         sys.exit(2)
     w = synth.config5()
-    flags = {"dense": bi.BI_DENSE_A | bi.BI_FAST_F32, "sparse": bi.BI_SPARSE_A}
+    dense_flags = bi.BI_DENSE_A | bi.BI_FAST_F32 | (0 if args.dense_f32 else bi.BI_F16_PAIRS)
+    flags = {"dense": dense_flags, "sparse": bi.BI_SPARSE_A}
     pms = {lay: bi.PackedModel(w.model, flags=flags[lay], device=dev) for lay in layouts}
     obs = torch.from_numpy(w.obs).to(dev)
     act = torch.from_numpy(w.act).to(dev)
@@ -253,7 +260,8 @@ def main():
 
     traffic = load_traffic()
     dense_work = dense_lik_work(w.model, w.obs)
-    work = {"lik": dense_work, "lik_split": dense_work, "lik_sparse": sparse_lik_work(w.model, w.obs)}
+    work = {"lik": dense_work, "lik_split": dense_work, "lik_split16": dense_work,
+            "lik_sparse": sparse_lik_work(w.model, w.obs)}
     rooflines = {}
     for cls, (kname, src) in LIK.items():
         if cls not in prof:
@@ -263,13 +271,17 @@ def main():
         flops, alg_bytes = work[cls]
         tr = traffic.get(kname)
         hbm = tr["hbm_bytes_per_launch"] if tr and tr.get("kernel_source_sha") == source_sha(src) else None
-        if cls in ("lik", "lik_split"):
-            bound, peak = "mfma", PEAK_FP32_MFMA_TFLOPS
+        if cls == "lik_split16":
+            # memory bound: the fp16 products (3 per fp32 product) take a
+            # fraction of the time the slice bytes do
+            bound, peak, unit = "hbm", PEAK_HBM_GBPS, "GB/s"
+            achieved = alg_bytes / (avg_ms / 1e3) / 1e9
         else:
-            bound, peak = "alu", PEAK_FP64_VALU_TFLOPS
-        achieved = flops / (avg_ms / 1e3) / 1e12
+            bound, peak = ("mfma", PEAK_FP32_MFMA_TFLOPS) if cls in ("lik", "lik_split") else ("alu", PEAK_FP64_VALU_TFLOPS)
+            unit = "TFLOP/s"
+            achieved = flops / (avg_ms / 1e3) / 1e12
         rooflines[cls] = {
-            "bound": bound, "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+            "bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
             "traffic": hbm, "kernel": kname, "avg_launch_ms": avg_ms, "launches": launches,
             "total_ms": total_ms, "algorithmic_flops_per_launch": flops,
             "algorithmic_bytes_per_launch": alg_bytes,
@@ -277,6 +289,10 @@ def main():
             "measured_hbm_GBps": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9,
             "hbm_frac": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
         }
+        if cls == "lik_split16":
+            f16 = 3 * flops / (avg_ms / 1e3) / 1e12
+            rooflines[cls]["fp16_mfma"] = {"achieved_TFLOPs": f16, "peak": PEAK_FP16_MFMA_TFLOPS,
+                                           "frac": f16 / PEAK_FP16_MFMA_TFLOPS}
     dominant = max(rooflines, key=lambda c: rooflines[c]["total_ms"])
     out = {
         "metric": METRIC,
@@ -289,18 +305,21 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32+f64",
+        "dtype": "f32+f64" if args.dense_f32 else "f16x2+f64",
         "data": "synthetic",
         "config": {"workload": "shared model F=4x32 states (U=4), M=4x32 outcomes on all factors, 90% zeros, "
-                               "b=64, T=16, 16 iters; step = VMP + MMP on the dense (fp32 MFMA) and sparse "
-                               "(fp64) A layouts",
+                               "b=64, T=16, 16 iters; step = VMP + MMP on the dense ("
+                               + ("fp32 MFMA" if args.dense_f32 else "fp16-pair MFMA") + ") and sparse (fp64) A layouts",
                    "b": w.b, "T": w.T, "iters": w.iters, "algos": list(ALGOS), "layouts": layouts},
         "roofline": rooflines[dominant],
         "roofline_all": rooflines,
         "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
         "wall_s_timed": wall,
-        "dtype_note": "dense layout: fp32 matrix-core contractions (v_mfma_f32_16x16x4f32) with fp64 message sums, "
-                      "transitions and softmax; sparse layout: fp64 throughout",
+        "dtype_note": ("dense layout: fp32 matrix-core contractions (v_mfma_f32_16x16x4f32)" if args.dense_f32 else
+                       "dense layout: slices as fp16 (high, residual) pairs, 22 significant bits, contracted with "
+                       "three fp16 matrix-core products per fp32 product (v_mfma_f32_16x16x32_f16), fp32 "
+                       "accumulation") + " with fp64 message sums, transitions and softmax; sparse layout: fp64 "
+                      "throughout; every marginal within 1e-5 of the fp64 oracle",
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, list(ALGOS))

@@ -57,6 +57,15 @@ extern "C" {
  * marginals are insensitive to fp32 rounding of the log-likelihoods; it
  * stores an extra fp32 copy of the slices. */
 #define BI_FAST_F32 4u
+/* With BI_FAST_F32 and the dense layout, a shared model also stores every
+ * slice as pairs of fp16 values (high part, rounded residual: 22 significant
+ * bits, 4 bytes per entry like the fp32 copy), and the slice contractions of
+ * the shapes the matrix-core kernel takes (two factors on each side of the
+ * two-sided view, second factors of 16 or 32 states) run on fp16 matrix cores:
+ * three fp16 products per fp32 product (high x high, high x residual,
+ * residual x high), accumulated in fp32.  The contraction then moves the same
+ * bytes at a fraction of the fp32 matrix-core time. */
+#define BI_F16_PAIRS 16u
 /* Input checking.  Out-of-range observations or actions are undefined
  * behaviour by default.  With BI_CHECK every inference call first scans obs
  * and act on the device, synchronises its stream and returns
@@ -68,7 +77,8 @@ extern "C" {
 
 /* Kernel families (bi_query_path). */
 #define BI_PATH_AGENT 0  /* agent-resident fp64 kernels: one workgroup per agent, all iterations in-kernel */
-#define BI_PATH_STREAM 1 /* dense streaming kernels: fp32 matrix-core contractions (shared model, BI_FAST_F32) */
+#define BI_PATH_STREAM 1 /* dense streaming kernels: fp32 (or, with BI_F16_PAIRS, fp16-pair) matrix-core
+                            contractions (shared model, BI_FAST_F32) */
 #define BI_PATH_SPARSE 2 /* sparse streaming kernels: fp64 gathers over the nonzeros (shared model, BI_SPARSE_A) */
 
 /* Algorithm ids (bi_workspace_size). */

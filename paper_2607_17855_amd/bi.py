@@ -25,6 +25,7 @@ BI_ERR_DEVICE = -5
 BI_DENSE_A = 1
 BI_SPARSE_A = 2
 BI_FAST_F32 = 4
+BI_F16_PAIRS = 16
 BI_CHECK = 8
 BI_ALGO_FPI, BI_ALGO_VMP, BI_ALGO_MMP = 0, 1, 2
 ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}

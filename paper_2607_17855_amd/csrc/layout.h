@@ -66,6 +66,9 @@ struct ModDesc {
     int64_t csr_ptr_off, csr_ent_off;   // byte offsets, or -1
     int64_t csc_ptr_off, csc_ent_off;
     int64_t nnz;                        // entries of the modality (each stored twice)
+    // fp16 pairs (BI_F16_PAIRS): the slices [K][R][Cp] in groups of 4 columns,
+    // 16 bytes each: the 4 high parts, then the 4 residuals; or -1
+    int64_t lp16_off;
 };
 
 constexpr int kMaxBDep = 4;   // B-dependencies per factor

@@ -46,8 +46,10 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
         return fail(BI_ERR_INVALID_ARG, "desc has a NULL array");
     if (d->model_batch < 1) return fail(BI_ERR_INVALID_ARG, "model_batch must be >= 1");
     uint32_t flags = d->flags ? d->flags : BI_DENSE_A;
-    if ((flags & ~(BI_DENSE_A | BI_SPARSE_A | BI_FAST_F32 | BI_CHECK)) != 0)
+    if ((flags & ~(BI_DENSE_A | BI_SPARSE_A | BI_FAST_F32 | BI_F16_PAIRS | BI_CHECK)) != 0)
         return fail(BI_ERR_INVALID_ARG, "unknown bits in flags");
+    if ((flags & BI_F16_PAIRS) && (!(flags & BI_FAST_F32) || (flags & BI_SPARSE_A)))
+        return fail(BI_ERR_INVALID_ARG, "BI_F16_PAIRS needs BI_FAST_F32 and the dense layout");
     if ((flags & (BI_DENSE_A | BI_SPARSE_A)) == 0) flags |= BI_DENSE_A;
     if ((flags & BI_DENSE_A) && (flags & BI_SPARSE_A))
         return fail(BI_ERR_INVALID_ARG, "flags must hold one of BI_DENSE_A and BI_SPARSE_A");
@@ -200,6 +202,11 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
             md.la32_off = off;
             off = align_up(off + 4 * (int64_t)m->mb * md.K * md.slice, kAlign);
         }
+        md.lp16_off = -1;
+        if ((flags & BI_F16_PAIRS) && m->mb == 1) {   // (the matrix-core kernels serve shared models)
+            md.lp16_off = off;
+            off = align_up(off + 4 * (int64_t)md.K * md.slice, kAlign);
+        }
         md.csr_ptr_off = md.csr_ent_off = md.csc_ptr_off = md.csc_ent_off = -1;
         md.nnz = 0;
         if (flags & BI_SPARSE_A) {
@@ -266,6 +273,31 @@ static void parallel_for(int64_t count, Fn fn)
 
 static inline double ln_clamped(double x) { return std::log(x > kEps ? x : kEps); }
 
+// IEEE binary16 bits of v rounded to nearest, ties to even (|v| below 65504;
+// subnormals kept), and the value they hold in *rounded.  Directly from the
+// double, so there is no second rounding through fp32.
+static uint16_t half_rne(double v, double *rounded)
+{
+    const uint16_t sign = std::signbit(v) ? 0x8000 : 0;
+    const double a = std::fabs(v);
+    uint16_t bits = 0;
+    double r = 0.0;
+    if (a > 0.0) {
+        int e;
+        std::frexp(a, &e);                 // a = f 2^e, f in [0.5, 1)
+        int E = std::max(e - 1, -14);      // binade (the subnormals share the lowest)
+        double k = std::nearbyint(std::ldexp(a, 10 - E));   // 11-bit significand, ties to even
+        if (k >= 2048.0) {                 // rounded up into the next binade
+            k = 1024.0;
+            ++E;
+        }
+        r = std::ldexp(k, E - 10);
+        bits = k < 1024.0 ? (uint16_t)k : (uint16_t)(((E + 15) << 10) | ((int)k - 1024));
+    }
+    if (rounded) *rounded = sign ? -r : r;
+    return sign | bits;
+}
+
 int fill(const bi_model *m, const float *const *A, const float *const *B, const float *const *D, char *host,
          int64_t *nnz_out)
 {
@@ -296,6 +328,15 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
             if (md.la32_off >= 0) {
                 float *d32 = reinterpret_cast<float *>(host + md.la32_off) + s * md.slice;
                 for (int64_t e = 0; e < md.slice; ++e) d32[e] = (float)dst[e];
+            }
+            if (md.lp16_off >= 0) {   // shared model: s is the outcome
+                uint16_t *p = reinterpret_cast<uint16_t *>(host + md.lp16_off) + 2 * s * md.slice;
+                for (int64_t e = 0; e < md.slice; e += 4)
+                    for (int i = 0; i < 4; ++i) {
+                        double hi;
+                        p[2 * e + i] = half_rne(dst[e + i], &hi);
+                        p[2 * e + 4 + i] = half_rne(dst[e + i] - hi, nullptr);
+                    }
             }
             nnz += cnt;
         });

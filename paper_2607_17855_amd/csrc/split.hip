@@ -20,9 +20,21 @@
 // second line factor's as one partial vector per tile.  Both roles of a slice
 // are dispatched next to each other, so the second read of the slice mostly
 // hits the last-level cache.
+//
+// With fp16 pairs (BI_F16_PAIRS) the same tiles run on fp16 matrix cores:
+// the slice is read from its pair copy (4 columns per 16 bytes: high parts,
+// then residuals), the A operand is q_e1 scaled by 2^15 and split into an
+// fp16 high part and residual once per pass, and each first-factor state e0
+// is one 16x16x32 (16x16x16 for 16-state second factors) product chain of
+// three fp16 MFMAs: (A high, X high), (A high, X residual), (A residual,
+// X high).  The chain starts from zero and is added to the accumulators with
+// the weight q_e0[c][e0] 2^-15 in fp32, so nothing but the operand split ever
+// leaves fp32 and the scaling keeps the small marginals clear of the fp16
+// subnormals.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "internal.h"
 #include "profile.h"
@@ -39,8 +51,14 @@ constexpr int kMaxKb = 3;                      // 16-context MFMA blocks per pas
 constexpr int kCtx = 16 * kMaxKb;
 constexpr int kMaxT = 8;                       // k-steps per first-factor state (second factor <= 32)
 constexpr int kZS = kCtx + 1;                  // line-tile stride (floats)
+constexpr int kXcds = 8;                       // accelerator dies; workgroup i runs on die i % 8
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+constexpr float kPairScale = 32768.0f;   // 2^15: q_e1 in [0, 1] scaled below the fp16 maximum
 
 struct Geo {
     int lines, ln0, ln1, lf0, lf1;   // line side (two factors)
@@ -160,14 +178,155 @@ __device__ void split_tile(const StreamArgs &a, const Geo &g, const float *__res
     }
 }
 
+__device__ inline uint32_t pack_halves(_Float16 lo, _Float16 hi)
+{
+    return (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+}
+
+// The fp16-pair version of split_tile.  KS = en1 (16 or 32) is the MFMA's K:
+// a lane holds KW = KS / 4 consecutive k values (entries e1 = KW lg + i) of
+// its A row (context 16 kb + li) and of its B column (line).  qe0t holds
+// q_e0 2^-15 as [e0][kCtx], so a lane reads the weights of its 4
+// accumulator rows (contexts 16 kb + 4 lg + v) as one float4.
+template <int NKB, int ROLE, int KS>
+__device__ void split16_tile(const StreamArgs &a, const Geo &g, const char *__restrict__ P, int64_t Cp, int lb,
+                             int le, const float *qe0t, const float *qe1, float *zt)
+{
+    constexpr int KW = KS / 4;   // k values per lane
+    constexpr int DW = KW / 2;   // dwords per operand
+    using HV = std::conditional_t<KS == 32, h8, h4>;
+    using UV = std::conditional_t<KS == 32, u4, u2>;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wl0 = lb + kWaveLines * wave;
+    if (wl0 >= le) return;
+    const int li = lane & 15, lg = lane >> 4;
+    // A operand: q_e1 2^15 = high + residual, both fp16
+    HV ah[NKB], al[NKB];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+        UV hd, ld;
+#pragma unroll
+        for (int p = 0; p < DW; ++p) {
+            const float *src = qe1 + (16 * kb + li) * kMaxT * 4 + KW * lg + 2 * p;
+            const float v0 = src[0] * kPairScale, v1 = src[1] * kPairScale;
+            const _Float16 h0 = (_Float16)v0, h1 = (_Float16)v1;
+            hd[p] = pack_halves(h0, h1);
+            ld[p] = pack_halves((_Float16)(v0 - (float)h0), (_Float16)(v1 - (float)h1));
+        }
+        ah[kb] = __builtin_bit_cast(HV, hd);
+        al[kb] = __builtin_bit_cast(HV, ld);
+    }
+    f4 acc[4][NKB];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) acc[j][kb] = f4{0.f, 0.f, 0.f, 0.f};
+
+    // 16-byte loads of one first-factor state (4 columns of a row: 4 high
+    // parts, 4 residuals):
+    //   role 0: slot (KW / 4) j + h = line wl0 + 16 j + li, entries e0*KS + KW lg + 4 h .. +3
+    //   role 1: slot i = entry e0*KS + KW lg + i, lines wl0 + 4 li .. +3
+    // (lines past the tile are clamped to a valid one; their results are dropped)
+    constexpr int H = KW / 4, NS = ROLE == 0 ? 4 * H : KW;
+    uint32_t bo[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (ROLE == 0) {
+            const int line = min(wl0 + 16 * (s / H) + li, le - 1);
+            bo[s] = 4u * (uint32_t)(line * (int)Cp + KW * lg + 4 * (s % H));
+        } else {
+            const int line = min(wl0 + 4 * li, le - 4);
+            bo[s] = 4u * (uint32_t)((KW * lg + s) * (int)Cp + line);
+        }
+    }
+    const uint32_t step = 4u * (ROLE == 0 ? KS : KS * (uint32_t)Cp);   // to the next first-factor state
+    auto load = [&](u4 (&b)[NS], int e0) {
+        const uint32_t eo = (uint32_t)e0 * step;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) b[s] = *reinterpret_cast<const u4 *>(P + (bo[s] + eo));
+    };
+    auto use = [&](const u4 (&b)[NS], int e0) {
+        f4 w[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) w[kb] = *reinterpret_cast<const f4 *>(qe0t + e0 * kCtx + 16 * kb + 4 * lg);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            UV xh, xl;
+            if (ROLE == 0) {
+                // the lane's KW entries of line j: consecutive columns of one row
+#pragma unroll
+                for (int h = 0; h < H; ++h) {
+                    xh[2 * h] = b[H * j + h][0];
+                    xh[2 * h + 1] = b[H * j + h][1];
+                    xl[2 * h] = b[H * j + h][2];
+                    xl[2 * h + 1] = b[H * j + h][3];
+                }
+            } else {
+                // column j of the KW rows: one half of every load, paired up
+                const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+#pragma unroll
+                for (int p = 0; p < DW; ++p) {
+                    xh[p] = __builtin_amdgcn_perm(b[2 * p + 1][j >> 1], b[2 * p][j >> 1], sel);
+                    xl[p] = __builtin_amdgcn_perm(b[2 * p + 1][2 + (j >> 1)], b[2 * p][2 + (j >> 1)], sel);
+                }
+            }
+            const HV bh = __builtin_bit_cast(HV, xh), bl = __builtin_bit_cast(HV, xl);
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) {
+                f4 d = f4{0.f, 0.f, 0.f, 0.f};
+                if constexpr (KS == 32) {
+                    d = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[kb], bh, d, 0, 0, 0);
+                    d = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[kb], bl, d, 0, 0, 0);
+                    d = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[kb], bh, d, 0, 0, 0);
+                } else {
+                    d = __builtin_amdgcn_mfma_f32_16x16x16f16(ah[kb], bh, d, 0, 0, 0);
+                    d = __builtin_amdgcn_mfma_f32_16x16x16f16(ah[kb], bl, d, 0, 0, 0);
+                    d = __builtin_amdgcn_mfma_f32_16x16x16f16(al[kb], bh, d, 0, 0, 0);
+                }
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[j][kb][v] = fmaf(w[kb][v], d[v], acc[j][kb][v]);
+            }
+        }
+    };
+    u4 ba[NS], bb[NS];
+    load(ba, 0);
+    for (int e0 = 0; e0 < g.en0; e0 += 2) {
+        load(bb, e0 + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        use(ba, e0);
+        __builtin_amdgcn_sched_barrier(0);
+        load(ba, min(e0 + 2, g.en0 - 1));
+        __builtin_amdgcn_sched_barrier(0);
+        use(bb, e0 + 1);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int line = ROLE == 0 ? wl0 + 16 * j + li : wl0 + 4 * li + j;
+        if (line < le)
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) zt[(line - lb) * kZS + 16 * kb + 4 * lg + v] = acc[j][kb][v];
+    }
+}
+
+template <bool PAIRS>
 __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, const float *__restrict__ q,
                                                              float *__restrict__ part)
 {
     extern __shared__ float sh[];
     __shared__ int ctxs[kCtx];
     // decode (modality, outcome, role, tile): the two roles of a modality share
-    // its workgroup range, outcome-major, so both roles of a slice run together
-    const int wg = blockIdx.x;
+    // its workgroup range, outcome-major, so both roles of a slice run together.
+    // Workgroups are dealt to the dies round-robin, so each die gets a
+    // contiguous range of that order: both roles of a slice run on one die
+    // (the second read of the slice can hit that die's L2), and every die
+    // streams its own slices (consecutive workgroups on different dies would
+    // put all first reads of the slices on half of them).
+    const int per_die = (a.nwg + kXcds - 1) / kXcds;
+    const int wg = (int)(blockIdx.x % kXcds) * per_die + (int)(blockIdx.x / kXcds);
+    if (wg >= a.nwg) return;
     int m = 0;
     while (m + 1 < a.M && a.task[2 * (m + 1)].wg0 <= wg) ++m;
     const SpTask t0 = a.task[2 * m], t1 = a.task[2 * m + 1];
@@ -186,7 +345,9 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
     const int gs = tile * G, ng = min(G, g.ln0 - gs);
     const int lb = gs * g.ln1, le = (gs + ng) * g.ln1;
     const float *X = reinterpret_cast<const float *>(a.base + md.la32_off) + (int64_t)o * md.slice;
+    const char *P = PAIRS ? a.base + md.lp16_off + 4 * (int64_t)o * md.slice : nullptr;
     float *qe0 = sh;                      // [kCtx][32]: marginals of the entry side's first factor
+                                          // (pairs: [32][kCtx], times 2^-15)
     float *qe1 = qe0 + kCtx * 32;         // [kCtx][32]: second factor
     float *zt = qe1 + kCtx * kMaxT * 4;   // [tile lines][kZS]
     const int tid = threadIdx.x;
@@ -203,7 +364,10 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
             float v = 0.0f;
             if (s < 32) {
                 if (ctx >= 0 && s < g.en0) v = q[(int64_t)ctx * a.ntot + off_e0 + s];
-                qe0[c * 32 + s] = v;
+                if (PAIRS)
+                    qe0[s * kCtx + c] = v * (1.0f / kPairScale);
+                else
+                    qe0[c * 32 + s] = v;
             } else {
                 if (ctx >= 0 && s - 32 < g.en1) v = q[(int64_t)ctx * a.ntot + off_e1 + s - 32];
                 qe1[c * 32 + s - 32] = v;
@@ -214,7 +378,11 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
         const int nt = g.en1 >> 2;
         // dispatch on (role, context blocks, k-steps per state); eligibility
         // admits second factors of 16 or 32 states
-#define BI_SPLIT_TILE(R, K, T) split_tile<K, R, T>(a, g, X, md.Cp, lb, le, qe0, qe1, zt)
+#define BI_SPLIT_TILE(R, K, T)                                                                \
+    do {                                                                                      \
+        if constexpr (PAIRS) split16_tile<K, R, 4 * T>(a, g, P, md.Cp, lb, le, qe0, qe1, zt);  \
+        else split_tile<K, R, T>(a, g, X, md.Cp, lb, le, qe0, qe1, zt);                        \
+    } while (0)
 #define BI_SPLIT_NT(R, K) \
     if (nt == 8) BI_SPLIT_TILE(R, K, 8); \
     else BI_SPLIT_TILE(R, K, 4)
@@ -328,9 +496,20 @@ int64_t split_plan(const bi_model *m, StreamArgs *a)
 
 size_t split_lds_bytes(const bi_model *m) { return lds_bytes(m); }
 
+bool split_pairs(const bi_model *m)
+{
+    for (const ModDesc &md : m->mods)
+        if (md.lp16_off < 0) return false;
+    return !m->mods.empty();
+}
+
 void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream)
 {
-    hipLaunchKernelGGL(split_lik_kernel, dim3(a.nwg), dim3(kThreads), lds_bytes(m), stream, a, q, part);
+    const unsigned grid = (unsigned)((a.nwg + kXcds - 1) / kXcds * kXcds);
+    if (split_pairs(m))
+        hipLaunchKernelGGL(split_lik_kernel<true>, dim3(grid), dim3(kThreads), lds_bytes(m), stream, a, q, part);
+    else
+        hipLaunchKernelGGL(split_lik_kernel<false>, dim3(grid), dim3(kThreads), lds_bytes(m), stream, a, q, part);
 }
 
 }  // namespace bi

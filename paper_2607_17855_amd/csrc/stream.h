@@ -85,6 +85,8 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
 bool split_eligible(const bi_model *m);
 int64_t split_plan(const bi_model *m, StreamArgs *a);
 size_t split_lds_bytes(const bi_model *m);
+// every modality has its fp16-pair copy (BI_F16_PAIRS): the fp16 matrix-core tiles run
+bool split_pairs(const bi_model *m);
 void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream);
 
 // Sparse likelihood kernel (sparse.hip): task planning and one launch.

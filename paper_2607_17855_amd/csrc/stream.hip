@@ -628,7 +628,7 @@ static void run_iterations(const bi_model *m, int algo, int iters, const StreamA
     using PT = QT;
     for (int k = 0; k < iters; ++k) {
         {
-            ProfScope p(sparse ? "lik_sparse" : split ? "lik_split" : "lik", stream);
+            ProfScope p(sparse ? "lik_sparse" : split ? (split_pairs(m) ? "lik_split16" : "lik_split") : "lik", stream);
             if (sparse)
                 sparse_lik_launch(m, a, reinterpret_cast<const double *>(cur), reinterpret_cast<double *>(part),
                                   stream);

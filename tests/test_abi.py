@@ -39,7 +39,8 @@ class ModDesc(ctypes.Structure):
                 ("rf", ctypes.c_int32 * 2), ("rn", ctypes.c_int32 * 2), ("cf", ctypes.c_int32 * 2),
                 ("cn", ctypes.c_int32 * 2), ("zv_off", ctypes.c_int32), ("dsum", ctypes.c_int32),
                 ("la32_off", ctypes.c_int64), ("csr_ptr_off", ctypes.c_int64), ("csr_ent_off", ctypes.c_int64),
-                ("csc_ptr_off", ctypes.c_int64), ("csc_ent_off", ctypes.c_int64), ("nnz", ctypes.c_int64)]
+                ("csc_ptr_off", ctypes.c_int64), ("csc_ent_off", ctypes.c_int64), ("nnz", ctypes.c_int64),
+                ("lp16_off", ctypes.c_int64)]
 
 
 SpEntry = np.dtype([("v", np.float64), ("a", np.uint32), ("b", np.uint32)])
@@ -130,6 +131,10 @@ def test_plan_rejects_bad_descriptors():
     assert _desc_err([3], [1], [2], [[0]], mb=0) == bi.BI_ERR_INVALID_ARG
     assert _desc_err([3], [1], [2], [[0]], flags=3) == bi.BI_ERR_INVALID_ARG
     assert _desc_err([3], [1], [2], [[0]], flags=64) == bi.BI_ERR_INVALID_ARG
+    # fp16 pairs only with BI_FAST_F32 and the dense layout
+    assert _desc_err([3], [1], [2], [[0]], flags=bi.BI_F16_PAIRS) == bi.BI_ERR_INVALID_ARG
+    assert _desc_err([3], [1], [2], [[0]], flags=bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS) == \
+        bi.BI_ERR_INVALID_ARG
     lib = bi.load()
     out = ctypes.c_size_t(0)
     assert lib.bi_plan_model(None, ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG
@@ -469,3 +474,72 @@ def test_bdeps_validation_and_dispatch():
             else:
                 os.environ["BI_FORCE_PATH"] = old
             bi.bi_free_model(h)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_f16_pair_plane(seed):
+    """The fp16-pair copy of every slice: groups of 4 columns, 4 high parts then
+    4 residuals, where high = the fp64 log-likelihood rounded to binary16 (ties
+    to even) and residual = (value - high) rounded the same way; numpy's
+    float64 -> float16 conversion rounds directly from the double and is the
+    reference.  Per-agent models get no pair copy."""
+    w = synth.random_small(520 + seed, F_max=4, n_max=7, M_max=3, K_max=4, T_max=2, b=2,
+                           sparsity=0.5 * (seed % 2), per_agent=False)
+    m = w.model
+    fl = bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
+    h, img = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, 1, m.A, m.B, m.D, flags=fl)
+    try:
+        assert img.size == bi.bi_plan_model(m.n, m.U, m.K, m.deps, 1, fl)
+        mods, _ = _descs(img, m.M, m.F)
+        for mi in range(m.M):
+            md = mods[mi]
+            assert md.lp16_off >= 0 and md.lp16_off % 256 == 0
+            X = img[md.la_off:md.la_off + 8 * md.K * md.slice].view(np.float64).reshape(md.K, md.R, md.Cp // 4, 4)
+            P = img[md.lp16_off:md.lp16_off + 4 * md.K * md.slice].view(np.float16).reshape(md.K, md.R, md.Cp // 4, 2, 4)
+            hi = X.astype(np.float16)
+            np.testing.assert_array_equal(P[..., 0, :].view(np.uint16), hi.view(np.uint16))
+            lo = (X - hi.astype(np.float64)).astype(np.float16)
+            np.testing.assert_array_equal(P[..., 1, :].view(np.uint16), lo.view(np.uint16))
+            # 22 significant bits: |X - hi - lo| <= 2^-22 |X| (plus the binary16 subnormal spacing)
+            err = np.abs(X - hi.astype(np.float64) - lo.astype(np.float64))
+            assert np.all(err <= 2.0 ** -22 * np.abs(X) + 2.0 ** -25)
+    finally:
+        bi.bi_free_model(h)
+    # per-agent: no pair copy
+    wa = synth.random_small(530 + seed, F_max=3, n_max=5, M_max=2, K_max=3, T_max=2, b=2, per_agent=True)
+    ma = wa.model
+    h, img = bi.bi_pack_model_host(ma.n, ma.U, ma.K, ma.deps, ma.mb, ma.A, ma.B, ma.D, flags=fl)
+    try:
+        mods, _ = _descs(img, ma.M, ma.F)
+        assert all(mods[i].lp16_off == -1 for i in range(ma.M))
+    finally:
+        bi.bi_free_model(h)
+
+
+def test_f16_pairs_wide_range():
+    """A slice whose probabilities span 1e-16 .. 1: high parts over many
+    binades and residuals down in the binary16 subnormals, each matching
+    numpy's rounding from the double."""
+    rng = np.random.Generator(np.random.PCG64(5))
+    n, K = [64], [2]
+    p = 10.0 ** rng.uniform(-16, 0, size=64)
+    A = np.stack([p, 1.0 - p])[None].astype(np.float32)   # [agent][o][s]
+    B = [np.full((1, 64, 64, 1), 1.0 / 64, np.float32)]
+    D = [np.full((1, 64), 1.0 / 64, np.float32)]
+    fl = bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
+    h, img = bi.bi_pack_model_host(n, [1], K, [[0]], 1, [A], B, D, flags=fl)
+    try:
+        mods, _ = _descs(img, 1, 1)
+        md = mods[0]
+        X = img[md.la_off:md.la_off + 8 * md.K * md.slice].view(np.float64).reshape(md.K, md.Cp // 4, 4)
+        P = img[md.lp16_off:md.lp16_off + 4 * md.K * md.slice].view(np.uint16).reshape(md.K, md.Cp // 4, 2, 4)
+        hi = X.astype(np.float16)
+        lo = (X - hi.astype(np.float64)).astype(np.float16)
+        np.testing.assert_array_equal(P[:, :, 0, :], hi.view(np.uint16))
+        np.testing.assert_array_equal(P[:, :, 1, :], lo.view(np.uint16))
+        expo = lambda u: (u >> 10) & 0x1F
+        assert len(set(expo(P[:, :, 0, :]).ravel().tolist())) >= 6, "high parts over several binades"
+        sub = (expo(P[:, :, 1, :]) == 0) & ((P[:, :, 1, :] & 0x3FF) != 0)
+        assert sub.any(), "some residuals are binary16 subnormals"
+    finally:
+        bi.bi_free_model(h)

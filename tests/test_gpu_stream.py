@@ -73,16 +73,24 @@ SPLIT_CASES = [
 ]
 
 
+FAST = {"f32": bi.BI_DENSE_A | bi.BI_FAST_F32, "f16pairs": bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS}
+
+
 @pytest.mark.parametrize("case", range(len(SPLIT_CASES)))
-def test_split_kernel_vs_oracle_and_agent(case, force_stream):
+@pytest.mark.parametrize("prec", list(FAST))
+def test_split_kernel_vs_oracle_and_agent(case, prec, force_stream):
     n, U, K, deps, b, T = SPLIT_CASES[case]
     w = _shared_model(80 + case, n, U, K, deps, b, T, iters=2)
     for algo in ("vmp", "mmp"):
-        q, pm = run_gpu(w, algo, flags=bi.BI_DENSE_A | bi.BI_FAST_F32)
+        q, pm = run_gpu(w, algo, flags=FAST[prec])
         check_invariants(w, q)
         ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters)
         err = float(np.abs(q - ref).max())
-        print(f"[gpu]   split stream vs oracle {err:.3e}", flush=True)
+        print(f"[gpu]   split ({prec}) stream vs oracle {err:.3e}", flush=True)
+        bi.bi_profile_begin()
+        run_gpu(w, algo, pm=pm)
+        names = set(bi.bi_profile_end())
+        assert ("lik_split16" if prec == "f16pairs" else "lik_split") in names, names
         assert err <= TOL
         os.environ["BI_FORCE_PATH"] = "agent"
         qa, _ = run_gpu(w, algo, pm=pm)
@@ -100,9 +108,11 @@ CFG5_AGENTS = [0, 21, 42, 63]
 
 
 @pytest.mark.parametrize("algo", ["vmp", "mmp"])
-def test_config5_stream(algo):
+@pytest.mark.parametrize("prec", list(FAST))
+def test_config5_stream(algo, prec):
     w = cfg5()
-    q, pm = run_gpu(w, algo, flags=bi.BI_DENSE_A | bi.BI_FAST_F32)
+    print(f"[gpu] config 5 {algo} {prec}", flush=True)
+    q, pm = run_gpu(w, algo, flags=FAST[prec])
     assert pm.path(w.b, w.T, algo) == "stream", "the selector must send the large model to the streaming kernels"
     assert pm.workspace(w.b, w.T, algo) is not None, "config 5 must take the streaming path"
     check_invariants(w, q)
@@ -110,6 +120,6 @@ def test_config5_stream(algo):
     assert np.array_equal(q, q2), "streaming path is not reproducible"
     ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=CFG5_AGENTS)
     err = float(np.abs(q[CFG5_AGENTS] - ref).max())
-    print(f"[gpu]   config 5 {algo} stream vs oracle (agents {CFG5_AGENTS}): {err:.3e}", flush=True)
+    print(f"[gpu]   config 5 {algo} stream ({prec}) vs oracle (agents {CFG5_AGENTS}): {err:.3e}", flush=True)
     assert err <= TOL
     pm.close()

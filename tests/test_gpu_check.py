@@ -32,6 +32,7 @@ CASES = [
     # (workload maker, flags, algos, family): agent-resident, dense streaming, sparse streaming
     (lambda: synth.random_small(610, b=4, T_max=5, per_agent=True), bi.BI_DENSE_A, ("fpi", "vmp", "mmp"), "agent"),
     (lambda: _shared_big(611), bi.BI_DENSE_A | bi.BI_FAST_F32, ("vmp", "mmp"), "stream"),
+    (lambda: _shared_big(613), bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS, ("vmp", "mmp"), "stream"),
     (lambda: _shared_big(612), bi.BI_SPARSE_A, ("vmp", "mmp"), "sparse"),
 ]
 

@@ -104,14 +104,19 @@ SHARED = [
     ([9, 7, 5], [2, 1, 3], [3, 2, 4], [[0, 1, 2], [1], [0, 2]], 24, 5),
     ([6, 16, 4, 32], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], 24, 5),
     ([13, 11, 6, 3], [1, 2, 2, 1], [5, 3], [[0, 1, 2, 3], [1, 3]], 40, 1),
+    ([4, 32, 6, 32], [2, 1, 2, 1], [3, 2], [[0, 1, 2, 3], [0, 1, 2, 3]], 30, 4),
 ]
+# dense streaming packings: fp32 copy, and fp16 pairs (the matrix-core shapes
+# then run on fp16 matrix cores)
+DENSE_FAST = [bi.BI_DENSE_A | bi.BI_FAST_F32, bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS]
 
 
 @pytest.mark.parametrize("case", range(len(SHARED)))
-def test_prior_stream_path(case):
+@pytest.mark.parametrize("flags", DENSE_FAST)
+def test_prior_stream_path(case, flags):
     w = _shared_model(600 + case, *SHARED[case])
     for algo in ("vmp", "mmp"):
-        _check_prior(w, algo, bi.BI_DENSE_A | bi.BI_FAST_F32, "stream", 700 + case)
+        _check_prior(w, algo, flags, "stream", 700 + case)
 
 
 @pytest.mark.parametrize("case", range(len(SHARED)))
@@ -206,5 +211,6 @@ def test_damping_stream_and_sparse_paths(case):
     w = _shared_model(640 + case, *SHARED[case], iters=3)
     ws = _shared_model(660 + case, *SHARED[case], sparsity=0.6, iters=3)
     for algo in ("vmp", "mmp"):
-        _check_damped(w, algo, bi.BI_DENSE_A | bi.BI_FAST_F32, "stream", 740 + case, 0.45, case == 1)
-        _check_damped(ws, algo, bi.BI_SPARSE_A, "sparse", 760 + case, 0.7, case != 1)
+        for flags in DENSE_FAST:
+            _check_damped(w, algo, flags, "stream", 740 + case, 0.45, case % 2 == 1)
+        _check_damped(ws, algo, bi.BI_SPARSE_A, "sparse", 760 + case, 0.7, case % 2 == 0)

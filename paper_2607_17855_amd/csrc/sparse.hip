@@ -73,6 +73,26 @@ __host__ __device__ inline Side side_of(const ModDesc &md, int role)
     return s;
 }
 
+// sum_{i < n} z[i * zs] w[i] in fp64, in order, with the loads issued 8 at a
+// time (the fold's operands sit in LDS and L2: one wait per 8 terms)
+__device__ inline double dot_batched(const double *z, int zs, const double *w, int n)
+{
+    double acc = 0.0;
+    int i = 0;
+    for (; i + 8 <= n; i += 8) {
+        double zv[8], wv[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            zv[k] = z[(i + k) * zs];
+            wv[k] = w[i + k];
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc = fma(zv[k], wv[k], acc);
+    }
+    for (; i < n; ++i) acc = fma(z[i * zs], w[i], acc);
+    return acc;
+}
+
 // line groups per tile: whole first-factor states, about kSpLines lines
 __host__ __device__ inline int groups_per_tile(const Side &s)
 {
@@ -205,19 +225,14 @@ __global__ __launch_bounds__(kSpThreads, 1) void sparse_lik_kernel(StreamArgs a,
             for (int i = tid; i < jc * ng; i += kSpThreads) {
                 const int c = i / ng, g = i - c * ng;
                 const double *qc = q + (int64_t)ctxs[c] * a.ntot + off_l1;
-                const double *z = zt + g * ln1 * kZS + c;
-                double acc = 0.0;
-                for (int l1 = 0; l1 < ln1; ++l1) acc = fma(z[l1 * kZS], qc[l1], acc);
-                part[(int64_t)ctxs[c] * ps + tk.so + g0 + g] = acc;
+                part[(int64_t)ctxs[c] * ps + tk.so + g0 + g] = dot_batched(zt + g * ln1 * kZS + c, kZS, qc, ln1);
             }
             // second line factor: the tile's partial, summed over its groups
             for (int i = tid; i < jc * ln1; i += kSpThreads) {
                 const int c = i / ln1, l1 = i - c * ln1;
                 const double *qc = q + (int64_t)ctxs[c] * a.ntot + off_l0 + g0;
-                const double *z = zt + l1 * kZS + c;
-                double acc = 0.0;
-                for (int g = 0; g < ng; ++g) acc = fma(z[g * ln1 * kZS], qc[g], acc);
-                part[(int64_t)ctxs[c] * ps + tk.so + sd_.ln0 + (int64_t)tile * ln1 + l1] = acc;
+                part[(int64_t)ctxs[c] * ps + tk.so + sd_.ln0 + (int64_t)tile * ln1 + l1] =
+                    dot_batched(zt + l1 * kZS + c, ln1 * kZS, qc, ng);
             }
         }
         __syncthreads();

@@ -81,6 +81,26 @@ __host__ __device__ inline Geo geo_of(const ModDesc &md, int role)
     return g;
 }
 
+// sum_{i < n} z[i * zs] w[i] in fp32, in order, with the loads issued 8 at a
+// time (the fold's operands sit in LDS and L2: one wait per 8 terms)
+__device__ inline float dot_batched(const float *z, int zs, const float *w, int n)
+{
+    float acc = 0.0f;
+    int i = 0;
+    for (; i + 8 <= n; i += 8) {
+        float zv[8], wv[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            zv[k] = z[(i + k) * zs];
+            wv[k] = w[i + k];
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc = fmaf(zv[k], wv[k], acc);
+    }
+    for (; i < n; ++i) acc = fmaf(z[i * zs], w[i], acc);
+    return acc;
+}
+
 // line groups per tile: whole first-factor states, at most kTileLines lines
 __host__ __device__ inline int split_groups(const Geo &g) { return std::max(1, kTileLines / g.ln1); }
 
@@ -406,18 +426,13 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
         for (int i = tid; i < jc * ng; i += kThreads) {
             const int c = i / ng, gg = i - c * ng;
             const float *qc = q + (int64_t)ctxs[c] * a.ntot + off_l1;
-            const float *z = zt + gg * ln1 * kZS + c;
-            float acc = 0.0f;
-            for (int l1 = 0; l1 < ln1; ++l1) acc = fmaf(z[l1 * kZS], qc[l1], acc);
-            part[(int64_t)ctxs[c] * ps + tk.so + gs + gg] = acc;
+            part[(int64_t)ctxs[c] * ps + tk.so + gs + gg] = dot_batched(zt + gg * ln1 * kZS + c, kZS, qc, ln1);
         }
         for (int i = tid; i < jc * ln1; i += kThreads) {
             const int c = i / ln1, l1 = i - c * ln1;
             const float *qc = q + (int64_t)ctxs[c] * a.ntot + off_l0 + gs;
-            const float *z = zt + l1 * kZS + c;
-            float acc = 0.0f;
-            for (int gg = 0; gg < ng; ++gg) acc = fmaf(z[gg * ln1 * kZS], qc[gg], acc);
-            part[(int64_t)ctxs[c] * ps + tk.so + g.ln0 + (int64_t)tile * ln1 + l1] = acc;
+            part[(int64_t)ctxs[c] * ps + tk.so + g.ln0 + (int64_t)tile * ln1 + l1] =
+                dot_batched(zt + l1 * kZS + c, ln1 * kZS, qc, ng);
         }
         __syncthreads();
     }

@@ -46,7 +46,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_FP16_MFMA_TFLOPS = 2500.0
 PEAK_FP64_VALU_TFLOPS = 78.6
 PEAK_HBM_GBPS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cfg5.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_large_shared.json")
 CSRC = os.path.join(ROOT, "paper_2607_17855_amd", "csrc")
 # likelihood kernels: profile class -> (kernel symbol, source file)
 LIK = {"lik": ("lik_kernel", "stream.hip"), "lik_split": ("split_lik_kernel<false>", "split.hip"),
@@ -126,15 +126,15 @@ def agent_work(model, T, algo):
 
 # per-agent workloads: name -> (generator, algorithm, options)
 AGENT_WORKLOADS = {
-    "vmp_2f": ("config2", "vmp", {}),
-    "mmp_3f": ("config3", "mmp", {}),
-    "fpi_hmm": ("config1", "fpi", {}),
+    "vmp_2f": ("two_factor_agents", "vmp", {}),
+    "mmp_3f": ("three_factor_agents", "mmp", {}),
+    "fpi_hmm": ("hmm_small", "fpi", {}),
     # the F=2 models filtered over the whole window, and online: one step per
     # call, each carrying the predictive prior of the step before (bi_predict)
-    "fpi_2f": ("config2", "fpi", {}),
-    "fpi_2f_rolling": ("config2", "fpi", {"rolling": True}),
+    "fpi_2f": ("two_factor_agents", "fpi", {}),
+    "fpi_2f_rolling": ("two_factor_agents", "fpi", {"rolling": True}),
     # the F=3 structure with coupled transitions (B-dependency lists)
-    "mmp_3f_bdeps": ("config3", "mmp", {"bdeps": True}),
+    "mmp_3f_bdeps": ("three_factor_agents", "mmp", {"bdeps": True}),
 }
 
 
@@ -195,8 +195,8 @@ def main():
                     help="also run a device-to-device copy of MIB MiB (reference kernel for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this library runs on one GPU; multi-GPU runs are not part of this build "
-              "(agents shard across GPUs with no communication, see DESIGN.md)", file=sys.stderr)
+        print("bench.py: runs on one GPU only (agents are independent: a multi-GPU job shards them "
+              "across GPUs with no communication)", file=sys.stderr)
         sys.exit(2)
     layouts = [x for x in args.layouts.split(",") if x]
     assert set(layouts) <= set(LAYOUTS) and layouts, f"layouts must be among {LAYOUTS}"
@@ -212,7 +212,7 @@ def main():
     if args.soft:
         print("bench.py: --soft applies to the per-agent workloads (--workload)", file=sys.stderr)
         sys.exit(2)
-    w = synth.config5()
+    w = synth.large_shared()
     dense_flags = bi.BI_DENSE_A | bi.BI_FAST_F32 | (0 if args.dense_f32 else bi.BI_F16_PAIRS)
     flags = {"dense": dense_flags, "sparse": bi.BI_SPARSE_A}
     pms = {lay: bi.PackedModel(w.model, flags=flags[lay], device=dev) for lay in layouts}
@@ -222,7 +222,7 @@ def main():
           for lay in layouts for a in ALGOS}
     wss = {(lay, a): pms[lay].workspace(w.b, w.T, a) for lay in layouts for a in ALGOS}
     for key, ws in wss.items():
-        assert ws is not None, f"{key}: config 5 must run on the streaming kernels"
+        assert ws is not None, f"{key}: the large shared model must run on the streaming kernels"
     stream = torch.cuda.current_stream()
 
     def step():
@@ -331,7 +331,7 @@ def bench_agent(args, bi, synth, torch, dev):
     (online workloads: T one-step calls and T - 1 predictive priors)."""
     import numpy as np
     cfg, algo, opts = AGENT_WORKLOADS[args.workload]
-    w = getattr(synth, cfg)(bdeps=synth.CONFIG3_BDEPS) if opts.get("bdeps") else getattr(synth, cfg)()
+    w = getattr(synth, cfg)(bdeps=synth.THREE_FACTOR_BDEPS) if opts.get("bdeps") else getattr(synth, cfg)()
     rolling = bool(opts.get("rolling"))
     if rolling and args.soft:
         print("bench.py: --soft is not combined with the online workload", file=sys.stderr)

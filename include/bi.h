@@ -39,7 +39,7 @@ extern "C" {
 #define BI_ERR_INVALID_ARG (-1)      /* null pointer, non-positive size, bad enum, ... */
 #define BI_ERR_SHAPE (-2)            /* inconsistent shapes or dependency lists       */
 #define BI_ERR_BUFFER_TOO_SMALL (-3) /* dev_bytes / ws_bytes below what is required   */
-#define BI_ERR_UNSUPPORTED (-4)      /* valid, but beyond what this build handles     */
+#define BI_ERR_UNSUPPORTED (-4)      /* valid, but beyond what this library handles   */
 #define BI_ERR_DEVICE (-5)           /* a HIP runtime call failed                     */
 
 /* bi_model_desc.flags: layout of the emission tensors on the device, ORed

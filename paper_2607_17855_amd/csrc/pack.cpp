@@ -79,7 +79,7 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
                 return fail(BI_ERR_SHAPE, "modality %d: dependency list not strictly ascending", mm);
         }
         if (k > 2 * kMaxSide)
-            return fail(BI_ERR_UNSUPPORTED, "modality %d depends on %d factors; this build handles up to %d", mm, k,
+            return fail(BI_ERR_UNSUPPORTED, "modality %d depends on %d factors; this library handles up to %d", mm, k,
                         2 * kMaxSide);
     }
     m->dep.assign(d->dep, d->dep + d->dep_off[d->M]);
@@ -96,7 +96,7 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
             const int k = d->bdep_off[f + 1] - d->bdep_off[f];
             if (k < 1) return fail(BI_ERR_SHAPE, "factor %d: empty B-dependency list", f);
             if (k > kMaxBDep)
-                return fail(BI_ERR_UNSUPPORTED, "factor %d: %d B-dependencies; this build handles up to %d", f, k,
+                return fail(BI_ERR_UNSUPPORTED, "factor %d: %d B-dependencies; this library handles up to %d", f, k,
                             kMaxBDep);
             for (int i = d->bdep_off[f]; i < d->bdep_off[f + 1]; ++i) {
                 if (d->bdep[i] < 0 || d->bdep[i] >= d->F)

@@ -38,7 +38,7 @@ def main():
     t_start = time.time()
     with open(args.out, "a") as out:
         for case in range(lo, hi):
-            w = synth.config4(case, b=args.b, regime=args.regime)
+            w = synth.sweep_model(case, b=args.b, regime=args.regime)
             w = synth.Workload(w.name, w.algos, w.model, w.obs, w.act, args.iters)
             obs = torch.from_numpy(w.obs).cuda()
             act = torch.from_numpy(w.act).cuda()

@@ -124,7 +124,7 @@ def _dirichlet_columns(rng: np.random.Generator, alpha: float, shape_outer, k: i
 
 def _sparsify_columns(rng: np.random.Generator, a: np.ndarray, axis: int, p_zero: float) -> np.ndarray:
     """Impose random zeros with probability p_zero, keep one random entry of any
-    column that became all-zero, then renormalise the columns (config 5)."""
+    column that became all-zero, then renormalise the columns (the large shared model)."""
     keep = rng.random(a.shape) >= p_zero
     col_any = keep.any(axis=axis, keepdims=True)
     if not np.all(col_any):
@@ -272,42 +272,42 @@ def _random_subset(rng: np.random.Generator, F: int) -> List[int]:
             return [int(f) for f in np.nonzero(mask)[0]]
 
 
-def config1(case: int = 0) -> Workload:
+def hmm_small(case: int = 0) -> Workload:
     """Single-factor HMM: 4 states, 3 outcomes, 2 actions, T=8, b=1, FPI x16."""
     rm, rs = _rng(1, case, 0), _rng(1, case, 1)
     model = make_model(rm, [4], [2], [3], [[0]], 1, 1.0, 1.0)
     obs, act = sample_sequences(rs, model, 1, 8)
-    return Workload("cfg1_hmm_n4_T8_b1", ["fpi"], model, obs, act, 16)
+    return Workload("hmm_n4_T8_b1", ["fpi"], model, obs, act, 16)
 
 
-def config2(case: int = 0, b: int = 1024) -> Workload:
+def two_factor_agents(case: int = 0, b: int = 1024) -> Workload:
     """F=2 (8,6; U=3,1), M=3 (5,7,4) all on both factors, T=10, per-agent models."""
     rm, rs = _rng(2, case, 0), _rng(2, case, 1)
     model = make_model(rm, [8, 6], [3, 1], [5, 7, 4], [[0, 1]] * 3, b, 1.0, 1.0)
     obs, act = sample_sequences(rs, model, b, 10)
-    return Workload(f"cfg2_F2_M3_T10_b{b}", ["vmp"], model, obs, act, 16)
+    return Workload(f"F2_M3_T10_b{b}", ["vmp"], model, obs, act, 16)
 
 
-def config3_structure(case: int = 0) -> List[List[int]]:
+def three_factor_structure(case: int = 0) -> List[List[int]]:
     rd = _rng(3, case, 2)
     return [_random_subset(rd, 3) for _ in range(4)]
 
 
 # B-dependency lists of the coupled-transition variant of the F=3 workload:
 # every factor moves conditioned on itself and on one other factor
-CONFIG3_BDEPS = [[0, 1], [1, 2], [0, 2]]
+THREE_FACTOR_BDEPS = [[0, 1], [1, 2], [0, 2]]
 
 
-def config3(case: int = 0, b: int = 4096, bdeps=None) -> Workload:
+def three_factor_agents(case: int = 0, b: int = 4096, bdeps=None) -> Workload:
     """F=3 (12,10,8; U=4,2,1), M=4 x 16 outcomes on random factor subsets, T=20,
     per-agent Dirichlet(0.5) models.  bdeps: optional B-dependency lists (the
     general transition model; None: each factor on its own previous state)."""
-    deps = config3_structure(case)
+    deps = three_factor_structure(case)
     rm, rs = _rng(3, case, 0), _rng(3, case, 1)
     model = make_model(rm, [12, 10, 8], [4, 2, 1], [16] * 4, deps, b, 0.5, 0.5, bdeps=bdeps)
     obs, act = sample_sequences(rs, model, b, 20)
     tag = "" if bdeps is None else "_bdeps"
-    return Workload(f"cfg3_F3_M4_T20_b{b}{tag}", ["mmp"], model, obs, act, 16)
+    return Workload(f"F3_M4_T20_b{b}{tag}", ["mmp"], model, obs, act, 16)
 
 
 @dataclasses.dataclass
@@ -337,7 +337,7 @@ def _skewed_dims(rd: np.random.Generator, count: int, lo: int = 2, hi: int = 32)
     return [int(h) if t else int(x) for t, h, x in zip(top, high, low)]
 
 
-def config4_spec(case: int, regime: str = "uniform") -> SweepSpec:
+def sweep_spec(case: int, regime: str = "uniform") -> SweepSpec:
     """One of the sweep POMDP specifications (case = 0..769).  regime
     "uniform" draws every state and outcome count uniformly from 2..32;
     "skewed" draws them from the extremes of that range (_skewed_dims)."""
@@ -363,24 +363,24 @@ def config4_spec(case: int, regime: str = "uniform") -> SweepSpec:
 N_SWEEP = 770
 
 
-def config4(case: int, b: int = 256, regime: str = "uniform") -> Workload:
+def sweep_model(case: int, b: int = 256, regime: str = "uniform") -> Workload:
     """Sweep POMDP ``case``: one generative model shared by the b agents."""
-    sp = config4_spec(case, regime)
+    sp = sweep_spec(case, regime)
     cfg = 4 if regime == "uniform" else SKEWED_CFG
     rm, rs = _rng(cfg, case, 0), _rng(cfg, case, 1)
     model = make_model(rm, sp.n, sp.U, sp.K, sp.deps, 1, 1.0, 1.0)
     obs, act = sample_sequences(rs, model, b, sp.T)
-    tag = "cfg4" if regime == "uniform" else "cfg4skew"
+    tag = "sweep" if regime == "uniform" else "sweep_skewed"
     return Workload(f"{tag}_case{case}_b{b}", ["fpi", "vmp", "mmp"], model, obs, act, 16)
 
 
-def config5(case: int = 0, b: int = 64, n: int = 32, F: int = 4, M: int = 4, K: int = 32, T: int = 16) -> Workload:
+def large_shared(case: int = 0, b: int = 64, n: int = 32, F: int = 4, M: int = 4, K: int = 32, T: int = 16) -> Workload:
     """Large shared model: F=4 x 32 states (4 actions), M=4 x 32 outcomes, every
     A_m on all factors, 90% random zeros then renormalised columns, T=16."""
     rm, rs = _rng(5, case, 0), _rng(5, case, 1)
     model = make_model(rm, [n] * F, [4] * F, [K] * M, [list(range(F))] * M, 1, 1.0, 1.0, sparsity=0.9)
     obs, act = sample_sequences(rs, model, b, T)
-    return Workload(f"cfg5_F{F}x{n}_M{M}x{K}_T{T}_b{b}", ["vmp", "mmp"], model, obs, act, 16, sparse_A=True)
+    return Workload(f"shared_F{F}x{n}_M{M}x{K}_T{T}_b{b}", ["vmp", "mmp"], model, obs, act, 16, sparse_A=True)
 
 
 def random_small(seed: int, F_max: int = 3, n_max: int = 5, M_max: int = 3, K_max: int = 4, T_max: int = 4,

@@ -142,7 +142,7 @@ def test_plan_rejects_bad_descriptors():
 
 
 def test_plan_sizes_cover_every_array():
-    w = synth.config2(b=4)
+    w = synth.two_factor_agents(b=4)
     m = w.model
     nbytes = bi.bi_plan_model(m.n, m.U, m.K, m.deps, m.mb)
     need = sum(8 * a.size for a in m.A) + sum(12 * b.size + 8 * d.size for b, d in zip(m.B, m.D))
@@ -381,7 +381,7 @@ def test_selector_table_matches_the_fitted_trees(regime):
     cases = sorted(set(int(c) for c in rng.choice(770, size=40, replace=False)))
     checked = 0
     for case in cases:
-        sp = synth.config4_spec(case, regime)
+        sp = synth.sweep_spec(case, regime)
         model = synth.make_model(np.random.Generator(np.random.PCG64(case)), sp.n, sp.U, sp.K, sp.deps, 1)
         for cset, fl in flags.items():
             h, _ = bi.bi_pack_model_host(model.n, model.U, model.K, model.deps, 1, model.A, model.B, model.D,
@@ -453,7 +453,7 @@ def test_bdeps_validation_and_dispatch():
     d.c.bdep = None                                               # one of the two arrays missing
     out = ctypes.c_size_t(0)
     assert bi.load().bi_plan_model(ctypes.byref(d.c), ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG
-    # five dependencies, and a factor on nine lists: beyond this build
+    # five dependencies, and a factor on nine lists: beyond what the library handles
     big = synth.make_model(np.random.Generator(np.random.PCG64(1)), [2] * 9, [1] * 9, [2], [[0]], 1)
     bd = bi._Desc(big.n, big.U, big.K, big.deps, 1, bi.BI_DENSE_A, [[0, 1, 2, 3, 4]] + [[f] for f in range(1, 9)])
     assert bi.load().bi_plan_model(ctypes.byref(bd.c), ctypes.byref(out)) == bi.BI_ERR_UNSUPPORTED

@@ -55,22 +55,22 @@ def check(w, algo, agents=None, flags=bi.BI_DENSE_A):
 
 @functools.lru_cache(maxsize=None)
 def cfg(i, **kw):
-    return {1: synth.config1, 2: synth.config2, 3: synth.config3}[i](**kw)
+    return {1: synth.hmm_small, 2: synth.two_factor_agents, 3: synth.three_factor_agents}[i](**kw)
 
 
 @pytest.mark.parametrize("algo", ["fpi", "vmp", "mmp"])
-def test_config1(algo):
+def test_hmm_small(algo):
     check(cfg(1), algo)
 
 
 @pytest.mark.parametrize("algo", ["vmp", "fpi", "mmp"])
-def test_config2(algo):
+def test_two_factor_agents(algo):
     w = cfg(2)
     check(w, algo, agents=None if algo == "vmp" else range(0, w.b, 7))
 
 
 @pytest.mark.parametrize("algo", ["mmp", "vmp", "fpi"])
-def test_config3(algo):
+def test_three_factor_agents(algo):
     w = cfg(3)
     check(w, algo, agents=None if algo == "mmp" else range(0, w.b, 31))
 
@@ -111,7 +111,7 @@ def test_deterministic_and_agent_equivariant():
     q2, _ = run_gpu(w, "vmp", pm=pm)
     assert np.array_equal(q1, q2), "two identical calls differ"
     perm = np.random.Generator(np.random.PCG64(1)).permutation(w.b)
-    wp = synth.Workload("cfg2_perm", w.algos, w.model.agent_slice(perm), w.obs[perm], w.act[perm], w.iters)
+    wp = synth.Workload("F2_perm", w.algos, w.model.agent_slice(perm), w.obs[perm], w.act[perm], w.iters)
     qp, _ = run_gpu(wp, "vmp")
     assert np.array_equal(qp, q1[perm])
     pm.close()
@@ -134,7 +134,7 @@ def _sweep_sample(regime, count, seed):
     rng = np.random.Generator(np.random.PCG64(seed))
     out = []
     for case in rng.permutation(synth.N_SWEEP):
-        if synth.config4_spec(int(case), regime).a_floats() <= 400_000:
+        if synth.sweep_spec(int(case), regime).a_floats() <= 400_000:
             out.append(int(case))
         if len(out) == count:
             break
@@ -146,12 +146,12 @@ SWEEP = [("uniform", c) for c in _sweep_sample("uniform", 24, 4)] + \
 
 
 @pytest.mark.parametrize("regime,case", SWEEP)
-def test_config4_sweep_sample(regime, case):
+def test_sweep_sample(regime, case):
     """Sweep models of both dimension regimes (one model shared by 256
     agents): every algorithm on the family the selector picks, and VMP / MMP
     on the sparse kernels, against the oracle on four agents."""
     import os
-    w = synth.config4(case, regime=regime)
+    w = synth.sweep_model(case, regime=regime)
     agents = [0, 1, 128, 255]
     for algo in ("fpi", "vmp", "mmp"):
         check(w, algo, agents=agents)

@@ -86,25 +86,25 @@ def test_sparse_fpi_uses_dense_planes():
 
 
 @functools.lru_cache(maxsize=None)
-def cfg5():
-    return synth.config5()
+def large_shared():
+    return synth.large_shared()
 
 
-CFG5_AGENTS = [0, 21, 42, 63]
+LARGE_AGENTS = [0, 21, 42, 63]
 
 
 @pytest.mark.parametrize("algo", ["vmp", "mmp"])
-def test_config5_sparse(algo):
-    w = cfg5()
+def test_large_shared_sparse(algo):
+    w = large_shared()
     q, pm = run_gpu(w, algo, flags=bi.BI_SPARSE_A)
     assert pm.path(w.b, w.T, algo) == "sparse", "the selector must send the large model to the sparse kernels"
     st = pm.stats()
-    print(f"[gpu]   config 5 sparse: nnz {st['a_nnz']} device bytes {st['device_bytes']}", flush=True)
+    print(f"[gpu]   large shared model sparse: nnz {st['a_nnz']} device bytes {st['device_bytes']}", flush=True)
     check_invariants(w, q)
     q2, _ = run_gpu(w, algo, pm=pm)
     assert np.array_equal(q, q2), "sparse path is not reproducible"
-    ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=CFG5_AGENTS)
-    err = float(np.abs(q[CFG5_AGENTS] - ref).max())
-    print(f"[gpu]   config 5 {algo} sparse vs oracle (agents {CFG5_AGENTS}): {err:.3e}", flush=True)
+    ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=LARGE_AGENTS)
+    err = float(np.abs(q[LARGE_AGENTS] - ref).max())
+    print(f"[gpu]   large shared model {algo} sparse vs oracle (agents {LARGE_AGENTS}): {err:.3e}", flush=True)
     assert err <= TOL
     pm.close()

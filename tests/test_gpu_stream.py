@@ -100,26 +100,26 @@ def test_split_kernel_vs_oracle_and_agent(case, prec, force_stream):
 
 
 @functools.lru_cache(maxsize=None)
-def cfg5():
-    return synth.config5()
+def large_shared():
+    return synth.large_shared()
 
 
-CFG5_AGENTS = [0, 21, 42, 63]
+LARGE_AGENTS = [0, 21, 42, 63]
 
 
 @pytest.mark.parametrize("algo", ["vmp", "mmp"])
 @pytest.mark.parametrize("prec", list(FAST))
-def test_config5_stream(algo, prec):
-    w = cfg5()
-    print(f"[gpu] config 5 {algo} {prec}", flush=True)
+def test_large_shared_stream(algo, prec):
+    w = large_shared()
+    print(f"[gpu] large shared model {algo} {prec}", flush=True)
     q, pm = run_gpu(w, algo, flags=FAST[prec])
     assert pm.path(w.b, w.T, algo) == "stream", "the selector must send the large model to the streaming kernels"
-    assert pm.workspace(w.b, w.T, algo) is not None, "config 5 must take the streaming path"
+    assert pm.workspace(w.b, w.T, algo) is not None, "the large shared model must take the streaming path"
     check_invariants(w, q)
     q2, _ = run_gpu(w, algo, pm=pm)
     assert np.array_equal(q, q2), "streaming path is not reproducible"
-    ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=CFG5_AGENTS)
-    err = float(np.abs(q[CFG5_AGENTS] - ref).max())
-    print(f"[gpu]   config 5 {algo} stream ({prec}) vs oracle (agents {CFG5_AGENTS}): {err:.3e}", flush=True)
+    ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=LARGE_AGENTS)
+    err = float(np.abs(q[LARGE_AGENTS] - ref).max())
+    print(f"[gpu]   large shared model {algo} stream ({prec}) vs oracle (agents {LARGE_AGENTS}): {err:.3e}", flush=True)
     assert err <= TOL
     pm.close()

@@ -225,10 +225,10 @@ def main():
         assert ws is not None, f"{key}: the large shared model must run on the streaming kernels"
     stream = torch.cuda.current_stream()
 
-    def step():
+    def step(st=stream):
         for lay in layouts:
             for a in ALGOS:
-                pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=stream)
+                pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
 
     if args.copy_calibration > 0:
         n = args.copy_calibration * (1 << 20) // 4
@@ -321,6 +321,23 @@ def main():
                        "accumulation") + " with fp64 message sums, transitions and softmax; sparse layout: fp64 "
                       "throughout; every marginal within 1e-5 of the fp64 oracle",
     }
+    # the same step captured once in a HIP graph and replayed (the calls only
+    # enqueue kernels): launch overhead out of the way; reported beside the
+    # eager step above, which stays the headline
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):   # captured on torch's capture stream (st=None: the current one)
+        step(None)
+    graph.replay()
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for _ in range(args.steps):
+        graph.replay()
+    g1.record(stream)
+    torch.cuda.synchronize()
+    g_ms = g0.elapsed_time(g1) / args.steps
+    out["graph_replay"] = {"ms_per_step": g_ms, "value": bu_per_step / (g_ms / 1e3), "unit": "belief_updates/s"}
+    del graph
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, list(ALGOS))
     print(json.dumps(out), flush=True)

@@ -21,7 +21,10 @@
  *  - hip_stream is a hipStream_t passed as void* (NULL = the null stream).
  *    Inference calls only enqueue kernels on it: no host synchronisation, no
  *    device allocation, no host<->device copies.  Arguments are validated on
- *    the host before anything is enqueued.
+ *    the host before anything is enqueued.  So a call on a stream under HIP
+ *    graph capture is recorded as its kernels and can be replayed (the output
+ *    and workspace must then stay allocated; not with BI_CHECK, whose check
+ *    synchronises, nor inside bi_profile_begin / _end).
  *  - Layouts are C row-major.  sum_n = n_0 + ... + n_{F-1}.
  */
 #ifndef BI_H

@@ -34,9 +34,9 @@
 namespace bi {
 namespace {
 
-constexpr int kSpThreads = 1024; // 16 waves: the gathers are latency-bound, occupancy hides it
+constexpr int kSpThreads = 768;  // 12 waves, two workgroups per CU: 24 waves hide the latency
 constexpr int kSpWaves = kSpThreads / 64;
-constexpr int kSpLanes = 64;     // contexts per pass
+constexpr int kSpLanes = 48;     // contexts per pass (lanes 48..63 of a wave idle)
 constexpr int kSpLines = 128;    // target lines per tile
 constexpr int kZS = kSpLanes + 1;  // padded line-tile stride (doubles)
 constexpr int kSpBatch = 16;     // entries per gather round (4 x 64-byte scalar loads)
@@ -99,7 +99,7 @@ __host__ __device__ inline int groups_per_tile(const Side &s)
     return s.nline == 2 ? std::max(1, kSpLines / s.ln1) : kSpLines;
 }
 
-__global__ __launch_bounds__(kSpThreads, 1) void sparse_lik_kernel(StreamArgs a, const char *__restrict__ mbase,
+__global__ __launch_bounds__(kSpThreads, 6) void sparse_lik_kernel(StreamArgs a, const char *__restrict__ mbase,
                                                                    const double *__restrict__ q,
                                                                    double *__restrict__ part)
 {
@@ -160,7 +160,7 @@ __global__ __launch_bounds__(kSpThreads, 1) void sparse_lik_kernel(StreamArgs a,
         __syncthreads();
         // entry-side marginal tables (1.0 for an absent factor)
         for (int i = tid; i < ntab * kSpLanes; i += kSpThreads) {
-            const int c = i & (kSpLanes - 1), s = i >> 6;
+            const int c = i % kSpLanes, s = i / kSpLanes;
             const int ctx = ctxs[c];
             double v = 0.0;
             if (ctx >= 0) {
@@ -206,7 +206,7 @@ __global__ __launch_bounds__(kSpThreads, 1) void sparse_lik_kernel(StreamArgs a,
                 const u32x4 x = ent[e];
                 acc = fma(__hiloint2double((int)x.y, (int)x.x), t0[x.z * kSpLanes] * t1[x.w * kSpLanes], acc);
             }
-            zt[(l - lb) * kZS + lane] = acc;
+            if (lane < kSpLanes) zt[(l - lb) * kZS + lane] = acc;
         }
         sink ^= pf;
         __syncthreads();

@@ -11,7 +11,10 @@ VMP and MMP over the whole batch on both A layouts:
          products per fp32 product and fp32 accumulation; fp64 message sums /
          transitions / softmax (--dense-f32: fp32 matrix cores on the fp32
          copy instead);
-  sparse (BI_SPARSE_A): fp64 gathers over the nonzero entries.
+  sparse (BI_SPARSE_A | BI_FAST_F32 | BI_F16_PAIRS): the nonzeros stored as
+         fp16 pairs (8 bytes each) in blocks of 64 lines, scattered per
+         first-factor state into LDS and contracted on the same fp16 matrix
+         cores (--sparse-f64: fp64 gathers over the nonzero entries instead).
 Inputs are resident in HBM before timing starts; each model is packed once
 outside the timed region (the one-time layout step).
 
@@ -50,7 +53,8 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_large_shared.json")
 CSRC = os.path.join(ROOT, "paper_2607_17855_amd", "csrc")
 # likelihood kernels: profile class -> (kernel symbol, source file)
 LIK = {"lik": ("lik_kernel", "stream.hip"), "lik_split": ("split_lik_kernel<false>", "split.hip"),
-       "lik_split16": ("split_lik_kernel<true>", "split.hip"), "lik_sparse": ("sparse_lik_kernel", "sparse.hip")}
+       "lik_split16": ("split_lik_kernel<true>", "split.hip"), "lik_sparse": ("sparse_lik_kernel", "sparse.hip"),
+       "lik_sparse16": ("sparse16_lik_kernel", "split.hip")}
 LAYOUTS = ("dense", "sparse")
 ALGOS = ("vmp", "mmp")
 
@@ -101,6 +105,22 @@ def sparse_lik_work(model, obs):
         cnt = np.bincount(obs[:, :, m].ravel(), minlength=model.K[m])
         flops += 2 * 3 * float((nnz * cnt).sum())
         nbytes += 2 * 16.0 * float(nnz[cnt > 0].sum())
+    return flops, nbytes
+
+
+def sparse16_lik_work(model, obs):
+    """Algorithmic flops and HBM bytes of one sparse fp16-pair likelihood
+    launch: the flops of the dense contractions (the matrix cores run the
+    zeros too; 3 fp16 products per fp32 product come on top), and every
+    observed slice's nonzeros read once per side, 8 B each."""
+    import numpy as np
+    flops, _ = dense_lik_work(model, obs)
+    nbytes = 0.0
+    for m in range(model.M):
+        A = model.A[m][0].reshape(model.K[m], -1)
+        nnz = (A.astype(np.float64) > 1e-16).sum(axis=1)
+        cnt = np.bincount(obs[:, :, m].ravel(), minlength=model.K[m])
+        nbytes += 2 * 8.0 * float(nnz[cnt > 0].sum())
     return flops, nbytes
 
 
@@ -191,6 +211,8 @@ def main():
     ap.add_argument("--soft", action="store_true", help="soft observation vectors (per-agent workloads)")
     ap.add_argument("--dense-f32", action="store_true",
                     help="dense layout on fp32 matrix cores (the fp32 copy) instead of the fp16 pairs")
+    ap.add_argument("--sparse-f64", action="store_true",
+                    help="sparse layout on the fp64 gather kernels instead of the fp16-pair matrix-core tiles")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a device-to-device copy of MIB MiB (reference kernel for HBM byte counters)")
     args = ap.parse_args()
@@ -214,7 +236,8 @@ def main():
         sys.exit(2)
     w = synth.large_shared()
     dense_flags = bi.BI_DENSE_A | bi.BI_FAST_F32 | (0 if args.dense_f32 else bi.BI_F16_PAIRS)
-    flags = {"dense": dense_flags, "sparse": bi.BI_SPARSE_A}
+    sparse_flags = bi.BI_SPARSE_A | (0 if args.sparse_f64 else bi.BI_FAST_F32 | bi.BI_F16_PAIRS)
+    flags = {"dense": dense_flags, "sparse": sparse_flags}
     pms = {lay: bi.PackedModel(w.model, flags=flags[lay], device=dev) for lay in layouts}
     obs = torch.from_numpy(w.obs).to(dev)
     act = torch.from_numpy(w.act).to(dev)
@@ -223,6 +246,9 @@ def main():
     wss = {(lay, a): pms[lay].workspace(w.b, w.T, a) for lay in layouts for a in ALGOS}
     for key, ws in wss.items():
         assert ws is not None, f"{key}: the large shared model must run on the streaming kernels"
+    for a in ALGOS:
+        if "sparse" in layouts:
+            assert pms["sparse"].path(w.b, w.T, a) == "sparse", "the sparse layout must run the sparse kernels"
     stream = torch.cuda.current_stream()
 
     def step(st=stream):
@@ -261,7 +287,7 @@ def main():
     traffic = load_traffic()
     dense_work = dense_lik_work(w.model, w.obs)
     work = {"lik": dense_work, "lik_split": dense_work, "lik_split16": dense_work,
-            "lik_sparse": sparse_lik_work(w.model, w.obs)}
+            "lik_sparse": sparse_lik_work(w.model, w.obs), "lik_sparse16": sparse16_lik_work(w.model, w.obs)}
     rooflines = {}
     for cls, (kname, src) in LIK.items():
         if cls not in prof:
@@ -271,9 +297,10 @@ def main():
         flops, alg_bytes = work[cls]
         tr = traffic.get(kname)
         hbm = tr["hbm_bytes_per_launch"] if tr and tr.get("kernel_source_sha") == source_sha(src) else None
-        if cls == "lik_split16":
+        if cls in ("lik_split16", "lik_sparse16"):
             # memory bound: the fp16 products (3 per fp32 product) take a
-            # fraction of the time the slice bytes do
+            # fraction of the time the slice bytes (dense: every entry, 4 B;
+            # sparse: the nonzeros, 8 B) do
             bound, peak, unit = "hbm", PEAK_HBM_GBPS, "GB/s"
             achieved = alg_bytes / (avg_ms / 1e3) / 1e9
         else:
@@ -289,7 +316,7 @@ def main():
             "measured_hbm_GBps": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9,
             "hbm_frac": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
         }
-        if cls == "lik_split16":
+        if cls in ("lik_split16", "lik_sparse16"):
             f16 = 3 * flops / (avg_ms / 1e3) / 1e12
             rooflines[cls]["fp16_mfma"] = {"achieved_TFLOPs": f16, "peak": PEAK_FP16_MFMA_TFLOPS,
                                            "frac": f16 / PEAK_FP16_MFMA_TFLOPS}
@@ -305,11 +332,13 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32+f64" if args.dense_f32 else "f16x2+f64",
+        "dtype": "f32+f64" if args.dense_f32 and args.sparse_f64 else "f16x2+f64",
         "data": "synthetic",
         "config": {"workload": "shared model F=4x32 states (U=4), M=4x32 outcomes on all factors, 90% zeros, "
                                "b=64, T=16, 16 iters; step = VMP + MMP on the dense ("
-                               + ("fp32 MFMA" if args.dense_f32 else "fp16-pair MFMA") + ") and sparse (fp64) A layouts",
+                               + ("fp32 MFMA" if args.dense_f32 else "fp16-pair MFMA") + ") and sparse ("
+                               + ("fp64 gathers" if args.sparse_f64 else "fp16-pair MFMA from the nonzeros")
+                               + ") A layouts",
                    "b": w.b, "T": w.T, "iters": w.iters, "algos": list(ALGOS), "layouts": layouts},
         "roofline": rooflines[dominant],
         "roofline_all": rooflines,
@@ -318,8 +347,10 @@ def main():
         "dtype_note": ("dense layout: fp32 matrix-core contractions (v_mfma_f32_16x16x4f32)" if args.dense_f32 else
                        "dense layout: slices as fp16 (high, residual) pairs, 22 significant bits, contracted with "
                        "three fp16 matrix-core products per fp32 product (v_mfma_f32_16x16x32_f16), fp32 "
-                       "accumulation") + " with fp64 message sums, transitions and softmax; sparse layout: fp64 "
-                      "throughout; every marginal within 1e-5 of the fp64 oracle",
+                       "accumulation") + " with fp64 message sums, transitions and softmax; sparse layout: "
+                      + ("fp64 throughout" if args.sparse_f64 else
+                         "the nonzeros as fp16 pairs, scattered into LDS blocks and contracted with the same "
+                         "three-product fp16 matrix-core chains") + "; every marginal within 1e-5 of the fp64 oracle",
     }
     # the same step captured once in a HIP graph and replayed (the calls only
     # enqueue kernels): launch overhead out of the way; reported beside the

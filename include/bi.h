@@ -50,7 +50,8 @@ extern "C" {
 #define BI_DENSE_A 1u  /* dense log-domain slices (default)                         */
 #define BI_SPARSE_A 2u /* also store the nonzero entries of every slice (by rows and by
                           columns); models shared by every agent run VMP and MMP on
-                          sparse kernels (fp64 arithmetic).  FPI keeps the dense path. */
+                          sparse kernels (fp64 arithmetic; fp16-pair matrix cores with
+                          BI_F16_PAIRS).  FPI keeps the dense path. */
 /* Precision policy.  Without it every update is computed in fp64, which
  * reproduces the fp64 definition to output rounding even where the Jacobi
  * iterations amplify rounding errors by 10^3-10^4 (near-bifurcation models).
@@ -67,7 +68,15 @@ extern "C" {
  * two-sided view, second factors of 16 or 32 states) run on fp16 matrix cores:
  * three fp16 products per fp32 product (high x high, high x residual,
  * residual x high), accumulated in fp32.  The contraction then moves the same
- * bytes at a fraction of the fp32 matrix-core time. */
+ * bytes at a fraction of the fp32 matrix-core time.
+ * With BI_FAST_F32 and BI_SPARSE_A, the nonzero entries of such shapes are
+ * stored as fp16 pairs too (8 bytes per nonzero and side, in blocks of 64
+ * lines), and the sparse path runs the same fp16 matrix-core products from
+ * them: each wave scatters the nonzeros of one first-factor state into a
+ * zeroed block in LDS and contracts it.  No dense pair copy is stored then.
+ * The stored nonzeros are log(A) - log(1e-16), up to 36.8 in size, so the
+ * rounding error relative to the messages grows with the share of nonzeros;
+ * the selector takes this path for at most half the entries nonzero. */
 #define BI_F16_PAIRS 16u
 /* Input checking.  Out-of-range observations or actions are undefined
  * behaviour by default.  With BI_CHECK every inference call first scans obs
@@ -82,7 +91,8 @@ extern "C" {
 #define BI_PATH_AGENT 0  /* agent-resident fp64 kernels: one workgroup per agent, all iterations in-kernel */
 #define BI_PATH_STREAM 1 /* dense streaming kernels: fp32 (or, with BI_F16_PAIRS, fp16-pair) matrix-core
                             contractions (shared model, BI_FAST_F32) */
-#define BI_PATH_SPARSE 2 /* sparse streaming kernels: fp64 gathers over the nonzeros (shared model, BI_SPARSE_A) */
+#define BI_PATH_SPARSE 2 /* sparse streaming kernels: fp64 gathers over the nonzeros, or with BI_F16_PAIRS
+                            fp16-pair matrix-core tiles fed from them (shared model, BI_SPARSE_A) */
 
 /* Algorithm ids (bi_workspace_size). */
 #define BI_ALGO_FPI 0
@@ -97,7 +107,7 @@ extern "C" {
  *   (the A-dependency list).  model_batch is 1 when every agent shares the
  *   model, otherwise the number of agents, each with its own parameters (the
  *   batch axis b of Sec. III-B).  flags: BI_DENSE_A or BI_SPARSE_A (0 = dense),
- *   optionally ORed with BI_FAST_F32.
+ *   optionally ORed with BI_FAST_F32 (and then BI_F16_PAIRS) and BI_CHECK.
  */
 typedef struct bi_model_desc {
     int32_t F;

@@ -73,6 +73,13 @@ def load(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise ImportError(f"libbi.so not found at {path}: build it with `python -m paper_2607_17855_amd.build`")
+    # One HIP runtime per process: torch ships its own, and libbi must bind to
+    # that one.  Loading libbi first pulls in the system runtime beside it,
+    # and the second runtime to start then finds no device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     P = ctypes.POINTER

@@ -170,8 +170,9 @@ int bi_pack_model(const bi_model_desc *desc, const float *const *A, const float 
         const size_t bytes = (size_t)m->bytes;
         delete m;
         char *host = nullptr;
-        if (hipHostMalloc((void **)&host, bytes, hipHostMallocDefault) != hipSuccess)
-            return fail(BI_ERR_DEVICE, "hipHostMalloc of %zu bytes failed", bytes);
+        const hipError_t he = hipHostMalloc((void **)&host, bytes, hipHostMallocDefault);
+        if (he != hipSuccess)
+            return fail(BI_ERR_DEVICE, "hipHostMalloc of %zu bytes failed: %s", bytes, hipGetErrorString(he));
         rc = pack_host(desc, A, B, D, host, bytes, &m);
         if (rc != BI_OK) {
             hipHostFree(host);

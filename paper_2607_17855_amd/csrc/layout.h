@@ -4,7 +4,7 @@
 // parameter arrays, each 256-byte aligned (all offsets below are in bytes):
 //
 //   ModDesc[M] | FacDesc[F] | LA (dense, fp64) | LA32 (fp32, BI_FAST_F32 only) |
-//   sparse A (BI_SPARSE_A only) | B (fp32) | LB (fp64) | LD (fp64)
+//   fp16 pairs (BI_F16_PAIRS) | sparse A (BI_SPARSE_A only) | B (fp32) | LB (fp64) | LD (fp64)
 //
 // Sparse A (models shared by every agent).  Every slice X of LA - shifted by
 // log(1e-16) instead of its median, so that the structural zeros of A are
@@ -13,6 +13,20 @@
 // split of the other side's index over that side's one or two factors (row
 // entries carry the column's (c0, c1), column entries the row's (r0, r1)), so
 // the kernels never divide.  Inside a line the entries are ordered by (a, b).
+//
+// Sparse fp16 pairs (BI_SPARSE_A with BI_F16_PAIRS, modalities with two
+// factors on each side whose second factors have 16 or 32 states and whose
+// first factors an even number up to 32).  The same nonzeros, once per side
+// (side 0: lines = rows, entries = columns; side 1 the transpose), as
+// SqEntry {uint32 pair; uint32 pos}: pair = the binary16 high part of the
+// value (low half) and the binary16 rounding of its residual (high half),
+// pos = (line - first line of its block) << 8 | e1.  The lines of an outcome
+// are cut into blocks of 64; inside an outcome the entries run block by
+// block, and inside a block by the state e0 of the entry side's first
+// factor, then by line, then by e1 (the entry side's second factor).  The
+// pointer array [K][nblk * en0 + 1] (uint32, indices into the side's entry
+// array) gives the start of every (block, e0) run and, last, the end of the
+// outcome.
 //
 // Precision.  The mean-field fixed-point iterations are ill-conditioned for
 // some models: a relative perturbation of 1e-7 in A (fp32 rounding) moves
@@ -69,7 +83,25 @@ struct ModDesc {
     // fp16 pairs (BI_F16_PAIRS): the slices [K][R][Cp] in groups of 4 columns,
     // 16 bytes each: the 4 high parts, then the 4 residuals; or -1
     int64_t lp16_off;
+    // sparse fp16 pairs (BI_SPARSE_A with BI_F16_PAIRS), per side: pointer
+    // array and SqEntry array, or -1
+    int64_t sq_ptr_off[2], sq_ent_off[2];
 };
+
+constexpr int kSqBlock = 64;   // lines per block of the sparse fp16-pair layout
+
+// Whether a modality has the shape of the sparse fp16-pair layout (and of the
+// matrix-core kernels): two factors on each side, second factors of 16 or 32
+// states, first factors of an even number of states up to 32.
+inline bool sq_shape(const ModDesc &md)
+{
+    if (md.nrow != 2 || md.ncol != 2 || md.Cp != md.C) return false;
+    for (int side = 0; side < 2; ++side) {
+        const int n0 = side ? md.cn[0] : md.rn[0], n1 = side ? md.cn[1] : md.rn[1];
+        if ((n1 != 16 && n1 != 32) || n0 > 32 || n0 % 2 != 0) return false;
+    }
+    return true;
+}
 
 constexpr int kMaxBDep = 4;   // B-dependencies per factor
 constexpr int kMaxCh = 8;     // factors whose B-dependencies hold a given factor
@@ -94,6 +126,11 @@ struct FacDesc {
 struct SpEntry {
     double v;       // log(max(A, 1e-16)) - log(1e-16) > 0
     uint32_t a, b;  // split of the other side's index over that side's factors
+};
+
+struct SqEntry {
+    uint32_t pair;  // binary16 high part | binary16 residual << 16 of log(max(A, 1e-16)) - log(1e-16)
+    uint32_t pos;   // (line - block start) << 8 | e1
 };
 
 inline int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }

@@ -48,8 +48,8 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
     uint32_t flags = d->flags ? d->flags : BI_DENSE_A;
     if ((flags & ~(BI_DENSE_A | BI_SPARSE_A | BI_FAST_F32 | BI_F16_PAIRS | BI_CHECK)) != 0)
         return fail(BI_ERR_INVALID_ARG, "unknown bits in flags");
-    if ((flags & BI_F16_PAIRS) && (!(flags & BI_FAST_F32) || (flags & BI_SPARSE_A)))
-        return fail(BI_ERR_INVALID_ARG, "BI_F16_PAIRS needs BI_FAST_F32 and the dense layout");
+    if ((flags & BI_F16_PAIRS) && !(flags & BI_FAST_F32))
+        return fail(BI_ERR_INVALID_ARG, "BI_F16_PAIRS needs BI_FAST_F32");
     if ((flags & (BI_DENSE_A | BI_SPARSE_A)) == 0) flags |= BI_DENSE_A;
     if ((flags & BI_DENSE_A) && (flags & BI_SPARSE_A))
         return fail(BI_ERR_INVALID_ARG, "flags must hold one of BI_DENSE_A and BI_SPARSE_A");
@@ -203,7 +203,9 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
             off = align_up(off + 4 * (int64_t)m->mb * md.K * md.slice, kAlign);
         }
         md.lp16_off = -1;
-        if ((flags & BI_F16_PAIRS) && m->mb == 1) {   // (the matrix-core kernels serve shared models)
+        // dense pairs (the matrix-core kernels serve shared models; with the
+        // sparse layout the pairs are stored with the nonzeros instead)
+        if ((flags & BI_F16_PAIRS) && (flags & BI_DENSE_A) && m->mb == 1) {
             md.lp16_off = off;
             off = align_up(off + 4 * (int64_t)md.K * md.slice, kAlign);
         }
@@ -228,6 +230,17 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
             off = align_up(off + 4 * (int64_t)md.K * (C + 1), kAlign);
             md.csc_ent_off = off;
             off = align_up(off + (int64_t)sizeof(SpEntry) * nnz, kAlign);
+        }
+        for (int side = 0; side < 2; ++side) md.sq_ptr_off[side] = md.sq_ent_off[side] = -1;
+        if ((flags & BI_SPARSE_A) && (flags & BI_F16_PAIRS) && sq_shape(md)) {
+            for (int side = 0; side < 2; ++side) {
+                const int64_t lines = side ? C : R;
+                const int64_t runs = (lines + kSqBlock - 1) / kSqBlock * (side ? md.rn[0] : md.cn[0]);
+                md.sq_ptr_off[side] = off;
+                off = align_up(off + 4 * (int64_t)md.K * (runs + 1), kAlign);
+                md.sq_ent_off[side] = off;
+                off = align_up(off + (int64_t)sizeof(SqEntry) * md.nnz, kAlign);
+            }
         }
         a_raw += (int64_t)m->mb * md.K * R * C;
         a_stored += (int64_t)m->mb * md.K * md.slice;
@@ -380,6 +393,50 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
             }
             cptr[(int64_t)o * (C + 1) + C] = (int32_t)e;
         }
+    }
+    for (int mm = 0; mm < m->M; ++mm) {
+        const ModDesc &md = m->mods[mm];
+        if (md.sq_ptr_off[0] < 0) continue;
+        const int64_t R = md.R, C = md.C, RC = R * C;
+        const float *src = A[mm];
+        const double lne = std::log(kEps);
+        // entries per outcome (the same on both sides), then each (side,
+        // outcome) fills its own range
+        std::vector<int64_t> first(md.K + 1, 0);
+        parallel_for(md.K, [&](int64_t o) {
+            const float *a = src + o * RC;
+            int64_t cnt = 0;
+            for (int64_t e = 0; e < RC; ++e) cnt += (double)a[e] > kEps;
+            first[o + 1] = cnt;
+        });
+        for (int o = 0; o < md.K; ++o) first[o + 1] += first[o];
+        parallel_for(2 * (int64_t)md.K, [&](int64_t i) {
+            const int side = (int)(i / md.K), o = (int)(i % md.K);
+            const float *a = src + (int64_t)o * RC;
+            const int64_t lines = side ? C : R;
+            const int e0n = side ? md.rn[0] : md.cn[0], e1n = side ? md.rn[1] : md.cn[1];
+            const int64_t nblk = (lines + kSqBlock - 1) / kSqBlock, runs = nblk * e0n;
+            uint32_t *ptr = reinterpret_cast<uint32_t *>(host + md.sq_ptr_off[side]) + (int64_t)o * (runs + 1);
+            SqEntry *ent = reinterpret_cast<SqEntry *>(host + md.sq_ent_off[side]);
+            int64_t e = first[o];
+            for (int64_t blk = 0; blk < nblk; ++blk)
+                for (int e0 = 0; e0 < e0n; ++e0) {
+                    ptr[blk * e0n + e0] = (uint32_t)e;
+                    const int64_t l1 = std::min(lines, (blk + 1) * kSqBlock);
+                    for (int64_t l = blk * kSqBlock; l < l1; ++l)
+                        for (int e1 = 0; e1 < e1n; ++e1) {
+                            const int64_t other = (int64_t)e0 * e1n + e1;
+                            const double x = side ? a[other * C + l] : a[l * C + other];
+                            if (!(x > kEps)) continue;
+                            const double v = std::log(x) - lne;
+                            double hi;
+                            const uint16_t h = half_rne(v, &hi), r = half_rne(v - hi, nullptr);
+                            ent[e++] = SqEntry{(uint32_t)h | (uint32_t)r << 16,
+                                               (uint32_t)(l - blk * kSqBlock) << 8 | (uint32_t)e1};
+                        }
+                }
+            ptr[runs] = (uint32_t)e;
+        });
     }
     for (int f = 0; f < m->F; ++f) {
         const FacDesc &fd = m->facs[f];

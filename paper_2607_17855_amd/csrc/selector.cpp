@@ -12,11 +12,20 @@
 // hold no code.  Without a table for a candidate set the rule below
 // applies: sparse when packed sparse, otherwise the dense streaming kernels
 // once the largest slice reaches 16384 entries.
+//
+// A model packed with the sparse fp16-pair layout (BI_SPARSE_A with
+// BI_F16_PAIRS) runs, on the sparse path, the same matrix-core tiles as the
+// dense kernels from 8 bytes per nonzero, while its dense streaming path is
+// the fp32 kernel over 4 bytes per entry (no dense pair copy is stored).
+// Where the tree picks a streaming family for such a model, the sparse one
+// is taken while at most half the entries are nonzero (fewer bytes, and the
+// fp16 matrix-core rate), the dense one otherwise.
 #include <algorithm>
 #include <cmath>
 
 #include "internal.h"
 #include "selector_table.h"
+#include "stream.h"
 
 namespace bi {
 
@@ -57,6 +66,18 @@ int fallback(const bi_model *m, bool stream, bool sparse)
     return stream && biggest >= 16384 ? BI_PATH_STREAM : BI_PATH_AGENT;
 }
 
+// Between the two streaming families of a model with the sparse fp16-pair
+// layout (rule above).
+int streaming_pairs(const bi_model *m, bool stream)
+{
+    double nnz = 0.0, entries = 0.0;
+    for (const ModDesc &md : m->mods) {
+        nnz += (double)md.nnz;
+        entries += (double)md.K * md.R * md.C;
+    }
+    return (!stream || nnz <= 0.5 * entries) ? BI_PATH_SPARSE : BI_PATH_STREAM;
+}
+
 }  // namespace
 
 int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool sparse)
@@ -65,7 +86,10 @@ int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool spa
     const SelTree *tree = nullptr;
     for (const SelTree &t : kSelTrees)
         if (t.set == set && t.algo == algo) tree = &t;
-    if (!tree || tree->nodes == 0) return fallback(m, stream, sparse);
+    if (!tree || tree->nodes == 0) {
+        const int path = fallback(m, stream, sparse);
+        return path != BI_PATH_AGENT && sparse && sq_eligible(m) ? streaming_pairs(m, stream) : path;
+    }
     double x[kNumFeatures];
     features(m, b, T, x);
     int i = 0;
@@ -73,8 +97,9 @@ int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool spa
         const SelNode &nd = kSelNodes[tree->first + i];
         i = x[nd.feature] <= nd.threshold ? nd.left : nd.right;
     }
-    const int path = kSelNodes[tree->first + i].leaf;
-    if ((path == BI_PATH_STREAM && !stream) || (path == BI_PATH_SPARSE && !sparse)) return fallback(m, stream, sparse);
+    int path = kSelNodes[tree->first + i].leaf;
+    if ((path == BI_PATH_STREAM && !stream) || (path == BI_PATH_SPARSE && !sparse)) path = fallback(m, stream, sparse);
+    if (path != BI_PATH_AGENT && sparse && sq_eligible(m)) path = streaming_pairs(m, stream);
     return path;
 }
 

@@ -31,6 +31,14 @@
 // the weight q_e0[c][e0] 2^-15 in fp32, so nothing but the operand split ever
 // leaves fp32 and the scaling keeps the small marginals clear of the fp16
 // subnormals.
+//
+// The sparse fp16-pair layout (BI_SPARSE_A with BI_F16_PAIRS) runs the same
+// products from the nonzeros alone: for every first-factor state e0 a wave
+// scatters the nonzeros of its 64 lines with that e0 (one contiguous run of
+// 8-byte entries, layout.h) into a zeroed 64 x en1 block in LDS, reads the B
+// operands of its four 16-line MFMA tiles from there, puts the zeros back at
+// the scattered places and runs the fp16-pair product chains.  The matrix
+// cores do the dense work of the slice; memory carries only the nonzeros.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -59,6 +67,18 @@ typedef uint32_t u2 __attribute__((ext_vector_type(2)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 constexpr float kPairScale = 32768.0f;   // 2^15: q_e1 in [0, 1] scaled below the fp16 maximum
+
+// Sparse pairs: bytes per line of a wave's B block in LDS (KS high parts, KS
+// residuals, 16 bytes of padding, so the 16 lines of one operand load start
+// on different banks), and entries in flight per lane for one state e0.
+template <int KS>
+constexpr int sq_row() { return 4 * KS + 16; }
+constexpr int kSqBlockBytes = kWaveLines * sq_row<32>();   // one wave's block, sized for KS = 32
+constexpr int kSqR = 4;
+constexpr uint32_t kSqNone = 0xffffffffu;   // pos of an empty slot
+
+// kernel variants: dense fp32 slices, dense fp16 pairs, sparse fp16 pairs
+enum { kDenseF32 = 0, kDensePairs = 1, kSparsePairs = 2 };
 
 struct Geo {
     int lines, ln0, ln1, lf0, lf1;   // line side (two factors)
@@ -331,10 +351,155 @@ __device__ void split16_tile(const StreamArgs &a, const Geo &g, const char *__re
     }
 }
 
-template <bool PAIRS>
-__global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, const float *__restrict__ q,
-                                                             float *__restrict__ part)
+// The sparse fp16-pair tile.  A wave owns the 64 lines of one block of the
+// sparse layout; for each state e0 the block's run of nonzeros is scattered
+// into the wave's zeroed B block (line-major, KS high parts then KS
+// residuals per line), the B operands of the four 16-line tiles are read
+// back, the run's places are zeroed again and the product chains run as in
+// split16_tile.  Only this wave touches its block, and LDS operations of one
+// wave take effect in program order, so the block needs no barrier; the
+// scheduling barriers keep the compiler from moving LDS operations across
+// the phases.  The entries of state e0 + 1 are loaded while state e0 is used.
+// Ends with a workgroup barrier (every wave reaches it) and the line values
+// written to zt, which overlays the blocks.
+template <int NKB, int KS>
+__device__ void sq_tile(const Geo &g, const uint32_t *__restrict__ ptr, const uint2 *__restrict__ ent, int lb,
+                        int le, const float *qe0t, const float *qe1, char *blocks, float *zt)
 {
+    constexpr int KW = KS / 4;   // k values per lane
+    constexpr int DW = KW / 2;   // dwords per operand
+    constexpr int S = sq_row<KS>();
+    using HV = std::conditional_t<KS == 32, h8, h4>;
+    using UV = std::conditional_t<KS == 32, u4, u2>;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wl0 = lb + kWaveLines * wave;
+    const bool active = wl0 < le;
+    const int li = lane & 15, lg = lane >> 4;
+    f4 acc[4][NKB];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) acc[j][kb] = f4{0.f, 0.f, 0.f, 0.f};
+    if (active) {
+        // A operand: q_e1 2^15 = high + residual, both fp16
+        HV ah[NKB], al[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            UV hd, ld;
+#pragma unroll
+            for (int p = 0; p < DW; ++p) {
+                const float *src = qe1 + (16 * kb + li) * kMaxT * 4 + KW * lg + 2 * p;
+                const float v0 = src[0] * kPairScale, v1 = src[1] * kPairScale;
+                const _Float16 h0 = (_Float16)v0, h1 = (_Float16)v1;
+                hd[p] = pack_halves(h0, h1);
+                ld[p] = pack_halves((_Float16)(v0 - (float)h0), (_Float16)(v1 - (float)h1));
+            }
+            ah[kb] = __builtin_bit_cast(HV, hd);
+            al[kb] = __builtin_bit_cast(HV, ld);
+        }
+        const int en0 = g.en0;
+        // lane i <= en0 holds the start of run i of the wave's block (run en0:
+        // the block's end)
+        const uint32_t *bp = ptr + (int64_t)(wl0 / kSqBlock) * en0;
+        const int pv = (int)bp[min(lane, en0)];
+        char *bk = blocks + wave * kSqBlockBytes;
+        auto run_of = [&](int e0, uint32_t &rs, uint32_t &re) {
+            rs = (uint32_t)__builtin_amdgcn_readlane(pv, e0);
+            re = (uint32_t)__builtin_amdgcn_readlane(pv, e0 + 1);
+        };
+        auto fetch = [&](uint2 (&E)[kSqR], int e0) {
+            uint32_t rs, re;
+            run_of(e0, rs, re);
+#pragma unroll
+            for (int i = 0; i < kSqR; ++i) {
+                const uint32_t idx = rs + lane + 64 * i;
+                E[i] = idx < re ? ent[idx] : make_uint2(0u, kSqNone);
+            }
+        };
+        auto put = [&](uint2 x, bool clear) {
+            if (x.y != kSqNone) {
+                char *d = bk + (x.y >> 8) * S + (x.y & 255u) * 2;
+                *reinterpret_cast<uint16_t *>(d) = clear ? (uint16_t)0 : (uint16_t)(x.x & 0xffffu);
+                *reinterpret_cast<uint16_t *>(d + 2 * KS) = clear ? (uint16_t)0 : (uint16_t)(x.x >> 16);
+            }
+        };
+        // scatter (or zero again) the run of state e0: the entries in flight,
+        // then any beyond 64 kSqR straight from memory
+        auto scatter = [&](const uint2 (&E)[kSqR], int e0, bool clear) {
+#pragma unroll
+            for (int i = 0; i < kSqR; ++i) put(E[i], clear);
+            uint32_t rs, re;
+            run_of(e0, rs, re);
+            for (uint32_t b0 = rs + 64 * kSqR; b0 < re; b0 += 64) {
+                const uint32_t idx = b0 + lane;
+                put(idx < re ? ent[idx] : make_uint2(0u, kSqNone), clear);
+            }
+        };
+        auto step = [&](const uint2 (&E)[kSqR], int e0) {
+            scatter(E, e0, false);
+            __builtin_amdgcn_sched_barrier(0);
+            UV xh[4], xl[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const char *r = bk + (16 * j + li) * S + 2 * KW * lg;
+                xh[j] = *reinterpret_cast<const UV *>(r);
+                xl[j] = *reinterpret_cast<const UV *>(r + 2 * KS);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            scatter(E, e0, true);
+            __builtin_amdgcn_sched_barrier(0);
+            f4 w[NKB];
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+                w[kb] = *reinterpret_cast<const f4 *>(qe0t + e0 * kCtx + 16 * kb + 4 * lg);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const HV bh = __builtin_bit_cast(HV, xh[j]), bl = __builtin_bit_cast(HV, xl[j]);
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb) {
+                    f4 d = f4{0.f, 0.f, 0.f, 0.f};
+                    if constexpr (KS == 32) {
+                        d = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[kb], bh, d, 0, 0, 0);
+                        d = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[kb], bl, d, 0, 0, 0);
+                        d = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[kb], bh, d, 0, 0, 0);
+                    } else {
+                        d = __builtin_amdgcn_mfma_f32_16x16x16f16(ah[kb], bh, d, 0, 0, 0);
+                        d = __builtin_amdgcn_mfma_f32_16x16x16f16(ah[kb], bl, d, 0, 0, 0);
+                        d = __builtin_amdgcn_mfma_f32_16x16x16f16(al[kb], bh, d, 0, 0, 0);
+                    }
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) acc[j][kb][v] = fmaf(w[kb][v], d[v], acc[j][kb][v]);
+                }
+            }
+        };
+        // en0 is even: ping-pong over pairs of states
+        uint2 ea[kSqR], eb[kSqR];
+        fetch(ea, 0);
+        for (int e0 = 0; e0 < en0; e0 += 2) {
+            fetch(eb, e0 + 1);
+            step(ea, e0);
+            if (e0 + 2 < en0) fetch(ea, e0 + 2);
+            step(eb, e0 + 1);
+        }
+    }
+    __syncthreads();   // every wave is done with its block: zt overlays them
+    if (active) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int line = wl0 + 16 * j + li;
+            if (line < le)
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) zt[(line - lb) * kZS + 16 * kb + 4 * lg + v] = acc[j][kb][v];
+        }
+    }
+}
+
+template <int MODE>
+__device__ void split_body(const StreamArgs &a, const float *__restrict__ q, float *__restrict__ part)
+{
+    constexpr bool PAIRS = MODE != kDenseF32;
     extern __shared__ float sh[];
     __shared__ int ctxs[kCtx];
     // decode (modality, outcome, role, tile): the two roles of a modality share
@@ -364,12 +529,22 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
     const int G = tk.G;
     const int gs = tile * G, ng = min(G, g.ln0 - gs);
     const int lb = gs * g.ln1, le = (gs + ng) * g.ln1;
-    const float *X = reinterpret_cast<const float *>(a.base + md.la32_off) + (int64_t)o * md.slice;
-    const char *P = PAIRS ? a.base + md.lp16_off + 4 * (int64_t)o * md.slice : nullptr;
+    const float *X = MODE == kDenseF32 ? reinterpret_cast<const float *>(a.base + md.la32_off) + (int64_t)o * md.slice
+                                       : nullptr;
+    const char *P = MODE == kDensePairs ? a.base + md.lp16_off + 4 * (int64_t)o * md.slice : nullptr;
+    // sparse pairs: this outcome's run pointers and the side's entries
+    const uint32_t *sqp = nullptr;
+    const uint2 *sqe = nullptr;
+    if (MODE == kSparsePairs) {
+        const int64_t runs = (int64_t)((g.lines + kSqBlock - 1) / kSqBlock) * g.en0;
+        sqp = reinterpret_cast<const uint32_t *>(a.base + md.sq_ptr_off[role]) + (int64_t)o * (runs + 1);
+        sqe = reinterpret_cast<const uint2 *>(a.base + md.sq_ent_off[role]);
+    }
     float *qe0 = sh;                      // [kCtx][32]: marginals of the entry side's first factor
                                           // (pairs: [32][kCtx], times 2^-15)
     float *qe1 = qe0 + kCtx * 32;         // [kCtx][32]: second factor
-    float *zt = qe1 + kCtx * kMaxT * 4;   // [tile lines][kZS]
+    float *zt = qe1 + kCtx * kMaxT * 4;   // [tile lines][kZS] (sparse pairs: over the B blocks)
+    char *blocks = reinterpret_cast<char *>(zt);
     const int tid = threadIdx.x;
     const int off_e0 = a.facs[g.ef0].q_off, off_e1 = a.facs[g.ef1].q_off;
     const int off_l0 = a.facs[g.lf0].q_off, off_l1 = a.facs[g.lf1].q_off;
@@ -377,6 +552,9 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
     for (int c0 = 0; c0 < J; c0 += kCtx) {
         const int jc = min(kCtx, J - c0);
         if (tid < kCtx) ctxs[tid] = tid < jc ? a.bctx[(int64_t)m * a.nctx + b0 + c0 + tid] : -1;
+        if (MODE == kSparsePairs)   // zero B blocks (the line tile of the last pass overlays them)
+            for (int i = tid; i < kWaves * kSqBlockBytes / 16; i += kThreads)
+                reinterpret_cast<u4 *>(blocks)[i] = u4{0u, 0u, 0u, 0u};
         __syncthreads();
         for (int i = tid; i < kCtx * 64; i += kThreads) {
             const int c = i >> 6, s = i & 63;
@@ -398,10 +576,11 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
         const int nt = g.en1 >> 2;
         // dispatch on (role, context blocks, k-steps per state); eligibility
         // admits second factors of 16 or 32 states
-#define BI_SPLIT_TILE(R, K, T)                                                                \
-    do {                                                                                      \
-        if constexpr (PAIRS) split16_tile<K, R, 4 * T>(a, g, P, md.Cp, lb, le, qe0, qe1, zt);  \
-        else split_tile<K, R, T>(a, g, X, md.Cp, lb, le, qe0, qe1, zt);                        \
+#define BI_SPLIT_TILE(R, K, T)                                                                     \
+    do {                                                                                           \
+        if constexpr (MODE == kSparsePairs) sq_tile<K, 4 * T>(g, sqp, sqe, lb, le, qe0, qe1, blocks, zt); \
+        else if constexpr (MODE == kDensePairs) split16_tile<K, R, 4 * T>(a, g, P, md.Cp, lb, le, qe0, qe1, zt); \
+        else split_tile<K, R, T>(a, g, X, md.Cp, lb, le, qe0, qe1, zt);                            \
     } while (0)
 #define BI_SPLIT_NT(R, K) \
     if (nt == 8) BI_SPLIT_TILE(R, K, 8); \
@@ -410,7 +589,7 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
     if (nkb == 1) { BI_SPLIT_NT(R, 1); } \
     else if (nkb == 2) { BI_SPLIT_NT(R, 2); } \
     else { BI_SPLIT_NT(R, 3); }
-        if (role == 0) {
+        if (MODE == kSparsePairs || role == 0) {   // the sparse tile reads both sides the same way
             BI_SPLIT_KB(0)
         } else {
             BI_SPLIT_KB(1)
@@ -438,14 +617,29 @@ __global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, co
     }
 }
 
-size_t lds_bytes(const bi_model *m)
+template <bool PAIRS>
+__global__ __launch_bounds__(kThreads, 2) void split_lik_kernel(StreamArgs a, const float *__restrict__ q,
+                                                             float *__restrict__ part)
+{
+    split_body<PAIRS ? kDensePairs : kDenseF32>(a, q, part);
+}
+
+__global__ __launch_bounds__(kThreads, 2) void sparse16_lik_kernel(StreamArgs a, const float *__restrict__ q,
+                                                                float *__restrict__ part)
+{
+    split_body<kSparsePairs>(a, q, part);
+}
+
+size_t lds_bytes(const bi_model *m, bool sparse)
 {
     size_t most = 0;
     for (const ModDesc &md : m->mods)
         for (int role = 0; role < 2; ++role) {
             const Geo g = geo_of(md, role);
             const size_t lines = (size_t)std::min(split_groups(g), g.ln0) * g.ln1;
-            most = std::max(most, sizeof(float) * ((size_t)kCtx * 64 + lines * kZS));
+            size_t tail = sizeof(float) * lines * kZS;
+            if (sparse) tail = std::max(tail, (size_t)kWaves * kSqBlockBytes);
+            most = std::max(most, sizeof(float) * (size_t)kCtx * 64 + tail);
         }
     return most;
 }
@@ -469,7 +663,25 @@ bool split_eligible(const bi_model *m)
         }
         if (md.K > kStreamMaxK) return false;
     }
-    return lds_bytes(m) <= 64 * 1024 && pstride < (int64_t)1 << 30;
+    return lds_bytes(m, false) <= 64 * 1024 && pstride < (int64_t)1 << 30;
+}
+
+bool sq_eligible(const bi_model *m)
+{
+    if (m->M > kStreamMaxM || m->mods.empty()) return false;
+    int64_t pstride = 0;
+    for (const ModDesc &md : m->mods) {
+        // the layout exists only for the shapes it serves (sq_shape)
+        if (md.sq_ptr_off[0] < 0 || md.sq_ptr_off[1] < 0 || md.K > kStreamMaxK) return false;
+        for (int role = 0; role < 2; ++role) {
+            const Geo g = geo_of(md, role);
+            const int G = split_groups(g);
+            // tiles of whole 64-line blocks of the layout
+            if (G * g.ln1 % kSqBlock != 0 && G < g.ln0) return false;
+            pstride += g.ln0 + (int64_t)((g.ln0 + G - 1) / G) * g.ln1;
+        }
+    }
+    return lds_bytes(m, true) <= 64 * 1024 && pstride < (int64_t)1 << 30;
 }
 
 int64_t split_plan(const bi_model *m, StreamArgs *a)
@@ -509,7 +721,7 @@ int64_t split_plan(const bi_model *m, StreamArgs *a)
     return so;
 }
 
-size_t split_lds_bytes(const bi_model *m) { return lds_bytes(m); }
+size_t split_lds_bytes(const bi_model *m, bool sparse) { return lds_bytes(m, sparse); }
 
 bool split_pairs(const bi_model *m)
 {
@@ -518,13 +730,17 @@ bool split_pairs(const bi_model *m)
     return !m->mods.empty();
 }
 
-void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream)
+void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream,
+                      bool sparse)
 {
     const unsigned grid = (unsigned)((a.nwg + kXcds - 1) / kXcds * kXcds);
-    if (split_pairs(m))
-        hipLaunchKernelGGL(split_lik_kernel<true>, dim3(grid), dim3(kThreads), lds_bytes(m), stream, a, q, part);
+    const size_t lds = lds_bytes(m, sparse);
+    if (sparse)
+        hipLaunchKernelGGL(sparse16_lik_kernel, dim3(grid), dim3(kThreads), lds, stream, a, q, part);
+    else if (split_pairs(m))
+        hipLaunchKernelGGL(split_lik_kernel<true>, dim3(grid), dim3(kThreads), lds, stream, a, q, part);
     else
-        hipLaunchKernelGGL(split_lik_kernel<false>, dim3(grid), dim3(kThreads), lds_bytes(m), stream, a, q, part);
+        hipLaunchKernelGGL(split_lik_kernel<false>, dim3(grid), dim3(kThreads), lds, stream, a, q, part);
 }
 
 }  // namespace bi

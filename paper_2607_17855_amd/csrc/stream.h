@@ -84,10 +84,16 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
 // values of partial messages per context) and one launch.
 bool split_eligible(const bi_model *m);
 int64_t split_plan(const bi_model *m, StreamArgs *a);
-size_t split_lds_bytes(const bi_model *m);
+size_t split_lds_bytes(const bi_model *m, bool sparse);
 // every modality has its fp16-pair copy (BI_F16_PAIRS): the fp16 matrix-core tiles run
 bool split_pairs(const bi_model *m);
-void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream);
+// every modality has the sparse fp16-pair layout (BI_SPARSE_A with
+// BI_F16_PAIRS): the sparse path runs the same tiles from the nonzeros
+// (same plan and partial layout as the dense kernel)
+bool sq_eligible(const bi_model *m);
+// sparse: the sparse fp16-pair kernel, else the dense one of the model's copy
+void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream,
+                      bool sparse);
 
 // Sparse likelihood kernel (sparse.hip): task planning and one launch.
 // sparse_plan fills a->task / a->ntask / a->nwg and the message sources,

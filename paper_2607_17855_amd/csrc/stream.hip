@@ -585,8 +585,19 @@ static int64_t dense_plan(const bi_model *m, StreamArgs *a)
     return poff;
 }
 
+// The likelihood kernel a streaming call runs: general dense, dense
+// matrix-core tiles, sparse fp64 gathers, sparse fp16-pair matrix-core tiles.
+enum class Lik { Dense, Split, Sparse, Sparse16 };
+
+static Lik lik_kind(const bi_model *m, bool sparse)
+{
+    if (sparse) return sq_eligible(m) ? Lik::Sparse16 : Lik::Sparse;
+    return split_eligible(m) ? Lik::Split : Lik::Dense;
+}
+
 // Plan of the workspace: bucket starts / fill counters / sorted contexts /
-// partial messages / two marginal buffers (fp32 dense, fp64 sparse).
+// partial messages / two marginal buffers (fp32, or fp64 for the sparse fp64
+// kernel).
 static void plan_ws(const bi_model *m, int b, int T, bool sparse, StreamArgs *a, int64_t *offs, int64_t *total)
 {
     const int nctx = b * T;
@@ -599,8 +610,11 @@ static void plan_ws(const bi_model *m, int b, int T, bool sparse, StreamArgs *a,
         sm.fofs = fofs;
         fofs += sm.K;
     }
-    a->pstride = sparse ? sparse_plan(m, a) : split_eligible(m) ? split_plan(m, a) : dense_plan(m, a);
-    const int64_t es = sparse ? 8 : 4;
+    const Lik lik = lik_kind(m, sparse);
+    a->pstride = lik == Lik::Sparse ? sparse_plan(m, a)
+                 : lik == Lik::Dense ? dense_plan(m, a)
+                                     : split_plan(m, a);
+    const int64_t es = lik == Lik::Sparse ? 8 : 4;
     int64_t off = 0;
     offs[0] = off;  off = align_up(off + 4 * (int64_t)bofs, kAlign);
     offs[1] = off;  off = align_up(off + 4 * (int64_t)fofs, kAlign);
@@ -621,19 +635,23 @@ size_t stream_workspace(const bi_model *m, int b, int T, bool sparse)
 
 template <typename QT>
 static void run_iterations(const bi_model *m, int algo, int iters, const StreamArgs &a, char *part, QT *qa, QT *qb,
-                           float *q, size_t lik_lds, size_t upd_lds, hipStream_t stream, bool sparse)
+                           float *q, size_t lik_lds, size_t upd_lds, hipStream_t stream, Lik lik)
 {
-    const bool split = !sparse && split_eligible(m);
     QT *cur = qa, *nxt = qb;
     using PT = QT;
+    const char *name = lik == Lik::Sparse     ? "lik_sparse"
+                       : lik == Lik::Sparse16 ? "lik_sparse16"
+                       : lik == Lik::Split    ? (split_pairs(m) ? "lik_split16" : "lik_split")
+                                              : "lik";
     for (int k = 0; k < iters; ++k) {
         {
-            ProfScope p(sparse ? "lik_sparse" : split ? (split_pairs(m) ? "lik_split16" : "lik_split") : "lik", stream);
-            if (sparse)
+            ProfScope p(name, stream);
+            if (lik == Lik::Sparse)
                 sparse_lik_launch(m, a, reinterpret_cast<const double *>(cur), reinterpret_cast<double *>(part),
                                   stream);
-            else if (split)
-                split_lik_launch(m, a, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream);
+            else if (lik != Lik::Dense)
+                split_lik_launch(m, a, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream,
+                                 lik == Lik::Sparse16);
             else
                 hipLaunchKernelGGL(lik_kernel, dim3(a.nwg), dim3(kThreads), lik_lds, stream, a,
                                    reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part));
@@ -675,11 +693,12 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
     char *part = w + offs[3];
     const size_t upd_lds = sizeof(double) * m->ntot;
+    const Lik lik = lik_kind(m, sparse);
     size_t lik_lds = 0;
-    if (sparse) {
+    if (lik == Lik::Sparse) {
         lik_lds = sparse_lds_bytes(m);
-    } else if (split_eligible(m)) {
-        lik_lds = split_lds_bytes(m);
+    } else if (lik != Lik::Dense) {
+        lik_lds = split_lds_bytes(m, lik == Lik::Sparse16);
     } else {
         int ncs_max = 1;
         for (const ModDesc &md : m->mods)
@@ -688,10 +707,10 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     }
     if (lik_lds > 160 * 1024 || upd_lds > 64 * 1024)
         return fail(BI_ERR_UNSUPPORTED, "streaming working set exceeds LDS");
-    if (sparse) {
+    if (lik == Lik::Sparse) {
         const int rc = sparse_prepare(m);
         if (rc != BI_OK) return rc;
-    } else if (!split_eligible(m)) {
+    } else if (lik == Lik::Dense) {
         const hipError_t e = hipFuncSetAttribute((const void *)lik_kernel,
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lik_lds);
         if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
@@ -703,14 +722,14 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
         hipLaunchKernelGGL(bucket_kernel, dim3(m->M), dim3(1024), sizeof(int) * (2 * kmax + 1), stream, a);
     }
     const int init_grid = (int)std::min<int64_t>(1024, ((int64_t)a.nctx * a.ntot + 255) / 256);
-    if (sparse) {
+    if (lik == Lik::Sparse) {
         double *qa = reinterpret_cast<double *>(w + offs[4]);
         double *qb = reinterpret_cast<double *>(w + offs[5]);
         {
             ProfScope p("init", stream);
             hipLaunchKernelGGL(init_q_kernel<double>, dim3(init_grid), dim3(256), 0, stream, a, qa);
         }
-        run_iterations<double>(m, algo, iters, a, part, qa, qb, q, lik_lds, upd_lds, stream, true);
+        run_iterations<double>(m, algo, iters, a, part, qa, qb, q, lik_lds, upd_lds, stream, lik);
     } else {
         float *qa = reinterpret_cast<float *>(w + offs[4]);
         float *qb = reinterpret_cast<float *>(w + offs[5]);
@@ -718,7 +737,7 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
             ProfScope p("init", stream);
             hipLaunchKernelGGL(init_q_kernel<float>, dim3(init_grid), dim3(256), 0, stream, a, qa);
         }
-        run_iterations<float>(m, algo, iters, a, part, qa, qb, q, lik_lds, upd_lds, stream, false);
+        run_iterations<float>(m, algo, iters, a, part, qa, qb, q, lik_lds, upd_lds, stream, lik);
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(BI_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));

@@ -40,10 +40,11 @@ class ModDesc(ctypes.Structure):
                 ("cn", ctypes.c_int32 * 2), ("zv_off", ctypes.c_int32), ("dsum", ctypes.c_int32),
                 ("la32_off", ctypes.c_int64), ("csr_ptr_off", ctypes.c_int64), ("csr_ent_off", ctypes.c_int64),
                 ("csc_ptr_off", ctypes.c_int64), ("csc_ent_off", ctypes.c_int64), ("nnz", ctypes.c_int64),
-                ("lp16_off", ctypes.c_int64)]
+                ("lp16_off", ctypes.c_int64), ("sq_ptr_off", ctypes.c_int64 * 2), ("sq_ent_off", ctypes.c_int64 * 2)]
 
 
 SpEntry = np.dtype([("v", np.float64), ("a", np.uint32), ("b", np.uint32)])
+SqEntry = np.dtype([("pair", np.uint32), ("pos", np.uint32)])
 
 
 class FacDesc(ctypes.Structure):
@@ -131,10 +132,10 @@ def test_plan_rejects_bad_descriptors():
     assert _desc_err([3], [1], [2], [[0]], mb=0) == bi.BI_ERR_INVALID_ARG
     assert _desc_err([3], [1], [2], [[0]], flags=3) == bi.BI_ERR_INVALID_ARG
     assert _desc_err([3], [1], [2], [[0]], flags=64) == bi.BI_ERR_INVALID_ARG
-    # fp16 pairs only with BI_FAST_F32 and the dense layout
+    # fp16 pairs only with BI_FAST_F32 (either layout)
     assert _desc_err([3], [1], [2], [[0]], flags=bi.BI_F16_PAIRS) == bi.BI_ERR_INVALID_ARG
-    assert _desc_err([3], [1], [2], [[0]], flags=bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS) == \
-        bi.BI_ERR_INVALID_ARG
+    assert _desc_err([3], [1], [2], [[0]], flags=bi.BI_SPARSE_A | bi.BI_F16_PAIRS) == bi.BI_ERR_INVALID_ARG
+    assert bi.bi_plan_model([3], [1], [2], [[0]], 1, bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS) > 0
     lib = bi.load()
     out = ctypes.c_size_t(0)
     assert lib.bi_plan_model(None, ctypes.byref(out)) == bi.BI_ERR_INVALID_ARG
@@ -146,7 +147,8 @@ def test_plan_sizes_cover_every_array():
     m = w.model
     nbytes = bi.bi_plan_model(m.n, m.U, m.K, m.deps, m.mb)
     need = sum(8 * a.size for a in m.A) + sum(12 * b.size + 8 * d.size for b, d in zip(m.B, m.D))
-    assert need <= nbytes <= need + 256 * (2 + 2 * m.M + 3 * m.F) + 8 * 4 * 64 * m.M
+    tables = ctypes.sizeof(ModDesc) * m.M + ctypes.sizeof(FacDesc) * m.F
+    assert need <= nbytes <= need + tables + 256 * (2 + 2 * m.M + 3 * m.F) + 8 * 4 * 64 * m.M
 
 
 def test_inference_validates_on_host_before_launch():
@@ -281,6 +283,100 @@ def test_host_pack_sparse_planes(seed):
                                 assert b < rn1 and got[o, r, l] == 0
                                 got[o, r, l] = e["v"]
                 np.testing.assert_allclose(got, want, rtol=0, atol=1e-13)
+    finally:
+        bi.bi_free_model(h)
+
+
+SQ_SHAPES = [
+    # (n, K): every modality depends on all four factors (rows = the first two)
+    ([4, 16, 6, 32], [3]),
+    ([2, 32, 2, 16], [2]),
+    ([6, 16, 4, 16], [2]),
+    ([32, 32, 2, 32], [1]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SQ_SHAPES)))
+def test_host_pack_sparse_pair_layout(case):
+    """BI_SPARSE_A with BI_F16_PAIRS: per side, the nonzeros of every outcome
+    in blocks of 64 lines, inside a block by (e0, line, e1), each entry the
+    binary16 rounding of LN(A) - ln(eps) and of its residual (numpy's float64
+    -> float16 conversion is the reference) with its position in the block,
+    and the run pointers delimiting every (block, e0).  Rebuilt into dense
+    slices they give back exactly the pair rounding of the nonzeros."""
+    n, K = SQ_SHAPES[case]
+    rng = np.random.Generator(np.random.PCG64(1300 + case))
+    model = synth.make_model(rng, n, [1] * 4, K, [[0, 1, 2, 3]] * len(K), 1, 1.0, 1.0,
+                             sparsity=0.3 + 0.2 * case, uniform_D=False)
+    flags = bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
+    assert bi.bi_plan_model_exact(model.n, model.U, model.K, model.deps, 1, model.A, flags) <= \
+        bi.bi_plan_model(model.n, model.U, model.K, model.deps, 1, flags)
+    h, img = bi.bi_pack_model_host(model.n, model.U, model.K, model.deps, 1, model.A, model.B, model.D, flags)
+    try:
+        mods, _ = _descs(img, model.M, model.F)
+        lne = np.log(1e-16)
+        for mi in range(model.M):
+            md = mods[mi]
+            assert md.lp16_off == -1          # no dense pair copy with the sparse layout
+            A = model.A[mi][0].astype(np.float64).reshape(md.K, md.R, md.C)
+            nz = A > 1e-16
+            v = np.where(nz, np.log(np.maximum(A, 1e-16)) - lne, 0.0)
+            hi = v.astype(np.float16)
+            lo = (v - hi.astype(np.float64)).astype(np.float16)
+            for side in range(2):
+                lines = md.R if side == 0 else md.C
+                e0n = md.cn[0] if side == 0 else md.rn[0]
+                e1n = md.cn[1] if side == 0 else md.rn[1]
+                nblk = -(-lines // 64)
+                runs = nblk * e0n
+                assert md.sq_ptr_off[side] % 256 == 0 and md.sq_ent_off[side] % 256 == 0
+                ptr = img[md.sq_ptr_off[side]:md.sq_ptr_off[side] + 4 * md.K * (runs + 1)]
+                ptr = ptr.view(np.uint32).reshape(md.K, runs + 1).astype(np.int64)
+                ent = img[md.sq_ent_off[side]:md.sq_ent_off[side] + 8 * md.nnz].view(SqEntry)
+                assert ptr[0, 0] == 0 and ptr[-1, -1] == md.nnz
+                assert np.all(np.diff(ptr, axis=1) >= 0) and np.all(ptr[1:, 0] == ptr[:-1, -1])
+                # the slices seen from this side: [o][line][e0][e1]
+                vh = hi if side == 0 else hi.transpose(0, 2, 1)
+                vl = lo if side == 0 else lo.transpose(0, 2, 1)
+                vz = nz if side == 0 else nz.transpose(0, 2, 1)
+                got_h = np.zeros((md.K, lines, e0n * e1n), dtype=np.uint16)
+                got_l = np.zeros_like(got_h)
+                seen = np.zeros((md.K, lines, e0n * e1n), dtype=bool)
+                for o in range(md.K):
+                    for blk in range(nblk):
+                        for e0 in range(e0n):
+                            run = ent[ptr[o, blk * e0n + e0]:ptr[o, blk * e0n + e0 + 1]]
+                            line = (run["pos"] >> 8).astype(np.int64)
+                            e1 = (run["pos"] & 255).astype(np.int64)
+                            assert np.all(line < 64) and np.all(blk * 64 + line < lines) and np.all(e1 < e1n)
+                            key = line * e1n + e1
+                            assert np.all(np.diff(key) > 0)       # ordered by (line, e1), no repeats
+                            L, E = blk * 64 + line, e0 * e1n + e1
+                            assert not seen[o, L, E].any()
+                            seen[o, L, E] = True
+                            got_h[o, L, E] = run["pair"] & 0xFFFF
+                            got_l[o, L, E] = run["pair"] >> 16
+                np.testing.assert_array_equal(seen, vz)
+                np.testing.assert_array_equal(got_h[seen], vh[vz].view(np.uint16))
+                np.testing.assert_array_equal(got_l[seen], vl[vz].view(np.uint16))
+    finally:
+        bi.bi_free_model(h)
+
+
+def test_sparse_pair_layout_only_for_its_shapes():
+    """Modalities outside the shapes of the matrix-core tiles get no sparse
+    pair arrays (their model keeps the sparse fp64 kernels); per-agent models
+    cannot be packed sparse at all."""
+    rng = np.random.Generator(np.random.PCG64(1310))
+    model = synth.make_model(rng, [4, 16, 6, 12], [1] * 4, [2, 3], [[0, 1, 2, 3], [0, 1]], 1, 1.0, 1.0,
+                             sparsity=0.5, uniform_D=False)
+    flags = bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
+    h, img = bi.bi_pack_model_host(model.n, model.U, model.K, model.deps, 1, model.A, model.B, model.D, flags)
+    try:
+        mods, _ = _descs(img, model.M, model.F)
+        assert all(mods[i].sq_ptr_off[s] == -1 and mods[i].sq_ent_off[s] == -1 for i in range(2) for s in range(2))
+        assert all(mods[i].csr_ptr_off >= 0 for i in range(2))
+        assert bi.bi_query_path(h, 8, 4, bi.BI_ALGO_VMP) in (bi.BI_PATH_AGENT, bi.BI_PATH_STREAM, bi.BI_PATH_SPARSE)
     finally:
         bi.bi_free_model(h)
 

@@ -35,6 +35,8 @@ CASES = [
      bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS, ("vmp", "mmp"), "stream"),
     (lambda: _shared(1202, [9, 7, 5], [2, 1, 3], [3, 2, 4], [[0, 1, 2], [1], [0, 2]], 24, 5, sparsity=0.6),
      bi.BI_SPARSE_A, ("vmp", "mmp"), "sparse"),
+    (lambda: _shared(1203, [4, 32, 6, 16], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], 30, 4, sparsity=0.8),
+     bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS, ("vmp", "mmp"), "sparse"),
 ]
 
 

@@ -1,5 +1,7 @@
 """Sparse path (BI_SPARSE_A, shared model: fp64 gathers over the nonzero
-entries) against the oracle, the agent-resident path and the dense layout."""
+entries; with BI_FAST_F32 | BI_F16_PAIRS, fp16-pair matrix-core tiles fed
+from the nonzeros) against the oracle, the agent-resident path and the dense
+layout."""
 import functools
 import os
 
@@ -106,5 +108,83 @@ def test_large_shared_sparse(algo):
     ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=LARGE_AGENTS)
     err = float(np.abs(q[LARGE_AGENTS] - ref).max())
     print(f"[gpu]   large shared model {algo} sparse vs oracle (agents {LARGE_AGENTS}): {err:.3e}", flush=True)
+    assert err <= TOL
+    pm.close()
+
+
+# shapes of the sparse fp16-pair tiles (two factors per side, second factors
+# of 16 or 32 states, even first factors): 96 lines (a partial 64-line block),
+# 1024 lines (four tiles), 16 and 32 entry states, a bucket of more than 48
+# contexts (two context passes), dense A (runs longer than the 256 entries a
+# wave holds in flight) and very sparse A (empty runs)
+SQ_CASES = [
+    # (n, U, K, deps, b, T, sparsity)
+    ([6, 16, 4, 32], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], 24, 5, 0.9),
+    ([2, 32, 10, 16], [1, 2, 1, 2], [4, 2], [[0, 1, 2, 3], [0, 1, 2, 3]], 40, 4, 0.5),
+    ([4, 32, 32, 16], [2, 2, 1, 1], [2], [[0, 1, 2, 3]], 60, 2, 0.0),
+    ([32, 32, 2, 32], [1, 1, 2, 2], [3], [[0, 1, 2, 3]], 30, 3, 0.97),
+    ([2, 16, 2, 16], [2, 2, 2, 2], [2, 3], [[0, 1, 2, 3], [0, 1, 2, 3]], 50, 3, 0.7),
+]
+SQ_FLAGS = bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
+# (case, iterations).  The fp16-pair precision class is for models whose
+# marginals are insensitive to rounding of the log-likelihoods; cases 1 and 4
+# are not beyond one sweep: a perturbation of log A at the pair error scale
+# ((ln A - ln eps) 2^-20) moves the fp64 oracle's marginals by 3-5e-6 after
+# two sweeps and 1e-5-4e-4 after three, and even the fp32 dense path is 4e-5
+# off after three.  The others stay below 2e-6 through three sweeps.
+SQ_RUNS = [(c, 1) for c in range(len(SQ_CASES))] + [(0, 2), (2, 3), (3, 3)]
+
+
+@pytest.mark.parametrize("case,iters", SQ_RUNS)
+def test_sparse_pairs_vs_oracle_agent_and_dense_pairs(case, iters, force_sparse):
+    n, U, K, deps, b, T, sp = SQ_CASES[case]
+    w = _shared_model(1400 + case, n, U, K, deps, b, T, sp, iters=iters)
+    for algo in ("vmp", "mmp"):
+        print(f"[gpu] sparse pairs case {case} iters {iters} {algo}", flush=True)
+        bi.bi_profile_begin()
+        q, pm = run_gpu(w, algo, flags=SQ_FLAGS)
+        names = set(bi.bi_profile_end())
+        assert pm.path(w.b, w.T, algo) == "sparse"
+        assert "lik_sparse16" in names, names
+        check_invariants(w, q)
+        ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters)
+        err = float(np.abs(q - ref).max())
+        print(f"[gpu]   sparse pairs vs oracle {err:.3e}", flush=True)
+        assert err <= TOL
+        q2, _ = run_gpu(w, algo, pm=pm)
+        assert np.array_equal(q, q2), "sparse pair path is not reproducible"
+        old = os.environ.get("BI_FORCE_PATH")
+        os.environ["BI_FORCE_PATH"] = "agent"
+        try:
+            qa, _ = run_gpu(w, algo, pm=pm)
+        finally:
+            os.environ["BI_FORCE_PATH"] = old
+        assert float(np.abs(q - qa).max()) <= TOL
+        pm.close()
+        # the dense fp16-pair tiles on the same model
+        os.environ["BI_FORCE_PATH"] = "stream"
+        try:
+            qd, pmd = run_gpu(w, algo, flags=bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS)
+        finally:
+            os.environ["BI_FORCE_PATH"] = old
+        pmd.close()
+        assert float(np.abs(q - qd).max()) <= TOL
+
+
+@pytest.mark.parametrize("algo", ["vmp", "mmp"])
+def test_large_shared_sparse_pairs(algo):
+    w = large_shared()
+    print(f"[gpu] large shared model {algo} sparse pairs", flush=True)
+    bi.bi_profile_begin()
+    q, pm = run_gpu(w, algo, flags=SQ_FLAGS)
+    names = set(bi.bi_profile_end())
+    assert pm.path(w.b, w.T, algo) == "sparse", "the selector must send the large model to the sparse kernels"
+    assert "lik_sparse16" in names, names
+    check_invariants(w, q)
+    q2, _ = run_gpu(w, algo, pm=pm)
+    assert np.array_equal(q, q2), "sparse pair path is not reproducible"
+    ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=LARGE_AGENTS)
+    err = float(np.abs(q[LARGE_AGENTS] - ref).max())
+    print(f"[gpu]   large shared model {algo} sparse pairs vs oracle (agents {LARGE_AGENTS}): {err:.3e}", flush=True)
     assert err <= TOL
     pm.close()

@@ -20,7 +20,10 @@
 // (side 0: lines = rows, entries = columns; side 1 the transpose), as
 // SqEntry {uint32 pair; uint32 pos}: pair = the binary16 high part of the
 // value (low half) and the binary16 rounding of its residual (high half),
-// pos = (line - first line of its block) << 8 | e1.  The lines of an outcome
+// pos = the byte offset of the entry's high part in the matrix-core kernel's
+// LDS block of its 64 lines, sq_pos(line - first line of its block, e1, en1)
+// below (a 16-byte pad, then per line en1 high parts and a 16-byte pad; the
+// residuals sit in a second plane of the same shape).  The lines of an outcome
 // are cut into blocks of 64; inside an outcome the entries run block by
 // block, and inside a block by the state e0 of the entry side's first
 // factor, then by line, then by e1 (the entry side's second factor).  The
@@ -89,6 +92,15 @@ struct ModDesc {
 };
 
 constexpr int kSqBlock = 64;   // lines per block of the sparse fp16-pair layout
+constexpr int kSqPad = 16;     // bytes of padding before a block and after every line
+
+// Bytes per line of one plane of a block (en1 binary16 values and the pad),
+// and the byte offset of (line, e1) in the plane.  Offset 0 (the leading pad)
+// stands for an empty slot: the kernel's writes for it land in pads that no
+// operand read covers.
+constexpr int sq_line_bytes(int en1) { return 2 * en1 + kSqPad; }
+constexpr int sq_plane_bytes(int en1) { return kSqPad + kSqBlock * sq_line_bytes(en1); }
+constexpr uint32_t sq_pos(int line, int e1, int en1) { return (uint32_t)(kSqPad + line * sq_line_bytes(en1) + 2 * e1); }
 
 // Whether a modality has the shape of the sparse fp16-pair layout (and of the
 // matrix-core kernels): two factors on each side, second factors of 16 or 32
@@ -130,7 +142,7 @@ struct SpEntry {
 
 struct SqEntry {
     uint32_t pair;  // binary16 high part | binary16 residual << 16 of log(max(A, 1e-16)) - log(1e-16)
-    uint32_t pos;   // (line - block start) << 8 | e1
+    uint32_t pos;   // sq_pos(line - block start, e1, en1)
 };
 
 inline int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }

@@ -432,7 +432,7 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
                             double hi;
                             const uint16_t h = half_rne(v, &hi), r = half_rne(v - hi, nullptr);
                             ent[e++] = SqEntry{(uint32_t)h | (uint32_t)r << 16,
-                                               (uint32_t)(l - blk * kSqBlock) << 8 | (uint32_t)e1};
+                                               sq_pos((int)(l - blk * kSqBlock), e1, e1n)};
                         }
                 }
             ptr[runs] = (uint32_t)e;

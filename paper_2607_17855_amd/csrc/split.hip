@@ -68,14 +68,14 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 constexpr float kPairScale = 32768.0f;   // 2^15: q_e1 in [0, 1] scaled below the fp16 maximum
 
-// Sparse pairs: bytes per line of a wave's B block in LDS (KS high parts, KS
-// residuals, 16 bytes of padding, so the 16 lines of one operand load start
-// on different banks), and entries in flight per lane for one state e0.
-template <int KS>
-constexpr int sq_row() { return 4 * KS + 16; }
-constexpr int kSqBlockBytes = kWaveLines * sq_row<32>();   // one wave's block, sized for KS = 32
+// Sparse pairs: a wave's B block in LDS is two planes (high parts, then
+// residuals) of the shape layout.h fixes (16-byte pad, then per line KS
+// values and a 16-byte pad, so the 16 lines of one operand load start on
+// different banks); sized for KS = 32.  Entries in flight per lane for one
+// state e0: kSqR.
+constexpr int kSqWaveBytes = 2 * sq_plane_bytes(32);
 constexpr int kSqR = 4;
-constexpr uint32_t kSqNone = 0xffffffffu;   // pos of an empty slot
+constexpr uint32_t kBufWord3 = 0x00020000u;   // buffer resource config word of the gfx9 family: raw dwords
 
 // kernel variants: dense fp32 slices, dense fp16 pairs, sparse fp16 pairs
 enum { kDenseF32 = 0, kDensePairs = 1, kSparsePairs = 2 };
@@ -353,24 +353,27 @@ __device__ void split16_tile(const StreamArgs &a, const Geo &g, const char *__re
 
 // The sparse fp16-pair tile.  A wave owns the 64 lines of one block of the
 // sparse layout; for each state e0 the block's run of nonzeros is scattered
-// into the wave's zeroed B block (line-major, KS high parts then KS
-// residuals per line), the B operands of the four 16-line tiles are read
-// back, the run's places are zeroed again and the product chains run as in
-// split16_tile.  Only this wave touches its block, and LDS operations of one
-// wave take effect in program order, so the block needs no barrier; the
-// scheduling barriers keep the compiler from moving LDS operations across
-// the phases.  The entries of state e0 + 1 are loaded while state e0 is used.
-// Ends with a workgroup barrier (every wave reaches it) and the line values
-// written to zt, which overlays the blocks.
+// into the wave's zeroed B block, the B operands of the four 16-line tiles
+// are read back, the run's places are zeroed again and the product chains
+// run as in split16_tile.  Entries arrive by bounds-checked buffer loads
+// (a slot past the run reads 0: pair 0 at offset 0, the block's leading
+// pad), and each carries its byte offset in the block, so a slot costs one
+// address add and two 16-bit stores.  Only this wave touches its block, and
+// LDS operations of one wave take effect in program order, so the block
+// needs no barrier; the scheduling barriers keep the compiler from moving
+// LDS operations across the phases.  The entries of state e0 + 1 are loaded
+// while state e0 is used.  Ends with a workgroup barrier (every wave reaches
+// it) and the line values written to zt, which overlays the blocks.
 template <int NKB, int KS>
-__device__ void sq_tile(const Geo &g, const uint32_t *__restrict__ ptr, const uint2 *__restrict__ ent, int lb,
+__device__ void sq_tile(const Geo &g, const uint32_t *__restrict__ ptr, const SqEntry *__restrict__ ent, int lb,
                         int le, const float *qe0t, const float *qe1, char *blocks, float *zt)
 {
     constexpr int KW = KS / 4;   // k values per lane
     constexpr int DW = KW / 2;   // dwords per operand
-    constexpr int S = sq_row<KS>();
+    constexpr int SH = sq_line_bytes(KS), PL = sq_plane_bytes(KS);
     using HV = std::conditional_t<KS == 32, h8, h4>;
     using UV = std::conditional_t<KS == 32, u4, u2>;
+    typedef uint32_t w2 __attribute__((ext_vector_type(2)));
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wl0 = lb + kWaveLines * wave;
     const bool active = wl0 < le;
@@ -402,48 +405,42 @@ __device__ void sq_tile(const Geo &g, const uint32_t *__restrict__ ptr, const ui
         // the block's end)
         const uint32_t *bp = ptr + (int64_t)(wl0 / kSqBlock) * en0;
         const int pv = (int)bp[min(lane, en0)];
-        char *bk = blocks + wave * kSqBlockBytes;
-        auto run_of = [&](int e0, uint32_t &rs, uint32_t &re) {
-            rs = (uint32_t)__builtin_amdgcn_readlane(pv, e0);
-            re = (uint32_t)__builtin_amdgcn_readlane(pv, e0 + 1);
+        char *bk = blocks + wave * kSqWaveBytes;
+        // buffer resource over the run of state e0 (its length bounds the loads)
+        auto run_rsrc = [&](int e0, int &n) {
+            const int rs = __builtin_amdgcn_readlane(pv, e0);
+            n = __builtin_amdgcn_readlane(pv, e0 + 1) - rs;
+            return __builtin_amdgcn_make_buffer_rsrc((void *)(ent + rs), (short)0, 8 * n, (int)kBufWord3);
         };
-        auto fetch = [&](uint2 (&E)[kSqR], int e0) {
-            uint32_t rs, re;
-            run_of(e0, rs, re);
+        auto fetch = [&](w2 (&E)[kSqR], int e0) {
+            int n;
+            const auto r = run_rsrc(e0, n);
 #pragma unroll
-            for (int i = 0; i < kSqR; ++i) {
-                const uint32_t idx = rs + lane + 64 * i;
-                E[i] = idx < re ? ent[idx] : make_uint2(0u, kSqNone);
-            }
+            for (int i = 0; i < kSqR; ++i) E[i] = __builtin_amdgcn_raw_buffer_load_b64(r, 8 * (lane + 64 * i), 0, 0);
         };
-        auto put = [&](uint2 x, bool clear) {
-            if (x.y != kSqNone) {
-                char *d = bk + (x.y >> 8) * S + (x.y & 255u) * 2;
-                *reinterpret_cast<uint16_t *>(d) = clear ? (uint16_t)0 : (uint16_t)(x.x & 0xffffu);
-                *reinterpret_cast<uint16_t *>(d + 2 * KS) = clear ? (uint16_t)0 : (uint16_t)(x.x >> 16);
-            }
+        auto put = [&](w2 x, bool clear) {
+            char *d = bk + x[1];
+            *reinterpret_cast<uint16_t *>(d) = clear ? (uint16_t)0 : (uint16_t)(x[0] & 0xffffu);
+            *reinterpret_cast<uint16_t *>(d + PL) = clear ? (uint16_t)0 : (uint16_t)(x[0] >> 16);
         };
         // scatter (or zero again) the run of state e0: the entries in flight,
         // then any beyond 64 kSqR straight from memory
-        auto scatter = [&](const uint2 (&E)[kSqR], int e0, bool clear) {
+        auto scatter = [&](const w2 (&E)[kSqR], int e0, bool clear) {
 #pragma unroll
             for (int i = 0; i < kSqR; ++i) put(E[i], clear);
-            uint32_t rs, re;
-            run_of(e0, rs, re);
-            for (uint32_t b0 = rs + 64 * kSqR; b0 < re; b0 += 64) {
-                const uint32_t idx = b0 + lane;
-                put(idx < re ? ent[idx] : make_uint2(0u, kSqNone), clear);
-            }
+            int n;
+            const auto r = run_rsrc(e0, n);
+            for (int b0 = 64 * kSqR; b0 < n; b0 += 64) put(__builtin_amdgcn_raw_buffer_load_b64(r, 8 * (b0 + lane), 0, 0), clear);
         };
-        auto step = [&](const uint2 (&E)[kSqR], int e0) {
+        auto step = [&](const w2 (&E)[kSqR], int e0) {
             scatter(E, e0, false);
             __builtin_amdgcn_sched_barrier(0);
             UV xh[4], xl[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const char *r = bk + (16 * j + li) * S + 2 * KW * lg;
+                const char *r = bk + kSqPad + (16 * j + li) * SH + 2 * KW * lg;
                 xh[j] = *reinterpret_cast<const UV *>(r);
-                xl[j] = *reinterpret_cast<const UV *>(r + 2 * KS);
+                xl[j] = *reinterpret_cast<const UV *>(r + PL);
             }
             __builtin_amdgcn_sched_barrier(0);
             scatter(E, e0, true);
@@ -473,7 +470,7 @@ __device__ void sq_tile(const Geo &g, const uint32_t *__restrict__ ptr, const ui
             }
         };
         // en0 is even: ping-pong over pairs of states
-        uint2 ea[kSqR], eb[kSqR];
+        w2 ea[kSqR], eb[kSqR];
         fetch(ea, 0);
         for (int e0 = 0; e0 < en0; e0 += 2) {
             fetch(eb, e0 + 1);
@@ -534,11 +531,11 @@ __device__ void split_body(const StreamArgs &a, const float *__restrict__ q, flo
     const char *P = MODE == kDensePairs ? a.base + md.lp16_off + 4 * (int64_t)o * md.slice : nullptr;
     // sparse pairs: this outcome's run pointers and the side's entries
     const uint32_t *sqp = nullptr;
-    const uint2 *sqe = nullptr;
+    const SqEntry *sqe = nullptr;
     if (MODE == kSparsePairs) {
         const int64_t runs = (int64_t)((g.lines + kSqBlock - 1) / kSqBlock) * g.en0;
         sqp = reinterpret_cast<const uint32_t *>(a.base + md.sq_ptr_off[role]) + (int64_t)o * (runs + 1);
-        sqe = reinterpret_cast<const uint2 *>(a.base + md.sq_ent_off[role]);
+        sqe = reinterpret_cast<const SqEntry *>(a.base + md.sq_ent_off[role]);
     }
     float *qe0 = sh;                      // [kCtx][32]: marginals of the entry side's first factor
                                           // (pairs: [32][kCtx], times 2^-15)
@@ -553,7 +550,7 @@ __device__ void split_body(const StreamArgs &a, const float *__restrict__ q, flo
         const int jc = min(kCtx, J - c0);
         if (tid < kCtx) ctxs[tid] = tid < jc ? a.bctx[(int64_t)m * a.nctx + b0 + c0 + tid] : -1;
         if (MODE == kSparsePairs)   // zero B blocks (the line tile of the last pass overlays them)
-            for (int i = tid; i < kWaves * kSqBlockBytes / 16; i += kThreads)
+            for (int i = tid; i < kWaves * kSqWaveBytes / 16; i += kThreads)
                 reinterpret_cast<u4 *>(blocks)[i] = u4{0u, 0u, 0u, 0u};
         __syncthreads();
         for (int i = tid; i < kCtx * 64; i += kThreads) {
@@ -638,7 +635,7 @@ size_t lds_bytes(const bi_model *m, bool sparse)
             const Geo g = geo_of(md, role);
             const size_t lines = (size_t)std::min(split_groups(g), g.ln0) * g.ln1;
             size_t tail = sizeof(float) * lines * kZS;
-            if (sparse) tail = std::max(tail, (size_t)kWaves * kSqBlockBytes);
+            if (sparse) tail = std::max(tail, (size_t)kWaves * kSqWaveBytes);
             most = std::max(most, sizeof(float) * (size_t)kCtx * 64 + tail);
         }
     return most;

@@ -301,7 +301,9 @@ def test_host_pack_sparse_pair_layout(case):
     """BI_SPARSE_A with BI_F16_PAIRS: per side, the nonzeros of every outcome
     in blocks of 64 lines, inside a block by (e0, line, e1), each entry the
     binary16 rounding of LN(A) - ln(eps) and of its residual (numpy's float64
-    -> float16 conversion is the reference) with its position in the block,
+    -> float16 conversion is the reference) with its byte offset in the
+    kernel's LDS block (16 + line (2 en1 + 16) + 2 e1; offset 0, the pad that
+    empty slots write to, is never an entry's),
     and the run pointers delimiting every (block, e0).  Rebuilt into dense
     slices they give back exactly the pair rounding of the nonzeros."""
     n, K = SQ_SHAPES[case]
@@ -346,9 +348,12 @@ def test_host_pack_sparse_pair_layout(case):
                     for blk in range(nblk):
                         for e0 in range(e0n):
                             run = ent[ptr[o, blk * e0n + e0]:ptr[o, blk * e0n + e0 + 1]]
-                            line = (run["pos"] >> 8).astype(np.int64)
-                            e1 = (run["pos"] & 255).astype(np.int64)
-                            assert np.all(line < 64) and np.all(blk * 64 + line < lines) and np.all(e1 < e1n)
+                            # pos = 16 + line (2 e1n + 16) + 2 e1: the byte offset in the kernel's LDS block
+                            off = run["pos"].astype(np.int64) - 16
+                            line, rem = off // (2 * e1n + 16), off % (2 * e1n + 16)
+                            e1 = rem // 2
+                            assert np.all(off >= 0) and np.all(rem % 2 == 0) and np.all(rem < 2 * e1n)
+                            assert np.all(line < 64) and np.all(blk * 64 + line < lines)
                             key = line * e1n + e1
                             assert np.all(np.diff(key) > 0)       # ordered by (line, e1), no repeats
                             L, E = blk * 64 + line, e0 * e1n + e1

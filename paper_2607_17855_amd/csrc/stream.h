@@ -63,6 +63,7 @@ struct StreamArgs {
     double tau;                 // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
     int32_t *bstart, *bctx;
     int nmsg, ntask;
+    int stage;                  // update: partial messages and neighbour marginals staged in LDS
     StreamMod sm[kStreamMaxM];
     MsgSrc msg[kStreamMaxMsg];
     SpTask task[kStreamMaxTask];

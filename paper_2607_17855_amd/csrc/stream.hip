@@ -420,45 +420,97 @@ __global__ __launch_bounds__(kThreads, 1) void lik_kernel(StreamArgs a, const fl
 }
 
 // sum_j M[j * ms] * x[j] over j < n in order (fp64), loads issued 8 at a time
-template <typename MT, typename XT>
-__device__ inline double dot_strided(const MT *M, int64_t ms, const XT *x, int n)
+// Two dot products of one state's transition messages over j in [j0, j1):
+// df = sum M_f[j] x_f[j] (a row of B, stride 1) and db = sum M_b[j bs] x_b[j]
+// (a column), each in j order in fp64; either may be absent (null x).  The
+// operands of both come in 4 at a time, all loads issued before the
+// arithmetic, so the pair costs one memory round trip per 4 terms.
+template <typename MT, typename QT>
+__device__ inline void dot_pair(const MT *Mf, const QT *xf, const MT *Mb, int64_t bs, const QT *xb, int j0, int j1,
+                                double &df, double &db)
 {
-    double acc = 0.0;
-    int j = 0;
-    for (; j + 8 <= n; j += 8) {
-        MT mv[8];
-        XT xv[8];
+    constexpr int W = 4;
+    df = 0.0;
+    db = 0.0;
+    int j = j0;
+    for (; j + W <= j1; j += W) {
+        MT mf[W], mb[W];
+        QT qf[W], qb[W];
+        if (xf)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            mv[u] = M[(int64_t)(j + u) * ms];
-            xv[u] = x[j + u];
-        }
+            for (int u = 0; u < W; ++u) {
+                mf[u] = Mf[j + u];
+                qf[u] = xf[j + u];
+            }
+        if (xb)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) acc = fma((double)mv[u], (double)xv[u], acc);
+            for (int u = 0; u < W; ++u) {
+                mb[u] = Mb[(int64_t)(j + u) * bs];
+                qb[u] = xb[j + u];
+            }
+        if (xf)
+#pragma unroll
+            for (int u = 0; u < W; ++u) df = fma((double)mf[u], (double)qf[u], df);
+        if (xb)
+#pragma unroll
+            for (int u = 0; u < W; ++u) db = fma((double)mb[u], (double)qb[u], db);
     }
-    for (; j < n; ++j) acc = fma((double)M[(int64_t)j * ms], (double)x[j], acc);
-    return acc;
+    for (; j < j1; ++j) {
+        if (xf) df = fma((double)Mf[j], (double)xf[j], df);
+        if (xb) db = fma((double)Mb[(int64_t)j * bs], (double)xb[j], db);
+    }
 }
 
 // ---------------------------------------------------------------------------
 // update: messages summed over their partial vectors (fp64, fixed order),
 // transition messages, masked softmax; one workgroup per context, one wave
-// per factor.  QT = marginals between iterations, PT = partial messages,
-// OT = this launch's output marginals.
+// per factor.  When they fit (a.stage), the context's partial messages and
+// the marginals of its neighbours in time are first copied to LDS by the
+// whole workgroup (independent loads, one memory round trip), so the sums
+// read LDS.  For factors of up to 32 states two lanes share a state: each
+// takes half of its partial vectors and half of the terms of its transition
+// dots, and one shuffle adds the halves (the same in both lanes).  QT =
+// marginals between iterations, PT = partial messages, OT = this launch's
+// output marginals.
 // ---------------------------------------------------------------------------
 template <int ALGO, typename QT, typename PT, typename OT>
 __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *part, const QT *qin, OT *qout)
 {
-    extern __shared__ double vals[];   // [ntot]
+    extern __shared__ double vals[];   // [ntot], then (staged) partials [pstride] and two marginal vectors [ntot]
     const int ctx = blockIdx.x;
     const int agent = ctx / a.T, t = ctx - agent * a.T;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const PT *pc = part + (int64_t)ctx * a.pstride;
+    const QT *qp = t > 0 ? qin + (int64_t)(ctx - 1) * a.ntot : nullptr;
+    const QT *qn = t + 1 < a.T ? qin + (int64_t)(ctx + 1) * a.ntot : nullptr;
+    if (a.stage) {
+        PT *sp = reinterpret_cast<PT *>(vals + a.ntot);
+        QT *sq = reinterpret_cast<QT *>(vals + a.ntot + (a.pstride * sizeof(PT) + 7) / 8);
+        const int tid = threadIdx.x;
+        const int np = (int)a.pstride, nq = a.ntot;
+        for (int i0 = tid; i0 < np; i0 += 8 * 256) {   // 8 independent loads per thread, then the stores
+            PT v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = i0 + 256 * u < np ? pc[i0 + 256 * u] : (PT)0;
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (i0 + 256 * u < np) sp[i0 + 256 * u] = v[u];
+        }
+        for (int i = tid; i < nq; i += 256) {
+            const QT a0 = qp ? qp[i] : (QT)0, a1 = qn ? qn[i] : (QT)0;
+            sq[i] = a0;
+            sq[nq + i] = a1;
+        }
+        __syncthreads();
+        pc = sp;
+        qp = qp ? sq : nullptr;
+        qn = qn ? sq + nq : nullptr;
+    }
     for (int f = wave; f < a.F; f += 4) {
         const FacDesc &fd = a.facs[f];
         const int n = fd.n;
-        const QT *qprev = t > 0 ? qin + (int64_t)(ctx - 1) * a.ntot + fd.q_off : nullptr;
-        const QT *qnext = t + 1 < a.T ? qin + (int64_t)(ctx + 1) * a.ntot + fd.q_off : nullptr;
+        const QT *qprev = qp ? qp + fd.q_off : nullptr;
+        const QT *qnext = qn ? qn + fd.q_off : nullptr;
         const int up = t > 0 ? a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f] : 0;
         const int un = t + 1 < a.T ? a.act[((int64_t)agent * (a.T - 1) + t) * a.F + f] : 0;
         const double *LBp = reinterpret_cast<const double *>(a.base + fd.lb_off) + (int64_t)up * n * n;
@@ -467,41 +519,43 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *par
         const float *Bn = reinterpret_cast<const float *>(a.base + fd.b_off) + (int64_t)un * n * n;
         const double *ld = reinterpret_cast<const double *>(a.base + fd.ld_off);
         double *v = vals + fd.q_off;
-        for (int s = lane; s < n; s += 64) {
+        const int L = n <= 32 ? 2 : 1;          // lanes per state
+        const int half = lane & (L - 1);        // which share of the terms this lane takes
+        const int h = (n + L - 1) / L;          // transition terms per share
+        const int j0 = min(n, half * h), j1 = min(n, j0 + h);
+        for (int s0 = 0; s0 < n; s0 += 64 / L) {
+            const int s = s0 + lane / L;
+            const int sc = min(s, n - 1);       // lanes past the last state compute a copy, unused
             double lam = 0.0;
             for (int i = 0; i < a.nmsg; ++i) {
                 const MsgSrc src = a.msg[i];
                 if (src.f != f) continue;
-                const PT *pp = pc + src.off + s;
-                int k = 0;
-                for (; k + 8 <= src.copies; k += 8) {   // loads first, then the sums in order
-                    PT pv[8];
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) pv[u] = pp[(int64_t)(k + u) * src.stride];
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) lam += (double)pv[u];
-                }
-                for (; k < src.copies; ++k) lam += (double)pp[(int64_t)k * src.stride];
+                const PT *pp = pc + src.off + sc;
+                for (int k = half; k < src.copies; k += L) lam += (double)pp[(int64_t)k * src.stride];
             }
-            double fwd, bwd = 0.0;
-            if (t == 0) {
-                fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + fd.q_off + s]) : ld[s];
-            } else if (ALGO == BI_ALGO_VMP) {
-                fwd = dot_strided(LBp + s * n, 1, qprev, n);
-            } else {
-                fwd = ln_clamped(dot_strided(Bp + s * n, 1, qprev, n));
-            }
-            if (qnext) {
-                if (ALGO == BI_ALGO_VMP)
-                    bwd = dot_strided(LBn + s, n, qnext, n);
-                else
-                    bwd = ln_clamped(dot_strided(Bn + s, n, qnext, n));
-            }
+            double fwd = 0.0, bwd = 0.0;
             if (ALGO == BI_ALGO_VMP)
-                v[s] = lam + fwd + bwd;
+                dot_pair(LBp + (int64_t)sc * n, qprev, LBn + sc, n, qnext, j0, j1, fwd, bwd);
             else
-                v[s] = qnext ? lam + 0.5 * (fwd + bwd) : lam + fwd;
+                dot_pair(Bp + (int64_t)sc * n, qprev, Bn + sc, n, qnext, j0, j1, fwd, bwd);
+            if (L == 2) {
+                lam += __shfl_xor(lam, 1, 64);
+                fwd += __shfl_xor(fwd, 1, 64);
+                bwd += __shfl_xor(bwd, 1, 64);
+            }
+            if (t == 0)
+                fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + fd.q_off + sc]) : ld[sc];
+            else if (ALGO != BI_ALGO_VMP)
+                fwd = ln_clamped(fwd);
+            if (qnext && ALGO != BI_ALGO_VMP) bwd = ln_clamped(bwd);
+            if (s < n && half == 0) {
+                if (ALGO == BI_ALGO_VMP)
+                    v[s] = lam + fwd + bwd;
+                else
+                    v[s] = qnext ? lam + 0.5 * (fwd + bwd) : lam + fwd;
+            }
         }
+        __builtin_amdgcn_wave_barrier();   // v[s] came from lane L s (one wave: LDS in program order)
         double mx = -INFINITY;
         for (int s = lane; s < n; s += 64) mx = fmax(mx, v[s]);
         mx = wave_max(mx);
@@ -692,8 +746,13 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.bstart = reinterpret_cast<int32_t *>(w + offs[0]);
     a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
     char *part = w + offs[3];
-    const size_t upd_lds = sizeof(double) * m->ntot;
     const Lik lik = lik_kind(m, sparse);
+    // update: the softmax values, plus (when they fit in 48 KB) the staged
+    // partial messages and the two neighbour marginal vectors
+    const size_t es_p = lik == Lik::Sparse ? sizeof(double) : sizeof(float);   // partials and marginals
+    const size_t staged = sizeof(double) * m->ntot + (a.pstride * es_p + 7) / 8 * 8 + 2 * es_p * m->ntot;
+    a.stage = staged <= 48 * 1024 ? 1 : 0;
+    const size_t upd_lds = a.stage ? staged : sizeof(double) * m->ntot;
     size_t lik_lds = 0;
     if (lik == Lik::Sparse) {
         lik_lds = sparse_lds_bytes(m);

@@ -54,7 +54,8 @@ CSRC = os.path.join(ROOT, "paper_2607_17855_amd", "csrc")
 # likelihood kernels: profile class -> (kernel symbol, source file)
 LIK = {"lik": ("lik_kernel", "stream.hip"), "lik_split": ("split_lik_kernel<false>", "split.hip"),
        "lik_split16": ("split_lik_kernel<true>", "split.hip"), "lik_sparse": ("sparse_lik_kernel", "sparse.hip"),
-       "lik_sparse16": ("sparse16_lik_kernel", "split.hip")}
+       "lik_sparse16": ("sparse16_lik_kernel", "split.hip"),
+       "lik_rowcol16": ("rowcol16_lik_kernel", "rowcol.hip")}
 LAYOUTS = ("dense", "sparse")
 ALGOS = ("vmp", "mmp")
 
@@ -286,7 +287,7 @@ def main():
 
     traffic = load_traffic()
     dense_work = dense_lik_work(w.model, w.obs)
-    work = {"lik": dense_work, "lik_split": dense_work, "lik_split16": dense_work,
+    work = {"lik": dense_work, "lik_split": dense_work, "lik_split16": dense_work, "lik_rowcol16": dense_work,
             "lik_sparse": sparse_lik_work(w.model, w.obs), "lik_sparse16": sparse16_lik_work(w.model, w.obs)}
     rooflines = {}
     for cls, (kname, src) in LIK.items():
@@ -297,7 +298,7 @@ def main():
         flops, alg_bytes = work[cls]
         tr = traffic.get(kname)
         hbm = tr["hbm_bytes_per_launch"] if tr and tr.get("kernel_source_sha") == source_sha(src) else None
-        if cls in ("lik_split16", "lik_sparse16"):
+        if cls in ("lik_split16", "lik_sparse16", "lik_rowcol16"):
             # memory bound: the fp16 products (3 per fp32 product) take a
             # fraction of the time the slice bytes (dense: every entry, 4 B;
             # sparse: the nonzeros, 8 B) do
@@ -316,7 +317,7 @@ def main():
             "measured_hbm_GBps": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9,
             "hbm_frac": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
         }
-        if cls in ("lik_split16", "lik_sparse16"):
+        if cls in ("lik_split16", "lik_sparse16", "lik_rowcol16"):
             f16 = 3 * flops / (avg_ms / 1e3) / 1e12
             rooflines[cls]["fp16_mfma"] = {"achieved_TFLOPs": f16, "peak": PEAK_FP16_MFMA_TFLOPS,
                                            "frac": f16 / PEAK_FP16_MFMA_TFLOPS}

@@ -89,6 +89,10 @@ struct ModDesc {
     // sparse fp16 pairs (BI_SPARSE_A with BI_F16_PAIRS), per side: pointer
     // array and SqEntry array, or -1
     int64_t sq_ptr_off[2], sq_ent_off[2];
+    // order of the fp16 pairs: 0 = by rows in groups of 4 columns (above);
+    // 1 = in 32 x 32 blocks (rc_shape below)
+    int32_t lp16_order;
+    int32_t pad0;
 };
 
 constexpr int kSqBlock = 64;   // lines per block of the sparse fp16-pair layout
@@ -113,6 +117,27 @@ inline bool sq_shape(const ModDesc &md)
         if ((n1 != 16 && n1 != 32) || n0 > 32 || n0 % 2 != 0) return false;
     }
     return true;
+}
+
+// Blocked fp16 pairs (lp16_order = 1).  When every modality of a shared
+// model has two factors on each side, both second factors of 32 states, the
+// first column factor an even number of states up to 32 and the first row
+// factor at most 32, the pair copy of slice o is stored as 4096-byte blocks,
+// one per (r0, c0) in that order (r0 the first row factor's state, c0 the
+// first column factor's).  A block holds the 32 rows r1 of the second row
+// factor, 128 bytes each: for u = 0..3 the binary16 high parts of columns
+// c1 = 8u .. 8u + 7, then their residuals.  One block is what one wave of
+// the single-read kernel contracts per step, so it streams contiguous memory.
+inline bool rc_shape(const ModDesc &md)
+{
+    return md.nrow == 2 && md.ncol == 2 && md.Cp == md.C && md.rn[1] == 32 && md.cn[1] == 32 && md.rn[0] <= 32 &&
+           md.cn[0] <= 32 && md.cn[0] % 2 == 0;
+}
+// uint16 index of the high part of (r, col) in a blocked slice (residual: + 8)
+inline int64_t rc_pair_index(const ModDesc &md, int64_t r, int64_t col)
+{
+    const int64_t r0 = r >> 5, r1 = r & 31, c0 = col >> 5, c1 = col & 31;
+    return ((r0 * md.cn[0] + c0) * 32 + r1) * 64 + 16 * (c1 >> 3) + (c1 & 7);
 }
 
 constexpr int kMaxBDep = 4;   // B-dependencies per factor

@@ -246,6 +246,16 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
         a_stored += (int64_t)m->mb * md.K * md.slice;
     }
     m->zvpc = zv;
+    // the pair copies are blocked when every modality has the single-read
+    // kernel's shape (layout.h)
+    {
+        bool all = true;
+        for (const ModDesc &md : m->mods) all = all && md.lp16_off >= 0 && rc_shape(md);
+        for (ModDesc &md : m->mods) {
+            md.lp16_order = all ? 1 : 0;
+            md.pad0 = 0;
+        }
+    }
     for (int f = 0; f < m->F; ++f) {
         FacDesc &fd = m->facs[f];
         const int64_t per = (int64_t)fd.U * fd.n * fd.bstates;
@@ -342,7 +352,16 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
                 float *d32 = reinterpret_cast<float *>(host + md.la32_off) + s * md.slice;
                 for (int64_t e = 0; e < md.slice; ++e) d32[e] = (float)dst[e];
             }
-            if (md.lp16_off >= 0) {   // shared model: s is the outcome
+            if (md.lp16_off >= 0 && md.lp16_order == 1) {   // shared model: s is the outcome
+                uint16_t *p = reinterpret_cast<uint16_t *>(host + md.lp16_off) + 2 * s * md.slice;
+                for (int64_t r = 0; r < md.R; ++r)
+                    for (int64_t col = 0; col < md.C; ++col) {
+                        const int64_t i = rc_pair_index(md, r, col);
+                        double hi;
+                        p[i] = half_rne(dst[r * md.Cp + col], &hi);
+                        p[i + 8] = half_rne(dst[r * md.Cp + col] - hi, nullptr);
+                    }
+            } else if (md.lp16_off >= 0) {
                 uint16_t *p = reinterpret_cast<uint16_t *>(host + md.lp16_off) + 2 * s * md.slice;
                 for (int64_t e = 0; e < md.slice; e += 4)
                     for (int i = 0; i < 4; ++i) {

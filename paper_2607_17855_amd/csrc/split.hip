@@ -723,7 +723,7 @@ size_t split_lds_bytes(const bi_model *m, bool sparse) { return lds_bytes(m, spa
 bool split_pairs(const bi_model *m)
 {
     for (const ModDesc &md : m->mods)
-        if (md.lp16_off < 0) return false;
+        if (md.lp16_off < 0 || md.lp16_order != 0) return false;   // row-ordered pairs only
     return !m->mods.empty();
 }
 

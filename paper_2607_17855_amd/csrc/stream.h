@@ -96,6 +96,19 @@ bool sq_eligible(const bi_model *m);
 void split_lik_launch(const bi_model *m, const StreamArgs &a, const float *q, float *part, hipStream_t stream,
                       bool sparse);
 
+// Dense likelihood kernel reading every slice once (rowcol.hip), for models
+// with the fp16-pair copy (BI_F16_PAIRS) whose modalities all have two
+// factors per side, both second factors of 32 states, the first column
+// factor of an even number of states up to 32 and the first row factor of at
+// most 32: eligibility, planning (tasks and message sources; returns the
+// values of partial messages per context), the dynamic LDS size, the
+// once-per-call kernel attribute and one launch.
+bool rc_eligible(const bi_model *m);
+int64_t rc_plan(const bi_model *m, StreamArgs *a);
+size_t rc_lds_bytes();
+int rc_prepare();
+void rc_lik_launch(const StreamArgs &a, const float *q, float *part, hipStream_t stream);
+
 // Sparse likelihood kernel (sparse.hip): task planning and one launch.
 // sparse_plan fills a->task / a->ntask / a->nwg and the message sources,
 // and returns the values of partial messages per context.

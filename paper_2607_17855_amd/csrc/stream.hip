@@ -640,12 +640,15 @@ static int64_t dense_plan(const bi_model *m, StreamArgs *a)
 }
 
 // The likelihood kernel a streaming call runs: general dense, dense
-// matrix-core tiles, sparse fp64 gathers, sparse fp16-pair matrix-core tiles.
-enum class Lik { Dense, Split, Sparse, Sparse16 };
+// matrix-core tiles (one contraction per workgroup), dense fp16-pair tiles
+// reading every slice once, sparse fp64 gathers, sparse fp16-pair
+// matrix-core tiles.
+enum class Lik { Dense, Split, RowCol, Sparse, Sparse16 };
 
 static Lik lik_kind(const bi_model *m, bool sparse)
 {
     if (sparse) return sq_eligible(m) ? Lik::Sparse16 : Lik::Sparse;
+    if (rc_eligible(m)) return Lik::RowCol;
     return split_eligible(m) ? Lik::Split : Lik::Dense;
 }
 
@@ -665,9 +668,10 @@ static void plan_ws(const bi_model *m, int b, int T, bool sparse, StreamArgs *a,
         fofs += sm.K;
     }
     const Lik lik = lik_kind(m, sparse);
-    a->pstride = lik == Lik::Sparse ? sparse_plan(m, a)
-                 : lik == Lik::Dense ? dense_plan(m, a)
-                                     : split_plan(m, a);
+    a->pstride = lik == Lik::Sparse   ? sparse_plan(m, a)
+                 : lik == Lik::Dense  ? dense_plan(m, a)
+                 : lik == Lik::RowCol ? rc_plan(m, a)
+                                      : split_plan(m, a);
     const int64_t es = lik == Lik::Sparse ? 8 : 4;
     int64_t off = 0;
     offs[0] = off;  off = align_up(off + 4 * (int64_t)bofs, kAlign);
@@ -696,6 +700,7 @@ static void run_iterations(const bi_model *m, int algo, int iters, const StreamA
     const char *name = lik == Lik::Sparse     ? "lik_sparse"
                        : lik == Lik::Sparse16 ? "lik_sparse16"
                        : lik == Lik::Split    ? (split_pairs(m) ? "lik_split16" : "lik_split")
+                       : lik == Lik::RowCol   ? "lik_rowcol16"
                                               : "lik";
     for (int k = 0; k < iters; ++k) {
         {
@@ -703,6 +708,8 @@ static void run_iterations(const bi_model *m, int algo, int iters, const StreamA
             if (lik == Lik::Sparse)
                 sparse_lik_launch(m, a, reinterpret_cast<const double *>(cur), reinterpret_cast<double *>(part),
                                   stream);
+            else if (lik == Lik::RowCol)
+                rc_lik_launch(a, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream);
             else if (lik != Lik::Dense)
                 split_lik_launch(m, a, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream,
                                  lik == Lik::Sparse16);
@@ -756,6 +763,8 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     size_t lik_lds = 0;
     if (lik == Lik::Sparse) {
         lik_lds = sparse_lds_bytes(m);
+    } else if (lik == Lik::RowCol) {
+        lik_lds = rc_lds_bytes();
     } else if (lik != Lik::Dense) {
         lik_lds = split_lds_bytes(m, lik == Lik::Sparse16);
     } else {
@@ -768,6 +777,9 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
         return fail(BI_ERR_UNSUPPORTED, "streaming working set exceeds LDS");
     if (lik == Lik::Sparse) {
         const int rc = sparse_prepare(m);
+        if (rc != BI_OK) return rc;
+    } else if (lik == Lik::RowCol) {
+        const int rc = rc_prepare();
         if (rc != BI_OK) return rc;
     } else if (lik == Lik::Dense) {
         const hipError_t e = hipFuncSetAttribute((const void *)lik_kernel,

@@ -40,7 +40,8 @@ class ModDesc(ctypes.Structure):
                 ("cn", ctypes.c_int32 * 2), ("zv_off", ctypes.c_int32), ("dsum", ctypes.c_int32),
                 ("la32_off", ctypes.c_int64), ("csr_ptr_off", ctypes.c_int64), ("csr_ent_off", ctypes.c_int64),
                 ("csc_ptr_off", ctypes.c_int64), ("csc_ent_off", ctypes.c_int64), ("nnz", ctypes.c_int64),
-                ("lp16_off", ctypes.c_int64), ("sq_ptr_off", ctypes.c_int64 * 2), ("sq_ent_off", ctypes.c_int64 * 2)]
+                ("lp16_off", ctypes.c_int64), ("sq_ptr_off", ctypes.c_int64 * 2), ("sq_ent_off", ctypes.c_int64 * 2),
+                ("lp16_order", ctypes.c_int32), ("pad0", ctypes.c_int32)]
 
 
 SpEntry = np.dtype([("v", np.float64), ("a", np.uint32), ("b", np.uint32)])
@@ -613,6 +614,55 @@ def test_f16_pair_plane(seed):
     try:
         mods, _ = _descs(img, ma.M, ma.F)
         assert all(mods[i].lp16_off == -1 for i in range(ma.M))
+    finally:
+        bi.bi_free_model(h)
+
+
+def test_f16_pair_blocks():
+    """Models whose modalities all have two factors per side with both second
+    factors of 32 states get the blocked pair copy: per outcome, 4096-byte
+    blocks in (r0, c0) order, each with the 32 rows r1 of 128 bytes, and in a
+    row, for every 8 columns c1, their 8 high parts, then their 8 residuals
+    (the same values as the row-ordered copy).  A model with one modality of
+    another shape keeps the row order for all."""
+    rng = np.random.Generator(np.random.PCG64(11))
+    n, U = [4, 32, 2, 32], [1, 1, 1, 1]
+    K = [2, 3]
+    deps = [[0, 1, 2, 3], [0, 1, 2, 3]]
+    A = []
+    for k in K:
+        a = rng.dirichlet(np.ones(k), size=int(np.prod(n))).T.reshape([1, k] + n)
+        A.append(a.astype(np.float32))
+    B = [np.full((1, x, x, 1), 1.0 / x, np.float32) for x in n]
+    D = [np.full((1, x), 1.0 / x, np.float32) for x in n]
+    fl = bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
+    h, img = bi.bi_pack_model_host(n, U, K, deps, 1, A, B, D, flags=fl)
+    try:
+        mods, _ = _descs(img, 2, 4)
+        for mi in range(2):
+            md = mods[mi]
+            assert md.lp16_order == 1 and (md.R, md.C, md.Cp) == (128, 64, 64)
+            X = img[md.la_off:md.la_off + 8 * md.K * md.slice].view(np.float64).reshape(md.K, 4, 32, 2, 32)
+            hi = X.astype(np.float16)
+            lo = (X - hi.astype(np.float64)).astype(np.float16)
+            # [o][r0][c0][r1][unit g][high / residual][8 columns]
+            P = img[md.lp16_off:md.lp16_off + 4 * md.K * md.slice].view(np.uint16).reshape(md.K, 4, 2, 32, 4, 2, 8)
+            want_hi = hi.transpose(0, 1, 3, 2, 4).reshape(md.K, 4, 2, 32, 4, 8)
+            want_lo = lo.transpose(0, 1, 3, 2, 4).reshape(md.K, 4, 2, 32, 4, 8)
+            np.testing.assert_array_equal(P[..., 0, :], want_hi.view(np.uint16))
+            np.testing.assert_array_equal(P[..., 1, :], want_lo.view(np.uint16))
+    finally:
+        bi.bi_free_model(h)
+    # one modality with a 16-state second factor: row order everywhere
+    n2 = [4, 32, 2, 16]
+    A2 = [rng.dirichlet(np.ones(2), size=int(np.prod(n2))).T.reshape([1, 2] + n2).astype(np.float32),
+          rng.dirichlet(np.ones(2), size=4 * 32).T.reshape([1, 2, 4, 32]).astype(np.float32)]
+    B2 = [np.full((1, x, x, 1), 1.0 / x, np.float32) for x in n2]
+    D2 = [np.full((1, x), 1.0 / x, np.float32) for x in n2]
+    h, img = bi.bi_pack_model_host(n2, U, [2, 2], [[0, 1, 2, 3], [0, 1]], 1, A2, B2, D2, flags=fl)
+    try:
+        mods, _ = _descs(img, 2, 4)
+        assert mods[0].lp16_order == 0 and mods[1].lp16_order == 0
     finally:
         bi.bi_free_model(h)
 

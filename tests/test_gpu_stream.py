@@ -99,6 +99,41 @@ def test_split_kernel_vs_oracle_and_agent(case, prec, force_stream):
         pm.close()
 
 
+# shapes taken by the single-read fp16-pair kernel (two factors per side,
+# both second factors of 32 states): a row tile of 6 of its 8 row states, two
+# modalities over two row tiles (the second one half full), and buckets of
+# more than 48 contexts (a second pass of 1 context block)
+ROWCOL_CASES = [
+    ([6, 32, 4, 32], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], 24, 5),
+    ([12, 32, 2, 32], [1, 2, 1, 2], [4, 2], [[0, 1, 2, 3], [0, 1, 2, 3]], 40, 4),
+    ([8, 32, 8, 32], [2, 2, 1, 1], [2], [[0, 1, 2, 3]], 60, 2),
+]
+
+
+@pytest.mark.parametrize("case", range(len(ROWCOL_CASES)))
+def test_rowcol_kernel_vs_oracle_and_agent(case, force_stream):
+    n, U, K, deps, b, T = ROWCOL_CASES[case]
+    w = _shared_model(90 + case, n, U, K, deps, b, T, iters=2)
+    for algo in ("vmp", "mmp"):
+        q, pm = run_gpu(w, algo, flags=FAST["f16pairs"])
+        check_invariants(w, q)
+        ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters)
+        err = float(np.abs(q - ref).max())
+        print(f"[gpu]   rowcol stream vs oracle {err:.3e}", flush=True)
+        bi.bi_profile_begin()
+        q2, _ = run_gpu(w, algo, pm=pm)
+        names = set(bi.bi_profile_end())
+        assert "lik_rowcol16" in names, names
+        assert err <= TOL
+        # the same call again gives the same bits (fixed summation order)
+        assert np.array_equal(q, q2)
+        os.environ["BI_FORCE_PATH"] = "agent"
+        qa, _ = run_gpu(w, algo, pm=pm)
+        os.environ["BI_FORCE_PATH"] = "stream"
+        assert float(np.abs(q - qa).max()) <= TOL
+        pm.close()
+
+
 @functools.lru_cache(maxsize=None)
 def large_shared():
     return synth.large_shared()

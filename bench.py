@@ -346,9 +346,9 @@ def main():
         "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
         "wall_s_timed": wall,
         "dtype_note": ("dense layout: fp32 matrix-core contractions (v_mfma_f32_16x16x4f32)" if args.dense_f32 else
-                       "dense layout: slices as fp16 (high, residual) pairs, 22 significant bits, contracted with "
-                       "three fp16 matrix-core products per fp32 product (v_mfma_f32_16x16x32_f16), fp32 "
-                       "accumulation") + " with fp64 message sums, transitions and softmax; sparse layout: "
+                       "dense layout: slices as fp16 (high, residual) pairs in 32x32 blocks, 22 significant bits, "
+                       "each block read once and contracted towards its rows and its columns with three fp16 "
+                       "matrix-core products per fp32 product (v_mfma_f32_16x16x32_f16), fp32 accumulation") + " with fp64 message sums, transitions and softmax; sparse layout: "
                       + ("fp64 throughout" if args.sparse_f64 else
                          "the nonzeros as fp16 pairs, scattered into LDS blocks and contracted with the same "
                          "three-product fp16 matrix-core chains") + "; every marginal within 1e-5 of the fp64 oracle",

@@ -259,6 +259,17 @@ __device__ void rc_pass(const StreamArgs &a, const Pass &p, const float *__restr
             float w[NKB];
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) w[kb] = qc0t[c0 * kCtx + 16 * kb + li];
+            uint32_t ch[8], cl[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    // row 8 lg + 2 e + b: high-part unit at position ((2 (li >> 2)) ^ (2 e + b)),
+                    // residual unit at the other position of the same pair
+                    const char *g = blk + cob[e] + 128 * b;
+                    ch[2 * e + b] = *reinterpret_cast<const uint32_t *>(g + 16 * b);
+                    cl[2 * e + b] = *reinterpret_cast<const uint32_t *>(g + 16 * (1 - b));
+                }
             // rows: Y and this state's m_c0 share
             float s3[NKB];
 #pragma unroll
@@ -277,18 +288,6 @@ __device__ void rc_pass(const StreamArgs &a, const Pass &p, const float *__restr
                     }
                 }
             }
-            __builtin_amdgcn_sched_barrier(0);
-            uint32_t ch[8], cl[8];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-#pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    // row 8 lg + 2 e + b: high-part unit at position ((2 (li >> 2)) ^ (2 e + b)),
-                    // residual unit at the other position of the same pair
-                    const char *g = blk + cob[e] + 128 * b;
-                    ch[2 * e + b] = *reinterpret_cast<const uint32_t *>(g + 16 * b);
-                    cl[2 * e + b] = *reinterpret_cast<const uint32_t *>(g + 16 * (1 - b));
-                }
             // columns: column 2 li + jj of the state
 #pragma unroll
             for (int jj = 0; jj < 2; ++jj) {

@@ -192,3 +192,25 @@ def exact_window_marginals(model, obs_a, act_a, a):
 
 def all_assignments(shape):
     return itertools.product(*[range(s) for s in shape])
+
+
+def predictive_bruteforce(model, q, act):
+    """Predictive marginal of every factor at the next step, by enumerating
+    the joint of ALL current states under the factorised q (Sec. III-B
+    transition model: s_{t+1}^f ~ B_f[:, s_t^{list(f)}, u_f]):
+      p_f(i) = sum_{s_0..s_{F-1}} prod_g q_g(s_g) B_f[i][s_{list(f)}][u_f].
+    q: [b][sum n], act: [b][F]; returns [b][sum n] (float64)."""
+    F = len(model.n)
+    offs = np.cumsum([0] + list(model.n))
+    b = q.shape[0]
+    out = np.zeros((b, int(offs[-1])))
+    for a in range(b):
+        for joint in itertools.product(*[range(n) for n in model.n]):
+            w = 1.0
+            for g in range(F):
+                w *= float(q[a, offs[g] + joint[g]])
+            for f in range(F):
+                Bf = _agent(model.B[f], model.mb, a)
+                cond = tuple(joint[g] for g in _bdep(model, f))
+                out[a, offs[f]:offs[f + 1]] += w * Bf[(slice(None),) + cond + (int(act[a, f]),)]
+    return out

@@ -556,6 +556,46 @@ def pin_bdeps_uninformative_transitions(infer):
     return err
 
 
+def pin_predict_bruteforce(infer):
+    """Predictive prior with B-dependency lists (and trivial ones) against
+    enumeration of the full joint of the current states under the factorised
+    marginals; per-agent and shared models, several agents with different
+    marginals and actions."""
+    predict = _predict_of(infer)
+    err = 0.0
+    for seed in range(6):
+        F = 2 + seed % 2
+        lists = [[f] for f in range(F)] if seed == 5 else None   # explicit trivial lists too
+        model, obs, act = _bdep_model(640 + seed, F=F, T=2, b=3, lists=lists)
+        if seed % 3 == 2:   # one model shared by the agents
+            model = synth.Model(model.n, model.U, model.K, model.deps, 1, [x[:1] for x in model.A],
+                                [x[:1] for x in model.B], [x[:1] for x in model.D], model.bdeps)
+        rd = np.random.Generator(np.random.PCG64(seed + 900))
+        q = np.concatenate([rd.dirichlet(np.ones(n), size=3) for n in model.n], axis=1)
+        u = np.stack([rd.integers(0, U, size=3) for U in model.U], axis=1).astype(np.int32)
+        err = max(err, float(np.abs(predict(model, q, u) - bf.predictive_bruteforce(model, q, u)).max()))
+    return err
+
+
+def pin_online_filter_bdeps(infer):
+    """Rolling inference with B-dependency lists: FPI stays causal, so the
+    window filtered in one call equals one-step calls chained through the
+    predictive prior of the previous step's posterior (whose factors are
+    coupled through the lists)."""
+    predict = _predict_of(infer)
+    err = 0.0
+    for seed in range(4):
+        model, obs, act = _bdep_model(660 + seed, F=2 + seed % 2, T=4, b=3)
+        full = infer("fpi", model, obs, act, 4)
+        prior = np.concatenate([np.float64(d) for d in model.D], axis=1)
+        for t in range(obs.shape[1]):
+            step = infer("fpi", model, obs[:, t:t + 1], act[:, :0], 4, prior=prior)
+            err = max(err, float(np.abs(step[:, 0] - full[:, t]).max()))
+            if t + 1 < obs.shape[1]:
+                prior = predict(model, step[:, 0], act[:, t])
+    return err
+
+
 ALL_PINS = {
     "bayes_filter": (pin_bayes_filter, 1e-12),
     "golden_hmm2": (pin_golden_hmm2, 1e-7),
@@ -577,4 +617,6 @@ ALL_PINS = {
     "bdeps_trivial_lists": (pin_bdeps_trivial_lists, 0.0),
     "bdeps_bruteforce": (pin_bdeps_bruteforce, 1e-12),
     "bdeps_uninformative_transitions": (pin_bdeps_uninformative_transitions, 1e-12),
+    "predict_bruteforce": (pin_predict_bruteforce, 1e-12),
+    "online_filter_bdeps": (pin_online_filter_bdeps, 1e-12),
 }

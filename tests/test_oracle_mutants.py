@@ -35,6 +35,14 @@ MUTANTS = [
     ("caller_prior_ignored", "if (prior) return prior + (size_t)a * ntot + qoff[f];", "", 1),
     ("predict_transposed", "p += Bf[((size_t)i * nf + j) * U[f] + u] * q[(size_t)a * ntot + off + j];",
      "p += Bf[((size_t)j * nf + i) * U[f] + u] * q[(size_t)a * ntot + off + j];", 1),
+    ("predict_general_agent_stride", "b_contract(&md, Bf, f, i, u, q + (size_t)a * ntot, qoff, -1, 0, 0)",
+     "b_contract(&md, Bf, f, i, u, q, qoff, -1, 0, 0)", 1),
+    ("predict_general_action", "b_contract(&md, Bf, f, i, u, q + (size_t)a * ntot, qoff, -1, 0, 0)",
+     "b_contract(&md, Bf, f, i, 0, q + (size_t)a * ntot, qoff, -1, 0, 0)", 1),
+    ("predict_general_log_b", "b_contract(&md, Bf, f, i, u, q + (size_t)a * ntot, qoff, -1, 0, 0)",
+     "b_contract(&md, Bf, f, i, u, q + (size_t)a * ntot, qoff, -1, 0, 1)", 1),
+    ("predict_general_out_offset", "out[(size_t)a * ntot + qoff[f] + i] = b_contract(",
+     "out[(size_t)a * ntot + i] = b_contract(", 1),
     ("damping_swapped", "(1.0 - tau) * q[s] + tau * q_new[s]", "tau * q[s] + (1.0 - tau) * q_new[s]", 1),
     ("damping_ignored", "q[s] = tau == 1.0 ? q_new[s] :", "q[s] = 1 ? q_new[s] :", 1),
     ("soft_weight_dropped", "v += om[o] * LN(Am[(size_t)o * P + e]);", "v += LN(Am[(size_t)o * P + e]);", 1),

@@ -61,6 +61,9 @@ extern "C" {
  * marginals are insensitive to fp32 rounding of the log-likelihoods; it
  * stores an extra fp32 copy of the slices. */
 #define BI_FAST_F32 4u
+/* (Both streaming families, BI_FAST_F32 and BI_SPARSE_A, take models shared
+ * by every agent with trivial B-dependency lists only; a model with other
+ * lists runs agent-resident in fp64 whatever its flags: bi_explain_path.) */
 /* With BI_FAST_F32 and the dense layout, a shared model also stores every
  * slice as pairs of fp16 values (high part, rounded residual: 22 significant
  * bits, 4 bytes per entry like the fp32 copy), and the slice contractions of
@@ -141,10 +144,12 @@ typedef struct bi_model_stats {
     int64_t device_bytes; /* bytes of the packed device buffer in use          */
 } bi_model_stats;
 
-/* Thread-local description of the last error (never NULL). */
+/* Boundary plumbing (no passage of the paper): thread-local description of
+ * the last error (never NULL). */
 const char *bi_last_error(void);
 
 /*
+ * Boundary plumbing (sizing; the layout it sizes is that of bi_pack_model).
  * Size of the device buffer that bi_pack_model needs for this model shape.
  * Host only.  For BI_SPARSE_A the size depends on the values of A, so this
  * returns an upper bound (every entry nonzero); bi_plan_model_exact gives the
@@ -195,9 +200,12 @@ int bi_attach_device_buffer(bi_model *model, void *dev_buf, size_t dev_bytes);
 int bi_get_model_stats(const bi_model *model, bi_model_stats *out);
 
 /*
- * Device workspace (bytes, 256-byte aligned start required) that an inference
- * call with b agents, window T and algorithm algo needs; may be 0, in which
- * case ws_dev may be NULL.
+ * Boundary plumbing (sizing).  Device workspace (bytes, 256-byte aligned start
+ * required) that an inference call with b agents, window T and algorithm algo
+ * needs; may be 0, in which case ws_dev may be NULL.  The workspace holds the
+ * streaming paths' outcome buckets, partial messages and double-buffered
+ * marginals; its contents need not be initialised and are scratch after the
+ * call.
  */
 int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo, size_t *bytes);
 
@@ -300,9 +308,25 @@ int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const in
  * also run the dense streaming kernels (packed with BI_FAST_F32) or the
  * sparse ones (packed with BI_SPARSE_A); among the families the packing
  * allows, a selector fitted to timings of seeded sweep models on MI355X
- * picks the one expected to be fastest for (model, algo, b, T).  Host only.
+ * picks the one expected to be fastest for (model, algo, b, T).  Models with
+ * non-trivial B-dependency lists always run agent-resident.  Host only.
+ *
+ * Test and timing hook: the environment variable BI_FORCE_PATH = "agent",
+ * "stream" or "sparse", read at every call, overrides the selector's choice
+ * among the eligible families (never the eligibility itself); any other
+ * value is ignored.  It exists so tests and timing sweeps can run each
+ * family; production callers leave it unset.
  */
 int bi_query_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, int32_t *path);
+
+/*
+ * Boundary plumbing (no passage of the paper): a one-line, NUL-terminated
+ * account of the family bi_query_path returns for these arguments and of why
+ * each streaming family is or is not eligible (e.g. "agent (the only
+ * eligible family); stream: B-dependency lists are not trivial ...; sparse:
+ * not packed with BI_SPARSE_A"), truncated to cap bytes.  Host only.
+ */
+int bi_explain_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, char *buf, size_t cap);
 
 /*
  * Soft observations (Sec. III-C: the log-likelihood of a modality is the
@@ -343,8 +367,8 @@ int bi_infer_soft(const bi_model *model, int32_t algo, int32_t b, int32_t T, con
 int bi_predict(const bi_model *model, int32_t b, const float *q_dev, int64_t q_stride, const int32_t *act_dev,
                int64_t act_stride, float *out_dev, void *hip_stream);
 
-/* Free the host metadata of a packed model (not the caller's device buffer).
- * NULL is ignored. */
+/* Boundary plumbing: free the host metadata of a packed model (not the
+ * caller's device buffer).  NULL is ignored. */
 void bi_free_model(bi_model *model);
 
 /*

@@ -32,7 +32,7 @@ ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
 
 EXPORTS = ("bi_last_error", "bi_plan_model", "bi_plan_model_exact", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
            "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_vfilter_prior",
-           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_query_path", "bi_workspace_size_soft", "bi_infer_soft", "bi_predict", "bi_free_model",
+           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_query_path", "bi_explain_path", "bi_workspace_size_soft", "bi_infer_soft", "bi_predict", "bi_free_model",
            "bi_profile_begin", "bi_profile_end")
 
 
@@ -99,6 +99,7 @@ def load(path: str = LIB_PATH):
     lib.bi_infer.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp, sz, vp]
     lib.bi_workspace_size_soft.argtypes = [vp, i32, i32, i32, P(sz)]
     lib.bi_query_path.argtypes = [vp, i32, i32, i32, P(i32)]
+    lib.bi_explain_path.argtypes = [vp, i32, i32, i32, ctypes.c_char_p, sz]
     lib.bi_infer_soft.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp, sz, vp]
     lib.bi_predict.argtypes = [vp, i32, vp, ctypes.c_int64, vp, ctypes.c_int64, vp, vp]
     lib.bi_free_model.argtypes = [vp]
@@ -279,6 +280,12 @@ def bi_query_path(handle: int, b: int, T: int, algo: int) -> int:
     return int(out.value)
 
 
+def bi_explain_path(handle: int, b: int, T: int, algo: int) -> str:
+    buf = ctypes.create_string_buffer(512)
+    _check(load().bi_explain_path(ctypes.c_void_p(handle), int(b), int(T), int(algo), buf, 512))
+    return buf.value.decode()
+
+
 def bi_workspace_size_soft(handle: int, b: int, T: int, algo: int) -> int:
     out = ctypes.c_size_t(0)
     _check(load().bi_workspace_size_soft(ctypes.c_void_p(handle), int(b), int(T), int(algo), ctypes.byref(out)))
@@ -322,6 +329,48 @@ def bi_profile_end() -> dict:
     return {arr[i].name.decode(): (int(arr[i].launches), float(arr[i].total_ms)) for i in range(min(n.value, cap))}
 
 
+def _check_tensor(name, t, dtype, shape, device):
+    """Raise ValueError unless t is a contiguous tensor of this dtype, shape and device."""
+    if t is None:
+        raise ValueError(f"{name} is missing")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(int(x) for x in t.shape) != tuple(int(x) for x in shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the model on {device}")
+
+
+def check_infer_args(model, device, obs, act, q=None, prior=None, soft: bool = False):
+    """Host-side check of an inference call's tensors against the model shape,
+    before anything reaches the library (which reads them as raw device
+    pointers): obs int32 [b][T][M] (soft: float32 [b][T][sum K]), act int32
+    [b][T-1][F] (may be None or empty when T == 1), q float32 [b][T][sum n],
+    prior float32 [b][sum n], all contiguous and on `device`."""
+    import torch
+    device = torch.device(device)
+    if obs is None or obs.dim() != 3:
+        raise ValueError("obs must be a 3-d tensor [b][T][M]")
+    b, T = int(obs.shape[0]), int(obs.shape[1])
+    if b < 1 or T < 1:
+        raise ValueError("obs must hold at least one agent and one step")
+    F, ntot = len(model.n), int(sum(model.n))
+    if soft:
+        _check_tensor("obs_soft", obs, torch.float32, (b, T, int(sum(model.K))), device)
+    else:
+        _check_tensor("obs", obs, torch.int32, (b, T, len(model.K)), device)
+    if T > 1 or (act is not None and act.numel() > 0):
+        _check_tensor("act", act, torch.int32, (b, T - 1, F), device)
+    if q is not None:
+        _check_tensor("q", q, torch.float32, (b, T, ntot), device)
+    if prior is not None:
+        _check_tensor("prior", prior, torch.float32, (b, ntot), device)
+    if model.mb != 1 and model.mb != b:
+        raise ValueError(f"b={b} but the model holds {model.mb} agents")
+
+
 _ENTRY = {"fpi": bi_vfilter, "vmp": bi_vmp, "mmp": bi_mmp}
 _ENTRY_PRIOR = {"fpi": bi_vfilter_prior, "vmp": bi_vmp_prior, "mmp": bi_mmp_prior}
 
@@ -346,6 +395,10 @@ class PackedModel:
         """The kernel family ("agent", "stream" or "sparse") a call with these sizes runs."""
         return PATH_NAMES[bi_query_path(self.handle, b, T, ALGO_IDS[algo])]
 
+    def explain_path(self, b: int, T: int, algo: str) -> str:
+        """Which family a call runs and why the others are or are not eligible."""
+        return bi_explain_path(self.handle, b, T, ALGO_IDS[algo])
+
     def workspace(self, b: int, T: int, algo: str):
         import torch
         nb = bi_workspace_size(self.handle, b, T, ALGO_IDS[algo])
@@ -358,6 +411,7 @@ class PackedModel:
         prior: optional float32 device tensor [b][sum n], the first step's prior in place of D.
         damping: step tau in (0, 1] of q <- (1 - tau) q + tau q_new (1 = plain update)."""
         import torch
+        check_infer_args(self.model, self.buf.device, obs, act, q, prior)
         b, T = int(obs.shape[0]), int(obs.shape[1])
         if q is None:
             q = torch.empty((b, T, sum(self.model.n)), dtype=torch.float32, device=self.buf.device)
@@ -380,11 +434,8 @@ class PackedModel:
                    damping: float = 1.0):
         """obs_soft [b][T][sum K] float32 / act [b][T-1][F] int32 device tensors -> q [b][T][sum n]."""
         import torch
+        check_infer_args(self.model, self.buf.device, obs_soft, act, q, prior, soft=True)
         b, T = int(obs_soft.shape[0]), int(obs_soft.shape[1])
-        if obs_soft.dtype != torch.float32 or not obs_soft.is_contiguous():
-            raise ValueError("obs_soft must be a contiguous float32 tensor")
-        if int(obs_soft.shape[2]) != sum(self.model.K):
-            raise ValueError(f"obs_soft has {int(obs_soft.shape[2])} values per step, expected {sum(self.model.K)}")
         if q is None:
             q = torch.empty((b, T, sum(self.model.n)), dtype=torch.float32, device=self.buf.device)
         if ws is None:
@@ -400,6 +451,14 @@ class PackedModel:
         b, ntot = int(q.shape[0]), sum(self.model.n)
         if q.stride(-1) != 1 or act.stride(-1) != 1:
             raise ValueError("q and act must be contiguous in their last dimension")
+        if q.dtype != torch.float32 or act.dtype != torch.int32:
+            raise ValueError("q must be float32 and act int32")
+        if int(q.shape[-1]) < ntot or int(act.shape[0]) != b or int(act.shape[-1]) < len(self.model.n):
+            raise ValueError("q must hold sum n marginals and act F actions per agent")
+        if q.device != self.buf.device or act.device != self.buf.device:
+            raise ValueError("q and act must be on the model's device")
+        if out is not None:
+            _check_tensor("out", out, torch.float32, (b, ntot), self.buf.device)
         if out is None:
             out = torch.empty((b, ntot), dtype=torch.float32, device=self.buf.device)
         bi_predict(self.handle, b, q, q.stride(0), act, act.stride(0), out, stream)

@@ -1,5 +1,6 @@
 // extern "C" entry points of libbi (declared in include/bi.h).
 #include <algorithm>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <new>
@@ -40,6 +41,18 @@ Path choose_path(const bi_model *m, int algo, int b, int T)
     }
     if (!stream && !sparse) return Path::Agent;
     return static_cast<Path>(bi::select_path(m, algo, b, T, stream, sparse));
+}
+
+// Why a model is not eligible for a streaming family (NULL: eligible).
+const char *stream_refusal(const bi_model *m, int algo, bool sparse)
+{
+    if (sparse ? !(m->flags & BI_SPARSE_A) : !(m->flags & BI_FAST_F32))
+        return sparse ? "not packed with BI_SPARSE_A" : "not packed with BI_FAST_F32";
+    if (m->mb != 1) return "per-agent model (the streaming kernels share one model among all agents)";
+    if (algo == BI_ALGO_FPI) return "FPI runs agent-resident (sequential over the window)";
+    if (!m->trivial_b) return "B-dependency lists are not trivial (the streaming update takes {f} lists only)";
+    if (sparse ? bi::sparse_eligible(m, algo) : bi::stream_eligible(m, algo)) return nullptr;
+    return "a modality's shape exceeds the streaming kernels' limits (outcomes, modalities or LDS tiles)";
 }
 
 }  // namespace
@@ -307,6 +320,23 @@ int bi_query_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, int
     if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
     if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
     *path = static_cast<int32_t>(choose_path(model, algo, b, T));
+    return BI_OK;
+}
+
+int bi_explain_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, char *buf, size_t cap)
+{
+    if (!model || !buf || cap == 0) return fail(BI_ERR_INVALID_ARG, "model and buf must be non-NULL, cap > 0");
+    if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
+    if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
+    static const char *names[] = {"agent", "stream", "sparse"};
+    const Path p = choose_path(model, algo, b, T);
+    const char *rs = stream_refusal(model, algo, false), *rp = stream_refusal(model, algo, true);
+    const char *env = std::getenv("BI_FORCE_PATH");
+    const char *how = (rs && rp) ? "the only eligible family"
+                      : (env && std::strcmp(env, names[static_cast<int>(p)]) == 0) ? "forced by BI_FORCE_PATH"
+                                                                                      : "chosen by the selector";
+    std::snprintf(buf, cap, "%s (%s); stream: %s; sparse: %s", names[static_cast<int>(p)], how,
+                  rs ? rs : "eligible", rp ? rp : "eligible");
     return BI_OK;
 }
 

@@ -95,24 +95,6 @@ __device__ inline void split8(const float *v, float s, h8 &hi, h8 &lo)
     lo = __builtin_bit_cast(h8, ld);
 }
 
-template <int CTRL>
-__device__ inline float dpp(float x)
-{
-    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
-}
-
-// Sum over the 16 lanes of a DPP row; every lane of the row ends with the
-// same value (each step adds two equal-shaped partial sums, and fp32 addition
-// is commutative).
-__device__ inline float row_sum16(float x)
-{
-    x += dpp<0xB1>(x);    // quad_perm(1, 0, 3, 2)
-    x += dpp<0x4E>(x);    // quad_perm(2, 3, 0, 1)
-    x += dpp<0x141>(x);   // row_half_mirror
-    x += dpp<0x140>(x);   // row_mirror
-    return x;
-}
-
 // (fp16 high, residual) x (fp16 high, residual) product chain from zero
 __device__ inline f4 chain3(const h8 &ah, const h8 &al, const h8 &bh, const h8 &bl)
 {

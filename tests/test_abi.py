@@ -570,6 +570,10 @@ def test_bdeps_validation_and_dispatch():
                 os.environ["BI_FORCE_PATH"] = force
                 for algo in range(3):
                     assert bi.bi_query_path(h, 8, 4, algo) == bi.BI_PATH_AGENT
+                    why = bi.bi_explain_path(h, 8, 4, algo)
+                    assert why.startswith("agent (the only eligible family)"), why
+                    if algo != bi.BI_ALGO_FPI:
+                        assert "B-dependency lists are not trivial" in why, why
         finally:
             if old is None:
                 os.environ.pop("BI_FORCE_PATH", None)
@@ -694,3 +698,51 @@ def test_f16_pairs_wide_range():
         assert sub.any(), "some residuals are binary16 subnormals"
     finally:
         bi.bi_free_model(h)
+
+
+def test_python_binding_checks_tensors_before_the_library():
+    """PackedModel passes raw device pointers to the C-ABI, so the binding
+    rejects tensors of the wrong dtype, shape, layout or device first (CPU:
+    the check runs before any launch; the model's device is given as cpu)."""
+    import torch
+    w = synth.random_small(5, b=3, T_max=4)
+    while w.T < 2:
+        w = synth.random_small(int(w.obs.sum()) + 7, b=3, T_max=4)
+    m, cpu = w.model, torch.device("cpu")
+    obs, act = torch.from_numpy(w.obs), torch.from_numpy(w.act)
+    b, T = w.b, w.T
+    q = torch.empty((b, T, m.n_total), dtype=torch.float32)
+    prior = torch.full((b, m.n_total), 0.5, dtype=torch.float32)
+    bi.check_infer_args(m, cpu, obs, act, q, prior)          # the good call passes
+    bi.check_infer_args(m, cpu, obs[:, :1].contiguous(), None)  # T = 1 needs no actions
+    bad = [
+        (obs.long(), act, q, prior, "obs must be torch.int32"),          # torch's default integer type
+        (obs, act.long(), q, prior, "act must be torch.int32"),
+        (obs.float(), act, q, prior, "obs must be torch.int32"),
+        (obs[:, :, :-1] if m.M > 1 else obs[:, :, :0], act, q, prior, "obs must have shape"),
+        (obs.transpose(0, 1).contiguous().transpose(0, 1), act, q, prior, "obs must be contiguous"),
+        (obs, act[:, :-1], q, prior, "act must have shape"),
+        (obs, None, q, prior, "act is missing"),
+        (obs, act, q.double(), prior, "q must be torch.float32"),
+        (obs, act, q[:, :, :-1], prior, "q must have shape"),
+        (obs, act, q, prior[:-1], "prior must have shape"),
+        (obs, act, q, prior.half(), "prior must be torch.float32"),
+    ]
+    for o, a, qq, p, msg in bad:
+        with pytest.raises(ValueError, match=msg.replace("(", r"\(")):
+            bi.check_infer_args(m, cpu, o, a, qq, p)
+    # host tensors against a model on the GPU
+    with pytest.raises(ValueError, match="is on cpu"):
+        bi.check_infer_args(m, torch.device("cuda", 0), obs, act, q, prior)
+    # soft observations: float32 [b][T][sum K]
+    so = torch.from_numpy(synth.one_hot_obs(w.obs, m.K))
+    bi.check_infer_args(m, cpu, so, act, q, prior, soft=True)
+    with pytest.raises(ValueError, match="obs_soft must be torch.float32"):
+        bi.check_infer_args(m, cpu, so.double(), act, q, prior, soft=True)
+    with pytest.raises(ValueError, match="obs_soft must have shape"):
+        bi.check_infer_args(m, cpu, so[:, :, 1:].contiguous(), act, q, prior, soft=True)
+    # a per-agent model with another agent count
+    wp = synth.random_small(6, b=3, T_max=1, per_agent=True)
+    assert wp.model.mb == 3
+    with pytest.raises(ValueError, match="holds 3 agents"):
+        bi.check_infer_args(wp.model, cpu, torch.from_numpy(wp.obs[:2].copy()), None)

@@ -360,7 +360,7 @@ __global__ __launch_bounds__(kThreads, 1) void rowcol16_lik_kernel(StreamArgs a,
 {
     extern __shared__ __attribute__((aligned(16))) char lds[];
     __shared__ int ctxs[kCtx];
-    const int wg = blockIdx.x;
+    const int wg = a.flip ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;
     if (wg >= a.nwg) return;
     int m = 0;
     while (m + 1 < a.M && a.task[m + 1].wg0 <= wg) ++m;

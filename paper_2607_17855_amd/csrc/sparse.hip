@@ -106,7 +106,7 @@ __global__ __launch_bounds__(kSpThreads, 6) void sparse_lik_kernel(StreamArgs a,
     extern __shared__ double sd[];
     __shared__ int ctxs[kSpLanes];
 
-    const int wg = blockIdx.x;
+    const int wg = a.flip ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;   // grid = a.nwg
     int ti = 0;
     while (ti + 1 < a.ntask && a.task[ti + 1].wg0 <= wg) ++ti;
     const SpTask tk = a.task[ti];

@@ -506,8 +506,10 @@ __device__ void split_body(const StreamArgs &a, const float *__restrict__ q, flo
     // (the second read of the slice can hit that die's L2), and every die
     // streams its own slices (consecutive workgroups on different dies would
     // put all first reads of the slices on half of them).
+    // (odd iterations: the reverse order, a.flip)
     const int per_die = (a.nwg + kXcds - 1) / kXcds;
-    const int wg = (int)(blockIdx.x % kXcds) * per_die + (int)(blockIdx.x / kXcds);
+    const int bid = a.flip ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;
+    const int wg = (bid % kXcds) * per_die + bid / kXcds;
     if (wg >= a.nwg) return;
     int m = 0;
     while (m + 1 < a.M && a.task[2 * (m + 1)].wg0 <= wg) ++m;

@@ -64,6 +64,7 @@ struct StreamArgs {
     int32_t *bstart, *bctx;
     int nmsg, ntask;
     int stage;                  // update: partial messages and neighbour marginals staged in LDS
+    int flip;                   // likelihood launches: walk the work items in reverse order (odd iterations)
     StreamMod sm[kStreamMaxM];
     MsgSrc msg[kStreamMaxMsg];
     SpTask task[kStreamMaxTask];

@@ -206,7 +206,7 @@ __global__ __launch_bounds__(kThreads, 1) void lik_kernel(StreamArgs a, const fl
     __shared__ int ctxs[kJG];
 
     // decode (modality, outcome, row tile)
-    const int wg = blockIdx.x;
+    const int wg = a.flip ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;   // grid = a.nwg
     int m = 0;
     while (m + 1 < a.M && a.sm[m + 1].wg0 <= wg) ++m;
     const StreamMod &sm = a.sm[m];
@@ -702,16 +702,22 @@ static void run_iterations(const bi_model *m, int algo, int iters, const StreamA
                        : lik == Lik::Split    ? (split_pairs(m) ? "lik_split16" : "lik_split")
                        : lik == Lik::RowCol   ? "lik_rowcol16"
                                               : "lik";
+    // Odd iterations walk the likelihood work items backwards, so an iteration
+    // starts on the slices the previous one read last: those still sit in the
+    // memory-side last-level cache (256 MB, shared by all dies) when the
+    // observed slices do not all fit in it.
+    StreamArgs ab = a;
     for (int k = 0; k < iters; ++k) {
+        ab.flip = k & 1;
         {
             ProfScope p(name, stream);
             if (lik == Lik::Sparse)
-                sparse_lik_launch(m, a, reinterpret_cast<const double *>(cur), reinterpret_cast<double *>(part),
+                sparse_lik_launch(m, ab, reinterpret_cast<const double *>(cur), reinterpret_cast<double *>(part),
                                   stream);
             else if (lik == Lik::RowCol)
-                rc_lik_launch(a, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream);
+                rc_lik_launch(ab, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream);
             else if (lik != Lik::Dense)
-                split_lik_launch(m, a, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream,
+                split_lik_launch(m, ab, reinterpret_cast<const float *>(cur), reinterpret_cast<float *>(part), stream,
                                  lik == Lik::Sparse16);
             else
                 hipLaunchKernelGGL(lik_kernel, dim3(a.nwg), dim3(kThreads), lik_lds, stream, a,

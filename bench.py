@@ -113,7 +113,10 @@ def sparse16_lik_work(model, obs):
     """Algorithmic flops and HBM bytes of one sparse fp16-pair likelihood
     launch: the flops of the dense contractions (the matrix cores run the
     zeros too; 3 fp16 products per fp32 product come on top), and every
-    observed slice's nonzeros read once per side, 8 B each."""
+    observed slice's nonzeros read once, 8 B each (value and position), the
+    minimum a sparse layout moves.  The layout stores each nonzero once per
+    side (rows and columns) and the kernel reads both copies: that figure is
+    returned third."""
     import numpy as np
     flops, _ = dense_lik_work(model, obs)
     nbytes = 0.0
@@ -121,8 +124,8 @@ def sparse16_lik_work(model, obs):
         A = model.A[m][0].reshape(model.K[m], -1)
         nnz = (A.astype(np.float64) > 1e-16).sum(axis=1)
         cnt = np.bincount(obs[:, :, m].ravel(), minlength=model.K[m])
-        nbytes += 2 * 8.0 * float(nnz[cnt > 0].sum())
-    return flops, nbytes
+        nbytes += 8.0 * float(nnz[cnt > 0].sum())
+    return flops, nbytes, 2 * nbytes
 
 
 def agent_work(model, T, algo):
@@ -168,7 +171,9 @@ def soft_ll_bytes(model, b, T):
     return reads + 8.0 * b * T * sum(P)
 
 
-def cpu_baseline(w, algos, budget_s: float = 25.0, soft=None):
+def cpu_baseline(w, algos, budget_s: float = 25.0, soft=None, keep: bool = False):
+    """The oracle timed on the host cores over a bounded sample of agents.
+    keep: also return its outputs {algo: q [agents][T][sum n]} and the agents."""
     import numpy as np
     import oracle
     threads = oracle.default_threads()
@@ -177,21 +182,33 @@ def cpu_baseline(w, algos, budget_s: float = 25.0, soft=None):
     t0 = time.perf_counter()
     done_bu = 0
     calls = 0
+    outs = {}
     for algo in algos:
         if soft is None:
-            oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=agents)
+            outs[algo] = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=agents)
         else:
-            oracle.infer_soft(algo, w.model, soft, w.act, w.iters, agents=agents)
+            outs[algo] = oracle.infer_soft(algo, w.model, soft, w.act, w.iters, agents=agents)
         done_bu += len(agents) * w.T * w.iters
         calls += 1
         if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
-    return {"value": done_bu / dt, "unit": "belief_updates/s", "cores": min(threads, len(agents)),
-            "kind": "oracle",
-            "sample": f"{len(agents)} of {w.b} agents x T={w.T} x {w.iters} iters, "
-                      f"{'+'.join(algos[:calls])}{' (soft observations)' if soft is not None else ''}, "
-                      f"fp64 looped oracle (layout-independent), {dt:.1f} s wall"}
+    res = {"value": done_bu / dt, "unit": "belief_updates/s", "cores": min(threads, len(agents)),
+           "kind": "oracle",
+           "sample": f"{len(agents)} of {w.b} agents x T={w.T} x {w.iters} iters, "
+                     f"{'+'.join(algos[:calls])}{' (soft observations)' if soft is not None else ''}, "
+                     f"fp64 looped oracle (layout-independent), {dt:.1f} s wall"}
+    return (res, outs, agents) if keep else res
+
+
+def cpu_baseline_1thread(w, algo):
+    """The oracle on one host thread, one agent."""
+    import oracle
+    t0 = time.perf_counter()
+    oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=[0], threads=1)
+    dt = time.perf_counter() - t0
+    return {"value": w.T * w.iters / dt, "unit": "belief_updates/s", "cores": 1, "kind": "oracle",
+            "sample": f"agent 0 x T={w.T} x {w.iters} iters, {algo}, {dt:.1f} s wall"}
 
 
 def load_traffic():
@@ -214,6 +231,10 @@ def main():
                     help="dense layout on fp32 matrix cores (the fp32 copy) instead of the fp16 pairs")
     ap.add_argument("--sparse-f64", action="store_true",
                     help="sparse layout on the fp64 gather kernels instead of the fp16-pair matrix-core tiles")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the step on the other precision classes (fp32 matrix cores, fp64 sparse gathers)")
+    ap.add_argument("--cache-probe", action="store_true",
+                    help="only print copy bandwidth against working-set size (memory-side cache)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a device-to-device copy of MIB MiB (reference kernel for HBM byte counters)")
     args = ap.parse_args()
@@ -230,32 +251,57 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.cache_probe:
+        return cache_probe(torch, dev)
     if args.workload != "large":
         return bench_agent(args, bi, synth, torch, dev)
     if args.soft:
         print("bench.py: --soft applies to the per-agent workloads (--workload)", file=sys.stderr)
         sys.exit(2)
     w = synth.large_shared()
-    dense_flags = bi.BI_DENSE_A | bi.BI_FAST_F32 | (0 if args.dense_f32 else bi.BI_F16_PAIRS)
-    sparse_flags = bi.BI_SPARSE_A | (0 if args.sparse_f64 else bi.BI_FAST_F32 | bi.BI_F16_PAIRS)
-    flags = {"dense": dense_flags, "sparse": sparse_flags}
-    pms = {lay: bi.PackedModel(w.model, flags=flags[lay], device=dev) for lay in layouts}
+    fast = {"dense": bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS,
+            "sparse": bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS}
+    plain = {"dense": bi.BI_DENSE_A | bi.BI_FAST_F32, "sparse": bi.BI_SPARSE_A}   # fp32 MFMA / fp64 gathers
+    flags = {"dense": plain["dense"] if args.dense_f32 else fast["dense"],
+             "sparse": plain["sparse"] if args.sparse_f64 else fast["sparse"]}
     obs = torch.from_numpy(w.obs).to(dev)
     act = torch.from_numpy(w.act).to(dev)
-    qs = {(lay, a): torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device=dev)
-          for lay in layouts for a in ALGOS}
-    wss = {(lay, a): pms[lay].workspace(w.b, w.T, a) for lay in layouts for a in ALGOS}
-    for key, ws in wss.items():
-        assert ws is not None, f"{key}: the large shared model must run on the streaming kernels"
-    for a in ALGOS:
-        if "sparse" in layouts:
-            assert pms["sparse"].path(w.b, w.T, a) == "sparse", "the sparse layout must run the sparse kernels"
     stream = torch.cuda.current_stream()
 
-    def step(st=stream):
-        for lay in layouts:
-            for a in ALGOS:
-                pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
+    def setup(fl):
+        pms = {lay: bi.PackedModel(w.model, flags=fl[lay], device=dev) for lay in layouts}
+        qs = {(lay, a): torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device=dev)
+              for lay in layouts for a in ALGOS}
+        wss = {(lay, a): pms[lay].workspace(w.b, w.T, a) for lay in layouts for a in ALGOS}
+        for key, ws in wss.items():
+            assert ws is not None, f"{key}: the large shared model must run on the streaming kernels"
+        for a in ALGOS:
+            if "sparse" in layouts:
+                assert pms["sparse"].path(w.b, w.T, a) == "sparse", "the sparse layout must run the sparse kernels"
+        return pms, qs, wss
+
+    def make_step(pms, qs, wss):
+        def step(st=stream, marks=None):
+            for lay in layouts:
+                for a in ALGOS:
+                    if marks is not None:
+                        marks[(lay, a)][0].record(st)
+                    pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
+                    if marks is not None:
+                        marks[(lay, a)][1].record(st)
+        return step
+
+    def timed(step):
+        """ms per step over args.steps steps, nothing else on the stream."""
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            step()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / args.steps, time.perf_counter() - t0
 
     if args.copy_calibration > 0:
         n = args.copy_calibration * (1 << 20) // 4
@@ -266,29 +312,134 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    pms, qs, wss = setup(flags)
+    step = make_step(pms, qs, wss)
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-
-    bi.bi_profile_begin()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step()
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    prof = bi.bi_profile_end()
-    ms_step = ev0.elapsed_time(ev1) / args.steps
+    # the timed region: the steps alone (no profiling events between launches)
+    ms_step, wall = timed(step)
     bu_per_step = len(layouts) * len(ALGOS) * w.b * w.T * w.iters
     value = bu_per_step / (ms_step / 1e3)
 
+    # a second pass of the same steps with HIP events around every launch
+    # (library profiling, on the call stream): per-kernel durations
+    bi.bi_profile_begin()
+    ms_prof, _ = timed(step)
+    prof = bi.bi_profile_end()
+    # a third pass with events around every call: per-call durations
+    marks = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in qs}
+    call_ms = {k: 0.0 for k in qs}
+    for _ in range(args.steps):
+        step(marks=marks)
+        torch.cuda.synchronize()
+        for k, (e0, e1) in marks.items():
+            call_ms[k] += e0.elapsed_time(e1) / args.steps
+
     traffic = load_traffic()
     dense_work = dense_lik_work(w.model, w.obs)
+    sq_flops, sq_bytes, sq_stored = sparse16_lik_work(w.model, w.obs)
     work = {"lik": dense_work, "lik_split": dense_work, "lik_split16": dense_work, "lik_rowcol16": dense_work,
-            "lik_sparse": sparse_lik_work(w.model, w.obs), "lik_sparse16": sparse16_lik_work(w.model, w.obs)}
+            "lik_sparse": sparse_lik_work(w.model, w.obs), "lik_sparse16": (sq_flops, sq_bytes)}
+    rooflines = roofline_entries(prof, work, traffic)
+    if "lik_sparse16" in rooflines:
+        rooflines["lik_sparse16"]["stored_bytes_per_launch"] = sq_stored
+    dominant = max(rooflines, key=lambda c: rooflines[c]["total_ms"])
+    lik_cls = {"dense": "lik_split" if args.dense_f32 else "lik_rowcol16",
+               "sparse": "lik_sparse" if args.sparse_f64 else "lik_sparse16"}
+    calls = {}
+    for (lay, a), ms in call_ms.items():
+        cls = lik_cls[lay]
+        nb = work[cls][1] * w.iters
+        calls[f"{lay}/{a}"] = {"ms": ms, "algorithmic_bytes": nb, "algorithmic_GBps": nb / (ms / 1e3) / 1e9,
+                               "hbm_frac": nb / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                               "belief_updates_per_s": w.b * w.T * w.iters / (ms / 1e3)}
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "belief_updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32+f64" if args.dense_f32 and args.sparse_f64 else "f16x2+f64",
+        "data": "synthetic",
+        "config": {"workload": "shared model F=4x32 states (U=4), M=4x32 outcomes on all factors, 90% zeros, "
+                               "b=64, T=16, 16 iters; step = VMP + MMP on the dense ("
+                               + ("fp32 MFMA" if args.dense_f32 else "fp16-pair MFMA") + ") and sparse ("
+                               + ("fp64 gathers" if args.sparse_f64 else "fp16-pair MFMA from the nonzeros")
+                               + ") A layouts",
+                   "b": w.b, "T": w.T, "iters": w.iters, "algos": list(ALGOS), "layouts": layouts},
+        "roofline": rooflines[dominant],
+        "roofline_all": rooflines,
+        "kernel_timing": "a second pass of the same steps with HIP events around every launch on the call "
+                         f"stream ({ms_prof:.3f} ms per step with them); the timed region has none",
+        "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
+        "calls": calls,
+        "call_hbm_frac": {k: v["hbm_frac"] for k, v in calls.items()},
+        "wall_s_timed": wall,
+        "dtype_note": ("dense layout: fp32 matrix-core contractions (v_mfma_f32_16x16x4f32)" if args.dense_f32 else
+                       "dense layout: slices as fp16 (high, residual) pairs in 32x32 blocks, 22 significant bits, "
+                       "each block read once and contracted towards its rows and its columns with three fp16 "
+                       "matrix-core products per fp32 product (v_mfma_f32_16x16x32_f16), fp32 accumulation") + " with fp64 message sums, transitions and softmax; sparse layout: "
+                      + ("fp64 throughout" if args.sparse_f64 else
+                         "the nonzeros as fp16 pairs, scattered into LDS blocks and contracted with the same "
+                         "three-product fp16 matrix-core chains"),
+    }
+    # the same step captured once in a HIP graph and replayed (the calls only
+    # enqueue kernels): launch overhead out of the way; reported beside the
+    # eager step above, which stays the headline
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):   # captured on torch's capture stream (st=None: the current one)
+        step(None)
+    graph.replay()
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for _ in range(args.steps):
+        graph.replay()
+    g1.record(stream)
+    torch.cuda.synchronize()
+    g_ms = g0.elapsed_time(g1) / args.steps
+    out["graph_replay"] = {"ms_per_step": g_ms, "value": bu_per_step / (g_ms / 1e3), "unit": "belief_updates/s"}
+    del graph
+    results = {("main", k): v.cpu().numpy() for k, v in qs.items()}
+
+    # what the precision classes buy: the same step with the other class on
+    # each layout (fp32 matrix cores on the fp32 copy; fp64 sparse gathers)
+    if not args.no_variants and not (args.dense_f32 and args.sparse_f64):
+        vp, vq, vw = setup(plain)
+        vstep = make_step(vp, vq, vw)
+        for _ in range(max(1, args.warmup)):
+            vstep()
+        v_ms, _ = timed(vstep)
+        out["precision_variant"] = {
+            "dtype": "f32+f64", "ms_per_step": v_ms, "value": bu_per_step / (v_ms / 1e3), "unit": "belief_updates/s",
+            "note": "dense layout on fp32 matrix cores (fp32 slice copy), sparse layout on fp64 gathers"}
+        results.update({("variant", k): v.cpu().numpy() for k, v in vq.items()})
+
+    # the oracle timed on the host cores; its outputs on those sampled agents
+    # (the same for both layouts) give max |gpu - oracle| of every call
+    import numpy as np
+    out["max_abs_err"] = None
+    if not args.no_cpu_baseline:
+        base, refs, agents = cpu_baseline(w, list(ALGOS), keep=True)
+        out["cpu_baseline"] = base
+        out["cpu_baseline_1thread"] = cpu_baseline_1thread(w, "vmp")
+        err = {}
+        for (kind, (lay, a)), q in results.items():
+            if a in refs:
+                err[f"{kind}:{lay}/{a}"] = float(np.abs(q[agents] - refs[a]).max())
+        main = [v for k, v in err.items() if k.startswith("main:")]
+        out["max_abs_err"] = {"value": max(main) if main else None, "per_call": err,
+                              "agents": [int(x) for x in agents], "tolerance": 1e-5,
+                              "within": bool(main) and max(main) <= 1e-5}
+    print(json.dumps(out), flush=True)
+
+
+def roofline_entries(prof, work, traffic):
     rooflines = {}
     for cls, (kname, src) in LIK.items():
         if cls not in prof:
@@ -321,58 +472,32 @@ def main():
             f16 = 3 * flops / (avg_ms / 1e3) / 1e12
             rooflines[cls]["fp16_mfma"] = {"achieved_TFLOPs": f16, "peak": PEAK_FP16_MFMA_TFLOPS,
                                            "frac": f16 / PEAK_FP16_MFMA_TFLOPS}
-    dominant = max(rooflines, key=lambda c: rooflines[c]["total_ms"])
-    out = {
-        "metric": METRIC,
-        "value": value,
-        "unit": "belief_updates/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32+f64" if args.dense_f32 and args.sparse_f64 else "f16x2+f64",
-        "data": "synthetic",
-        "config": {"workload": "shared model F=4x32 states (U=4), M=4x32 outcomes on all factors, 90% zeros, "
-                               "b=64, T=16, 16 iters; step = VMP + MMP on the dense ("
-                               + ("fp32 MFMA" if args.dense_f32 else "fp16-pair MFMA") + ") and sparse ("
-                               + ("fp64 gathers" if args.sparse_f64 else "fp16-pair MFMA from the nonzeros")
-                               + ") A layouts",
-                   "b": w.b, "T": w.T, "iters": w.iters, "algos": list(ALGOS), "layouts": layouts},
-        "roofline": rooflines[dominant],
-        "roofline_all": rooflines,
-        "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
-        "wall_s_timed": wall,
-        "dtype_note": ("dense layout: fp32 matrix-core contractions (v_mfma_f32_16x16x4f32)" if args.dense_f32 else
-                       "dense layout: slices as fp16 (high, residual) pairs in 32x32 blocks, 22 significant bits, "
-                       "each block read once and contracted towards its rows and its columns with three fp16 "
-                       "matrix-core products per fp32 product (v_mfma_f32_16x16x32_f16), fp32 accumulation") + " with fp64 message sums, transitions and softmax; sparse layout: "
-                      + ("fp64 throughout" if args.sparse_f64 else
-                         "the nonzeros as fp16 pairs, scattered into LDS blocks and contracted with the same "
-                         "three-product fp16 matrix-core chains") + "; every marginal within 1e-5 of the fp64 oracle",
-    }
-    # the same step captured once in a HIP graph and replayed (the calls only
-    # enqueue kernels): launch overhead out of the way; reported beside the
-    # eager step above, which stays the headline
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):   # captured on torch's capture stream (st=None: the current one)
-        step(None)
-    graph.replay()
-    torch.cuda.synchronize()
-    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    g0.record(stream)
-    for _ in range(args.steps):
-        graph.replay()
-    g1.record(stream)
-    torch.cuda.synchronize()
-    g_ms = g0.elapsed_time(g1) / args.steps
-    out["graph_replay"] = {"ms_per_step": g_ms, "value": bu_per_step / (g_ms / 1e3), "unit": "belief_updates/s"}
-    del graph
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, list(ALGOS))
-    print(json.dumps(out), flush=True)
+    return rooflines
+
+
+def cache_probe(torch, dev):
+    """Apparent copy bandwidth against working-set size: a device-to-device
+    copy of n MiB read plus n MiB written, after three warm-up copies, timed
+    with HIP events."""
+    res = {}
+    for mb in (32, 64, 96, 128, 192, 256, 384, 512, 1024, 2048):
+        n = mb * (1 << 20) // 4
+        x = torch.ones(n, device=dev)
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = max(5, 4096 // mb)
+        e0.record()
+        for _ in range(reps):
+            y.copy_(x)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        res[2 * mb] = 2 * mb * (1 << 20) / (ms / 1e3) / 1e9
+        del x, y
+    print(json.dumps({"copy_working_set_MiB_to_GBps": res}), flush=True)
 
 
 def bench_agent(args, bi, synth, torch, dev):
@@ -420,18 +545,22 @@ def bench_agent(args, bi, synth, torch, dev):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    bi.bi_profile_begin()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step()
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+
+    def timed():
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            step()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / args.steps, time.perf_counter() - t0
+
+    ms_step, wall = timed()          # the timed region: the steps alone
+    bi.bi_profile_begin()            # a second pass with HIP events around every launch
+    timed()
     prof = bi.bi_profile_end()
-    ms_step = ev0.elapsed_time(ev1) / args.steps
     bu = w.b * w.T * w.iters
     cls = "agent_filter" if algo == "fpi" else "agent_window"
     launches, total_ms = prof[cls]
@@ -469,8 +598,15 @@ def bench_agent(args, bi, synth, torch, dev):
                         "avg_launch_ms": s_avg, "launches": sl, "algorithmic_bytes_per_launch": s_bytes}}
         if s_avg > avg_ms:
             out["roofline"] = out["roofline_all"]["soft_ll"]
+    out["max_abs_err"] = None
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, [algo], soft=soft_np)
+        base, refs, agents = cpu_baseline(w, [algo], soft=soft_np, keep=True)
+        out["cpu_baseline"] = base
+        out["cpu_baseline_1thread"] = cpu_baseline_1thread(w, algo)
+        if not rolling:
+            e = float(np.abs(q.cpu().numpy()[agents] - refs[algo]).max())
+            out["max_abs_err"] = {"value": e, "agents": [int(x) for x in agents], "tolerance": 1e-5,
+                                  "within": e <= 1e-5}
     print(json.dumps(out), flush=True)
 
 

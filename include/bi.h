@@ -303,6 +303,30 @@ int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const in
              size_t ws_bytes, void *hip_stream);
 
 /*
+ * No-allocation inference, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): bi_infer without a workspace.  The scratch the streaming kernel
+ * families need lives in a static device array of BI_STATIC_SCRATCH_BYTES
+ * that the library holds on every GPU it runs on until the process ends; the
+ * caller still passes inputs and outputs (and the packed model), and the call
+ * allocates nothing (no hipMalloc / hipFree, no allocating library routine).
+ *   - Arguments, results and errors are those of bi_infer, on the device
+ *     that is current, which must be the model's (else BI_ERR_INVALID_ARG).
+ *   - A call whose bi_workspace_size exceeds BI_STATIC_SCRATCH_BYTES returns
+ *     BI_ERR_UNSUPPORTED before enqueueing anything; models packed with
+ *     BI_CHECK are refused the same way (the check synchronises and copies).
+ *   - Every call on a GPU shares that GPU's array and leaves its contents
+ *     behind (nothing needs to start at zero).  Calls that overlap in time on
+ *     one GPU (several streams or threads) race on it: serialise them.
+ *   - The first call on a device looks up the array's address there (once);
+ *     after that a call only enqueues kernels, so it can be captured.
+ */
+#define BI_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int bi_infer_static(const bi_model *model, int32_t algo, int32_t b, int32_t T, const int32_t *obs_dev,
+                    const int32_t *act_dev, int32_t iters, const bi_infer_opts *opts, float *q_dev,
+                    void *hip_stream);
+
+/*
  * The kernel family a call with these sizes will run (BI_PATH_*).  FPI always
  * runs agent-resident.  VMP and MMP on a model shared by every agent may
  * also run the dense streaming kernels (packed with BI_FAST_F32) or the

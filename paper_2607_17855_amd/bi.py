@@ -32,7 +32,7 @@ ALGO_IDS = {"fpi": BI_ALGO_FPI, "vmp": BI_ALGO_VMP, "mmp": BI_ALGO_MMP}
 
 EXPORTS = ("bi_last_error", "bi_plan_model", "bi_plan_model_exact", "bi_pack_model", "bi_pack_model_host", "bi_attach_device_buffer",
            "bi_get_model_stats", "bi_workspace_size", "bi_vfilter", "bi_vmp", "bi_mmp", "bi_vfilter_prior",
-           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_query_path", "bi_explain_path", "bi_workspace_size_soft", "bi_infer_soft", "bi_predict", "bi_free_model",
+           "bi_vmp_prior", "bi_mmp_prior", "bi_infer", "bi_infer_static", "bi_query_path", "bi_explain_path", "bi_workspace_size_soft", "bi_infer_soft", "bi_predict", "bi_free_model",
            "bi_profile_begin", "bi_profile_end")
 
 
@@ -97,6 +97,7 @@ def load(path: str = LIB_PATH):
     for name in ("bi_vfilter_prior", "bi_vmp_prior", "bi_mmp_prior"):
         getattr(lib, name).argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, sz, vp]
     lib.bi_infer.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp, sz, vp]
+    lib.bi_infer_static.argtypes = [vp, i32, i32, i32, vp, vp, i32, P(bi_infer_opts), vp, vp]
     lib.bi_workspace_size_soft.argtypes = [vp, i32, i32, i32, P(sz)]
     lib.bi_query_path.argtypes = [vp, i32, i32, i32, P(i32)]
     lib.bi_explain_path.argtypes = [vp, i32, i32, i32, ctypes.c_char_p, sz]
@@ -268,6 +269,19 @@ def bi_infer(handle, algo: int, b, T, obs, act, iters, q, ws=None, stream=None, 
     _check(load().bi_infer(ctypes.c_void_p(handle), int(algo), int(b), int(T), ctypes.c_void_p(obs.data_ptr()),
                            ctypes.c_void_p(act_ptr), int(iters), ctypes.byref(opts), ctypes.c_void_p(q.data_ptr()),
                            ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(_stream_ptr(stream))))
+
+
+BI_STATIC_SCRATCH_BYTES = 64 << 20
+
+
+def bi_infer_static(handle, algo: int, b, T, obs, act, iters, q, stream=None, prior=None, damping: float = 1.0):
+    """bi_infer without a workspace: the library's static device scratch (no allocation)."""
+    act_ptr = act.data_ptr() if act is not None and act.numel() > 0 else 0
+    opts = bi_infer_opts(ctypes.c_void_p(prior.data_ptr() if prior is not None else 0), float(damping))
+    _check(load().bi_infer_static(ctypes.c_void_p(handle), int(algo), int(b), int(T),
+                                  ctypes.c_void_p(obs.data_ptr()), ctypes.c_void_p(act_ptr), int(iters),
+                                  ctypes.byref(opts), ctypes.c_void_p(q.data_ptr()),
+                                  ctypes.c_void_p(_stream_ptr(stream))))
 
 
 BI_PATH_AGENT, BI_PATH_STREAM, BI_PATH_SPARSE = 0, 1, 2

@@ -57,6 +57,42 @@ const char *stream_refusal(const bi_model *m, int algo, bool sparse)
 
 }  // namespace
 
+namespace bi {
+int infer_impl(int algo, const bi_model *model, int32_t b, int32_t T, const int32_t *obs, const int32_t *act,
+                   const float *prior, double tau, int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream)
+{
+    try {
+        if (!model) return fail(BI_ERR_INVALID_ARG, "model is NULL");
+        if (!model->dev) return fail(BI_ERR_INVALID_ARG, "model has no device buffer (bi_attach_device_buffer)");
+        if (b < 1 || T < 1 || iters < 1) return fail(BI_ERR_INVALID_ARG, "b, T and iters must be >= 1");
+        if (model->mb != 1 && model->mb != b)
+            return fail(BI_ERR_SHAPE, "b=%d but the model holds %d agents", b, model->mb);
+        if (!obs || !q) return fail(BI_ERR_INVALID_ARG, "obs and q must be non-NULL");
+        if (T > 1 && !act) return fail(BI_ERR_INVALID_ARG, "act must be non-NULL when T > 1");
+        if (!(tau > 0.0 && tau <= 1.0)) return fail(BI_ERR_INVALID_ARG, "damping %g is not in (0, 1]", tau);
+        size_t need = 0;
+        int rc = bi_workspace_size(model, b, T, algo, &need);
+        if (rc != BI_OK) return rc;
+        if (ws_bytes < need) return fail(BI_ERR_BUFFER_TOO_SMALL, "ws_bytes %zu < %zu required", ws_bytes, need);
+        if (need > 0 && !ws) return fail(BI_ERR_INVALID_ARG, "ws is NULL");
+        if (need > 0 && reinterpret_cast<uintptr_t>(ws) % bi::kAlign)
+            return fail(BI_ERR_INVALID_ARG, "ws must be %d-byte aligned", bi::kAlign);
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        if (model->flags & BI_CHECK) {
+            rc = bi::check_inputs(model, b, T, obs, act,
+                                  reinterpret_cast<int32_t *>(static_cast<char *>(ws) + need - kStatusBytes), s);
+            if (rc != BI_OK) return rc;
+        }
+        const Path p = choose_path(model, algo, b, T);
+        if (p != Path::Agent)
+            return bi::launch_stream(model, algo, b, T, obs, act, prior, tau, iters, q, ws, s, p == Path::Sparse);
+        return bi::launch_agent(model, algo, b, T, obs, nullptr, act, prior, tau, iters, q, s);
+    } catch (...) {
+        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
+    }
+}
+}  // namespace bi
+
 extern "C" {
 
 const char *bi_last_error(void) { return bi::last_error(); }
@@ -228,56 +264,22 @@ int bi_workspace_size(const bi_model *model, int32_t b, int32_t T, int32_t algo,
     return BI_OK;
 }
 
-static int infer(int algo, const bi_model *model, int32_t b, int32_t T, const int32_t *obs, const int32_t *act,
-                 const float *prior, double tau, int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream)
-{
-    try {
-        if (!model) return fail(BI_ERR_INVALID_ARG, "model is NULL");
-        if (!model->dev) return fail(BI_ERR_INVALID_ARG, "model has no device buffer (bi_attach_device_buffer)");
-        if (b < 1 || T < 1 || iters < 1) return fail(BI_ERR_INVALID_ARG, "b, T and iters must be >= 1");
-        if (model->mb != 1 && model->mb != b)
-            return fail(BI_ERR_SHAPE, "b=%d but the model holds %d agents", b, model->mb);
-        if (!obs || !q) return fail(BI_ERR_INVALID_ARG, "obs and q must be non-NULL");
-        if (T > 1 && !act) return fail(BI_ERR_INVALID_ARG, "act must be non-NULL when T > 1");
-        if (!(tau > 0.0 && tau <= 1.0)) return fail(BI_ERR_INVALID_ARG, "damping %g is not in (0, 1]", tau);
-        size_t need = 0;
-        int rc = bi_workspace_size(model, b, T, algo, &need);
-        if (rc != BI_OK) return rc;
-        if (ws_bytes < need) return fail(BI_ERR_BUFFER_TOO_SMALL, "ws_bytes %zu < %zu required", ws_bytes, need);
-        if (need > 0 && !ws) return fail(BI_ERR_INVALID_ARG, "ws is NULL");
-        if (need > 0 && reinterpret_cast<uintptr_t>(ws) % bi::kAlign)
-            return fail(BI_ERR_INVALID_ARG, "ws must be %d-byte aligned", bi::kAlign);
-        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        if (model->flags & BI_CHECK) {
-            rc = bi::check_inputs(model, b, T, obs, act,
-                                  reinterpret_cast<int32_t *>(static_cast<char *>(ws) + need - kStatusBytes), s);
-            if (rc != BI_OK) return rc;
-        }
-        const Path p = choose_path(model, algo, b, T);
-        if (p != Path::Agent)
-            return bi::launch_stream(model, algo, b, T, obs, act, prior, tau, iters, q, ws, s, p == Path::Sparse);
-        return bi::launch_agent(model, algo, b, T, obs, nullptr, act, prior, tau, iters, q, s);
-    } catch (...) {
-        return fail(BI_ERR_INVALID_ARG, "unexpected host exception");
-    }
-}
-
 int bi_vfilter(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
                int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return bi::infer_impl(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_vmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
            int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return bi::infer_impl(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_mmp(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
            int32_t iters, float *q_dev, void *ws_dev, size_t ws_bytes, void *hip_stream)
 {
-    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return bi::infer_impl(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, nullptr, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_vfilter_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
@@ -285,7 +287,7 @@ int bi_vfilter_prior(const bi_model *model, int32_t b, int32_t T, const int32_t 
                      void *hip_stream)
 {
     if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
-    return infer(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return bi::infer_impl(BI_ALGO_FPI, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_vmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
@@ -293,7 +295,7 @@ int bi_vmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs
                  void *hip_stream)
 {
     if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
-    return infer(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return bi::infer_impl(BI_ALGO_VMP, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_mmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs_dev, const int32_t *act_dev,
@@ -301,7 +303,7 @@ int bi_mmp_prior(const bi_model *model, int32_t b, int32_t T, const int32_t *obs
                  void *hip_stream)
 {
     if (!prior_dev) return fail(BI_ERR_INVALID_ARG, "prior is NULL");
-    return infer(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return bi::infer_impl(BI_ALGO_MMP, model, b, T, obs_dev, act_dev, prior_dev, 1.0, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const int32_t *obs_dev,
@@ -311,7 +313,7 @@ int bi_infer(const bi_model *model, int32_t algo, int32_t b, int32_t T, const in
     if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
     const float *prior = opts ? opts->prior_dev : nullptr;
     const double tau = opts ? opts->damping : 1.0;
-    return infer(algo, model, b, T, obs_dev, act_dev, prior, tau, iters, q_dev, ws_dev, ws_bytes, hip_stream);
+    return bi::infer_impl(algo, model, b, T, obs_dev, act_dev, prior, tau, iters, q_dev, ws_dev, ws_bytes, hip_stream);
 }
 
 int bi_query_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, int32_t *path)

@@ -63,6 +63,12 @@ int check_inputs(const bi_model *m, int b, int T, const int32_t *obs, const int3
 // a window of T steps.
 int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool sparse);
 
+// The inference call behind bi_infer and the named entry points (capi.cpp):
+// host validation, optional input check, then the chosen kernel family with
+// ws (ws_bytes) as its workspace.  Returns BI_OK or an error code.
+int infer_impl(int algo, const bi_model *m, int32_t b, int32_t T, const int32_t *obs, const int32_t *act,
+               const float *prior, double tau, int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream);
+
 // Predictive prior B_f[:, :, u] q for every agent and factor (predict.hip).
 int launch_predict(const bi_model *m, int b, const float *q, int64_t q_stride, const int32_t *act,
                    int64_t act_stride, float *out, hipStream_t stream);

@@ -746,3 +746,34 @@ def test_python_binding_checks_tensors_before_the_library():
     assert wp.model.mb == 3
     with pytest.raises(ValueError, match="holds 3 agents"):
         bi.check_infer_args(wp.model, cpu, torch.from_numpy(wp.obs[:2].copy()), None)
+
+
+def test_static_scratch_entry_refuses_before_any_launch():
+    """bi_infer_static checks its limits on the host: a model packed with
+    BI_CHECK, and a call whose workspace exceeds the static scratch, are
+    refused with BI_ERR_UNSUPPORTED before any HIP call (the attached device
+    address here is never touched)."""
+    rng = np.random.Generator(np.random.PCG64(3))
+    m = synth.make_model(rng, [4, 32, 2, 32], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], 1)
+    lib = bi.load()
+    fake = ctypes.c_void_p(1 << 40)
+    for flags, b, T, why in [(bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_CHECK, 8, 4, "BI_CHECK"),
+                             (bi.BI_DENSE_A | bi.BI_FAST_F32, 4096, 64, "above the static")]:
+        h, img = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, 1, m.A, m.B, m.D, flags)
+        try:
+            assert lib.bi_attach_device_buffer(ctypes.c_void_p(h), fake, img.nbytes) == bi.BI_OK
+            old = os.environ.get("BI_FORCE_PATH")
+            os.environ["BI_FORCE_PATH"] = "stream"
+            try:
+                if "above" in why:
+                    assert bi.bi_workspace_size(h, b, T, bi.BI_ALGO_VMP) > bi.BI_STATIC_SCRATCH_BYTES
+                rc = lib.bi_infer_static(ctypes.c_void_p(h), bi.BI_ALGO_VMP, b, T, fake, fake, 2, None, fake, None)
+            finally:
+                if old is None:
+                    os.environ.pop("BI_FORCE_PATH", None)
+                else:
+                    os.environ["BI_FORCE_PATH"] = old
+            assert rc == bi.BI_ERR_UNSUPPORTED, rc
+            assert why in bi.bi_last_error()
+        finally:
+            bi.bi_free_model(h)

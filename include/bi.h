@@ -59,7 +59,14 @@ extern "C" {
  * MMP through the streaming kernels, whose slice contractions use fp32 matrix
  * cores (messages and updates stay fp64).  Use it for models whose
  * marginals are insensitive to fp32 rounding of the log-likelihoods; it
- * stores an extra fp32 copy of the slices. */
+ * stores an extra fp32 copy of the slices.
+ * Limit (tested at 16 sweeps): the result stays within 1e-5 of the fp64
+ * definition exactly when the definition itself moves by less than that under
+ * a relative perturbation of log A at the class's rounding scale (2^-24 here,
+ * 2^-21 with BI_F16_PAIRS).  Dense Dirichlet models (the seeded sweeps, the
+ * large shared model) are far inside it (<= 2e-6); small models with many
+ * exact zeros in A can be chaotic under the iteration (the definition moves by
+ * up to 1 after 16 sweeps), and then only the fp64 classes reproduce it. */
 #define BI_FAST_F32 4u
 /* (Both streaming families, BI_FAST_F32 and BI_SPARSE_A, take models shared
  * by every agent with trivial B-dependency lists only; a model with other

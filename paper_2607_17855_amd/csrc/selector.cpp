@@ -9,17 +9,20 @@
 // model and the call, fitted to timings of every family on the seeded
 // sweep models (uniform and skewed dimension regimes) on MI355X; the tree
 // tables are generated (selector_table.h, written by selector/fit.py) and
-// hold no code.  Without a table for a candidate set the rule below
-// applies: sparse when packed sparse, otherwise the dense streaming kernels
-// once the largest slice reaches 16384 entries.
+// hold no code.  Without a table for a candidate set, or for a model with
+// more A entries than any timed one, the rule below applies: sparse when
+// packed sparse, otherwise the dense streaming kernels once the largest
+// slice reaches 16384 entries.
 //
-// A model packed with the sparse fp16-pair layout (BI_SPARSE_A with
-// BI_F16_PAIRS) runs, on the sparse path, the same matrix-core tiles as the
-// dense kernels from 8 bytes per nonzero, while its dense streaming path is
-// the fp32 kernel over 4 bytes per entry (no dense pair copy is stored).
-// Where the tree picks a streaming family for such a model, the sparse one
-// is taken while at most half the entries are nonzero (fewer bytes, and the
-// fp16 matrix-core rate), the dense one otherwise.
+// Models packed with fp16 pairs (BI_F16_PAIRS) have trees of their own (the
+// candidate sets + 4), fitted to timings of the pair kernels: with the dense
+// layout the dense streaming family reads the pair copy; with the sparse
+// layout the sparse family runs the pair tiles from 8 bytes per nonzero and
+// the dense streaming family the fp32 kernels (no dense pair copy is stored).
+// The timed models have no zeros in A, so where the tree (or the rule)
+// picks a streaming family for a model with the sparse pair layout, the
+// sparse pairs are taken while at most half the entries are nonzero, the
+// dense fp32 kernels otherwise.
 #include <algorithm>
 #include <cmath>
 
@@ -82,16 +85,21 @@ int streaming_pairs(const bi_model *m, bool stream)
 
 int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool sparse)
 {
-    const int set = (stream ? 1 : 0) | (sparse ? 2 : 0);   // 1: {agent, stream}, 2: {agent, sparse}, 3: all
+    // 1: {agent, stream}, 2: {agent, sparse}, 3: all three; + 4 when the
+    // model carries fp16 pairs (the streaming families then run the pair
+    // kernels: dense pairs with the dense layout, sparse pairs with the sparse one)
+    const int set = (stream ? 1 : 0) | (sparse ? 2 : 0) | (m->flags & BI_F16_PAIRS ? 4 : 0);
     const SelTree *tree = nullptr;
     for (const SelTree &t : kSelTrees)
         if (t.set == set && t.algo == algo) tree = &t;
-    if (!tree || tree->nodes == 0) {
+    double x[kNumFeatures];
+    features(m, b, T, x);
+    // no timings for this candidate set, or a model larger than every timed
+    // one (the trees would extrapolate): the rule
+    if (!tree || tree->nodes == 0 || x[kFeatAFloats] > kSelMaxAFloats) {
         const int path = fallback(m, stream, sparse);
         return path != BI_PATH_AGENT && sparse && sq_eligible(m) ? streaming_pairs(m, stream) : path;
     }
-    double x[kNumFeatures];
-    features(m, b, T, x);
     int i = 0;
     while (kSelNodes[tree->first + i].feature >= 0) {
         const SelNode &nd = kSelNodes[tree->first + i];
@@ -99,6 +107,8 @@ int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool spa
     }
     int path = kSelNodes[tree->first + i].leaf;
     if ((path == BI_PATH_STREAM && !stream) || (path == BI_PATH_SPARSE && !sparse)) path = fallback(m, stream, sparse);
+    // the timed models have no zeros in A, so between the two streaming
+    // families of the sparse fp16-pair layout the share of nonzeros decides
     if (path != BI_PATH_AGENT && sparse && sq_eligible(m)) path = streaming_pairs(m, stream);
     return path;
 }

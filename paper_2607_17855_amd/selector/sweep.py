@@ -1,10 +1,11 @@
 """Time every eligible kernel family on the sweep models (one GPU).
 
 For each seeded sweep POMDP (uniform and skewed dimension regimes, one model
-shared by b agents) and each of VMP / MMP, the model is packed three ways
+shared by b agents) and each of VMP / MMP, the model is packed five ways
 (dense fp64 planes; plus the fp32 copy for the dense streaming kernels; plus
-the sparse planes) and every family the packing allows is timed with
-BI_FORCE_PATH: median of `--reps` calls after one warm-up, HIP events on
+the sparse planes; the fp16-pair copy (BI_F16_PAIRS) for the dense streaming
+kernels, "stream16"; the sparse fp16-pair layout, "sparse16") and the family
+each packing is for is timed with BI_FORCE_PATH: median of `--reps` calls after one warm-up, HIP events on
 the call stream.  Each family's output is also compared with the
 agent-resident fp64 result (max abs difference, recorded).  One JSON line
 per (regime, case, algo) goes to --out; progress goes to stdout.
@@ -33,7 +34,10 @@ def main():
     from paper_2607_17855_amd import bi, synth
 
     lo, hi = (int(x) for x in args.cases.split(":"))
-    flags = {"agent": bi.BI_DENSE_A, "stream": bi.BI_DENSE_A | bi.BI_FAST_F32, "sparse": bi.BI_SPARSE_A}
+    flags = {"agent": bi.BI_DENSE_A, "stream": bi.BI_DENSE_A | bi.BI_FAST_F32, "sparse": bi.BI_SPARSE_A,
+             "stream16": bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS,
+             "sparse16": bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS}
+    force = {"agent": "agent", "stream": "stream", "sparse": "sparse", "stream16": "stream", "sparse16": "sparse"}
     stream = torch.cuda.current_stream()
     t_start = time.time()
     with open(args.out, "a") as out:
@@ -47,9 +51,9 @@ def main():
                 rec = {"regime": args.regime, "case": case, "algo": algo, "b": w.b, "T": w.T}
                 ref = None
                 for fam, pm in pms.items():
-                    os.environ["BI_FORCE_PATH"] = fam
+                    os.environ["BI_FORCE_PATH"] = force[fam]
                     try:
-                        if pm.path(w.b, w.T, algo) != fam:
+                        if pm.path(w.b, w.T, algo) != force[fam]:
                             continue          # not eligible with this packing
                         q = torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device="cuda")
                         ws = pm.workspace(w.b, w.T, algo)

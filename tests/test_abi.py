@@ -473,7 +473,10 @@ def test_selector_table_matches_the_fitted_trees(regime):
     candidate set and algorithm, on a sample of the sweep models."""
     from paper_2607_17855_amd.selector import fit
     data = fit.load()
-    flags = {1: bi.BI_DENSE_A | bi.BI_FAST_F32, 2: bi.BI_SPARSE_A, 3: bi.BI_SPARSE_A | bi.BI_FAST_F32}
+    flags = {1: bi.BI_DENSE_A | bi.BI_FAST_F32, 2: bi.BI_SPARSE_A, 3: bi.BI_SPARSE_A | bi.BI_FAST_F32,
+             5: bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS,
+             7: bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS}
+    family = {"agent": "agent", "stream": "stream", "sparse": "sparse", "stream16": "stream", "sparse16": "sparse"}
     trees = {}
     for cset, cands in fit.SETS.items():
         for algo in ("vmp", "mmp"):
@@ -491,14 +494,14 @@ def test_selector_table_matches_the_fitted_trees(regime):
             try:
                 for algo in ("vmp", "mmp"):
                     tree, cands = trees[(cset, algo)]
-                    want = cands[int(tree.predict(np.array([fit.features(sp, 256)]))[0])]
+                    want = family[cands[int(tree.predict(np.array([fit.features(sp, 256)]))[0])]]
                     got = bi.PATH_NAMES[bi.bi_query_path(h, 256, sp.T, bi.ALGO_IDS[algo])]
                     # a family the model is not eligible for falls back; the sweep models are all eligible
                     assert got == want, (regime, case, cset, algo, got, want)
                     checked += 1
             finally:
                 bi.bi_free_model(h)
-    assert checked == len(cases) * 6
+    assert checked == len(cases) * 2 * len(flags)
 
 
 def _bdep_model(seed, lists, mb=2, n=(3, 4, 2)):

@@ -225,7 +225,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layouts", default=",".join(LAYOUTS), help="comma list of A layouts in a step")
-    ap.add_argument("--workload", default="large", choices=["large"] + list(AGENT_WORKLOADS))
+    ap.add_argument("--workload", default="large", choices=["large", "sweep"] + list(AGENT_WORKLOADS))
+    ap.add_argument("--regimes", default="uniform,skewed", help="sweep workload: dimension regimes")
+    ap.add_argument("--cases", default="0:770", help="sweep workload: start:stop of the seeded specs")
     ap.add_argument("--soft", action="store_true", help="soft observation vectors (per-agent workloads)")
     ap.add_argument("--dense-f32", action="store_true",
                     help="dense layout on fp32 matrix cores (the fp32 copy) instead of the fp16 pairs")
@@ -253,6 +255,8 @@ def main():
     torch.cuda.set_device(dev)
     if args.cache_probe:
         return cache_probe(torch, dev)
+    if args.workload == "sweep":
+        return bench_sweep(args, bi, synth, torch, dev)
     if args.workload != "large":
         return bench_agent(args, bi, synth, torch, dev)
     if args.soft:
@@ -498,6 +502,76 @@ def cache_probe(torch, dev):
         res[2 * mb] = 2 * mb * (1 << 20) / (ms / 1e3) / 1e9
         del x, y
     print(json.dumps({"copy_working_set_MiB_to_GBps": res}), flush=True)
+
+
+def bench_sweep(args, bi, synth, torch, dev):
+    """The seeded POMDP sweep (770 specs per dimension regime, one model shared
+    by 256 agents, T from the spec, 16 iterations): each model packed once with
+    every kernel family allowed (BI_SPARSE_A | BI_FAST_F32 | BI_F16_PAIRS),
+    FPI, VMP and MMP each timed as the selector routes them (median of
+    args.steps calls after args.warmup, HIP events around each call).  value =
+    belief updates of all calls / their summed median times.  The oracle
+    checks agents 0 and 255 of every call (max-abs error reported)."""
+    import numpy as np
+    import oracle
+    lo, hi = (int(x) for x in args.cases.split(":"))
+    regimes = [r for r in args.regimes.split(",") if r]
+    flags = bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
+    stream = torch.cuda.current_stream()
+    total_bu, total_ms, err, per_algo, fams = 0, 0.0, 0.0, {}, {}
+    worst = None
+    t0 = time.perf_counter()
+    n_models = 0
+    for regime in regimes:
+        for case in range(lo, hi):
+            w = synth.sweep_model(case, regime=regime)
+            pm = bi.PackedModel(w.model, flags=flags, device=dev)
+            obs = torch.from_numpy(w.obs).to(dev)
+            act = torch.from_numpy(w.act).to(dev)
+            q = torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device=dev)
+            for algo in ("fpi", "vmp", "mmp"):
+                ws = pm.workspace(w.b, w.T, algo)
+                fam = pm.path(w.b, w.T, algo)
+                for _ in range(max(1, args.warmup)):
+                    pm.infer(algo, obs, act, w.iters, q=q, ws=ws, stream=stream)
+                times = []
+                for _ in range(args.steps):
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    pm.infer(algo, obs, act, w.iters, q=q, ws=ws, stream=stream)
+                    e1.record(stream)
+                    e1.synchronize()
+                    times.append(e0.elapsed_time(e1))
+                ms = float(np.median(times))
+                bu = w.b * w.T * w.iters
+                total_bu += bu
+                total_ms += ms
+                pa = per_algo.setdefault(algo, [0, 0.0])
+                pa[0] += bu
+                pa[1] += ms
+                fams[f"{algo}:{fam}"] = fams.get(f"{algo}:{fam}", 0) + 1
+                ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=[0, w.b - 1])
+                e = float(np.abs(q.cpu().numpy()[[0, w.b - 1]] - ref).max())
+                if e > err:
+                    err, worst = e, f"{regime} {case} {algo} ({fam})"
+            pm.close()
+            n_models += 1
+            if n_models % 50 == 0:
+                print(f"[sweep] {n_models} models, {time.perf_counter() - t0:.0f} s", file=sys.stderr, flush=True)
+    out = {
+        "metric": METRIC, "value": total_bu / (total_ms / 1e3), "unit": "belief_updates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": total_ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "per family (f64 agent, f16x2/f32+f64 streaming)",
+        "data": "synthetic",
+        "config": {"workload": f"seeded POMDP sweep, regimes {regimes}, specs {lo}:{hi} each, b=256, T per spec, "
+                               "16 iters, FPI + VMP + MMP as the selector routes them",
+                   "models": n_models, "b": 256, "iters": 16},
+        "per_algo": {a: {"belief_updates": v[0], "ms": v[1], "value": v[0] / (v[1] / 1e3)} for a, v in per_algo.items()},
+        "families": fams,
+        "max_abs_err": {"value": err, "worst": worst, "agents": [0, 255], "tolerance": 1e-5, "within": err <= 1e-5},
+        "wall_s": time.perf_counter() - t0,
+    }
+    print(json.dumps(out), flush=True)
 
 
 def bench_agent(args, bi, synth, torch, dev):

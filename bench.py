@@ -211,6 +211,14 @@ def cpu_baseline_1thread(w, algo):
             "sample": f"agent 0 x T={w.T} x {w.iters} iters, {algo}, {dt:.1f} s wall"}
 
 
+def load_agent_traffic():
+    path = os.path.join(ROOT, "profiles", "traffic_agent.json")
+    if not os.path.exists(path):
+        return {}
+    with open(path) as fh:
+        return json.load(fh)
+
+
 def load_traffic():
     if not os.path.exists(TRAFFIC_FILE):
         return {}
@@ -519,6 +527,7 @@ def bench_sweep(args, bi, synth, torch, dev):
     flags = bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
     stream = torch.cuda.current_stream()
     total_bu, total_ms, err, per_algo, fams = 0, 0.0, 0.0, {}, {}
+    orc_bu, orc_s = 0, 0.0
     worst = None
     t0 = time.perf_counter()
     n_models = 0
@@ -550,7 +559,10 @@ def bench_sweep(args, bi, synth, torch, dev):
                 pa[0] += bu
                 pa[1] += ms
                 fams[f"{algo}:{fam}"] = fams.get(f"{algo}:{fam}", 0) + 1
+                o0 = time.perf_counter()
                 ref = oracle.infer(algo, w.model, w.obs, w.act, w.iters, agents=[0, w.b - 1])
+                orc_s += time.perf_counter() - o0
+                orc_bu += 2 * w.T * w.iters
                 e = float(np.abs(q.cpu().numpy()[[0, w.b - 1]] - ref).max())
                 if e > err:
                     err, worst = e, f"{regime} {case} {algo} ({fam})"
@@ -571,6 +583,11 @@ def bench_sweep(args, bi, synth, torch, dev):
         "max_abs_err": {"value": err, "worst": worst, "agents": [0, 255], "tolerance": 1e-5, "within": err <= 1e-5},
         "wall_s": time.perf_counter() - t0,
     }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = {"value": orc_bu / max(orc_s, 1e-9), "unit": "belief_updates/s", "cores": 2,
+                               "kind": "oracle",
+                               "sample": f"agents 0 and 255 of every call ({orc_bu} belief updates, one thread per "
+                                         f"agent), {orc_s:.1f} s"}
     print(json.dumps(out), flush=True)
 
 
@@ -653,23 +670,37 @@ def bench_agent(args, bi, synth, torch, dev):
                                + (f", B-dependency lists {w.model.bdeps}" if w.model.bdeps else ""),
                    "b": w.b, "T": w.T, "iters": w.iters, "algos": [algo], "soft": soft_np is not None,
                    "rolling": rolling},
-        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP64_VALU_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP64_VALU_TFLOPS, "traffic": None, "kernel": cls + "_kernel",
-                     "avg_launch_ms": avg_ms, "launches": launches, "algorithmic_flops_per_launch": flops,
-                     "algorithmic_bytes_per_launch": nb * w.b * t_launch},
+        "roofline": None,
         "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},
         "wall_s_timed": wall,
     }
+    # Both rooflines of the agent kernel: the fp64 arithmetic, and the bytes
+    # of one read of the observed fp64 slices per belief update (its counted
+    # traffic from profiles/traffic_agent.json while the kernel source is
+    # unchanged).  The counters show the kernel waiting on memory, not on
+    # arithmetic; the headline roofline is the one it is closer to.
+    alg_bytes = nb * w.b * t_launch * w.iters
+    tr = load_agent_traffic().get(args.workload)
+    hbm = tr["hbm_bytes_per_launch"] if tr and tr.get("kernel_source_sha") == source_sha("agent.hip") else None
+    gbps = alg_bytes / (avg_ms / 1e3) / 1e9
+    out["roofline_all"] = {
+        "hbm": {"bound": "hbm", "achieved": gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": gbps / PEAK_HBM_GBPS,
+                "traffic": hbm, "kernel": cls + "_kernel", "avg_launch_ms": avg_ms, "launches": launches,
+                "algorithmic_bytes_per_launch": alg_bytes,
+                "measured_hbm_GBps": None if hbm is None else hbm / (avg_ms / 1e3) / 1e9},
+        "alu": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP64_VALU_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_FP64_VALU_TFLOPS, "traffic": hbm, "kernel": cls + "_kernel",
+                "avg_launch_ms": avg_ms, "launches": launches, "algorithmic_flops_per_launch": flops}}
+    out["roofline"] = max(out["roofline_all"].values(), key=lambda r: r["frac"])
     if soft_np is not None:
         sl, sms = prof["soft_ll"]
         s_avg = sms / max(sl, 1)
         s_bytes = soft_ll_bytes(w.model, w.b, w.T)
         s_ach = s_bytes / (s_avg / 1e3) / 1e9
-        out["roofline_all"] = {
-            cls: dict(out["roofline"]),
+        out["roofline_all"].update({
             "soft_ll": {"bound": "hbm", "achieved": s_ach, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                         "frac": s_ach / PEAK_HBM_GBPS, "traffic": None, "kernel": "soft_ll_kernel",
-                        "avg_launch_ms": s_avg, "launches": sl, "algorithmic_bytes_per_launch": s_bytes}}
+                        "avg_launch_ms": s_avg, "launches": sl, "algorithmic_bytes_per_launch": s_bytes}})
         if s_avg > avg_ms:
             out["roofline"] = out["roofline_all"]["soft_ll"]
     out["max_abs_err"] = None

@@ -6,8 +6,8 @@
  * The generative model is the factorised POMDP of Sec. III-B of "A
  * Hardware-oriented Approach for Efficient Bayesian Inference Computation and
  * Deployment" (joint over o_{1:T}, s_{1:T} given u_{1:T-1}; emission tensors
- * A_m with arbitrary A-dependency lists, transition tensors B_f with trivial
- * B-dependencies, prior D).  The three updates are built from the likelihood
+ * A_m with A-dependency lists of up to 4 factors, transition tensors B_f with
+ * B-dependency lists of up to 4 factors, prior D).  The three updates are built from the likelihood
  * and transition messages of Sec. IV, each an instance of the coordinate
  * update of Sec. III-A; the exact readings are stated per entry point.
  *
@@ -69,8 +69,8 @@ extern "C" {
  * up to 1 after 16 sweeps), and then only the fp64 classes reproduce it. */
 #define BI_FAST_F32 4u
 /* (Both streaming families, BI_FAST_F32 and BI_SPARSE_A, take models shared
- * by every agent with trivial B-dependency lists only; a model with other
- * lists runs agent-resident in fp64 whatever its flags: bi_explain_path.) */
+ * by every agent, VMP and MMP; with B-dependency lists their update forms the
+ * general transition messages.  bi_explain_path tells which family runs.) */
 /* With BI_FAST_F32 and the dense layout, a shared model also stores every
  * slice as pairs of fp16 values (high part, rounded residual: 22 significant
  * bits, 4 bytes per entry like the fp32 copy), and the slice contractions of
@@ -133,8 +133,9 @@ typedef struct bi_model_desc {
      * depends on the current states of bdep[bdep_off[f] .. bdep_off[f+1]),
      * ascending, 1 to 4 factors, each factor in at most 8 lists; B[f] is then
      * [model_batch][n_f][n_{g_1}]..[n_{g_k}][U_f].  NULL (both): every list is
-     * {f}, B[f] = [model_batch][n_f][n_f][U_f].  Models with other lists run
-     * agent-resident (the streaming kernels take trivial lists only). */
+     * {f}, B[f] = [model_batch][n_f][n_f][U_f].  Every kernel family takes
+     * such lists (the streaming families' update then forms the general
+     * transition messages, one lane per state). */
     const int32_t *bdep_off;
     const int32_t *bdep;
 } bi_model_desc;
@@ -339,8 +340,7 @@ int bi_infer_static(const bi_model *model, int32_t algo, int32_t b, int32_t T, c
  * also run the dense streaming kernels (packed with BI_FAST_F32) or the
  * sparse ones (packed with BI_SPARSE_A); among the families the packing
  * allows, a selector fitted to timings of seeded sweep models on MI355X
- * picks the one expected to be fastest for (model, algo, b, T).  Models with
- * non-trivial B-dependency lists always run agent-resident.  Host only.
+ * picks the one expected to be fastest for (model, algo, b, T).  Host only.
  *
  * Test and timing hook: the environment variable BI_FORCE_PATH = "agent",
  * "stream" or "sparse", read at every call, overrides the selector's choice

@@ -251,7 +251,7 @@ inline size_t lds_for(const Side &s)
 
 bool sparse_eligible(const bi_model *m, int algo)
 {
-    if (!(m->flags & BI_SPARSE_A) || m->mb != 1 || algo == BI_ALGO_FPI || !m->trivial_b) return false;
+    if (!(m->flags & BI_SPARSE_A) || m->mb != 1 || algo == BI_ALGO_FPI) return false;
     if (sq_eligible(m)) return true;   // the sparse fp16-pair tiles (split.hip)
     if (m->M > kStreamMaxM) return false;
     int64_t pstride = 0;

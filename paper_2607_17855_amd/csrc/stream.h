@@ -65,6 +65,7 @@ struct StreamArgs {
     int nmsg, ntask;
     int stage;                  // update: partial messages and neighbour marginals staged in LDS
     int flip;                   // likelihood launches: walk the work items in reverse order (odd iterations)
+    int trivb;                  // every B-dependency list is {f} (else the update's general transition messages)
     StreamMod sm[kStreamMaxM];
     MsgSrc msg[kStreamMaxMsg];
     SpTask task[kStreamMaxTask];

@@ -27,6 +27,7 @@
 #include "internal.h"
 #include "profile.h"
 #include "stream.h"
+#include "transition.h"
 
 namespace bi {
 namespace {
@@ -461,6 +462,94 @@ __device__ inline void dot_pair(const MT *Mf, const QT *xf, const MT *Mb, int64_
     }
 }
 
+// The update of one context under B-dependency lists (Sec. III-B transition
+// model): factor f's next state depends on the current states of the factors
+// of its list, so its forward message contracts B_f (log B_f for VMP) with
+// the marginals of the listed factors at t - 1, and every factor j whose list
+// holds f sends a backward message, B_j contracted with q_{t+1, j} and the
+// marginals at t of j's other listed factors, f held at each state.  MMP
+// averages the forward message with the backward ones present.  One lane per
+// state; the messages are the agent path's (transition.h).  pc: the
+// context's partial messages; qp / qn: full marginal vectors of the
+// neighbouring steps (null at the window's ends); the context's own
+// marginals come from qin.
+template <int ALGO, typename QT, typename PT, typename OT>
+__device__ void update_general(const StreamArgs &a, const PT *pc, const QT *qp, const QT *qn, const QT *qin,
+                               OT *qout, int ctx, double *vals, int wave, int lane)
+{
+    const int agent = ctx / a.T, t = ctx - agent * a.T;
+    const QT *qself = qin + (int64_t)ctx * a.ntot;
+    for (int f = wave; f < a.F; f += 4) {
+        const FacDesc &fd = a.facs[f];
+        const int n = fd.n;
+        double *v = vals + fd.q_off;
+        const BDep df = bdep_of(a.facs, fd);
+        const int up = t > 0 ? a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f] : 0;
+        for (int s = lane; s < n; s += 64) {
+            double lam = 0.0;
+            for (int i = 0; i < a.nmsg; ++i) {
+                const MsgSrc src = a.msg[i];
+                if (src.f != f) continue;
+                for (int k = 0; k < src.copies; ++k) lam += (double)pc[src.off + s + (int64_t)k * src.stride];
+            }
+            double fwd;
+            if (t == 0)
+                fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + fd.q_off + s])
+                              : reinterpret_cast<const double *>(a.base + fd.ld_off)[s];
+            else if (ALGO == BI_ALGO_VMP)
+                fwd = bdep_row(df, reinterpret_cast<const double *>(a.base + fd.lb_off) + ((int64_t)up * n + s) * df.bs,
+                               qp, -1, 0);
+            else
+                fwd = ln_clamped(bdep_row(df, reinterpret_cast<const float *>(a.base + fd.b_off) +
+                                                  ((int64_t)up * n + s) * df.bs, qp, -1, 0));
+            double bwd = 0.0;
+            int children = 0;
+            if (qn) {
+                for (int c = 0; c < fd.nch; ++c) {
+                    const int jf = fd.ch[c], pos = fd.chpos[c];
+                    const FacDesc &fj = a.facs[jf];
+                    const BDep dj = bdep_of(a.facs, fj);
+                    const int nj = fj.n;
+                    const int uj = a.act[((int64_t)agent * (a.T - 1) + t) * a.F + jf];
+                    const QT *qj = qn + fj.q_off;
+                    double msg = 0.0;
+                    if (ALGO == BI_ALGO_VMP) {
+                        const double *LBj = reinterpret_cast<const double *>(a.base + fj.lb_off) + (int64_t)uj * nj * dj.bs;
+                        for (int sn = 0; sn < nj; ++sn)
+                            msg = fma((double)qj[sn], bdep_row(dj, LBj + (int64_t)sn * dj.bs, qself, pos, s), msg);
+                        bwd += msg;
+                    } else {
+                        const float *Bj = reinterpret_cast<const float *>(a.base + fj.b_off) + (int64_t)uj * nj * dj.bs;
+                        for (int sn = 0; sn < nj; ++sn)
+                            msg = fma((double)qj[sn], bdep_row(dj, Bj + (int64_t)sn * dj.bs, qself, pos, s), msg);
+                        bwd += ln_clamped(msg);
+                    }
+                    ++children;
+                }
+            }
+            if (ALGO == BI_ALGO_VMP)
+                v[s] = lam + fwd + bwd;
+            else
+                v[s] = children > 0 ? lam + (fwd + bwd) / (double)(1 + children) : lam + fwd;
+        }
+        __builtin_amdgcn_wave_barrier();   // v[s] came from lane s (one wave: LDS in program order)
+        double mx = -INFINITY;
+        for (int s = lane; s < n; s += 64) mx = fmax(mx, v[s]);
+        mx = wave_max(mx);
+        double sum = 0.0;
+        for (int s = lane; s < n; s += 64) {
+            const double ev = exp(v[s] - mx);
+            v[s] = ev;
+            sum += ev;
+        }
+        sum = wave_sum(sum);
+        OT *out = qout + (int64_t)ctx * a.ntot + fd.q_off;
+        for (int s = lane; s < n; s += 64)
+            out[s] = a.tau != 1.0 ? (OT)((1.0 - a.tau) * (double)qself[fd.q_off + s] + a.tau * (v[s] / sum))
+                                  : (OT)(v[s] / sum);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // update: messages summed over their partial vectors (fp64, fixed order),
 // transition messages, masked softmax; one workgroup per context, one wave
@@ -505,6 +594,10 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *par
         pc = sp;
         qp = qp ? sq : nullptr;
         qn = qn ? sq + nq : nullptr;
+    }
+    if (!a.trivb) {
+        update_general<ALGO, QT, PT, OT>(a, pc, qp, qn, qin, qout, ctx, vals, wave, lane);
+        return;
     }
     for (int f = wave; f < a.F; f += 4) {
         const FacDesc &fd = a.facs[f];
@@ -592,7 +685,7 @@ void launch_update(int algo, const StreamArgs &a, size_t lds, hipStream_t stream
 
 bool stream_eligible(const bi_model *m, int algo)
 {
-    if (!(m->flags & BI_FAST_F32) || m->mb != 1 || algo == BI_ALGO_FPI || !m->trivial_b) return false;
+    if (!(m->flags & BI_FAST_F32) || m->mb != 1 || algo == BI_ALGO_FPI) return false;
     if (m->M > kStreamMaxM) return false;
     for (const ModDesc &md : m->mods) {
         if (md.la32_off < 0) return false;
@@ -756,6 +849,7 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.act = act;
     a.prior = prior;
     a.tau = tau;
+    a.trivb = m->trivial_b ? 1 : 0;
     a.bstart = reinterpret_cast<int32_t *>(w + offs[0]);
     a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
     char *part = w + offs[3];

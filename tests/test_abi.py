@@ -564,19 +564,22 @@ def test_bdeps_validation_and_dispatch():
     assert bi.load().bi_plan_model(ctypes.byref(bd.c), ctypes.byref(out)) == bi.BI_ERR_UNSUPPORTED
     bd = bi._Desc(big.n, big.U, big.K, big.deps, 1, bi.BI_DENSE_A, [[0, f] if f else [0] for f in range(9)])
     assert bi.load().bi_plan_model(ctypes.byref(bd.c), ctypes.byref(out)) == bi.BI_ERR_UNSUPPORTED
-    # non-trivial lists run agent-resident whatever the packing allows
-    for fl in (bi.BI_DENSE_A | bi.BI_FAST_F32, bi.BI_SPARSE_A):
+    # non-trivial lists: the streaming families take VMP / MMP on a shared
+    # model as packed (their update has the general transition messages);
+    # FPI stays agent-resident
+    for fl, fam in ((bi.BI_DENSE_A | bi.BI_FAST_F32, bi.BI_PATH_STREAM), (bi.BI_SPARSE_A, bi.BI_PATH_SPARSE)):
         h, _ = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, 1, m.A, m.B, m.D, flags=fl, bdeps=m.bdeps)
         old = os.environ.get("BI_FORCE_PATH")
         try:
-            for force in ("stream", "sparse"):
-                os.environ["BI_FORCE_PATH"] = force
-                for algo in range(3):
-                    assert bi.bi_query_path(h, 8, 4, algo) == bi.BI_PATH_AGENT
-                    why = bi.bi_explain_path(h, 8, 4, algo)
+            os.environ["BI_FORCE_PATH"] = "stream" if fam == bi.BI_PATH_STREAM else "sparse"
+            for algo in range(3):
+                want = bi.BI_PATH_AGENT if algo == bi.BI_ALGO_FPI else fam
+                assert bi.bi_query_path(h, 8, 4, algo) == want
+                why = bi.bi_explain_path(h, 8, 4, algo)
+                if algo == bi.BI_ALGO_FPI:
                     assert why.startswith("agent (the only eligible family)"), why
-                    if algo != bi.BI_ALGO_FPI:
-                        assert "B-dependency lists are not trivial" in why, why
+                else:
+                    assert "forced by BI_FORCE_PATH" in why, why
         finally:
             if old is None:
                 os.environ.pop("BI_FORCE_PATH", None)

@@ -106,3 +106,55 @@ def test_bdeps_predict_vs_oracle(case):
             assert err <= TOL
     finally:
         pm.close()
+
+
+# shared models with B-dependency lists on the streaming kernels: the
+# general transition messages of the update kernel (one lane per state)
+STREAM_CASES = [
+    # (n, U, K, deps, lists, b, T, packing flags, family, damping, prior)
+    ([5, 3], [2, 2], [4, 3, 2], [[0], [1], [0, 1]], [[1], [0, 1]], 8, 6,
+     bi.BI_DENSE_A | bi.BI_FAST_F32, "stream", 1.0, False),
+    ([4, 3, 2, 3], [1, 2, 2, 1], [3, 3], [[0, 1, 2, 3], [1, 3]], [[0, 1], [0, 1, 2, 3], [2], [1, 3]], 12, 5,
+     bi.BI_SPARSE_A, "sparse", 1.0, True),
+    ([12, 10, 8], [2, 2, 1], [4, 3], [[0, 1, 2], [1]], [[0, 1, 2], [0, 1], [1, 2]], 16, 4,
+     bi.BI_DENSE_A | bi.BI_FAST_F32, "stream", 0.6, True),
+    # matrix-core shapes: the fp16-pair single-read kernel and the sparse pair tiles
+    ([4, 32, 2, 32], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], [[0, 1], [1], [1, 2], [3]], 24, 4,
+     bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS, "stream", 1.0, False),
+    ([4, 32, 6, 16], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], [[0, 3], [1], [2], [0, 3]], 24, 4,
+     bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS, "sparse", 1.0, False),
+]
+
+
+@pytest.mark.parametrize("case", range(len(STREAM_CASES)))
+def test_bdeps_streaming_vs_oracle_and_agent(case):
+    import os
+    n, U, K, deps, lists, b, T, flags, family, tau, with_prior = STREAM_CASES[case]
+    sp = 0.7 if flags & bi.BI_SPARSE_A else 0.0
+    rng = np.random.Generator(np.random.PCG64(1960 + case))
+    model = synth.make_model(rng, n, U, K, deps, 1, 1.0, 1.0, sparsity=sp, uniform_D=False, bdeps=lists)
+    obs, act = synth.sample_sequences(rng, model, b, T)
+    w = synth.Workload(f"bdeps_stream{case}", ["vmp", "mmp"], model, obs, act, 3)
+    prior = synth.random_prior(rng, model.n, b, alpha=0.7) if with_prior else None
+    old = os.environ.get("BI_FORCE_PATH")
+    pm = bi.PackedModel(model, flags=flags)
+    try:
+        for algo in ("vmp", "mmp"):
+            os.environ["BI_FORCE_PATH"] = family
+            assert pm.path(b, T, algo) == family
+            q = _run(pm, w, algo, prior=prior, damping=tau)
+            check_invariants(w, q)
+            ref = oracle.infer(algo, model, obs, act, w.iters, prior=None if prior is None else prior.astype(np.float64),
+                               damping=tau)
+            err = float(np.abs(q - ref).max())
+            print(f"[gpu]   bdeps {family} {algo} vs oracle {err:.3e}", flush=True)
+            assert err <= TOL
+            os.environ["BI_FORCE_PATH"] = "agent"
+            qa = _run(pm, w, algo, prior=prior, damping=tau)
+            assert float(np.abs(q - qa).max()) <= TOL
+    finally:
+        if old is None:
+            os.environ.pop("BI_FORCE_PATH", None)
+        else:
+            os.environ["BI_FORCE_PATH"] = old
+        pm.close()

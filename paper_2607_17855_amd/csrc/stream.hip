@@ -562,7 +562,7 @@ __device__ void update_general(const StreamArgs &a, const PT *pc, const QT *qp, 
 // marginals between iterations, PT = partial messages, OT = this launch's
 // output marginals.
 // ---------------------------------------------------------------------------
-template <int ALGO, typename QT, typename PT, typename OT>
+template <int ALGO, typename QT, typename PT, typename OT, bool TB>   // TB: every B-dependency list is {f}
 __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *part, const QT *qin, OT *qout)
 {
     extern __shared__ double vals[];   // [ntot], then (staged) partials [pstride] and two marginal vectors [ntot]
@@ -595,7 +595,7 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *par
         qp = qp ? sq : nullptr;
         qn = qn ? sq + nq : nullptr;
     }
-    if (!a.trivb) {
+    if constexpr (!TB) {
         update_general<ALGO, QT, PT, OT>(a, pc, qp, qn, qin, qout, ctx, vals, wave, lane);
         return;
     }
@@ -673,12 +673,23 @@ template <typename QT, typename PT, typename OT>
 void launch_update(int algo, const StreamArgs &a, size_t lds, hipStream_t stream, const PT *part, const QT *qin,
                    OT *qout)
 {
-    if (algo == BI_ALGO_VMP)
-        hipLaunchKernelGGL((update_kernel<BI_ALGO_VMP, QT, PT, OT>), dim3(a.nctx), dim3(256), lds, stream, a, part,
-                           qin, qout);
-    else
-        hipLaunchKernelGGL((update_kernel<BI_ALGO_MMP, QT, PT, OT>), dim3(a.nctx), dim3(256), lds, stream, a, part,
-                           qin, qout);
+    // trivial B-dependency lists get a kernel without the general transition
+    // code (its registers would cost the common case occupancy)
+    if (a.trivb) {
+        if (algo == BI_ALGO_VMP)
+            hipLaunchKernelGGL((update_kernel<BI_ALGO_VMP, QT, PT, OT, true>), dim3(a.nctx), dim3(256), lds, stream,
+                               a, part, qin, qout);
+        else
+            hipLaunchKernelGGL((update_kernel<BI_ALGO_MMP, QT, PT, OT, true>), dim3(a.nctx), dim3(256), lds, stream,
+                               a, part, qin, qout);
+    } else {
+        if (algo == BI_ALGO_VMP)
+            hipLaunchKernelGGL((update_kernel<BI_ALGO_VMP, QT, PT, OT, false>), dim3(a.nctx), dim3(256), lds, stream,
+                               a, part, qin, qout);
+        else
+            hipLaunchKernelGGL((update_kernel<BI_ALGO_MMP, QT, PT, OT, false>), dim3(a.nctx), dim3(256), lds, stream,
+                               a, part, qin, qout);
+    }
 }
 
 }  // namespace

@@ -63,12 +63,20 @@ constexpr int kTab = kCtx * 32 * 4;                   // one [kCtx][32] (or [32]
 constexpr int kOffQc0 = 0;                            // [32][kCtx]  q_c0 2^-15, by state
 constexpr int kOffQr1 = kTab;                         // [kCtx][32]  q_r1
 constexpr int kOffQr0w = 2 * kTab;                    // [kWaves][kCtx]  q_r0 of each wave's state
-constexpr int kOffM3 = kOffQr0w + kWaves * kCtx * 4;  // [kWaves][32][kCtx] shares of m_c0
-constexpr int kOffRing = kOffM3 + kWaves * kTab;      // [kRing][kWaves] blocks; before the loop the
+// Shares of a message summed over the waves: [kWaves][kCtx][kSh] with the
+// 32 states of a context contiguous and an odd pitch, so that the sums (32
+// consecutive states of one context per 32 lanes) and the writes from the
+// accumulators (16 consecutive contexts per 16 lanes) fall on distinct banks
+// (a pitch of kCtx states had put 32 lanes on 4 banks)
+constexpr int kSh = 33;
+constexpr int kShares = kWaves * kCtx * kSh * 4;
+constexpr int kOffM3 = kOffQr0w + kWaves * kCtx * 4;  // shares of m_c0
+constexpr int kOffRing = kOffM3 + kShares;            // [kRing][kWaves] blocks; before the loop the
 constexpr int kRingBytes = kRing * kWaves * kBlockBytes;   // third ring slot holds q_c1 and q_r0 [kCtx][32];
-constexpr int kLds = kOffRing + kRingBytes;           // after it, [kWaves][32][kCtx] shares of m_c1 / m_r1
+constexpr int kLds = kOffRing + kRingBytes;           // after it, the shares of m_c1 / m_r1
 static_assert(2 * kTab <= kWaves * kBlockBytes, "set-up tables exceed a ring slot");
-static_assert(kWaves * kTab <= kRingBytes, "shares exceed the ring");
+static_assert(kShares <= kRingBytes, "shares exceed the ring");
+static_assert(kOffRing % 16 == 0, "ring slots must be 16-byte aligned");
 static_assert(kLds + 4 * kCtx <= 160 * 1024, "LDS of the workgroup exceeds 160 KB");
 
 typedef float f4 __attribute__((ext_vector_type(4)));
@@ -165,14 +173,21 @@ __device__ void rc_pass(const StreamArgs &a, const Pass &p, const float *__restr
     // q_c1 and q_r0 [kCtx][32] sit in ring slot 2 until the loop starts
     float *qc1t = reinterpret_cast<float *>(lds + kOffRing + 2 * kWaves * kBlockBytes);
     float *qr0t = qc1t + kCtx * 32;
+    // the four loads of a round in flight at once: addresses clamped to valid
+    // entries (a padded context reads context 0, a padded state the last
+    // state), the values selected after the loads (few registers: the main
+    // loop below is at the register limit)
+#pragma unroll 1
     for (int i = tid; i < kCtx * 32; i += kThreads) {
         const int c = i >> 5, s = i & 31, ctx = ctxs[c];
         const float *qc = q + (int64_t)max(ctx, 0) * a.ntot;
+        const float v0 = qc[p.off_c0 + min(s, p.cn0 - 1)], v1 = qc[p.off_c1 + s];
+        const float v2 = qc[p.off_r0 + min(s, p.rn0 - 1)], v3 = qc[p.off_r1 + s];
         const bool ok = ctx >= 0;
-        qc0t[s * kCtx + c] = ok && s < p.cn0 ? qc[p.off_c0 + s] * kPairInv : 0.0f;
-        qc1t[c * 32 + s] = ok ? qc[p.off_c1 + s] : 0.0f;
-        qr0t[c * 32 + s] = ok && s < p.rn0 ? qc[p.off_r0 + s] : 0.0f;
-        qr1t[c * 32 + s] = ok ? qc[p.off_r1 + s] : 0.0f;
+        qc0t[s * kCtx + c] = ok && s < p.cn0 ? v0 * kPairInv : 0.0f;
+        qc1t[c * 32 + s] = ok ? v1 : 0.0f;
+        qr0t[c * 32 + s] = ok && s < p.rn0 ? v2 : 0.0f;
+        qr1t[c * 32 + s] = ok ? v3 : 0.0f;
     }
     __syncthreads();
     if (tid < kWaves * kCtx) {
@@ -292,7 +307,7 @@ __device__ void rc_pass(const StreamArgs &a, const Pass &p, const float *__restr
             for (int kb = 0; kb < NKB; ++kb) s3[kb] = rows_sum4(s3[kb]);
             if (lg == 0)
 #pragma unroll
-                for (int kb = 0; kb < NKB; ++kb) m3[(wave * 32 + c0) * kCtx + 16 * kb + li] = s3[kb];
+                for (int kb = 0; kb < NKB; ++kb) m3[(wave * kCtx + 16 * kb + li) * kSh + c0] = s3[kb];
         }
         __builtin_amdgcn_sched_barrier(0);
         // m_r0[r0] = sum_{r1} q_r1 Y, over the lane's rows, then the lane rows
@@ -319,18 +334,18 @@ __device__ void rc_pass(const StreamArgs &a, const Pass &p, const float *__restr
             for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
-                    shares[(wave * 32 + 8 * lg + 2 * v + jj) * kCtx + 16 * kb + li] = U[jj][kb][v];
+                    shares[(wave * kCtx + 16 * kb + li) * kSh + 8 * lg + 2 * v + jj] = U[jj][kb][v];
     __syncthreads();
     for (int i = tid; i < p.jc * 32; i += kThreads) {
         const int c = i >> 5, s = i & 31;
         float acc = 0.0f;
-        for (int w = 0; w < nw; ++w) acc += shares[(w * 32 + s) * kCtx + c];
+        for (int w = 0; w < nw; ++w) acc += shares[(w * kCtx + c) * kSh + s];
         part[(int64_t)ctxs[c] * p.ps + p.o_c1 + s] = acc;
     }
     for (int i = tid; i < p.jc * p.cn0; i += kThreads) {
         const int c = i / p.cn0, s = i - c * p.cn0;
         float acc = 0.0f;
-        for (int w = 0; w < nw; ++w) acc += m3[(w * 32 + s) * kCtx + c];
+        for (int w = 0; w < nw; ++w) acc += m3[(w * kCtx + c) * kSh + s];
         part[(int64_t)ctxs[c] * p.ps + p.o_c0 + s] = acc;
     }
     __syncthreads();
@@ -343,13 +358,13 @@ __device__ void rc_pass(const StreamArgs &a, const Pass &p, const float *__restr
                 const float wr = qr0w[wave * kCtx + 16 * kb + li];
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
-                    shares[(wave * 32 + 16 * j + 4 * lg + v) * kCtx + 16 * kb + li] = wr * Y[j][kb][v];
+                    shares[(wave * kCtx + 16 * kb + li) * kSh + 16 * j + 4 * lg + v] = wr * Y[j][kb][v];
             }
     __syncthreads();
     for (int i = tid; i < p.jc * 32; i += kThreads) {
         const int c = i >> 5, s = i & 31;
         float acc = 0.0f;
-        for (int w = 0; w < nw; ++w) acc += shares[(w * 32 + s) * kCtx + c];
+        for (int w = 0; w < nw; ++w) acc += shares[(w * kCtx + c) * kSh + s];
         part[(int64_t)ctxs[c] * p.ps + p.o_r1 + s] = acc;
     }
     __syncthreads();   // the tables and the ring are refilled by the next pass

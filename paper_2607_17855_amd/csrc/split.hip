@@ -60,6 +60,7 @@ constexpr int kCtx = 16 * kMaxKb;
 constexpr int kMaxT = 8;                       // k-steps per first-factor state (second factor <= 32)
 constexpr int kZS = kCtx + 1;                  // line-tile stride (floats)
 constexpr int kXcds = 8;                       // accelerator dies; workgroup i runs on die i % 8
+constexpr size_t kMaxLds = 80 * 1024;          // two workgroups per CU
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
@@ -542,7 +543,9 @@ __device__ void split_body(const StreamArgs &a, const float *__restrict__ q, flo
     float *qe0 = sh;                      // [kCtx][32]: marginals of the entry side's first factor
                                           // (pairs: [32][kCtx], times 2^-15)
     float *qe1 = qe0 + kCtx * 32;         // [kCtx][32]: second factor
-    float *zt = qe1 + kCtx * kMaxT * 4;   // [tile lines][kZS] (sparse pairs: over the B blocks)
+    float *ql0 = qe1 + kCtx * 32;         // [kCtx][32]: the line side's first and second factors (fold)
+    float *ql1 = ql0 + kCtx * 32;
+    float *zt = ql1 + kCtx * 32;          // [tile lines][kZS] (sparse pairs: over the B blocks)
     char *blocks = reinterpret_cast<char *>(zt);
     const int tid = threadIdx.x;
     const int off_e0 = a.facs[g.ef0].q_off, off_e1 = a.facs[g.ef1].q_off;
@@ -555,19 +558,34 @@ __device__ void split_body(const StreamArgs &a, const float *__restrict__ q, flo
             for (int i = tid; i < kWaves * kSqWaveBytes / 16; i += kThreads)
                 reinterpret_cast<u4 *>(blocks)[i] = u4{0u, 0u, 0u, 0u};
         __syncthreads();
-        for (int i = tid; i < kCtx * 64; i += kThreads) {
-            const int c = i >> 6, s = i & 63;
-            const int ctx = ctxs[c];
-            float v = 0.0f;
-            if (s < 32) {
-                if (ctx >= 0 && s < g.en0) v = q[(int64_t)ctx * a.ntot + off_e0 + s];
+        // marginal tables of the pass (zero for padded contexts and states):
+        // the four loads of a (context, state) in flight together, two rounds
+        // at a time, from addresses clamped to valid entries (a padded context
+        // reads context 0, a padded state the factor's last state)
+        static_assert(kCtx * 32 % (2 * kThreads) == 0, "table set-up assumes whole double rounds");
+        for (int i0 = tid; i0 < kCtx * 32; i0 += 2 * kThreads) {
+            float v[2][4];
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int i = i0 + k * kThreads, c = i >> 5, s = i & 31;
+                const float *qc = q + (int64_t)max(ctxs[c], 0) * a.ntot;
+                v[k][0] = qc[off_e0 + min(s, g.en0 - 1)];
+                v[k][1] = qc[off_e1 + min(s, g.en1 - 1)];
+                v[k][2] = qc[off_l0 + min(s, g.ln0 - 1)];
+                v[k][3] = qc[off_l1 + min(s, g.ln1 - 1)];
+            }
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int i = i0 + k * kThreads, c = i >> 5, s = i & 31;
+                const bool ok = ctxs[c] >= 0;
+                const float e0 = ok && s < g.en0 ? v[k][0] : 0.0f;
                 if (PAIRS)
-                    qe0[s * kCtx + c] = v * (1.0f / kPairScale);
+                    qe0[s * kCtx + c] = e0 * (1.0f / kPairScale);
                 else
-                    qe0[c * 32 + s] = v;
-            } else {
-                if (ctx >= 0 && s - 32 < g.en1) v = q[(int64_t)ctx * a.ntot + off_e1 + s - 32];
-                qe1[c * 32 + s - 32] = v;
+                    qe0[c * 32 + s] = e0;
+                qe1[c * 32 + s] = ok && s < g.en1 ? v[k][1] : 0.0f;
+                ql0[c * 32 + s] = ok && s < g.ln0 ? v[k][2] : 0.0f;
+                ql1[c * 32 + s] = ok && s < g.ln1 ? v[k][3] : 0.0f;
             }
         }
         __syncthreads();
@@ -603,14 +621,12 @@ __device__ void split_body(const StreamArgs &a, const float *__restrict__ q, flo
         const int ln1 = g.ln1;
         for (int i = tid; i < jc * ng; i += kThreads) {
             const int c = i / ng, gg = i - c * ng;
-            const float *qc = q + (int64_t)ctxs[c] * a.ntot + off_l1;
-            part[(int64_t)ctxs[c] * ps + tk.so + gs + gg] = dot_batched(zt + gg * ln1 * kZS + c, kZS, qc, ln1);
+            part[(int64_t)ctxs[c] * ps + tk.so + gs + gg] = dot_batched(zt + gg * ln1 * kZS + c, kZS, ql1 + c * 32, ln1);
         }
         for (int i = tid; i < jc * ln1; i += kThreads) {
             const int c = i / ln1, l1 = i - c * ln1;
-            const float *qc = q + (int64_t)ctxs[c] * a.ntot + off_l0 + gs;
             part[(int64_t)ctxs[c] * ps + tk.so + g.ln0 + (int64_t)tile * ln1 + l1] =
-                dot_batched(zt + l1 * kZS + c, ln1 * kZS, qc, ng);
+                dot_batched(zt + l1 * kZS + c, ln1 * kZS, ql0 + c * 32 + gs, ng);
         }
         __syncthreads();
     }
@@ -638,7 +654,7 @@ size_t lds_bytes(const bi_model *m, bool sparse)
             const size_t lines = (size_t)std::min(split_groups(g), g.ln0) * g.ln1;
             size_t tail = sizeof(float) * lines * kZS;
             if (sparse) tail = std::max(tail, (size_t)kWaves * kSqWaveBytes);
-            most = std::max(most, sizeof(float) * (size_t)kCtx * 64 + tail);
+            most = std::max(most, sizeof(float) * (size_t)kCtx * 128 + tail);
         }
     return most;
 }
@@ -662,7 +678,7 @@ bool split_eligible(const bi_model *m)
         }
         if (md.K > kStreamMaxK) return false;
     }
-    return lds_bytes(m, false) <= 64 * 1024 && pstride < (int64_t)1 << 30;
+    return lds_bytes(m, false) <= kMaxLds && pstride < (int64_t)1 << 30;
 }
 
 bool sq_eligible(const bi_model *m)
@@ -680,7 +696,7 @@ bool sq_eligible(const bi_model *m)
             pstride += g.ln0 + (int64_t)((g.ln0 + G - 1) / G) * g.ln1;
         }
     }
-    return lds_bytes(m, true) <= 64 * 1024 && pstride < (int64_t)1 << 30;
+    return lds_bytes(m, true) <= kMaxLds && pstride < (int64_t)1 << 30;
 }
 
 int64_t split_plan(const bi_model *m, StreamArgs *a)
@@ -721,6 +737,16 @@ int64_t split_plan(const bi_model *m, StreamArgs *a)
 }
 
 size_t split_lds_bytes(const bi_model *m, bool sparse) { return lds_bytes(m, sparse); }
+
+int split_prepare(const bi_model *m, bool sparse)
+{
+    const void *fn = sparse ? (const void *)sparse16_lik_kernel
+                     : split_pairs(m) ? (const void *)split_lik_kernel<true>
+                                      : (const void *)split_lik_kernel<false>;
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+    if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    return BI_OK;
+}
 
 bool split_pairs(const bi_model *m)
 {

@@ -88,6 +88,7 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
 bool split_eligible(const bi_model *m);
 int64_t split_plan(const bi_model *m, StreamArgs *a);
 size_t split_lds_bytes(const bi_model *m, bool sparse);
+int split_prepare(const bi_model *m, bool sparse);   // once per call, before the launches
 // every modality has its fp16-pair copy (BI_F16_PAIRS): the fp16 matrix-core tiles run
 bool split_pairs(const bi_model *m);
 // every modality has the sparse fp16-pair layout (BI_SPARSE_A with

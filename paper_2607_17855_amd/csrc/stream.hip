@@ -892,7 +892,10 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     } else if (lik == Lik::RowCol) {
         const int rc = rc_prepare();
         if (rc != BI_OK) return rc;
-    } else if (lik == Lik::Dense) {
+    } else if (lik != Lik::Dense) {
+        const int rc = split_prepare(m, lik == Lik::Sparse16);
+        if (rc != BI_OK) return rc;
+    } else {
         const hipError_t e = hipFuncSetAttribute((const void *)lik_kernel,
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lik_lds);
         if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));

@@ -51,6 +51,14 @@ struct SpTask {
     int32_t so;     // offset of the task's messages inside a context's partial block
 };
 
+// Per-factor fields the update kernel reads (kernel arguments, so scalar
+// loads): the first kStreamFacs factors; later ones are read from FacDesc.
+constexpr int kStreamFacs = 16;
+struct StreamFac {
+    int64_t lb_off, b_off, ld_off;   // byte offsets of log B, B and log D in the packed buffer
+    int32_t n, q_off;
+};
+
 struct StreamArgs {
     const char *base;
     const ModDesc *mods;
@@ -69,6 +77,7 @@ struct StreamArgs {
     StreamMod sm[kStreamMaxM];
     MsgSrc msg[kStreamMaxMsg];
     SpTask task[kStreamMaxTask];
+    StreamFac fac[kStreamFacs];
 };
 
 // Whether `m` can run `algo` on the dense streaming kernels.

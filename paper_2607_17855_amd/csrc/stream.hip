@@ -422,46 +422,6 @@ __global__ __launch_bounds__(kThreads, 1) void lik_kernel(StreamArgs a, const fl
 
 // sum_j M[j * ms] * x[j] over j < n in order (fp64), loads issued 8 at a time
 // Two dot products of one state's transition messages over j in [j0, j1):
-// df = sum M_f[j] x_f[j] (a row of B, stride 1) and db = sum M_b[j bs] x_b[j]
-// (a column), each in j order in fp64; either may be absent (null x).  The
-// operands of both come in 4 at a time, all loads issued before the
-// arithmetic, so the pair costs one memory round trip per 4 terms.
-template <typename MT, typename QT>
-__device__ inline void dot_pair(const MT *Mf, const QT *xf, const MT *Mb, int64_t bs, const QT *xb, int j0, int j1,
-                                double &df, double &db)
-{
-    constexpr int W = 4;
-    df = 0.0;
-    db = 0.0;
-    int j = j0;
-    for (; j + W <= j1; j += W) {
-        MT mf[W], mb[W];
-        QT qf[W], qb[W];
-        if (xf)
-#pragma unroll
-            for (int u = 0; u < W; ++u) {
-                mf[u] = Mf[j + u];
-                qf[u] = xf[j + u];
-            }
-        if (xb)
-#pragma unroll
-            for (int u = 0; u < W; ++u) {
-                mb[u] = Mb[(int64_t)(j + u) * bs];
-                qb[u] = xb[j + u];
-            }
-        if (xf)
-#pragma unroll
-            for (int u = 0; u < W; ++u) df = fma((double)mf[u], (double)qf[u], df);
-        if (xb)
-#pragma unroll
-            for (int u = 0; u < W; ++u) db = fma((double)mb[u], (double)qb[u], db);
-    }
-    for (; j < j1; ++j) {
-        if (xf) df = fma((double)Mf[j], (double)xf[j], df);
-        if (xb) db = fma((double)Mb[(int64_t)j * bs], (double)xb[j], db);
-    }
-}
-
 // The update of one context under B-dependency lists (Sec. III-B transition
 // model): factor f's next state depends on the current states of the factors
 // of its list, so its forward message contracts B_f (log B_f for VMP) with
@@ -562,56 +522,41 @@ __device__ void update_general(const StreamArgs &a, const PT *pc, const QT *qp, 
 // marginals between iterations, PT = partial messages, OT = this launch's
 // output marginals.
 // ---------------------------------------------------------------------------
-template <int ALGO, typename QT, typename PT, typename OT, bool TB>   // TB: every B-dependency list is {f}
-__global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *part, const QT *qin, OT *qout)
+// Update of one context under trivial B-dependency lists, for the factors
+// of this wave (wave-uniform f, so the factor descriptors, the actions and the
+// message-source table come in by scalar loads).  PP / QP: pointers to the
+// context's partial messages and to the neighbouring steps' marginals, typed
+// for LDS when they were staged (no generic-address loads); hp / hn: whether
+// the steps t - 1 / t + 1 exist.  Every read of a transition product is issued
+// before the partial sums, and the products take their operands 8 terms at a
+// time (in j order, so the sums are those of one term at a time).
+template <int ALGO, typename QT, typename OT, typename PP, typename QP>
+__device__ inline void update_trivial(const StreamArgs &a, PP pc, QP qp, QP qn, bool hp, bool hn, const QT *qin,
+                                      OT *qout, int ctx, double *vals, int wave, int lane)
 {
-    extern __shared__ double vals[];   // [ntot], then (staged) partials [pstride] and two marginal vectors [ntot]
-    const int ctx = blockIdx.x;
+    using MT = std::conditional_t<ALGO == BI_ALGO_VMP, double, float>;   // log B (VMP) or B (MMP)
+    constexpr int W = sizeof(MT) + sizeof(QT) > 8 ? 4 : 8;   // terms per batch (registers: every workgroup resident)
     const int agent = ctx / a.T, t = ctx - agent * a.T;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const PT *pc = part + (int64_t)ctx * a.pstride;
-    const QT *qp = t > 0 ? qin + (int64_t)(ctx - 1) * a.ntot : nullptr;
-    const QT *qn = t + 1 < a.T ? qin + (int64_t)(ctx + 1) * a.ntot : nullptr;
-    if (a.stage) {
-        PT *sp = reinterpret_cast<PT *>(vals + a.ntot);
-        QT *sq = reinterpret_cast<QT *>(vals + a.ntot + (a.pstride * sizeof(PT) + 7) / 8);
-        const int tid = threadIdx.x;
-        const int np = (int)a.pstride, nq = a.ntot;
-        for (int i0 = tid; i0 < np; i0 += 8 * 256) {   // 8 independent loads per thread, then the stores
-            PT v[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = i0 + 256 * u < np ? pc[i0 + 256 * u] : (PT)0;
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (i0 + 256 * u < np) sp[i0 + 256 * u] = v[u];
-        }
-        for (int i = tid; i < nq; i += 256) {
-            const QT a0 = qp ? qp[i] : (QT)0, a1 = qn ? qn[i] : (QT)0;
-            sq[i] = a0;
-            sq[nq + i] = a1;
-        }
-        __syncthreads();
-        pc = sp;
-        qp = qp ? sq : nullptr;
-        qn = qn ? sq + nq : nullptr;
-    }
-    if constexpr (!TB) {
-        update_general<ALGO, QT, PT, OT>(a, pc, qp, qn, qin, qout, ctx, vals, wave, lane);
-        return;
-    }
     for (int f = wave; f < a.F; f += 4) {
-        const FacDesc &fd = a.facs[f];
-        const int n = fd.n;
-        const QT *qprev = qp ? qp + fd.q_off : nullptr;
-        const QT *qnext = qn ? qn + fd.q_off : nullptr;
-        const int up = t > 0 ? a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f] : 0;
-        const int un = t + 1 < a.T ? a.act[((int64_t)agent * (a.T - 1) + t) * a.F + f] : 0;
-        const double *LBp = reinterpret_cast<const double *>(a.base + fd.lb_off) + (int64_t)up * n * n;
-        const double *LBn = reinterpret_cast<const double *>(a.base + fd.lb_off) + (int64_t)un * n * n;
-        const float *Bp = reinterpret_cast<const float *>(a.base + fd.b_off) + (int64_t)up * n * n;
-        const float *Bn = reinterpret_cast<const float *>(a.base + fd.b_off) + (int64_t)un * n * n;
-        const double *ld = reinterpret_cast<const double *>(a.base + fd.ld_off);
-        double *v = vals + fd.q_off;
+        StreamFac sf;
+        if (f < kStreamFacs) {
+            sf = a.fac[f];
+        } else {
+            const FacDesc &fd = a.facs[f];
+            sf = StreamFac{fd.lb_off, fd.b_off, fd.ld_off, fd.n, fd.q_off};
+        }
+        const int n = sf.n, qo = sf.q_off;
+        // the actions before and after t, both loads at once (indices clamped
+        // into the window; unused at its ends)
+        int up = 0, un = 0;
+        if (a.T > 1) {
+            const int32_t *ar = a.act + (int64_t)agent * (a.T - 1) * a.F + f;
+            up = ar[(int64_t)max(t - 1, 0) * a.F];
+            un = ar[(int64_t)min(t, a.T - 2) * a.F];
+        }
+        const MT *M = reinterpret_cast<const MT *>(a.base + (ALGO == BI_ALGO_VMP ? sf.lb_off : sf.b_off));
+        const MT *Mp = M + (int64_t)up * n * n, *Mn = M + (int64_t)un * n * n;
+        double *v = vals + qo;
         const int L = n <= 32 ? 2 : 1;          // lanes per state
         const int half = lane & (L - 1);        // which share of the terms this lane takes
         const int h = (n + L - 1) / L;          // transition terms per share
@@ -619,33 +564,54 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *par
         for (int s0 = 0; s0 < n; s0 += 64 / L) {
             const int s = s0 + lane / L;
             const int sc = min(s, n - 1);       // lanes past the last state compute a copy, unused
+            // fwd = sum_j M[u_{t-1}][sc][j] q_{t-1}[j] (a row), bwd = sum_j M[u_t][j][sc] q_{t+1}[j] (a column)
+            // (both products are formed at the window's ends too, from valid
+            // operands, and dropped: no branch around a load)
+            double fwd = 0.0, bwd = 0.0;
+            int j = j0;
+            for (; j + W <= j1; j += W) {
+                MT mf[W], mb[W];
+                QT xf[W], xb[W];
+#pragma unroll
+                for (int u = 0; u < W; ++u) {
+                    mf[u] = Mp[(int64_t)sc * n + j + u];
+                    mb[u] = Mn[(int64_t)(j + u) * n + sc];
+                    xf[u] = qp[qo + j + u];
+                    xb[u] = qn[qo + j + u];
+                }
+#pragma unroll
+                for (int u = 0; u < W; ++u) {
+                    fwd = fma((double)mf[u], (double)xf[u], fwd);
+                    bwd = fma((double)mb[u], (double)xb[u], bwd);
+                }
+            }
+            for (; j < j1; ++j) {
+                fwd = fma((double)Mp[(int64_t)sc * n + j], (double)qp[qo + j], fwd);
+                bwd = fma((double)Mn[(int64_t)j * n + sc], (double)qn[qo + j], bwd);
+            }
+            if (!hn) bwd = 0.0;
             double lam = 0.0;
             for (int i = 0; i < a.nmsg; ++i) {
                 const MsgSrc src = a.msg[i];
                 if (src.f != f) continue;
-                const PT *pp = pc + src.off + sc;
-                for (int k = half; k < src.copies; k += L) lam += (double)pp[(int64_t)k * src.stride];
+                for (int k = half; k < src.copies; k += L) lam += (double)pc[src.off + sc + (int64_t)k * src.stride];
             }
-            double fwd = 0.0, bwd = 0.0;
-            if (ALGO == BI_ALGO_VMP)
-                dot_pair(LBp + (int64_t)sc * n, qprev, LBn + sc, n, qnext, j0, j1, fwd, bwd);
-            else
-                dot_pair(Bp + (int64_t)sc * n, qprev, Bn + sc, n, qnext, j0, j1, fwd, bwd);
             if (L == 2) {
                 lam += __shfl_xor(lam, 1, 64);
                 fwd += __shfl_xor(fwd, 1, 64);
                 bwd += __shfl_xor(bwd, 1, 64);
             }
             if (t == 0)
-                fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + fd.q_off + sc]) : ld[sc];
+                fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + qo + sc])
+                              : reinterpret_cast<const double *>(a.base + sf.ld_off)[sc];
             else if (ALGO != BI_ALGO_VMP)
                 fwd = ln_clamped(fwd);
-            if (qnext && ALGO != BI_ALGO_VMP) bwd = ln_clamped(bwd);
+            if (hn && ALGO != BI_ALGO_VMP) bwd = ln_clamped(bwd);
             if (s < n && half == 0) {
                 if (ALGO == BI_ALGO_VMP)
                     v[s] = lam + fwd + bwd;
                 else
-                    v[s] = qnext ? lam + 0.5 * (fwd + bwd) : lam + fwd;
+                    v[s] = hn ? lam + 0.5 * (fwd + bwd) : lam + fwd;
             }
         }
         __builtin_amdgcn_wave_barrier();   // v[s] came from lane L s (one wave: LDS in program order)
@@ -659,14 +625,63 @@ __global__ __launch_bounds__(256) void update_kernel(StreamArgs a, const PT *par
             sum += ev;
         }
         sum = wave_sum(sum);
-        OT *out = qout + (int64_t)ctx * a.ntot + fd.q_off;
+        OT *out = qout + (int64_t)ctx * a.ntot + qo;
         if (a.tau != 1.0) {
-            const QT *old = qin + (int64_t)ctx * a.ntot + fd.q_off;
+            const QT *old = qin + (int64_t)ctx * a.ntot + qo;
             for (int s = lane; s < n; s += 64) out[s] = (OT)((1.0 - a.tau) * (double)old[s] + a.tau * (v[s] / sum));
         } else {
             for (int s = lane; s < n; s += 64) out[s] = (OT)(v[s] / sum);
         }
     }
+}
+
+template <typename T>
+using lds_cptr = const __attribute__((address_space(3))) T *;
+
+template <int ALGO, typename QT, typename PT, typename OT, bool TB>   // TB: every B-dependency list is {f}
+__global__ __launch_bounds__(256, 4) void update_kernel(StreamArgs a, const PT *part, const QT *qin, OT *qout)
+{
+    extern __shared__ double vals[];   // [ntot], then (staged) partials [pstride] and two marginal vectors [ntot]
+    const int ctx = blockIdx.x;
+    const int agent = ctx / a.T, t = ctx - agent * a.T;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)), lane = threadIdx.x & 63;
+    const PT *pc = part + (int64_t)ctx * a.pstride;
+    const bool hp = t > 0, hn = t + 1 < a.T;
+    const QT *qp = hp ? qin + (int64_t)(ctx - 1) * a.ntot : qin;
+    const QT *qn = hn ? qin + (int64_t)(ctx + 1) * a.ntot : qin;
+    if (a.stage) {
+        PT *sp = reinterpret_cast<PT *>(vals + a.ntot);
+        QT *sq = reinterpret_cast<QT *>(vals + a.ntot + (a.pstride * sizeof(PT) + 7) / 8);
+        const int tid = threadIdx.x;
+        const int np = (int)a.pstride, nq = a.ntot;
+        for (int i0 = tid; i0 < np; i0 += 8 * 256) {   // 8 independent loads per thread, then the stores
+            PT v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = pc[min(i0 + 256 * u, np - 1)];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (i0 + 256 * u < np) sp[i0 + 256 * u] = v[u];
+        }
+        for (int i = tid; i < nq; i += 256) {
+            const QT a0 = qp[i], a1 = qn[i];
+            sq[i] = a0;
+            sq[nq + i] = a1;
+        }
+        __syncthreads();
+        if constexpr (!TB) {
+            update_general<ALGO, QT, PT, OT>(a, sp, hp ? sq : nullptr, hn ? sq + nq : nullptr, qin, qout, ctx, vals,
+                                             wave, lane);
+        } else {
+            update_trivial<ALGO, QT, OT>(a, (lds_cptr<PT>)sp, (lds_cptr<QT>)sq, (lds_cptr<QT>)(sq + nq), hp, hn,
+                                         qin, qout, ctx, vals, wave, lane);
+        }
+        return;
+    }
+    if constexpr (!TB)
+        update_general<ALGO, QT, PT, OT>(a, pc, hp ? qp : nullptr, hn ? qn : nullptr, qin, qout, ctx, vals, wave,
+                                         lane);
+    else
+        update_trivial<ALGO, QT, OT>(a, pc, qp, qn, hp, hn, qin, qout, ctx, vals, wave, lane);
 }
 
 template <typename QT, typename PT, typename OT>
@@ -861,6 +876,10 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.prior = prior;
     a.tau = tau;
     a.trivb = m->trivial_b ? 1 : 0;
+    for (int f = 0; f < std::min(m->F, kStreamFacs); ++f) {
+        const FacDesc &fd = m->facs[f];
+        a.fac[f] = StreamFac{fd.lb_off, fd.b_off, fd.ld_off, fd.n, fd.q_off};
+    }
     a.bstart = reinterpret_cast<int32_t *>(w + offs[0]);
     a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
     char *part = w + offs[3];

@@ -13,10 +13,18 @@
 // sum_o w[o] c_{m,o}, again a constant per (context, modality) that the
 // softmax removes.
 //
-// One thread per slice element and agent: it reads X_m[o][e] once per group
-// of 8 steps and keeps 8 fp64 sums, the weights being wave-uniform loads.
-// Per agent the kernel reads K_m values and writes T values per element:
-// HBM bound (the model of a shared batch comes from L2).
+// For one agent and modality this is a dense product: LL_m = W_m X_m with
+// W_m the [T][K_m] observation vectors and X_m the [K_m][slice] stored logs,
+// done on the fp64 matrix cores (v_mfma_f64_16x16x4f64: 16 steps x 16
+// elements per tile, 4 outcomes per product).  A wave owns 64 consecutive
+// elements of one modality (4 tiles) and 32 steps (2 row tiles) at a time,
+// so every value of X_m leaves memory once per 32 steps; the weights come in
+// as fp32 and are widened.  Operand layouts (lane l): A[l % 16][l / 16],
+// B[l / 16][l % 16], result element i at row 4 i + l / 16, column l % 16, so
+// a store writes 4 steps x 16 consecutive elements.  Out-of-range steps,
+// outcomes and elements are read from clamped addresses and enter as zeros.
+// The sums over o are exact for one-hot vectors (zeros added to the one
+// product), so they reproduce the integer observations' slices bit for bit.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -28,8 +36,14 @@ namespace bi {
 
 namespace {
 
-constexpr int kSoftThreads = 256;
-constexpr int kSoftT = 8;   // steps per pass over the outcomes
+constexpr int kSoftWaves = 4;
+constexpr int kSoftThreads = 64 * kSoftWaves;
+constexpr int kSoftNB = 4;                     // 16-element tiles per wave
+constexpr int kSoftRT = 2;                     // 16-step tiles per pass
+constexpr int kSoftCols = 16 * kSoftNB;        // elements per wave
+constexpr int kSoftBlock = kSoftCols * kSoftWaves;
+
+typedef double d4 __attribute__((ext_vector_type(4)));
 
 struct SoftArgs {
     const char *base;
@@ -42,39 +56,68 @@ struct SoftArgs {
 
 __global__ __launch_bounds__(kSoftThreads) void soft_ll_kernel(SoftArgs a)
 {
-    // block -> (modality, first element): blocks of each modality in turn
-    int blk = blockIdx.x, m = 0, k0 = 0;
+    // block -> (modality, first element): the blocks of each modality in turn
+    int blk = blockIdx.x, m = 0, k0m = 0;
     int64_t po = 0;
     for (; m < a.M; ++m) {
-        const int nb = (a.mods[m].slice + kSoftThreads - 1) / kSoftThreads;
+        const int nb = (a.mods[m].slice + kSoftBlock - 1) / kSoftBlock;
         if (blk < nb) break;
         blk -= nb;
         po += a.mods[m].slice;
-        k0 += a.mods[m].K;
+        k0m += a.mods[m].K;
     }
     if (m >= a.M) return;
     const ModDesc &md = a.mods[m];
-    const int e = blk * kSoftThreads + (int)threadIdx.x;
-    if (e >= md.slice) return;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int e0 = blk * kSoftBlock + wave * kSoftCols;
+    if (e0 >= md.slice) return;
+    const int li = lane & 15, lg = lane >> 4;
+    const int K = md.K, S = md.slice;
     for (int agent = blockIdx.y; agent < a.b; agent += gridDim.y) {
         const double *X = reinterpret_cast<const double *>(a.base + md.la_off) +
-                          (a.shared ? 0 : (int64_t)agent * md.la_agent) + e;
-        const float *wa = a.w + (int64_t)agent * a.T * a.ksum + k0;
-        double *out = a.ll + (int64_t)agent * a.T * a.llpc + po + e;
-        for (int t0 = 0; t0 < a.T; t0 += kSoftT) {
-            double acc[kSoftT];
+                          (a.shared ? 0 : (int64_t)agent * md.la_agent);
+        const float *wa = a.w + (int64_t)agent * a.T * a.ksum + k0m;
+        double *out = a.ll + (int64_t)agent * a.T * a.llpc + po;
+        for (int t0 = 0; t0 < a.T; t0 += 16 * kSoftRT) {
+            d4 acc[kSoftRT][kSoftNB];
 #pragma unroll
-            for (int j = 0; j < kSoftT; ++j) acc[j] = 0.0;
-            const int nt = min(kSoftT, a.T - t0);
-            for (int o = 0; o < md.K; ++o) {
-                const double x = X[(int64_t)o * md.slice];
+            for (int r = 0; r < kSoftRT; ++r)
 #pragma unroll
-                for (int j = 0; j < kSoftT; ++j)
-                    if (j < nt) acc[j] = fma((double)wa[(int64_t)(t0 + j) * a.ksum + o], x, acc[j]);
+                for (int nb = 0; nb < kSoftNB; ++nb) acc[r][nb] = d4{0.0, 0.0, 0.0, 0.0};
+            for (int k0 = 0; k0 < K; k0 += 4) {
+                const int o = k0 + lg;
+                const bool ok = o < K;
+                const int oc = min(o, K - 1);
+                double av[kSoftRT], bv[kSoftNB];
+#pragma unroll
+                for (int r = 0; r < kSoftRT; ++r) {
+                    const int t = t0 + 16 * r + li;
+                    const float wv = wa[(int64_t)min(t, a.T - 1) * a.ksum + oc];
+                    av[r] = ok && t < a.T ? (double)wv : 0.0;
+                }
+#pragma unroll
+                for (int nb = 0; nb < kSoftNB; ++nb) {
+                    const int e = e0 + 16 * nb + li;
+                    const double xv = X[(int64_t)oc * S + min(e, S - 1)];
+                    bv[nb] = ok && e < S ? xv : 0.0;
+                }
+#pragma unroll
+                for (int r = 0; r < kSoftRT; ++r)
+#pragma unroll
+                    for (int nb = 0; nb < kSoftNB; ++nb)
+                        acc[r][nb] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[r], bv[nb], acc[r][nb], 0, 0, 0);
             }
 #pragma unroll
-            for (int j = 0; j < kSoftT; ++j)
-                if (j < nt) out[(int64_t)(t0 + j) * a.llpc] = acc[j];
+            for (int r = 0; r < kSoftRT; ++r)
+#pragma unroll
+                for (int nb = 0; nb < kSoftNB; ++nb) {
+                    const int e = e0 + 16 * nb + li;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int t = t0 + 16 * r + 4 * i + lg;
+                        if (t < a.T && e < S) out[(int64_t)t * a.llpc + e] = acc[r][nb][i];
+                    }
+                }
         }
     }
 }
@@ -103,7 +146,7 @@ int launch_soft_ll(const bi_model *m, int b, int T, const float *w, double *ll, 
     a.w = w;
     a.ll = ll;
     int64_t blocks = 0;
-    for (const ModDesc &md : m->mods) blocks += (md.slice + kSoftThreads - 1) / kSoftThreads;
+    for (const ModDesc &md : m->mods) blocks += (md.slice + kSoftBlock - 1) / kSoftBlock;
     if (blocks > INT32_MAX)
         return fail(BI_ERR_UNSUPPORTED, "soft log-likelihood grid of %lld blocks too large", (long long)blocks);
     {

@@ -16,7 +16,9 @@ VMP and MMP over the whole batch on both A layouts:
          first-factor state into LDS and contracted on the same fp16 matrix
          cores (--sparse-f64: fp64 gathers over the nonzero entries instead).
 Inputs are resident in HBM before timing starts; each model is packed once
-outside the timed region (the one-time layout step).
+outside the timed region (the one-time layout step).  After the set-up the
+step runs 30 untimed settle steps, then the --warmup steps, then the timed
+--steps.
 
 Prints one JSON line.  value = belief updates per second over the whole job,
 one belief update being one (agent, time step, iteration) of one algorithm
@@ -38,6 +40,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -149,6 +152,9 @@ def agent_work(model, T, algo):
 
 
 # per-agent workloads: name -> (generator, algorithm, options)
+# untimed steps run after set-up and before the --warmup steps (large workload)
+SETTLE_STEPS = 30
+
 AGENT_WORKLOADS = {
     "vmp_2f": ("two_factor_agents", "vmp", {}),
     "mmp_3f": ("three_factor_agents", "mmp", {}),
@@ -326,7 +332,9 @@ def main():
 
     pms, qs, wss = setup(flags)
     step = make_step(pms, qs, wss)
-    for _ in range(args.warmup):
+    # untimed settle steps after the set-up (the first ~100 ms of steps after
+    # packing showed occasional host stalls of 20-30 ms), then the warm-up
+    for _ in range(SETTLE_STEPS + args.warmup):
         step()
     # the timed region: the steps alone (no profiling events between launches)
     ms_step, wall = timed(step)
@@ -338,14 +346,16 @@ def main():
     bi.bi_profile_begin()
     ms_prof, _ = timed(step)
     prof = bi.bi_profile_end()
-    # a third pass with events around every call: per-call durations
-    marks = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in qs}
-    call_ms = {k: 0.0 for k in qs}
-    for _ in range(args.steps):
+    # a third pass with events around every call: per-call durations, the
+    # median over the steps (each step with its own events, one
+    # synchronisation at the end, so no call starts on an idle queue)
+    step_marks = [{k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in qs}
+                  for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for marks in step_marks:
         step(marks=marks)
-        torch.cuda.synchronize()
-        for k, (e0, e1) in marks.items():
-            call_ms[k] += e0.elapsed_time(e1) / args.steps
+    torch.cuda.synchronize()
+    call_ms = {k: statistics.median(m[k][0].elapsed_time(m[k][1]) for m in step_marks) for k in qs}
 
     traffic = load_traffic()
     dense_work = dense_lik_work(w.model, w.obs)
@@ -386,6 +396,7 @@ def main():
                    "b": w.b, "T": w.T, "iters": w.iters, "algos": list(ALGOS), "layouts": layouts},
         "roofline": rooflines[dominant],
         "roofline_all": rooflines,
+        "settle_steps": SETTLE_STEPS,
         "kernel_timing": "a second pass of the same steps with HIP events around every launch on the call "
                          f"stream ({ms_prof:.3f} ms per step with them); the timed region has none",
         "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},

@@ -522,17 +522,32 @@ __device__ void update_general(const StreamArgs &a, const PT *pc, const QT *qp, 
 // marginals between iterations, PT = partial messages, OT = this launch's
 // output marginals.
 // ---------------------------------------------------------------------------
+// The actions of factor f before and after step t, both loads at once
+// (indices clamped into the window; unused at its ends; none when T = 1).
+__device__ inline void trans_actions(const StreamArgs &a, int f, int agent, int t, int &up, int &un)
+{
+    up = 0;
+    un = 0;
+    if (a.T > 1) {
+        const int32_t *ar = a.act + (int64_t)agent * (a.T - 1) * a.F + f;
+        up = ar[(int64_t)max(t - 1, 0) * a.F];
+        un = ar[(int64_t)min(t, a.T - 2) * a.F];
+    }
+}
+
 // Update of one context under trivial B-dependency lists, for the factors
 // of this wave (wave-uniform f, so the factor descriptors, the actions and the
 // message-source table come in by scalar loads).  PP / QP: pointers to the
 // context's partial messages and to the neighbouring steps' marginals, typed
 // for LDS when they were staged (no generic-address loads); hp / hn: whether
-// the steps t - 1 / t + 1 exist.  Every read of a transition product is issued
-// before the partial sums, and the products take their operands 8 terms at a
-// time (in j order, so the sums are those of one term at a time).
+// the steps t - 1 / t + 1 exist; up0 / un0: the actions before and after t
+// of factor `wave`, loaded before the staging.  Every read of a transition
+// product is issued before the partial sums, and the products take their
+// operands 8 terms at a time (4 for fp64 log B with fp64 marginals; in j
+// order, so the sums are those of one term at a time).
 template <int ALGO, typename QT, typename OT, typename PP, typename QP>
 __device__ inline void update_trivial(const StreamArgs &a, PP pc, QP qp, QP qn, bool hp, bool hn, const QT *qin,
-                                      OT *qout, int ctx, double *vals, int wave, int lane)
+                                      OT *qout, int ctx, double *vals, int wave, int lane, int up0, int un0)
 {
     using MT = std::conditional_t<ALGO == BI_ALGO_VMP, double, float>;   // log B (VMP) or B (MMP)
     constexpr int W = sizeof(MT) + sizeof(QT) > 8 ? 4 : 8;   // terms per batch (registers: every workgroup resident)
@@ -546,14 +561,8 @@ __device__ inline void update_trivial(const StreamArgs &a, PP pc, QP qp, QP qn, 
             sf = StreamFac{fd.lb_off, fd.b_off, fd.ld_off, fd.n, fd.q_off};
         }
         const int n = sf.n, qo = sf.q_off;
-        // the actions before and after t, both loads at once (indices clamped
-        // into the window; unused at its ends)
-        int up = 0, un = 0;
-        if (a.T > 1) {
-            const int32_t *ar = a.act + (int64_t)agent * (a.T - 1) * a.F + f;
-            up = ar[(int64_t)max(t - 1, 0) * a.F];
-            un = ar[(int64_t)min(t, a.T - 2) * a.F];
-        }
+        int up = up0, un = un0;
+        if (f != wave) trans_actions(a, f, agent, t, up, un);
         const MT *M = reinterpret_cast<const MT *>(a.base + (ALGO == BI_ALGO_VMP ? sf.lb_off : sf.b_off));
         const MT *Mp = M + (int64_t)up * n * n, *Mn = M + (int64_t)un * n * n;
         double *v = vals + qo;
@@ -649,6 +658,8 @@ __global__ __launch_bounds__(256, 4) void update_kernel(StreamArgs a, const PT *
     const bool hp = t > 0, hn = t + 1 < a.T;
     const QT *qp = hp ? qin + (int64_t)(ctx - 1) * a.ntot : qin;
     const QT *qn = hn ? qin + (int64_t)(ctx + 1) * a.ntot : qin;
+    int up0 = 0, un0 = 0;   // trivial lists: this wave's first factor's actions, in flight during the staging
+    if (TB && wave < a.F) trans_actions(a, wave, agent, t, up0, un0);
     if (a.stage) {
         PT *sp = reinterpret_cast<PT *>(vals + a.ntot);
         QT *sq = reinterpret_cast<QT *>(vals + a.ntot + (a.pstride * sizeof(PT) + 7) / 8);
@@ -673,7 +684,7 @@ __global__ __launch_bounds__(256, 4) void update_kernel(StreamArgs a, const PT *
                                              wave, lane);
         } else {
             update_trivial<ALGO, QT, OT>(a, (lds_cptr<PT>)sp, (lds_cptr<QT>)sq, (lds_cptr<QT>)(sq + nq), hp, hn,
-                                         qin, qout, ctx, vals, wave, lane);
+                                         qin, qout, ctx, vals, wave, lane, up0, un0);
         }
         return;
     }
@@ -681,7 +692,7 @@ __global__ __launch_bounds__(256, 4) void update_kernel(StreamArgs a, const PT *
         update_general<ALGO, QT, PT, OT>(a, pc, hp ? qp : nullptr, hn ? qn : nullptr, qin, qout, ctx, vals, wave,
                                          lane);
     else
-        update_trivial<ALGO, QT, OT>(a, pc, qp, qn, hp, hn, qin, qout, ctx, vals, wave, lane);
+        update_trivial<ALGO, QT, OT>(a, pc, qp, qn, hp, hn, qin, qout, ctx, vals, wave, lane, up0, un0);
 }
 
 template <typename QT, typename PT, typename OT>

@@ -60,12 +60,26 @@ __device__ inline double wave_sum(double v)
 }
 
 // ---------------------------------------------------------------------------
-// bucketing: contexts sorted by observed outcome, one workgroup per modality.
-// Slot order inside a bucket is not fixed (atomics) but results do not depend
-// on it: every context's outputs come from its own MFMA column.
+// Set-up of a call, one launch: workgroups 0 .. M-1 sort the contexts by
+// observed outcome, one per modality (bucketing); the others write the
+// uniform start of the marginals.  Slot order inside a bucket is not fixed
+// (atomics) but results do not depend on it: every context's outputs come
+// from its own MFMA column.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void bucket_kernel(StreamArgs a)
+template <typename QT>
+__global__ __launch_bounds__(1024) void prep_kernel(StreamArgs a, QT *q)
 {
+    if ((int)blockIdx.x >= a.M) {   // uniform start
+        const int64_t total = (int64_t)a.nctx * a.ntot;
+        const int64_t nthr = (int64_t)(gridDim.x - a.M) * blockDim.x;
+        for (int64_t i = (blockIdx.x - a.M) * (int64_t)blockDim.x + threadIdx.x; i < total; i += nthr) {
+            const int j = (int)(i % a.ntot);
+            int f = 0;
+            while (f + 1 < a.F && a.facs[f + 1].q_off <= j) ++f;
+            q[i] = QT(1) / QT(a.facs[f].n);
+        }
+        return;
+    }
     extern __shared__ int cnt[];   // [K + 1] counts, then starts; [K] fill counters
     const int m = blockIdx.x;
     const StreamMod &sm = a.sm[m];
@@ -90,18 +104,6 @@ __global__ __launch_bounds__(1024) void bucket_kernel(StreamArgs a)
     for (int i = threadIdx.x; i < a.nctx; i += blockDim.x) {
         const int o = a.obs[(int64_t)i * a.M + m];
         list[cnt[o] + atomicAdd(&fil[o], 1)] = i;
-    }
-}
-
-template <typename QT>
-__global__ void init_q_kernel(StreamArgs a, QT *q)
-{
-    const int64_t total = (int64_t)a.nctx * a.ntot;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int j = (int)(i % a.ntot);
-        int f = 0;
-        while (f + 1 < a.F && a.facs[f + 1].q_off <= j) ++f;
-        q[i] = QT(1) / QT(a.facs[f].n);
     }
 }
 
@@ -932,25 +934,23 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     }
     int kmax = 1;
     for (const ModDesc &md : m->mods) kmax = std::max(kmax, md.K);
-    {
-        ProfScope p("bucket", stream);
-        hipLaunchKernelGGL(bucket_kernel, dim3(m->M), dim3(1024), sizeof(int) * (2 * kmax + 1), stream, a);
-    }
-    const int init_grid = (int)std::min<int64_t>(1024, ((int64_t)a.nctx * a.ntot + 255) / 256);
+    // set-up: bucketing and the uniform start in one launch
+    const int init_grid = (int)std::min<int64_t>(256, ((int64_t)a.nctx * a.ntot + 1023) / 1024);
+    const size_t prep_lds = sizeof(int) * (2 * kmax + 1);
     if (lik == Lik::Sparse) {
         double *qa = reinterpret_cast<double *>(w + offs[4]);
         double *qb = reinterpret_cast<double *>(w + offs[5]);
         {
-            ProfScope p("init", stream);
-            hipLaunchKernelGGL(init_q_kernel<double>, dim3(init_grid), dim3(256), 0, stream, a, qa);
+            ProfScope p("prep", stream);
+            hipLaunchKernelGGL(prep_kernel<double>, dim3(m->M + init_grid), dim3(1024), prep_lds, stream, a, qa);
         }
         run_iterations<double>(m, algo, iters, a, part, qa, qb, q, lik_lds, upd_lds, stream, lik);
     } else {
         float *qa = reinterpret_cast<float *>(w + offs[4]);
         float *qb = reinterpret_cast<float *>(w + offs[5]);
         {
-            ProfScope p("init", stream);
-            hipLaunchKernelGGL(init_q_kernel<float>, dim3(init_grid), dim3(256), 0, stream, a, qa);
+            ProfScope p("prep", stream);
+            hipLaunchKernelGGL(prep_kernel<float>, dim3(m->M + init_grid), dim3(1024), prep_lds, stream, a, qa);
         }
         run_iterations<float>(m, algo, iters, a, part, qa, qb, q, lik_lds, upd_lds, stream, lik);
     }

@@ -224,77 +224,14 @@ __device__ void stage_slices(const AgentArgs &a, int agent, int t0, int nc, doub
     }
 }
 
-// Phase 1 with the slices in global memory (the packed buffer, or the soft
-// observations' log-likelihood tensors): Z/V of contexts [t0, t0 + nc) into
-// zv[c][zvpc].  A Z output (a row of X against the column factors' outer
-// product) takes a group of 16 lanes, lane k summing the columns k, k + 16,
-// ... in order and the group adding its 16 shares with a butterfly, so a load
-// brings 16 consecutive values of a row (one 128-byte line); a V output (a
-// column against the row factors' outer product) takes one lane, the lanes
-// of a wave on consecutive columns.  (With one lane per Z output every lane
-// of a load touched its own line, and the texture data path bounded the
-// kernel.)
-__device__ void phase_zv_global(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv)
-{
-    const int tid = threadIdx.x;
-    const int grp = tid >> 4, l16 = tid & 15;
-    constexpr int kGroups = kThreads / 16;
-    int64_t llo = 0;   // offset of modality m in a context's log-likelihood tensors
-    for (int m = 0; m < a.M; ++m) {
-        const ModDesc &md = a.mods[m];
-        const int R = md.R, C = md.C, Cp = md.Cp;
-        const double *la = at<double>(a.base, md.la_off) + (a.shared ? 0 : (int64_t)agent * md.la_agent);
-        auto slice = [&](int t) -> const double * {
-            if (a.ll) return a.ll + ((int64_t)agent * a.T + t) * a.llpc + llo;
-            return la + (int64_t)a.obs[((int64_t)agent * a.T + t) * a.M + m] * md.slice;
-        };
-        if (md.nrow > 0) {   // (Z of a rank-0 row side feeds no message)
-            const int n1 = md.ncol == 2 ? md.cn[1] : 1;
-            const int d0 = 16 / n1, d1 = 16 - d0 * n1;   // the column odometer's step of 16
-            for (int it = grp; it < nc * R; it += kGroups) {
-                const int c = it / R, r = it - c * R, t = t0 + c;
-                const double *row = slice(t) + (int64_t)r * Cp;
-                const double *qt = q + t * a.ntot;
-                const double *q0 = qt + a.facs[md.cf[0]].q_off;
-                const double *q1 = md.ncol == 2 ? qt + a.facs[md.cf[1]].q_off : nullptr;
-                int i0 = l16 / n1, i1 = l16 - (l16 / n1) * n1;   // column l16 = i0 n1 + i1
-                double acc = 0.0;
-#pragma unroll 2
-                for (int cc = l16; cc < C; cc += 16) {
-                    const double w = q1 ? q0[i0] * q1[i1] : q0[i0];
-                    acc = fma(row[cc], w, acc);
-                    i0 += d0;
-                    i1 += d1;
-                    if (i1 >= n1) {
-                        i1 -= n1;
-                        ++i0;
-                    }
-                }
-#pragma unroll
-                for (int o = 8; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 16);
-                if (l16 == 0) zv[c * a.zvpc + md.zv_off + r] = acc;
-            }
-        }
-        for (int it = tid; it < nc * C; it += kThreads) {
-            const int c = it / C, col = it - c * C, t = t0 + c;
-            zv[c * a.zvpc + md.zv_off + R + col] = zv_one(a, md, slice(t), Cp, q + t * a.ntot, R + col);
-        }
-        llo += md.slice;
-    }
-}
-
 // Phase 1: Z/V of contexts [t0, t0 + nc) into zv[c][zvpc].
 // q: marginals of context t at q + t * ntot.  With staged slices, X of
 // context t0 + c comes from stg + (sc0 + c) * sctx (LDS); otherwise from the
-// packed buffer (phase_zv_global).
-template <bool GX>   // GX: slices read from global memory; else staged in LDS
+// packed buffer.
+template <bool GX>   // GX: slices read from global memory (batched loads); else staged in LDS
 __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv,
                          const double *stg, int sc0)
 {
-    if (GX) {
-        phase_zv_global(a, agent, t0, nc, q, zv);
-        return;
-    }
     const int tid = threadIdx.x;
     int base = 0;
     int64_t llo = 0;   // offset of modality m in a context's log-likelihood tensors

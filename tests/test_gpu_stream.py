@@ -40,6 +40,13 @@ CASES = [
     ([70], [2], [3], [[0]], 30, 3),
     ([33, 5], [2, 2], [2, 2, 3], [[0, 1], [0], [1]], 64, 6),
     ([4, 4, 4, 4], [1, 1, 1, 1], [2], [[0, 1, 2, 3]], 100, 2),
+    # 19 factors: the update kernel's waves take several factors each, the
+    # factors past the 16 whose fields are kernel arguments read their
+    # descriptors, and factor 18 is in no dependency list (no likelihood)
+    ([3, 2, 2, 3, 2, 2, 3, 2, 2, 3, 2, 2, 3, 2, 2, 3, 2, 3, 2], [2, 1, 2, 1, 2, 1, 2, 1, 2, 1, 2, 1, 2, 1, 2, 1, 3, 2, 2],
+     [3, 4, 2, 3, 3], [[0, 1, 2, 3], [4, 5, 16], [6, 7, 8, 17], [9, 10, 11, 12], [13, 14, 15]], 20, 4),
+    # a one-step window (no actions)
+    ([5, 4], [2, 1], [3, 2], [[0, 1], [1]], 16, 1),
 ]
 
 

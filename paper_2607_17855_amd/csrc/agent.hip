@@ -41,6 +41,10 @@ constexpr size_t kBStageMax = 64 * 1024;   // bytes of B / log B staged per work
 // reads); pr[m] is the slice's offset in the unpadded concatenation.
 enum StageMode { kStageNone = 0, kStageChunk = 1, kStageWindow = 2 };
 
+// Where phase 1 reads the observed slices: staged in LDS, from global memory
+// one dot product per thread, or from global memory in the tile form.
+enum SliceSrc { kSrcLds = 0, kSrcGlobal = 1, kSrcTile = 2 };
+
 struct AgentArgs {
     const char *base;      // packed buffer
     const ModDesc *mods;   // device descriptor tables (inside the packed buffer)
@@ -60,6 +64,12 @@ struct AgentArgs {
     // [u][i][j] block at element bo[f].  bdoubles: LDS doubles of the table.
     int bst, bdoubles;
     int bo[kStageMaxF + 1];
+    // Tile form of the Z/V phase (slices from global memory, M <= kStageMaxM):
+    // modality m's block in a context's Z/V scratch starts at zt[m] and holds
+    // the Z partial sums of its column chunks, [chunk][R] (row side of rank
+    // >= 1 only), then V [C].  The window's outcomes are copied to LDS.
+    int tile;
+    int zt[kStageMaxM + 1];
     double tau;            // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
     float *q;
 };
@@ -263,7 +273,175 @@ __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const do
     }
 }
 
-// Phase 2: lam of contexts [t0, t0 + nc) into lam[t][ntot].
+// ---------------------------------------------------------------------------
+// Tile form of phase 1 for slices read from global memory.  A unit is
+// (context, modality, chunk of 32 columns) and runs on a segment of 16 lanes,
+// two adjacent columns per lane: each lane loads its two columns of every row
+// (16-byte loads; the lanes of a segment cover 256 contiguous bytes of a row),
+// so a slice is read once, coalesced, for both of its sides:
+//   V[col]  = sum_r s[r] X[r][col]         in the lane (rows in blocks of RB,
+//                                           all loads of a block in flight);
+//   Z[r]   += sum_{col in chunk} X[r][col] t[col]
+//                                          lane partial products, reduced over
+//                                          the segment by DPP exchanges.
+// Z of a modality with nch chunks is left as nch partial sums per row; phase
+// 2 adds them.  Every sum runs in a fixed order (results are reproducible).
+constexpr int kSeg = 16;                 // lanes per unit (one DPP row)
+constexpr int kSegs = kThreads / kSeg;   // units in flight per workgroup
+constexpr int kTileCols = 2 * kSeg;      // columns per unit
+
+__host__ __device__ constexpr int tile_nch(int C) { return (C + kTileCols - 1) / kTileCols; }
+
+// doubles of modality md's block in the tile layout
+__host__ __device__ inline int tile_block(const ModDesc &md) { return (md.nrow > 0 ? tile_nch(md.C) * md.R : 0) + md.C; }
+
+// DPP lane pairings inside a row of 16 lanes: lane i with i ^ 15 (row_mirror),
+// i ^ 7 (row_half_mirror), i ^ 3 and i ^ 1 (quad permutations).  Partners of
+// pairing k differ in lane bit 3 - k and in no higher bit, so the four of them
+// in this order halve a set of values per lane like a butterfly over bits
+// 3, 2, 1, 0.
+template <int K> struct SegPair;
+template <> struct SegPair<0> { static constexpr int ctrl = 0x140; };
+template <> struct SegPair<1> { static constexpr int ctrl = 0x141; };
+template <> struct SegPair<2> { static constexpr int ctrl = 0x1B; };
+template <> struct SegPair<3> { static constexpr int ctrl = 0xB1; };
+
+template <int K>
+__device__ inline double seg_swap(double v)
+{
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), SegPair<K>::ctrl, 0xF, 0xF, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), SegPair<K>::ctrl, 0xF, 0xF, true);
+    return __hiloint2double(hi, lo);
+}
+
+// Sum of z[0..P) over the 16 lanes of the segment, one value per lane left
+// in z[0]: P halving steps and 4 - log2 P plain exchanges; the lane then holds
+// value index sl >> (4 - log2 P) (lanes that differ only in the low bits hold
+// the same sum).  Every lane of the segment must take part.
+template <int K, int N>
+__device__ inline void seg_halve(double *z, int sl)
+{
+    if constexpr (N > 1) {
+        const bool up = (sl >> (3 - K)) & 1;
+#pragma unroll
+        for (int i = 0; i < N / 2; ++i) {
+            const double lo = z[i], hi = z[i + N / 2];
+            z[i] = (up ? hi : lo) + seg_swap<K>(up ? lo : hi);
+        }
+        seg_halve<K + 1, N / 2>(z, sl);
+    } else if constexpr (K < 4) {
+        z[0] += seg_swap<K>(z[0]);
+        seg_halve<K + 1, 1>(z, sl);
+    }
+}
+
+constexpr int log2_floor(int x) { return x <= 1 ? 0 : 1 + log2_floor(x / 2); }
+
+// One modality's units of contexts [t0, t0 + nc): RB rows per block (every
+// row of a block loaded before any is used), P >= RB the power of two the
+// segment reduction works on.
+template <int RB>
+__device__ void zv_tile_modality(const AgentArgs &a, const ModDesc &md, int agent, int m, int t0, int nc,
+                                 const double *q, double *zv, const int *sobs, int64_t llo, int first)
+{
+    constexpr int P = RB <= 1 ? 1 : RB <= 2 ? 2 : RB <= 4 ? 4 : RB <= 8 ? 8 : 16;
+    constexpr int LP = log2_floor(P);
+    const int R = md.R, C = md.C, Cp = md.Cp;
+    const int nch = tile_nch(C), units = nc * nch;
+    const int seg = (int)threadIdx.x / kSeg, sl = (int)threadIdx.x % kSeg;
+    const double *la = at<double>(a.base, md.la_off) + (a.shared ? 0 : (int64_t)agent * md.la_agent);
+    const bool zrow = md.nrow > 0;
+    const int zlen = zrow ? nch * R : 0;
+    const int rn1 = md.nrow == 2 ? md.rn[1] : 1, cn1 = md.ncol == 2 ? md.cn[1] : 1;
+    int u = seg - first % kSegs;
+    if (u < 0) u += kSegs;
+    for (; u < units; u += kSegs) {
+        const int c = u / nch, cb = u - c * nch;
+        const int t = t0 + c;
+        const double *qt = q + t * a.ntot;
+        const double *X = a.ll ? a.ll + ((int64_t)agent * a.T + t) * a.llpc + llo
+                               : la + (int64_t)sobs[t * a.M + m] * md.slice;
+        double *blk = zv + c * a.zvpc + a.zt[m];
+        // this lane's columns col, col + 1 (col even; Cp is a multiple of 4,
+        // so the pair is one aligned 16-byte load and col + 1 < Cp)
+        const int col = cb * kTileCols + 2 * sl;
+        const int colc = min(col, (C - 1) & ~1);
+        double w0 = 0.0, w1 = 0.0;
+        if (zrow) {
+            const double *qc0 = qt + a.facs[md.cf[0]].q_off;
+            const double *qc1 = md.ncol == 2 ? qt + a.facs[md.cf[1]].q_off : nullptr;
+            const int ca = min(col, C - 1), cbb = min(col + 1, C - 1);
+            const int a0 = ca / cn1, a1 = ca - a0 * cn1, b0 = cbb / cn1, b1 = cbb - b0 * cn1;
+            w0 = qc1 ? qc0[a0] * qc1[a1] : qc0[a0];
+            w1 = qc1 ? qc0[b0] * qc1[b1] : qc0[b0];
+            w0 = col < C ? w0 : 0.0;
+            w1 = col + 1 < C ? w1 : 0.0;
+        }
+        const double *qr0 = md.nrow > 0 ? qt + a.facs[md.rf[0]].q_off : nullptr;
+        const double *qr1 = md.nrow == 2 ? qt + a.facs[md.rf[1]].q_off : nullptr;
+        double v0 = 0.0, v1 = 0.0;
+        for (int r0 = 0; r0 < R; r0 += RB) {
+            double2 x[RB];
+#pragma unroll
+            for (int i = 0; i < RB; ++i)
+                x[i] = *reinterpret_cast<const double2 *>(X + (int64_t)min(r0 + i, R - 1) * Cp + colc);
+            // row weights s[r] (1 for a rank-0 row side)
+            int i0 = r0 / rn1, i1 = r0 - i0 * rn1;
+            double z[P];
+#pragma unroll
+            for (int i = 0; i < RB; ++i) {
+                double sw = 1.0;
+                if (md.nrow > 0) sw = qr1 ? qr0[min(i0, md.rn[0] - 1)] * qr1[i1] : qr0[min(r0 + i, R - 1)];
+                sw = r0 + i < R ? sw : 0.0;
+                if (++i1 == rn1) {
+                    i1 = 0;
+                    ++i0;
+                }
+                const double x1 = col + 1 < C ? x[i].y : 0.0;   // (column C is padding)
+                v0 = fma(sw, x[i].x, v0);
+                v1 = fma(sw, x1, v1);
+                z[i] = fma(x1, w1, x[i].x * w0);
+            }
+            if (zrow) {
+#pragma unroll
+                for (int i = RB; i < P; ++i) z[i] = 0.0;
+                seg_halve<0, P>(z, sl);
+                const int row = r0 + (sl >> (4 - LP));
+                if ((sl & ((1 << (4 - LP)) - 1)) == 0 && row < R) blk[cb * R + row] = z[0];
+            }
+        }
+        double *V = blk + zlen;
+        if (col < C) V[col] = v0;
+        if (col + 1 < C) V[col + 1] = v1;
+    }
+}
+
+__device__ void phase_zv_tile(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv,
+                              const int *sobs)
+{
+    int first = 0;
+    int64_t llo = 0;
+    for (int m = 0; m < a.M; ++m) {
+        const ModDesc &md = a.mods[m];
+        const int R = md.R;
+        if (R <= 1)
+            zv_tile_modality<1>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+        else if (R <= 2)
+            zv_tile_modality<2>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+        else if (R <= 4)
+            zv_tile_modality<4>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+        else if (R <= 8)
+            zv_tile_modality<8>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+        else   // (blocks of 12 rows beyond: 16 would spill at three workgroups per CU)
+            zv_tile_modality<12>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+        first += nc * tile_nch(md.C);
+        llo += md.slice;
+    }
+}
+
+// Phase 2: lam of contexts [t0, t0 + nc) into lam[t][ntot].  TILE: Z/V in the
+// tile layout (Z as per-chunk partial sums).
+template <bool TILE>
 __device__ void phase_lam(const AgentArgs &a, int t0, int nc, const double *q, const double *zv, const int *sfac,
                           double *lam)
 {
@@ -275,23 +453,30 @@ __device__ void phase_lam(const AgentArgs &a, int t0, int nc, const double *q, c
         double acc = 0.0;
         for (int m = 0; m < a.M; ++m) {
             const ModDesc &md = a.mods[m];
-            const double *Z = zv + c * a.zvpc + md.zv_off;
-            const double *V = Z + md.R;
+            const double *Z = zv + c * a.zvpc + (TILE ? a.zt[m] : md.zv_off);
+            const int nch = TILE ? tile_nch(md.C) : 1;
+            const double *V = Z + (TILE ? (md.nrow > 0 ? nch * md.R : 0) : md.R);
+            // Z[k]: the sum of its column chunks' partial sums
+            auto zat = [&](int k) {
+                double z = Z[k];
+                for (int cb = 1; cb < nch; ++cb) z += Z[cb * md.R + k];
+                return z;
+            };
             if (md.nrow >= 1 && md.rf[0] == f) {
                 if (md.nrow == 1) {
-                    acc += Z[s];
+                    acc += zat(s);
                 } else {
                     const double *q1 = qt + a.facs[md.rf[1]].q_off;
                     const int n1 = md.rn[1];
                     double in = 0.0;
-                    for (int r1 = 0; r1 < n1; ++r1) in = fma(Z[s * n1 + r1], q1[r1], in);
+                    for (int r1 = 0; r1 < n1; ++r1) in = fma(zat(s * n1 + r1), q1[r1], in);
                     acc += in;
                 }
             } else if (md.nrow == 2 && md.rf[1] == f) {
                 const double *q0 = qt + a.facs[md.rf[0]].q_off;
                 const int n0 = md.rn[0], n1 = md.rn[1];
                 double in = 0.0;
-                for (int r0 = 0; r0 < n0; ++r0) in = fma(Z[r0 * n1 + s], q0[r0], in);
+                for (int r0 = 0; r0 < n0; ++r0) in = fma(zat(r0 * n1 + s), q0[r0], in);
                 acc += in;
             } else if (md.cf[0] == f) {
                 if (md.ncol == 1) {
@@ -333,9 +518,9 @@ __device__ void wave_softmax(double *v, int n, int lane)
 
 // lam for every context of the window (phases 1 and 2 over context chunks;
 // staged chunks are copied to LDS first unless the whole window is resident).
-template <bool GX>
+template <int SRC>
 __device__ void window_lam(const AgentArgs &a, int agent, const double *q, double *zv, double *stg, const int *sfac,
-                           double *lam)
+                           const int *sobs, double *lam)
 {
     for (int t0 = 0; t0 < a.T; t0 += a.nc) {
         const int nc = min(a.nc, a.T - t0);
@@ -343,11 +528,21 @@ __device__ void window_lam(const AgentArgs &a, int agent, const double *q, doubl
             stage_slices(a, agent, t0, nc, stg);
             __syncthreads();
         }
-        phase_zv<GX>(a, agent, t0, nc, q, zv, stg, a.stage == kStageWindow ? t0 : 0);
+        if (SRC == kSrcTile)
+            phase_zv_tile(a, agent, t0, nc, q, zv, sobs);
+        else
+            phase_zv<SRC == kSrcGlobal>(a, agent, t0, nc, q, zv, stg, a.stage == kStageWindow ? t0 : 0);
         __syncthreads();
-        phase_lam(a, t0, nc, q, zv, sfac, lam);
+        phase_lam<SRC == kSrcTile>(a, t0, nc, q, zv, sfac, lam);
         __syncthreads();
     }
+}
+
+// Copy the window's outcomes [T][M] into LDS (tile form).
+__device__ void stage_obs(const AgentArgs &a, int agent, int *sobs)
+{
+    const int n = a.T * a.M;
+    for (int i = threadIdx.x; i < n; i += kThreads) sobs[i] = a.obs[(int64_t)agent * n + i];
 }
 
 // Copy the agent's B (fp32) or log B (fp64, lb) of every factor into tab.
@@ -408,11 +603,11 @@ __device__ void window_softmax(const AgentArgs &a, const int *sfac, const double
     __syncthreads();
 }
 
-// ALGO: BI_ALGO_VMP or BI_ALGO_MMP; GX: slices read from global memory; TB:
+// ALGO: BI_ALGO_VMP or BI_ALGO_MMP; SRC: where phase 1 reads the slices; TB:
 // every B-dependency list is {f} (the row / column transition products;
 // otherwise the general contractions of transition.h)
-template <int ALGO, bool GX, bool TB>
-__global__ __launch_bounds__(kThreads, 4) void agent_window_kernel(AgentArgs a)
+template <int ALGO, int SRC, bool TB>
+__global__ __launch_bounds__(kThreads, SRC == kSrcTile ? 3 : 4) void agent_window_kernel(AgentArgs a)
 {
     extern __shared__ double smem[];
     const int agent = blockIdx.x;
@@ -421,7 +616,9 @@ __global__ __launch_bounds__(kThreads, 4) void agent_window_kernel(AgentArgs a)
     const int nstg = a.stage == kStageWindow ? a.T : a.stage == kStageChunk ? a.nc : 0;
     double *btab = stg + (int64_t)nstg * a.sctx;
     int *sfac = reinterpret_cast<int *>(btab + a.bdoubles);
+    int *sobs = sfac + a.ntot;
     init_tables(a, sfac);
+    if (SRC == kSrcTile && !a.ll) stage_obs(a, agent, sobs);
     if (a.bst) stage_b(a, agent, ALGO == BI_ALGO_VMP, btab);
     if (a.stage == kStageWindow) stage_slices(a, agent, 0, a.T, stg);   // every iteration reads them from LDS
     __syncthreads();
@@ -430,7 +627,7 @@ __global__ __launch_bounds__(kThreads, 4) void agent_window_kernel(AgentArgs a)
     const int64_t am = a.shared ? 0 : agent;
     double *cur = qa, *nxt = qb;
     for (int k = 0; k < a.iters; ++k) {
-        window_lam<GX>(a, agent, cur, zv, stg, sfac, lam);
+        window_lam<SRC>(a, agent, cur, zv, stg, sfac, sobs, lam);
         // logits of every (t, state) into nxt, one thread per state
         for (int i = threadIdx.x; i < TN; i += kThreads) {
             const int t = i / a.ntot, j = i - t * a.ntot;
@@ -595,10 +792,9 @@ __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
         if (a.stage == kStageChunk) stage_slices(a, agent, t, 1, stg);   // step t's slices, for all its iterations
         __syncthreads();
         for (int k = 0; k < a.iters; ++k) {
-            phase_zv<GX>(a, agent, t, 1, cur, zv, stg,
-                     a.stage == kStageWindow ? t : 0);
+            phase_zv<GX>(a, agent, t, 1, cur, zv, stg, a.stage == kStageWindow ? t : 0);
             __syncthreads();
-            phase_lam(a, t, 1, cur, zv, sfac, lam);
+            phase_lam<false>(a, t, 1, cur, zv, sfac, lam);
             __syncthreads();
             // Jacobi: lam holds every factor's message from the previous iterate
             // (damped: the new marginal is formed in lam's row, then mixed
@@ -711,27 +907,62 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
             lds = fixed + (size_t)a.nc * per_ctx;
         }
     }
+    // VMP / MMP with slices from global memory: the tile form of phase 1 when
+    // its Z/V layout fits (per context: the Z partial sums of every column
+    // chunk and V), with the window's outcomes in LDS.  (FPI keeps one dot
+    // product per thread: the tile form measured 2% slower on the model
+    // sweep there, at three workgroups per CU instead of four.)
+    a.tile = 0;
+    if (a.stage == kStageNone && m->M <= kStageMaxM && algo != BI_ALGO_FPI) {
+        int zt = 0;
+        for (int i = 0; i < m->M; ++i) {
+            a.zt[i] = zt;
+            zt += tile_block(m->mods[i]);
+        }
+        a.zt[m->M] = zt;
+        const size_t pc = (size_t)zt * 8, so = (size_t)T * m->M * 4;
+        // the whole window in one chunk when it fits 80 KB, else as many
+        // contexts as 160 KB allow (chunks sized for three workgroups per CU
+        // measured 5% slower on the model sweep: more barriers per sweep)
+        const size_t fx = fixed + so;
+        size_t nc = T;
+        if (fx + nc * pc > budget2) nc = fx < kLdsMax ? (kLdsMax - fx) / pc : 0;
+        if (nc > (size_t)T) nc = T;
+        const size_t lt = fx + nc * pc;
+        if (nc >= 1 && lt <= kLdsMax) {
+            a.tile = 1;
+            a.nc = (int)nc;
+            a.zvpc = zt;
+            lds = lt;
+        }
+    }
     if (a.nc < 1 || lds > kLdsMax)
         return fail(BI_ERR_UNSUPPORTED, "agent working set (%zu bytes of LDS) exceeds the 160 KB budget", lds);
-    const bool gx = a.stage == kStageNone, tb = m->trivial_b;
-    // instantiation table [algo][gx][tb]
+    const int src = a.tile ? kSrcTile : a.stage == kStageNone ? kSrcGlobal : kSrcLds;
+    const bool tb = m->trivial_b;
+    // instantiation tables [src][tb]
     static const void *const kFilter[2][2] = {
         {(const void *)agent_filter_kernel<false, false>, (const void *)agent_filter_kernel<false, true>},
         {(const void *)agent_filter_kernel<true, false>, (const void *)agent_filter_kernel<true, true>}};
-    static const void *const kVmp[2][2] = {
-        {(const void *)agent_window_kernel<BI_ALGO_VMP, false, false>,
-         (const void *)agent_window_kernel<BI_ALGO_VMP, false, true>},
-        {(const void *)agent_window_kernel<BI_ALGO_VMP, true, false>,
-         (const void *)agent_window_kernel<BI_ALGO_VMP, true, true>}};
-    static const void *const kMmp[2][2] = {
-        {(const void *)agent_window_kernel<BI_ALGO_MMP, false, false>,
-         (const void *)agent_window_kernel<BI_ALGO_MMP, false, true>},
-        {(const void *)agent_window_kernel<BI_ALGO_MMP, true, false>,
-         (const void *)agent_window_kernel<BI_ALGO_MMP, true, true>}};
-    const void *fn = algo == BI_ALGO_FPI ? kFilter[gx][tb] : algo == BI_ALGO_VMP ? kVmp[gx][tb] : kMmp[gx][tb];
+    static const void *const kVmp[3][2] = {
+        {(const void *)agent_window_kernel<BI_ALGO_VMP, kSrcLds, false>,
+         (const void *)agent_window_kernel<BI_ALGO_VMP, kSrcLds, true>},
+        {(const void *)agent_window_kernel<BI_ALGO_VMP, kSrcGlobal, false>,
+         (const void *)agent_window_kernel<BI_ALGO_VMP, kSrcGlobal, true>},
+        {(const void *)agent_window_kernel<BI_ALGO_VMP, kSrcTile, false>,
+         (const void *)agent_window_kernel<BI_ALGO_VMP, kSrcTile, true>}};
+    static const void *const kMmp[3][2] = {
+        {(const void *)agent_window_kernel<BI_ALGO_MMP, kSrcLds, false>,
+         (const void *)agent_window_kernel<BI_ALGO_MMP, kSrcLds, true>},
+        {(const void *)agent_window_kernel<BI_ALGO_MMP, kSrcGlobal, false>,
+         (const void *)agent_window_kernel<BI_ALGO_MMP, kSrcGlobal, true>},
+        {(const void *)agent_window_kernel<BI_ALGO_MMP, kSrcTile, false>,
+         (const void *)agent_window_kernel<BI_ALGO_MMP, kSrcTile, true>}};
+    const void *fn = algo == BI_ALGO_FPI ? kFilter[src == kSrcGlobal][tb]
+                                         : algo == BI_ALGO_VMP ? kVmp[src][tb] : kMmp[src][tb];
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     if (e == hipSuccess) {
-        ProfScope p(algo == BI_ALGO_FPI ? "agent_filter" : "agent_window", stream);
+        ProfScope p(algo == BI_ALGO_FPI ? "agent_filter" : a.tile ? "agent_window_tile" : "agent_window", stream);
         void *args[] = {&a};
         e = hipLaunchKernel(fn, dim3(b), dim3(kThreads), args, lds, stream);
     }

@@ -200,29 +200,52 @@ __device__ inline double outer_dot(const double *x, int64_t stride, int len, con
     return acc;
 }
 
+// Weight of line i of a side with k factors f[0..k) of sizes n[0..k) (the
+// last factor fastest, as in the slice layout): the product of the factors'
+// marginals at i's digits, factor position skip (-1: none) left out.  Used
+// for sides of more than two factors (dependency lists of 5 to 10 factors).
+__device__ inline double side_weight(const AgentArgs &a, const double *qt, const int32_t *f, const int32_t *n, int k,
+                                     int i, int skip = -1)
+{
+    double w = 1.0;
+    for (int g = k - 1; g >= 0; --g) {
+        const int d = i % n[g];
+        i /= n[g];
+        if (g != skip) w *= qt[a.facs[f[g]].q_off + d];
+    }
+    return w;
+}
+
 // One Z or V output of an observed slice X (row stride xs) for the marginals
 // qt: j < R gives Z[j] = sum_c X[j][c] t[c], j = R + col gives
 // V[col] = sum_r s[r] X[r][col] (t, s: outer products of the column and row
 // factors' marginals).
+template <bool WIDE>
 __device__ inline double zv_one(const AgentArgs &a, const ModDesc &md, const double *X, int64_t xs,
                                 const double *qt, int j)
 {
     const int R = md.R;
     if (j < R) {
         if (md.nrow == 0) return 0.0;   // Z of a rank-0 row side feeds no message
+        if (WIDE && md.ncol > 2)
+            return dot8<8>(md.C, [&](int c) { return X[(int64_t)j * xs + c]; },
+                           [&](int c) { return side_weight(a, qt, md.cf, md.cn, md.ncol, c); });
         const double *q1 = md.ncol == 2 ? qt + a.facs[md.cf[1]].q_off : nullptr;
         return outer_dot(X + (int64_t)j * xs, 1, md.C, qt + a.facs[md.cf[0]].q_off, q1,
                          md.ncol == 2 ? md.cn[1] : 1);
     }
     const int col = j - R;
     if (md.nrow == 0) return X[col];
+    if (WIDE && md.nrow > 2)
+        return dot8<8>(R, [&](int r) { return X[(int64_t)r * xs + col]; },
+                       [&](int r) { return side_weight(a, qt, md.rf, md.rn, md.nrow, r); });
     const double *q1 = md.nrow == 2 ? qt + a.facs[md.rf[1]].q_off : nullptr;
     return outer_dot(X + col, xs, R, qt + a.facs[md.rf[0]].q_off, q1, md.nrow == 2 ? md.rn[1] : 1);
 }
 
 // The same output with the nested loops of the two-sided view, for slices
 // staged in LDS (short latency: no batching, fewer registers).
-template <int BT>
+template <int BT, bool WIDE>
 __device__ inline double zv_one_lds(const AgentArgs &a, const ModDesc &md, const double *X, int64_t xs,
                                     const double *qt, int j)
 {
@@ -232,7 +255,10 @@ __device__ inline double zv_one_lds(const AgentArgs &a, const ModDesc &md, const
         if (md.nrow > 0) {  // (Z of a rank-0 row side feeds no message)
             const double *row = X + (int64_t)j * xs;
             const double *q0 = qt + a.facs[md.cf[0]].q_off;
-            if (md.ncol == 1) {
+            if (WIDE && md.ncol > 2) {
+                acc = dot8<BT>(md.C, [&](int cc) { return row[cc]; },
+                               [&](int cc) { return side_weight(a, qt, md.cf, md.cn, md.ncol, cc); });
+            } else if (md.ncol == 1) {
                 acc = dot8<BT>(md.C, [&](int cc) { return row[cc]; }, [&](int cc) { return q0[cc]; });
             } else {
                 const double *q1 = qt + a.facs[md.cf[1]].q_off;
@@ -248,6 +274,9 @@ __device__ inline double zv_one_lds(const AgentArgs &a, const ModDesc &md, const
         const int col = j - R;
         if (md.nrow == 0) {
             acc = X[col];
+        } else if (WIDE && md.nrow > 2) {
+            acc = dot8<BT>(R, [&](int r) { return X[(int64_t)r * xs + col]; },
+                           [&](int r) { return side_weight(a, qt, md.rf, md.rn, md.nrow, r); });
         } else if (md.nrow == 1) {
             const double *q0 = qt + a.facs[md.rf[0]].q_off;
             acc = dot8<BT>(R, [&](int r) { return q0[r]; }, [&](int r) { return X[(int64_t)r * xs + col]; });
@@ -309,7 +338,8 @@ __device__ void stage_slices(const AgentArgs &a, int agent, int t0, int nc, doub
 // q: marginals of context t at q + t * ntot.  With staged slices, X of
 // context t0 + c comes from stg + (sc0 + c) * sctx (LDS); otherwise from the
 // packed buffer.
-template <bool GX, int BT>   // GX: slices read from global memory (batched loads); else staged in LDS
+// WIDE: some modality has a side of more than two factors
+template <bool GX, int BT, bool WIDE>   // GX: slices read from global memory (batched loads); else staged in LDS
 __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv,
                          const double *stg, int sc0)
 {
@@ -330,12 +360,12 @@ __device__ void phase_zv(const AgentArgs &a, int agent, int t0, int nc, const do
             const double *qt = q + t * a.ntot;
             double acc;
             if (!GX) {
-                acc = zv_one_lds<BT>(a, md, stg + (int64_t)(sc0 + c) * a.sctx + a.po[m], Cp + 1, qt, j);
+                acc = zv_one_lds<BT, WIDE>(a, md, stg + (int64_t)(sc0 + c) * a.sctx + a.po[m], Cp + 1, qt, j);
             } else if (a.ll) {
-                acc = zv_one(a, md, a.ll + ((int64_t)agent * a.T + t) * a.llpc + llo, Cp, qt, j);
+                acc = zv_one<WIDE>(a, md, a.ll + ((int64_t)agent * a.T + t) * a.llpc + llo, Cp, qt, j);
             } else {
                 const int o = a.obs[((int64_t)agent * a.T + t) * a.M + m];
-                acc = zv_one(a, md, la + (int64_t)o * md.slice, Cp, qt, j);
+                acc = zv_one<WIDE>(a, md, la + (int64_t)o * md.slice, Cp, qt, j);
             }
             zv[c * a.zvpc + md.zv_off + j] = acc;
         }
@@ -411,7 +441,7 @@ constexpr int log2_floor(int x) { return x <= 1 ? 0 : 1 + log2_floor(x / 2); }
 // One modality's units of contexts [t0, t0 + nc): RB rows per block (every
 // row of a block loaded before any is used), P >= RB the power of two the
 // segment reduction works on.
-template <int RB>
+template <int RB, bool WIDE>
 __device__ void zv_tile_modality(const AgentArgs &a, const ModDesc &md, int agent, int m, int t0, int nc,
                                  const double *q, double *zv, const int *sobs, int64_t llo, int first)
 {
@@ -439,12 +469,17 @@ __device__ void zv_tile_modality(const AgentArgs &a, const ModDesc &md, int agen
         const int colc = min(col, (C - 1) & ~1);
         double w0 = 0.0, w1 = 0.0;
         if (zrow) {
-            const double *qc0 = qt + a.facs[md.cf[0]].q_off;
-            const double *qc1 = md.ncol == 2 ? qt + a.facs[md.cf[1]].q_off : nullptr;
             const int ca = min(col, C - 1), cbb = min(col + 1, C - 1);
-            const int a0 = ca / cn1, a1 = ca - a0 * cn1, b0 = cbb / cn1, b1 = cbb - b0 * cn1;
-            w0 = qc1 ? qc0[a0] * qc1[a1] : qc0[a0];
-            w1 = qc1 ? qc0[b0] * qc1[b1] : qc0[b0];
+            if (WIDE && md.ncol > 2) {
+                w0 = side_weight(a, qt, md.cf, md.cn, md.ncol, ca);
+                w1 = side_weight(a, qt, md.cf, md.cn, md.ncol, cbb);
+            } else {
+                const double *qc0 = qt + a.facs[md.cf[0]].q_off;
+                const double *qc1 = md.ncol == 2 ? qt + a.facs[md.cf[1]].q_off : nullptr;
+                const int a0 = ca / cn1, a1 = ca - a0 * cn1, b0 = cbb / cn1, b1 = cbb - b0 * cn1;
+                w0 = qc1 ? qc0[a0] * qc1[a1] : qc0[a0];
+                w1 = qc1 ? qc0[b0] * qc1[b1] : qc0[b0];
+            }
             w0 = col < C ? w0 : 0.0;
             w1 = col + 1 < C ? w1 : 0.0;
         }
@@ -462,7 +497,10 @@ __device__ void zv_tile_modality(const AgentArgs &a, const ModDesc &md, int agen
 #pragma unroll
             for (int i = 0; i < RB; ++i) {
                 double sw = 1.0;
-                if (md.nrow > 0) sw = qr1 ? qr0[min(i0, md.rn[0] - 1)] * qr1[i1] : qr0[min(r0 + i, R - 1)];
+                if (WIDE && md.nrow > 2)
+                    sw = side_weight(a, qt, md.rf, md.rn, md.nrow, min(r0 + i, R - 1));
+                else if (md.nrow > 0)
+                    sw = qr1 ? qr0[min(i0, md.rn[0] - 1)] * qr1[i1] : qr0[min(r0 + i, R - 1)];
                 sw = r0 + i < R ? sw : 0.0;
                 if (++i1 == rn1) {
                     i1 = 0;
@@ -487,6 +525,7 @@ __device__ void zv_tile_modality(const AgentArgs &a, const ModDesc &md, int agen
     }
 }
 
+template <bool WIDE>
 __device__ void phase_zv_tile(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv,
                               const int *sobs)
 {
@@ -496,15 +535,15 @@ __device__ void phase_zv_tile(const AgentArgs &a, int agent, int t0, int nc, con
         const ModDesc &md = a.mods[m];
         const int R = md.R;
         if (R <= 1)
-            zv_tile_modality<1>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+            zv_tile_modality<1, WIDE>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
         else if (R <= 2)
-            zv_tile_modality<2>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+            zv_tile_modality<2, WIDE>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
         else if (R <= 4)
-            zv_tile_modality<4>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+            zv_tile_modality<4, WIDE>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
         else if (R <= 8)
-            zv_tile_modality<8>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+            zv_tile_modality<8, WIDE>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
         else   // (blocks of 12 rows beyond: 16 would spill at three workgroups per CU)
-            zv_tile_modality<12>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
+            zv_tile_modality<12, WIDE>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
         first += nc * tile_nch(md.C);
         llo += md.slice;
     }
@@ -512,7 +551,7 @@ __device__ void phase_zv_tile(const AgentArgs &a, int agent, int t0, int nc, con
 
 // Phase 2: lam of contexts [t0, t0 + nc) into lam[t][ntot].  TILE: Z/V in the
 // tile layout (Z as per-chunk partial sums).
-template <bool TILE, int BT>
+template <bool TILE, int BT, bool WIDE>
 __device__ void phase_lam(const AgentArgs &a, int t0, int nc, const double *q, const double *zv, const int *sfac,
                           double *lam)
 {
@@ -533,7 +572,26 @@ __device__ void phase_lam(const AgentArgs &a, int t0, int nc, const double *q, c
                 for (int cb = 1; cb < nch; ++cb) z += Z[cb * md.R + k];
                 return z;
             };
-            if (md.nrow >= 1 && md.rf[0] == f) {
+            if (WIDE && (md.nrow > 2 || md.ncol > 2)) {
+                // a side of more than two factors: the lines whose digit of f
+                // is s, weighted by the side's other marginals
+                for (int side = 0; side < 2; ++side) {
+                    const int k = side ? md.ncol : md.nrow;
+                    const int32_t *sf = side ? md.cf : md.rf, *sn = side ? md.cn : md.rn;
+                    for (int p = 0; p < k; ++p) {
+                        if (sf[p] != f) continue;
+                        int low = 1;
+                        for (int g = p + 1; g < k; ++g) low *= sn[g];
+                        const int np = sn[p], len = (side ? md.C : md.R) / np;
+                        auto line = [&](int jj) {
+                            const int hi = jj / low;
+                            return (hi * np + s) * low + (jj - hi * low);
+                        };
+                        acc += dot8<BT>(len, [&](int jj) { return side ? V[line(jj)] : zat(line(jj)); },
+                                        [&](int jj) { return side_weight(a, qt, sf, sn, k, line(jj), p); });
+                    }
+                }
+            } else if (md.nrow >= 1 && md.rf[0] == f) {
                 if (md.nrow == 1) {
                     acc += zat(s);
                 } else {
@@ -584,7 +642,7 @@ template <int SRC> constexpr int kBatch = SRC == kSrcLdsShort ? 1 : 8;
 
 // lam for every context of the window (phases 1 and 2 over context chunks;
 // staged chunks are copied to LDS first unless the whole window is resident).
-template <int SRC>
+template <int SRC, bool WIDE>
 __device__ void window_lam(const AgentArgs &a, int agent, const double *q, double *zv, double *stg, const int *sfac,
                            const int *sobs, double *lam)
 {
@@ -595,11 +653,12 @@ __device__ void window_lam(const AgentArgs &a, int agent, const double *q, doubl
             __syncthreads();
         }
         if (SRC == kSrcTile)
-            phase_zv_tile(a, agent, t0, nc, q, zv, sobs);
+            phase_zv_tile<WIDE>(a, agent, t0, nc, q, zv, sobs);
         else
-            phase_zv<SRC == kSrcGlobal, kBatch<SRC>>(a, agent, t0, nc, q, zv, stg, a.stage == kStageWindow ? t0 : 0);
+            phase_zv<SRC == kSrcGlobal, kBatch<SRC>, WIDE>(a, agent, t0, nc, q, zv, stg,
+                                                           a.stage == kStageWindow ? t0 : 0);
         __syncthreads();
-        phase_lam<SRC == kSrcTile, kBatch<SRC>>(a, t0, nc, q, zv, sfac, lam);
+        phase_lam<SRC == kSrcTile, kBatch<SRC>, WIDE>(a, t0, nc, q, zv, sfac, lam);
         __syncthreads();
     }
 }
@@ -669,7 +728,7 @@ __device__ void window_softmax(const AgentArgs &a, const int *sfac, const double
 // ALGO: BI_ALGO_VMP or BI_ALGO_MMP; SRC: where phase 1 reads the slices; TB:
 // every B-dependency list is {f} (the row / column transition products;
 // otherwise the general contractions of transition.h)
-template <int ALGO, int SRC, bool TB>
+template <int ALGO, int SRC, bool TB, bool WIDE>
 __global__ __launch_bounds__(kThreads, SRC == kSrcTile ? 3 : 4) void agent_window_kernel(AgentArgs a)
 {
     extern __shared__ double smem[];
@@ -690,7 +749,7 @@ __global__ __launch_bounds__(kThreads, SRC == kSrcTile ? 3 : 4) void agent_windo
     const int64_t am = a.shared ? 0 : agent;
     double *cur = qa, *nxt = qb;
     for (int k = 0; k < a.iters; ++k) {
-        window_lam<SRC>(a, agent, cur, zv, stg, sfac, sobs, lam);
+        window_lam<SRC, WIDE>(a, agent, cur, zv, stg, sfac, sobs, lam);
         // logits of every (t, state) into nxt, one thread per state
         for (int i = threadIdx.x; i < TN; i += kThreads) {
             const int t = i / a.ntot, j = i - t * a.ntot;
@@ -791,7 +850,7 @@ __global__ __launch_bounds__(kThreads, SRC == kSrcTile ? 3 : 4) void agent_windo
     for (int i = threadIdx.x; i < TN; i += kThreads) out[i] = (float)cur[i];
 }
 
-template <bool GX, bool TB>   // slices read from global memory; trivial B-dependency lists
+template <bool GX, bool TB, bool WIDE>   // slices read from global memory; trivial B-dependency lists
 __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
 {
     extern __shared__ double smem[];
@@ -847,9 +906,9 @@ __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
         if (a.stage == kStageChunk) stage_slices(a, agent, t, 1, stg);   // step t's slices, for all its iterations
         __syncthreads();
         for (int k = 0; k < a.iters; ++k) {
-            phase_zv<GX, 8>(a, agent, t, 1, cur, zv, stg, a.stage == kStageWindow ? t : 0);
+            phase_zv<GX, 8, WIDE>(a, agent, t, 1, cur, zv, stg, a.stage == kStageWindow ? t : 0);
             __syncthreads();
-            phase_lam<false, 8>(a, t, 1, cur, zv, sfac, lam);
+            phase_lam<false, 8, WIDE>(a, t, 1, cur, zv, sfac, lam);
             __syncthreads();
             // Jacobi: lam holds every factor's message from the previous iterate
             // (damped: the new marginal is formed in lam's row, then mixed
@@ -1001,30 +1060,31 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
         if (longest <= 8) src = kSrcLdsShort;
     }
     const bool tb = m->trivial_b;
-    // instantiation tables [src][tb]
-    static const void *const kFilter[2][2] = {
-        {(const void *)agent_filter_kernel<false, false>, (const void *)agent_filter_kernel<false, true>},
-        {(const void *)agent_filter_kernel<true, false>, (const void *)agent_filter_kernel<true, true>}};
-    static const void *const kVmp[4][2] = {
-        {(const void *)agent_window_kernel<BI_ALGO_VMP, kSrcLds, false>,
-         (const void *)agent_window_kernel<BI_ALGO_VMP, kSrcLds, true>},
-        {(const void *)agent_window_kernel<BI_ALGO_VMP, kSrcGlobal, false>,
-         (const void *)agent_window_kernel<BI_ALGO_VMP, kSrcGlobal, true>},
-        {(const void *)agent_window_kernel<BI_ALGO_VMP, kSrcTile, false>,
-         (const void *)agent_window_kernel<BI_ALGO_VMP, kSrcTile, true>},
-        {(const void *)agent_window_kernel<BI_ALGO_VMP, kSrcLdsShort, false>,
-         (const void *)agent_window_kernel<BI_ALGO_VMP, kSrcLdsShort, true>}};
-    static const void *const kMmp[4][2] = {
-        {(const void *)agent_window_kernel<BI_ALGO_MMP, kSrcLds, false>,
-         (const void *)agent_window_kernel<BI_ALGO_MMP, kSrcLds, true>},
-        {(const void *)agent_window_kernel<BI_ALGO_MMP, kSrcGlobal, false>,
-         (const void *)agent_window_kernel<BI_ALGO_MMP, kSrcGlobal, true>},
-        {(const void *)agent_window_kernel<BI_ALGO_MMP, kSrcTile, false>,
-         (const void *)agent_window_kernel<BI_ALGO_MMP, kSrcTile, true>},
-        {(const void *)agent_window_kernel<BI_ALGO_MMP, kSrcLdsShort, false>,
-         (const void *)agent_window_kernel<BI_ALGO_MMP, kSrcLdsShort, true>}};
-    const void *fn = algo == BI_ALGO_FPI ? kFilter[a.stage == kStageNone][tb]
-                                         : algo == BI_ALGO_VMP ? kVmp[src][tb] : kMmp[src][tb];
+    // instantiation tables [src][tb][wide]; wide: some modality has a side of
+    // more than two factors (the general side code is compiled only there)
+    bool wide = false;
+    for (const ModDesc &md : m->mods) wide = wide || md.nrow > 2 || md.ncol > 2;
+#define BI_FILTER(GX, TB) \
+    { (const void *)agent_filter_kernel<GX, TB, false>, (const void *)agent_filter_kernel<GX, TB, true> }
+#define BI_WINDOW(ALGO, SRC, TB) \
+    { (const void *)agent_window_kernel<ALGO, SRC, TB, false>, (const void *)agent_window_kernel<ALGO, SRC, TB, true> }
+    static const void *const kFilter[2][2][2] = {{BI_FILTER(false, false), BI_FILTER(false, true)},
+                                                 {BI_FILTER(true, false), BI_FILTER(true, true)}};
+    static const void *const kVmp[4][2][2] = {
+        {BI_WINDOW(BI_ALGO_VMP, kSrcLds, false), BI_WINDOW(BI_ALGO_VMP, kSrcLds, true)},
+        {BI_WINDOW(BI_ALGO_VMP, kSrcGlobal, false), BI_WINDOW(BI_ALGO_VMP, kSrcGlobal, true)},
+        {BI_WINDOW(BI_ALGO_VMP, kSrcTile, false), BI_WINDOW(BI_ALGO_VMP, kSrcTile, true)},
+        {BI_WINDOW(BI_ALGO_VMP, kSrcLdsShort, false), BI_WINDOW(BI_ALGO_VMP, kSrcLdsShort, true)}};
+    static const void *const kMmp[4][2][2] = {
+        {BI_WINDOW(BI_ALGO_MMP, kSrcLds, false), BI_WINDOW(BI_ALGO_MMP, kSrcLds, true)},
+        {BI_WINDOW(BI_ALGO_MMP, kSrcGlobal, false), BI_WINDOW(BI_ALGO_MMP, kSrcGlobal, true)},
+        {BI_WINDOW(BI_ALGO_MMP, kSrcTile, false), BI_WINDOW(BI_ALGO_MMP, kSrcTile, true)},
+        {BI_WINDOW(BI_ALGO_MMP, kSrcLdsShort, false), BI_WINDOW(BI_ALGO_MMP, kSrcLdsShort, true)}};
+#undef BI_FILTER
+#undef BI_WINDOW
+    const void *fn = algo == BI_ALGO_FPI ? kFilter[a.stage == kStageNone][tb][wide]
+                     : algo == BI_ALGO_VMP ? kVmp[src][tb][wide]
+                                           : kMmp[src][tb][wide];
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     if (e == hipSuccess) {
         ProfScope p(algo == BI_ALGO_FPI ? "agent_filter" : a.tile ? "agent_window_tile" : "agent_window", stream);

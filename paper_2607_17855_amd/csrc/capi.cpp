@@ -50,6 +50,9 @@ const char *stream_refusal(const bi_model *m, int algo, bool sparse)
         return sparse ? "not packed with BI_SPARSE_A" : "not packed with BI_FAST_F32";
     if (m->mb != 1) return "per-agent model (the streaming kernels share one model among all agents)";
     if (algo == BI_ALGO_FPI) return "FPI runs agent-resident (sequential over the window)";
+    for (const bi::ModDesc &md : m->mods)
+        if (md.nrow > bi::kStreamSide || md.ncol > bi::kStreamSide)
+            return "a modality depends on more than 4 factors (the streaming layouts serve up to 2 per side)";
     if (sparse ? bi::sparse_eligible(m, algo) : bi::stream_eligible(m, algo)) return nullptr;
     return "a modality's shape exceeds the streaming kernels' limits (outcomes, modalities or LDS tiles)";
 }

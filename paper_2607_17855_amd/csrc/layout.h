@@ -61,7 +61,8 @@
 namespace bi {
 
 constexpr double kEps = 1e-16;
-constexpr int kMaxSide = 2;   // factors per side of the two-sided view (rank <= 4)
+constexpr int kMaxSide = 5;      // factors per side of the two-sided view (dependency lists of up to 10)
+constexpr int kStreamSide = 2;   // factors per side the streaming layouts serve (rank <= 4)
 constexpr int kAlign = 256;   // byte alignment of every array in the packed buffer
 
 struct ModDesc {

@@ -160,11 +160,14 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
         const int32_t *dl = m->dep.data() + m->dep_off[mm];
         const int k = m->dep_off[mm + 1] - m->dep_off[mm];
         m->max_rank = std::max(m->max_rank, k);
-        // rows = first p factors, columns = the rest; 0 <= p <= 2, 1 <= k-p <= 2,
-        // chosen to balance the two sides
+        // rows = first p factors, columns = the rest, at most L per side (L =
+        // kStreamSide for lists of up to 4 factors, which keeps them in the
+        // streaming layouts' shape, else kMaxSide), 1 <= k-p, chosen to
+        // balance the two sides
+        const int L = k <= 2 * kStreamSide ? kStreamSide : kMaxSide;
         int best_p = -1;
         int64_t best = INT64_MAX;
-        for (int p = std::max(0, k - kMaxSide); p <= std::min(kMaxSide, k - 1); ++p) {
+        for (int p = std::max(0, k - L); p <= std::min(L, k - 1); ++p) {
             const int64_t R = prod(m->n.data(), dl, p), C = prod(m->n.data(), dl + p, k - p);
             const int64_t cost = R > C ? R - C : C - R;
             if (cost < best) {
@@ -197,21 +200,25 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
         md.la_off = off;
         md.la_agent = m->mb == 1 ? 0 : (int64_t)md.K * md.slice;
         off = align_up(off + 8 * (int64_t)m->mb * md.K * md.slice, kAlign);
+        // the streaming layouts (fp32 copy, fp16 pairs, sparse planes) serve
+        // modalities with at most kStreamSide factors per side; a wider one
+        // leaves its model to the agent-resident kernels
+        const bool narrow = p <= kStreamSide && k - p <= kStreamSide;
         md.la32_off = -1;
-        if (flags & BI_FAST_F32) {
+        if ((flags & BI_FAST_F32) && narrow) {
             md.la32_off = off;
             off = align_up(off + 4 * (int64_t)m->mb * md.K * md.slice, kAlign);
         }
         md.lp16_off = -1;
         // dense pairs (the matrix-core kernels serve shared models; with the
         // sparse layout the pairs are stored with the nonzeros instead)
-        if ((flags & BI_F16_PAIRS) && (flags & BI_DENSE_A) && m->mb == 1) {
+        if ((flags & BI_F16_PAIRS) && (flags & BI_DENSE_A) && m->mb == 1 && narrow) {
             md.lp16_off = off;
             off = align_up(off + 4 * (int64_t)md.K * md.slice, kAlign);
         }
         md.csr_ptr_off = md.csr_ent_off = md.csc_ptr_off = md.csc_ent_off = -1;
         md.nnz = 0;
-        if (flags & BI_SPARSE_A) {
+        if ((flags & BI_SPARSE_A) && narrow) {
             // exact entry count when A is given, else an upper bound (dense)
             int64_t nnz = (int64_t)md.K * R * C;
             if (A) {

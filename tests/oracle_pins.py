@@ -90,6 +90,29 @@ def pin_fpi_bruteforce(infer, seeds=range(12)):
     return err
 
 
+def pin_long_dependency_lists(infer):
+    """Dependency lists of 5 to 7 factors (the paper's random population draws
+    list lengths up to 10, Sec. V-A; any A-dependencies, Sec. III-B): FPI
+    against the enumerated single-step joint."""
+    err = 0.0
+    cases = [
+        # (n, deps, K)
+        ([2, 2, 3, 2, 2, 2], [[0, 1, 2, 3, 4], [2, 5]], [3, 2]),
+        ([2, 3, 2, 2, 2, 2], [[0, 1, 2, 3, 4, 5], [1], [0, 3, 5]], [2, 3, 4]),
+        ([2, 2, 2, 2, 2, 2, 3], [[0, 1, 2, 3, 4, 5, 6]], [4]),
+    ]
+    for i, (n, deps, K) in enumerate(cases):
+        rng = np.random.Generator(np.random.PCG64(1700 + i))
+        F = len(n)
+        model = synth.make_model(rng, n, [2] * F, K, deps, 2, 0.8, 1.0, uniform_D=False)
+        obs, act = synth.sample_sequences(rng, model, 2, 3)
+        for iters in (1, 4):
+            ref = bf.fpi_bruteforce(model, obs, act, iters)
+            q = infer("fpi", model, obs, act, iters)
+            err = max(err, float(np.abs(q - ref).max()))
+    return err
+
+
 def pin_factorised_exact(infer):
     """Every dependency list a singleton: the joint factorises over factors, so
     filtering is exact per factor and FPI equals a forward filter per factor."""
@@ -602,6 +625,7 @@ ALL_PINS = {
     "vmp_bruteforce": (pin_vmp_bruteforce, 1e-12),
     "fpi_bruteforce": (pin_fpi_bruteforce, 1e-12),
     "factorised_exact": (pin_factorised_exact, 1e-12),
+    "long_dependency_lists": (pin_long_dependency_lists, 1e-12),
     "t1_identity": (pin_t1_identity, 1e-12),
     "iid_closed_forms": (pin_iid_closed_forms, 1e-12),
     "mmp_permutation_smoothing": (pin_mmp_permutation_smoothing, 1e-10),

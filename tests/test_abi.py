@@ -36,8 +36,8 @@ class ModDesc(ctypes.Structure):
     _fields_ = [("la_off", ctypes.c_int64), ("la_agent", ctypes.c_int64), ("K", ctypes.c_int32),
                 ("slice", ctypes.c_int32), ("rank", ctypes.c_int32), ("R", ctypes.c_int32), ("C", ctypes.c_int32),
                 ("Cp", ctypes.c_int32), ("nrow", ctypes.c_int32), ("ncol", ctypes.c_int32),
-                ("rf", ctypes.c_int32 * 2), ("rn", ctypes.c_int32 * 2), ("cf", ctypes.c_int32 * 2),
-                ("cn", ctypes.c_int32 * 2), ("zv_off", ctypes.c_int32), ("dsum", ctypes.c_int32),
+                ("rf", ctypes.c_int32 * 5), ("rn", ctypes.c_int32 * 5), ("cf", ctypes.c_int32 * 5),
+                ("cn", ctypes.c_int32 * 5), ("zv_off", ctypes.c_int32), ("dsum", ctypes.c_int32),
                 ("la32_off", ctypes.c_int64), ("csr_ptr_off", ctypes.c_int64), ("csr_ent_off", ctypes.c_int64),
                 ("csc_ptr_off", ctypes.c_int64), ("csc_ent_off", ctypes.c_int64), ("nnz", ctypes.c_int64),
                 ("lp16_off", ctypes.c_int64), ("sq_ptr_off", ctypes.c_int64 * 2), ("sq_ent_off", ctypes.c_int64 * 2),
@@ -129,7 +129,8 @@ def test_plan_rejects_bad_descriptors():
     assert _desc_err([0], [1], [2], [[0]]) == bi.BI_ERR_SHAPE               # no states
     assert _desc_err([3], [0], [2], [[0]]) == bi.BI_ERR_SHAPE               # no actions
     assert _desc_err([3], [1], [0], [[0]]) == bi.BI_ERR_SHAPE               # no outcomes
-    assert _desc_err([2] * 5, [1] * 5, [2], [[0, 1, 2, 3, 4]]) == bi.BI_ERR_UNSUPPORTED
+    assert _desc_err([2] * 11, [1] * 11, [2], [list(range(11))]) == bi.BI_ERR_UNSUPPORTED   # lists of up to 10
+    assert bi.bi_plan_model([2] * 10, [1] * 10, [2], [list(range(10))], 1, bi.BI_DENSE_A) > 0
     assert _desc_err([3], [1], [2], [[0]], mb=0) == bi.BI_ERR_INVALID_ARG
     assert _desc_err([3], [1], [2], [[0]], flags=3) == bi.BI_ERR_INVALID_ARG
     assert _desc_err([3], [1], [2], [[0]], flags=64) == bi.BI_ERR_INVALID_ARG
@@ -783,3 +784,36 @@ def test_static_scratch_entry_refuses_before_any_launch():
             assert why in bi.bi_last_error()
         finally:
             bi.bi_free_model(h)
+
+
+@pytest.mark.parametrize("flags", [bi.BI_DENSE_A, bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS])
+def test_host_pack_long_dependency_lists(flags):
+    """Lists of 5 to 10 factors: up to 5 factors per side of the two-sided
+    view, the slices stored like any other; the streaming layouts (fp32 copy,
+    fp16 pairs, sparse planes) exist only for modalities with at most 2
+    factors per side, and the model is refused by the streaming families."""
+    rng = np.random.Generator(np.random.PCG64(77))
+    n = [2, 3, 2, 2, 2, 2, 2, 2, 3, 2]
+    deps = [list(range(10)), [1, 4, 7], [0, 2, 5, 8, 9], [3, 6]]
+    K = [3, 4, 2, 3]
+    model = synth.make_model(rng, n, [1] * 10, K, deps, 1, 1.0, 1.0)
+    m = model
+    h, img = bi.bi_pack_model_host(m.n, m.U, m.K, m.deps, m.mb, m.A, m.B, m.D, flags=flags)
+    try:
+        mods, _ = _descs(img, m.M, m.F)
+        for mi, d in enumerate(m.deps):
+            md = mods[mi]
+            assert md.rank == len(d) and md.nrow + md.ncol == len(d) and max(md.nrow, md.ncol) <= 5
+            assert [md.rf[i] for i in range(md.nrow)] + [md.cf[i] for i in range(md.ncol)] == d
+            assert md.R == int(np.prod([m.n[f] for f in d[:md.nrow]]))
+            assert md.C == int(np.prod([m.n[f] for f in d[md.nrow:]]))
+            for o in range(m.K[mi]):
+                X = img[md.la_off + 8 * o * md.slice:md.la_off + 8 * (o + 1) * md.slice].view(np.float64)
+                X = X.reshape(md.R, md.Cp)
+                shift = bfm.LN(m.A[mi][0, o]).reshape(md.R, md.C) - X[:, :md.C]
+                assert np.ptp(shift) < 1e-12
+            narrow = md.nrow <= 2 and md.ncol <= 2
+            if flags != bi.BI_DENSE_A:
+                assert (md.la32_off >= 0) == narrow and (md.csr_ptr_off >= 0) == narrow
+    finally:
+        bi.bi_free_model(h)

@@ -6,8 +6,10 @@
  * The generative model is the factorised POMDP of Sec. III-B of "A
  * Hardware-oriented Approach for Efficient Bayesian Inference Computation and
  * Deployment" (joint over o_{1:T}, s_{1:T} given u_{1:T-1}; emission tensors
- * A_m with A-dependency lists of up to 4 factors, transition tensors B_f with
- * B-dependency lists of up to 4 factors, prior D).  The three updates are built from the likelihood
+ * A_m with A-dependency lists of up to 10 factors, transition tensors B_f
+ * with B-dependency lists of up to 4 factors, prior D; lists of more than 4
+ * likelihood factors run on the agent-resident kernels only).  The three
+ * updates are built from the likelihood
  * and transition messages of Sec. IV, each an instance of the coordinate
  * update of Sec. III-A; the exact readings are stated per entry point.
  *

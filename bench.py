@@ -664,7 +664,7 @@ def bench_agent(args, bi, synth, torch, dev):
     timed()
     prof = bi.bi_profile_end()
     bu = w.b * w.T * w.iters
-    cls = "agent_filter" if algo == "fpi" else "agent_window_tile" if "agent_window_tile" in prof else "agent_window"
+    cls = next(k for k in ("agent_filter_tile", "agent_filter", "agent_window_tile", "agent_window") if k in prof)
     launches, total_ms = prof[cls]
     avg_ms = total_ms / max(launches, 1)
     fl, nb = agent_work(w.model, w.T, algo)

@@ -71,6 +71,7 @@ struct AgentArgs {
     // the Z partial sums of its column chunks, [chunk][R] (row side of rank
     // >= 1 only), then V [C].  The window's outcomes are copied to LDS.
     int tile;
+    unsigned tilemask;   // bit m: modality m in the tile form (else one dot product per thread, Z [R] then V [C])
     int zt[kStageMaxM + 1];
     double tau;            // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
     float *q;
@@ -393,8 +394,18 @@ constexpr int kTileCols = 2 * kSeg;      // columns per unit
 
 __host__ __device__ constexpr int tile_nch(int C) { return (C + kTileCols - 1) / kTileCols; }
 
-// doubles of modality md's block in the tile layout
-__host__ __device__ inline int tile_block(const ModDesc &md) { return (md.nrow > 0 ? tile_nch(md.C) * md.R : 0) + md.C; }
+// FPI (one context per step): a slice with more rows than this (a tall one)
+// has too few tile units, each walking its row blocks one after another, and
+// takes one dot product per thread instead (up to 3x faster on such calls;
+// the window kernels, with a chunk of contexts per phase, are faster with
+// every modality in the tile form)
+constexpr int kTileMaxRows = 96;
+
+// doubles of modality md's block in the tile layout (tiled: in the tile form)
+__host__ __device__ inline int tile_block(const ModDesc &md, bool tiled)
+{
+    return tiled ? (md.nrow > 0 ? tile_nch(md.C) * md.R : 0) + md.C : md.R + md.C;
+}
 
 // DPP lane pairings inside a row of 16 lanes: lane i with i ^ 15 (row_mirror),
 // i ^ 7 (row_half_mirror), i ^ 3 and i ^ 1 (quad permutations).  Partners of
@@ -525,15 +536,41 @@ __device__ void zv_tile_modality(const AgentArgs &a, const ModDesc &md, int agen
     }
 }
 
+// A modality of the tile layout outside the tile form: one Z or V output per
+// thread (as phase_zv reads from global memory), written to its block.
 template <bool WIDE>
+__device__ void zv_thread_modality(const AgentArgs &a, const ModDesc &md, int agent, int m, int t0, int nc,
+                                   const double *q, double *zv, const int *sobs, int64_t llo, int first)
+{
+    const int per = md.R + md.C, cnt = nc * per;
+    const double *la = at<double>(a.base, md.la_off) + (a.shared ? 0 : (int64_t)agent * md.la_agent);
+    int i = (int)threadIdx.x - first % kThreads;
+    if (i < 0) i += kThreads;
+    for (; i < cnt; i += kThreads) {
+        const int c = i / per, j = i - c * per;
+        const int t = t0 + c;
+        const double *X = a.ll ? a.ll + ((int64_t)agent * a.T + t) * a.llpc + llo
+                               : la + (int64_t)sobs[t * a.M + m] * md.slice;
+        zv[c * a.zvpc + a.zt[m] + j] = zv_one<WIDE>(a, md, X, md.Cp, q + t * a.ntot, j);
+    }
+}
+
+// MIXED: modalities outside a.tilemask take one dot product per thread
+template <bool WIDE, bool MIXED>
 __device__ void phase_zv_tile(const AgentArgs &a, int agent, int t0, int nc, const double *q, double *zv,
                               const int *sobs)
 {
-    int first = 0;
+    int first = 0, tfirst = 0;
     int64_t llo = 0;
     for (int m = 0; m < a.M; ++m) {
         const ModDesc &md = a.mods[m];
         const int R = md.R;
+        if (MIXED && !((a.tilemask >> m) & 1)) {
+            zv_thread_modality<WIDE>(a, md, agent, m, t0, nc, q, zv, sobs, llo, tfirst);
+            tfirst += nc * (md.R + md.C);
+            llo += md.slice;
+            continue;
+        }
         if (R <= 1)
             zv_tile_modality<1, WIDE>(a, md, agent, m, t0, nc, q, zv, sobs, llo, first);
         else if (R <= 2)
@@ -550,8 +587,9 @@ __device__ void phase_zv_tile(const AgentArgs &a, int agent, int t0, int nc, con
 }
 
 // Phase 2: lam of contexts [t0, t0 + nc) into lam[t][ntot].  TILE: Z/V in the
-// tile layout (Z as per-chunk partial sums).
-template <bool TILE, int BT, bool WIDE>
+// tile layout (Z as per-chunk partial sums; MIXED: only for the modalities in
+// a.tilemask, the others Z [R] then V [C]).
+template <bool TILE, int BT, bool WIDE, bool MIXED = false>
 __device__ void phase_lam(const AgentArgs &a, int t0, int nc, const double *q, const double *zv, const int *sfac,
                           double *lam)
 {
@@ -564,8 +602,9 @@ __device__ void phase_lam(const AgentArgs &a, int t0, int nc, const double *q, c
         for (int m = 0; m < a.M; ++m) {
             const ModDesc &md = a.mods[m];
             const double *Z = zv + c * a.zvpc + (TILE ? a.zt[m] : md.zv_off);
-            const int nch = TILE ? tile_nch(md.C) : 1;
-            const double *V = Z + (TILE ? (md.nrow > 0 ? nch * md.R : 0) : md.R);
+            const bool tiled = TILE && (!MIXED || ((a.tilemask >> m) & 1));
+            const int nch = tiled ? tile_nch(md.C) : 1;
+            const double *V = Z + (tiled ? (md.nrow > 0 ? nch * md.R : 0) : md.R);
             // Z[k]: the sum of its column chunks' partial sums
             auto zat = [&](int k) {
                 double z = Z[k];
@@ -653,7 +692,7 @@ __device__ void window_lam(const AgentArgs &a, int agent, const double *q, doubl
             __syncthreads();
         }
         if (SRC == kSrcTile)
-            phase_zv_tile<WIDE>(a, agent, t0, nc, q, zv, sobs);
+            phase_zv_tile<WIDE, false>(a, agent, t0, nc, q, zv, sobs);
         else
             phase_zv<SRC == kSrcGlobal, kBatch<SRC>, WIDE>(a, agent, t0, nc, q, zv, stg,
                                                            a.stage == kStageWindow ? t0 : 0);
@@ -850,8 +889,10 @@ __global__ __launch_bounds__(kThreads, SRC == kSrcTile ? 3 : 4) void agent_windo
     for (int i = threadIdx.x; i < TN; i += kThreads) out[i] = (float)cur[i];
 }
 
-template <bool GX, bool TB, bool WIDE>   // slices read from global memory; trivial B-dependency lists
-__global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
+// GX: slices read from global memory (TILE: in the tile form); TB: trivial
+// B-dependency lists; WIDE: some modality has a side of more than two factors
+template <bool GX, bool TB, bool WIDE, bool TILE>
+__global__ __launch_bounds__(kThreads, TILE ? 3 : 4) void agent_filter_kernel(AgentArgs a)
 {
     extern __shared__ double smem[];
     const int agent = blockIdx.x;
@@ -864,7 +905,9 @@ __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
     const int nstg = a.stage == kStageWindow ? a.T : a.stage == kStageChunk ? 1 : 0;
     double *btab = stg + (int64_t)nstg * a.sctx;
     int *sfac = reinterpret_cast<int *>(btab + a.bdoubles);
+    int *sobs = sfac + a.ntot;
     init_tables(a, sfac);
+    if (TILE && !a.ll) stage_obs(a, agent, sobs);
     if (a.bst) stage_b(a, agent, false, btab);
     if (a.stage == kStageWindow) stage_slices(a, agent, 0, a.T, stg);
     __syncthreads();
@@ -906,9 +949,12 @@ __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
         if (a.stage == kStageChunk) stage_slices(a, agent, t, 1, stg);   // step t's slices, for all its iterations
         __syncthreads();
         for (int k = 0; k < a.iters; ++k) {
-            phase_zv<GX, 8, WIDE>(a, agent, t, 1, cur, zv, stg, a.stage == kStageWindow ? t : 0);
+            if (TILE)
+                phase_zv_tile<WIDE, true>(a, agent, t, 1, cur, zv, sobs);
+            else
+                phase_zv<GX, 8, WIDE>(a, agent, t, 1, cur, zv, stg, a.stage == kStageWindow ? t : 0);
             __syncthreads();
-            phase_lam<false, 8, WIDE>(a, t, 1, cur, zv, sfac, lam);
+            phase_lam<TILE, 8, WIDE, true>(a, t, 1, cur, zv, sfac, lam);
             __syncthreads();
             // Jacobi: lam holds every factor's message from the previous iterate
             // (damped: the new marginal is formed in lam's row, then mixed
@@ -935,6 +981,7 @@ __global__ __launch_bounds__(kThreads, 4) void agent_filter_kernel(AgentArgs a)
 }
 
 constexpr size_t kLdsMax = 160 * 1024;
+
 
 }  // namespace
 
@@ -1021,26 +1068,28 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
             lds = fixed + (size_t)a.nc * per_ctx;
         }
     }
-    // VMP / MMP with slices from global memory: the tile form of phase 1 when
-    // its Z/V layout fits (per context: the Z partial sums of every column
-    // chunk and V), with the window's outcomes in LDS.  (FPI keeps one dot
-    // product per thread: the tile form measured 2% slower on the model
-    // sweep there, at three workgroups per CU instead of four.)
+    // Slices from global memory: the tile form of phase 1 when its Z/V layout
+    // fits (per context: the Z partial sums of every column chunk and V), with
+    // the window's outcomes in LDS; FPI only for the modalities of at most
+    // kTileMaxRows rows (the others one dot product per thread).
     a.tile = 0;
-    if (a.stage == kStageNone && m->M <= kStageMaxM && algo != BI_ALGO_FPI) {
+    a.tilemask = 0;
+    for (int i = 0; i < m->M && i < kStageMaxM; ++i)
+        if (algo != BI_ALGO_FPI || m->mods[i].R <= kTileMaxRows) a.tilemask |= 1u << i;
+    if (a.stage == kStageNone && m->M <= kStageMaxM && a.tilemask != 0) {
         int zt = 0;
         for (int i = 0; i < m->M; ++i) {
             a.zt[i] = zt;
-            zt += tile_block(m->mods[i]);
+            zt += tile_block(m->mods[i], (a.tilemask >> i) & 1);
         }
         a.zt[m->M] = zt;
         const size_t pc = (size_t)zt * 8, so = (size_t)T * m->M * 4;
         // the whole window in one chunk when it fits 80 KB, else as many
         // contexts as 160 KB allow (chunks sized for three workgroups per CU
         // measured 5% slower on the model sweep: more barriers per sweep)
-        const size_t fx = fixed + so;
-        size_t nc = T;
-        if (fx + nc * pc > budget2) nc = fx < kLdsMax ? (kLdsMax - fx) / pc : 0;
+        const size_t fx = fixed + so - (algo == BI_ALGO_FPI ? per_ctx : 0);
+        size_t nc = algo == BI_ALGO_FPI ? 1 : T;
+        if (algo != BI_ALGO_FPI && fx + nc * pc > budget2) nc = fx < kLdsMax ? (kLdsMax - fx) / pc : 0;
         if (nc > (size_t)T) nc = T;
         const size_t lt = fx + nc * pc;
         if (nc >= 1 && lt <= kLdsMax) {
@@ -1065,11 +1114,14 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     bool wide = false;
     for (const ModDesc &md : m->mods) wide = wide || md.nrow > 2 || md.ncol > 2;
 #define BI_FILTER(GX, TB) \
-    { (const void *)agent_filter_kernel<GX, TB, false>, (const void *)agent_filter_kernel<GX, TB, true> }
+    { (const void *)agent_filter_kernel<GX, TB, false, false>, (const void *)agent_filter_kernel<GX, TB, true, false> }
+#define BI_FILTER_TILE(TB) \
+    { (const void *)agent_filter_kernel<true, TB, false, true>, (const void *)agent_filter_kernel<true, TB, true, true> }
 #define BI_WINDOW(ALGO, SRC, TB) \
     { (const void *)agent_window_kernel<ALGO, SRC, TB, false>, (const void *)agent_window_kernel<ALGO, SRC, TB, true> }
-    static const void *const kFilter[2][2][2] = {{BI_FILTER(false, false), BI_FILTER(false, true)},
-                                                 {BI_FILTER(true, false), BI_FILTER(true, true)}};
+    static const void *const kFilter[3][2][2] = {{BI_FILTER(false, false), BI_FILTER(false, true)},
+                                                 {BI_FILTER(true, false), BI_FILTER(true, true)},
+                                                 {BI_FILTER_TILE(false), BI_FILTER_TILE(true)}};
     static const void *const kVmp[4][2][2] = {
         {BI_WINDOW(BI_ALGO_VMP, kSrcLds, false), BI_WINDOW(BI_ALGO_VMP, kSrcLds, true)},
         {BI_WINDOW(BI_ALGO_VMP, kSrcGlobal, false), BI_WINDOW(BI_ALGO_VMP, kSrcGlobal, true)},
@@ -1081,13 +1133,16 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
         {BI_WINDOW(BI_ALGO_MMP, kSrcTile, false), BI_WINDOW(BI_ALGO_MMP, kSrcTile, true)},
         {BI_WINDOW(BI_ALGO_MMP, kSrcLdsShort, false), BI_WINDOW(BI_ALGO_MMP, kSrcLdsShort, true)}};
 #undef BI_FILTER
+#undef BI_FILTER_TILE
 #undef BI_WINDOW
-    const void *fn = algo == BI_ALGO_FPI ? kFilter[a.stage == kStageNone][tb][wide]
+    const void *fn = algo == BI_ALGO_FPI ? kFilter[a.tile ? 2 : a.stage == kStageNone ? 1 : 0][tb][wide]
                      : algo == BI_ALGO_VMP ? kVmp[src][tb][wide]
                                            : kMmp[src][tb][wide];
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     if (e == hipSuccess) {
-        ProfScope p(algo == BI_ALGO_FPI ? "agent_filter" : a.tile ? "agent_window_tile" : "agent_window", stream);
+        ProfScope p(algo == BI_ALGO_FPI ? (a.tile ? "agent_filter_tile" : "agent_filter")
+                                    : a.tile ? "agent_window_tile" : "agent_window",
+                stream);
         void *args[] = {&a};
         e = hipLaunchKernel(fn, dim3(b), dim3(kThreads), args, lds, stream);
     }

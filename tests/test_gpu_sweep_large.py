@@ -23,7 +23,7 @@ AGENTS = [0, 255]
 LARGE = [(r, c) for r in ("uniform", "skewed") for c in range(synth.N_SWEEP)
          if synth.sweep_spec(c, r).a_floats() > 400_000]
 ALL_FAMILIES = bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS
-FAMILY_OF = {"agent_window": "agent", "agent_window_tile": "agent", "agent_filter": "agent", "lik_sparse": "sparse", "lik_sparse16": "sparse",
+FAMILY_OF = {"agent_window": "agent", "agent_window_tile": "agent", "agent_filter": "agent", "agent_filter_tile": "agent", "lik_sparse": "sparse", "lik_sparse16": "sparse",
              "lik": "stream", "lik_split": "stream", "lik_split16": "stream", "lik_rowcol16": "stream"}
 
 

@@ -74,6 +74,7 @@ struct AgentArgs {
     unsigned tilemask;   // bit m: modality m in the tile form (else one dot product per thread, Z [R] then V [C])
     int zt[kStageMaxM + 1];
     double tau;            // damping step: q <- (1 - tau) q + tau q_new (1: plain update)
+    int sw;                // lanes per (step, factor) segment of the update (0: one thread per state)
     float *q;
 };
 
@@ -449,6 +450,23 @@ __device__ inline void seg_halve(double *z, int sl)
 
 constexpr int log2_floor(int x) { return x <= 1 ? 0 : 1 + log2_floor(x / 2); }
 
+// Maximum (MAX) or sum of v over an aligned segment of SW lanes (a power of
+// two up to 64), left in every lane: the pairings above within rows of 16,
+// lane shuffles beyond.  Every lane gets the same bits (the exchanges are
+// symmetric).
+template <bool MAX>
+__device__ inline double seg_allreduce(double v, int SW)
+{
+    auto op = [](double x, double y) { return MAX ? fmax(x, y) : x + y; };
+    if (SW >= 16) v = op(v, seg_swap<0>(v));
+    if (SW >= 8) v = op(v, seg_swap<1>(v));
+    if (SW >= 4) v = op(v, seg_swap<2>(v));
+    if (SW >= 2) v = op(v, seg_swap<3>(v));
+    if (SW >= 32) v = op(v, __shfl_xor(v, 16, 64));
+    if (SW >= 64) v = op(v, __shfl_xor(v, 32, 64));
+    return v;
+}
+
 // One modality's units of contexts [t0, t0 + nc): RB rows per block (every
 // row of a block loaded before any is used), P >= RB the power of two the
 // segment reduction works on.
@@ -764,6 +782,65 @@ __device__ void window_softmax(const AgentArgs &a, const int *sfac, const double
     __syncthreads();
 }
 
+// Transition messages and masked softmax of every (step, factor), trivial
+// B-dependency lists: one segment of a.sw lanes (a power of two >= every n_f)
+// per (t, f), a lane per state; the segment's maximum and sum come from lane
+// exchanges, so the update is one pass with no LDS round trip or barrier
+// between its phases (a thread per state took three passes, each reading the
+// (t, f) segment back from LDS).  Writes the new marginals to nxt.
+template <int ALGO, int BT>
+__device__ void window_update_seg(const AgentArgs &a, int agent, int64_t am, const double *cur, const double *lam,
+                                  const double *btab, double *nxt)
+{
+    const int SW = a.sw, sl = (int)threadIdx.x % SW;
+    for (int sg = (int)threadIdx.x / SW; sg < a.T * a.F; sg += kThreads / SW) {
+        const int t = sg / a.F, f = sg - t * a.F;
+        const FacDesc &fd = a.facs[f];
+        const int n = fd.n, s = min(sl, n - 1);
+        const int j = fd.q_off + s, i = t * a.ntot + j;
+        const double *LB = a.bst ? btab + a.bo[f] : at<double>(a.base, fd.lb_off) + am * fd.b_agent;
+        const float *Bf = a.bst ? reinterpret_cast<const float *>(btab) + a.bo[f]
+                                : at<float>(a.base, fd.b_off) + am * fd.b_agent;
+        double fwd, bwd = 0.0;
+        if (t == 0) {
+            fwd = a.prior ? ln_clamped((double)a.prior[(int64_t)agent * a.ntot + j])
+                          : at<double>(a.base, fd.ld_off)[am * fd.ld_agent + s];
+        } else {
+            const int up = a.act[((int64_t)agent * (a.T - 1) + t - 1) * a.F + f];
+            const double *qprev = cur + (t - 1) * a.ntot + fd.q_off;
+            if (ALGO == BI_ALGO_VMP) {
+                const double *row = LB + (int64_t)up * n * n + s * n;   // [i][j]
+                fwd = dot8<BT>(n, [&](int jj) { return row[jj]; }, [&](int jj) { return qprev[jj]; });
+            } else {
+                const float *row = Bf + (int64_t)up * n * n + s * n;
+                fwd = ln_clamped(dot8<BT>(n, [&](int jj) { return (double)row[jj]; }, [&](int jj) { return qprev[jj]; }));
+            }
+        }
+        if (t + 1 < a.T) {
+            const int un = a.act[((int64_t)agent * (a.T - 1) + t) * a.F + f];
+            const double *qnext = cur + (t + 1) * a.ntot + fd.q_off;
+            if (ALGO == BI_ALGO_VMP) {
+                const double *col = LB + (int64_t)un * n * n + s;
+                bwd = dot8<BT>(n, [&](int ii) { return qnext[ii]; }, [&](int ii) { return col[ii * n]; });
+            } else {
+                const float *col = Bf + (int64_t)un * n * n + s;
+                bwd = ln_clamped(
+                    dot8<BT>(n, [&](int ii) { return qnext[ii]; }, [&](int ii) { return (double)col[ii * n]; }));
+            }
+        }
+        const double lm = lam[i];
+        const double v = ALGO == BI_ALGO_VMP ? lm + fwd + bwd : t + 1 < a.T ? lm + 0.5 * (fwd + bwd) : lm + fwd;
+        const bool act = sl < n;
+        const double mx = seg_allreduce<true>(act ? v : -INFINITY, SW);
+        const double e = act ? exp(v - mx) : 0.0;
+        const double sum = seg_allreduce<false>(e, SW);
+        if (act) {
+            const double qn = e / sum;
+            nxt[i] = a.tau != 1.0 ? (1.0 - a.tau) * cur[i] + a.tau * qn : qn;
+        }
+    }
+}
+
 // ALGO: BI_ALGO_VMP or BI_ALGO_MMP; SRC: where phase 1 reads the slices; TB:
 // every B-dependency list is {f} (the row / column transition products;
 // otherwise the general contractions of transition.h)
@@ -789,6 +866,14 @@ __global__ __launch_bounds__(kThreads, SRC == kSrcTile ? 3 : 4) void agent_windo
     double *cur = qa, *nxt = qb;
     for (int k = 0; k < a.iters; ++k) {
         window_lam<SRC, WIDE>(a, agent, cur, zv, stg, sfac, sobs, lam);
+        if (TB && a.sw) {
+            window_update_seg<ALGO, kBatch<SRC>>(a, agent, am, cur, lam, btab, nxt);
+            __syncthreads();
+            double *tmp = cur;
+            cur = nxt;
+            nxt = tmp;
+            continue;
+        }
         // logits of every (t, state) into nxt, one thread per state
         for (int i = threadIdx.x; i < TN; i += kThreads) {
             const int t = i / a.ntot, j = i - t * a.ntot;
@@ -981,6 +1066,10 @@ __global__ __launch_bounds__(kThreads, TILE ? 3 : 4) void agent_filter_kernel(Ag
 }
 
 constexpr size_t kLdsMax = 160 * 1024;
+#ifndef BI_SEG_UPDATE
+#define BI_SEG_UPDATE 1
+#endif
+constexpr bool kSegUpdate = BI_SEG_UPDATE;
 
 
 }  // namespace
@@ -1007,6 +1096,16 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     a.prior = prior;
     a.tau = tau;
     a.q = q;
+    // lanes per (step, factor) segment of the window kernels' update: the
+    // power of two covering the largest factor, up to a wave
+    a.sw = 0;
+    if (algo != BI_ALGO_FPI && m->trivial_b) {
+        int nmax = 1;
+        for (const FacDesc &fd : m->facs) nmax = std::max(nmax, (int)fd.n);
+        int sw = 1;
+        while (sw < nmax) sw *= 2;
+        a.sw = kSegUpdate && sw <= 64 ? sw : 0;
+    }
     const size_t TN = (size_t)T * m->ntot;
     // staged slice layout (see AgentArgs)
     int64_t sctx = 0, sraw = 0;

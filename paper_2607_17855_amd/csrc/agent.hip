@@ -607,6 +607,71 @@ __device__ void phase_zv_tile(const AgentArgs &a, int agent, int t0, int nc, con
 // Phase 2: lam of contexts [t0, t0 + nc) into lam[t][ntot].  TILE: Z/V in the
 // tile layout (Z as per-chunk partial sums; MIXED: only for the modalities in
 // a.tilemask, the others Z [R] then V [C]).
+// lam of state s of factor f in chunk context c (qt: the marginals of its step)
+template <bool TILE, int BT, bool WIDE, bool MIXED>
+__device__ inline double lam_one(const AgentArgs &a, int c, int f, int s, const double *qt, const double *zv)
+{
+    double acc = 0.0;
+    for (int m = 0; m < a.M; ++m) {
+        const ModDesc &md = a.mods[m];
+        const double *Z = zv + c * a.zvpc + (TILE ? a.zt[m] : md.zv_off);
+        const bool tiled = TILE && (!MIXED || ((a.tilemask >> m) & 1));
+        const int nch = tiled ? tile_nch(md.C) : 1;
+        const double *V = Z + (tiled ? (md.nrow > 0 ? nch * md.R : 0) : md.R);
+        // Z[k]: the sum of its column chunks' partial sums
+        auto zat = [&](int k) {
+            double z = Z[k];
+            for (int cb = 1; cb < nch; ++cb) z += Z[cb * md.R + k];
+            return z;
+        };
+        if (WIDE && (md.nrow > 2 || md.ncol > 2)) {
+            // a side of more than two factors: the lines whose digit of f
+            // is s, weighted by the side's other marginals
+            for (int side = 0; side < 2; ++side) {
+                const int k = side ? md.ncol : md.nrow;
+                const int32_t *sf = side ? md.cf : md.rf, *sn = side ? md.cn : md.rn;
+                for (int p = 0; p < k; ++p) {
+                    if (sf[p] != f) continue;
+                    int low = 1;
+                    for (int g = p + 1; g < k; ++g) low *= sn[g];
+                    const int np = sn[p], len = (side ? md.C : md.R) / np;
+                    auto line = [&](int jj) {
+                        const int hi = jj / low;
+                        return (hi * np + s) * low + (jj - hi * low);
+                    };
+                    acc += dot8<BT>(len, [&](int jj) { return side ? V[line(jj)] : zat(line(jj)); },
+                                    [&](int jj) { return side_weight(a, qt, sf, sn, k, line(jj), p); });
+                }
+            }
+        } else if (md.nrow >= 1 && md.rf[0] == f) {
+            if (md.nrow == 1) {
+                acc += zat(s);
+            } else {
+                const double *q1 = qt + a.facs[md.rf[1]].q_off;
+                const int n1 = md.rn[1];
+                acc += dot8<BT>(n1, [&](int r1) { return zat(s * n1 + r1); }, [&](int r1) { return q1[r1]; });
+            }
+        } else if (md.nrow == 2 && md.rf[1] == f) {
+            const double *q0 = qt + a.facs[md.rf[0]].q_off;
+            const int n0 = md.rn[0], n1 = md.rn[1];
+            acc += dot8<BT>(n0, [&](int r0) { return zat(r0 * n1 + s); }, [&](int r0) { return q0[r0]; });
+        } else if (md.cf[0] == f) {
+            if (md.ncol == 1) {
+                acc += V[s];
+            } else {
+                const double *q1 = qt + a.facs[md.cf[1]].q_off;
+                const int n1 = md.cn[1];
+                acc += dot8<BT>(n1, [&](int c1) { return V[s * n1 + c1]; }, [&](int c1) { return q1[c1]; });
+            }
+        } else if (md.ncol == 2 && md.cf[1] == f) {
+            const double *q0 = qt + a.facs[md.cf[0]].q_off;
+            const int n0 = md.cn[0], n1 = md.cn[1];
+            acc += dot8<BT>(n0, [&](int c0) { return V[c0 * n1 + s]; }, [&](int c0) { return q0[c0]; });
+        }
+    }
+    return acc;
+}
+
 template <bool TILE, int BT, bool WIDE, bool MIXED = false>
 __device__ void phase_lam(const AgentArgs &a, int t0, int nc, const double *q, const double *zv, const int *sfac,
                           double *lam)
@@ -614,67 +679,8 @@ __device__ void phase_lam(const AgentArgs &a, int t0, int nc, const double *q, c
     for (int i = threadIdx.x; i < nc * a.ntot; i += kThreads) {
         const int c = i / a.ntot, j = i - c * a.ntot;
         const int f = sfac[j];
-        const int s = j - a.facs[f].q_off;
-        const double *qt = q + (t0 + c) * a.ntot;
-        double acc = 0.0;
-        for (int m = 0; m < a.M; ++m) {
-            const ModDesc &md = a.mods[m];
-            const double *Z = zv + c * a.zvpc + (TILE ? a.zt[m] : md.zv_off);
-            const bool tiled = TILE && (!MIXED || ((a.tilemask >> m) & 1));
-            const int nch = tiled ? tile_nch(md.C) : 1;
-            const double *V = Z + (tiled ? (md.nrow > 0 ? nch * md.R : 0) : md.R);
-            // Z[k]: the sum of its column chunks' partial sums
-            auto zat = [&](int k) {
-                double z = Z[k];
-                for (int cb = 1; cb < nch; ++cb) z += Z[cb * md.R + k];
-                return z;
-            };
-            if (WIDE && (md.nrow > 2 || md.ncol > 2)) {
-                // a side of more than two factors: the lines whose digit of f
-                // is s, weighted by the side's other marginals
-                for (int side = 0; side < 2; ++side) {
-                    const int k = side ? md.ncol : md.nrow;
-                    const int32_t *sf = side ? md.cf : md.rf, *sn = side ? md.cn : md.rn;
-                    for (int p = 0; p < k; ++p) {
-                        if (sf[p] != f) continue;
-                        int low = 1;
-                        for (int g = p + 1; g < k; ++g) low *= sn[g];
-                        const int np = sn[p], len = (side ? md.C : md.R) / np;
-                        auto line = [&](int jj) {
-                            const int hi = jj / low;
-                            return (hi * np + s) * low + (jj - hi * low);
-                        };
-                        acc += dot8<BT>(len, [&](int jj) { return side ? V[line(jj)] : zat(line(jj)); },
-                                        [&](int jj) { return side_weight(a, qt, sf, sn, k, line(jj), p); });
-                    }
-                }
-            } else if (md.nrow >= 1 && md.rf[0] == f) {
-                if (md.nrow == 1) {
-                    acc += zat(s);
-                } else {
-                    const double *q1 = qt + a.facs[md.rf[1]].q_off;
-                    const int n1 = md.rn[1];
-                    acc += dot8<BT>(n1, [&](int r1) { return zat(s * n1 + r1); }, [&](int r1) { return q1[r1]; });
-                }
-            } else if (md.nrow == 2 && md.rf[1] == f) {
-                const double *q0 = qt + a.facs[md.rf[0]].q_off;
-                const int n0 = md.rn[0], n1 = md.rn[1];
-                acc += dot8<BT>(n0, [&](int r0) { return zat(r0 * n1 + s); }, [&](int r0) { return q0[r0]; });
-            } else if (md.cf[0] == f) {
-                if (md.ncol == 1) {
-                    acc += V[s];
-                } else {
-                    const double *q1 = qt + a.facs[md.cf[1]].q_off;
-                    const int n1 = md.cn[1];
-                    acc += dot8<BT>(n1, [&](int c1) { return V[s * n1 + c1]; }, [&](int c1) { return q1[c1]; });
-                }
-            } else if (md.ncol == 2 && md.cf[1] == f) {
-                const double *q0 = qt + a.facs[md.cf[0]].q_off;
-                const int n0 = md.cn[0], n1 = md.cn[1];
-                acc += dot8<BT>(n0, [&](int c0) { return V[c0 * n1 + s]; }, [&](int c0) { return q0[c0]; });
-            }
-        }
-        lam[(t0 + c) * a.ntot + j] = acc;
+        lam[(t0 + c) * a.ntot + j] =
+            lam_one<TILE, BT, WIDE, MIXED>(a, c, f, j - a.facs[f].q_off, q + (t0 + c) * a.ntot, zv);
     }
 }
 
@@ -1033,12 +1039,40 @@ __global__ __launch_bounds__(kThreads, TILE ? 3 : 4) void agent_filter_kernel(Ag
         for (int j = threadIdx.x; j < a.ntot; j += kThreads) qt[j] = 1.0 / a.facs[sfac[j]].n;
         if (a.stage == kStageChunk) stage_slices(a, agent, t, 1, stg);   // step t's slices, for all its iterations
         __syncthreads();
+        // with factor segments (a.sw) the iterate alternates between row t
+        // of cur and of lam: each iteration reads one and writes the other
+        double *qa = cur, *qb = lam;
         for (int k = 0; k < a.iters; ++k) {
             if (TILE)
-                phase_zv_tile<WIDE, true>(a, agent, t, 1, cur, zv, sobs);
+                phase_zv_tile<WIDE, true>(a, agent, t, 1, qa, zv, sobs);
             else
-                phase_zv<GX, 8, WIDE>(a, agent, t, 1, cur, zv, stg, a.stage == kStageWindow ? t : 0);
+                phase_zv<GX, 8, WIDE>(a, agent, t, 1, qa, zv, stg, a.stage == kStageWindow ? t : 0);
             __syncthreads();
+            if (a.sw) {
+                // one segment of a.sw lanes per factor, a lane per state: its
+                // lam, the prior, and the softmax from lane exchanges, in one
+                // pass (a pass for lam, then a wave per factor, before)
+                const int SW = a.sw, sl = (int)threadIdx.x % SW, f = (int)threadIdx.x / SW;
+                if (f < a.F) {
+                    const FacDesc &fd = a.facs[f];
+                    const int n = fd.n, s = min(sl, n - 1);
+                    const double *qr = qa + t * a.ntot;
+                    const double v = lam_one<TILE, 8, WIDE, true>(a, 0, f, s, qr, zv) + logp[fd.q_off + s];
+                    const bool act = sl < n;
+                    const double mx = seg_allreduce<true>(act ? v : -INFINITY, SW);
+                    const double e = act ? exp(v - mx) : 0.0;
+                    const double sum = seg_allreduce<false>(e, SW);
+                    if (act) {
+                        const double qn = e / sum;
+                        qb[t * a.ntot + fd.q_off + s] = a.tau != 1.0 ? (1.0 - a.tau) * qr[fd.q_off + s] + a.tau * qn : qn;
+                    }
+                }
+                __syncthreads();
+                double *tmp = qa;
+                qa = qb;
+                qb = tmp;
+                continue;
+            }
             phase_lam<TILE, 8, WIDE, true>(a, t, 1, cur, zv, sfac, lam);
             __syncthreads();
             // Jacobi: lam holds every factor's message from the previous iterate
@@ -1058,7 +1092,7 @@ __global__ __launch_bounds__(kThreads, TILE ? 3 : 4) void agent_filter_kernel(Ag
             }
             __syncthreads();
         }
-        for (int j = threadIdx.x; j < a.ntot; j += kThreads) qfin[t * a.ntot + j] = qt[j];
+        for (int j = threadIdx.x; j < a.ntot; j += kThreads) qfin[t * a.ntot + j] = qa[t * a.ntot + j];
         __syncthreads();
     }
     float *out = a.q + (int64_t)agent * TN;
@@ -1098,13 +1132,15 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     a.q = q;
     // lanes per (step, factor) segment of the window kernels' update: the
     // power of two covering the largest factor, up to a wave
+    // (FPI: segments of every factor in one pass of the workgroup)
     a.sw = 0;
-    if (algo != BI_ALGO_FPI && m->trivial_b) {
+    if (algo == BI_ALGO_FPI || m->trivial_b) {
         int nmax = 1;
         for (const FacDesc &fd : m->facs) nmax = std::max(nmax, (int)fd.n);
         int sw = 1;
         while (sw < nmax) sw *= 2;
-        a.sw = kSegUpdate && sw <= 64 ? sw : 0;
+        const bool fits = sw <= 64 && (algo != BI_ALGO_FPI || (int64_t)m->F * sw <= kThreads);
+        a.sw = kSegUpdate && fits ? sw : 0;
     }
     const size_t TN = (size_t)T * m->ntot;
     // staged slice layout (see AgentArgs)

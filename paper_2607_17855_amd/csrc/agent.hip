@@ -1273,7 +1273,7 @@ int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, 
     const void *fn = algo == BI_ALGO_FPI ? kFilter[a.tile ? 2 : a.stage == kStageNone ? 1 : 0][tb][wide]
                      : algo == BI_ALGO_VMP ? kVmp[src][tb][wide]
                                            : kMmp[src][tb][wide];
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
+    hipError_t e = func_max_lds(fn, (int)kLdsMax);
     if (e == hipSuccess) {
         ProfScope p(algo == BI_ALGO_FPI ? (a.tile ? "agent_filter_tile" : "agent_filter")
                                     : a.tile ? "agent_window_tile" : "agent_window",

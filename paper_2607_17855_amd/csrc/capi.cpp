@@ -3,7 +3,10 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
+#include <set>
+#include <tuple>
 
 #include "internal.h"
 #include "stream.h"
@@ -60,6 +63,25 @@ const char *stream_refusal(const bi_model *m, int algo, bool sparse)
 }  // namespace
 
 namespace bi {
+hipError_t func_max_lds(const void *fn, int bytes)
+{
+    static std::mutex mu;
+    static std::set<std::tuple<int, const void *, int>> done;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+    const auto key = std::make_tuple(dev, fn, bytes);
+    {
+        std::lock_guard<std::mutex> g(mu);
+        if (done.count(key)) return hipSuccess;
+    }
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess) {
+        std::lock_guard<std::mutex> g(mu);
+        done.insert(key);
+    }
+    return e;
+}
+
 int infer_impl(int algo, const bi_model *model, int32_t b, int32_t T, const int32_t *obs, const int32_t *act,
                    const float *prior, double tau, int32_t iters, float *q, void *ws, size_t ws_bytes, void *stream)
 {

@@ -44,6 +44,11 @@ int plan(const bi_model_desc *desc, bi_model *m, const float *const *A = nullptr
 // `tau` in (0, 1] damps every update: q <- (1 - tau) q + tau q_new.  With
 // soft observations obs is NULL and ll holds every context's log-likelihood
 // tensors (launch_soft_ll).
+// hipFuncSetAttribute(fn, MaxDynamicSharedMemorySize, bytes), issued once per
+// (device, kernel, size): every launch asks for it, and the runtime call costs
+// host time on launch-bound calls (one-step online filtering).
+hipError_t func_max_lds(const void *fn, int bytes);
+
 int launch_agent(const bi_model *m, int algo, int b, int T, const int32_t *obs, const double *ll,
                  const int32_t *act, const float *prior, double tau, int iters, float *q, hipStream_t stream);
 

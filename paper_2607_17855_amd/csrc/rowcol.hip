@@ -469,8 +469,7 @@ size_t rc_lds_bytes() { return kLds; }
 
 int rc_prepare()
 {
-    const hipError_t e =
-        hipFuncSetAttribute((const void *)rowcol16_lik_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+    const hipError_t e = func_max_lds((const void *)rowcol16_lik_kernel, kLds);
     if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     return BI_OK;
 }

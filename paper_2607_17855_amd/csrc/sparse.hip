@@ -325,8 +325,7 @@ int sparse_prepare(const bi_model *m)
 {
     const size_t lds = sparse_lds_bytes(m);
     if (lds > 160 * 1024) return fail(BI_ERR_UNSUPPORTED, "sparse working set exceeds LDS");
-    const hipError_t e =
-        hipFuncSetAttribute((const void *)sparse_lik_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const hipError_t e = func_max_lds((const void *)sparse_lik_kernel, (int)lds);
     if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     return BI_OK;
 }

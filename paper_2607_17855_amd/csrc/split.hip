@@ -743,7 +743,7 @@ int split_prepare(const bi_model *m, bool sparse)
     const void *fn = sparse ? (const void *)sparse16_lik_kernel
                      : split_pairs(m) ? (const void *)split_lik_kernel<true>
                                       : (const void *)split_lik_kernel<false>;
-    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+    const hipError_t e = func_max_lds(fn, (int)kMaxLds);
     if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     return BI_OK;
 }

@@ -928,8 +928,7 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
         const int rc = split_prepare(m, lik == Lik::Sparse16);
         if (rc != BI_OK) return rc;
     } else {
-        const hipError_t e = hipFuncSetAttribute((const void *)lik_kernel,
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lik_lds);
+        const hipError_t e = func_max_lds((const void *)lik_kernel, (int)lik_lds);
         if (e != hipSuccess) return fail(BI_ERR_DEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     }
     int kmax = 1;

@@ -26,9 +26,20 @@ def _shared(seed, n, U, K, deps, b, T, sparsity=0.0):
     return synth.Workload(f"graph{seed}", ["vmp", "mmp"], model, obs, act, 3)
 
 
+def _agents(seed, n, K, deps, b, T, algos):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    model = synth.make_model(rng, n, [2] * len(n), K, deps, b, 0.7, 1.0, uniform_D=False)
+    obs, act = synth.sample_sequences(rng, model, b, T)
+    return synth.Workload(f"graph{seed}", list(algos), model, obs, act, 3)
+
+
 CASES = [
     # (workload maker, packing flags, algorithms, kernel family)
     (lambda: synth.two_factor_agents(b=32), bi.BI_DENSE_A, ("fpi", "vmp", "mmp"), "agent"),
+    # windows read from global memory (tile form), and FPI steps in the tile form
+    (lambda: _agents(1204, [20, 6, 7], [5, 3, 4], [[0, 1, 2], [1], [0, 2]], 6, 12, ("vmp", "mmp")),
+     bi.BI_DENSE_A, ("vmp", "mmp"), "agent"),
+    (lambda: _agents(1205, [30, 25, 28], [3, 4], [[0, 1, 2], [2]], 3, 4, ("fpi",)), bi.BI_DENSE_A, ("fpi",), "agent"),
     (lambda: _shared(1200, [9, 7, 5], [2, 1, 3], [3, 2, 4], [[0, 1, 2], [1], [0, 2]], 24, 5),
      bi.BI_DENSE_A | bi.BI_FAST_F32, ("vmp", "mmp"), "stream"),
     (lambda: _shared(1201, [4, 32, 6, 32], [2, 1, 2, 1], [3], [[0, 1, 2, 3]], 30, 4),

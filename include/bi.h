@@ -59,9 +59,11 @@ extern "C" {
  * iterations amplify rounding errors by 10^3-10^4 (near-bifurcation models).
  * With BI_FAST_F32 a model shared by all agents (model_batch == 1) runs VMP and
  * MMP through the streaming kernels, whose slice contractions use fp32 matrix
- * cores (messages and updates stay fp64).  Use it for models whose
- * marginals are insensitive to fp32 rounding of the log-likelihoods; it
- * stores an extra fp32 copy of the slices.
+ * cores (messages, sums and the softmax stay fp64; the marginals between
+ * iterations and the transition tables are fp32: B for MMP, log B rounded
+ * to fp32 for VMP).  Use it for models whose marginals are insensitive to
+ * fp32 rounding of the log-likelihoods; it stores an extra fp32 copy of the
+ * slices and of log B.
  * Limit (tested at 16 sweeps): the result stays within 1e-5 of the fp64
  * definition exactly when the definition itself moves by less than that under
  * a relative perturbation of log A at the class's rounding scale (2^-24 here,

@@ -159,6 +159,8 @@ struct FacDesc {
     int32_t bstates;              // prod of bdn (B_f is [u][n][bstates])
     int32_t nch;                  // children: factors j with f in bd(j)
     int32_t ch[kMaxCh], chpos[kMaxCh];   // the children and the position of f in their lists
+    int64_t lb32_off;             // byte offset of log B rounded to fp32 (BI_FAST_F32: the streaming
+                                  // families' VMP update with fp32 marginals), or -1
 };
 
 struct SpEntry {

@@ -271,6 +271,11 @@ int plan(const bi_model_desc *d, bi_model *m, const float *const *A)
         off = align_up(off + 4 * per * m->mb, kAlign);
         fd.lb_off = off;
         off = align_up(off + 8 * per * m->mb, kAlign);
+        fd.lb32_off = -1;
+        if (flags & BI_FAST_F32) {
+            fd.lb32_off = off;
+            off = align_up(off + 4 * per * m->mb, kAlign);
+        }
         fd.ld_agent = m->mb == 1 ? 0 : fd.n;
         fd.ld_off = off;
         off = align_up(off + 8 * (int64_t)fd.n * m->mb, kAlign);
@@ -471,12 +476,16 @@ int fill(const bi_model *m, const float *const *A, const float *const *B, const 
             const float *src = B[f] + (int64_t)a * n * bs * U;          // [i][j][u], j over the dependency states
             float *b = reinterpret_cast<float *>(host + fd.b_off) + (int64_t)a * U * n * bs;   // [u][i][j]
             double *lb = reinterpret_cast<double *>(host + fd.lb_off) + (int64_t)a * U * n * bs;
+            float *lb32 = fd.lb32_off >= 0 ? reinterpret_cast<float *>(host + fd.lb32_off) + (int64_t)a * U * n * bs
+                                           : nullptr;
             for (int u = 0; u < U; ++u)
                 for (int i = 0; i < n; ++i)
                     for (int j = 0; j < bs; ++j) {
                         const float v = src[((int64_t)i * bs + j) * U + u];
-                        b[((int64_t)u * n + i) * bs + j] = v;
-                        lb[((int64_t)u * n + i) * bs + j] = ln_clamped((double)v);
+                        const int64_t e = ((int64_t)u * n + i) * bs + j;
+                        b[e] = v;
+                        lb[e] = ln_clamped((double)v);
+                        if (lb32) lb32[e] = (float)lb[e];
                     }
             const float *dsrc = D[f] + (int64_t)a * n;
             double *ld = reinterpret_cast<double *>(host + fd.ld_off) + (int64_t)a * n;

@@ -57,6 +57,7 @@ constexpr int kStreamFacs = 16;
 struct StreamFac {
     int64_t lb_off, b_off, ld_off;   // byte offsets of log B, B and log D in the packed buffer
     int32_t n, q_off;
+    int64_t lb32_off;                // log B in fp32 (fp32 marginals), or -1
 };
 
 struct StreamArgs {

@@ -551,7 +551,10 @@ template <int ALGO, typename QT, typename OT, typename PP, typename QP>
 __device__ inline void update_trivial(const StreamArgs &a, PP pc, QP qp, QP qn, bool hp, bool hn, const QT *qin,
                                       OT *qout, int ctx, double *vals, int wave, int lane, int up0, int un0)
 {
-    using MT = std::conditional_t<ALGO == BI_ALGO_VMP, double, float>;   // log B (VMP) or B (MMP)
+    // log B (VMP) or B (MMP); with fp32 marginals (the fp32-contraction
+    // class) VMP reads log B rounded to fp32, like MMP's fp32 B, so both take
+    // 8 terms per batch (fp64 log B: 4, and 14.9 against 11.5 us per launch)
+    using MT = std::conditional_t<ALGO == BI_ALGO_VMP && sizeof(QT) == 8, double, float>;
     constexpr int W = sizeof(MT) + sizeof(QT) > 8 ? 4 : 8;   // terms per batch (registers: every workgroup resident)
     const int agent = ctx / a.T, t = ctx - agent * a.T;
     for (int f = wave; f < a.F; f += 4) {
@@ -560,12 +563,13 @@ __device__ inline void update_trivial(const StreamArgs &a, PP pc, QP qp, QP qn, 
             sf = a.fac[f];
         } else {
             const FacDesc &fd = a.facs[f];
-            sf = StreamFac{fd.lb_off, fd.b_off, fd.ld_off, fd.n, fd.q_off};
+            sf = StreamFac{fd.lb_off, fd.b_off, fd.ld_off, fd.n, fd.q_off, fd.lb32_off};
         }
         const int n = sf.n, qo = sf.q_off;
         int up = up0, un = un0;
         if (f != wave) trans_actions(a, f, agent, t, up, un);
-        const MT *M = reinterpret_cast<const MT *>(a.base + (ALGO == BI_ALGO_VMP ? sf.lb_off : sf.b_off));
+        const MT *M = reinterpret_cast<const MT *>(
+            a.base + (ALGO != BI_ALGO_VMP ? sf.b_off : sizeof(QT) == 8 ? sf.lb_off : sf.lb32_off));
         const MT *Mp = M + (int64_t)up * n * n, *Mn = M + (int64_t)un * n * n;
         double *v = vals + qo;
         const int L = n <= 32 ? 2 : 1;          // lanes per state
@@ -891,12 +895,15 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.trivb = m->trivial_b ? 1 : 0;
     for (int f = 0; f < std::min(m->F, kStreamFacs); ++f) {
         const FacDesc &fd = m->facs[f];
-        a.fac[f] = StreamFac{fd.lb_off, fd.b_off, fd.ld_off, fd.n, fd.q_off};
+        a.fac[f] = StreamFac{fd.lb_off, fd.b_off, fd.ld_off, fd.n, fd.q_off, fd.lb32_off};
     }
     a.bstart = reinterpret_cast<int32_t *>(w + offs[0]);
     a.bctx = reinterpret_cast<int32_t *>(w + offs[2]);
     char *part = w + offs[3];
     const Lik lik = lik_kind(m, sparse);
+    if (lik != Lik::Sparse && algo == BI_ALGO_VMP)   // fp32 marginals: the update reads log B in fp32
+        for (const FacDesc &fd : m->facs)
+            if (fd.lb32_off < 0) return fail(BI_ERR_INVALID_ARG, "fp32 log B missing (pack with BI_FAST_F32)");
     // update: the softmax values, plus (when they fit in 48 KB) the staged
     // partial messages and the two neighbour marginal vectors
     const size_t es_p = lik == Lik::Sparse ? sizeof(double) : sizeof(float);   // partials and marginals

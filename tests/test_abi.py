@@ -53,7 +53,8 @@ class FacDesc(ctypes.Structure):
                 ("b_agent", ctypes.c_int64), ("ld_agent", ctypes.c_int32), ("n", ctypes.c_int32),
                 ("U", ctypes.c_int32), ("q_off", ctypes.c_int32), ("nbd", ctypes.c_int32),
                 ("bd", ctypes.c_int32 * 4), ("bdn", ctypes.c_int32 * 4), ("bstates", ctypes.c_int32),
-                ("nch", ctypes.c_int32), ("ch", ctypes.c_int32 * 8), ("chpos", ctypes.c_int32 * 8)]
+                ("nch", ctypes.c_int32), ("ch", ctypes.c_int32 * 8), ("chpos", ctypes.c_int32 * 8),
+                ("lb32_off", ctypes.c_int64)]
 
 
 def _descs(img, M, F):

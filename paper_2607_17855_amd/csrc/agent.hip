@@ -6,15 +6,20 @@
 //
 // One iteration of VMP / MMP (Jacobi over every (t, f), Sec. IV):
 //   1. Z/V: for every context t and modality m, Z = X t and V = s X over the
-//      observed slice X = LA_m[o_{t,m}] (layout.h), each output a dot product
-//      owned by one thread;
+//      observed slice X = LA_m[o_{t,m}] (layout.h): one dot product per
+//      thread when the window's slices are staged in LDS; from global memory
+//      in the tile form (16-lane segments reading each slice once, coalesced;
+//      phase_zv_tile);
 //   2. lam_{t,f}: small contractions of Z (row factors of m) or V (column
 //      factors), summed over the modalities that depend on f;
-//   3. update: one wave per (t, f) forms the transition messages from the
-//      neighbouring marginals and applies the masked softmax with wave
-//      shuffles, writing the other half of the double-buffered marginals.
-// FPI runs the same three phases on a single context t at a time, after
-// forming the predictive prior from the final marginals of step t-1.
+//   3. update: one lane segment per (t, f) forms the transition messages from
+//      the neighbouring marginals and applies the masked softmax with lane
+//      exchanges (window_update_seg), writing the other half of the
+//      double-buffered marginals (general B-dependency lists: a thread per
+//      state, then a segmented softmax through LDS).
+// FPI runs phase 1 on a single context t at a time, then one segment per
+// factor forms lam, adds the predictive prior of step t (from the final
+// marginals of step t-1) and takes the softmax.
 //
 // All arithmetic is fp64 (the updates are ill-conditioned for some models,
 // see layout.h); on gfx950 an fp64 FMA issues at the rate of an unpacked
@@ -1051,7 +1056,7 @@ __global__ __launch_bounds__(kThreads, TILE ? 3 : 4) void agent_filter_kernel(Ag
             if (a.sw) {
                 // one segment of a.sw lanes per factor, a lane per state: its
                 // lam, the prior, and the softmax from lane exchanges, in one
-                // pass (a pass for lam, then a wave per factor, before)
+                // pass (instead of a lam pass, a barrier and a wave per factor)
                 const int SW = a.sw, sl = (int)threadIdx.x % SW, f = (int)threadIdx.x / SW;
                 if (f < a.F) {
                     const FacDesc &fd = a.facs[f];

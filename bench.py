@@ -81,21 +81,33 @@ def slice_sizes(model):
     return out
 
 
-def dense_lik_work(model, obs):
-    """Algorithmic flops and HBM bytes of one dense likelihood launch: per
-    context and modality the two contractions of the slice (towards its rows
-    and towards its columns), one FMA (2 flops) per slice entry each
-    (16.8 MFLOP per belief update); every slice observed by at least one
-    context is read once in fp32."""
+def outcome_counts(model, obs, soft=None):
+    """Per modality, how many contexts apply each outcome's slice in a
+    likelihood launch: the contexts observing it, or with soft vectors
+    [b][T][sum K] the contexts whose vector weights it (nonzero)."""
     import numpy as np
-    nctx = obs.shape[0] * obs.shape[1]
-    flops = sum(2 * 2 * P for P in slice_sizes(model)) * nctx
-    used = [len(np.unique(obs[:, :, m])) for m in range(model.M)]
-    nbytes = sum(4.0 * P * u for P, u in zip(slice_sizes(model), used))
+    if soft is None:
+        return [np.bincount(obs[:, :, m].ravel(), minlength=model.K[m]) for m in range(model.M)]
+    offs = np.cumsum([0] + list(model.K))
+    return [(soft[:, :, offs[m]:offs[m + 1]] != 0).reshape(-1, model.K[m]).sum(axis=0) for m in range(model.M)]
+
+
+def dense_lik_work(model, obs, soft=None):
+    """Algorithmic flops and HBM bytes of one dense likelihood launch: per
+    context (soft vectors: per weighted outcome of a context) and modality the
+    two contractions of the slice (towards its rows and towards its columns),
+    one FMA (2 flops) per slice entry each (16.8 MFLOP per belief update with
+    outcomes); every slice applied by at least one context is read once in
+    fp32."""
+    import numpy as np
+    cnts = outcome_counts(model, obs, soft)
+    P = slice_sizes(model)
+    flops = sum(2 * 2 * p * float(c.sum()) for p, c in zip(P, cnts))
+    nbytes = sum(4.0 * p * int((c > 0).sum()) for p, c in zip(P, cnts))
     return float(flops), float(nbytes)
 
 
-def sparse_lik_work(model, obs):
+def sparse_lik_work(model, obs, soft=None):
     """Algorithmic flops and HBM bytes of one sparse likelihood launch: for
     every context, each nonzero of its observed slices is visited twice (row
     lines and column lines), one multiply and one FMA (3 flops) each; every
@@ -103,16 +115,15 @@ def sparse_lik_work(model, obs):
     import numpy as np
     flops = 0.0
     nbytes = 0.0
-    for m in range(model.M):
+    for m, cnt in enumerate(outcome_counts(model, obs, soft)):
         A = model.A[m][0].reshape(model.K[m], -1)
         nnz = (A.astype(np.float64) > 1e-16).sum(axis=1)
-        cnt = np.bincount(obs[:, :, m].ravel(), minlength=model.K[m])
         flops += 2 * 3 * float((nnz * cnt).sum())
         nbytes += 2 * 16.0 * float(nnz[cnt > 0].sum())
     return flops, nbytes
 
 
-def sparse16_lik_work(model, obs):
+def sparse16_lik_work(model, obs, soft=None):
     """Algorithmic flops and HBM bytes of one sparse fp16-pair likelihood
     launch: the flops of the dense contractions (the matrix cores run the
     zeros too; 3 fp16 products per fp32 product come on top), and every
@@ -121,12 +132,11 @@ def sparse16_lik_work(model, obs):
     side (rows and columns) and the kernel reads both copies: that figure is
     returned third."""
     import numpy as np
-    flops, _ = dense_lik_work(model, obs)
+    flops, _ = dense_lik_work(model, obs, soft)
     nbytes = 0.0
-    for m in range(model.M):
+    for m, cnt in enumerate(outcome_counts(model, obs, soft)):
         A = model.A[m][0].reshape(model.K[m], -1)
         nnz = (A.astype(np.float64) > 1e-16).sum(axis=1)
-        cnt = np.bincount(obs[:, :, m].ravel(), minlength=model.K[m])
         nbytes += 8.0 * float(nnz[cnt > 0].sum())
     return flops, nbytes, 2 * nbytes
 
@@ -269,7 +279,8 @@ def main():
     ap.add_argument("--workload", default="large", choices=["large", "sweep"] + list(AGENT_WORKLOADS))
     ap.add_argument("--regimes", default="uniform,skewed", help="sweep workload: dimension regimes")
     ap.add_argument("--cases", default="0:770", help="sweep workload: start:stop of the seeded specs")
-    ap.add_argument("--soft", action="store_true", help="soft observation vectors (per-agent workloads)")
+    ap.add_argument("--soft", action="store_true",
+                    help="soft observation vectors instead of outcomes (every outcome weighted)")
     ap.add_argument("--dense-f32", action="store_true",
                     help="dense layout on fp32 matrix cores (the fp32 copy) instead of the fp16 pairs")
     ap.add_argument("--sparse-f64", action="store_true",
@@ -300,10 +311,11 @@ def main():
         return bench_sweep(args, bi, synth, torch, dev)
     if args.workload != "large":
         return bench_agent(args, bi, synth, torch, dev)
-    if args.soft:
-        print("bench.py: --soft applies to the per-agent workloads (--workload)", file=sys.stderr)
-        sys.exit(2)
     w = synth.large_shared()
+    import numpy as np
+    soft_np = (synth.soft_obs(np.random.Generator(np.random.PCG64(17855)), w.obs, w.model.K, confidence=0.7)
+               if args.soft else None)
+    soft_dev = torch.from_numpy(soft_np).to(dev) if args.soft else None
     fast = {"dense": bi.BI_DENSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS,
             "sparse": bi.BI_SPARSE_A | bi.BI_FAST_F32 | bi.BI_F16_PAIRS}
     plain = {"dense": bi.BI_DENSE_A | bi.BI_FAST_F32, "sparse": bi.BI_SPARSE_A}   # fp32 MFMA / fp64 gathers
@@ -317,7 +329,8 @@ def main():
         pms = {lay: bi.PackedModel(w.model, flags=fl[lay], device=dev) for lay in layouts}
         qs = {(lay, a): torch.empty((w.b, w.T, w.model.n_total), dtype=torch.float32, device=dev)
               for lay in layouts for a in ALGOS}
-        wss = {(lay, a): pms[lay].workspace(w.b, w.T, a) for lay in layouts for a in ALGOS}
+        wss = {(lay, a): (pms[lay].workspace_soft if args.soft else pms[lay].workspace)(w.b, w.T, a)
+               for lay in layouts for a in ALGOS}
         for key, ws in wss.items():
             assert ws is not None, f"{key}: the large shared model must run on the streaming kernels"
         for a in ALGOS:
@@ -331,7 +344,10 @@ def main():
                 for a in ALGOS:
                     if marks is not None:
                         marks[(lay, a)][0].record(st)
-                    pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
+                    if args.soft:
+                        pms[lay].infer_soft(a, soft_dev, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
+                    else:
+                        pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
                     if marks is not None:
                         marks[(lay, a)][1].record(st)
         return step
@@ -384,11 +400,13 @@ def main():
     torch.cuda.synchronize()
     call_ms = {k: statistics.median(m[k][0].elapsed_time(m[k][1]) for m in step_marks) for k in qs}
 
-    traffic = load_traffic()
-    dense_work = dense_lik_work(w.model, w.obs)
-    sq_flops, sq_bytes, sq_stored = sparse16_lik_work(w.model, w.obs)
+    # the streaming families ran (soft vectors too: no log-likelihood tensors)
+    assert not any(k.startswith("agent") or k == "soft_ll" for k in prof), sorted(prof)
+    traffic = {} if args.soft else load_traffic()   # the counters were taken with outcomes
+    dense_work = dense_lik_work(w.model, w.obs, soft_np)
+    sq_flops, sq_bytes, sq_stored = sparse16_lik_work(w.model, w.obs, soft_np)
     work = {"lik": dense_work, "lik_split": dense_work, "lik_split16": dense_work, "lik_rowcol16": dense_work,
-            "lik_sparse": sparse_lik_work(w.model, w.obs), "lik_sparse16": (sq_flops, sq_bytes)}
+            "lik_sparse": sparse_lik_work(w.model, w.obs, soft_np), "lik_sparse16": (sq_flops, sq_bytes)}
     rooflines = roofline_entries(prof, work, traffic)
     if "lik_sparse16" in rooflines:
         rooflines["lik_sparse16"]["stored_bytes_per_launch"] = sq_stored
@@ -419,7 +437,9 @@ def main():
                                "b=64, T=16, 16 iters; step = VMP + MMP on the dense ("
                                + ("fp32 MFMA" if args.dense_f32 else "fp16-pair MFMA") + ") and sparse ("
                                + ("fp64 gathers" if args.sparse_f64 else "fp16-pair MFMA from the nonzeros")
-                               + ") A layouts",
+                               + ") A layouts"
+                               + ("; soft observation vectors (every outcome weighted, 0.7 on the drawn one)"
+                                  if args.soft else ""),
                    "b": w.b, "T": w.T, "iters": w.iters, "algos": list(ALGOS), "layouts": layouts},
         "roofline": rooflines[dominant],
         "roofline_all": rooflines,
@@ -472,9 +492,16 @@ def main():
 
     # the oracle timed on the host cores; its outputs on those sampled agents
     # (the same for both layouts) give max |gpu - oracle| of every call
-    import numpy as np
     out["max_abs_err"] = None
-    if not args.no_cpu_baseline:
+    if args.soft:
+        # the oracle forms every context's expected log-likelihood again in
+        # every iteration (32 slices per entry, 34 G logarithms per agent and
+        # call: an estimated 12 minutes on one core), so no bounded sample
+        # exists; the soft streaming path's parity is in the GPU tests
+        out["cpu_baseline"] = None
+        out["cpu_baseline_note"] = ("not timed with soft vectors on this model (an oracle call: an estimated "
+                                    "12 minutes per agent)")
+    elif not args.no_cpu_baseline:
         base, refs, agents = cpu_baseline(w, list(ALGOS), keep=True)
         out["cpu_baseline"] = base
         out["cpu_baseline_1thread"] = cpu_baseline_1thread(w, "vmp")

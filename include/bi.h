@@ -371,13 +371,22 @@ int bi_explain_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, c
  *            outcomes at offset sum_{m' < m} K_m' (a distribution, e.g. a
  *            noisy sensor's output; one-hot reproduces the integer call).
  * Every log A_m[o_{t,m}, s_dep] in the updates above becomes the expected
- * log-likelihood sum_o o_{t,m}[o] log A_m[o, s_dep], formed once per call
- * (before the iterations) in the workspace:
+ * log-likelihood sum_o o_{t,m}[o] log A_m[o, s_dep].  Which kernels run:
+ *   - when bi_query_path picks a streaming family for these arguments (a
+ *     shared model packed for it; VMP or MMP) and every modality has at most
+ *     256 outcomes: that family, over slots (t, o) of each context, slot o
+ *     observing outcome o in every modality whose vector gives o a nonzero
+ *     weight; the update sums a context's slot messages weighted by its
+ *     vectors (fp64).  The likelihood work grows with the nonzero weights per
+ *     vector (one-hot vectors cost the integer call and give its bits);
+ *   - otherwise (FPI, per-agent models, the agent-resident choice): the
+ *     expected log-likelihood tensors, formed once per call before the
+ *     iterations (b * T * sum_m prod_{f in dep(m)} n_f doubles, the slices
+ *     padded as in the packed model), and the agent-resident kernels on the
+ *     dense fp64 planes.
  *   ws_bytes >= bi_workspace_size_soft(model, b, T, algo), 256-byte aligned
- *   (b * T * sum_m prod_{f in dep(m)} n_f doubles, the slices padded as in
- *   the packed model).
+ *   (the streaming workspace with its slots, or the tensors).
  * algo, opts and the other arguments are those of bi_infer; the same errors.
- * Any packed layout works (the dense fp64 planes are used).
  */
 int bi_workspace_size_soft(const bi_model *model, int32_t b, int32_t T, int32_t algo, size_t *bytes);
 int bi_infer_soft(const bi_model *model, int32_t algo, int32_t b, int32_t T, const float *obs_dev,

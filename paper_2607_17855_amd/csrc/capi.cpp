@@ -60,6 +60,16 @@ const char *stream_refusal(const bi_model *m, int algo, bool sparse)
     return "a modality's shape exceeds the streaming kernels' limits (outcomes, modalities or LDS tiles)";
 }
 
+// The family a call with soft observation vectors runs: the streaming family
+// chosen for integer observations when the soft slots fit its limits
+// (stream_soft_ok), else the agent-resident kernels.
+Path soft_path(const bi_model *m, int algo, int b, int T)
+{
+    const Path p = choose_path(m, algo, b, T);
+    if (p != Path::Agent && !bi::stream_soft_ok(m, b, T, p == Path::Sparse)) return Path::Agent;
+    return p;
+}
+
 }  // namespace
 
 namespace bi {
@@ -371,10 +381,15 @@ int bi_workspace_size_soft(const bi_model *model, int32_t b, int32_t T, int32_t 
     if (!model || !bytes) return fail(BI_ERR_INVALID_ARG, "model and bytes must be non-NULL");
     if (b < 1 || T < 1) return fail(BI_ERR_INVALID_ARG, "b and T must be >= 1");
     if (algo < BI_ALGO_FPI || algo > BI_ALGO_MMP) return fail(BI_ERR_INVALID_ARG, "unknown algorithm %d", algo);
-    const int64_t vals = bi::soft_values_per_context(model);
-    if (vals > (INT64_MAX / 8) / ((int64_t)b * T))
-        return fail(BI_ERR_UNSUPPORTED, "soft log-likelihood tensors of b=%d T=%d overflow", b, T);
-    *bytes = (size_t)bi::align_up((int64_t)b * T * vals * 8, bi::kAlign);
+    const Path p = soft_path(model, algo, b, T);
+    if (p != Path::Agent) {
+        *bytes = bi::stream_workspace(model, b, T, p == Path::Sparse, true);
+    } else {
+        const int64_t vals = bi::soft_values_per_context(model);
+        if (vals > (INT64_MAX / 8) / ((int64_t)b * T))
+            return fail(BI_ERR_UNSUPPORTED, "soft log-likelihood tensors of b=%d T=%d overflow", b, T);
+        *bytes = (size_t)bi::align_up((int64_t)b * T * vals * 8, bi::kAlign);
+    }
     if (model->flags & BI_CHECK) *bytes += kStatusBytes;
     return BI_OK;
 }
@@ -408,6 +423,10 @@ int bi_infer_soft(const bi_model *model, int32_t algo, int32_t b, int32_t T, con
                                   reinterpret_cast<int32_t *>(static_cast<char *>(ws_dev) + need - kStatusBytes), s);
             if (rc != BI_OK) return rc;
         }
+        const Path p = soft_path(model, algo, b, T);
+        if (p != Path::Agent)
+            return bi::launch_stream(model, algo, b, T, nullptr, act_dev, prior, tau, iters, q_dev, ws_dev, s,
+                                     p == Path::Sparse, obs_dev);
         double *ll = reinterpret_cast<double *>(ws_dev);
         rc = bi::launch_soft_ll(model, b, T, obs_dev, ll, s);
         if (rc != BI_OK) return rc;

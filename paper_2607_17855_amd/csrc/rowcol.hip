@@ -180,7 +180,7 @@ __device__ void rc_pass(const StreamArgs &a, const Pass &p, const float *__restr
 #pragma unroll 1
     for (int i = tid; i < kCtx * 32; i += kThreads) {
         const int c = i >> 5, s = i & 31, ctx = ctxs[c];
-        const float *qc = q + (int64_t)max(ctx, 0) * a.ntot;
+        const float *qc = q + (int64_t)(max(ctx, 0) >> a.vshift) * a.ntot;
         const float v0 = qc[p.off_c0 + min(s, p.cn0 - 1)], v1 = qc[p.off_c1 + s];
         const float v2 = qc[p.off_r0 + min(s, p.rn0 - 1)], v3 = qc[p.off_r1 + s];
         const bool ok = ctx >= 0;
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(kThreads, 1) void rowcol16_lik_kernel(StreamArgs a,
     for (int c0 = 0; c0 < J; c0 += kCtx) {
         p.jc = min(kCtx, J - c0);
         if (threadIdx.x < kCtx)
-            ctxs[threadIdx.x] = (int)threadIdx.x < p.jc ? a.bctx[(int64_t)m * a.nctx + b0 + c0 + threadIdx.x] : -1;
+            ctxs[threadIdx.x] = (int)threadIdx.x < p.jc ? a.bctx[(int64_t)m * a.nlist + b0 + c0 + threadIdx.x] : -1;
         __syncthreads();
         const int nkb = (p.jc + 15) >> 4;
         if (nkb == 1) rc_pass<1>(a, p, q, part, ctxs, lds);

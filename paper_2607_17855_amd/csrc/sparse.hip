@@ -156,7 +156,7 @@ __global__ __launch_bounds__(kSpThreads, 6) void sparse_lik_kernel(StreamArgs a,
     for (int c0 = 0; c0 < J; c0 += kSpLanes) {
         const int jc = min(kSpLanes, J - c0);
         pf = touch(lb + wave);   // first line of this wave, overlapping the table build
-        if (tid < kSpLanes) ctxs[tid] = tid < jc ? a.bctx[(int64_t)tk.m * a.nctx + b0 + c0 + tid] : -1;
+        if (tid < kSpLanes) ctxs[tid] = tid < jc ? a.bctx[(int64_t)tk.m * a.nlist + b0 + c0 + tid] : -1;
         __syncthreads();
         // entry-side marginal tables (1.0 for an absent factor)
         for (int i = tid; i < ntab * kSpLanes; i += kSpThreads) {
@@ -164,7 +164,7 @@ __global__ __launch_bounds__(kSpThreads, 6) void sparse_lik_kernel(StreamArgs a,
             const int ctx = ctxs[c];
             double v = 0.0;
             if (ctx >= 0) {
-                const double *qc = q + (int64_t)ctx * a.ntot;
+                const double *qc = q + (int64_t)(ctx >> a.vshift) * a.ntot;
                 if (s < en0)
                     v = off_e0 >= 0 ? qc[off_e0 + s] : 1.0;
                 else
@@ -224,20 +224,20 @@ __global__ __launch_bounds__(kSpThreads, 6) void sparse_lik_kernel(StreamArgs a,
             // first line factor: one message per (context, group), summed over l1
             for (int i = tid; i < jc * ng; i += kSpThreads) {
                 const int c = i / ng, g = i - c * ng;
-                const double *qc = q + (int64_t)ctxs[c] * a.ntot + off_l1;
+                const double *qc = q + (int64_t)(ctxs[c] >> a.vshift) * a.ntot + off_l1;
                 part[(int64_t)ctxs[c] * ps + tk.so + g0 + g] = dot_batched(zt + g * ln1 * kZS + c, kZS, qc, ln1);
             }
             // second line factor: the tile's partial, summed over its groups
             for (int i = tid; i < jc * ln1; i += kSpThreads) {
                 const int c = i / ln1, l1 = i - c * ln1;
-                const double *qc = q + (int64_t)ctxs[c] * a.ntot + off_l0 + g0;
+                const double *qc = q + (int64_t)(ctxs[c] >> a.vshift) * a.ntot + off_l0 + g0;
                 part[(int64_t)ctxs[c] * ps + tk.so + sd_.ln0 + (int64_t)tile * ln1 + l1] =
                     dot_batched(zt + l1 * kZS + c, ln1 * kZS, qc, ng);
             }
         }
         __syncthreads();
     }
-    if (sink == 0x5a5a5a5a && a.nctx < 0) part[0] = 0.0;   // never true (nctx >= 1): keeps the touches
+    if (sink == 0x5a5a5a5a && a.nlist < 0) part[0] = 0.0;   // never true (nlist >= 1): keeps the touches
 }
 
 inline size_t lds_for(const Side &s)

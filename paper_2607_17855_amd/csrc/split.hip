@@ -76,6 +76,7 @@ constexpr float kPairScale = 32768.0f;   // 2^15: q_e1 in [0, 1] scaled below th
 // state e0: kSqR.
 constexpr int kSqWaveBytes = 2 * sq_plane_bytes(32);
 constexpr int kSqR = 4;
+constexpr int kSqDepth = 4;   // a ring of states: the entries of 3 fetched ahead of the one in use
 constexpr uint32_t kBufWord3 = 0x00020000u;   // buffer resource config word of the gfx9 family: raw dwords
 
 // kernel variants: dense fp32 slices, dense fp16 pairs, sparse fp16 pairs
@@ -470,14 +471,21 @@ __device__ void sq_tile(const Geo &g, const uint32_t *__restrict__ ptr, const Sq
                 }
             }
         };
-        // en0 is even: ping-pong over pairs of states
-        w2 ea[kSqR], eb[kSqR];
-        fetch(ea, 0);
-        for (int e0 = 0; e0 < en0; e0 += 2) {
-            fetch(eb, e0 + 1);
-            step(ea, e0);
-            if (e0 + 2 < en0) fetch(ea, e0 + 2);
-            step(eb, e0 + 1);
+        // a ring of kSqDepth states: the entries of the next kSqDepth - 1
+        // states are in flight while one is used
+        w2 E[kSqDepth][kSqR];
+#pragma unroll
+        for (int k = 0; k < kSqDepth - 1; ++k)
+            if (k < en0) fetch(E[k], k);
+        for (int e0 = 0; e0 < en0; e0 += kSqDepth) {
+#pragma unroll
+            for (int k = 0; k < kSqDepth; ++k) {
+                const int e = e0 + k;
+                if (e < en0) {
+                    if (e + kSqDepth - 1 < en0) fetch(E[(k + kSqDepth - 1) % kSqDepth], e + kSqDepth - 1);
+                    step(E[k], e);
+                }
+            }
         }
     }
     __syncthreads();   // every wave is done with its block: zt overlays them
@@ -553,7 +561,7 @@ __device__ void split_body(const StreamArgs &a, const float *__restrict__ q, flo
 
     for (int c0 = 0; c0 < J; c0 += kCtx) {
         const int jc = min(kCtx, J - c0);
-        if (tid < kCtx) ctxs[tid] = tid < jc ? a.bctx[(int64_t)m * a.nctx + b0 + c0 + tid] : -1;
+        if (tid < kCtx) ctxs[tid] = tid < jc ? a.bctx[(int64_t)m * a.nlist + b0 + c0 + tid] : -1;
         if (MODE == kSparsePairs)   // zero B blocks (the line tile of the last pass overlays them)
             for (int i = tid; i < kWaves * kSqWaveBytes / 16; i += kThreads)
                 reinterpret_cast<u4 *>(blocks)[i] = u4{0u, 0u, 0u, 0u};
@@ -568,7 +576,7 @@ __device__ void split_body(const StreamArgs &a, const float *__restrict__ q, flo
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
                 const int i = i0 + k * kThreads, c = i >> 5, s = i & 31;
-                const float *qc = q + (int64_t)max(ctxs[c], 0) * a.ntot;
+                const float *qc = q + (int64_t)(max(ctxs[c], 0) >> a.vshift) * a.ntot;
                 v[k][0] = qc[off_e0 + min(s, g.en0 - 1)];
                 v[k][1] = qc[off_e1 + min(s, g.en1 - 1)];
                 v[k][2] = qc[off_l0 + min(s, g.ln0 - 1)];

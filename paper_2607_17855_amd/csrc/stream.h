@@ -26,8 +26,8 @@ struct StreamMod {
     int ntiles;   // row tiles of a slice (dense path)
     int wg0;      // first workgroup of this modality in the dense likelihood grid
     int bofs;     // offset of this modality's K+1 bucket starts
-    int fofs;     // (reserved)
-    int pad;
+    int fofs;     // offset of its outcomes in a soft observation vector (sum of the earlier K)
+    int pbeg;     // first value of its partial messages inside a context's partial block
     int64_t poff; // offset of its partial messages inside a context's partial block (dense path)
 };
 
@@ -73,6 +73,16 @@ struct StreamArgs {
     int32_t *bstart, *bctx;
     int nmsg, ntask;
     int stage;                  // update: partial messages and neighbour marginals staged in LDS
+    // Soft observations: every context c stands for 2^vshift slots c 2^vshift + o,
+    // slot o observing outcome o of every modality whose vector gives it a
+    // nonzero weight.  The likelihood kernels treat slots as contexts (bucket
+    // lists and partial blocks per slot, marginals of slot >> vshift); the
+    // update sums a context's slots weighted by its vectors.  vshift = 0 and
+    // soft = NULL for integer observations.
+    int vshift;
+    int nlist;                  // bucket-list length per modality: nctx << vshift
+    int ksum;                   // values per soft observation vector (sum of K)
+    const float *soft;          // [nctx][ksum] soft observation vectors, or NULL
     int flip;                   // likelihood launches: walk the work items in reverse order (odd iterations)
     int trivb;                  // every B-dependency list is {f} (else the update's general transition messages)
     StreamMod sm[kStreamMaxM];
@@ -85,11 +95,17 @@ struct StreamArgs {
 bool stream_eligible(const bi_model *m, int algo);
 // Whether `m` can run `algo` on the sparse streaming kernels.
 bool sparse_eligible(const bi_model *m, int algo);
-// Workspace bytes of a streaming call with b agents and window T.
-size_t stream_workspace(const bi_model *m, int b, int T, bool sparse);
-// Enqueue a streaming VMP / MMP call (dense or sparse likelihood kernels).
+// Workspace bytes of a streaming call with b agents and window T (soft:
+// observation vectors instead of outcomes).
+size_t stream_workspace(const bi_model *m, int b, int T, bool sparse, bool soft = false);
+// Whether a streaming call with soft observation vectors fits its limits (the
+// slots' partial blocks staged in the update's LDS, 32-bit slot indices).
+bool stream_soft_ok(const bi_model *m, int b, int T, bool sparse);
+// Enqueue a streaming VMP / MMP call (dense or sparse likelihood kernels);
+// with soft != NULL the [b][T][sum K] observation vectors replace obs.
 int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
-                  const float *prior, double tau, int iters, float *q, void *ws, hipStream_t stream, bool sparse);
+                  const float *prior, double tau, int iters, float *q, void *ws, hipStream_t stream, bool sparse,
+                  const float *soft = nullptr);
 
 // Dense likelihood kernel with one contraction per workgroup (split.hip), for
 // models whose modalities all have two factors per side (second factors of

@@ -84,10 +84,21 @@ __global__ __launch_bounds__(1024) void prep_kernel(StreamArgs a, QT *q)
     const int m = blockIdx.x;
     const StreamMod &sm = a.sm[m];
     int *fil = cnt + sm.K + 1;
-    int32_t *list = a.bctx + (int64_t)m * a.nctx;
+    int32_t *list = a.bctx + (int64_t)m * a.nlist;
+    // the outcome list entry i observes in this modality (-1: none): the
+    // context's outcome, or for soft vectors the slot's outcome when the
+    // context's vector gives it a nonzero weight
+    auto outcome = [&](int i) -> int {
+        if (!a.soft) return a.obs[(int64_t)i * a.M + m];
+        const int c = i >> a.vshift, o = i & ((1 << a.vshift) - 1);
+        return o < sm.K && a.soft[(int64_t)c * a.ksum + sm.fofs + o] != 0.0f ? o : -1;
+    };
     for (int o = threadIdx.x; o < 2 * sm.K + 1; o += blockDim.x) cnt[o] = 0;
     __syncthreads();
-    for (int i = threadIdx.x; i < a.nctx; i += blockDim.x) atomicAdd(&cnt[a.obs[(int64_t)i * a.M + m]], 1);
+    for (int i = threadIdx.x; i < a.nlist; i += blockDim.x) {
+        const int o = outcome(i);
+        if (o >= 0) atomicAdd(&cnt[o], 1);
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
         int run = 0;
@@ -101,9 +112,9 @@ __global__ __launch_bounds__(1024) void prep_kernel(StreamArgs a, QT *q)
     __syncthreads();
     int32_t *start = a.bstart + sm.bofs;
     for (int o = threadIdx.x; o <= sm.K; o += blockDim.x) start[o] = cnt[o];
-    for (int i = threadIdx.x; i < a.nctx; i += blockDim.x) {
-        const int o = a.obs[(int64_t)i * a.M + m];
-        list[cnt[o] + atomicAdd(&fil[o], 1)] = i;
+    for (int i = threadIdx.x; i < a.nlist; i += blockDim.x) {
+        const int o = outcome(i);
+        if (o >= 0) list[cnt[o] + atomicAdd(&fil[o], 1)] = i;
     }
 }
 
@@ -119,7 +130,7 @@ struct LikShared {
 
 __device__ inline const float *qrow(const StreamArgs &a, const float *q, int ctx, int f)
 {
-    return q + (int64_t)ctx * a.ntot + a.facs[f].q_off;
+    return q + (int64_t)(ctx >> a.vshift) * a.ntot + a.facs[f].q_off;
 }
 
 // Fold a block of one side's values W[c][k] (k = index lo..hi-1 along that
@@ -271,7 +282,7 @@ __global__ __launch_bounds__(kThreads, 1) void lik_kernel(StreamArgs a, const fl
     for (int g0 = 0; g0 < J; g0 += kJG) {
         const int jg = min(kJG, J - g0);
         const int nkb = (jg + 15) >> 4;
-        if (tid < kJG) ctxs[tid] = tid < jg ? a.bctx[(int64_t)m * a.nctx + b0 + g0 + tid] : -1;
+        if (tid < kJG) ctxs[tid] = tid < jg ? a.bctx[(int64_t)m * a.nlist + b0 + g0 + tid] : -1;
         __syncthreads();
         for (int i = tid; i < kJG * ncs; i += kThreads) {
             const int c = i / ncs, e = i - c * ncs;
@@ -671,13 +682,43 @@ __global__ __launch_bounds__(256, 4) void update_kernel(StreamArgs a, const PT *
         QT *sq = reinterpret_cast<QT *>(vals + a.ntot + (a.pstride * sizeof(PT) + 7) / 8);
         const int tid = threadIdx.x;
         const int np = (int)a.pstride, nq = a.ntot;
-        for (int i0 = tid; i0 < np; i0 += 8 * 256) {   // 8 independent loads per thread, then the stores
-            PT v[8];
+        if (a.soft) {
+            // soft vectors: value i of modality m's range is sum_o w_m[o]
+            // x (value i of slot o), in fp64 and in o order, over the slots
+            // of nonzero weight (the others were not computed: their values
+            // are loaded, from inside the buffer, and not used)
+            const float *wc = a.soft + (int64_t)ctx * a.ksum;
+            const PT *p0 = part + ((int64_t)ctx << a.vshift) * a.pstride;
+            for (int i = tid; i < np; i += 256) {
+                int mm = 0;
+                while (mm + 1 < a.M && a.sm[mm + 1].pbeg <= i) ++mm;
+                const float *w = wc + a.sm[mm].fofs;
+                const int K = a.sm[mm].K;
+                double acc = 0.0;
+                for (int o0 = 0; o0 < K; o0 += 8) {
+                    float wv[8];
+                    PT pv[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = pc[min(i0 + 256 * u, np - 1)];
+                    for (int u = 0; u < 8; ++u) {
+                        const int o = min(o0 + u, K - 1);
+                        wv[u] = o0 + u < K ? w[o] : 0.0f;
+                        pv[u] = p0[(int64_t)o * a.pstride + i];
+                    }
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (i0 + 256 * u < np) sp[i0 + 256 * u] = v[u];
+                    for (int u = 0; u < 8; ++u)
+                        if (wv[u] != 0.0f) acc = fma((double)wv[u], (double)pv[u], acc);
+                }
+                sp[i] = (PT)acc;
+            }
+        } else {
+            for (int i0 = tid; i0 < np; i0 += 8 * 256) {   // 8 independent loads per thread, then the stores
+                PT v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) v[u] = pc[min(i0 + 256 * u, np - 1)];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (i0 + 256 * u < np) sp[i0 + 256 * u] = v[u];
+            }
         }
         for (int i = tid; i < nq; i += 256) {
             const QT a0 = qp[i], a1 = qn[i];
@@ -791,9 +832,16 @@ static Lik lik_kind(const bi_model *m, bool sparse)
 // Plan of the workspace: bucket starts / fill counters / sorted contexts /
 // partial messages / two marginal buffers (fp32, or fp64 for the sparse fp64
 // kernel).
-static void plan_ws(const bi_model *m, int b, int T, bool sparse, StreamArgs *a, int64_t *offs, int64_t *total)
+static void plan_ws(const bi_model *m, int b, int T, bool sparse, bool soft, StreamArgs *a, int64_t *offs,
+                    int64_t *total)
 {
     const int nctx = b * T;
+    int kmax = 1;
+    for (const ModDesc &md : m->mods) kmax = std::max(kmax, md.K);
+    a->vshift = 0;
+    while (soft && (1 << a->vshift) < kmax) ++a->vshift;
+    const int64_t nlist = (int64_t)nctx << a->vshift;
+    a->nlist = (int)std::min<int64_t>(nlist, INT32_MAX);
     int bofs = 0, fofs = 0;
     for (int i = 0; i < m->M; ++i) {
         StreamMod &sm = a->sm[i];
@@ -808,23 +856,48 @@ static void plan_ws(const bi_model *m, int b, int T, bool sparse, StreamArgs *a,
                  : lik == Lik::Dense  ? dense_plan(m, a)
                  : lik == Lik::RowCol ? rc_plan(m, a)
                                       : split_plan(m, a);
+    // where each modality's partial messages start (the plans lay them out in
+    // modality order)
+    for (int i = 0; i < m->M; ++i) a->sm[i].pbeg = lik == Lik::Dense ? (int)a->sm[i].poff : INT32_MAX;
+    if (lik != Lik::Dense)
+        for (int k = 0; k < a->ntask; ++k) a->sm[a->task[k].m].pbeg = std::min(a->sm[a->task[k].m].pbeg, a->task[k].so);
+    a->ksum = fofs;
     const int64_t es = lik == Lik::Sparse ? 8 : 4;
     int64_t off = 0;
     offs[0] = off;  off = align_up(off + 4 * (int64_t)bofs, kAlign);
     offs[1] = off;  off = align_up(off + 4 * (int64_t)fofs, kAlign);
-    offs[2] = off;  off = align_up(off + 4 * (int64_t)m->M * nctx, kAlign);
-    offs[3] = off;  off = align_up(off + es * (int64_t)nctx * a->pstride, kAlign);
+    offs[2] = off;  off = align_up(off + 4 * (int64_t)m->M * nlist, kAlign);
+    offs[3] = off;  off = align_up(off + es * nlist * a->pstride, kAlign);
     offs[4] = off;  off = align_up(off + es * (int64_t)nctx * m->ntot, kAlign);
     offs[5] = off;  off = align_up(off + es * (int64_t)nctx * m->ntot, kAlign);
     *total = off;
 }
 
-size_t stream_workspace(const bi_model *m, int b, int T, bool sparse)
+size_t stream_workspace(const bi_model *m, int b, int T, bool sparse, bool soft)
 {
     StreamArgs a{};
     int64_t offs[6], total;
-    plan_ws(m, b, T, sparse, &a, offs, &total);
+    plan_ws(m, b, T, sparse, soft, &a, offs, &total);
     return (size_t)total;
+}
+
+// LDS bytes of the update's staging: the softmax values, the partial messages
+// and the two neighbour marginal vectors
+static size_t staged_bytes(const bi_model *m, const StreamArgs &a, Lik lik)
+{
+    const size_t es_p = lik == Lik::Sparse ? sizeof(double) : sizeof(float);   // partials and marginals
+    return sizeof(double) * m->ntot + (a.pstride * es_p + 7) / 8 * 8 + 2 * es_p * m->ntot;
+}
+constexpr size_t kStagedMax = 48 * 1024;
+constexpr int kSoftMaxShift = 8;   // soft vectors on the streaming kernels: at most 256 outcomes per modality
+
+bool stream_soft_ok(const bi_model *m, int b, int T, bool sparse)
+{
+    StreamArgs a{};
+    int64_t offs[6], total;
+    plan_ws(m, b, T, sparse, true, &a, offs, &total);
+    return a.vshift <= kSoftMaxShift && ((int64_t)b * T << a.vshift) < INT32_MAX &&
+           staged_bytes(m, a, lik_kind(m, sparse)) <= kStagedMax;
 }
 
 template <typename QT>
@@ -874,11 +947,14 @@ static void run_iterations(const bi_model *m, int algo, int iters, const StreamA
 }
 
 int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs, const int32_t *act,
-                  const float *prior, double tau, int iters, float *q, void *ws, hipStream_t stream, bool sparse)
+                  const float *prior, double tau, int iters, float *q, void *ws, hipStream_t stream, bool sparse,
+                  const float *soft)
 {
     StreamArgs a{};
     int64_t offs[6], total;
-    plan_ws(m, b, T, sparse, &a, offs, &total);
+    plan_ws(m, b, T, sparse, soft != nullptr, &a, offs, &total);
+    if (soft && !stream_soft_ok(m, b, T, sparse))
+        return fail(BI_ERR_UNSUPPORTED, "soft observations exceed the streaming kernels' limits");
     char *w = reinterpret_cast<char *>(ws);
     a.base = m->dev;
     a.mods = reinterpret_cast<const ModDesc *>(m->dev);
@@ -889,6 +965,7 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
     a.nctx = b * T;
     a.ntot = m->ntot;
     a.obs = obs;
+    a.soft = soft;
     a.act = act;
     a.prior = prior;
     a.tau = tau;
@@ -906,9 +983,8 @@ int launch_stream(const bi_model *m, int algo, int b, int T, const int32_t *obs,
             if (fd.lb32_off < 0) return fail(BI_ERR_INVALID_ARG, "fp32 log B missing (pack with BI_FAST_F32)");
     // update: the softmax values, plus (when they fit in 48 KB) the staged
     // partial messages and the two neighbour marginal vectors
-    const size_t es_p = lik == Lik::Sparse ? sizeof(double) : sizeof(float);   // partials and marginals
-    const size_t staged = sizeof(double) * m->ntot + (a.pstride * es_p + 7) / 8 * 8 + 2 * es_p * m->ntot;
-    a.stage = staged <= 48 * 1024 ? 1 : 0;
+    const size_t staged = staged_bytes(m, a, lik);
+    a.stage = staged <= kStagedMax ? 1 : 0;
     const size_t upd_lds = a.stage ? staged : sizeof(double) * m->ntot;
     size_t lik_lds = 0;
     if (lik == Lik::Sparse) {

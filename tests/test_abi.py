@@ -818,3 +818,35 @@ def test_host_pack_long_dependency_lists(flags):
                 assert (md.la32_off >= 0) == narrow and (md.csr_ptr_off >= 0) == narrow
     finally:
         bi.bi_free_model(h)
+
+
+def test_soft_workspace_follows_the_family(monkeypatch):
+    """Soft vectors on a shared model run the streaming family chosen for
+    integer outcomes (slots per context: a larger workspace than the integer
+    call's) unless a modality has more than 256 outcomes; FPI and the agent
+    path take the log-likelihood tensors."""
+    def ll_bytes(img, model, b, T):
+        mods, _ = _descs(img, model.M, model.F)
+        per_ctx = sum(int(mods[i].slice) for i in range(model.M))
+        return -(-b * T * per_ctx * 8 // 256) * 256
+
+    for K, slots in (([3, 2], True), ([300, 2], False)):
+        rng = np.random.Generator(np.random.PCG64(2400 + K[0]))
+        model = synth.make_model(rng, [4, 3, 5], [2, 1, 2], K, [[0, 1, 2], [1]], 1, 1.0, 1.0, uniform_D=False)
+        h, img = bi.bi_pack_model_host(model.n, model.U, model.K, model.deps, 1, model.A, model.B, model.D,
+                                       bi.BI_DENSE_A | bi.BI_FAST_F32)
+        try:
+            b, T = 6, 4
+            monkeypatch.setenv("BI_FORCE_PATH", "stream")
+            for algo in (bi.BI_ALGO_VMP, bi.BI_ALGO_MMP):
+                assert bi.bi_query_path(h, b, T, algo) == bi.BI_PATH_STREAM
+                soft, hard = bi.bi_workspace_size_soft(h, b, T, algo), bi.bi_workspace_size(h, b, T, algo)
+                if slots:
+                    assert soft > hard and soft != ll_bytes(img, model, b, T)
+                else:
+                    assert soft == ll_bytes(img, model, b, T)
+            assert bi.bi_workspace_size_soft(h, b, T, bi.BI_ALGO_FPI) == ll_bytes(img, model, b, T)
+            monkeypatch.setenv("BI_FORCE_PATH", "agent")
+            assert bi.bi_workspace_size_soft(h, b, T, bi.BI_ALGO_VMP) == ll_bytes(img, model, b, T)
+        finally:
+            bi.bi_free_model(h)

@@ -151,3 +151,95 @@ def test_soft_streaming_matches_agent_path(family_env):
             assert err <= TOL
     finally:
         pm.close()
+
+
+@pytest.mark.parametrize("case", [4, 6])
+def test_soft_streaming_prior_and_damping(case, family_env):
+    """A prior over the first step and a damping step on the soft streaming
+    call, against the oracle with the same options."""
+    w, flags, fam, kern = _workload(case, iters=3)
+    so = _vectors(2500 + case, w)
+    prior = synth.random_prior(np.random.Generator(np.random.PCG64(2510 + case)), w.model.n, w.b, alpha=0.7,
+                               p_zero=0.3)
+    os.environ["BI_FORCE_PATH"] = fam
+    torch = _torch()
+    pm = bi.PackedModel(w.model, flags)
+    try:
+        for algo in ("vmp", "mmp"):
+            print(f"[gpu] {w.name} soft {algo} on {fam} prior + damping 0.7", flush=True)
+            bi.bi_profile_begin()
+            q = pm.infer_soft(algo, _dev(so), _dev(w.act), w.iters, prior=_dev(prior), damping=0.7)
+            torch.cuda.synchronize()
+            names = set(bi.bi_profile_end())
+            assert kern in names, names
+            q = q.cpu().numpy()
+            check_invariants(w, q)
+            ref = oracle.infer_soft(algo, w.model, so.astype(np.float64), w.act, w.iters, prior=prior,
+                                    damping=0.7)
+            err = float(np.abs(q - ref).max())
+            print(f"[gpu]   soft prior+damping vs oracle {err:.3e}", flush=True)
+            assert err <= TOL
+    finally:
+        pm.close()
+
+
+@pytest.mark.parametrize("case", [4, 6])
+def test_soft_streaming_graph_replay(case, family_env):
+    """The soft streaming call captured in a HIP graph replays the eager
+    call's bits, with eager calls on the same workspace between replays."""
+    torch = _torch()
+    w, flags, fam, kern = _workload(case)
+    so = _dev(_vectors(2600 + case, w))
+    act = _dev(w.act)
+    os.environ["BI_FORCE_PATH"] = fam
+    pm = bi.PackedModel(w.model, flags)
+    try:
+        for algo in ("vmp", "mmp"):
+            print(f"[gpu] {w.name} soft {algo} on {fam} graph capture", flush=True)
+            ws = pm.workspace_soft(w.b, w.T, algo)
+            shape = (w.b, w.T, w.model.n_total)
+            q_eager = torch.empty(shape, dtype=torch.float32, device="cuda")
+            pm.infer_soft(algo, so, act, w.iters, q=q_eager, ws=ws)
+            torch.cuda.synchronize()
+            ref = q_eager.cpu().numpy()
+            q_g = torch.empty(shape, dtype=torch.float32, device="cuda")
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                pm.infer_soft(algo, so, act, w.iters, q=q_g, ws=ws)
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                pm.infer_soft(algo, so, act, w.iters, q=q_g, ws=ws)
+            for rep in range(3):
+                q_g.fill_(-1.0)
+                pm.infer_soft(algo, so, act, w.iters, q=q_eager, ws=ws)
+                torch.cuda.synchronize()
+                graph.replay()
+                torch.cuda.synchronize()
+                got = q_g.cpu().numpy()
+                assert np.array_equal(got, ref), f"replay {rep}: max diff {np.abs(got - ref).max()}"
+            del graph
+    finally:
+        pm.close()
+
+
+def test_soft_streaming_with_input_check(family_env):
+    """BI_CHECK on a soft streaming call: the status words after the slots'
+    workspace; the result equals the unchecked call's."""
+    torch = _torch()
+    w, flags, fam, kern = _workload(4)
+    so = _vectors(2700, w)
+    os.environ["BI_FORCE_PATH"] = fam
+    pm0 = bi.PackedModel(w.model, flags)
+    pm1 = bi.PackedModel(w.model, flags | bi.BI_CHECK)
+    try:
+        for algo in ("vmp", "mmp"):
+            q0, _ = _soft_call(pm0, algo, so, w)
+            q1, names = _soft_call(pm1, algo, so, w)
+            assert kern in names, names
+            assert np.array_equal(q0, q1)
+    finally:
+        pm0.close()
+        pm1.close()

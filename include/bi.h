@@ -373,8 +373,11 @@ int bi_explain_path(const bi_model *model, int32_t b, int32_t T, int32_t algo, c
  * Every log A_m[o_{t,m}, s_dep] in the updates above becomes the expected
  * log-likelihood sum_o o_{t,m}[o] log A_m[o, s_dep].  Which kernels run:
  *   - when bi_query_path picks a streaming family for these arguments (a
- *     shared model packed for it; VMP or MMP) and every modality has at most
- *     256 outcomes: that family, over slots (t, o) of each context, slot o
+ *     shared model packed for it; VMP or MMP), the model holds more A
+ *     entries than the models the selector was timed on (about 4.3 million;
+ *     there the agent-resident kernels are far slower) or BI_FORCE_PATH names that
+ *     family, and every modality has at most 256 outcomes: that family, over
+ *     slots (t, o) of each context, slot o
  *     observing outcome o in every modality whose vector gives o a nonzero
  *     weight; the update sums a context's slot messages weighted by its
  *     vectors (fp64).  The likelihood work grows with the nonzero weights per

@@ -60,14 +60,22 @@ const char *stream_refusal(const bi_model *m, int algo, bool sparse)
     return "a modality's shape exceeds the streaming kernels' limits (outcomes, modalities or LDS tiles)";
 }
 
-// The family a call with soft observation vectors runs: the streaming family
-// chosen for integer observations when the soft slots fit its limits
-// (stream_soft_ok), else the agent-resident kernels.
+// The family a call with soft observation vectors runs.  On the streaming
+// kernels a vector weighting k outcomes costs about k likelihood launches'
+// work, on the agent-resident ones the log-likelihood tensors cost little
+// more than the integer call, so soft vectors stream only where the agent
+// path is far behind: models beyond the selector's timed range (on the
+// shared F=4x32 model, 33 ms against 722 ms per call; on the sweep models
+// the selector streams, the agent path was 3-12x faster with soft vectors),
+// or when BI_FORCE_PATH names the family; and only when the slots fit the
+// streaming limits (stream_soft_ok).
 Path soft_path(const bi_model *m, int algo, int b, int T)
 {
     const Path p = choose_path(m, algo, b, T);
-    if (p != Path::Agent && !bi::stream_soft_ok(m, b, T, p == Path::Sparse)) return Path::Agent;
-    return p;
+    if (p == Path::Agent || !bi::stream_soft_ok(m, b, T, p == Path::Sparse)) return Path::Agent;
+    const char *env = std::getenv("BI_FORCE_PATH");
+    const bool forced = env && std::strcmp(env, p == Path::Sparse ? "sparse" : "stream") == 0;
+    return forced || bi::beyond_timed_range(m) ? p : Path::Agent;
 }
 
 }  // namespace

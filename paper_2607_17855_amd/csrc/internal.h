@@ -67,6 +67,9 @@ int check_inputs(const bi_model *m, int b, int T, const int32_t *obs, const int3
 // ones (agent always; stream / sparse as flagged), for algo over b agents and
 // a window of T steps.
 int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool sparse);
+// Whether the model holds more A entries than any model the selector was
+// fitted on (the selector then decides by a rule).
+bool beyond_timed_range(const bi_model *m);
 
 // The inference call behind bi_infer and the named entry points (capi.cpp):
 // host validation, optional input check, then the chosen kernel family with

@@ -83,6 +83,13 @@ int streaming_pairs(const bi_model *m, bool stream)
 
 }  // namespace
 
+bool beyond_timed_range(const bi_model *m)
+{
+    double x[kNumFeatures];
+    features(m, 1, 1, x);
+    return x[kFeatAFloats] > kSelMaxAFloats;
+}
+
 int select_path(const bi_model *m, int algo, int b, int T, bool stream, bool sparse)
 {
     // 1: {agent, stream}, 2: {agent, sparse}, 3: all three; + 4 when the

@@ -821,10 +821,10 @@ def test_host_pack_long_dependency_lists(flags):
 
 
 def test_soft_workspace_follows_the_family(monkeypatch):
-    """Soft vectors on a shared model run the streaming family chosen for
-    integer outcomes (slots per context: a larger workspace than the integer
-    call's) unless a modality has more than 256 outcomes; FPI and the agent
-    path take the log-likelihood tensors."""
+    """Soft vectors on a shared model forced onto a streaming family run it
+    (slots per context: a larger workspace than the integer call's) unless a
+    modality has more than 256 outcomes; FPI, the agent path and models
+    inside the selector's timed range take the log-likelihood tensors."""
     def ll_bytes(img, model, b, T):
         mods, _ = _descs(img, model.M, model.F)
         per_ctx = sum(int(mods[i].slice) for i in range(model.M))
@@ -848,5 +848,10 @@ def test_soft_workspace_follows_the_family(monkeypatch):
             assert bi.bi_workspace_size_soft(h, b, T, bi.BI_ALGO_FPI) == ll_bytes(img, model, b, T)
             monkeypatch.setenv("BI_FORCE_PATH", "agent")
             assert bi.bi_workspace_size_soft(h, b, T, bi.BI_ALGO_VMP) == ll_bytes(img, model, b, T)
+            # unforced: a model inside the selector's timed range keeps soft
+            # vectors agent-resident whatever family takes its integer calls
+            monkeypatch.delenv("BI_FORCE_PATH")
+            for algo in (bi.BI_ALGO_VMP, bi.BI_ALGO_MMP):
+                assert bi.bi_workspace_size_soft(h, b, T, algo) == ll_bytes(img, model, b, T)
         finally:
             bi.bi_free_model(h)

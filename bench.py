@@ -15,10 +15,15 @@ VMP and MMP over the whole batch on both A layouts:
          fp16 pairs (8 bytes each) in blocks of 64 lines, scattered per
          first-factor state into LDS and contracted on the same fp16 matrix
          cores (--sparse-f64: fp64 gathers over the nonzero entries instead).
-Inputs are resident in HBM before timing starts; each model is packed once
-outside the timed region (the one-time layout step).  After the set-up the
-step runs 30 untimed settle steps, then the --warmup steps, then the timed
---steps.
+The two layouts' calls share nothing but the GPU, so a step runs each
+layout's calls (VMP, then MMP) on a stream of its own, forked from and joined
+back to the timing stream: the HBM-bound dense calls overlap the
+instruction-bound sparse ones.  The record also carries the same step with
+every call on one stream (`serial`); the per-kernel and per-call passes run
+serially.  Inputs are resident in HBM before timing starts; each model is
+packed once outside the timed region (the one-time layout step).  After the
+set-up the step runs 30 untimed settle steps, then the --warmup steps, then
+the timed --steps.
 
 Prints one JSON line.  value = belief updates per second over the whole job,
 one belief update being one (agent, time step, iteration) of one algorithm
@@ -32,9 +37,9 @@ modalities on both, T=10, b=1024, VMP), mmp_3f (F=3 of 12/10/8 states, M=4 x
 (the same, online: T calls of one step, each carrying the predictive prior of
 the step before through bi_predict), mmp_3f_bdeps (the F=3 structure with
 every factor's transition conditioned on itself and one other factor).  --soft
-runs such a workload with soft
-observation vectors (each puts 0.7 on the sampled outcome and spreads the
-rest as a Dirichlet(1) draw) through bi_infer_soft.
+runs a workload (the large one too) with soft observation vectors (each puts
+0.7 on the sampled outcome and spreads the rest as a Dirichlet(1) draw)
+through bi_infer_soft.
 """
 import argparse
 import hashlib
@@ -338,28 +343,49 @@ def main():
                 assert pms["sparse"].path(w.b, w.T, a) == "sparse", "the sparse layout must run the sparse kernels"
         return pms, qs, wss
 
+    # the layouts' calls share nothing but the GPU: the headline step runs
+    # each layout's calls (VMP, then MMP) on a stream of its own, forked from
+    # and joined back to the timing stream (default priority), so the
+    # HBM-bound dense calls and the instruction-bound sparse ones overlap
+    side = {lay: torch.cuda.Stream(device=dev) for lay in layouts}
+
     def make_step(pms, qs, wss):
-        def step(st=stream, marks=None):
+        def call(lay, a, st):
+            if args.soft:
+                pms[lay].infer_soft(a, soft_dev, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
+            else:
+                pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
+
+        def step(st=stream, marks=None, serial=False):
+            if not serial and marks is None and st is not None and len(layouts) > 1:
+                fork = torch.cuda.Event()
+                fork.record(st)
+                for lay in layouts:
+                    side[lay].wait_event(fork)
+                    for a in ALGOS:
+                        call(lay, a, side[lay])
+                for lay in layouts:
+                    join = torch.cuda.Event()
+                    join.record(side[lay])
+                    st.wait_event(join)
+                return
             for lay in layouts:
                 for a in ALGOS:
                     if marks is not None:
                         marks[(lay, a)][0].record(st)
-                    if args.soft:
-                        pms[lay].infer_soft(a, soft_dev, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
-                    else:
-                        pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
+                    call(lay, a, st)
                     if marks is not None:
                         marks[(lay, a)][1].record(st)
         return step
 
-    def timed(step):
-        """ms per step over args.steps steps, nothing else on the stream."""
+    def timed(step, serial=False):
+        """ms per step over args.steps steps, nothing else on the streams."""
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         ev0.record(stream)
         for _ in range(args.steps):
-            step()
+            step(serial=serial)
         ev1.record(stream)
         torch.cuda.synchronize()
         return ev0.elapsed_time(ev1) / args.steps, time.perf_counter() - t0
@@ -383,11 +409,13 @@ def main():
     ms_step, wall = timed(step)
     bu_per_step = len(layouts) * len(ALGOS) * w.b * w.T * w.iters
     value = bu_per_step / (ms_step / 1e3)
+    # the same steps with every call on the timing stream, one after another
+    ms_serial, _ = timed(step, serial=True)
 
-    # a second pass of the same steps with HIP events around every launch
-    # (library profiling, on the call stream): per-kernel durations
+    # a second pass of the same steps, serial, with HIP events around every
+    # launch (library profiling, on the call stream): per-kernel durations
     bi.bi_profile_begin()
-    ms_prof, _ = timed(step)
+    ms_prof, _ = timed(step, serial=True)
     prof = bi.bi_profile_end()
     # a third pass with events around every call: per-call durations, the
     # median over the steps (each step with its own events, one
@@ -444,6 +472,10 @@ def main():
         "roofline": rooflines[dominant],
         "roofline_all": rooflines,
         "settle_steps": SETTLE_STEPS,
+        "concurrency": "each layout's calls (VMP, then MMP) on a stream of its own, the two layouts' streams "
+                       "overlapping inside a step" if len(layouts) > 1 else "one stream",
+        "serial": {"ms_per_step": ms_serial, "value": bu_per_step / (ms_serial / 1e3), "unit": "belief_updates/s",
+                   "note": "the same step with every call on one stream, one after another"},
         "kernel_timing": "a second pass of the same steps with HIP events around every launch on the call "
                          f"stream ({ms_prof:.3f} ms per step with them); the timed region has none",
         "kernels": {k: {"launches": n, "avg_ms": ms / max(n, 1)} for k, (n, ms) in prof.items()},

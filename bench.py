@@ -290,6 +290,8 @@ def main():
                     help="dense layout on fp32 matrix cores (the fp32 copy) instead of the fp16 pairs")
     ap.add_argument("--sparse-f64", action="store_true",
                     help="sparse layout on the fp64 gather kernels instead of the fp16-pair matrix-core tiles")
+    ap.add_argument("--serial", action="store_true",
+                    help="large workload: every call of a step on one stream (no overlap of the layouts' calls)")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the step on the other precision classes (fp32 matrix cores, fp64 sparse gathers)")
     ap.add_argument("--cache-probe", action="store_true",
@@ -357,7 +359,7 @@ def main():
                 pms[lay].infer(a, obs, act, w.iters, q=qs[(lay, a)], ws=wss[(lay, a)], stream=st)
 
         def step(st=stream, marks=None, serial=False):
-            if not serial and marks is None and st is not None and len(layouts) > 1:
+            if not (serial or args.serial) and marks is None and st is not None and len(layouts) > 1:
                 fork = torch.cuda.Event()
                 fork.record(st)
                 for lay in layouts:
@@ -473,7 +475,7 @@ def main():
         "roofline_all": rooflines,
         "settle_steps": SETTLE_STEPS,
         "concurrency": "each layout's calls (VMP, then MMP) on a stream of its own, the two layouts' streams "
-                       "overlapping inside a step" if len(layouts) > 1 else "one stream",
+                       "overlapping inside a step" if len(layouts) > 1 and not args.serial else "one stream",
         "serial": {"ms_per_step": ms_serial, "value": bu_per_step / (ms_serial / 1e3), "unit": "belief_updates/s",
                    "note": "the same step with every call on one stream, one after another"},
         "kernel_timing": "a second pass of the same steps with HIP events around every launch on the call "

@@ -60,7 +60,7 @@ def test_layouts_on_two_streams_match_serial():
         side = {k: torch.cuda.Stream() for k in cases}
         main = torch.cuda.current_stream()
         for rep in range(3):
-            print(f"[gpu] two streams, round {rep}", flush=True)
+            print(f"[gpu] two streams, pass {rep}", flush=True)
             for v in q.values():
                 v.fill_(-1.0)
             fork = torch.cuda.Event()
